@@ -1,0 +1,362 @@
+/*
+ * ifq.h -- C ABI of the integrated fixed-point quantized convolution library
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The library implements one "quantized substructure" of IFQ-Net
+ * (Integrated Fixed-point Quantization Networks for Embedded Vision):
+ *
+ *   a    = W_b (x) X_q                       integer part of Eq. (1):
+ *                                            +-1 weights convolved with k-bit
+ *                                            activation codes, int32 sums
+ *   code = #{ i : s*a > T_i }                Eq. (7)/(8): the float data of
+ *                                            conv, BN (Eq. 2) and quantizer
+ *                                            (Eq. 3) composed into per-channel
+ *                                            integer thresholds (Sec. 3.2)
+ *   y    = max over a window of codes        Eq. (4), applied to the codes
+ *
+ * Conventions shared by every entry point:
+ *  - Status codes are ifq_status values; IFQ_OK is 0. INVALID_ARGUMENT,
+ *    UNSUPPORTED and INSUFFICIENT_BUFFER are decided before any launch, so
+ *    nothing has been launched and no output written; IFQ_ERR_HIP reports a
+ *    failed launch (for a stack, earlier layers may have been launched). A
+ *    text for the last error of the calling thread is in ifq_last_error().
+ *  - Every argument is validated on the host before any launch. Device faults
+ *    and kernel errors surface at the caller's next synchronisation.
+ *  - Device functions are asynchronous on the caller's stream. The caller owns
+ *    all memory (device and host); the library never allocates device memory
+ *    and keeps no state between calls beyond its loaded code object.
+ *  - Tensors are dense NHWC. Codes are unsigned: layout IFQ_LAYOUT_I8_NHWC
+ *    stores one code per byte; IFQ_LAYOUT_U2_NHWC_PACKED stores four 2-bit
+ *    codes per byte along C (channel c in bits 2*(c%4)..2*(c%4)+1 of byte
+ *    c/4; C must be a multiple of 4); IFQ_LAYOUT_I32_NHWC holds int32 sums.
+ *  - No C++ exception crosses this interface. All functions are reentrant.
+ */
+#ifndef IFQ_H_
+#define IFQ_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define IFQ_API __attribute__((visibility("default")))
+
+typedef int32_t ifq_status;
+
+#define IFQ_OK 0
+#define IFQ_ERR_INVALID_ARGUMENT (-1)   /* a value is out of its domain     */
+#define IFQ_ERR_UNSUPPORTED (-2)        /* valid but not implemented combo  */
+#define IFQ_ERR_HIP (-3)                /* a HIP launch or query failed     */
+#define IFQ_ERR_INSUFFICIENT_BUFFER (-4)/* a caller buffer is too small     */
+
+#define IFQ_LAYOUT_I8_NHWC 0
+#define IFQ_LAYOUT_U2_NHWC_PACKED 1
+#define IFQ_LAYOUT_I32_NHWC 2
+
+#define IFQ_POOL_VALID 0 /* ho = (h-k)/stride + 1, windows fully inside       */
+#define IFQ_POOL_SAME 1  /* ho = ceil(h/stride), windows clipped bottom/right */
+
+#define IFQ_JOIN_NONE 0
+#define IFQ_JOIN_IDENTITY 1 /* shortcut = the block input codes             */
+#define IFQ_JOIN_CONV 2     /* shortcut = int32 sums of a 1x1 downsample conv */
+
+#define IFQ_LAYER_CONV 0
+#define IFQ_LAYER_POOL 1
+
+#define IFQ_MAX_THRESHOLDS 15 /* 2^4 - 1: codes of up to 4 bits */
+
+/*
+ * One quantized convolution (Eq. 1 with the epilogue of Eq. 7/8).
+ *   n, h, w        batch and input spatial size
+ *   c_in, c_out    channels
+ *   kh, kw         filter size; stride and pad apply to both axes, the
+ *                  padded input positions hold code 0 (the level 0 is the
+ *                  real value 0)
+ *   in_bits        bits per input code, 1..8 (codes 0 .. 2^in_bits - 1)
+ *   out_bits       0: the output is the int32 sum a itself (no quantizer);
+ *                  1..4: the output is a code with 2^out_bits - 1 thresholds
+ *   in_layout      IFQ_LAYOUT_I8_NHWC, or IFQ_LAYOUT_U2_NHWC_PACKED when
+ *                  in_bits == 2
+ *   out_layout     IFQ_LAYOUT_I32_NHWC iff out_bits == 0; otherwise
+ *                  IFQ_LAYOUT_I8_NHWC, or IFQ_LAYOUT_U2_NHWC_PACKED when
+ *                  out_bits == 2
+ * Output size: ho = (h + 2*pad - kh)/stride + 1, wo likewise.
+ */
+typedef struct ifq_conv_desc {
+  int32_t n, h, w;
+  int32_t c_in, c_out;
+  int32_t kh, kw, stride, pad;
+  int32_t in_bits, out_bits;
+  int32_t in_layout, out_layout;
+} ifq_conv_desc;
+
+/*
+ * Parameters of the threshold fold of one layer (Sec. 3.2, Eq. 6 -> Eq. 7).
+ * All arrays are host arrays of c_out doubles; nullable ones take the default
+ * in brackets.
+ *   alpha[c] > 0     scale of filter c (W = alpha * W_b, Eq. 1)
+ *   beta_in > 0      step of the input codes (X = beta * X_q, Eq. 1)
+ *   bias    [0]      conv bias b (Eq. 1)
+ *   mean    [0], var [1], gamma [1], bn_beta [0], eps
+ *                    batch normalisation Y_bn = gamma*(Y - mean)/sqrt(var+eps)
+ *                    + bn_beta (Eq. 2 with its scale read as the standard
+ *                    deviation and the affine scale/shift included)
+ *   q_thr[i]         the 2^out_bits - 1 quantizer thresholds of Eq. (3),
+ *                    strictly increasing (equality goes to the lower code)
+ *   k                contraction length kh*kw*c_in; with in_bits it bounds the
+ *                    sums: |a| <= B = k * (2^in_bits - 1)
+ */
+typedef struct ifq_fold_params {
+  int32_t c_out;
+  int32_t in_bits;
+  int32_t out_bits;
+  int32_t reserved;
+  int64_t k;
+  const double* alpha;
+  double beta_in;
+  const double* bias;
+  const double* mean;
+  const double* var;
+  const double* gamma;
+  const double* bn_beta;
+  double eps;
+  const double* q_thr;
+} ifq_fold_params;
+
+/*
+ * Residual join of a basic block (not part of the paper; used by the
+ * ResNet-shaped stack). The quantizer input is the main branch after its BN
+ * plus the dequantized shortcut:
+ *   z = gamma*(alpha*beta_in*a + bias - mean)/sqrt(var+eps) + bn_beta + sc
+ *   sc = beta_x * x_q                                   (IFQ_JOIN_IDENTITY)
+ *   sc = gamma_d*(alpha_d*beta_x*d + bias_d - mean_d)/sqrt(var_d+eps_d)
+ *        + bn_beta_d                                    (IFQ_JOIN_CONV)
+ * with a the block's conv2 sum, x_q the block input code and d the 1x1
+ * downsample sum. ifq_fold_join writes per channel {p, q, cc} such that
+ * z = fma(p, a, fma(q, s, cc)) with s = x_q or d. Nullable: bias, bias_d
+ * [0]. The _d arrays are ignored for IFQ_JOIN_IDENTITY.
+ */
+typedef struct ifq_join_params {
+  int32_t c_out;
+  int32_t kind;
+  const double* alpha;
+  double beta_in;
+  const double* bias;
+  const double* mean;
+  const double* var;
+  const double* gamma;
+  const double* bn_beta;
+  double eps;
+  double beta_x;
+  const double* alpha_d;
+  const double* bias_d;
+  const double* mean_d;
+  const double* var_d;
+  const double* gamma_d;
+  const double* bn_beta_d;
+  double eps_d;
+} ifq_join_params;
+
+/*
+ * Device-side join operand of ifq_conv_forward.
+ *   kind      IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY or IFQ_JOIN_CONV
+ *   layout    layout of shortcut: codes (I8 / U2) for IDENTITY, I32 for CONV
+ *   shortcut  device tensor [n][ho][wo][c_out]
+ *   coef      device array [c_out][3] written by ifq_fold_join
+ *   n_q       number of quantizer thresholds, 2^out_bits - 1
+ *   q_thr     the quantizer thresholds of Eq. (3), strictly increasing
+ */
+typedef struct ifq_join {
+  int32_t kind;
+  int32_t layout;
+  const void* shortcut;
+  const double* coef;
+  int32_t n_q;
+  int32_t reserved;
+  double q_thr[IFQ_MAX_THRESHOLDS];
+} ifq_join;
+
+/*
+ * Integer max-pool on codes (Eq. 4 applied after the quantizer; for channels
+ * with a positive BN scale this equals pooling the conv output first).
+ *   n, h, w, c     input tensor; bits: code width; layout I8 or U2 (bits 2)
+ *   k, stride      square window; mode IFQ_POOL_VALID or IFQ_POOL_SAME
+ */
+typedef struct ifq_pool_desc {
+  int32_t n, h, w, c;
+  int32_t k, stride;
+  int32_t mode;
+  int32_t bits;
+  int32_t layout;
+} ifq_pool_desc;
+
+/*
+ * One layer of a stack (Sec. 3.1: a network is a chain of substructures).
+ *   kind        IFQ_LAYER_CONV or IFQ_LAYER_POOL
+ *   src, dst    tensor slots: 0 is the stack input x, 1 the stack output y,
+ *               2 .. n_slots-1 live in the caller's workspace
+ *   join_src    slot of the join shortcut (conv layers with join.kind != 0),
+ *               else -1; join.shortcut is ignored inside a stack
+ *   conv        shape of a conv layer; w_packed/thr as for ifq_conv_forward
+ *   pool        shape of a pool layer
+ */
+typedef struct ifq_layer {
+  int32_t kind;
+  int32_t src;
+  int32_t dst;
+  int32_t join_src;
+  ifq_conv_desc conv;
+  const void* w_packed;
+  const int32_t* thr;
+  ifq_join join;
+  ifq_pool_desc pool;
+} ifq_layer;
+
+/*
+ * A layer chain run on one stream.
+ *   events   optional array of n_layers + 1 HIP events; when non-null,
+ *            events[i] is recorded before layer i and events[n_layers] after
+ *            the last layer (per-layer timing)
+ */
+typedef struct ifq_stack {
+  int32_t n_layers;
+  int32_t n_slots;
+  const ifq_layer* layers;
+  hipEvent_t* events;
+} ifq_stack;
+
+/* Library version string, e.g. "ifq 1.0.0 gfx950". Host. */
+IFQ_API const char* ifq_version(void);
+
+/* Text of the last non-OK status of the calling thread ("" if none). Host. */
+IFQ_API const char* ifq_last_error(void);
+
+/* Bytes of a dense NHWC tensor in the given layout (0 if invalid). Host. */
+IFQ_API size_t ifq_tensor_bytes(int64_t n, int64_t h, int64_t w, int64_t c,
+                                int32_t layout);
+
+/*
+ * Output spatial size of a conv descriptor (Eq. 1 with stride and zero
+ * padding). Host. Returns IFQ_ERR_INVALID_ARGUMENT for an invalid desc.
+ */
+IFQ_API ifq_status ifq_conv_output_dims(const ifq_conv_desc* d, int32_t* ho,
+                                        int32_t* wo);
+
+/*
+ * Bytes of the device-ready weight blob of a layer (W_b of Eq. 1 as +-1
+ * int8 rows plus per-row sums), 0 for an invalid desc. Host.
+ */
+IFQ_API size_t ifq_packed_weight_bytes(const ifq_conv_desc* d);
+
+/*
+ * Pack the binary filters W_b of Eq. (1) for the device. Host only.
+ *   w_oihw     host int8 [c_out][c_in][kh][kw], every value +1 or -1
+ *              (alpha is not part of it: it is folded into the thresholds)
+ *   dst        host buffer of at least ifq_packed_weight_bytes(d) bytes; the
+ *              caller uploads it unchanged and passes it as w_packed
+ * Errors: INVALID_ARGUMENT (bad desc, a value other than +-1; dst untouched),
+ * INSUFFICIENT_BUFFER.
+ */
+IFQ_API ifq_status ifq_pack_weights(const ifq_conv_desc* d,
+                                    const int8_t* w_oihw, void* dst,
+                                    size_t dst_bytes);
+
+/*
+ * Threshold fold of Sec. 3.2 (Eq. 6 -> Eq. 7 -> floor; Eq. 8 for k bits).
+ * Host only. For channel c it writes the record
+ *   thr_out[c*R + 0]      s = +1, or -1 when gamma < 0 (the division by the
+ *                         negative BN scale flips every inequality)
+ *   thr_out[c*R + i]      T_i = clamp(floor(s * t_i), -B-1, B), i = 1..R-1
+ * with R = 2^out_bits and t_i = ((q_i - bn_beta)*sd/gamma + mean - bias) /
+ * (alpha*beta_in), sd = sqrt(var+eps), evaluated in fp64 in exactly that
+ * order. For every integer a, #{i : s*a > T_i} is the code Eq. (3) assigns to
+ * BN(alpha*beta_in*a + bias). gamma == 0 gives the constant code
+ * #{i : bn_beta > q_i}. thr_out holds c_out * 2^out_bits int32 (host).
+ * Errors: INVALID_ARGUMENT (alpha <= 0, beta_in <= 0, var+eps <= 0, NaN,
+ * q_thr not strictly increasing, out_bits outside 1..4, in_bits outside 1..8).
+ */
+IFQ_API ifq_status ifq_fold_thresholds(const ifq_fold_params* p,
+                                       int32_t* thr_out);
+
+/*
+ * Join coefficients (see ifq_join_params), fp64 in this order:
+ *   p  = (gamma * (alpha*beta_in)) / sd
+ *   c2 = (gamma * (bias - mean)) / sd + bn_beta
+ *   q  = beta_x (identity) or (gamma_d * (alpha_d*beta_x)) / sd_d
+ *   cd = 0 (identity) or (gamma_d * (bias_d - mean_d)) / sd_d + bn_beta_d
+ *   coef_out[c*3 + 0..2] = {p, q, c2 + cd}
+ * Host only. Errors: INVALID_ARGUMENT (bad kind, alpha <= 0, var+eps <= 0,
+ * NaN, beta <= 0).
+ */
+IFQ_API ifq_status ifq_fold_join(const ifq_join_params* p, double* coef_out);
+
+/* Device workspace bytes ifq_conv_forward needs for d (may be 0). Host. */
+IFQ_API size_t ifq_conv_workspace_bytes(const ifq_conv_desc* d);
+
+/*
+ * One quantized substructure on the GPU, asynchronous on stream.
+ *   x          device input [n][h][w][c_in] in d->in_layout
+ *   w_packed   device copy of ifq_pack_weights(d, ...)
+ *   thr        device copy of ifq_fold_thresholds(...) for this layer; must
+ *              be NULL iff out_bits == 0 or join->kind != IFQ_JOIN_NONE
+ *   join       nullable; residual join in place of the thresholds
+ *   y          device output [n][ho][wo][c_out] in d->out_layout
+ *   acc_dump   nullable device int32 [n][ho][wo][c_out]: also receives the
+ *              raw sums a
+ *   ws         device workspace of ws_bytes >= ifq_conv_workspace_bytes(d)
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED, INSUFFICIENT_BUFFER, HIP.
+ */
+IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
+                                    const void* w_packed, const int32_t* thr,
+                                    const ifq_join* join, void* y,
+                                    int32_t* acc_dump, void* ws,
+                                    size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Max-pool on codes (Eq. 4), asynchronous on stream. x, y device tensors in
+ * d->layout; y is [n][ho][wo][c]. Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
+ */
+IFQ_API ifq_status ifq_maxpool_codes(const ifq_pool_desc* d, const void* x,
+                                     void* y, hipStream_t stream);
+
+/*
+ * Convert codes between IFQ_LAYOUT_I8_NHWC and IFQ_LAYOUT_U2_NHWC_PACKED
+ * (npix pixels of c channels, c a multiple of 4), asynchronous. Converting to
+ * U2 keeps the low two bits of each code. Errors: INVALID_ARGUMENT, HIP.
+ */
+IFQ_API ifq_status ifq_convert_codes(int64_t npix, int32_t c,
+                                     int32_t src_layout, int32_t dst_layout,
+                                     const void* src, void* dst,
+                                     hipStream_t stream);
+
+/* Device workspace bytes of a stack (its work slots, 256-byte aligned). */
+IFQ_API size_t ifq_stack_workspace_bytes(const ifq_stack* s);
+
+/*
+ * Where work slot `slot` (2 .. n_slots-1) of a stack lives in the workspace:
+ * its byte offset and capacity (the largest tensor any layer writes to it).
+ * After ifq_run_stack a slot holds the tensor its last writer produced, in
+ * that layer's output layout. Host. Errors: INVALID_ARGUMENT.
+ */
+IFQ_API ifq_status ifq_stack_slot_info(const ifq_stack* s, int32_t slot,
+                                       size_t* offset, size_t* bytes);
+
+/*
+ * Run a layer chain (Sec. 3.1) on one stream with no host synchronisation.
+ * All layers are validated before the first launch. x is slot 0, y slot 1;
+ * ws holds the other slots. Errors: as ifq_conv_forward / ifq_maxpool_codes,
+ * plus INVALID_ARGUMENT for a slot read before it is written.
+ */
+IFQ_API ifq_status ifq_run_stack(const ifq_stack* s, const void* x, void* y,
+                                 void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* IFQ_H_ */

@@ -1,0 +1,692 @@
+// Host side of the C ABI declared in include/ifq.h: argument validation,
+// the weight packer, the threshold and join folds (Sec. 3.2, Eq. 6 -> 7 -> 8),
+// launch resolution and the layer-chain driver. Compiled with
+// -ffp-contract=off: the folds evaluate their fp64 expressions one operation
+// per statement in a fixed order.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "ifq.h"
+#include "ifq_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ifq_status fail(ifq_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+ifq_status ok() {
+  g_last_error.clear();
+  return IFQ_OK;
+}
+
+constexpr int64_t kMaxIndex = (int64_t)1 << 31;  // byte offsets kept below 2^31
+
+bool is_finite(double v) { return std::isfinite(v); }
+
+int64_t out_extent(int64_t in, int64_t k, int64_t stride, int64_t pad) {
+  return (in + 2 * pad - k) / stride + 1;
+}
+
+int64_t tensor_bytes(int64_t n, int64_t h, int64_t w, int64_t c, int layout) {
+  if (n < 0 || h < 0 || w < 0 || c < 0) return -1;
+  const int64_t e = n * h * w * c;
+  switch (layout) {
+    case IFQ_LAYOUT_I8_NHWC: return e;
+    case IFQ_LAYOUT_U2_NHWC_PACKED: return (c % 4) ? -1 : e / 4;
+    case IFQ_LAYOUT_I32_NHWC: return 4 * e;
+    default: return -1;
+  }
+}
+
+// Structural validation of a conv descriptor. UNSUPPORTED marks shapes the
+// kernels do not handle although the descriptor itself is meaningful.
+ifq_status check_conv(const ifq_conv_desc* d, int64_t* ho_out = nullptr,
+                      int64_t* wo_out = nullptr) {
+  if (!d) return fail(IFQ_ERR_INVALID_ARGUMENT, "conv desc is NULL");
+  if (d->n < 0 || d->h < 1 || d->w < 1 || d->c_in < 1 || d->c_out < 1)
+    return fail(IFQ_ERR_INVALID_ARGUMENT,
+                "conv: need n >= 0 and h, w, c_in, c_out >= 1 (got n=%d h=%d "
+                "w=%d c_in=%d c_out=%d)", d->n, d->h, d->w, d->c_in, d->c_out);
+  if (d->kh < 1 || d->kw < 1 || d->stride < 1 || d->pad < 0)
+    return fail(IFQ_ERR_INVALID_ARGUMENT,
+                "conv: need kh, kw, stride >= 1 and pad >= 0");
+  if (d->h + 2 * d->pad < d->kh || d->w + 2 * d->pad < d->kw)
+    return fail(IFQ_ERR_INVALID_ARGUMENT,
+                "conv: filter larger than the padded input");
+  if (d->in_bits < 1 || d->in_bits > 8)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: in_bits must be 1..8");
+  if (d->out_bits < 0 || d->out_bits > 4)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: out_bits must be 0..4");
+  if (d->in_layout == IFQ_LAYOUT_U2_NHWC_PACKED) {
+    if (d->in_bits != 2)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "conv: 2-bit packed input needs in_bits == 2");
+    if (d->c_in % 4)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "conv: 2-bit packed input needs c_in %% 4 == 0");
+    if (d->c_in % 16)
+      return fail(IFQ_ERR_UNSUPPORTED,
+                  "conv: 2-bit packed input needs c_in %% 16 == 0");
+  } else if (d->in_layout != IFQ_LAYOUT_I8_NHWC) {
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: bad in_layout %d", d->in_layout);
+  }
+  if (d->out_bits == 0) {
+    if (d->out_layout != IFQ_LAYOUT_I32_NHWC)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "conv: out_bits == 0 needs out_layout I32_NHWC");
+  } else if (d->out_layout == IFQ_LAYOUT_U2_NHWC_PACKED) {
+    if (d->out_bits != 2)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "conv: 2-bit packed output needs out_bits == 2");
+    if (d->c_out % 4)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "conv: 2-bit packed output needs c_out %% 4 == 0");
+  } else if (d->out_layout != IFQ_LAYOUT_I8_NHWC) {
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: bad out_layout %d", d->out_layout);
+  }
+  const int64_t ho = out_extent(d->h, d->kh, d->stride, d->pad);
+  const int64_t wo = out_extent(d->w, d->kw, d->stride, d->pad);
+  const int64_t xb = tensor_bytes(d->n, d->h, d->w, d->c_in, d->in_layout);
+  const int64_t yb = tensor_bytes(d->n, ho, wo, d->c_out, IFQ_LAYOUT_I32_NHWC);
+  if (xb >= kMaxIndex || yb >= kMaxIndex)
+    return fail(IFQ_ERR_UNSUPPORTED, "conv: tensors of 2^31 bytes or more");
+  const int64_t k = (int64_t)d->kh * d->kw * d->c_in;
+  if (k * ((1 << d->in_bits) - 1) >= kMaxIndex / 2)
+    return fail(IFQ_ERR_UNSUPPORTED, "conv: sums could overflow int32");
+  if (ho_out) *ho_out = ho;
+  if (wo_out) *wo_out = wo;
+  return IFQ_OK;
+}
+
+ifq_status check_pool(const ifq_pool_desc* d, int64_t* ho, int64_t* wo) {
+  if (!d) return fail(IFQ_ERR_INVALID_ARGUMENT, "pool desc is NULL");
+  if (d->n < 0 || d->h < 1 || d->w < 1 || d->c < 1)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "pool: need n >= 0, h, w, c >= 1");
+  if (d->k < 1 || d->stride < 1)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "pool: need k, stride >= 1");
+  if (d->bits < 1 || d->bits > 8)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "pool: bits must be 1..8");
+  if (d->layout == IFQ_LAYOUT_U2_NHWC_PACKED) {
+    if (d->bits != 2 || d->c % 4)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "pool: 2-bit packed codes need bits == 2 and c %% 4 == 0");
+  } else if (d->layout != IFQ_LAYOUT_I8_NHWC) {
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "pool: bad layout %d", d->layout);
+  }
+  if (d->mode == IFQ_POOL_VALID) {
+    if (d->k > d->h || d->k > d->w)
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "pool: window larger than input");
+    *ho = (d->h - d->k) / d->stride + 1;
+    *wo = (d->w - d->k) / d->stride + 1;
+  } else if (d->mode == IFQ_POOL_SAME) {
+    *ho = (d->h + d->stride - 1) / d->stride;
+    *wo = (d->w + d->stride - 1) / d->stride;
+  } else {
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "pool: bad mode %d", d->mode);
+  }
+  if (tensor_bytes(d->n, d->h, d->w, d->c, IFQ_LAYOUT_I8_NHWC) >= kMaxIndex)
+    return fail(IFQ_ERR_UNSUPPORTED, "pool: tensors of 2^31 bytes or more");
+  return IFQ_OK;
+}
+
+ifq_status check_join(const ifq_join* j, const ifq_conv_desc* d) {
+  if (j->kind != IFQ_JOIN_IDENTITY && j->kind != IFQ_JOIN_CONV)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join: bad kind %d", j->kind);
+  if (d->out_bits == 0)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join: needs a quantized output");
+  if (j->n_q != (1 << d->out_bits) - 1)
+    return fail(IFQ_ERR_INVALID_ARGUMENT,
+                "join: n_q must be 2^out_bits - 1 = %d", (1 << d->out_bits) - 1);
+  for (int i = 0; i < j->n_q; ++i) {
+    if (!is_finite(j->q_thr[i]) || (i > 0 && !(j->q_thr[i] > j->q_thr[i - 1])))
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "join: q_thr must be finite and strictly increasing");
+  }
+  if (!j->coef) return fail(IFQ_ERR_INVALID_ARGUMENT, "join: coef is NULL");
+  if (j->kind == IFQ_JOIN_CONV && j->layout != IFQ_LAYOUT_I32_NHWC)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join: conv shortcut must be I32_NHWC");
+  if (j->kind == IFQ_JOIN_IDENTITY) {
+    if (j->layout == IFQ_LAYOUT_U2_NHWC_PACKED) {
+      if (d->c_out % 4)
+        return fail(IFQ_ERR_INVALID_ARGUMENT,
+                    "join: packed shortcut needs c_out %% 4 == 0");
+    } else if (j->layout != IFQ_LAYOUT_I8_NHWC) {
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "join: identity shortcut must be codes (I8 or U2)");
+    }
+  }
+  return IFQ_OK;
+}
+
+// Resolve a validated conv into kernel arguments.
+ifq::ConvLaunch make_launch(const ifq_conv_desc* d, int64_t ho, int64_t wo,
+                            const void* x, const void* w, const int32_t* thr,
+                            const ifq_join* join, const void* shortcut, void* y,
+                            int32_t* acc_dump) {
+  const ifq::WeightGeom g = ifq::weight_geom(*d);
+  ifq::ConvLaunch a;
+  std::memset(&a, 0, sizeof(a));
+  a.x = static_cast<const uint8_t*>(x);
+  a.wgt = static_cast<const int8_t*>(w);
+  a.rowsum = reinterpret_cast<const int32_t*>(static_cast<const uint8_t*>(w) +
+                                              g.rows_bytes);
+  a.thr = thr;
+  a.y = y;
+  a.acc_dump = acc_dump;
+  a.join_kind = IFQ_JOIN_NONE;
+  if (join && join->kind != IFQ_JOIN_NONE) {
+    a.join_kind = join->kind;
+    a.sc_layout = join->layout;
+    a.shortcut = shortcut;
+    a.coef = join->coef;
+    for (int i = 0; i < join->n_q; ++i) a.qthr[i] = join->q_thr[i];
+  }
+  a.nq = d->out_bits ? (1 << d->out_bits) - 1 : 0;
+  a.rec = d->out_bits ? (1 << d->out_bits) : 0;
+  a.n = d->n;
+  a.h = d->h;
+  a.w = d->w;
+  a.cin = d->c_in;
+  a.cout = d->c_out;
+  a.cout_pad = (int32_t)g.cout_pad;
+  a.kh = d->kh;
+  a.kw = d->kw;
+  a.stride = d->stride;
+  a.pad = d->pad;
+  a.ho = (int32_t)ho;
+  a.wo = (int32_t)wo;
+  a.m = (int32_t)((int64_t)d->n * ho * wo);
+  a.kpad = (int32_t)g.kpad;
+  a.nk = (int32_t)(g.kpad / ifq::kKStep);
+  a.in_layout = d->in_layout;
+  a.in_bits = d->in_bits;
+  a.out_mode = d->out_bits == 0 ? 0
+               : d->out_layout == IFQ_LAYOUT_U2_NHWC_PACKED ? 2 : 1;
+  return a;
+}
+
+ifq_status hip_status(hipError_t e, const char* what) {
+  if (e != hipSuccess)
+    return fail(IFQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return IFQ_OK;
+}
+
+ifq_status conv_args_check(const ifq_conv_desc* d, const void* x,
+                           const void* w, const int32_t* thr,
+                           const ifq_join* join, const void* shortcut,
+                           const void* y) {
+  const bool joined = join && join->kind != IFQ_JOIN_NONE;
+  if (joined) {
+    ifq_status st = check_join(join, d);
+    if (st != IFQ_OK) return st;
+    if (!shortcut) return fail(IFQ_ERR_INVALID_ARGUMENT, "join: shortcut is NULL");
+  }
+  if (d->n > 0 && (!x || !w || !y))
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: x, w_packed and y are required");
+  const bool want_thr = d->out_bits != 0 && !joined;
+  if (want_thr && !thr)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: thresholds required");
+  if (!want_thr && thr)
+    return fail(IFQ_ERR_INVALID_ARGUMENT,
+                "conv: thr must be NULL for int32 output or a join");
+  return IFQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+IFQ_API const char* ifq_version(void) { return "ifq 1.0.0 gfx950"; }
+
+IFQ_API const char* ifq_last_error(void) { return g_last_error.c_str(); }
+
+IFQ_API size_t ifq_tensor_bytes(int64_t n, int64_t h, int64_t w, int64_t c,
+                                int32_t layout) {
+  const int64_t b = tensor_bytes(n, h, w, c, layout);
+  return b < 0 ? 0 : (size_t)b;
+}
+
+IFQ_API ifq_status ifq_conv_output_dims(const ifq_conv_desc* d, int32_t* ho,
+                                        int32_t* wo) {
+  int64_t h, w;
+  ifq_status st = check_conv(d, &h, &w);
+  if (st != IFQ_OK) return st;
+  if (!ho || !wo) return fail(IFQ_ERR_INVALID_ARGUMENT, "NULL output pointer");
+  *ho = (int32_t)h;
+  *wo = (int32_t)w;
+  return ok();
+}
+
+IFQ_API size_t ifq_packed_weight_bytes(const ifq_conv_desc* d) {
+  if (check_conv(d) != IFQ_OK) return 0;
+  return (size_t)ifq::weight_geom(*d).total_bytes;
+}
+
+IFQ_API ifq_status ifq_pack_weights(const ifq_conv_desc* d,
+                                    const int8_t* w_oihw, void* dst,
+                                    size_t dst_bytes) {
+  ifq_status st = check_conv(d);
+  if (st != IFQ_OK) return st;
+  if (!w_oihw || !dst) return fail(IFQ_ERR_INVALID_ARGUMENT, "NULL pointer");
+  const ifq::WeightGeom g = ifq::weight_geom(*d);
+  if (dst_bytes < (size_t)g.total_bytes)
+    return fail(IFQ_ERR_INSUFFICIENT_BUFFER, "pack: need %lld bytes, got %zu",
+                (long long)g.total_bytes, dst_bytes);
+  const int64_t total = (int64_t)d->c_out * d->c_in * d->kh * d->kw;
+  for (int64_t i = 0; i < total; ++i)
+    if (w_oihw[i] != 1 && w_oihw[i] != -1)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "pack: weight %lld is %d, must be +1 or -1", (long long)i,
+                  (int)w_oihw[i]);
+  const bool u2 = d->in_layout == IFQ_LAYOUT_U2_NHWC_PACKED;
+  int8_t* rows = static_cast<int8_t*>(dst);
+  int32_t* rowsum = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(dst) + g.rows_bytes);
+  std::memset(dst, 0, (size_t)g.total_bytes);
+  for (int64_t co = 0; co < d->c_out; ++co) {
+    int32_t sum = 0;
+    for (int64_t r = 0; r < d->kh; ++r)
+      for (int64_t s = 0; s < d->kw; ++s)
+        for (int64_t c = 0; c < d->c_in; ++c) {
+          int64_t cp = c;
+          if (u2) {  // 4x4 transpose inside each group of 16 channels
+            const int64_t base = c & ~(int64_t)15, in = c & 15;
+            cp = base + (in & 3) * 4 + (in >> 2);
+          }
+          const int8_t v = w_oihw[((co * d->c_in + c) * d->kh + r) * d->kw + s];
+          rows[co * g.kpad + (r * d->kw + s) * d->c_in + cp] = v;
+          sum += v;
+        }
+    rowsum[co] = sum;
+  }
+  return ok();
+}
+
+IFQ_API ifq_status ifq_fold_thresholds(const ifq_fold_params* p,
+                                       int32_t* thr_out) {
+  if (!p || !thr_out) return fail(IFQ_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if (p->c_out < 1) return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: c_out < 1");
+  if (p->in_bits < 1 || p->in_bits > 8)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: in_bits must be 1..8");
+  if (p->out_bits < 1 || p->out_bits > 4)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: out_bits must be 1..4");
+  if (p->k < 1 || p->k * ((1 << p->in_bits) - 1) >= kMaxIndex / 2)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: bad contraction length");
+  if (!p->alpha || !p->q_thr)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: alpha and q_thr are required");
+  if (!(p->beta_in > 0.0) || !is_finite(p->beta_in))
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: beta_in must be > 0");
+  if (!is_finite(p->eps)) return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: eps not finite");
+  const int nq = (1 << p->out_bits) - 1;
+  const int rec = nq + 1;
+  for (int i = 0; i < nq; ++i)
+    if (!is_finite(p->q_thr[i]) || (i > 0 && !(p->q_thr[i] > p->q_thr[i - 1])))
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "fold: q_thr must be finite and strictly increasing");
+  const double bound = (double)p->k * (double)((1 << p->in_bits) - 1);
+  // validate every channel before writing anything
+  for (int c = 0; c < p->c_out; ++c) {
+    const double al = p->alpha[c];
+    const double bi = p->bias ? p->bias[c] : 0.0;
+    const double mu = p->mean ? p->mean[c] : 0.0;
+    const double va = p->var ? p->var[c] : 1.0;
+    const double ga = p->gamma ? p->gamma[c] : 1.0;
+    const double be = p->bn_beta ? p->bn_beta[c] : 0.0;
+    if (!(al > 0.0) || !is_finite(al))
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: alpha[%d] must be > 0", c);
+    if (!is_finite(bi) || !is_finite(mu) || !is_finite(va) || !is_finite(ga) || !is_finite(be))
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: channel %d not finite", c);
+    if (!(va + p->eps > 0.0))
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: var[%d] + eps must be > 0", c);
+  }
+  for (int c = 0; c < p->c_out; ++c) {
+    const double alpha = p->alpha[c];
+    const double bias = p->bias ? p->bias[c] : 0.0;
+    const double mean = p->mean ? p->mean[c] : 0.0;
+    const double var = p->var ? p->var[c] : 1.0;
+    const double gamma = p->gamma ? p->gamma[c] : 1.0;
+    const double bn_beta = p->bn_beta ? p->bn_beta[c] : 0.0;
+    int32_t* rec_c = thr_out + (int64_t)c * rec;
+    const double sd = std::sqrt(var + p->eps);
+    const double ab = alpha * p->beta_in;
+    if (gamma == 0.0) {
+      // BN output is the constant bn_beta: the code is #{i : bn_beta > q_i}
+      rec_c[0] = 1;
+      int level = 0;
+      for (int i = 0; i < nq; ++i) level += bn_beta > p->q_thr[i] ? 1 : 0;
+      for (int i = 0; i < nq; ++i)
+        rec_c[1 + i] = i < level ? (int32_t)(-bound - 1.0) : (int32_t)bound;
+      continue;
+    }
+    // a negative BN scale flips the direction of every comparison
+    const double sign = gamma > 0.0 ? 1.0 : -1.0;
+    rec_c[0] = gamma > 0.0 ? 1 : -1;
+    for (int i = 0; i < nq; ++i) {
+      double t = p->q_thr[i] - bn_beta;
+      t = t * sd;
+      t = t / gamma;
+      t = t + mean;
+      t = t - bias;
+      t = t / ab;
+      // integer sums: s*a > s*t  <=>  s*a > floor(s*t)
+      double f = std::floor(sign * t);
+      if (f < -bound - 1.0) f = -bound - 1.0;
+      if (f > bound) f = bound;
+      rec_c[1 + i] = (int32_t)f;
+    }
+  }
+  return ok();
+}
+
+IFQ_API ifq_status ifq_fold_join(const ifq_join_params* p, double* coef_out) {
+  if (!p || !coef_out) return fail(IFQ_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if (p->c_out < 1) return fail(IFQ_ERR_INVALID_ARGUMENT, "join: c_out < 1");
+  if (p->kind != IFQ_JOIN_IDENTITY && p->kind != IFQ_JOIN_CONV)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join: bad kind %d", p->kind);
+  const bool conv = p->kind == IFQ_JOIN_CONV;
+  if (!p->alpha || !p->mean || !p->var || !p->gamma || !p->bn_beta)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join: main-branch arrays required");
+  if (conv && (!p->alpha_d || !p->mean_d || !p->var_d || !p->gamma_d || !p->bn_beta_d))
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join: shortcut arrays required");
+  if (!(p->beta_in > 0.0) || !is_finite(p->beta_in) || !(p->beta_x > 0.0) ||
+      !is_finite(p->beta_x) || !is_finite(p->eps) || (conv && !is_finite(p->eps_d)))
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join: steps must be > 0");
+  for (int c = 0; c < p->c_out; ++c) {
+    const double b = p->bias ? p->bias[c] : 0.0;
+    if (!(p->alpha[c] > 0.0) || !is_finite(p->alpha[c]) || !is_finite(b) ||
+        !is_finite(p->mean[c]) || !is_finite(p->gamma[c]) || !is_finite(p->bn_beta[c]) ||
+        !is_finite(p->var[c]) || !(p->var[c] + p->eps > 0.0))
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "join: bad main channel %d", c);
+    if (conv) {
+      const double bd = p->bias_d ? p->bias_d[c] : 0.0;
+      if (!(p->alpha_d[c] > 0.0) || !is_finite(p->alpha_d[c]) || !is_finite(bd) ||
+          !is_finite(p->mean_d[c]) || !is_finite(p->gamma_d[c]) ||
+          !is_finite(p->bn_beta_d[c]) || !is_finite(p->var_d[c]) ||
+          !(p->var_d[c] + p->eps_d > 0.0))
+        return fail(IFQ_ERR_INVALID_ARGUMENT, "join: bad shortcut channel %d", c);
+    }
+  }
+  for (int c = 0; c < p->c_out; ++c) {
+    const double sd = std::sqrt(p->var[c] + p->eps);
+    double pm = p->alpha[c] * p->beta_in;
+    pm = p->gamma[c] * pm;
+    pm = pm / sd;
+    double c2 = (p->bias ? p->bias[c] : 0.0) - p->mean[c];
+    c2 = p->gamma[c] * c2;
+    c2 = c2 / sd;
+    c2 = c2 + p->bn_beta[c];
+    double q = p->beta_x;
+    double cd = 0.0;
+    if (conv) {
+      const double sdd = std::sqrt(p->var_d[c] + p->eps_d);
+      q = p->alpha_d[c] * p->beta_x;
+      q = p->gamma_d[c] * q;
+      q = q / sdd;
+      cd = (p->bias_d ? p->bias_d[c] : 0.0) - p->mean_d[c];
+      cd = p->gamma_d[c] * cd;
+      cd = cd / sdd;
+      cd = cd + p->bn_beta_d[c];
+    }
+    coef_out[3 * c + 0] = pm;
+    coef_out[3 * c + 1] = q;
+    coef_out[3 * c + 2] = c2 + cd;
+  }
+  return ok();
+}
+
+IFQ_API size_t ifq_conv_workspace_bytes(const ifq_conv_desc* d) {
+  (void)d;
+  return 0;
+}
+
+IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
+                                    const void* w_packed, const int32_t* thr,
+                                    const ifq_join* join, void* y,
+                                    int32_t* acc_dump, void* ws,
+                                    size_t ws_bytes, hipStream_t stream) {
+  int64_t ho, wo;
+  ifq_status st = check_conv(d, &ho, &wo);
+  if (st != IFQ_OK) return st;
+  const void* sc = (join && join->kind != IFQ_JOIN_NONE) ? join->shortcut : nullptr;
+  st = conv_args_check(d, x, w_packed, thr, join, sc, y);
+  if (st != IFQ_OK) return st;
+  if (ws_bytes < ifq_conv_workspace_bytes(d) || (ifq_conv_workspace_bytes(d) && !ws))
+    return fail(IFQ_ERR_INSUFFICIENT_BUFFER, "conv: workspace too small");
+  const ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_packed, thr, join, sc, y, acc_dump);
+  st = hip_status(ifq::launch_conv(a, stream), "conv launch");
+  if (st != IFQ_OK) return st;
+  return ok();
+}
+
+IFQ_API ifq_status ifq_maxpool_codes(const ifq_pool_desc* d, const void* x,
+                                     void* y, hipStream_t stream) {
+  int64_t ho, wo;
+  ifq_status st = check_pool(d, &ho, &wo);
+  if (st != IFQ_OK) return st;
+  if (d->n > 0 && (!x || !y)) return fail(IFQ_ERR_INVALID_ARGUMENT, "pool: NULL tensor");
+  ifq::PoolLaunch a;
+  a.x = static_cast<const uint8_t*>(x);
+  a.y = static_cast<uint8_t*>(y);
+  a.n = d->n;
+  a.h = d->h;
+  a.w = d->w;
+  a.c = d->c;
+  a.k = d->k;
+  a.stride = d->stride;
+  a.ho = (int32_t)ho;
+  a.wo = (int32_t)wo;
+  a.layout = d->layout;
+  a.bits = d->bits;
+  st = hip_status(ifq::launch_pool(a, stream), "pool launch");
+  if (st != IFQ_OK) return st;
+  return ok();
+}
+
+IFQ_API ifq_status ifq_convert_codes(int64_t npix, int32_t c,
+                                     int32_t src_layout, int32_t dst_layout,
+                                     const void* src, void* dst,
+                                     hipStream_t stream) {
+  if (npix < 0 || c < 1 || c % 4)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "convert: need npix >= 0, c %% 4 == 0");
+  const bool fwd = src_layout == IFQ_LAYOUT_I8_NHWC && dst_layout == IFQ_LAYOUT_U2_NHWC_PACKED;
+  const bool back = src_layout == IFQ_LAYOUT_U2_NHWC_PACKED && dst_layout == IFQ_LAYOUT_I8_NHWC;
+  if (!fwd && !back)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "convert: layouts must be I8 <-> U2");
+  if (npix * c >= kMaxIndex) return fail(IFQ_ERR_UNSUPPORTED, "convert: too large");
+  if (npix > 0 && (!src || !dst)) return fail(IFQ_ERR_INVALID_ARGUMENT, "convert: NULL");
+  ifq_status st = hip_status(ifq::launch_convert(npix * c, src_layout, src, dst, stream),
+                             "convert launch");
+  if (st != IFQ_OK) return st;
+  return ok();
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Layer-chain driver
+// ---------------------------------------------------------------------------
+namespace {
+
+struct SlotPlan {
+  std::vector<int64_t> offset;  // byte offset of each work slot in ws
+  std::vector<int64_t> bytes;   // capacity of each slot
+  int64_t slots_bytes = 0;      // end of the slot area
+  int64_t conv_ws = 0;          // per-conv workspace (shared by all layers)
+  int64_t total = 0;
+};
+
+int64_t layer_out_bytes(const ifq_layer& L) {
+  if (L.kind == IFQ_LAYER_CONV) {
+    const int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);
+    const int64_t wo = out_extent(L.conv.w, L.conv.kw, L.conv.stride, L.conv.pad);
+    return tensor_bytes(L.conv.n, ho, wo, L.conv.c_out, L.conv.out_layout);
+  }
+  int64_t ho, wo;
+  if (L.pool.mode == IFQ_POOL_VALID) {
+    ho = (L.pool.h - L.pool.k) / L.pool.stride + 1;
+    wo = (L.pool.w - L.pool.k) / L.pool.stride + 1;
+  } else {
+    ho = (L.pool.h + L.pool.stride - 1) / L.pool.stride;
+    wo = (L.pool.w + L.pool.stride - 1) / L.pool.stride;
+  }
+  return tensor_bytes(L.pool.n, ho, wo, L.pool.c, L.pool.layout);
+}
+
+int64_t layer_in_bytes(const ifq_layer& L) {
+  if (L.kind == IFQ_LAYER_CONV)
+    return tensor_bytes(L.conv.n, L.conv.h, L.conv.w, L.conv.c_in, L.conv.in_layout);
+  return tensor_bytes(L.pool.n, L.pool.h, L.pool.w, L.pool.c, L.pool.layout);
+}
+
+ifq_status plan_stack(const ifq_stack* s, SlotPlan* plan) {
+  if (!s) return fail(IFQ_ERR_INVALID_ARGUMENT, "stack is NULL");
+  if (s->n_layers < 0 || (s->n_layers > 0 && !s->layers))
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "stack: bad layer array");
+  if (s->n_slots < 2) return fail(IFQ_ERR_INVALID_ARGUMENT, "stack: n_slots < 2");
+  plan->offset.assign(s->n_slots, 0);
+  plan->bytes.assign(s->n_slots, 0);
+  std::vector<char> written(s->n_slots, 0);
+  written[0] = 1;
+  for (int i = 0; i < s->n_layers; ++i) {
+    const ifq_layer& L = s->layers[i];
+    ifq_status st;
+    if (L.kind == IFQ_LAYER_CONV) {
+      st = check_conv(&L.conv);
+      if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+      const bool joined = L.join.kind != IFQ_JOIN_NONE;
+      st = conv_args_check(&L.conv, (const void*)1, L.w_packed, L.thr, &L.join,
+                           joined ? (const void*)1 : nullptr, (const void*)1);
+      if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+      if (joined) {
+        if (L.join_src < 0 || L.join_src >= s->n_slots || !written[L.join_src] ||
+            L.join_src == L.dst)
+          return fail(IFQ_ERR_INVALID_ARGUMENT,
+                      "layer %d: join slot %d not written before", i, L.join_src);
+      }
+      plan->conv_ws = std::max<int64_t>(plan->conv_ws,
+                                        (int64_t)ifq_conv_workspace_bytes(&L.conv));
+    } else if (L.kind == IFQ_LAYER_POOL) {
+      int64_t ho, wo;
+      st = check_pool(&L.pool, &ho, &wo);
+      if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+    } else {
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "layer %d: bad kind %d", i, L.kind);
+    }
+    if (L.src < 0 || L.src >= s->n_slots || !written[L.src])
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "layer %d: src slot %d not written before",
+                  i, L.src);
+    if (L.dst < 1 || L.dst >= s->n_slots || L.dst == L.src)
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "layer %d: bad dst slot %d", i, L.dst);
+    if (L.src >= 2 && layer_in_bytes(L) > plan->bytes[L.src])
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "layer %d: reads %lld bytes from slot %d holding %lld", i,
+                  (long long)layer_in_bytes(L), L.src, (long long)plan->bytes[L.src]);
+    const int64_t ob = layer_out_bytes(L);
+    if (ob > plan->bytes[L.dst]) plan->bytes[L.dst] = ob;
+    written[L.dst] = 1;
+  }
+  int64_t off = 0;
+  for (int k = 2; k < s->n_slots; ++k) {
+    plan->offset[k] = off;
+    off += ifq::round_up(plan->bytes[k], 256);
+  }
+  plan->slots_bytes = off;
+  plan->total = off + ifq::round_up(plan->conv_ws, 256);
+  return IFQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+IFQ_API size_t ifq_stack_workspace_bytes(const ifq_stack* s) {
+  SlotPlan plan;
+  if (plan_stack(s, &plan) != IFQ_OK) return 0;
+  return (size_t)plan.total;
+}
+
+IFQ_API ifq_status ifq_stack_slot_info(const ifq_stack* s, int32_t slot,
+                                       size_t* offset, size_t* bytes) {
+  SlotPlan plan;
+  ifq_status st = plan_stack(s, &plan);
+  if (st != IFQ_OK) return st;
+  if (slot < 2 || slot >= s->n_slots || !offset || !bytes)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "slot_info: bad slot %d", slot);
+  *offset = (size_t)plan.offset[slot];
+  *bytes = (size_t)plan.bytes[slot];
+  return ok();
+}
+
+IFQ_API ifq_status ifq_run_stack(const ifq_stack* s, const void* x, void* y,
+                                 void* ws, size_t ws_bytes, hipStream_t stream) {
+  SlotPlan plan;
+  ifq_status st = plan_stack(s, &plan);
+  if (st != IFQ_OK) return st;
+  if ((int64_t)ws_bytes < plan.total || (plan.total > 0 && !ws))
+    return fail(IFQ_ERR_INSUFFICIENT_BUFFER, "stack: workspace needs %lld bytes",
+                (long long)plan.total);
+  if (!x || !y) return fail(IFQ_ERR_INVALID_ARGUMENT, "stack: x and y are required");
+  uint8_t* base = static_cast<uint8_t*>(ws);
+  auto slot = [&](int k) -> void* {
+    if (k == 0) return const_cast<void*>(x);
+    if (k == 1) return y;
+    return base + plan.offset[k];
+  };
+  void* conv_ws = base ? base + plan.slots_bytes : nullptr;
+  for (int i = 0; i < s->n_layers; ++i) {
+    const ifq_layer& L = s->layers[i];
+    if (s->events) {
+      st = hip_status(hipEventRecord(s->events[i], stream), "event record");
+      if (st != IFQ_OK) return st;
+    }
+    if (L.kind == IFQ_LAYER_CONV) {
+      ifq_join j = L.join;
+      const void* sc = nullptr;
+      if (j.kind != IFQ_JOIN_NONE) sc = slot(L.join_src);
+      int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);
+      int64_t wo = out_extent(L.conv.w, L.conv.kw, L.conv.stride, L.conv.pad);
+      const ifq::ConvLaunch a = make_launch(&L.conv, ho, wo, slot(L.src), L.w_packed,
+                                            L.thr, &j, sc, slot(L.dst), nullptr);
+      (void)conv_ws;
+      st = hip_status(ifq::launch_conv(a, stream), "conv launch");
+    } else {
+      int64_t ho, wo;
+      check_pool(&L.pool, &ho, &wo);
+      ifq::PoolLaunch a;
+      a.x = static_cast<const uint8_t*>(slot(L.src));
+      a.y = static_cast<uint8_t*>(slot(L.dst));
+      a.n = L.pool.n;
+      a.h = L.pool.h;
+      a.w = L.pool.w;
+      a.c = L.pool.c;
+      a.k = L.pool.k;
+      a.stride = L.pool.stride;
+      a.ho = (int32_t)ho;
+      a.wo = (int32_t)wo;
+      a.layout = L.pool.layout;
+      a.bits = L.pool.bits;
+      st = hip_status(ifq::launch_pool(a, stream), "pool launch");
+    }
+    if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+  }
+  if (s->events) {
+    st = hip_status(hipEventRecord(s->events[s->n_layers], stream), "event record");
+    if (st != IFQ_OK) return st;
+  }
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,224 @@
+"""Layer-chain builder: turns a list of layer specs plus their float
+parameters into a device-resident ifq_stack and runs it with ifq_run_stack.
+
+This is the "convert once, then deploy" step of IFQ-Net (Sec. 3): weights are
+packed and thresholds folded once, on the host, by the library's own C++
+entry points, then uploaded; a forward pass is one ifq_run_stack call that
+launches every layer on one stream without host synchronisation.
+
+Layer specs are duck-typed. A conv spec has name, src, dst, h, w, cin, cout,
+k, stride, pad, in_bits, out_bits and join (None, ("identity", slot) or
+("conv", slot, down_layer_name)); a pool spec has name, src, dst, h, w, c, k,
+stride, mode ("valid" / "same") and bits. Slot "x" is the stack input, "y"
+the output. Parameters of a conv are a dict with w (OIHW +-1 int8), alpha,
+bias, mean, var, gamma, bn_beta (per output channel), eps, beta_in, q_thr.
+"""
+import ctypes
+
+import numpy as np
+
+from . import _ffi, api
+from ._ffi import (Layer, Stack, IFQ_LAYER_CONV, IFQ_LAYER_POOL,
+                   IFQ_LAYOUT_I8_NHWC, IFQ_LAYOUT_U2_NHWC_PACKED,
+                   IFQ_LAYOUT_I32_NHWC, IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY,
+                   IFQ_JOIN_CONV, IFQ_POOL_VALID, IFQ_POOL_SAME)
+
+
+def _is_conv(L):
+    return hasattr(L, "cin")
+
+
+def conv_ops(L, batch):
+    """Dense int-ops of a conv layer: 2 * N*Ho*Wo * Cout * kh*kw*Cin."""
+    ho = (L.h + 2 * L.pad - L.k) // L.stride + 1
+    wo = (L.w + 2 * L.pad - L.k) // L.stride + 1
+    return 2 * batch * ho * wo * L.cout * L.k * L.k * L.cin
+
+
+class DeviceStack:
+    """A stack of quantized substructures resident on one GPU.
+
+    code_layout: "i8" (one byte per code) or "u2" (2-bit codes packed four
+    per byte) for every 2-bit code tensor whose channel count is a multiple of
+    16; other tensors use one byte per code, int32 sums stay int32.
+    """
+
+    def __init__(self, layers, params, batch, code_layout="i8",
+                 device="cuda"):
+        import torch
+        if code_layout not in ("i8", "u2"):
+            raise ValueError("code_layout must be 'i8' or 'u2'")
+        self.layers = list(layers)
+        self.batch = int(batch)
+        self.device = torch.device(device)
+        self._keep = []
+        slots = {"x": 0, "y": 1}
+        layout_of = {}
+
+        def sid(name):
+            if name not in slots:
+                slots[name] = len(slots)
+            return slots[name]
+
+        def code_layout_for(bits, channels):
+            if code_layout == "u2" and bits == 2 and channels % 16 == 0:
+                return IFQ_LAYOUT_U2_NHWC_PACKED
+            return IFQ_LAYOUT_I8_NHWC
+
+        L0 = self.layers[0]
+        c0 = L0.cin if _is_conv(L0) else L0.c
+        b0 = L0.in_bits if _is_conv(L0) else L0.bits
+        layout_of["x"] = code_layout_for(b0, c0)
+        self.input_shape = (self.batch, L0.h, L0.w, c0)
+        self.input_bits = b0
+        self.input_layout = layout_of["x"]
+
+        by_name = {L.name: (i, L) for i, L in enumerate(self.layers)}
+        self.tensor_info = {"x": (self.input_shape, layout_of["x"], b0)}
+        arr = (Layer * len(self.layers))()
+        self.ops = 0
+        for i, L in enumerate(self.layers):
+            rec = arr[i]
+            rec.src = sid(L.src)
+            rec.dst = sid(L.dst)
+            rec.join_src = -1
+            in_layout = layout_of[L.src]
+            if _is_conv(L):
+                p = params[i]
+                rec.kind = IFQ_LAYER_CONV
+                if L.out_bits == 0:
+                    out_layout = IFQ_LAYOUT_I32_NHWC
+                else:
+                    out_layout = code_layout_for(L.out_bits, L.cout)
+                d = api.conv_desc(self.batch, L.h, L.w, L.cin, L.cout, L.k,
+                                  L.stride, L.pad, L.in_bits, L.out_bits,
+                                  in_layout, out_layout)
+                rec.conv = d
+                blob = api.ifq_pack_weights(d, p["w"])
+                wdev = torch.from_numpy(blob).to(self.device)
+                self._keep.append(wdev)
+                rec.w_packed = wdev.data_ptr()
+                if L.out_bits != 0 and L.join is None:
+                    thr = api.ifq_fold_thresholds(
+                        L.cout, L.in_bits, L.out_bits, L.k * L.k * L.cin,
+                        p["alpha"], p["beta_in"], p["q_thr"], bias=p.get("bias"),
+                        mean=p["mean"], var=p["var"], gamma=p["gamma"],
+                        bn_beta=p["bn_beta"], eps=p["eps"])
+                    tdev = torch.from_numpy(thr).to(self.device)
+                    self._keep.append(tdev)
+                    rec.thr = tdev.data_ptr()
+                if L.join is not None:
+                    if L.join[0] == "identity":
+                        coef = api.ifq_fold_join(IFQ_JOIN_IDENTITY, p, p["beta_in"])
+                        kind = IFQ_JOIN_IDENTITY
+                    else:
+                        _, D = by_name[L.join[2]]
+                        pd = params[by_name[L.join[2]][0]]
+                        coef = api.ifq_fold_join(IFQ_JOIN_CONV, p, pd["beta_in"],
+                                                 down=pd)
+                        kind = IFQ_JOIN_CONV
+                    cdev = torch.from_numpy(coef).to(self.device)
+                    self._keep.append(cdev)
+                    rec.join = api.make_join(kind, layout_of[L.join[1]], None,
+                                             cdev, p["q_thr"])
+                    rec.join_src = sid(L.join[1])
+                self.ops += conv_ops(L, self.batch)
+                ho, wo = api.ifq_conv_output_dims(d)
+                out_shape = (self.batch, ho, wo, L.cout)
+                out_bits = L.out_bits
+            else:
+                rec.kind = IFQ_LAYER_POOL
+                mode = {"valid": IFQ_POOL_VALID, "same": IFQ_POOL_SAME}[L.mode]
+                out_layout = in_layout
+                rec.pool = api.pool_desc(self.batch, L.h, L.w, L.c, L.k,
+                                         L.stride, mode, L.bits, in_layout)
+                if mode == IFQ_POOL_VALID:
+                    ho, wo = (L.h - L.k) // L.stride + 1, (L.w - L.k) // L.stride + 1
+                else:
+                    ho, wo = -(-L.h // L.stride), -(-L.w // L.stride)
+                out_shape = (self.batch, ho, wo, L.c)
+                out_bits = L.bits
+            layout_of[L.dst] = out_layout
+            self.tensor_info[L.dst] = (out_shape, out_layout, out_bits)
+            if L.dst == "y":
+                self.output_shape = out_shape
+                self.output_layout = out_layout
+                self.output_bits = out_bits
+        self._layers = arr
+        self.n_slots = len(slots)
+        self.slots = dict(slots)
+        self.stack = Stack(len(self.layers), self.n_slots,
+                           ctypes.cast(arr, ctypes.POINTER(Layer)), None)
+        nbytes = api.ifq_stack_workspace_bytes(self.stack)
+        if nbytes == 0 and self.n_slots > 2:
+            raise api.IfqError(-1, "ifq_stack_workspace_bytes",
+                               api.ifq_last_error())
+        self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8,
+                              device=self.device)
+
+    # -- buffers ---------------------------------------------------------------
+    def _bytes(self, shape, layout):
+        n, h, w, c = shape
+        return api.ifq_tensor_bytes(n, h, w, c, layout)
+
+    def alloc_input(self):
+        import torch
+        return torch.empty(self._bytes(self.input_shape, self.input_layout),
+                           dtype=torch.uint8, device=self.device)
+
+    def alloc_output(self):
+        import torch
+        return torch.empty(self._bytes(self.output_shape, self.output_layout),
+                           dtype=torch.uint8, device=self.device)
+
+    def upload_input(self, codes, out=None):
+        """NHWC uint8 codes (host) -> device input in the stack's layout."""
+        import torch
+        codes = np.ascontiguousarray(codes, dtype=np.uint8)
+        assert codes.shape == self.input_shape, (codes.shape, self.input_shape)
+        if out is None:
+            out = self.alloc_input()
+        src = torch.from_numpy(codes.reshape(-1)).to(self.device)
+        if self.input_layout == IFQ_LAYOUT_U2_NHWC_PACKED:
+            n, h, w, c = self.input_shape
+            api.ifq_convert_codes(n * h * w, c, IFQ_LAYOUT_I8_NHWC,
+                                  IFQ_LAYOUT_U2_NHWC_PACKED, src, out)
+        else:
+            out.copy_(src)
+        return out
+
+    def download_output(self, y):
+        """Device output -> host NHWC array (uint8 codes or int32 sums)."""
+        import torch
+        n, h, w, c = self.output_shape
+        if self.output_layout == IFQ_LAYOUT_I32_NHWC:
+            return y.view(torch.int32).cpu().numpy().reshape(n, h, w, c)
+        if self.output_layout == IFQ_LAYOUT_U2_NHWC_PACKED:
+            full = torch.empty(n * h * w * c, dtype=torch.uint8, device=self.device)
+            api.ifq_convert_codes(n * h * w, c, IFQ_LAYOUT_U2_NHWC_PACKED,
+                                  IFQ_LAYOUT_I8_NHWC, y, full)
+            return full.cpu().numpy().reshape(n, h, w, c)
+        return y.cpu().numpy().reshape(n, h, w, c)
+
+    def read_slot(self, name):
+        """Host copy of a work slot's last tensor (after a run has finished):
+        NHWC uint8 codes or int32 sums; 2-bit packed codes are returned
+        packed (uint8 [n][h][w][c/4])."""
+        import torch
+        (n, h, w, c), layout, _ = self.tensor_info[name]
+        off, _ = api.ifq_stack_slot_info(self.stack, self.slots[name])
+        nb = self._bytes((n, h, w, c), layout)
+        raw = self.ws[off:off + nb]
+        if layout == IFQ_LAYOUT_I32_NHWC:
+            return raw.view(torch.int32).cpu().numpy().reshape(n, h, w, c)
+        if layout == IFQ_LAYOUT_U2_NHWC_PACKED:
+            return raw.cpu().numpy().reshape(n, h, w, c // 4)
+        return raw.cpu().numpy().reshape(n, h, w, c)
+
+    # -- execution -------------------------------------------------------------
+    def run(self, x, y, stream=None, events=None):
+        """One forward pass (asynchronous on stream). events: optional ctypes
+        array of n_layers + 1 hipEvent_t handles for per-layer timing."""
+        self.stack.events = (None if events is None
+                             else ctypes.cast(events, ctypes.c_void_p).value)
+        api.ifq_run_stack(self.stack, x, y, self.ws, stream)

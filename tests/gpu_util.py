@@ -1,0 +1,125 @@
+"""Helpers for the GPU parity tests: run one layer through the C ABI and the
+same layer through the oracle, on the same seeded inputs."""
+import numpy as np
+
+import oracle
+from oracle import layout as olayout
+from workloads import Conv, layer_params, stack_input
+
+I8, U2, I32 = 0, 1, 2
+
+
+def device():
+    import torch
+    return torch.device("cuda:0")
+
+
+def to_dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a).reshape(-1)).to(device())
+
+
+def upload_codes(P, codes, layout):
+    """Host NHWC codes -> device tensor in `layout` (library converter)."""
+    import torch
+    src = to_dev(codes.astype(np.uint8))
+    if layout == I8:
+        return src
+    n, h, w, c = codes.shape
+    out = torch.empty(n * h * w * c // 4, dtype=torch.uint8, device=device())
+    P.ifq_convert_codes(n * h * w, c, I8, U2, src, out)
+    return out
+
+
+def oracle_layer(L, x, p, shortcut=None, down=None):
+    """Expected (acc, output) of one layer from the oracle."""
+    acc = oracle.conv_acc(x, p["w"], L.stride, L.pad, L.in_bits)
+    if L.out_bits == 0:
+        return acc, acc
+    if L.join is not None:
+        if L.join[0] == "identity":
+            coef = oracle.join_coeffs("identity", p, p["beta_in"], p["beta_in"])
+        else:
+            coef = oracle.join_coeffs("conv", p, p["beta_in"], down["beta_in"],
+                                      down=down)
+        return acc, oracle.join_codes(acc, shortcut.astype(np.int32), coef,
+                                      p["q_thr"])
+    s, t = oracle.fold(p["alpha"], p["beta_in"], p["mean"], p["var"],
+                       p["gamma"], p["bn_beta"], p["eps"], p["q_thr"],
+                       L.k * L.k * L.cin, L.in_bits, bias=p["bias"])
+    return acc, oracle.codes(acc, s, t)
+
+
+def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
+              sc_layout=I8, down=None, dump=True):
+    """Run one conv through ifq_conv_forward; returns (acc or None, output).
+
+    output is uint8 codes NHWC (packed [..., c/4] for U2) or int32 sums."""
+    import torch
+    if out_layout is None:
+        out_layout = I32 if L.out_bits == 0 else I8
+    d = P.conv_desc(n, L.h, L.w, L.cin, L.cout, L.k, L.stride, L.pad,
+                    L.in_bits, L.out_bits, in_layout, out_layout)
+    ho, wo = P.ifq_conv_output_dims(d)
+    blob = P.ifq_pack_weights(d, p["w"])
+    wd = to_dev(blob)
+    td = None
+    join = None
+    if L.out_bits != 0 and L.join is None:
+        thr = P.ifq_fold_thresholds(L.cout, L.in_bits, L.out_bits,
+                                    L.k * L.k * L.cin, p["alpha"], p["beta_in"],
+                                    p["q_thr"], bias=p["bias"], mean=p["mean"],
+                                    var=p["var"], gamma=p["gamma"],
+                                    bn_beta=p["bn_beta"], eps=p["eps"])
+        td = to_dev(thr)
+    keep = []
+    if L.join is not None:
+        if L.join[0] == "identity":
+            coef = P.ifq_fold_join(P.IFQ_JOIN_IDENTITY, p, p["beta_in"])
+            scd = upload_codes(P, shortcut, sc_layout)
+            kind = P.IFQ_JOIN_IDENTITY
+        else:
+            coef = P.ifq_fold_join(P.IFQ_JOIN_CONV, p, down["beta_in"], down=down)
+            scd = to_dev(shortcut.astype(np.int32))
+            kind = P.IFQ_JOIN_CONV
+            sc_layout = I32
+        cd = to_dev(coef)
+        keep += [scd, cd]
+        join = P.make_join(kind, sc_layout, scd, cd, p["q_thr"])
+    xd = upload_codes(P, x, in_layout) if L.in_bits <= 8 else None
+    ob = P.ifq_tensor_bytes(n, ho, wo, L.cout, out_layout)
+    y = torch.empty(max(ob, 1), dtype=torch.uint8, device=device())
+    acc = None
+    if dump:
+        acc = torch.empty(max(n * ho * wo * L.cout, 1), dtype=torch.int32,
+                          device=device())
+    P.ifq_conv_forward(d, xd, wd, td, y, join=join, acc_dump=acc)
+    torch.cuda.synchronize()
+    shape = (n, ho, wo, L.cout)
+    acc_h = None if acc is None else acc[:np.prod(shape)].cpu().numpy().reshape(shape)
+    if out_layout == I32:
+        out = y[:ob].view(torch.int32).cpu().numpy().reshape(shape)
+    elif out_layout == U2:
+        out = y[:ob].cpu().numpy().reshape(n, ho, wo, L.cout // 4)
+    else:
+        out = y[:ob].cpu().numpy().reshape(shape)
+    return acc_h, out
+
+
+def expect_layout(codes, out_layout):
+    """Oracle codes in the byte layout the GPU wrote."""
+    return olayout.pack2(codes) if out_layout == U2 else codes
+
+
+def make_layer(name, h, w, cin, cout, k, stride, pad, in_bits=2, out_bits=2,
+               join=None):
+    return Conv(name, "x", "y", h, w, cin, cout, k, stride, pad, in_bits,
+                out_bits, join)
+
+
+def params_for(seed, L, variant="calibrated"):
+    return layer_params(1000 + seed, 0, L, variant)
+
+
+def codes_for(seed, shape, bits):
+    return stack_input(1000 + seed, shape, bits)

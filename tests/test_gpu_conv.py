@@ -1,0 +1,190 @@
+"""GPU parity of single layers through the C ABI: int32 sums and output codes
+must equal the oracle's bit for bit on the same seeded inputs."""
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import layout as olayout
+from gpu_util import (I8, U2, I32, gpu_layer, oracle_layer, expect_layout,
+                      make_layer, params_for, codes_for, upload_codes, to_dev,
+                      device)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def P():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1911_08076_amd as P
+    return P
+
+
+# (name, n, h, w, cin, cout, k, stride, pad, in_bits, out_bits)
+LAYERS = [
+    ("stack0_3x3_64", 1, 28, 28, 64, 64, 3, 1, 1, 2, 2),
+    ("ragged_m", 2, 13, 11, 64, 128, 3, 1, 1, 2, 2),
+    ("stride2", 2, 15, 15, 64, 128, 3, 2, 1, 2, 2),
+    ("5x5_cin96", 1, 9, 9, 96, 256, 5, 1, 2, 2, 2),
+    ("1x1_s2_int32", 2, 14, 14, 64, 128, 1, 2, 0, 2, 0),
+    ("head_1x1_c30", 1, 13, 13, 512, 30, 1, 1, 0, 2, 0),
+    ("first_8bit_cin3", 1, 20, 20, 3, 16, 3, 1, 1, 8, 2),
+    ("cin16_cout32", 1, 18, 18, 16, 32, 3, 1, 1, 2, 2),
+    ("cin32_cout64", 1, 12, 12, 32, 64, 3, 1, 1, 2, 2),
+    ("cin5_cout24", 1, 7, 9, 5, 24, 3, 1, 1, 2, 2),
+    ("cout7_bytes", 1, 6, 6, 16, 7, 3, 1, 1, 2, 2),
+    ("k4608", 1, 7, 7, 512, 512, 3, 1, 1, 2, 2),
+    ("in4_out4", 1, 8, 8, 64, 64, 3, 1, 1, 4, 4),
+    ("in1_out1", 1, 9, 7, 32, 48, 3, 1, 1, 1, 1),
+    ("cout384_cin384", 1, 13, 13, 384, 384, 3, 1, 1, 2, 2),
+    ("valid_no_pad", 1, 10, 10, 64, 64, 3, 1, 0, 2, 2),
+    ("8bit_cin16", 1, 10, 10, 16, 32, 3, 2, 1, 8, 2),
+]
+
+
+@pytest.mark.parametrize("case", LAYERS, ids=[c[0] for c in LAYERS])
+def test_conv_layer_bit_exact(P, case):
+    name, n, h, w, cin, cout, k, st, pad, ib, ob = case
+    L = make_layer(name, h, w, cin, cout, k, st, pad, ib, ob)
+    seed = zlib.crc32(name.encode()) % 997
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, w, cin), ib)
+    want_acc, want = oracle_layer(L, x, p)
+    acc, got = gpu_layer(P, L, n, x, p)
+    assert np.array_equal(acc, want_acc), name
+    assert np.array_equal(got, want), name
+    if ob:
+        # the codes use more than one level (the comparison has teeth)
+        assert len(np.unique(want)) > 1
+
+
+U2_LAYERS = [
+    ("u2_3x3_64", 2, 14, 14, 64, 64, 3, 1, 1),
+    ("u2_stride2_128", 2, 15, 15, 64, 128, 3, 2, 1),
+    ("u2_cin16", 1, 18, 18, 16, 32, 3, 1, 1),
+    ("u2_cin32", 1, 12, 12, 32, 64, 3, 1, 1),
+    ("u2_k4608", 1, 7, 7, 512, 512, 3, 1, 1),
+    ("u2_cin96_5x5", 1, 9, 9, 96, 256, 5, 1, 2),
+]
+
+
+@pytest.mark.parametrize("case", U2_LAYERS, ids=[c[0] for c in U2_LAYERS])
+@pytest.mark.parametrize("io", [(U2, U2), (U2, I8), (I8, U2)],
+                         ids=["u2u2", "u2i8", "i8u2"])
+def test_conv_packed_layouts_bit_exact(P, case, io):
+    name, n, h, w, cin, cout, k, st, pad = case
+    L = make_layer(name, h, w, cin, cout, k, st, pad)
+    seed = zlib.crc32(name.encode()) % 991
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, w, cin), 2)
+    want_acc, want = oracle_layer(L, x, p)
+    acc, got = gpu_layer(P, L, n, x, p, in_layout=io[0], out_layout=io[1])
+    assert np.array_equal(acc, want_acc)
+    assert np.array_equal(got, expect_layout(want, io[1]))
+
+
+@pytest.mark.parametrize("sc_layout", [I8, U2], ids=["i8", "u2"])
+@pytest.mark.parametrize("shape", [(2, 10, 10, 64, 64), (1, 7, 7, 512, 512),
+                                   (1, 9, 11, 128, 128)])
+def test_identity_join_bit_exact(P, shape, sc_layout):
+    n, h, w, cin, cout = shape
+    L = make_layer("join_id", h, w, cin, cout, 3, 1, 1, join=("identity", "s"))
+    p = params_for(31 + h, L)
+    x = codes_for(31 + h, (n, h, w, cin), 2)
+    sc = codes_for(77 + h, (n, h, w, cout), 2)
+    want_acc, want = oracle_layer(L, x, p, shortcut=sc)
+    acc, got = gpu_layer(P, L, n, x, p, shortcut=sc, sc_layout=sc_layout)
+    assert np.array_equal(acc, want_acc)
+    assert np.array_equal(got, want)
+
+
+def test_conv_join_bit_exact(P):
+    # conv2 of a downsampling block: the shortcut is the int32 sum of a 1x1/2
+    # conv of the block input, computed by the GPU path itself first
+    n, hin, cin, cout = 2, 16, 64, 128
+    D = make_layer("down", hin, hin, cin, cout, 1, 2, 0, 2, 0)
+    L = make_layer("conv2", hin // 2, hin // 2, cout, cout, 3, 1, 1,
+                   join=("conv", "d", "down"))
+    pd = params_for(5, D)
+    p = params_for(6, L)
+    xin = codes_for(5, (n, hin, hin, cin), 2)
+    x = codes_for(6, (n, hin // 2, hin // 2, cout), 2)
+    want_d, _ = oracle_layer(D, xin, pd)
+    _, got_d = gpu_layer(P, D, n, xin, pd)
+    assert np.array_equal(got_d, want_d)
+    want_acc, want = oracle_layer(L, x, p, shortcut=want_d, down=pd)
+    acc, got = gpu_layer(P, L, n, x, p, shortcut=want_d, down=pd)
+    assert np.array_equal(acc, want_acc)
+    assert np.array_equal(got, want)
+
+
+def test_conv_without_dump_and_determinism(P):
+    L = make_layer("det", 28, 28, 128, 128, 3, 1, 1)
+    p = params_for(9, L)
+    x = codes_for(9, (4, 28, 28, 128), 2)
+    _, a = gpu_layer(P, L, 4, x, p, dump=False)
+    _, b = gpu_layer(P, L, 4, x, p, dump=False)
+    assert np.array_equal(a, b)
+    assert np.array_equal(a, oracle_layer(L, x, p)[1])
+
+
+def test_empty_batch_launches_nothing(P):
+    import torch
+    d = P.conv_desc(0, 8, 8, 64, 64, 3, 1, 1, 2, 2)
+    dummy = torch.zeros(16, dtype=torch.uint8, device=device())
+    thr = torch.zeros(64 * 4, dtype=torch.int32, device=device())
+    P.ifq_conv_forward(d, dummy, dummy, thr, dummy)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("case", [
+    ((2, 27, 27, 256), 3, 2, "valid"), ((1, 13, 13, 256), 3, 2, "valid"),
+    ((2, 224, 224, 64), 2, 2, "valid"), ((1, 13, 13, 512), 2, 1, "same"),
+    ((1, 9, 9, 20), 3, 2, "same"), ((3, 7, 5, 12), 2, 2, "valid"),
+    ((1, 8, 8, 3), 2, 2, "valid"),
+])
+@pytest.mark.parametrize("lay", [I8, U2], ids=["i8", "u2"])
+def test_maxpool_bit_exact(P, case, lay):
+    import torch
+    shape, k, st, mode = case
+    n, h, w, c = shape
+    if lay == U2 and c % 4:
+        pytest.skip("packed layout needs C % 4 == 0")
+    x = codes_for(h * 31 + c, shape, 2)
+    want = oracle.maxpool(x, k, st, mode)
+    m = P.IFQ_POOL_VALID if mode == "valid" else P.IFQ_POOL_SAME
+    d = P.pool_desc(n, h, w, c, k, st, m, 2, lay)
+    xd = upload_codes(P, x, lay)
+    nb = P.ifq_tensor_bytes(*want.shape, lay)
+    y = torch.empty(nb, dtype=torch.uint8, device=device())
+    P.ifq_maxpool_codes(d, xd, y)
+    torch.cuda.synchronize()
+    got = y.cpu().numpy()
+    assert np.array_equal(got, expect_layout(want, lay).reshape(-1))
+
+
+def test_maxpool_8bit_codes(P):
+    import torch
+    x = codes_for(3, (1, 10, 10, 16), 8)
+    want = oracle.maxpool(x, 2, 2, "valid")
+    d = P.pool_desc(1, 10, 10, 16, 2, 2, P.IFQ_POOL_VALID, 8, I8)
+    y = torch.empty(want.size, dtype=torch.uint8, device=device())
+    P.ifq_maxpool_codes(d, to_dev(x), y)
+    torch.cuda.synchronize()
+    assert np.array_equal(y.cpu().numpy(), want.reshape(-1))
+
+
+@pytest.mark.parametrize("npix,c", [(1, 4), (7, 12), (1000, 64), (33, 16)])
+def test_convert_codes_round_trip(P, npix, c):
+    import torch
+    x = codes_for(npix + c, (1, 1, npix, c), 2)
+    packed = torch.empty(npix * c // 4, dtype=torch.uint8, device=device())
+    P.ifq_convert_codes(npix, c, I8, U2, to_dev(x), packed)
+    back = torch.empty(npix * c, dtype=torch.uint8, device=device())
+    P.ifq_convert_codes(npix, c, U2, I8, packed, back)
+    torch.cuda.synchronize()
+    assert np.array_equal(packed.cpu().numpy(), olayout.pack2(x).reshape(-1))
+    assert np.array_equal(back.cpu().numpy(), x.reshape(-1))

@@ -1,0 +1,84 @@
+"""GPU parity of whole stacks through ifq_run_stack: every tensor the stack
+leaves in its workspace and its output must equal the oracle's bit for bit.
+
+Small cases use a reduced batch; the full cases run each stack at its own
+batch size in the launch configuration the benchmark times, and compare every
+output element against the oracle run on the host cores.
+"""
+import numpy as np
+import pytest
+
+from oracle import stack as ostack
+from oracle import layout as olayout
+from workloads import get_stack
+
+pytestmark = pytest.mark.gpu
+
+_ORACLE = {}
+
+
+def oracle_run(cfg, batch, variant):
+    key = (cfg, batch, variant)
+    if key not in _ORACLE:
+        params = ostack.stack_params(cfg, variant)
+        x = ostack.stack_x(cfg, batch)
+        _ORACLE.clear()
+        _ORACLE[key] = (params, x, ostack.run_stack(cfg, x=x, params=params))
+    return _ORACLE[key]
+
+
+@pytest.fixture(scope="module")
+def P():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1911_08076_amd as P
+    return P
+
+
+def check_stack(P, cfg, batch, layout, variant):
+    import torch
+    params, x, want = oracle_run(cfg, batch, variant)
+    layers = get_stack(cfg).layers
+    dev = P.DeviceStack(layers, params, batch, code_layout=layout)
+    xd = dev.upload_input(x)
+    y = dev.alloc_output()
+    dev.run(xd, y)
+    torch.cuda.synchronize()
+    got = dev.download_output(y)
+    assert got.shape == want["y"].shape
+    assert np.array_equal(got, want["y"]), "stack output differs"
+    checked = 1
+    for name, (shape, lay, bits) in dev.tensor_info.items():
+        if name in ("x", "y"):
+            continue
+        g = dev.read_slot(name)
+        w = want[name]
+        if lay == P.IFQ_LAYOUT_U2_NHWC_PACKED:
+            w = olayout.pack2(w)
+        assert np.array_equal(g, w), "slot %s differs" % name
+        checked += 1
+    # running again gives the same bytes (no state carried between runs)
+    y2 = dev.alloc_output()
+    dev.run(xd, y2)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
+    return checked
+
+
+SMALL = [(0, 1), (1, 2), (2, 1), (3, 2), (4, 1)]
+
+
+@pytest.mark.parametrize("layout", ["i8", "u2"])
+@pytest.mark.parametrize("cfg,batch", SMALL)
+def test_stack_small_batch(P, cfg, batch, layout):
+    for variant in ("calibrated", "plain"):
+        assert check_stack(P, cfg, batch, layout, variant) >= 1
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("layout", ["u2", "i8"])
+@pytest.mark.parametrize("cfg", [0, 1, 3, 4, 2])
+def test_stack_full_size(P, cfg, layout):
+    batch = get_stack(cfg).batch
+    check_stack(P, cfg, batch, layout, "plain")
