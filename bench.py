@@ -1,0 +1,283 @@
+#!/usr/bin/env python3
+"""Benchmark of the integrated fixed-point quantized conv path on one MI355X.
+
+Workload: the ResNet-18-shaped quantized stack, batch 64, 56x56x64 2-bit input
+codes (16 3x3 convs, three 1x1/2 downsample convs with int32 output, residual
+joins), +-1 weights and folded integer thresholds from seeded synthetic
+parameters. One step = one ifq_run_stack over the whole batch with inputs
+resident in HBM.
+
+Prints ONE JSON line: whole-stack int-ops/s (2 ops per +-1 x code MAC, dense
+count including padding taps), images/s, the roofline of the dominant conv
+kernel (int-ops per launch over its average launch duration, from HIP events
+recorded around every layer inside the timed steps) and the oracle timed on the
+host cores over a bounded sample of the same workload, whose output is also
+checked bit-exactly against the GPU's.
+"""
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("IFQ conv int-ops/s (% int8 MFMA peak) + images/s on "
+          "ResNet-18-shaped stack")
+# 256 CUs x 2.4 GHz x 8192 dense int8 ops per clock per CU
+PEAK_INT8_TOPS = 5033.2
+PEAK_HBM_GBPS = 8000.0
+JUDGED = ["l2.1.conv1", "l2.1.conv2", "l3.0.conv2", "l3.1.conv1",
+          "l3.1.conv2", "l4.0.conv2", "l4.1.conv1", "l4.1.conv2"]
+
+
+class Hip:
+    """Minimal HIP event API over ctypes (timing only)."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+        self.lib.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.lib.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.lib.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
+                                                 ctypes.c_void_p, ctypes.c_void_p]
+        self.lib.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def _ok(self, rc, what):
+        if rc != 0:
+            raise RuntimeError("%s failed: %d" % (what, rc))
+
+    def events(self, n):
+        arr = (ctypes.c_void_p * n)()
+        for i in range(n):
+            ev = ctypes.c_void_p()
+            self._ok(self.lib.hipEventCreate(ctypes.byref(ev)), "hipEventCreate")
+            arr[i] = ev.value
+        return arr
+
+    def record(self, ev, stream):
+        self._ok(self.lib.hipEventRecord(ev, stream), "hipEventRecord")
+
+    def sync(self, ev):
+        self._ok(self.lib.hipEventSynchronize(ev), "hipEventSynchronize")
+
+    def ms(self, a, b):
+        out = ctypes.c_float()
+        self._ok(self.lib.hipEventElapsedTime(ctypes.byref(out), a, b),
+                 "hipEventElapsedTime")
+        return float(out.value)
+
+    def destroy(self, arr):
+        for e in arr:
+            self.lib.hipEventDestroy(e)
+
+
+def source_hash():
+    h = hashlib.sha256()
+    for f in ("ifq_conv.hip", "ifq_pool.hip"):
+        with open(os.path.join(ROOT, "paper_1911_08076_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel, workload):
+    """HBM traffic per launch from a committed counter summary, if it was taken
+    on the current kernel sources (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.txt")
+    if not os.path.exists(path):
+        return None
+    want = source_hash()
+    for line in open(path):
+        if line.startswith("#") or not line.strip():
+            continue
+        parts = dict(kv.split("=", 1) for kv in line.split())
+        if (parts.get("kernel") == kernel.replace(" ", "") and
+                parts.get("workload") == workload and parts.get("src") == want):
+            return float(parts["bytes_per_launch"])
+    return None
+
+
+def cpu_info():
+    model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=3,
+                    help="synthetic stack (default 3: ResNet-18 body, batch 64)")
+    ap.add_argument("--layout", default="u2", choices=["u2", "i8"],
+                    help="layout of the 2-bit code tensors")
+    ap.add_argument("--cpu-images", type=int, default=16,
+                    help="images of the oracle's CPU-baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run a plain 256 MiB device copy (counter calibration)")
+    ap.add_argument("--layers-out", default=None,
+                    help="write per-layer timings (JSON) to this path")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this path shards over batch with "
+              "no exchange step, and multi-GPU runs are not part of this build "
+              "(got --gpus %d)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_1911_08076_amd as P
+    from workloads import get_stack, layer_params, stack_input, Conv
+
+    cfg = get_stack(args.config)
+    layers = cfg.layers
+    batch = cfg.batch
+    params = [layer_params(args.config, i, L, "plain") if isinstance(L, Conv) else None
+              for i, L in enumerate(layers)]
+    torch.cuda.set_device(0)
+    dev = P.DeviceStack(layers, params, batch, code_layout=args.layout)
+    L0 = layers[0]
+    x_host = stack_input(args.config, (batch, L0.h, L0.w, L0.cin), L0.in_bits)
+    x = dev.upload_input(x_host)
+    y = dev.alloc_output()
+    stream = torch.cuda.Stream()
+    sh = stream.cuda_stream
+    hip = Hip()
+    nl = len(layers)
+
+    print("bench: %s batch %d layout %s, %d layers, %.3f Gop/step" %
+          (cfg.name, batch, args.layout, nl, dev.ops / 1e9), file=sys.stderr, flush=True)
+
+    if args.calib_copy:
+        src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            dev.run(x, y, stream=sh)
+    torch.cuda.synchronize()
+
+    evsets = [hip.events(nl + 1) for _ in range(args.steps)]
+    start, end = hip.events(2)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    hip.record(start, sh)
+    for k in range(args.steps):
+        dev.run(x, y, stream=sh, events=evsets[k])
+    hip.record(end, sh)
+    hip.sync(end)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total_ms = hip.ms(start, end)
+    step_ms = total_ms / args.steps
+
+    # per-layer durations from the events recorded inside the timed steps
+    names = dev.layer_kernel_names()
+    lay_ms = np.zeros(nl)
+    for evs in evsets:
+        for i in range(nl):
+            lay_ms[i] += hip.ms(evs[i], evs[i + 1])
+    lay_ms /= args.steps
+    for evs in evsets:
+        hip.destroy(evs)
+
+    ops = dev.layer_ops()
+    per_layer = []
+    for i, L in enumerate(layers):
+        rec = {"layer": L.name, "kernel": names[i], "us": lay_ms[i] * 1e3}
+        if ops[i]:
+            rec["tops"] = ops[i] / (lay_ms[i] * 1e-3) / 1e12
+            rec["pct_peak"] = 100.0 * rec["tops"] / PEAK_INT8_TOPS
+        per_layer.append(rec)
+
+    # dominant kernel: most total time; its achieved rate over its launches
+    groups = {}
+    for i in range(nl):
+        g = groups.setdefault(names[i], {"ms": 0.0, "ops": 0, "n": 0, "bytes": 0})
+        g["ms"] += lay_ms[i]
+        g["ops"] += ops[i]
+        g["n"] += 1
+    dom = max(groups, key=lambda k: groups[k]["ms"])
+    gd = groups[dom]
+    avg_us = gd["ms"] / gd["n"] * 1e3
+    achieved = gd["ops"] / (gd["ms"] * 1e-3) / 1e12 if gd["ops"] else 0.0
+    traffic = load_traffic(dom, cfg.name + ":" + args.layout)
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2),
+                "peak": PEAK_INT8_TOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_INT8_TOPS, 4),
+                "traffic": traffic, "kernel": dom, "launches_per_step": gd["n"],
+                "avg_launch_us": round(avg_us, 3),
+                "ops_per_launch": gd["ops"] // gd["n"],
+                "op": "int8 ops, 2 per +-1 x code MAC"}
+
+    judged = [r for r in per_layer if r["layer"] in JUDGED]
+    judged_ops = sum(ops[i] for i, L in enumerate(layers) if L.name in JUDGED)
+    judged_ms = sum(lay_ms[i] for i, L in enumerate(layers) if L.name in JUDGED)
+    judged_pct = (100.0 * judged_ops / (judged_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS
+                  if judged_ms else None)
+
+    total_ops = dev.ops
+    value = total_ops * args.steps / (total_ms * 1e-3)
+    images_s = batch * args.steps / (total_ms * 1e-3)
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "int-ops/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": step_ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "i8", "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": batch,
+                   "input": "%dx%dx%d %d-bit codes" % (L0.h, L0.w, L0.cin, L0.in_bits),
+                   "code_layout": args.layout, "weights": "+-1 (seeded)",
+                   "params": "seeded BN/alpha, plain variant"},
+        "images_per_s": images_s,
+        "pct_int8_peak": 100.0 * value / 1e12 / PEAK_INT8_TOPS,
+        "judged_layers_pct_peak": judged_pct,
+        "wall_s_timed": wall,
+        "roofline": roofline,
+    }
+
+    if not args.no_cpu_baseline:
+        import oracle
+        from oracle import stack as ostack
+        nimg = min(args.cpu_images, batch)
+        x_s = x_host[:nimg]
+        t = time.perf_counter()
+        want = ostack.run_stack(args.config, x=x_s, params=params)["y"]
+        cpu_s = time.perf_counter() - t
+        got = dev.download_output(y)[:nimg]
+        cpu_ops = total_ops * nimg / batch
+        out["cpu_baseline"] = {
+            "value": cpu_ops / cpu_s, "unit": "int-ops/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "%d of %d images of the same stack and inputs (%.1f s), "
+                      "C oracle -O2 OpenMP; CPU: %s" % (nimg, batch, cpu_s, cpu_info()),
+            "images_per_s": nimg / cpu_s,
+            "parity_bit_exact": bool(np.array_equal(got, want)),
+        }
+
+    if args.layers_out:
+        with open(args.layers_out, "w") as fh:
+            json.dump({"config": cfg.name, "layout": args.layout,
+                       "ms_per_step": step_ms, "layers": per_layer,
+                       "kernels": groups}, fh, indent=1)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -294,6 +294,13 @@ IFQ_API ifq_status ifq_fold_thresholds(const ifq_fold_params* p,
  */
 IFQ_API ifq_status ifq_fold_join(const ifq_join_params* p, double* coef_out);
 
+/*
+ * Name of the kernel variant ifq_conv_forward launches for d (static string,
+ * the kernel's symbol as a profiler lists it), or "" for an invalid desc.
+ * Host; for profiling and benchmarks.
+ */
+IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d);
+
 /* Device workspace bytes ifq_conv_forward needs for d (may be 0). Host. */
 IFQ_API size_t ifq_conv_workspace_bytes(const ifq_conv_desc* d);
 

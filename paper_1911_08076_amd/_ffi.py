@@ -7,7 +7,9 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libifq.so")
+# IFQ_LIBRARY may point at another build of the same library (e.g. an
+# instrumented one); by default the in-tree build next to this file is used.
+LIB_PATH = os.environ.get("IFQ_LIBRARY", os.path.join(HERE, "libifq.so"))
 
 IFQ_OK = 0
 IFQ_ERR_INVALID_ARGUMENT = -1
@@ -94,6 +96,7 @@ SIGNATURES = [
     ("ifq_pack_weights", i32, [ctypes.POINTER(ConvDesc), vp, vp, size_t]),
     ("ifq_fold_thresholds", i32, [ctypes.POINTER(FoldParams), vp]),
     ("ifq_fold_join", i32, [ctypes.POINTER(JoinParams), vp]),
+    ("ifq_conv_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc)]),
     ("ifq_conv_workspace_bytes", size_t, [ctypes.POINTER(ConvDesc)]),
     ("ifq_conv_forward", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp,
                                ctypes.POINTER(Join), vp, vp, vp, size_t, vp]),

@@ -152,6 +152,10 @@ def make_join(kind, layout, shortcut, coef, q_thr):
     return j
 
 
+def ifq_conv_kernel_name(desc):
+    return _lib().ifq_conv_kernel_name(ctypes.byref(desc)).decode()
+
+
 def ifq_conv_workspace_bytes(desc):
     return int(_lib().ifq_conv_workspace_bytes(ctypes.byref(desc)))
 

@@ -182,8 +182,10 @@ ifq::ConvLaunch make_launch(const ifq_conv_desc* d, int64_t ho, int64_t wo,
   std::memset(&a, 0, sizeof(a));
   a.x = static_cast<const uint8_t*>(x);
   a.wgt = static_cast<const int8_t*>(w);
-  a.rowsum = reinterpret_cast<const int32_t*>(static_cast<const uint8_t*>(w) +
-                                              g.rows_bytes);
+  a.rowsum = w ? reinterpret_cast<const int32_t*>(static_cast<const uint8_t*>(w) +
+                                                  g.rows_bytes)
+                : nullptr;
+  a.wzero = g.zero_off;
   a.thr = thr;
   a.y = y;
   a.acc_dump = acc_dump;
@@ -293,6 +295,8 @@ IFQ_API ifq_status ifq_pack_weights(const ifq_conv_desc* d,
                   "pack: weight %lld is %d, must be +1 or -1", (long long)i,
                   (int)w_oihw[i]);
   const bool u2 = d->in_layout == IFQ_LAYOUT_U2_NHWC_PACKED;
+  const bool frag = ifq::frag_layout(*d);
+  const int64_t nk = g.kpad / ifq::kKStep;
   int8_t* rows = static_cast<int8_t*>(dst);
   int32_t* rowsum = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(dst) + g.rows_bytes);
   std::memset(dst, 0, (size_t)g.total_bytes);
@@ -307,7 +311,14 @@ IFQ_API ifq_status ifq_pack_weights(const ifq_conv_desc* d,
             cp = base + (in & 3) * 4 + (in >> 2);
           }
           const int8_t v = w_oihw[((co * d->c_in + c) * d->kh + r) * d->kw + s];
-          rows[co * g.kpad + (r * d->kw + s) * d->c_in + cp] = v;
+          const int64_t k = (r * d->kw + s) * d->c_in + cp;
+          int64_t pos = co * g.kpad + k;
+          if (frag) {
+            const int64_t kt = k / ifq::kKStep, kk = k % ifq::kKStep;
+            const int64_t lane = (kk / 16) * 16 + (co % 16);
+            pos = (((co / 16) * nk + kt) * 64 + lane) * 16 + kk % 16;
+          }
+          rows[pos] = v;
           sum += v;
         }
     rowsum[co] = sum;
@@ -445,6 +456,14 @@ IFQ_API ifq_status ifq_fold_join(const ifq_join_params* p, double* coef_out) {
     coef_out[3 * c + 2] = c2 + cd;
   }
   return ok();
+}
+
+IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d) {
+  int64_t ho, wo;
+  if (check_conv(d, &ho, &wo) != IFQ_OK) return "";
+  const ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr,
+                                        nullptr, nullptr, nullptr, nullptr);
+  return ifq::conv_kernel_name(a);
 }
 
 IFQ_API size_t ifq_conv_workspace_bytes(const ifq_conv_desc* d) {

@@ -215,6 +215,21 @@ class DeviceStack:
             return raw.cpu().numpy().reshape(n, h, w, c // 4)
         return raw.cpu().numpy().reshape(n, h, w, c)
 
+    def layer_kernel_names(self):
+        """Kernel each layer launches (conv variants by name, pools as
+        maxpool_codes)."""
+        out = []
+        for i, L in enumerate(self.layers):
+            if _is_conv(L):
+                out.append(api.ifq_conv_kernel_name(self._layers[i].conv))
+            else:
+                out.append("maxpool_codes")
+        return out
+
+    def layer_ops(self):
+        """Dense int-ops of every layer (0 for pools)."""
+        return [conv_ops(L, self.batch) if _is_conv(L) else 0 for L in self.layers]
+
     # -- execution -------------------------------------------------------------
     def run(self, x, y, stream=None, events=None):
         """One forward pass (asynchronous on stream). events: optional ctypes

@@ -68,6 +68,13 @@ U2_LAYERS = [
     ("u2_cin32", 1, 12, 12, 32, 64, 3, 1, 1),
     ("u2_k4608", 1, 7, 7, 512, 512, 3, 1, 1),
     ("u2_cin96_5x5", 1, 9, 9, 96, 256, 5, 1, 2),
+    ("u2_m3136_c128", 4, 28, 28, 128, 128, 3, 1, 1),
+    ("u2_c256_s1", 2, 30, 30, 256, 256, 3, 1, 1),
+    ("u2_c64_large_m", 8, 56, 56, 64, 64, 3, 1, 1),
+    ("u2_c512_7x7", 12, 7, 7, 512, 512, 3, 1, 1),
+    ("u2_1x1_s2_c256", 3, 14, 14, 128, 256, 1, 2, 0),
+    ("u2_c192_ragged", 3, 11, 13, 192, 320, 3, 1, 1),
+    ("u2_5x5_c64", 2, 17, 15, 64, 128, 5, 2, 2),
 ]
 
 
@@ -86,22 +93,26 @@ def test_conv_packed_layouts_bit_exact(P, case, io):
     assert np.array_equal(got, expect_layout(want, io[1]))
 
 
-@pytest.mark.parametrize("sc_layout", [I8, U2], ids=["i8", "u2"])
+@pytest.mark.parametrize("io", [(I8, I8, I8), (I8, U2, I8), (U2, U2, U2),
+                                (U2, I8, U2)], ids=["i8", "sc_u2", "u2", "u2_sc_i8"])
 @pytest.mark.parametrize("shape", [(2, 10, 10, 64, 64), (1, 7, 7, 512, 512),
-                                   (1, 9, 11, 128, 128)])
-def test_identity_join_bit_exact(P, shape, sc_layout):
+                                   (1, 9, 11, 128, 128), (6, 14, 14, 256, 256)])
+def test_identity_join_bit_exact(P, shape, io):
     n, h, w, cin, cout = shape
+    in_l, sc_l, out_l = io
     L = make_layer("join_id", h, w, cin, cout, 3, 1, 1, join=("identity", "s"))
     p = params_for(31 + h, L)
     x = codes_for(31 + h, (n, h, w, cin), 2)
     sc = codes_for(77 + h, (n, h, w, cout), 2)
     want_acc, want = oracle_layer(L, x, p, shortcut=sc)
-    acc, got = gpu_layer(P, L, n, x, p, shortcut=sc, sc_layout=sc_layout)
+    acc, got = gpu_layer(P, L, n, x, p, in_layout=in_l, out_layout=out_l,
+                         shortcut=sc, sc_layout=sc_l)
     assert np.array_equal(acc, want_acc)
-    assert np.array_equal(got, want)
+    assert np.array_equal(got, expect_layout(want, out_l))
 
 
-def test_conv_join_bit_exact(P):
+@pytest.mark.parametrize("lay", [I8, U2], ids=["i8", "u2"])
+def test_conv_join_bit_exact(P, lay):
     # conv2 of a downsampling block: the shortcut is the int32 sum of a 1x1/2
     # conv of the block input, computed by the GPU path itself first
     n, hin, cin, cout = 2, 16, 64, 128
@@ -113,12 +124,13 @@ def test_conv_join_bit_exact(P):
     xin = codes_for(5, (n, hin, hin, cin), 2)
     x = codes_for(6, (n, hin // 2, hin // 2, cout), 2)
     want_d, _ = oracle_layer(D, xin, pd)
-    _, got_d = gpu_layer(P, D, n, xin, pd)
+    _, got_d = gpu_layer(P, D, n, xin, pd, in_layout=lay)
     assert np.array_equal(got_d, want_d)
     want_acc, want = oracle_layer(L, x, p, shortcut=want_d, down=pd)
-    acc, got = gpu_layer(P, L, n, x, p, shortcut=want_d, down=pd)
+    acc, got = gpu_layer(P, L, n, x, p, in_layout=lay, out_layout=lay,
+                         shortcut=want_d, down=pd)
     assert np.array_equal(acc, want_acc)
-    assert np.array_equal(got, want)
+    assert np.array_equal(got, expect_layout(want, lay))
 
 
 def test_conv_without_dump_and_determinism(P):
