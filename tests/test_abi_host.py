@@ -1,0 +1,496 @@
+"""Host side of the C ABI, on the CPU: the library loads and exports every
+entry point include/ifq.h declares, the weight packer writes the documented
+layout, the threshold and join folds equal the oracle's bit for bit (two
+separate implementations of the same fixed fp64 order of Sec. 3.2), and every
+validation error is returned before anything is launched.
+
+No test here launches a kernel: every device entry point is called only with
+arguments its host-side validation rejects.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_1911_08076_amd as P
+from paper_1911_08076_amd import _ffi
+from workloads import get_stack, layer_params, Conv
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ifq.h")
+
+OK = 0
+EINVAL = -1
+EUNSUP = -2
+EBUF = -4
+I8, U2, I32 = 0, 1, 2
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"IFQ_API\s+[\w\s\*]+?\b(ifq_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_symbols()
+    for want in ("ifq_pack_weights", "ifq_fold_thresholds", "ifq_conv_forward",
+                 "ifq_maxpool_codes", "ifq_run_stack"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(_ffi.LIB_PATH)
+    names = declared_symbols()
+    out = subprocess.run(["nm", "-D", "--defined-only", _ffi.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    for n in names:
+        assert n in exported, n
+        assert getattr(lib, n) is not None
+    # the binding wraps exactly the declared set
+    assert sorted(s[0] for s in _ffi.SIGNATURES) == names
+    # nothing else with the library's prefix leaks out
+    assert {e for e in exported if e.startswith("ifq_")} == set(names)
+
+
+def test_version_and_no_error_text():
+    assert P.ifq_version().endswith("gfx950")
+    P.ifq_tensor_bytes(1, 1, 1, 4, U2)
+
+
+# --- tensor sizes -----------------------------------------------------------
+
+def test_tensor_bytes_of_the_layouts():
+    assert P.ifq_tensor_bytes(2, 3, 5, 8, I8) == 240
+    assert P.ifq_tensor_bytes(2, 3, 5, 8, U2) == 60
+    assert P.ifq_tensor_bytes(2, 3, 5, 8, I32) == 960
+    assert P.ifq_tensor_bytes(1, 1, 1, 6, U2) == 0     # C % 4 != 0
+    assert P.ifq_tensor_bytes(1, 1, 1, 4, 7) == 0      # unknown layout
+    assert P.ifq_tensor_bytes(-1, 1, 1, 4, I8) == 0
+
+
+def test_tensor_bytes_matches_table4_conv1_map():
+    # Table 4: the conv1 feature map of IFQ-AlexNet, 55x55x96 at k = 2 bits,
+    # is 0.58 Mbit (printed 0.6); the packed layout stores exactly that
+    nb = P.ifq_tensor_bytes(1, 55, 55, 96, U2)
+    assert nb == 72600
+    assert abs(nb * 8 / 1e6 - 0.6) < 0.05
+
+
+@pytest.mark.parametrize("h,k,s,p,want", [(28, 3, 1, 1, 28), (56, 3, 2, 1, 28),
+                                         (56, 1, 2, 0, 28), (27, 5, 1, 2, 27),
+                                         (416, 3, 1, 1, 416), (7, 7, 1, 0, 1)])
+def test_conv_output_dims(h, k, s, p, want):
+    d = P.conv_desc(1, h, h, 16, 16, k, s, p, 2, 2)
+    assert P.ifq_conv_output_dims(d) == (want, want)
+
+
+# --- weight packer ------------------------------------------------------------
+
+def unpack_blob(blob, cout, cin, kh, kw, u2, frag):
+    """Reads W_b back out of a packed blob following the documented layout."""
+    k = kh * kw * cin
+    kpad = -(-k // 64) * 64
+    cpad = -(-cout // 16) * 16
+    nk = kpad // 64
+    rows = np.frombuffer(blob[:cpad * kpad].tobytes(), dtype=np.int8)
+    if frag:
+        # [row block][k step][lane][16 bytes], lane = 16*(kk/16) + row%16
+        r = rows.reshape(cpad // 16, nk, 4, 16, 16)     # rb, kt, g, i, b
+        mat = r.transpose(0, 3, 1, 2, 4).reshape(cpad, kpad)
+    else:
+        mat = rows.reshape(cpad, kpad)
+    rowsum = np.frombuffer(blob[cpad * kpad:cpad * kpad + 4 * cpad].tobytes(),
+                           dtype=np.int32)
+    w = np.zeros((cout, cin, kh, kw), dtype=np.int8)
+    for r_ in range(kh):
+        for s_ in range(kw):
+            for c in range(cin):
+                cp = c
+                if u2:
+                    base, i = c & ~15, c & 15
+                    cp = base + (i & 3) * 4 + (i >> 2)
+                w[:, c, r_, s_] = mat[:cout, (r_ * kw + s_) * cin + cp]
+    return w, mat, rowsum, k
+
+
+@pytest.mark.parametrize("shape,layout", [
+    ((64, 64, 3, 3), I8), ((64, 64, 3, 3), U2), ((30, 512, 1, 1), I8),
+    ((16, 3, 3, 3), I8), ((256, 96, 5, 5), I8), ((128, 192, 3, 3), U2),
+    ((48, 32, 3, 3), U2), ((7, 16, 3, 3), I8)])
+def test_pack_weights_layout(shape, layout, rng):
+    cout, cin, kh, kw = shape
+    w = (rng.integers(0, 2, size=shape, dtype=np.int8) * 2 - 1).astype(np.int8)
+    d = P.conv_desc(1, 9, 9, cin, cout, kh, 1, kh // 2, 2, 2, layout,
+                    kw=kw)
+    blob = P.ifq_pack_weights(d, w)
+    assert blob.nbytes == P.ifq_packed_weight_bytes(d)
+    frag = layout == U2 and cin % 64 == 0
+    back, mat, rowsum, k = unpack_blob(blob, cout, cin, kh, kw, layout == U2, frag)
+    assert np.array_equal(back, w)
+    # padding rows and K columns are zero; row sums are sum_k W[co][k]
+    assert not mat[cout:].any() and not mat[:, k:].any()
+    assert np.array_equal(rowsum[:cout], w.reshape(cout, -1).sum(1))
+    assert not rowsum[cout:].any()
+    # the trailing zero block the kernels read for out-of-range fragments
+    assert not blob[-1024:].any()
+
+
+def test_pack_rejects_non_binary_weight_and_leaves_dst(rng):
+    d = P.conv_desc(1, 8, 8, 16, 16, 3, 1, 1, 2, 2)
+    w = np.ones((16, 16, 3, 3), dtype=np.int8)
+    w[3, 2, 1, 0] = 0
+    dst = np.full(P.ifq_packed_weight_bytes(d), 0x5A, dtype=np.uint8)
+    with pytest.raises(P.IfqError) as e:
+        P.ifq_pack_weights(d, w, dst)
+    assert e.value.status == EINVAL
+    assert (dst == 0x5A).all()
+
+
+def test_pack_rejects_small_buffer():
+    d = P.conv_desc(1, 8, 8, 16, 16, 3, 1, 1, 2, 2)
+    w = np.ones((16, 16, 3, 3), dtype=np.int8)
+    dst = np.zeros(P.ifq_packed_weight_bytes(d) - 1, dtype=np.uint8)
+    with pytest.raises(P.IfqError) as e:
+        P.ifq_pack_weights(d, w, dst)
+    assert e.value.status == EBUF
+
+
+# --- threshold fold: library vs oracle ---------------------------------------
+
+def lib_fold(p, k, in_bits, out_bits=2):
+    return P.ifq_fold_thresholds(len(p["alpha"]), in_bits, out_bits, k,
+                                 p["alpha"], p["beta_in"], p["q_thr"],
+                                 bias=p["bias"], mean=p["mean"], var=p["var"],
+                                 gamma=p["gamma"], bn_beta=p["bn_beta"],
+                                 eps=p["eps"])
+
+
+def orc_fold(p, k, in_bits):
+    return oracle.fold(p["alpha"], p["beta_in"], p["mean"], p["var"], p["gamma"],
+                       p["bn_beta"], p["eps"], p["q_thr"], k, in_bits,
+                       bias=p["bias"])
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("variant", ["plain", "calibrated"])
+def test_fold_equals_oracle_on_every_stack_layer(cfg, variant):
+    layers = get_stack(cfg).layers
+    n = 0
+    for i, L in enumerate(layers):
+        if not isinstance(L, Conv) or L.out_bits == 0:
+            continue
+        p = layer_params(cfg, i, L, variant)
+        k = L.k * L.k * L.cin
+        rec = lib_fold(p, k, L.in_bits, L.out_bits)
+        s, t = orc_fold(p, k, L.in_bits)
+        assert np.array_equal(rec[:, 0], s)
+        assert np.array_equal(rec[:, 1:], t)
+        n += 1
+    assert n >= 1
+
+
+def edge_params(rng, c=64):
+    p = dict(alpha=rng.uniform(0.01, 0.1, c), bias=rng.normal(0, 0.3, c),
+             mean=rng.normal(0, 2, c), var=rng.uniform(0.5, 2, c),
+             gamma=rng.uniform(0.5, 1.5, c), bn_beta=rng.normal(0, 1, c),
+             eps=1e-5, beta_in=0.5, q_thr=np.array([0.25, 0.75, 1.25]))
+    p["gamma"][:8] *= -1          # flipped channels
+    p["gamma"][8:10] = 0.0        # constant-code channels
+    p["bn_beta"][8] = 1.0         # constant code 2
+    p["bn_beta"][9] = -3.0        # constant code 0
+    # channels whose thresholds land exactly on integers: with var+eps = 1,
+    # gamma = 1, bn_beta = 0, alpha*beta = 1/4 and mean = m, t_i = 4*(q_i + m)
+    for c_ in (10, 11):
+        p["alpha"][c_] = 0.5
+        p["var"][c_] = 1.0 - 1e-5
+        p["gamma"][c_] = 1.0 if c_ == 10 else -1.0
+        p["bn_beta"][c_] = 0.0
+        p["mean"][c_] = 0.75
+        p["bias"][c_] = 0.0
+    p["alpha"][12] = 1e-6        # thresholds far outside the reachable sums
+    return p
+
+
+def test_fold_edge_cases_equal_oracle(rng):
+    p = edge_params(rng)
+    k = 576
+    rec = lib_fold(p, k, 2)
+    s, t = orc_fold(p, k, 2)
+    assert np.array_equal(rec[:, 0], s)
+    assert np.array_equal(rec[:, 1:], t)
+    bound = k * 3
+    # gamma == 0: the constant code #{i : bn_beta > q_i}
+    acc = np.arange(-bound, bound + 1, dtype=np.int64)
+    for c_, want in ((8, 2), (9, 0)):
+        sv = rec[c_, 0] * acc
+        code = sum((sv > rec[c_, i]).astype(int) for i in (1, 2, 3))
+        assert (code == want).all()
+    # integer-valued thresholds (t_i = 3 + 4 q_i for gamma = 1, 3 - 4 q_i for
+    # gamma = -1): a sum that lands exactly on one makes Y_bn equal q_i, and
+    # Eq. (3) sends that tie to the lower code in both directions
+    assert list(rec[10, 1:]) == [4, 6, 8]
+    assert list(rec[11, 1:]) == [-2, 0, 2]
+    for c_, ties in ((10, (4, 6, 8)), (11, (2, 0, -2))):
+        for i, a in enumerate(ties):
+            sv = rec[c_, 0] * a
+            code = sum(int(sv > rec[c_, j]) for j in (1, 2, 3))
+            ybn = p["gamma"][c_] * (0.25 * a - 0.75)
+            assert code == sum(int(ybn > q) for q in p["q_thr"])
+            assert ybn == p["q_thr"][i]
+    # clamped to [-B-1, B]
+    assert rec[12, 1:].min() >= -bound - 1 and rec[12, 1:].max() <= bound
+
+
+@pytest.mark.parametrize("field,value", [
+    ("alpha", 0.0), ("alpha", -0.1), ("alpha", np.nan), ("var", -2.0),
+    ("gamma", np.nan), ("mean", np.inf), ("bn_beta", np.nan)])
+def test_fold_rejects_bad_channel(field, value, rng):
+    p = edge_params(rng, 16)
+    p[field] = p[field].copy()
+    p[field][3] = value
+    with pytest.raises(P.IfqError) as e:
+        lib_fold(p, 576, 2)
+    assert e.value.status == EINVAL
+
+
+@pytest.mark.parametrize("q", [[0.25, 0.25, 1.25], [0.75, 0.25, 1.25],
+                               [0.25, np.nan, 1.25]])
+def test_fold_rejects_bad_quantizer(q, rng):
+    p = edge_params(rng, 16)
+    p["q_thr"] = np.array(q)
+    with pytest.raises(P.IfqError):
+        lib_fold(p, 576, 2)
+
+
+def test_fold_rejects_bad_beta_and_bits(rng):
+    p = edge_params(rng, 16)
+    p["beta_in"] = 0.0
+    with pytest.raises(P.IfqError):
+        lib_fold(p, 576, 2)
+    p = edge_params(rng, 16)
+    with pytest.raises(P.IfqError):
+        lib_fold(p, 576, 9)
+    with pytest.raises(P.IfqError):
+        lib_fold(p, 576, 2, out_bits=5)
+
+
+# --- join fold: library vs oracle ----------------------------------------------
+
+@pytest.mark.parametrize("variant", ["plain", "calibrated"])
+def test_join_coefficients_equal_oracle(variant):
+    layers = get_stack(3).layers
+    names = {L.name: i for i, L in enumerate(layers)}
+    n = 0
+    for i, L in enumerate(layers):
+        if not isinstance(L, Conv) or L.join is None:
+            continue
+        p = layer_params(3, i, L, variant)
+        if L.join[0] == "identity":
+            got = P.ifq_fold_join(P.IFQ_JOIN_IDENTITY, p, p["beta_in"])
+            want = oracle.join_coeffs("identity", p, p["beta_in"], p["beta_in"])
+        else:
+            j = names[L.join[2]]
+            pd = layer_params(3, j, layers[j], variant)
+            got = P.ifq_fold_join(P.IFQ_JOIN_CONV, p, pd["beta_in"], down=pd)
+            want = oracle.join_coeffs("conv", p, p["beta_in"], pd["beta_in"],
+                                      down=pd)
+        assert np.array_equal(got.view(np.uint64), want.view(np.uint64))
+        n += 1
+    assert n == 8
+
+
+def test_join_rejects_bad_kind_and_alpha():
+    L = get_stack(3).layers[1]
+    p = layer_params(3, 1, L)
+    with pytest.raises(P.IfqError):
+        P.ifq_fold_join(7, p, 0.5)
+    q = dict(p)
+    q["alpha"] = p["alpha"].copy()
+    q["alpha"][0] = -1.0
+    with pytest.raises(P.IfqError):
+        P.ifq_fold_join(P.IFQ_JOIN_IDENTITY, q, 0.5)
+
+
+# --- validation of device entry points (nothing is launched) -------------------
+
+def status_of(fn, *args):
+    lib = _ffi.load()
+    return getattr(lib, fn)(*args)
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
+
+
+@pytest.mark.parametrize("desc,want", [
+    (dict(n=-1), EINVAL), (dict(h=0), EINVAL), (dict(c_in=0), EINVAL),
+    (dict(kh=0), EINVAL), (dict(stride=0), EINVAL), (dict(pad=-1), EINVAL),
+    (dict(h=2, pad=0), EINVAL),                       # filter larger than input
+    (dict(in_bits=9), EINVAL), (dict(out_bits=5), EINVAL),
+    (dict(in_layout=U2, in_bits=8), EINVAL),
+    (dict(in_layout=U2, c_in=6), EINVAL),
+    (dict(in_layout=U2, c_in=20), EUNSUP),             # C % 16 for packed input
+    (dict(in_layout=5), EINVAL),
+    (dict(out_bits=0, out_layout=I8), EINVAL),
+    (dict(out_layout=U2, out_bits=4), EINVAL),
+    (dict(out_layout=U2, c_out=30), EINVAL),
+    (dict(out_layout=I32), EINVAL),
+    (dict(n=100000, h=224, w=224, c_in=64), EUNSUP),    # 2^31-byte tensors
+])
+def test_conv_forward_rejects_bad_desc(desc, want):
+    base = dict(n=1, h=8, w=8, c_in=64, c_out=64, kh=3, kw=3, stride=1, pad=1,
+                in_bits=2, out_bits=2, in_layout=I8, out_layout=I8)
+    base.update(desc)
+    d = _ffi.ConvDesc(**base)
+    st = status_of("ifq_conv_forward", ctypes.byref(d), FAKE, FAKE, FAKE, None,
+                   FAKE, None, None, 0, None)
+    assert st == want
+    assert P.ifq_last_error() != ""
+    assert P.ifq_packed_weight_bytes(d) == 0
+
+
+def test_conv_forward_rejects_bad_pointers():
+    d = P.conv_desc(1, 8, 8, 64, 64, 3, 1, 1, 2, 2)
+    # thresholds required for a code output, forbidden for an int32 output
+    st = status_of("ifq_conv_forward", ctypes.byref(d), FAKE, FAKE, None, None,
+                   FAKE, None, None, 0, None)
+    assert st == EINVAL
+    d0 = P.conv_desc(1, 8, 8, 64, 64, 3, 1, 1, 2, 0)
+    st = status_of("ifq_conv_forward", ctypes.byref(d0), FAKE, FAKE, FAKE, None,
+                   FAKE, None, None, 0, None)
+    assert st == EINVAL
+    st = status_of("ifq_conv_forward", ctypes.byref(d), None, FAKE, FAKE, None,
+                   FAKE, None, None, 0, None)
+    assert st == EINVAL
+
+
+def test_conv_forward_rejects_bad_join():
+    d = P.conv_desc(1, 8, 8, 64, 64, 3, 1, 1, 2, 2)
+    coef = np.zeros((64, 3))
+    for kind, layout, q, want in [
+            (9, I8, [0.25, 0.75, 1.25], EINVAL),
+            (P.IFQ_JOIN_IDENTITY, I32, [0.25, 0.75, 1.25], EINVAL),
+            (P.IFQ_JOIN_CONV, I8, [0.25, 0.75, 1.25], EINVAL),
+            (P.IFQ_JOIN_IDENTITY, I8, [0.25, 0.75], EINVAL),
+            (P.IFQ_JOIN_IDENTITY, I8, [0.75, 0.25, 1.25], EINVAL)]:
+        j = P.make_join(kind, layout, None, coef, q)
+        j.shortcut = 0x1000
+        st = status_of("ifq_conv_forward", ctypes.byref(d), FAKE, FAKE, None,
+                       ctypes.byref(j), FAKE, None, None, 0, None)
+        assert st == want, (kind, layout, q)
+    # a join with thresholds given as well
+    j = P.make_join(P.IFQ_JOIN_IDENTITY, I8, None, coef, [0.25, 0.75, 1.25])
+    j.shortcut = 0x1000
+    st = status_of("ifq_conv_forward", ctypes.byref(d), FAKE, FAKE, FAKE,
+                   ctypes.byref(j), FAKE, None, None, 0, None)
+    assert st == EINVAL
+
+
+@pytest.mark.parametrize("pool,want", [
+    (dict(k=0), EINVAL), (dict(stride=0), EINVAL), (dict(mode=3), EINVAL),
+    (dict(k=9), EINVAL), (dict(layout=U2, c=6), EINVAL),
+    (dict(layout=U2, bits=8), EINVAL), (dict(bits=0), EINVAL),
+    (dict(layout=I32), EINVAL)])
+def test_maxpool_rejects_bad_desc(pool, want):
+    base = dict(n=1, h=8, w=8, c=16, k=2, stride=2, mode=0, bits=2, layout=I8)
+    base.update(pool)
+    d = _ffi.PoolDesc(**base)
+    st = status_of("ifq_maxpool_codes", ctypes.byref(d), FAKE, FAKE, None)
+    assert st == want
+
+
+def test_convert_rejects_bad_args():
+    assert status_of("ifq_convert_codes", 10, 6, I8, U2, FAKE, FAKE, None) == EINVAL
+    assert status_of("ifq_convert_codes", 10, 8, I8, I8, FAKE, FAKE, None) == EINVAL
+    assert status_of("ifq_convert_codes", 10, 8, I8, U2, None, FAKE, None) == EINVAL
+
+
+# --- stack planning -------------------------------------------------------------
+
+def make_stack(layers, batch=1, layout="i8"):
+    """ifq_stack of fake device pointers (planning and validation only)."""
+    slots = {"x": 0, "y": 1}
+    lay_of = {}
+    arr = (_ffi.Layer * len(layers))()
+    for i, L in enumerate(layers):
+        for s in (L.src, L.dst):
+            slots.setdefault(s, len(slots))
+        rec = arr[i]
+        rec.src, rec.dst, rec.join_src = slots[L.src], slots[L.dst], -1
+        lin = lay_of.get(L.src, U2 if layout == "u2" else I8)
+        if isinstance(L, Conv):
+            lout = I32 if L.out_bits == 0 else (U2 if layout == "u2" else I8)
+            rec.kind = P.IFQ_LAYER_CONV
+            rec.conv = P.conv_desc(batch, L.h, L.w, L.cin, L.cout, L.k, L.stride,
+                                   L.pad, L.in_bits, L.out_bits, lin, lout)
+            rec.w_packed = 0x1000
+            if L.join is None and L.out_bits:
+                rec.thr = 0x1000
+            if L.join is not None:
+                rec.join = P.make_join(
+                    P.IFQ_JOIN_IDENTITY if L.join[0] == "identity" else P.IFQ_JOIN_CONV,
+                    lay_of.get(L.join[1], lin) if L.join[0] == "identity" else I32,
+                    None, np.zeros(3), L.out_bits and [0.25, 0.75, 1.25])
+                rec.join.coef = 0x1000
+                rec.join_src = slots[L.join[1]]
+        else:
+            lout = lin
+            rec.kind = P.IFQ_LAYER_POOL
+            rec.pool = P.pool_desc(batch, L.h, L.w, L.c, L.k, L.stride,
+                                   0 if L.mode == "valid" else 1, L.bits, lin)
+        lay_of[L.dst] = lout
+    st = _ffi.Stack(len(layers), len(slots),
+                    ctypes.cast(arr, ctypes.POINTER(_ffi.Layer)), None)
+    st._keep = arr
+    return st, slots
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 3, 4])
+def test_stack_workspace_covers_every_slot(cfg):
+    layers = get_stack(cfg).layers
+    for layout in ("i8", "u2"):
+        st, slots = make_stack(layers, 2, "i8" if cfg == 4 else layout)
+        total = P.ifq_stack_workspace_bytes(st)
+        spans = []
+        for name, k in slots.items():
+            if k < 2:
+                continue
+            off, nb = P.ifq_stack_slot_info(st, k)
+            assert off % 256 == 0 and off + nb <= total
+            spans.append((off, off + nb))
+        spans.sort()
+        for (a0, a1), (b0, b1) in zip(spans, spans[1:]):
+            assert a1 <= b0  # slots do not overlap
+
+
+def test_stack_rejects_unwritten_slot_and_small_workspace():
+    layers = list(get_stack(1).layers)
+    st, _ = make_stack(layers)
+    total = P.ifq_stack_workspace_bytes(st)
+    assert total > 0
+    lib = _ffi.load()
+    assert lib.ifq_run_stack(ctypes.byref(st), FAKE, FAKE, FAKE, total - 1,
+                             None) == EBUF
+    # layer 2 reads a slot nobody wrote
+    st.layers[2].src = st.n_slots - 1
+    st.layers[1].dst = 3
+    assert P.ifq_stack_workspace_bytes(st) == 0
+    assert lib.ifq_run_stack(ctypes.byref(st), FAKE, FAKE, FAKE, 1 << 30,
+                             None) == EINVAL
+
+
+def test_stack_rejects_bad_layer_kind_and_slots():
+    layers = list(get_stack(0).layers)
+    st, _ = make_stack(layers)
+    lib = _ffi.load()
+    st.layers[0].kind = 5
+    assert lib.ifq_run_stack(ctypes.byref(st), FAKE, FAKE, FAKE, 1 << 20,
+                             None) == EINVAL
+    st, _ = make_stack(layers)
+    st.layers[0].dst = 0          # writing the input slot
+    assert lib.ifq_run_stack(ctypes.byref(st), FAKE, FAKE, FAKE, 1 << 20,
+                             None) == EINVAL
