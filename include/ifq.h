@@ -25,10 +25,16 @@
  *  - Device functions are asynchronous on the caller's stream. The caller owns
  *    all memory (device and host); the library never allocates device memory
  *    and keeps no state between calls beyond its loaded code object.
- *  - Tensors are dense NHWC. Codes are unsigned: layout IFQ_LAYOUT_I8_NHWC
+ *  - Tensors are dense. Codes are unsigned: layout IFQ_LAYOUT_I8_NHWC
  *    stores one code per byte; IFQ_LAYOUT_U2_NHWC_PACKED stores four 2-bit
  *    codes per byte along C (channel c in bits 2*(c%4)..2*(c%4)+1 of byte
- *    c/4; C must be a multiple of 4); IFQ_LAYOUT_I32_NHWC holds int32 sums.
+ *    c/4; C must be a multiple of 4); IFQ_LAYOUT_U2_BLOCK64 stores 2-bit
+ *    codes in channel blocks of 64: the tensor is [n][c/64][h][w] cells of
+ *    16 bytes, each cell holding channels 64b .. 64b+63 of one pixel packed
+ *    as in IFQ_LAYOUT_U2_NHWC_PACKED (C must be a multiple of 64). In that
+ *    layout the 64 channels of one filter tap for a run of consecutive
+ *    output pixels are one contiguous span, so the convolution's gathers
+ *    are contiguous loads. IFQ_LAYOUT_I32_NHWC holds int32 sums.
  *  - No C++ exception crosses this interface. All functions are reentrant.
  */
 #ifndef IFQ_H_
@@ -56,6 +62,7 @@ typedef int32_t ifq_status;
 #define IFQ_LAYOUT_I8_NHWC 0
 #define IFQ_LAYOUT_U2_NHWC_PACKED 1
 #define IFQ_LAYOUT_I32_NHWC 2
+#define IFQ_LAYOUT_U2_BLOCK64 3
 
 #define IFQ_POOL_VALID 0 /* ho = (h-k)/stride + 1, windows fully inside       */
 #define IFQ_POOL_SAME 1  /* ho = ceil(h/stride), windows clipped bottom/right */
@@ -79,11 +86,13 @@ typedef int32_t ifq_status;
  *   in_bits        bits per input code, 1..8 (codes 0 .. 2^in_bits - 1)
  *   out_bits       0: the output is the int32 sum a itself (no quantizer);
  *                  1..4: the output is a code with 2^out_bits - 1 thresholds
- *   in_layout      IFQ_LAYOUT_I8_NHWC, or IFQ_LAYOUT_U2_NHWC_PACKED when
- *                  in_bits == 2
+ *   in_layout      IFQ_LAYOUT_I8_NHWC; or, when in_bits == 2,
+ *                  IFQ_LAYOUT_U2_NHWC_PACKED (c_in % 16 == 0) or
+ *                  IFQ_LAYOUT_U2_BLOCK64 (c_in % 64 == 0)
  *   out_layout     IFQ_LAYOUT_I32_NHWC iff out_bits == 0; otherwise
- *                  IFQ_LAYOUT_I8_NHWC, or IFQ_LAYOUT_U2_NHWC_PACKED when
- *                  out_bits == 2
+ *                  IFQ_LAYOUT_I8_NHWC, or when out_bits == 2
+ *                  IFQ_LAYOUT_U2_NHWC_PACKED (c_out % 4 == 0) or
+ *                  IFQ_LAYOUT_U2_BLOCK64 (c_out % 64 == 0)
  * Output size: ho = (h + 2*pad - kh)/stride + 1, wo likewise.
  */
 typedef struct ifq_conv_desc {
@@ -164,9 +173,14 @@ typedef struct ifq_join_params {
 /*
  * Device-side join operand of ifq_conv_forward.
  *   kind      IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY or IFQ_JOIN_CONV
- *   layout    layout of shortcut: codes (I8 / U2) for IDENTITY, I32 for CONV
+ *   layout    layout of shortcut: codes (I8, U2 or BLOCK64) for IDENTITY,
+ *             I32 for CONV
  *   shortcut  device tensor [n][ho][wo][c_out]
- *   coef      device array [c_out][3] written by ifq_fold_join
+ *   coef      IFQ_JOIN_CONV: device array [c_out][3] written by
+ *             ifq_fold_join (NULL for IDENTITY)
+ *   table     IFQ_JOIN_IDENTITY: device array [c_out][4][2^out_bits]
+ *             written by ifq_fold_join_table with x_bits = 2 (the shortcut
+ *             codes are 2-bit; NULL for CONV)
  *   n_q       number of quantizer thresholds, 2^out_bits - 1
  *   q_thr     the quantizer thresholds of Eq. (3), strictly increasing
  */
@@ -175,6 +189,7 @@ typedef struct ifq_join {
   int32_t layout;
   const void* shortcut;
   const double* coef;
+  const int32_t* table;
   int32_t n_q;
   int32_t reserved;
   double q_thr[IFQ_MAX_THRESHOLDS];
@@ -183,7 +198,8 @@ typedef struct ifq_join {
 /*
  * Integer max-pool on codes (Eq. 4 applied after the quantizer; for channels
  * with a positive BN scale this equals pooling the conv output first).
- *   n, h, w, c     input tensor; bits: code width; layout I8 or U2 (bits 2)
+ *   n, h, w, c     input tensor; bits: code width; layout I8, or U2 or
+ *                  BLOCK64 (bits 2); the output has the same layout
  *   k, stride      square window; mode IFQ_POOL_VALID or IFQ_POOL_SAME
  */
 typedef struct ifq_pool_desc {
@@ -295,6 +311,26 @@ IFQ_API ifq_status ifq_fold_thresholds(const ifq_fold_params* p,
 IFQ_API ifq_status ifq_fold_join(const ifq_join_params* p, double* coef_out);
 
 /*
+ * Integer thresholds of an identity join (the idea of Eq. 6 -> 7 applied to
+ * the join: the fixed-point test moves onto the integer sum). For channel c
+ * and shortcut code x in 0 .. X-1 (X = 2^x_bits) the record
+ *   table_out[(c*X + x)*R + 0]   s = +1, or -1 when the join's p < 0
+ *   table_out[(c*X + x)*R + i]   T_i, i = 1 .. R-1     (R = 2^out_bits)
+ * satisfies, for every integer a with |a| <= B = k * (2^in_bits - 1),
+ *   #{i : s*a > T_i} == #{i : fma(p, a, fma(q, x, cc)) > q_thr[i-1]}
+ * with {p, q, cc} of ifq_fold_join (p->kind must be IFQ_JOIN_IDENTITY) and
+ * the fma evaluated in fp64. fma is correctly rounded, so the left side of
+ * each comparison is monotone in a and every T_i is found by bisection of
+ * that predicate; the table is exact, not an approximation. p == 0 gives a
+ * constant code. Host only; table_out holds c_out * X * R int32.
+ * Errors: INVALID_ARGUMENT (as ifq_fold_join, bad bits, k < 1, q_thr not
+ * strictly increasing).
+ */
+IFQ_API ifq_status ifq_fold_join_table(const ifq_join_params* p, int32_t in_bits,
+                                       int64_t k, int32_t x_bits, int32_t out_bits,
+                                       const double* q_thr, int32_t* table_out);
+
+/*
  * Name of the kernel variant ifq_conv_forward launches for d (static string,
  * the kernel's symbol as a profiler lists it), or "" for an invalid desc.
  * Host; for profiling and benchmarks.
@@ -331,11 +367,13 @@ IFQ_API ifq_status ifq_maxpool_codes(const ifq_pool_desc* d, const void* x,
                                      void* y, hipStream_t stream);
 
 /*
- * Convert codes between IFQ_LAYOUT_I8_NHWC and IFQ_LAYOUT_U2_NHWC_PACKED
- * (npix pixels of c channels, c a multiple of 4), asynchronous. Converting to
- * U2 keeps the low two bits of each code. Errors: INVALID_ARGUMENT, HIP.
+ * Convert a code tensor of n images of h x w pixels and c channels between
+ * any two of IFQ_LAYOUT_I8_NHWC, IFQ_LAYOUT_U2_NHWC_PACKED (c % 4 == 0) and
+ * IFQ_LAYOUT_U2_BLOCK64 (c % 64 == 0), asynchronous; src and dst must not
+ * overlap. Converting to a 2-bit layout keeps the low two bits of each code.
+ * Errors: INVALID_ARGUMENT, HIP.
  */
-IFQ_API ifq_status ifq_convert_codes(int64_t npix, int32_t c,
+IFQ_API ifq_status ifq_convert_codes(int64_t n, int64_t h, int64_t w, int32_t c,
                                      int32_t src_layout, int32_t dst_layout,
                                      const void* src, void* dst,
                                      hipStream_t stream);

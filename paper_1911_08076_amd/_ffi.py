@@ -20,6 +20,7 @@ IFQ_ERR_INSUFFICIENT_BUFFER = -4
 IFQ_LAYOUT_I8_NHWC = 0
 IFQ_LAYOUT_U2_NHWC_PACKED = 1
 IFQ_LAYOUT_I32_NHWC = 2
+IFQ_LAYOUT_U2_BLOCK64 = 3
 
 IFQ_POOL_VALID = 0
 IFQ_POOL_SAME = 1
@@ -65,7 +66,7 @@ class JoinParams(ctypes.Structure):
 
 class Join(ctypes.Structure):
     _fields_ = [("kind", i32), ("layout", i32), ("shortcut", vp), ("coef", vp),
-                ("n_q", i32), ("reserved", i32),
+                ("table", vp), ("n_q", i32), ("reserved", i32),
                 ("q_thr", f64 * IFQ_MAX_THRESHOLDS)]
 
 
@@ -96,12 +97,14 @@ SIGNATURES = [
     ("ifq_pack_weights", i32, [ctypes.POINTER(ConvDesc), vp, vp, size_t]),
     ("ifq_fold_thresholds", i32, [ctypes.POINTER(FoldParams), vp]),
     ("ifq_fold_join", i32, [ctypes.POINTER(JoinParams), vp]),
+    ("ifq_fold_join_table", i32, [ctypes.POINTER(JoinParams), i32, i64, i32, i32,
+                                  vp, vp]),
     ("ifq_conv_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc)]),
     ("ifq_conv_workspace_bytes", size_t, [ctypes.POINTER(ConvDesc)]),
     ("ifq_conv_forward", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp,
                                ctypes.POINTER(Join), vp, vp, vp, size_t, vp]),
     ("ifq_maxpool_codes", i32, [ctypes.POINTER(PoolDesc), vp, vp, vp]),
-    ("ifq_convert_codes", i32, [i64, i32, i32, i32, vp, vp, vp]),
+    ("ifq_convert_codes", i32, [i64, i64, i64, i32, i32, i32, vp, vp, vp]),
     ("ifq_stack_workspace_bytes", size_t, [ctypes.POINTER(Stack)]),
     ("ifq_stack_slot_info", i32, [ctypes.POINTER(Stack), i32,
                                   ctypes.POINTER(size_t), ctypes.POINTER(size_t)]),

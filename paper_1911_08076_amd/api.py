@@ -114,12 +114,7 @@ def ifq_fold_thresholds(c_out, in_bits, out_bits, k, alpha, beta_in, q_thr,
     return out
 
 
-def ifq_fold_join(kind, main, beta_x, down=None):
-    """Join coefficients [c_out][3] = {p, q, cc}.
-
-    main / down: dicts with alpha, beta_in, bias, mean, var, gamma, bn_beta,
-    eps (down is used for IFQ_JOIN_CONV only).
-    """
+def _join_params(kind, main, beta_x, down=None):
     m = {k: _f64(main.get(k)) for k in ("alpha", "bias", "mean", "var", "gamma",
                                           "bn_beta")}
     d = {k: None for k in m}
@@ -134,17 +129,40 @@ def ifq_fold_join(kind, main, beta_x, down=None):
                    float(beta_x), _ptr(d["alpha"]), _ptr(d["bias"]),
                    _ptr(d["mean"]), _ptr(d["var"]), _ptr(d["gamma"]),
                    _ptr(d["bn_beta"]), eps_d)
+    return p, c_out, (m, d)
+
+
+def ifq_fold_join(kind, main, beta_x, down=None):
+    """Join coefficients [c_out][3] = {p, q, cc}.
+
+    main / down: dicts with alpha, beta_in, bias, mean, var, gamma, bn_beta,
+    eps (down is used for IFQ_JOIN_CONV only).
+    """
+    p, c_out, keep = _join_params(kind, main, beta_x, down)
     out = np.zeros((c_out, 3), dtype=np.float64)
     _check(_lib().ifq_fold_join(ctypes.byref(p), _ptr(out)), "ifq_fold_join")
     return out
 
 
-def make_join(kind, layout, shortcut, coef, q_thr):
+def ifq_fold_join_table(main, beta_x, in_bits, k, out_bits, q_thr, x_bits=2):
+    """Integer records of an identity join: int32 [c_out][2^x_bits][2^out_bits]
+    = {s, T_1 .. T_{2^out_bits - 1}} for every shortcut code x."""
+    p, c_out, keep = _join_params(_ffi.IFQ_JOIN_IDENTITY, main, beta_x)
+    q = _f64(q_thr)
+    out = np.zeros((c_out, 1 << x_bits, 1 << out_bits), dtype=np.int32)
+    _check(_lib().ifq_fold_join_table(ctypes.byref(p), int(in_bits), int(k),
+                                      int(x_bits), int(out_bits), _ptr(q),
+                                      _ptr(out)), "ifq_fold_join_table")
+    return out
+
+
+def make_join(kind, layout, shortcut, coef, q_thr, table=None):
     j = Join()
     j.kind = kind
     j.layout = layout
     j.shortcut = _ptr(shortcut)
     j.coef = _ptr(coef)
+    j.table = _ptr(table)
     q = list(np.asarray(q_thr, dtype=np.float64))
     j.n_q = len(q)
     for i, v in enumerate(q[:IFQ_MAX_THRESHOLDS]):
@@ -174,9 +192,10 @@ def ifq_maxpool_codes(desc, x, y, stream=None):
                                     _stream(stream)), "ifq_maxpool_codes")
 
 
-def ifq_convert_codes(npix, c, src_layout, dst_layout, src, dst, stream=None):
-    _check(_lib().ifq_convert_codes(int(npix), int(c), src_layout, dst_layout,
-                                    _ptr(src), _ptr(dst), _stream(stream)),
+def ifq_convert_codes(n, h, w, c, src_layout, dst_layout, src, dst, stream=None):
+    _check(_lib().ifq_convert_codes(int(n), int(h), int(w), int(c), src_layout,
+                                    dst_layout, _ptr(src), _ptr(dst),
+                                    _stream(stream)),
            "ifq_convert_codes")
 
 

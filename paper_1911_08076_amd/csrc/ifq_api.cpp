@@ -47,6 +47,7 @@ int64_t tensor_bytes(int64_t n, int64_t h, int64_t w, int64_t c, int layout) {
   switch (layout) {
     case IFQ_LAYOUT_I8_NHWC: return e;
     case IFQ_LAYOUT_U2_NHWC_PACKED: return (c % 4) ? -1 : e / 4;
+    case IFQ_LAYOUT_U2_BLOCK64: return (c % 64) ? -1 : e / 4;
     case IFQ_LAYOUT_I32_NHWC: return 4 * e;
     default: return -1;
   }
@@ -81,6 +82,10 @@ ifq_status check_conv(const ifq_conv_desc* d, int64_t* ho_out = nullptr,
     if (d->c_in % 16)
       return fail(IFQ_ERR_UNSUPPORTED,
                   "conv: 2-bit packed input needs c_in %% 16 == 0");
+  } else if (d->in_layout == IFQ_LAYOUT_U2_BLOCK64) {
+    if (d->in_bits != 2 || d->c_in % 64)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "conv: BLOCK64 input needs in_bits == 2 and c_in %% 64 == 0");
   } else if (d->in_layout != IFQ_LAYOUT_I8_NHWC) {
     return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: bad in_layout %d", d->in_layout);
   }
@@ -95,6 +100,10 @@ ifq_status check_conv(const ifq_conv_desc* d, int64_t* ho_out = nullptr,
     if (d->c_out % 4)
       return fail(IFQ_ERR_INVALID_ARGUMENT,
                   "conv: 2-bit packed output needs c_out %% 4 == 0");
+  } else if (d->out_layout == IFQ_LAYOUT_U2_BLOCK64) {
+    if (d->out_bits != 2 || d->c_out % 64)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "conv: BLOCK64 output needs out_bits == 2 and c_out %% 64 == 0");
   } else if (d->out_layout != IFQ_LAYOUT_I8_NHWC) {
     return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: bad out_layout %d", d->out_layout);
   }
@@ -124,6 +133,10 @@ ifq_status check_pool(const ifq_pool_desc* d, int64_t* ho, int64_t* wo) {
     if (d->bits != 2 || d->c % 4)
       return fail(IFQ_ERR_INVALID_ARGUMENT,
                   "pool: 2-bit packed codes need bits == 2 and c %% 4 == 0");
+  } else if (d->layout == IFQ_LAYOUT_U2_BLOCK64) {
+    if (d->bits != 2 || d->c % 64)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "pool: BLOCK64 codes need bits == 2 and c %% 64 == 0");
   } else if (d->layout != IFQ_LAYOUT_I8_NHWC) {
     return fail(IFQ_ERR_INVALID_ARGUMENT, "pool: bad layout %d", d->layout);
   }
@@ -156,7 +169,10 @@ ifq_status check_join(const ifq_join* j, const ifq_conv_desc* d) {
       return fail(IFQ_ERR_INVALID_ARGUMENT,
                   "join: q_thr must be finite and strictly increasing");
   }
-  if (!j->coef) return fail(IFQ_ERR_INVALID_ARGUMENT, "join: coef is NULL");
+  if (j->kind == IFQ_JOIN_CONV && !j->coef)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join: conv join needs coef");
+  if (j->kind == IFQ_JOIN_IDENTITY && !j->table)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join: identity join needs table");
   if (j->kind == IFQ_JOIN_CONV && j->layout != IFQ_LAYOUT_I32_NHWC)
     return fail(IFQ_ERR_INVALID_ARGUMENT, "join: conv shortcut must be I32_NHWC");
   if (j->kind == IFQ_JOIN_IDENTITY) {
@@ -164,9 +180,13 @@ ifq_status check_join(const ifq_join* j, const ifq_conv_desc* d) {
       if (d->c_out % 4)
         return fail(IFQ_ERR_INVALID_ARGUMENT,
                     "join: packed shortcut needs c_out %% 4 == 0");
+    } else if (j->layout == IFQ_LAYOUT_U2_BLOCK64) {
+      if (d->c_out % 64)
+        return fail(IFQ_ERR_INVALID_ARGUMENT,
+                    "join: BLOCK64 shortcut needs c_out %% 64 == 0");
     } else if (j->layout != IFQ_LAYOUT_I8_NHWC) {
       return fail(IFQ_ERR_INVALID_ARGUMENT,
-                  "join: identity shortcut must be codes (I8 or U2)");
+                  "join: identity shortcut must be codes (I8, U2 or BLOCK64)");
     }
   }
   return IFQ_OK;
@@ -195,6 +215,7 @@ ifq::ConvLaunch make_launch(const ifq_conv_desc* d, int64_t ho, int64_t wo,
     a.sc_layout = join->layout;
     a.shortcut = shortcut;
     a.coef = join->coef;
+    a.table = join->table;
     for (int i = 0; i < join->n_q; ++i) a.qthr[i] = join->q_thr[i];
   }
   a.nq = d->out_bits ? (1 << d->out_bits) - 1 : 0;
@@ -216,8 +237,29 @@ ifq::ConvLaunch make_launch(const ifq_conv_desc* d, int64_t ho, int64_t wo,
   a.nk = (int32_t)(g.kpad / ifq::kKStep);
   a.in_layout = d->in_layout;
   a.in_bits = d->in_bits;
-  a.out_mode = d->out_bits == 0 ? 0
-               : d->out_layout == IFQ_LAYOUT_U2_NHWC_PACKED ? 2 : 1;
+  a.out_layout = d->out_layout;
+  a.out_mode = d->out_bits == 0 ? 0 : d->out_layout == IFQ_LAYOUT_I8_NHWC ? 1 : 2;
+  return a;
+}
+
+// A BLOCK64 tensor of n images and c channels is pooled as the NHWC packed
+// tensor of n*c/64 images of 64 channels it is laid out as.
+ifq::PoolLaunch make_pool(const ifq_pool_desc& d, int64_t ho, int64_t wo,
+                          const void* x, void* y) {
+  ifq::PoolLaunch a;
+  a.x = static_cast<const uint8_t*>(x);
+  a.y = static_cast<uint8_t*>(y);
+  const bool b64 = d.layout == IFQ_LAYOUT_U2_BLOCK64;
+  a.n = b64 ? d.n * (d.c / 64) : d.n;
+  a.h = d.h;
+  a.w = d.w;
+  a.c = b64 ? 64 : d.c;
+  a.k = d.k;
+  a.stride = d.stride;
+  a.ho = (int32_t)ho;
+  a.wo = (int32_t)wo;
+  a.layout = b64 ? IFQ_LAYOUT_U2_NHWC_PACKED : d.layout;
+  a.bits = d.bits;
   return a;
 }
 
@@ -294,9 +336,10 @@ IFQ_API ifq_status ifq_pack_weights(const ifq_conv_desc* d,
       return fail(IFQ_ERR_INVALID_ARGUMENT,
                   "pack: weight %lld is %d, must be +1 or -1", (long long)i,
                   (int)w_oihw[i]);
+  const bool mfma = ifq::mfma_layout(*d);
   const bool u2 = d->in_layout == IFQ_LAYOUT_U2_NHWC_PACKED;
-  const bool frag = ifq::frag_layout(*d);
-  const int64_t nk = g.kpad / ifq::kKStep;
+  const int64_t nk32 = g.kpad / 32;
+  const int64_t groups = d->c_in / 64;
   int8_t* rows = static_cast<int8_t*>(dst);
   int32_t* rowsum = reinterpret_cast<int32_t*>(static_cast<uint8_t*>(dst) + g.rows_bytes);
   std::memset(dst, 0, (size_t)g.total_bytes);
@@ -305,18 +348,24 @@ IFQ_API ifq_status ifq_pack_weights(const ifq_conv_desc* d,
     for (int64_t r = 0; r < d->kh; ++r)
       for (int64_t s = 0; s < d->kw; ++s)
         for (int64_t c = 0; c < d->c_in; ++c) {
-          int64_t cp = c;
-          if (u2) {  // 4x4 transpose inside each group of 16 channels
-            const int64_t base = c & ~(int64_t)15, in = c & 15;
-            cp = base + (in & 3) * 4 + (in >> 2);
-          }
           const int8_t v = w_oihw[((co * d->c_in + c) * d->kh + r) * d->kw + s];
-          const int64_t k = (r * d->kw + s) * d->c_in + cp;
-          int64_t pos = co * g.kpad + k;
-          if (frag) {
-            const int64_t kt = k / ifq::kKStep, kk = k % ifq::kKStep;
-            const int64_t lane = (kk / 16) * 16 + (co % 16);
-            pos = (((co / 16) * nk + kt) * 64 + lane) * 16 + kk % 16;
+          const int64_t tap = r * d->kw + s;
+          int64_t pos;
+          if (mfma) {
+            // K64 step kk = tap*G + c/64; channel c' = c%64 = 32h + 16t + 4i + q
+            // sits in K32 step 2*kk + t, lane 32h + co%32, byte 4q + i
+            const int64_t kk = tap * groups + c / 64, cp = c % 64;
+            const int64_t h = cp / 32, t = (cp % 32) / 16, i = (cp % 16) / 4, q = cp % 4;
+            const int64_t k32 = 2 * kk + t;
+            const int64_t lane = 32 * h + co % 32;
+            pos = (((co / 32) * nk32 + k32) * 64 + lane) * 16 + 4 * q + i;
+          } else {
+            int64_t cp = c;
+            if (u2) {  // 4x4 transpose inside each group of 16 channels
+              const int64_t base = c & ~(int64_t)15, in = c & 15;
+              cp = base + (in & 3) * 4 + (in >> 2);
+            }
+            pos = co * g.kpad + tap * d->c_in + cp;
           }
           rows[pos] = v;
           sum += v;
@@ -458,6 +507,61 @@ IFQ_API ifq_status ifq_fold_join(const ifq_join_params* p, double* coef_out) {
   return ok();
 }
 
+IFQ_API ifq_status ifq_fold_join_table(const ifq_join_params* p, int32_t in_bits,
+                                       int64_t k, int32_t x_bits, int32_t out_bits,
+                                       const double* q_thr, int32_t* table_out) {
+  if (!p || !q_thr || !table_out) return fail(IFQ_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if (p->kind != IFQ_JOIN_IDENTITY)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join table: kind must be IFQ_JOIN_IDENTITY");
+  if (in_bits < 1 || in_bits > 8 || x_bits < 1 || x_bits > 8 || out_bits < 1 ||
+      out_bits > 4)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join table: bad bit widths");
+  if (k < 1 || k * ((1 << in_bits) - 1) >= kMaxIndex / 2)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "join table: bad contraction length");
+  const int nq = (1 << out_bits) - 1;
+  for (int i = 0; i < nq; ++i)
+    if (!is_finite(q_thr[i]) || (i > 0 && !(q_thr[i] > q_thr[i - 1])))
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "join table: q_thr must be finite and strictly increasing");
+  std::vector<double> coef((size_t)p->c_out * 3);
+  ifq_status st = ifq_fold_join(p, coef.data());
+  if (st != IFQ_OK) return st;
+  const int64_t bound = k * ((1 << in_bits) - 1);
+  const int nx = 1 << x_bits, rec = nq + 1;
+  for (int c = 0; c < p->c_out; ++c) {
+    const double pc = coef[3 * c], qc = coef[3 * c + 1], cc = coef[3 * c + 2];
+    const int32_t s = pc < 0.0 ? -1 : 1;
+    for (int x = 0; x < nx; ++x) {
+      const double inner = std::fma(qc, (double)x, cc);
+      int32_t* r = table_out + ((int64_t)c * nx + x) * rec;
+      r[0] = s;
+      for (int i = 0; i < nq; ++i) {
+        // with u = s*a the join value is non-decreasing in u (fma is
+        // correctly rounded), so "z > q_i" is false up to some u and true
+        // after it: T_i is the last u where it is false
+        auto pred = [&](int64_t u) {
+          return std::fma(pc, (double)(s * u), inner) > q_thr[i];
+        };
+        int64_t t;
+        if (pred(-bound)) {
+          t = -bound - 1;
+        } else if (!pred(bound)) {
+          t = bound;
+        } else {
+          int64_t lo = -bound, hi = bound;  // pred(lo) false, pred(hi) true
+          while (hi - lo > 1) {
+            const int64_t mid = lo + (hi - lo) / 2;
+            if (pred(mid)) hi = mid; else lo = mid;
+          }
+          t = lo;
+        }
+        r[1 + i] = (int32_t)t;
+      }
+    }
+  }
+  return ok();
+}
+
 IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d) {
   int64_t ho, wo;
   if (check_conv(d, &ho, &wo) != IFQ_OK) return "";
@@ -496,38 +600,33 @@ IFQ_API ifq_status ifq_maxpool_codes(const ifq_pool_desc* d, const void* x,
   ifq_status st = check_pool(d, &ho, &wo);
   if (st != IFQ_OK) return st;
   if (d->n > 0 && (!x || !y)) return fail(IFQ_ERR_INVALID_ARGUMENT, "pool: NULL tensor");
-  ifq::PoolLaunch a;
-  a.x = static_cast<const uint8_t*>(x);
-  a.y = static_cast<uint8_t*>(y);
-  a.n = d->n;
-  a.h = d->h;
-  a.w = d->w;
-  a.c = d->c;
-  a.k = d->k;
-  a.stride = d->stride;
-  a.ho = (int32_t)ho;
-  a.wo = (int32_t)wo;
-  a.layout = d->layout;
-  a.bits = d->bits;
+  const ifq::PoolLaunch a = make_pool(*d, ho, wo, x, y);
   st = hip_status(ifq::launch_pool(a, stream), "pool launch");
   if (st != IFQ_OK) return st;
   return ok();
 }
 
-IFQ_API ifq_status ifq_convert_codes(int64_t npix, int32_t c,
+IFQ_API ifq_status ifq_convert_codes(int64_t n, int64_t h, int64_t w, int32_t c,
                                      int32_t src_layout, int32_t dst_layout,
                                      const void* src, void* dst,
                                      hipStream_t stream) {
-  if (npix < 0 || c < 1 || c % 4)
-    return fail(IFQ_ERR_INVALID_ARGUMENT, "convert: need npix >= 0, c %% 4 == 0");
-  const bool fwd = src_layout == IFQ_LAYOUT_I8_NHWC && dst_layout == IFQ_LAYOUT_U2_NHWC_PACKED;
-  const bool back = src_layout == IFQ_LAYOUT_U2_NHWC_PACKED && dst_layout == IFQ_LAYOUT_I8_NHWC;
-  if (!fwd && !back)
-    return fail(IFQ_ERR_INVALID_ARGUMENT, "convert: layouts must be I8 <-> U2");
-  if (npix * c >= kMaxIndex) return fail(IFQ_ERR_UNSUPPORTED, "convert: too large");
-  if (npix > 0 && (!src || !dst)) return fail(IFQ_ERR_INVALID_ARGUMENT, "convert: NULL");
-  ifq_status st = hip_status(ifq::launch_convert(npix * c, src_layout, src, dst, stream),
-                             "convert launch");
+  auto code_layout = [](int32_t l) {
+    return l == IFQ_LAYOUT_I8_NHWC || l == IFQ_LAYOUT_U2_NHWC_PACKED ||
+           l == IFQ_LAYOUT_U2_BLOCK64;
+  };
+  if (n < 0 || h < 0 || w < 0 || c < 1 || c % 4)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "convert: need n, h, w >= 0, c %% 4 == 0");
+  if (!code_layout(src_layout) || !code_layout(dst_layout) || src_layout == dst_layout)
+    return fail(IFQ_ERR_INVALID_ARGUMENT,
+                "convert: layouts must be two different code layouts");
+  if ((src_layout == IFQ_LAYOUT_U2_BLOCK64 || dst_layout == IFQ_LAYOUT_U2_BLOCK64) && c % 64)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "convert: BLOCK64 needs c %% 64 == 0");
+  if (n * h * w * c >= kMaxIndex) return fail(IFQ_ERR_UNSUPPORTED, "convert: too large");
+  if (n * h * w > 0 && (!src || !dst))
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "convert: NULL");
+  ifq_status st = hip_status(
+      ifq::launch_convert(n, h * w, c, src_layout, dst_layout, src, dst, stream),
+      "convert launch");
   if (st != IFQ_OK) return st;
   return ok();
 }
@@ -684,19 +783,7 @@ IFQ_API ifq_status ifq_run_stack(const ifq_stack* s, const void* x, void* y,
     } else {
       int64_t ho, wo;
       check_pool(&L.pool, &ho, &wo);
-      ifq::PoolLaunch a;
-      a.x = static_cast<const uint8_t*>(slot(L.src));
-      a.y = static_cast<uint8_t*>(slot(L.dst));
-      a.n = L.pool.n;
-      a.h = L.pool.h;
-      a.w = L.pool.w;
-      a.c = L.pool.c;
-      a.k = L.pool.k;
-      a.stride = L.pool.stride;
-      a.ho = (int32_t)ho;
-      a.wo = (int32_t)wo;
-      a.layout = L.pool.layout;
-      a.bits = L.pool.bits;
+      const ifq::PoolLaunch a = make_pool(L.pool, ho, wo, slot(L.src), slot(L.dst));
       st = hip_status(ifq::launch_pool(a, stream), "pool launch");
     }
     if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());

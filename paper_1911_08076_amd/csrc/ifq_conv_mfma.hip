@@ -1,0 +1,544 @@
+// Fast path of the integrated fixed-point quantized convolution on gfx950
+// (MI355X): 2-bit input codes with c_in a multiple of 64, in the BLOCK64 or
+// the NHWC packed layout.
+//
+// The integer part of Eq. (1), a = W_b (x) X_q, is an implicit GEMM
+// D[co][pixel] = sum_k W[co][k] * X[pixel][k] on v_mfma_i32_32x32x32_i8:
+// A (rows = output channels) is the +-1 weight matrix in fragment order, B
+// (columns = output pixels) the input codes of one filter tap and 64 channels
+// per K64 step, unpacked from 2 bits to int8 in registers right before the
+// MFMA. K runs over K64 steps kk = (r*kw + s)*G + g (G = c_in/64).
+//
+// A workgroup of WM x WN x WK waves computes a tile of 32*FM*WM output
+// channels x up to 32*FN*WN pixels (bn, chosen per layer on the host); the
+// WK wave groups split the K64 steps and their sums are added in LDS at the
+// end. Operands reach LDS through the LDS-DMA form of the global load (one
+// wave instruction moves 64 x 16 bytes, lane i's bytes landing at base +
+// 16*i, no staging registers): a weight chunk is 1 KB of fragments, a code
+// chunk the 16-byte cells of 64 consecutive output pixels for one tap and
+// 64 channels, which in the BLOCK64 layout is one contiguous 1 KB span for a
+// stride-1 conv. A ring of D stages of S K64 steps per wave group keeps the
+// loads of the next D-1 stages in flight while one computes; every wave
+// issues the same number of loads per stage and waits for its part of a
+// stage with an explicit vmcnt that leaves younger stages in flight.
+// Out-of-range operands are read from blocks of zeros, so the main loop has
+// no branch around a load.
+//
+// Accumulator layout (32x32 MFMA): lane l = 32*h + j holds, for register v,
+// row 8*(v/4) + 4*h + v%4 and column j; each lane therefore holds groups of
+// four consecutive output channels of one pixel, and the fused epilogue of
+// ifq_epilogue.h turns them into codes with integer compares (Eq. 7/8) or the
+// residual join without cross-lane traffic.
+#include <hip/hip_runtime.h>
+
+#include "ifq_epilogue.h"
+#include "ifq_internal.h"
+
+namespace ifq {
+namespace {
+
+typedef int v2i __attribute__((ext_vector_type(2)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+constexpr uint32_t kLow2 = 0x03030303u;
+
+// Sixteen zero bytes in device memory: code loads that fall outside the
+// image read them instead of branching around the load.
+__device__ uint4 g_zero_cell;
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
+}
+
+// One wave-wide LDS-DMA load: 16 bytes per lane from src to LDS dst + 16*lane.
+// M0 carries the LDS base; nothing else in these kernels uses M0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(const void* src, uint32_t dst) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(dst), "v"(src) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+
+// Waits until at most ahead*CPW of this wave's loads are outstanding
+// (0 <= ahead <= MAXA).
+template <int MAXA, int CPW>
+__device__ __forceinline__ void wait_ahead(int ahead) {
+  if constexpr (MAXA <= 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (ahead >= MAXA) wait_vmcnt<MAXA * CPW>();
+    else wait_ahead<MAXA - 1, CPW>(ahead);
+  }
+}
+
+// Epilogue for the 32x32 accumulator layout when c_out % 32 == 0 and the
+// records have 4 entries (2-bit codes): every lane computes codes for all of
+// its accumulators without per-lane branches. A lane holds, per block
+// (fm, fn), output channels cb + 8b + 4h + i (b, i = 0..3) of one pixel; the
+// per-channel records of a 4-channel group are read from LDS once and used
+// for the FN pixel blocks. Codes go to the LDS output tile (rows past the
+// last pixel are never copied out); shortcut reads use a clamped pixel index.
+enum Epi32 { kE32I32 = 0, kE32Thr4 = 1, kE32Tab4 = 2, kE32Conv = 3 };
+
+template <int MODE, int FM, int FN>
+__device__ __forceinline__ void epilogue32(const ConvLaunch& a, const uint8_t* lds,
+                                           const v16i (&acc)[FM][FN], int wm, int wn,
+                                           int h, int l32, int co0, int p0, int bn,
+                                           uint8_t* otile, int orow) {
+  const int32_t* prm = reinterpret_cast<const int32_t*>(lds);
+  const bool u2 = a.out_mode == 2;
+  const int howo = a.ho * a.wo;
+  const uint8_t* sc8 = reinterpret_cast<const uint8_t*>(a.shortcut);
+  const int32_t* sc32 = reinterpret_cast<const int32_t*>(a.shortcut);
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    const int cb = (wm * FM + fm) * 32;         // local first channel of the block
+    if (co0 + cb >= a.cout) continue;           // uniform: whole 32-channel block
+    // shortcut codes of the 32 channels of each pixel block (identity join):
+    // byte 2b + h of the 8 holds the lane's channels cb + 8b + 4h .. +3
+    uint32_t scw[FN][2];
+    if constexpr (MODE == kE32Tab4) {
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        int p = p0 + wn * 32 * FN + fn * 32 + l32;
+        p = p < a.m ? p : a.m - 1;
+        const int co = co0 + cb;
+        if (a.sc_layout == IFQ_LAYOUT_I8_NHWC) {
+          const uint8_t* src = sc8 + (int64_t)p * a.cout + co;
+          uint32_t w[2] = {0u, 0u};
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const uint32_t v = *reinterpret_cast<const uint32_t*>(src + 8 * b + 4 * h) & kLow2;
+            const uint32_t byte = v | (v >> 6) | (v >> 12) | (v >> 18);
+            w[b >> 1] |= (byte & 0xFFu) << (8 * (2 * (b & 1) + h));
+          }
+          scw[fn][0] = w[0];
+          scw[fn][1] = w[1];
+        } else {
+          int64_t off;
+          if (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64) {
+            const int nimg = p / howo;
+            off = (((int64_t)nimg * (a.cout >> 6) + (co >> 6)) * howo + (p - nimg * howo)) * 16 +
+                  ((co & 63) >> 2);
+          } else {
+            off = ((int64_t)p * a.cout + co) >> 2;
+          }
+          const uint2 v = *reinterpret_cast<const uint2*>(sc8 + off);
+          scw[fn][0] = v.x;
+          scw[fn][1] = v.y;
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int cl = cb + 8 * b + 4 * h;        // local channel of value 4b + 0
+      int4 tr[4];
+      double cf[4][3];
+      if constexpr (MODE == kE32Thr4) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) tr[i] = *reinterpret_cast<const int4*>(prm + (cl + i) * 4);
+      }
+      if constexpr (MODE == kE32Conv) {
+        const double* c = reinterpret_cast<const double*>(lds) + 3 * cl;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          cf[i][0] = c[3 * i];
+          cf[i][1] = c[3 * i + 1];
+          cf[i][2] = c[3 * i + 2];
+        }
+      }
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        const int pl = wn * 32 * FN + fn * 32 + l32;
+        int v[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = acc[fm][fn][4 * b + i];
+        if constexpr (MODE == kE32I32) {
+          if (pl < bn && p0 + pl < a.m)
+            *reinterpret_cast<int4*>(reinterpret_cast<int32_t*>(a.y) +
+                                     (int64_t)(p0 + pl) * a.cout + co0 + cl) =
+                int4{v[0], v[1], v[2], v[3]};
+          continue;
+        }
+        int code[4];
+        if constexpr (MODE == kE32Thr4) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int sv = tr[i].x * v[i];
+            code[i] = (sv > tr[i].y) + (sv > tr[i].z) + (sv > tr[i].w);
+          }
+        } else if constexpr (MODE == kE32Tab4) {
+          const uint32_t xs = (scw[fn][b >> 1] >> (8 * (2 * (b & 1) + h))) & 0xFFu;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int x = (xs >> (2 * i)) & 3;
+            const int4 t = *reinterpret_cast<const int4*>(prm + ((cl + i) * 4 + x) * 4);
+            const int sv = t.x * v[i];
+            code[i] = (sv > t.y) + (sv > t.z) + (sv > t.w);
+          }
+        } else {
+          int p = p0 + pl;
+          p = p < a.m ? p : a.m - 1;
+          const int4 d = *reinterpret_cast<const int4*>(sc32 + (int64_t)p * a.cout + co0 + cl);
+          const int dv[4] = {d.x, d.y, d.z, d.w};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const double z = fma(cf[i][0], (double)v[i], fma(cf[i][1], (double)dv[i], cf[i][2]));
+            int c = 0;
+            for (int q = 0; q < a.nq; ++q) c += z > a.qthr[q];
+            code[i] = c;
+          }
+        }
+        if (u2) {
+          otile[pl * orow + (cl >> 2)] =
+              (uint8_t)(code[0] | (code[1] << 2) | (code[2] << 4) | (code[3] << 6));
+        } else {
+          *reinterpret_cast<uint32_t*>(otile + pl * orow + cl) =
+              (uint32_t)code[0] | ((uint32_t)code[1] << 8) | ((uint32_t)code[2] << 16) |
+              ((uint32_t)code[3] << 24);
+        }
+      }
+    }
+  }
+}
+
+// 16 two-bit codes (one 32-bit word of a cell) -> 16 int8 operand bytes.
+__device__ __forceinline__ v4i unpack2(uint32_t u) {
+  return v4i{(int)(u & kLow2), (int)((u >> 2) & kLow2), (int)((u >> 4) & kLow2),
+             (int)((u >> 6) & kLow2)};
+}
+
+template <int WM, int WN, int WK, int FM, int FN, int S, int D>
+__global__ __launch_bounds__(64 * WM * WN * WK) void conv_mfma(ConvLaunch a) {
+  constexpr int NWG = WM * WN;                  // waves per K group
+  constexpr int NW = NWG * WK;
+  constexpr int BM = 32 * FM * WM;
+  constexpr int BN = 32 * FN * WN;
+  constexpr int BNL = (BN + 63) / 64 * 64;      // pixels loaded per K64 step
+  constexpr int A_STEP = BM * 64;               // BM/32 row blocks x 2 K32 x 1 KB
+  constexpr int B_STEP = BNL * 16;
+  constexpr int STEP = A_STEP + B_STEP;
+  constexpr int SK = S * WK;                    // K64 steps per stage
+  constexpr int STAGE = SK * STEP;
+  constexpr int CA1 = BM / 16, CB1 = BNL / 64;  // 1 KB chunks per K64 step
+  constexpr int C = SK * (CA1 + CB1);
+  static_assert(C % NW == 0, "equal loads per wave");
+  constexpr int CPW = C / NW;
+  static_assert((D - 2) * CPW <= 63, "vmcnt range");
+  constexpr int EPI_BYTES = epilogue_param_bytes(BM);  // per-channel parameters
+  constexpr int OUT_BYTES = BN * BM;            // byte-per-code output tile
+  constexpr int RED_BYTES = (WK / 2) * NWG * FM * FN * 4096;
+  constexpr int LDS0 = D * STAGE > RED_BYTES ? D * STAGE : RED_BYTES;
+  constexpr int LDS_BYTES = LDS0 > EPI_BYTES + OUT_BYTES ? LDS0 : EPI_BYTES + OUT_BYTES;
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS_BYTES];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kg = wave / NWG;                    // K group
+  const int wig = wave - kg * NWG;              // wave in group
+  const int wm = wig % WM;
+  const int wn = wig / WM;
+  const int h = lane >> 5;
+  const int l32 = lane & 31;
+  const int bn = a.bn;
+  const int p0 = blockIdx.x * bn;
+  const int co0 = blockIdx.y * BM;
+  const int G = a.cin >> 6;
+  const int nk = a.nk;
+  const int nk32 = 2 * nk;
+  const int nst = (nk + SK - 1) / SK;
+  const int rbw = co0 >> 5;                     // first row block
+  const int nrb = a.cout_pad >> 5;
+  const int howo = a.ho * a.wo;
+  const uint8_t* wbase = reinterpret_cast<const uint8_t*>(a.wgt) + lane * 16;
+  const uint8_t* zero_src = reinterpret_cast<const uint8_t*>(&g_zero_cell);
+  const uint32_t lds0 = lds_addr(lds);
+
+  // input strides in 16-byte cells: n, channel block, row, column
+  int sN, sG, sH, sW;
+  if (a.in_layout == IFQ_LAYOUT_U2_BLOCK64) {
+    sW = 1; sH = a.w; sG = a.h * a.w; sN = G * sG;
+  } else {
+    sG = 1; sW = G; sH = a.w * G; sN = a.h * sH;
+  }
+
+  // The loads of wave w are chunks c = w + NW*i of a stage; for code chunks
+  // the lane's pixel is fixed across stages, so its position is computed once.
+  int px_base[CPW], px_iy0[CPW], px_ix0[CPW];
+  bool px_ok[CPW];
+#pragma unroll
+  for (int i = 0; i < CPW; ++i) {
+    const int c = wave + NW * i;
+    const int cb = (c % (CA1 + CB1)) - CA1;     // code chunk index in the step
+    px_ok[i] = false;
+    px_base[i] = px_iy0[i] = px_ix0[i] = 0;
+    if (cb >= 0) {
+      const int pl = cb * 64 + lane;
+      const int p = p0 + pl;
+      if (pl < bn && p < a.m) {
+        const int nimg = p / howo;
+        const int rem = p - nimg * howo;
+        const int oy = rem / a.wo;
+        const int ox = rem - oy * a.wo;
+        px_ok[i] = true;
+        px_iy0[i] = oy * a.stride - a.pad;
+        px_ix0[i] = ox * a.stride - a.pad;
+        px_base[i] = nimg * sN + px_iy0[i] * sH + px_ix0[i] * sW;
+      }
+    }
+  }
+
+  // Issue the loads of stage st into ring slot st % D. Chunk c covers K64
+  // step kk = st*SK + c / (CA1 + CB1) of the stage; within the step the
+  // first CA1 chunks are weights (row block, K32 half), the rest codes.
+  auto issue = [&](int st) {
+    const uint32_t slot = lds0 + (uint32_t)((st % D) * STAGE);
+#pragma unroll
+    for (int i = 0; i < CPW; ++i) {
+      const int c = wave + NW * i;
+      const int s_ = c / (CA1 + CB1);
+      const int local = c - s_ * (CA1 + CB1);
+      const int kk = st * SK + s_;
+      const uint32_t dst = slot + (uint32_t)(s_ * STEP + local * 1024);
+      if (local < CA1) {
+        const int rb = local >> 1, t = local & 1;
+        const bool ok = kk < nk && rbw + rb < nrb;
+        const int64_t off = ok ? ((int64_t)(rbw + rb) * nk32 + 2 * kk + t) * 1024 : a.wzero;
+        dma16(wbase + off, dst);
+      } else {
+        const int tap = kk / G;
+        const int g = kk - tap * G;
+        const int r = tap / a.kw;
+        const int s = tap - r * a.kw;
+        const int iy = px_iy0[i] + r;
+        const int ix = px_ix0[i] + s;
+        const bool ok = kk < nk && px_ok[i] && (unsigned)iy < (unsigned)a.h &&
+                        (unsigned)ix < (unsigned)a.w;
+        const uint8_t* src =
+            ok ? a.x + (int64_t)(px_base[i] + g * sG + r * sH + s * sW) * 16 : zero_src;
+        dma16(src, dst);
+      }
+    }
+  };
+
+  v16i acc[FM][FN];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = v16i{0};
+
+  // K64 steps beyond nk multiply zero weight fragments: no branch here.
+  auto compute = [&](int st) {
+    const uint8_t* sb = lds + (st % D) * STAGE + kg * S * STEP;
+#pragma unroll
+    for (int s_ = 0; s_ < S; ++s_) {
+      const uint8_t* as = sb + s_ * STEP;
+      const uint8_t* bs = as + A_STEP;
+      v2i braw[FN];
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+        braw[fn] = *reinterpret_cast<const v2i*>(
+            bs + (wn * 32 * FN + fn * 32 + l32) * 16 + 8 * h);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        v4i af[FM];
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+          af[fm] = *reinterpret_cast<const v4i*>(as + ((wm * FM + fm) * 2 + t) * 1024 +
+                                                 lane * 16);
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn) {
+          const v4i bf = unpack2((uint32_t)braw[fn][t]);
+#pragma unroll
+          for (int fm = 0; fm < FM; ++fm)
+            acc[fm][fn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[fm], bf, acc[fm][fn],
+                                                                0, 0, 0);
+        }
+      }
+    }
+  };
+
+  const int pre = nst < D - 1 ? nst : D - 1;
+  for (int st = 0; st < pre; ++st) issue(st);
+  for (int st = 0; st < nst; ++st) {
+    const int issued_after = nst - 1 - st;      // stages issued after st, capped
+    wait_ahead<D - 2, CPW>(issued_after < D - 2 ? issued_after : D - 2);
+    __syncthreads();                            // every wave's part landed; slot st-1 free
+    if (st + D - 1 < nst) issue(st + D - 1);
+    compute(st);
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  // K groups: sums of groups half..2*half-1 are added into groups 0..half-1
+  if constexpr (WK > 1) {
+#pragma unroll
+    for (int half = WK / 2; half >= 1; half /= 2) {
+      if (kg >= half && kg < 2 * half) {
+        uint8_t* dst = lds + (((kg - half) * NWG + wig) * FM * FN) * 4096;
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+              *reinterpret_cast<v4i*>(dst + (fm * FN + fn) * 4096 + j * 1024 + lane * 16) =
+                  v4i{acc[fm][fn][4 * j], acc[fm][fn][4 * j + 1], acc[fm][fn][4 * j + 2],
+                      acc[fm][fn][4 * j + 3]};
+      }
+      __syncthreads();
+      if (kg < half) {
+        const uint8_t* src = lds + ((kg * NWG + wig) * FM * FN) * 4096;
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const v4i v = *reinterpret_cast<const v4i*>(src + (fm * FN + fn) * 4096 +
+                                                          j * 1024 + lane * 16);
+              acc[fm][fn][4 * j] += v.x;
+              acc[fm][fn][4 * j + 1] += v.y;
+              acc[fm][fn][4 * j + 2] += v.z;
+              acc[fm][fn][4 * j + 3] += v.w;
+            }
+      }
+      __syncthreads();
+    }
+  }
+
+  stage_epilogue(a, lds, co0, BM);
+  __syncthreads();
+  const int orow = a.out_mode == 2 ? BM / 4 : BM;
+  uint8_t* otile = lds + EPI_BYTES;
+  if (kg == 0) {
+    const bool fast = (a.cout & 31) == 0 && (a.out_mode == 0 || a.rec == 4);
+    if (fast) {
+      if (a.acc_dump) {
+        ConvLaunch d = a;
+        d.y = a.acc_dump;
+        epilogue32<kE32I32, FM, FN>(d, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow);
+      }
+      if (a.out_mode == 0)
+        epilogue32<kE32I32, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow);
+      else if (a.join_kind == IFQ_JOIN_IDENTITY)
+        epilogue32<kE32Tab4, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow);
+      else if (a.join_kind == IFQ_JOIN_CONV)
+        epilogue32<kE32Conv, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow);
+      else
+        epilogue32<kE32Thr4, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow);
+    } else {
+      epilogue_lane<FM * 4, FN>(
+          a, lds, [&](int g, int fn, int i) { return acc[g >> 2][fn][4 * (g & 3) + i]; },
+          [&](int g) { return co0 + (wm * FM + (g >> 2)) * 32 + 8 * (g & 3) + 4 * h; }, co0,
+          p0,
+          [&](int fn) {
+            const int pl = wn * 32 * FN + fn * 32 + l32;
+            return (pl < bn && p0 + pl < a.m) ? pl : -1;
+          },
+          otile, orow);
+    }
+  }
+  __syncthreads();
+  const int npx = a.m - p0 < bn ? a.m - p0 : bn;
+  copy_out_tile(a, otile, orow, co0, BM, p0, npx);
+}
+
+// ---------------------------------------------------------------------------
+// Variants and per-layer planning
+// ---------------------------------------------------------------------------
+struct Variant {
+  int wm, wn, wk, fm, fn;
+  double eff;        // relative MFMA efficiency of the wave tile (measured)
+  const char* name;
+};
+
+// Index order must match the switch in launch_conv_mfma.
+const Variant kVariants[] = {
+    {2, 4, 1, 2, 4, 0.89, "conv_mfma<2, 4, 1, 2, 4, 1, 6>"},   // 128 x 512
+    {2, 4, 1, 2, 2, 0.83, "conv_mfma<2, 4, 1, 2, 2, 2, 4>"},   // 128 x 256
+    {1, 8, 1, 2, 2, 0.83, "conv_mfma<1, 8, 1, 2, 2, 2, 4>"},   //  64 x 512
+    {2, 4, 1, 1, 2, 0.70, "conv_mfma<2, 4, 1, 1, 2, 2, 6>"},   //  64 x 256
+    {2, 2, 2, 2, 2, 0.80, "conv_mfma<2, 2, 2, 2, 2, 2, 3>"},   // 128 x 128, K split 2
+    {2, 1, 4, 1, 4, 0.75, "conv_mfma<2, 1, 4, 1, 4, 1, 6>"},   //  64 x 128, K split 4
+};
+constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
+constexpr int kNumCUs = 256;
+
+struct Plan {
+  int variant;
+  int bn;        // pixels per workgroup
+  int blocks_m;  // workgroups along pixels
+};
+
+// For each variant take the fewest rounds of one workgroup per CU that fit
+// the layer, spread the pixels evenly over the workgroups of those rounds
+// (in multiples of 32), and score useful MACs over issued MACs times the
+// variant's measured efficiency.
+Plan plan_mfma(const ConvLaunch& a) {
+  Plan best{0, 0, 0};
+  double best_score = -1.0;
+  for (int v = 0; v < kNumVariants; ++v) {
+    const Variant& V = kVariants[v];
+    const int bm = 32 * V.fm * V.wm;
+    const int bnmax = 32 * V.fn * V.wn;
+    const int64_t nco = (a.cout + bm - 1) / bm;
+    const int64_t nb_min = (a.m + bnmax - 1) / bnmax;
+    const int64_t rounds = (nco * nb_min + kNumCUs - 1) / kNumCUs;
+    int64_t nb = rounds * kNumCUs / nco;
+    if (nb < nb_min) nb = nb_min;
+    int64_t bn = (a.m + nb - 1) / nb;
+    bn = (bn + 31) / 32 * 32;
+    if (bn > bnmax) bn = bnmax;
+    const int64_t blocks = nco * ((a.m + bn - 1) / bn);
+    const double issued = (double)((blocks + kNumCUs - 1) / kNumCUs) * kNumCUs * bm * bnmax;
+    const double score = (double)a.m * a.cout / issued * V.eff;
+    if (score > best_score + 1e-9) {
+      best_score = score;
+      best = Plan{v, (int)bn, (int)((a.m + bn - 1) / bn)};
+    }
+  }
+  return best;
+}
+
+template <int WM, int WN, int WK, int FM, int FN, int S, int D>
+hipError_t launch_variant(ConvLaunch a, const Plan& pl, hipStream_t stream) {
+  a.bn = pl.bn;
+  dim3 grid(pl.blocks_m, (a.cout + 32 * FM * WM - 1) / (32 * FM * WM));
+  hipLaunchKernelGGL((conv_mfma<WM, WN, WK, FM, FN, S, D>), grid,
+                     dim3(64 * WM * WN * WK), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool mfma_eligible(const ConvLaunch& a) {
+  return a.in_bits == 2 && a.cin % 64 == 0 &&
+         (a.in_layout == IFQ_LAYOUT_U2_NHWC_PACKED || a.in_layout == IFQ_LAYOUT_U2_BLOCK64);
+}
+
+const char* conv_mfma_name(const ConvLaunch& a) { return kVariants[plan_mfma(a).variant].name; }
+
+hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream) {
+  const Plan pl = plan_mfma(a);
+  switch (pl.variant) {
+    case 0: return launch_variant<2, 4, 1, 2, 4, 1, 6>(a, pl, stream);
+    case 1: return launch_variant<2, 4, 1, 2, 2, 2, 4>(a, pl, stream);
+    case 2: return launch_variant<1, 8, 1, 2, 2, 2, 4>(a, pl, stream);
+    case 3: return launch_variant<2, 4, 1, 1, 2, 2, 6>(a, pl, stream);
+    case 4: return launch_variant<2, 2, 2, 2, 2, 2, 3>(a, pl, stream);
+    default: return launch_variant<2, 1, 4, 1, 4, 1, 6>(a, pl, stream);
+  }
+}
+
+}  // namespace ifq

@@ -11,44 +11,53 @@
 namespace ifq {
 
 // Device weight blob of one layer (written by ifq_pack_weights):
-//   int8  W[cout_pad][kpad]      W_b, K index k = (r*kw + s)*c_in + c', zero
-//                                beyond K = kh*kw*c_in and beyond c_out
+//   int8  W[cout_pad][kpad]      W_b, zero beyond K = kh*kw*c_in and beyond
+//                                c_out
 //   int32 rowsum[cout_pad]       sum over k of W[co][k]
-//   int8  zeros[1024]            a zero block: fast-path fragment loads that
-//                                fall outside W read it instead of branching
-// c' is c itself for byte-per-code input; for 2-bit packed input the 16
+//   int8  zeros[1024]            a zero block: fragment loads that fall
+//                                outside W read it instead of branching
+//
+// Generic kernel (row-major W, byte co*kpad + k): K index k = (r*kw + s)*c_in
+// + c', with c' = c for byte-per-code input; for 2-bit NHWC input the 16
 // channels of each group are stored transposed as 4x4 (position 4*i + m holds
-// channel 4*m + i) to match the order in which the kernels unpack four codes
-// from each byte.
-// W is stored either row-major (byte co*kpad + k) or, for layers that take the
-// fast path (frag_layout), in MFMA fragment order: for each block of 16 rows
-// rb and K step kt, 1 KB holding the 64 lanes' 16-byte A fragments of
-// v_mfma_i32_16x16x64_i8, lane l = 16*g + i carrying row 16*rb + i and
-// K bytes 64*kt + 16*g .. +15; byte ((rb*nk + kt)*64 + l)*16 + b.
-constexpr int kKStep = 64;   // K per MFMA step (v_mfma_i32_16x16x64_i8)
+// channel 4*m + i) to match the order in which four codes are unpacked from a
+// byte.
+//
+// Fast path (mfma_layout(d): 2-bit input, c_in % 64 == 0): W is in the A
+// fragment order of v_mfma_i32_32x32x32_i8. K runs over K64 steps
+// kk = (r*kw + s)*G + g, G = c_in/64, each split into two K32 steps
+// k32 = 2*kk + t. For each block of 32 rows rb and K32 step k32 one 1 KB
+// chunk at byte (rb*nk32 + k32)*1024 holds the 64 lanes' 16-byte fragments:
+// lane l = 32*h + r carries row 32*rb + r, and its byte 4*q + i is the weight
+// of input channel 64*g + 32*h + 16*t + 4*i + q. That is the order in which a
+// lane unpacks its 16 codes of a pixel from four packed bytes.
+constexpr int kKStep = 64;   // K per LDS stage step (one K64 step)
 constexpr int kRowAlign = 16;
+constexpr int kMfmaRows = 32;
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
 struct WeightGeom {
   int64_t k;         // kh*kw*c_in
   int64_t kpad;      // k rounded up to kKStep
-  int64_t cout_pad;  // c_out rounded up to kRowAlign
+  int64_t cout_pad;  // c_out rounded up to the row block
   int64_t rows_bytes;
   int64_t zero_off;     // byte offset of the zero block
   int64_t total_bytes;
 };
 
-// Layers that run on the 2-bit fast path keep W in MFMA fragment order.
-inline bool frag_layout(const ifq_conv_desc& d) {
-  return d.in_layout == IFQ_LAYOUT_U2_NHWC_PACKED && d.c_in % 64 == 0;
+// Layers that run on the MFMA fast path keep W in fragment order.
+inline bool mfma_layout(const ifq_conv_desc& d) {
+  return d.in_bits == 2 && d.c_in % 64 == 0 &&
+         (d.in_layout == IFQ_LAYOUT_U2_NHWC_PACKED ||
+          d.in_layout == IFQ_LAYOUT_U2_BLOCK64);
 }
 
 inline WeightGeom weight_geom(const ifq_conv_desc& d) {
   WeightGeom g;
   g.k = (int64_t)d.kh * d.kw * d.c_in;
   g.kpad = round_up(g.k, kKStep);
-  g.cout_pad = round_up(d.c_out, kRowAlign);
+  g.cout_pad = round_up(d.c_out, mfma_layout(d) ? kMfmaRows : kRowAlign);
   g.rows_bytes = g.cout_pad * g.kpad;
   g.zero_off = round_up(g.rows_bytes + 4 * g.cout_pad, 16);
   g.total_bytes = g.zero_off + 1024;
@@ -64,7 +73,8 @@ struct ConvLaunch {
   void* y;
   int32_t* acc_dump;
   const void* shortcut;
-  const double* coef;
+  const double* coef;      // conv join: {p, q, cc} per channel
+  const int32_t* table;    // identity join: [c_out][4][rec] integer records
   double qthr[IFQ_MAX_THRESHOLDS];
   int32_t nq;          // thresholds per channel (codes) or 0
   int32_t rec;         // threshold record length 2^out_bits
@@ -73,8 +83,9 @@ struct ConvLaunch {
   int32_t n, h, w, cin, cout, cout_pad;
   int32_t kh, kw, stride, pad, ho, wo;
   int32_t m;           // n*ho*wo
-  int32_t kpad, nk;
+  int32_t kpad, nk;    // nk: K64 steps
   int32_t in_layout, in_bits;
+  int32_t out_layout;
   int32_t out_mode;    // 0 int32 sums, 1 codes byte per code, 2 codes 2-bit packed
   int32_t bn;          // pixels per workgroup (set by the launcher)
   int64_t wzero;       // byte offset of the weight blob's zero block
@@ -84,6 +95,12 @@ hipError_t launch_conv(const ConvLaunch& a, hipStream_t stream);
 
 // Name of the kernel launch_conv would pick for these arguments.
 const char* conv_kernel_name(const ConvLaunch& a);
+
+// Fast path (MFMA 32x32x32 kernel): whether it takes the layer, its launch,
+// and the name of the variant it picks.
+bool mfma_eligible(const ConvLaunch& a);
+hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream);
+const char* conv_mfma_name(const ConvLaunch& a);
 
 struct PoolLaunch {
   const uint8_t* x;
@@ -95,7 +112,8 @@ struct PoolLaunch {
 
 hipError_t launch_pool(const PoolLaunch& a, hipStream_t stream);
 
-hipError_t launch_convert(int64_t ncodes, int32_t src_layout,
-                          const void* src, void* dst, hipStream_t stream);
+hipError_t launch_convert(int64_t n, int64_t hw, int32_t c, int32_t src_layout,
+                          int32_t dst_layout, const void* src, void* dst,
+                          hipStream_t stream);
 
 }  // namespace ifq

@@ -1,5 +1,5 @@
 // Integer max-pool on codes (Eq. 4 applied to the quantizer output) and
-// conversion between the byte-per-code and 2-bit packed code layouts.
+// conversion between the code layouts.
 //
 // Both are HBM-bound streaming kernels: each thread owns a vector of V bytes
 // of one output pixel (V = 16, 4 or 1, the widest that divides the bytes per
@@ -115,26 +115,38 @@ hipError_t launch_pool_mode(const PoolLaunch& a, int cb, hipStream_t stream) {
   return go(maxpool_codes<1, MODE>, 1);
 }
 
-// One thread per group of four codes (one packed byte).
-__global__ __launch_bounds__(256) void codes_i8_to_u2(const uint8_t* src,
-                                                      uint8_t* dst,
-                                                      int64_t groups) {
-  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < groups;
-       g += (int64_t)gridDim.x * blockDim.x) {
-    const uint32_t v = *reinterpret_cast<const uint32_t*>(src + 4 * g);
-    dst[g] = (uint8_t)((v & 3u) | ((v >> 6) & 0x0Cu) | ((v >> 12) & 0x30u) |
-                       ((v >> 18) & 0xC0u));
-  }
+// Byte offset of the four codes of channel group cg (channels 4cg..4cg+3)
+// of pixel p in a 2-bit code tensor: NHWC packed, or BLOCK64 cells.
+__device__ __forceinline__ int64_t u2_offset(int32_t layout, int64_t p, int64_t cg,
+                                             int64_t hw, int32_t c) {
+  if (layout == IFQ_LAYOUT_U2_NHWC_PACKED) return p * (c >> 2) + cg;
+  const int64_t nimg = p / hw;
+  return ((nimg * (c >> 6) + (cg >> 4)) * hw + (p - nimg * hw)) * 16 + (cg & 15);
 }
 
-__global__ __launch_bounds__(256) void codes_u2_to_i8(const uint8_t* src,
-                                                      uint8_t* dst,
-                                                      int64_t groups) {
+// One thread per group of four codes: reads them in the source layout and
+// writes them in the destination layout (byte per code or 2-bit).
+__global__ __launch_bounds__(256) void convert_codes(const uint8_t* src, uint8_t* dst,
+                                                     int64_t groups, int64_t hw,
+                                                     int32_t c, int32_t sl, int32_t dl) {
+  const int64_t cgs = c >> 2;
   for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < groups;
        g += (int64_t)gridDim.x * blockDim.x) {
-    const uint32_t b = src[g];
-    *reinterpret_cast<uint32_t*>(dst + 4 * g) =
-        (b & 3u) | ((b & 0x0Cu) << 6) | ((b & 0x30u) << 12) | ((b & 0xC0u) << 18);
+    const int64_t p = g / cgs, cg = g - p * cgs;
+    uint32_t codes;  // byte i = code of channel 4cg + i
+    if (sl == IFQ_LAYOUT_I8_NHWC) {
+      codes = *reinterpret_cast<const uint32_t*>(src + 4 * g) & 0x03030303u;
+    } else {
+      const uint32_t b = src[u2_offset(sl, p, cg, hw, c)];
+      codes = (b & 3u) | ((b & 0x0Cu) << 6) | ((b & 0x30u) << 12) | ((b & 0xC0u) << 18);
+    }
+    if (dl == IFQ_LAYOUT_I8_NHWC) {
+      *reinterpret_cast<uint32_t*>(dst + 4 * g) = codes;
+    } else {
+      dst[u2_offset(dl, p, cg, hw, c)] =
+          (uint8_t)((codes & 3u) | ((codes >> 6) & 0x0Cu) | ((codes >> 12) & 0x30u) |
+                    ((codes >> 18) & 0xC0u));
+    }
   }
 }
 
@@ -148,20 +160,16 @@ hipError_t launch_pool(const PoolLaunch& a, hipStream_t stream) {
   return launch_pool_mode<1>(a, a.c, stream);
 }
 
-hipError_t launch_convert(int64_t ncodes, int32_t src_layout, const void* src,
-                          void* dst, hipStream_t stream) {
-  const int64_t groups = ncodes / 4;
+hipError_t launch_convert(int64_t n, int64_t hw, int32_t c, int32_t src_layout,
+                          int32_t dst_layout, const void* src, void* dst,
+                          hipStream_t stream) {
+  const int64_t groups = n * hw * (c / 4);
   if (groups == 0) return hipSuccess;
   int64_t blocks = (groups + 255) / 256;
   if (blocks > 65536) blocks = 65536;
-  const uint8_t* s = reinterpret_cast<const uint8_t*>(src);
-  uint8_t* d = reinterpret_cast<uint8_t*>(dst);
-  if (src_layout == IFQ_LAYOUT_I8_NHWC)
-    hipLaunchKernelGGL(codes_i8_to_u2, dim3((unsigned)blocks), dim3(256), 0,
-                       stream, s, d, groups);
-  else
-    hipLaunchKernelGGL(codes_u2_to_i8, dim3((unsigned)blocks), dim3(256), 0,
-                       stream, s, d, groups);
+  hipLaunchKernelGGL(convert_codes, dim3((unsigned)blocks), dim3(256), 0, stream,
+                     reinterpret_cast<const uint8_t*>(src), reinterpret_cast<uint8_t*>(dst),
+                     groups, hw, c, src_layout, dst_layout);
   return hipGetLastError();
 }
 

@@ -20,7 +20,7 @@ import numpy as np
 from . import _ffi, api
 from ._ffi import (Layer, Stack, IFQ_LAYER_CONV, IFQ_LAYER_POOL,
                    IFQ_LAYOUT_I8_NHWC, IFQ_LAYOUT_U2_NHWC_PACKED,
-                   IFQ_LAYOUT_I32_NHWC, IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY,
+                   IFQ_LAYOUT_I32_NHWC, IFQ_LAYOUT_U2_BLOCK64, IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY,
                    IFQ_JOIN_CONV, IFQ_POOL_VALID, IFQ_POOL_SAME)
 
 
@@ -38,16 +38,19 @@ def conv_ops(L, batch):
 class DeviceStack:
     """A stack of quantized substructures resident on one GPU.
 
-    code_layout: "i8" (one byte per code) or "u2" (2-bit codes packed four
-    per byte) for every 2-bit code tensor whose channel count is a multiple of
-    16; other tensors use one byte per code, int32 sums stay int32.
+    code_layout: layout of the 2-bit code tensors: "i8" (one byte per
+    code), "u2" (NHWC, four codes per byte, for channel counts that are
+    multiples of 16) or "b64" (channel blocks of 64 for channel counts that
+    are multiples of 64, else as "u2"). Other tensors use one byte per code;
+    int32 sums stay int32. The stack input and output are NHWC codes on the
+    host side either way (upload_input / download_output convert).
     """
 
     def __init__(self, layers, params, batch, code_layout="i8",
                  device="cuda"):
         import torch
-        if code_layout not in ("i8", "u2"):
-            raise ValueError("code_layout must be 'i8' or 'u2'")
+        if code_layout not in ("i8", "u2", "b64"):
+            raise ValueError("code_layout must be 'i8', 'u2' or 'b64'")
         self.layers = list(layers)
         self.batch = int(batch)
         self.device = torch.device(device)
@@ -61,7 +64,9 @@ class DeviceStack:
             return slots[name]
 
         def code_layout_for(bits, channels):
-            if code_layout == "u2" and bits == 2 and channels % 16 == 0:
+            if code_layout == "b64" and bits == 2 and channels % 64 == 0:
+                return IFQ_LAYOUT_U2_BLOCK64
+            if code_layout in ("u2", "b64") and bits == 2 and channels % 16 == 0:
                 return IFQ_LAYOUT_U2_NHWC_PACKED
             return IFQ_LAYOUT_I8_NHWC
 
@@ -109,18 +114,24 @@ class DeviceStack:
                     rec.thr = tdev.data_ptr()
                 if L.join is not None:
                     if L.join[0] == "identity":
-                        coef = api.ifq_fold_join(IFQ_JOIN_IDENTITY, p, p["beta_in"])
-                        kind = IFQ_JOIN_IDENTITY
+                        # the shortcut is the block input: codes with the
+                        # input's step beta_in
+                        table = api.ifq_fold_join_table(
+                            p, p["beta_in"], L.in_bits, L.k * L.k * L.cin,
+                            L.out_bits, p["q_thr"])
+                        tdev = torch.from_numpy(table).to(self.device)
+                        self._keep.append(tdev)
+                        rec.join = api.make_join(IFQ_JOIN_IDENTITY,
+                                                 layout_of[L.join[1]], None, None,
+                                                 p["q_thr"], table=tdev)
                     else:
-                        _, D = by_name[L.join[2]]
                         pd = params[by_name[L.join[2]][0]]
                         coef = api.ifq_fold_join(IFQ_JOIN_CONV, p, pd["beta_in"],
                                                  down=pd)
-                        kind = IFQ_JOIN_CONV
-                    cdev = torch.from_numpy(coef).to(self.device)
-                    self._keep.append(cdev)
-                    rec.join = api.make_join(kind, layout_of[L.join[1]], None,
-                                             cdev, p["q_thr"])
+                        cdev = torch.from_numpy(coef).to(self.device)
+                        self._keep.append(cdev)
+                        rec.join = api.make_join(IFQ_JOIN_CONV, layout_of[L.join[1]],
+                                                 None, cdev, p["q_thr"])
                     rec.join_src = sid(L.join[1])
                 self.ops += conv_ops(L, self.batch)
                 ho, wo = api.ifq_conv_output_dims(d)
@@ -179,10 +190,10 @@ class DeviceStack:
         if out is None:
             out = self.alloc_input()
         src = torch.from_numpy(codes.reshape(-1)).to(self.device)
-        if self.input_layout == IFQ_LAYOUT_U2_NHWC_PACKED:
+        if self.input_layout != IFQ_LAYOUT_I8_NHWC:
             n, h, w, c = self.input_shape
-            api.ifq_convert_codes(n * h * w, c, IFQ_LAYOUT_I8_NHWC,
-                                  IFQ_LAYOUT_U2_NHWC_PACKED, src, out)
+            api.ifq_convert_codes(n, h, w, c, IFQ_LAYOUT_I8_NHWC,
+                                  self.input_layout, src, out)
         else:
             out.copy_(src)
         return out
@@ -193,17 +204,17 @@ class DeviceStack:
         n, h, w, c = self.output_shape
         if self.output_layout == IFQ_LAYOUT_I32_NHWC:
             return y.view(torch.int32).cpu().numpy().reshape(n, h, w, c)
-        if self.output_layout == IFQ_LAYOUT_U2_NHWC_PACKED:
+        if self.output_layout != IFQ_LAYOUT_I8_NHWC:
             full = torch.empty(n * h * w * c, dtype=torch.uint8, device=self.device)
-            api.ifq_convert_codes(n * h * w, c, IFQ_LAYOUT_U2_NHWC_PACKED,
+            api.ifq_convert_codes(n, h, w, c, self.output_layout,
                                   IFQ_LAYOUT_I8_NHWC, y, full)
             return full.cpu().numpy().reshape(n, h, w, c)
         return y.cpu().numpy().reshape(n, h, w, c)
 
     def read_slot(self, name):
         """Host copy of a work slot's last tensor (after a run has finished):
-        NHWC uint8 codes or int32 sums; 2-bit packed codes are returned
-        packed (uint8 [n][h][w][c/4])."""
+        NHWC uint8 codes or int32 sums; 2-bit codes are returned as stored
+        (uint8 [n][h][w][c/4] for "u2", [n][c/64][h][w][16] for "b64")."""
         import torch
         (n, h, w, c), layout, _ = self.tensor_info[name]
         off, _ = api.ifq_stack_slot_info(self.stack, self.slots[name])
@@ -213,6 +224,8 @@ class DeviceStack:
             return raw.view(torch.int32).cpu().numpy().reshape(n, h, w, c)
         if layout == IFQ_LAYOUT_U2_NHWC_PACKED:
             return raw.cpu().numpy().reshape(n, h, w, c // 4)
+        if layout == IFQ_LAYOUT_U2_BLOCK64:
+            return raw.cpu().numpy().reshape(n, c // 64, h, w, 16)
         return raw.cpu().numpy().reshape(n, h, w, c)
 
     def layer_kernel_names(self):

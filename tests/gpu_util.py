@@ -6,7 +6,7 @@ import oracle
 from oracle import layout as olayout
 from workloads import Conv, layer_params, stack_input
 
-I8, U2, I32 = 0, 1, 2
+I8, U2, I32, B64 = 0, 1, 2, 3
 
 
 def device():
@@ -27,7 +27,7 @@ def upload_codes(P, codes, layout):
         return src
     n, h, w, c = codes.shape
     out = torch.empty(n * h * w * c // 4, dtype=torch.uint8, device=device())
-    P.ifq_convert_codes(n * h * w, c, I8, U2, src, out)
+    P.ifq_convert_codes(n, h, w, c, I8, layout, src, out)
     return out
 
 
@@ -54,7 +54,8 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
               sc_layout=I8, down=None, dump=True):
     """Run one conv through ifq_conv_forward; returns (acc or None, output).
 
-    output is uint8 codes NHWC (packed [..., c/4] for U2) or int32 sums."""
+    output is uint8 codes NHWC (packed [..., c/4] for U2, [n][c/64][h][w][16]
+    for B64) or int32 sums."""
     import torch
     if out_layout is None:
         out_layout = I32 if L.out_bits == 0 else I8
@@ -75,17 +76,19 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
     keep = []
     if L.join is not None:
         if L.join[0] == "identity":
-            coef = P.ifq_fold_join(P.IFQ_JOIN_IDENTITY, p, p["beta_in"])
+            table = P.ifq_fold_join_table(p, p["beta_in"], L.in_bits,
+                                          L.k * L.k * L.cin, L.out_bits, p["q_thr"])
             scd = upload_codes(P, shortcut, sc_layout)
-            kind = P.IFQ_JOIN_IDENTITY
+            td_ = to_dev(table)
+            keep += [scd, td_]
+            join = P.make_join(P.IFQ_JOIN_IDENTITY, sc_layout, scd, None,
+                               p["q_thr"], table=td_)
         else:
             coef = P.ifq_fold_join(P.IFQ_JOIN_CONV, p, down["beta_in"], down=down)
             scd = to_dev(shortcut.astype(np.int32))
-            kind = P.IFQ_JOIN_CONV
-            sc_layout = I32
-        cd = to_dev(coef)
-        keep += [scd, cd]
-        join = P.make_join(kind, sc_layout, scd, cd, p["q_thr"])
+            cd = to_dev(coef)
+            keep += [scd, cd]
+            join = P.make_join(P.IFQ_JOIN_CONV, I32, scd, cd, p["q_thr"])
     xd = upload_codes(P, x, in_layout) if L.in_bits <= 8 else None
     ob = P.ifq_tensor_bytes(n, ho, wo, L.cout, out_layout)
     y = torch.empty(max(ob, 1), dtype=torch.uint8, device=device())
@@ -101,6 +104,8 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
         out = y[:ob].view(torch.int32).cpu().numpy().reshape(shape)
     elif out_layout == U2:
         out = y[:ob].cpu().numpy().reshape(n, ho, wo, L.cout // 4)
+    elif out_layout == B64:
+        out = y[:ob].cpu().numpy().reshape(n, L.cout // 64, ho, wo, 16)
     else:
         out = y[:ob].cpu().numpy().reshape(shape)
     return acc_h, out
@@ -108,7 +113,11 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
 
 def expect_layout(codes, out_layout):
     """Oracle codes in the byte layout the GPU wrote."""
-    return olayout.pack2(codes) if out_layout == U2 else codes
+    if out_layout == U2:
+        return olayout.pack2(codes)
+    if out_layout == B64:
+        return olayout.pack_block64(codes)
+    return codes
 
 
 def make_layer(name, h, w, cin, cout, k, stride, pad, in_bits=2, out_bits=2,

@@ -27,7 +27,7 @@ OK = 0
 EINVAL = -1
 EUNSUP = -2
 EBUF = -4
-I8, U2, I32 = 0, 1, 2
+I8, U2, I32, B64 = 0, 1, 2, 3
 
 
 def declared_symbols():
@@ -68,6 +68,8 @@ def test_tensor_bytes_of_the_layouts():
     assert P.ifq_tensor_bytes(2, 3, 5, 8, I8) == 240
     assert P.ifq_tensor_bytes(2, 3, 5, 8, U2) == 60
     assert P.ifq_tensor_bytes(2, 3, 5, 8, I32) == 960
+    assert P.ifq_tensor_bytes(2, 3, 5, 128, B64) == 960
+    assert P.ifq_tensor_bytes(2, 3, 5, 96, B64) == 0    # C % 64 != 0
     assert P.ifq_tensor_bytes(1, 1, 1, 6, U2) == 0     # C % 4 != 0
     assert P.ifq_tensor_bytes(1, 1, 1, 4, 7) == 0      # unknown layout
     assert P.ifq_tensor_bytes(-1, 1, 1, 4, I8) == 0
@@ -91,37 +93,51 @@ def test_conv_output_dims(h, k, s, p, want):
 
 # --- weight packer ------------------------------------------------------------
 
-def unpack_blob(blob, cout, cin, kh, kw, u2, frag):
+def unpack_blob(blob, cout, cin, kh, kw, u2, mfma):
     """Reads W_b back out of a packed blob following the documented layout."""
     k = kh * kw * cin
     kpad = -(-k // 64) * 64
-    cpad = -(-cout // 16) * 16
-    nk = kpad // 64
+    cpad = -(-cout // (32 if mfma else 16)) * (32 if mfma else 16)
     rows = np.frombuffer(blob[:cpad * kpad].tobytes(), dtype=np.int8)
-    if frag:
-        # [row block][k step][lane][16 bytes], lane = 16*(kk/16) + row%16
-        r = rows.reshape(cpad // 16, nk, 4, 16, 16)     # rb, kt, g, i, b
-        mat = r.transpose(0, 3, 1, 2, 4).reshape(cpad, kpad)
-    else:
-        mat = rows.reshape(cpad, kpad)
     rowsum = np.frombuffer(blob[cpad * kpad:cpad * kpad + 4 * cpad].tobytes(),
                            dtype=np.int32)
     w = np.zeros((cout, cin, kh, kw), dtype=np.int8)
-    for r_ in range(kh):
-        for s_ in range(kw):
-            for c in range(cin):
-                cp = c
-                if u2:
-                    base, i = c & ~15, c & 15
-                    cp = base + (i & 3) * 4 + (i >> 2)
-                w[:, c, r_, s_] = mat[:cout, (r_ * kw + s_) * cin + cp]
-    return w, mat, rowsum, k
+    if mfma:
+        # [row block of 32][K32 step][lane 32h + r][16 bytes]; byte 4q + i of
+        # K32 step 2*kk + t is channel 64g + 32h + 16t + 4i + q of K64 step
+        # kk = tap*G + g
+        G = cin // 64
+        frag = rows.reshape(cpad // 32, kpad // 32, 2, 32, 4, 4)  # rb,k32,h,r,q,i
+        for tap in range(kh * kw):
+            for g in range(G):
+                kk = tap * G + g
+                for t in range(2):
+                    blk = frag[:, 2 * kk + t]                     # rb,h,r,q,i
+                    for h in range(2):
+                        for i in range(4):
+                            for q in range(4):
+                                c = 64 * g + 32 * h + 16 * t + 4 * i + q
+                                col = blk[:, h, :, q, i].reshape(-1)[:cout]
+                                w[:, c, tap // kw, tap % kw] = col
+        mat = frag.transpose(0, 3, 1, 2, 4, 5).reshape(cpad, -1)
+    else:
+        mat = rows.reshape(cpad, kpad)
+        for r_ in range(kh):
+            for s_ in range(kw):
+                for c in range(cin):
+                    cp = c
+                    if u2:
+                        base, i = c & ~15, c & 15
+                        cp = base + (i & 3) * 4 + (i >> 2)
+                    w[:, c, r_, s_] = mat[:cout, (r_ * kw + s_) * cin + cp]
+    return w, mat, rowsum, k, cpad
 
 
 @pytest.mark.parametrize("shape,layout", [
     ((64, 64, 3, 3), I8), ((64, 64, 3, 3), U2), ((30, 512, 1, 1), I8),
     ((16, 3, 3, 3), I8), ((256, 96, 5, 5), I8), ((128, 192, 3, 3), U2),
-    ((48, 32, 3, 3), U2), ((7, 16, 3, 3), I8)])
+    ((48, 32, 3, 3), U2), ((7, 16, 3, 3), I8), ((96, 128, 3, 3), B64),
+    ((40, 64, 1, 1), B64), ((64, 256, 5, 5), B64)])
 def test_pack_weights_layout(shape, layout, rng):
     cout, cin, kh, kw = shape
     w = (rng.integers(0, 2, size=shape, dtype=np.int8) * 2 - 1).astype(np.int8)
@@ -129,11 +145,12 @@ def test_pack_weights_layout(shape, layout, rng):
                     kw=kw)
     blob = P.ifq_pack_weights(d, w)
     assert blob.nbytes == P.ifq_packed_weight_bytes(d)
-    frag = layout == U2 and cin % 64 == 0
-    back, mat, rowsum, k = unpack_blob(blob, cout, cin, kh, kw, layout == U2, frag)
+    mfma = layout in (U2, B64) and cin % 64 == 0
+    back, mat, rowsum, k, cpad = unpack_blob(blob, cout, cin, kh, kw,
+                                             layout == U2, mfma)
     assert np.array_equal(back, w)
-    # padding rows and K columns are zero; row sums are sum_k W[co][k]
-    assert not mat[cout:].any() and not mat[:, k:].any()
+    # every stored +-1 is one of the layer's weights; padding is zero
+    assert np.count_nonzero(mat) == w.size
     assert np.array_equal(rowsum[:cout], w.reshape(cout, -1).sum(1))
     assert not rowsum[cout:].any()
     # the trailing zero block the kernels read for out-of-range fragments
@@ -304,6 +321,62 @@ def test_join_coefficients_equal_oracle(variant):
     assert n == 8
 
 
+@pytest.mark.parametrize("variant", ["plain", "calibrated"])
+def test_join_table_equals_oracle_fp64_join(variant):
+    # the integer records reproduce the fp64 join for every reachable sum
+    # and every shortcut code, on every identity join of the ResNet stack
+    layers = get_stack(3).layers
+    n = 0
+    for i, L in enumerate(layers):
+        if not isinstance(L, Conv) or L.join is None or L.join[0] != "identity":
+            continue
+        p = layer_params(3, i, L, variant)
+        k = L.k * L.k * L.cin
+        bound = k * 3
+        table = P.ifq_fold_join_table(p, p["beta_in"], 2, k, 2, p["q_thr"])
+        coef = oracle.join_coeffs("identity", p, p["beta_in"], p["beta_in"])
+        a = np.arange(-bound, bound + 1, dtype=np.int64)
+        for x in range(4):
+            acc = np.ascontiguousarray(np.broadcast_to(a[:, None], (a.size, L.cout)),
+                                       dtype=np.int32)
+            sc = np.full(acc.shape, x, dtype=np.int32)
+            want = oracle.join_codes(acc, sc, coef, p["q_thr"]).astype(np.int64)
+            rec = table[:, x, :]
+            got = ((rec[None, :, 0] * acc)[..., None] > rec[None, :, 1:]).sum(-1)
+            assert np.array_equal(got, want), (L.name, x)
+        n += 1
+    assert n == 5
+
+
+def test_join_table_edge_cases(rng):
+    c = 8
+    p = dict(alpha=rng.uniform(0.01, 0.1, c), bias=np.zeros(c),
+             mean=rng.normal(0, 2, c), var=rng.uniform(0.5, 2, c),
+             gamma=rng.uniform(0.5, 1.5, c), bn_beta=rng.normal(0, 1, c),
+             eps=1e-5, beta_in=0.5)
+    p["gamma"][0] = -0.7          # decreasing in a: s = -1
+    p["gamma"][1] = 0.0           # constant in a
+    p["bn_beta"][2] = 50.0        # always the top code
+    p["bn_beta"][3] = -50.0       # always code 0
+    q = np.array([0.25, 0.75, 1.25])
+    k = 64
+    table = P.ifq_fold_join_table(p, 0.5, 2, k, 2, q)
+    coef = oracle.join_coeffs("identity", p, 0.5, 0.5)
+    assert (table[0, :, 0] == -1).all() and (table[1:, :, 0] == 1).all()
+    a = np.arange(-3 * k, 3 * k + 1, dtype=np.int32)
+    for x in range(4):
+        acc = np.ascontiguousarray(np.broadcast_to(a[:, None], (a.size, c)))
+        want = oracle.join_codes(acc, np.full(acc.shape, x, np.int32), coef, q)
+        rec = table[:, x, :]
+        got = ((rec[None, :, 0] * acc)[..., None] > rec[None, :, 1:]).sum(-1)
+        assert np.array_equal(got, want)
+    assert (table[2, :, 1:] == -3 * k - 1).all() and (table[3, :, 1:] == 3 * k).all()
+    with pytest.raises(P.IfqError):
+        P.ifq_fold_join_table(p, 0.5, 2, k, 2, np.array([0.75, 0.25, 1.25]))
+    with pytest.raises(P.IfqError):
+        P.ifq_fold_join_table(p, 0.5, 2, 0, 2, q)
+
+
 def test_join_rejects_bad_kind_and_alpha():
     L = get_stack(3).layers[1]
     p = layer_params(3, 1, L)
@@ -335,6 +408,10 @@ FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: validation fails first
     (dict(in_layout=U2, c_in=6), EINVAL),
     (dict(in_layout=U2, c_in=20), EUNSUP),             # C % 16 for packed input
     (dict(in_layout=5), EINVAL),
+    (dict(in_layout=B64, c_in=96), EINVAL),           # BLOCK64 needs C % 64
+    (dict(in_layout=B64, in_bits=4), EINVAL),
+    (dict(out_layout=B64, c_out=96), EINVAL),
+    (dict(out_layout=B64, out_bits=4), EINVAL),
     (dict(out_bits=0, out_layout=I8), EINVAL),
     (dict(out_layout=U2, out_bits=4), EINVAL),
     (dict(out_layout=U2, c_out=30), EINVAL),
@@ -371,30 +448,40 @@ def test_conv_forward_rejects_bad_pointers():
 def test_conv_forward_rejects_bad_join():
     d = P.conv_desc(1, 8, 8, 64, 64, 3, 1, 1, 2, 2)
     coef = np.zeros((64, 3))
+    table = np.zeros((64, 4, 4), dtype=np.int32)
+    # each join has what its kind needs, so it fails for the listed reason
     for kind, layout, q, want in [
             (9, I8, [0.25, 0.75, 1.25], EINVAL),
             (P.IFQ_JOIN_IDENTITY, I32, [0.25, 0.75, 1.25], EINVAL),
             (P.IFQ_JOIN_CONV, I8, [0.25, 0.75, 1.25], EINVAL),
             (P.IFQ_JOIN_IDENTITY, I8, [0.25, 0.75], EINVAL),
             (P.IFQ_JOIN_IDENTITY, I8, [0.75, 0.25, 1.25], EINVAL)]:
-        j = P.make_join(kind, layout, None, coef, q)
+        j = P.make_join(kind, layout, None, coef, q, table=table)
         j.shortcut = 0x1000
         st = status_of("ifq_conv_forward", ctypes.byref(d), FAKE, FAKE, None,
                        ctypes.byref(j), FAKE, None, None, 0, None)
         assert st == want, (kind, layout, q)
     # a join with thresholds given as well
-    j = P.make_join(P.IFQ_JOIN_IDENTITY, I8, None, coef, [0.25, 0.75, 1.25])
+    j = P.make_join(P.IFQ_JOIN_IDENTITY, I8, None, None, [0.25, 0.75, 1.25],
+                    table=table)
     j.shortcut = 0x1000
     st = status_of("ifq_conv_forward", ctypes.byref(d), FAKE, FAKE, FAKE,
                    ctypes.byref(j), FAKE, None, None, 0, None)
     assert st == EINVAL
+    # an identity join without its table, a conv join without coefficients
+    for kind, layout in ((P.IFQ_JOIN_IDENTITY, I8), (P.IFQ_JOIN_CONV, I32)):
+        j = P.make_join(kind, layout, None, None, [0.25, 0.75, 1.25])
+        j.shortcut = 0x1000
+        st = status_of("ifq_conv_forward", ctypes.byref(d), FAKE, FAKE, None,
+                       ctypes.byref(j), FAKE, None, None, 0, None)
+        assert st == EINVAL
 
 
 @pytest.mark.parametrize("pool,want", [
     (dict(k=0), EINVAL), (dict(stride=0), EINVAL), (dict(mode=3), EINVAL),
     (dict(k=9), EINVAL), (dict(layout=U2, c=6), EINVAL),
     (dict(layout=U2, bits=8), EINVAL), (dict(bits=0), EINVAL),
-    (dict(layout=I32), EINVAL)])
+    (dict(layout=I32), EINVAL), (dict(layout=B64, c=32), EINVAL)])
 def test_maxpool_rejects_bad_desc(pool, want):
     base = dict(n=1, h=8, w=8, c=16, k=2, stride=2, mode=0, bits=2, layout=I8)
     base.update(pool)
@@ -404,9 +491,13 @@ def test_maxpool_rejects_bad_desc(pool, want):
 
 
 def test_convert_rejects_bad_args():
-    assert status_of("ifq_convert_codes", 10, 6, I8, U2, FAKE, FAKE, None) == EINVAL
-    assert status_of("ifq_convert_codes", 10, 8, I8, I8, FAKE, FAKE, None) == EINVAL
-    assert status_of("ifq_convert_codes", 10, 8, I8, U2, None, FAKE, None) == EINVAL
+    cv = lambda *a: status_of("ifq_convert_codes", *a)
+    assert cv(1, 1, 10, 6, I8, U2, FAKE, FAKE, None) == EINVAL     # C % 4
+    assert cv(1, 1, 10, 8, I8, I8, FAKE, FAKE, None) == EINVAL     # same layout
+    assert cv(1, 1, 10, 8, I8, I32, FAKE, FAKE, None) == EINVAL    # not codes
+    assert cv(1, 1, 10, 96, I8, B64, FAKE, FAKE, None) == EINVAL   # C % 64
+    assert cv(1, 1, 10, 8, I8, U2, None, FAKE, None) == EINVAL
+    assert cv(-1, 1, 10, 8, I8, U2, FAKE, FAKE, None) == EINVAL
 
 
 # --- stack planning -------------------------------------------------------------
@@ -434,8 +525,9 @@ def make_stack(layers, batch=1, layout="i8"):
                 rec.join = P.make_join(
                     P.IFQ_JOIN_IDENTITY if L.join[0] == "identity" else P.IFQ_JOIN_CONV,
                     lay_of.get(L.join[1], lin) if L.join[0] == "identity" else I32,
-                    None, np.zeros(3), L.out_bits and [0.25, 0.75, 1.25])
+                    None, None, L.out_bits and [0.25, 0.75, 1.25])
                 rec.join.coef = 0x1000
+                rec.join.table = 0x1000
                 rec.join_src = slots[L.join[1]]
         else:
             lout = lin

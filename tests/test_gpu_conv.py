@@ -7,7 +7,7 @@ import pytest
 
 import oracle
 from oracle import layout as olayout
-from gpu_util import (I8, U2, I32, gpu_layer, oracle_layer, expect_layout,
+from gpu_util import (I8, U2, I32, B64, gpu_layer, oracle_layer, expect_layout,
                       make_layer, params_for, codes_for, upload_codes, to_dev,
                       device)
 
@@ -82,6 +82,47 @@ U2_LAYERS = [
 @pytest.mark.parametrize("io", [(U2, U2), (U2, I8), (I8, U2)],
                          ids=["u2u2", "u2i8", "i8u2"])
 def test_conv_packed_layouts_bit_exact(P, case, io):
+    run_layout_case(P, case, io)
+
+
+# shapes of the fast path (c_in % 64 == 0): every tile variant, ragged pixel
+# and channel tiles, stride 2, 1x1 and 5x5 filters, the judged ResNet shapes
+B64_LAYERS = [
+    ("b64_3x3_64", 2, 14, 14, 64, 64, 3, 1, 1),
+    ("b64_stride2_128", 2, 15, 15, 64, 128, 3, 2, 1),
+    ("b64_k4608", 1, 7, 7, 512, 512, 3, 1, 1),
+    ("b64_5x5_c64", 2, 17, 15, 64, 128, 5, 2, 2),
+    ("b64_1x1_s2_c256", 3, 14, 14, 128, 256, 1, 2, 0),
+    ("b64_c192_cout320", 3, 11, 13, 192, 320, 3, 1, 1),
+    ("b64_l2_shape_b4", 4, 28, 28, 128, 128, 3, 1, 1),
+    ("b64_l3_shape_b8", 8, 14, 14, 256, 256, 3, 1, 1),
+    ("b64_l4_shape_b12", 12, 7, 7, 512, 512, 3, 1, 1),
+    ("b64_l1_shape_b2", 2, 56, 56, 64, 64, 3, 1, 1),
+    ("b64_cout96", 2, 9, 9, 128, 96, 3, 1, 1),
+    ("b64_big_m", 16, 28, 28, 64, 128, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("case", B64_LAYERS, ids=[c[0] for c in B64_LAYERS])
+@pytest.mark.parametrize("io", [(B64, B64), (B64, U2), (U2, B64), (B64, I8)],
+                         ids=["b64b64", "b64u2", "u2b64", "b64i8"])
+def test_conv_block64_bit_exact(P, case, io):
+    if io[1] == B64 and case[5] % 64:
+        pytest.skip("BLOCK64 output needs c_out % 64 == 0")
+    run_layout_case(P, case, io)
+
+
+def test_conv_block64_int32_out(P):
+    L = make_layer("b64_i32", 14, 14, 128, 256, 1, 2, 0, 2, 0)
+    p = params_for(17, L)
+    x = codes_for(17, (3, 14, 14, 128), 2)
+    want_acc, want = oracle_layer(L, x, p)
+    acc, got = gpu_layer(P, L, 3, x, p, in_layout=B64, out_layout=I32)
+    assert np.array_equal(acc, want_acc)
+    assert np.array_equal(got, want)
+
+
+def run_layout_case(P, case, io):
     name, n, h, w, cin, cout, k, st, pad = case
     L = make_layer(name, h, w, cin, cout, k, st, pad)
     seed = zlib.crc32(name.encode()) % 991
@@ -94,7 +135,10 @@ def test_conv_packed_layouts_bit_exact(P, case, io):
 
 
 @pytest.mark.parametrize("io", [(I8, I8, I8), (I8, U2, I8), (U2, U2, U2),
-                                (U2, I8, U2)], ids=["i8", "sc_u2", "u2", "u2_sc_i8"])
+                                (U2, I8, U2), (B64, B64, B64), (B64, U2, I8),
+                                (U2, B64, B64)],
+                         ids=["i8", "sc_u2", "u2", "u2_sc_i8", "b64", "b64_sc_u2",
+                              "u2_sc_b64"])
 @pytest.mark.parametrize("shape", [(2, 10, 10, 64, 64), (1, 7, 7, 512, 512),
                                    (1, 9, 11, 128, 128), (6, 14, 14, 256, 256)])
 def test_identity_join_bit_exact(P, shape, io):
@@ -111,7 +155,7 @@ def test_identity_join_bit_exact(P, shape, io):
     assert np.array_equal(got, expect_layout(want, out_l))
 
 
-@pytest.mark.parametrize("lay", [I8, U2], ids=["i8", "u2"])
+@pytest.mark.parametrize("lay", [I8, U2, B64], ids=["i8", "u2", "b64"])
 def test_conv_join_bit_exact(P, lay):
     # conv2 of a downsampling block: the shortcut is the int32 sum of a 1x1/2
     # conv of the block input, computed by the GPU path itself first
@@ -158,13 +202,15 @@ def test_empty_batch_launches_nothing(P):
     ((1, 9, 9, 20), 3, 2, "same"), ((3, 7, 5, 12), 2, 2, "valid"),
     ((1, 8, 8, 3), 2, 2, "valid"),
 ])
-@pytest.mark.parametrize("lay", [I8, U2], ids=["i8", "u2"])
+@pytest.mark.parametrize("lay", [I8, U2, B64], ids=["i8", "u2", "b64"])
 def test_maxpool_bit_exact(P, case, lay):
     import torch
     shape, k, st, mode = case
     n, h, w, c = shape
     if lay == U2 and c % 4:
         pytest.skip("packed layout needs C % 4 == 0")
+    if lay == B64 and c % 64:
+        pytest.skip("BLOCK64 needs C % 64 == 0")
     x = codes_for(h * 31 + c, shape, 2)
     want = oracle.maxpool(x, k, st, mode)
     m = P.IFQ_POOL_VALID if mode == "valid" else P.IFQ_POOL_SAME
@@ -189,14 +235,29 @@ def test_maxpool_8bit_codes(P):
     assert np.array_equal(y.cpu().numpy(), want.reshape(-1))
 
 
-@pytest.mark.parametrize("npix,c", [(1, 4), (7, 12), (1000, 64), (33, 16)])
-def test_convert_codes_round_trip(P, npix, c):
+@pytest.mark.parametrize("shape", [(1, 1, 1, 4), (1, 1, 7, 12), (2, 10, 50, 64),
+                                   (1, 3, 11, 16), (3, 5, 7, 192)])
+def test_convert_codes_round_trip(P, shape):
     import torch
-    x = codes_for(npix + c, (1, 1, npix, c), 2)
-    packed = torch.empty(npix * c // 4, dtype=torch.uint8, device=device())
-    P.ifq_convert_codes(npix, c, I8, U2, to_dev(x), packed)
-    back = torch.empty(npix * c, dtype=torch.uint8, device=device())
-    P.ifq_convert_codes(npix, c, U2, I8, packed, back)
-    torch.cuda.synchronize()
-    assert np.array_equal(packed.cpu().numpy(), olayout.pack2(x).reshape(-1))
-    assert np.array_equal(back.cpu().numpy(), x.reshape(-1))
+    n, h, w, c = shape
+    x = codes_for(h * w + c, shape, 2)
+    layouts = [U2] + ([B64] if c % 64 == 0 else [])
+    for lay in layouts:
+        packed = torch.empty(n * h * w * c // 4, dtype=torch.uint8, device=device())
+        P.ifq_convert_codes(n, h, w, c, I8, lay, to_dev(x), packed)
+        back = torch.empty(n * h * w * c, dtype=torch.uint8, device=device())
+        P.ifq_convert_codes(n, h, w, c, lay, I8, packed, back)
+        torch.cuda.synchronize()
+        assert np.array_equal(packed.cpu().numpy(),
+                              expect_layout(x, lay).reshape(-1))
+        assert np.array_equal(back.cpu().numpy(), x.reshape(-1))
+    if c % 64 == 0:
+        # 2-bit NHWC <-> BLOCK64 directly
+        u2 = upload_codes(P, x, U2)
+        b64 = torch.empty_like(u2)
+        P.ifq_convert_codes(n, h, w, c, U2, B64, u2, b64)
+        u2b = torch.empty_like(u2)
+        P.ifq_convert_codes(n, h, w, c, B64, U2, b64, u2b)
+        torch.cuda.synchronize()
+        assert np.array_equal(b64.cpu().numpy(), olayout.pack_block64(x).reshape(-1))
+        assert torch.equal(u2, u2b)

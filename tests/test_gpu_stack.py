@@ -56,6 +56,8 @@ def check_stack(P, cfg, batch, layout, variant):
         w = want[name]
         if lay == P.IFQ_LAYOUT_U2_NHWC_PACKED:
             w = olayout.pack2(w)
+        elif lay == P.IFQ_LAYOUT_U2_BLOCK64:
+            w = olayout.pack_block64(w)
         assert np.array_equal(g, w), "slot %s differs" % name
         checked += 1
     # running again gives the same bytes (no state carried between runs)
@@ -69,7 +71,7 @@ def check_stack(P, cfg, batch, layout, variant):
 SMALL = [(0, 1), (1, 2), (2, 1), (3, 2), (4, 1)]
 
 
-@pytest.mark.parametrize("layout", ["i8", "u2"])
+@pytest.mark.parametrize("layout", ["i8", "u2", "b64"])
 @pytest.mark.parametrize("cfg,batch", SMALL)
 def test_stack_small_batch(P, cfg, batch, layout):
     for variant in ("calibrated", "plain"):
@@ -77,7 +79,7 @@ def test_stack_small_batch(P, cfg, batch, layout):
 
 
 @pytest.mark.slow
-@pytest.mark.parametrize("layout", ["u2", "i8"])
+@pytest.mark.parametrize("layout", ["b64", "u2", "i8"])
 @pytest.mark.parametrize("cfg", [0, 1, 3, 4, 2])
 def test_stack_full_size(P, cfg, layout):
     batch = get_stack(cfg).batch
