@@ -77,7 +77,7 @@ class Hip:
 
 def source_hash():
     h = hashlib.sha256()
-    for f in ("ifq_conv.hip", "ifq_pool.hip"):
+    for f in ("ifq_conv.hip", "ifq_conv_mfma.hip", "ifq_epilogue.h", "ifq_pool.hip"):
         with open(os.path.join(ROOT, "paper_1911_08076_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -98,6 +98,126 @@ def load_traffic(kernel, workload):
                 parts.get("workload") == workload and parts.get("src") == want):
             return float(parts["bytes_per_launch"])
     return None
+
+
+def _pmc_per_kernel(path):
+    """Mean value of each counter per dispatch, by kernel name, and the largest
+    single-dispatch value, from a rocprofv3 --pmc counter_collection.csv."""
+    import csv
+    import collections
+    per_disp = collections.defaultdict(lambda: collections.defaultdict(float))
+    kname = {}
+    for r in csv.DictReader(open(path)):
+        per_disp[r["Dispatch_Id"]][r["Counter_Name"]] += float(r["Counter_Value"])
+        kname[r["Dispatch_Id"]] = r["Kernel_Name"]
+    tot = collections.defaultdict(lambda: collections.defaultdict(float))
+    peak = collections.defaultdict(lambda: collections.defaultdict(float))
+    nd = collections.Counter()
+    for d, cs in per_disp.items():
+        k = kname[d]
+        nd[k] += 1
+        for c, v in cs.items():
+            tot[k][c] += v
+            peak[k][c] = max(peak[k][c], v)
+    return {k: ({c: v / nd[k] for c, v in cs.items()}, nd[k], dict(peak[k]))
+            for k, cs in tot.items()}
+
+
+def summarize_profiles(run_dir, workload, commands):
+    """Writes the committed text summaries of one profiling run.
+
+    run_dir holds kt/*kernel_stats.csv (rocprofv3 --kernel-trace --stats
+    --output-format csv), fetch/*counter_collection.csv (--pmc FETCH_SIZE)
+    and write/*counter_collection.csv (--pmc WRITE_SIZE) of the same
+    benchmark command run with --calib-copy. The counters of the 256 MiB
+    device copy give the factors that turn each counter into bytes; the
+    conv kernels' scaled bytes per launch go to profiles/traffic.txt under
+    the current source hash.
+    """
+    import csv
+    import glob
+    prof = os.path.join(ROOT, "profiles")
+    os.makedirs(prof, exist_ok=True)
+
+    def one(pattern):
+        got = sorted(glob.glob(os.path.join(run_dir, pattern)))
+        if not got:
+            raise SystemExit("no %s under %s" % (pattern, run_dir))
+        return got[0]
+
+    rows = list(csv.DictReader(open(one("kt/*kernel_stats.csv"))))
+    fetch = _pmc_per_kernel(one("fetch/*counter_collection.csv"))
+    write = _pmc_per_kernel(one("write/*counter_collection.csv"))
+    copy_bytes = 256 << 20
+
+    def copy_counter(table, counter):
+        # the largest single dispatch of a copy kernel is the 256 MiB copy
+        best = None
+        for k, (_, _, pk) in table.items():
+            if "copy" in k.lower() and counter in pk:
+                if best is None or pk[counter] > best:
+                    best = pk[counter]
+        return best
+
+    cf, cw = copy_counter(fetch, "FETCH_SIZE"), copy_counter(write, "WRITE_SIZE")
+    f_fetch = copy_bytes / cf if cf else None
+    f_write = copy_bytes / cw if cw else None
+
+    def short(name):
+        base = name.replace("(anonymous namespace)::", "").split("(")[0]
+        return base.replace("void ", "").replace("ifq::", "").strip()
+
+    lines = ["# rocprofv3 summary: %s" % workload, ""]
+    lines += ["commands (run from the repository root):"] + ["  " + c for c in commands]
+    lines += ["", "kernel trace (--kernel-trace --stats):",
+              "%-44s %6s %10s %7s %10s %10s" % ("kernel", "calls", "avg_us", "pct",
+                                                 "min_us", "max_us")]
+    for r in rows:
+        lines.append("%-44s %6d %10.3f %7.2f %10.3f %10.3f" % (
+            short(r["Name"])[:44], int(r["Calls"]), float(r["AverageNs"]) / 1e3,
+            float(r["Percentage"]), float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3))
+    lines += ["", "HBM counters, mean per dispatch (KiB as read; bytes = KiB x factor)",
+              "calibration: 256 MiB device copy reads FETCH_SIZE %s KiB, writes "
+              "WRITE_SIZE %s KiB -> factors %s (fetch), %s (write) bytes per unit" % (
+                  "%.0f" % cf if cf else "n/a", "%.0f" % cw if cw else "n/a",
+                  "%.2f" % f_fetch if f_fetch else "n/a",
+                  "%.2f" % f_write if f_write else "n/a"),
+              "%-44s %6s %14s %14s %14s" % ("kernel", "disp", "FETCH_SIZE", "WRITE_SIZE",
+                                             "bytes/launch")]
+    traffic = []
+    for k in sorted(set(fetch) | set(write)):
+        fv, nd, _ = fetch.get(k, ({}, 0, {}))
+        wv, _, _ = write.get(k, ({}, 0, {}))
+        fz, wz = fv.get("FETCH_SIZE"), wv.get("WRITE_SIZE")
+        b = None
+        if fz is not None and wz is not None and f_fetch and f_write:
+            b = fz * f_fetch + wz * f_write
+        lines.append("%-44s %6d %14s %14s %14s" % (
+            short(k)[:44], nd, "%.1f" % fz if fz is not None else "-",
+            "%.1f" % wz if wz is not None else "-", "%.4g" % b if b else "-"))
+        if b and ("conv" in k):
+            traffic.append((short(k), b))
+    name = "conv_kernels_" + workload.replace(":", "_").replace("/", "_") + ".txt"
+    with open(os.path.join(prof, name), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    tpath = os.path.join(prof, "traffic.txt")
+    keep = []
+    if os.path.exists(tpath):
+        for line in open(tpath):
+            if line.startswith("#") or not line.strip():
+                continue
+            if ("workload=%s " % workload) in line + " ":
+                continue
+            keep.append(line.rstrip("\n"))
+    src = source_hash()
+    for k, b in traffic:
+        keep.append("kernel=%s workload=%s src=%s bytes_per_launch=%.0f" % (
+            k.replace(" ", ""), workload, src, b))
+    with open(tpath, "w") as fh:
+        fh.write("# HBM bytes per launch of each conv kernel (FETCH_SIZE + WRITE_SIZE, "
+                 "scaled by a 256 MiB copy), from %s\n" % name)
+        fh.write("\n".join(keep) + "\n")
+    print("wrote profiles/%s and profiles/traffic.txt" % name)
 
 
 def cpu_info():
@@ -128,9 +248,19 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run a plain 256 MiB device copy (counter calibration)")
+    ap.add_argument("--summarize", nargs=2, metavar=("RUN_DIR", "COMMANDS_FILE"),
+                    help="write profiles/ summaries from a rocprofv3 run and exit "
+                         "(no GPU use)")
     ap.add_argument("--layers-out", default=None,
                     help="write per-layer timings (JSON) to this path")
     args = ap.parse_args()
+
+    if args.summarize:
+        from workloads import get_stack
+        cmds = [c.strip() for c in open(args.summarize[1]) if c.strip()]
+        summarize_profiles(args.summarize[0],
+                           get_stack(args.config).name + ":" + args.layout, cmds)
+        return
 
     if args.gpus != 1:
         print("bench.py measures one GPU only: this path shards over batch with "

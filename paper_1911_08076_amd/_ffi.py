@@ -125,6 +125,12 @@ def load():
             "`python paper_1911_08076_amd/build.py` or "
             "`python -c 'import __graft_entry__; __graft_entry__.build()'`"
             % LIB_PATH)
+    # torch ships its own HIP runtime under the soname libamdhip64.so.7.
+    # Importing torch first makes the dynamic loader bind libifq.so to that
+    # same copy, so the process holds one HIP runtime and torch's streams and
+    # device pointers are valid in the library. Loaded the other way round,
+    # two runtimes end up in the process and the library's launches fail.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     for name, res, args in SIGNATURES:
         fn = getattr(lib, name)

@@ -239,6 +239,8 @@ ifq::ConvLaunch make_launch(const ifq_conv_desc* d, int64_t ho, int64_t wo,
   a.in_bits = d->in_bits;
   a.out_layout = d->out_layout;
   a.out_mode = d->out_bits == 0 ? 0 : d->out_layout == IFQ_LAYOUT_I8_NHWC ? 1 : 2;
+  a.div_howo = ifq::make_fastdiv((uint32_t)(ho * wo > 0 ? ho * wo : 1));
+  a.div_wo = ifq::make_fastdiv((uint32_t)(wo > 0 ? wo : 1));
   return a;
 }
 

@@ -91,7 +91,7 @@ template <int MODE, int FM, int FN>
 __device__ __forceinline__ void epilogue32(const ConvLaunch& a, const uint8_t* lds,
                                            const v16i (&acc)[FM][FN], int wm, int wn,
                                            int h, int l32, int co0, int p0, int bn,
-                                           uint8_t* otile, int orow) {
+                                           uint8_t* otile, int orow, int32_t* y32) {
   const int32_t* prm = reinterpret_cast<const int32_t*>(lds);
   const bool u2 = a.out_mode == 2;
   const int howo = a.ho * a.wo;
@@ -124,7 +124,7 @@ __device__ __forceinline__ void epilogue32(const ConvLaunch& a, const uint8_t* l
         } else {
           int64_t off;
           if (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64) {
-            const int nimg = p / howo;
+            const int nimg = fdiv(p, a.div_howo);
             off = (((int64_t)nimg * (a.cout >> 6) + (co >> 6)) * howo + (p - nimg * howo)) * 16 +
                   ((co & 63) >> 2);
           } else {
@@ -146,7 +146,7 @@ __device__ __forceinline__ void epilogue32(const ConvLaunch& a, const uint8_t* l
         for (int i = 0; i < 4; ++i) tr[i] = *reinterpret_cast<const int4*>(prm + (cl + i) * 4);
       }
       if constexpr (MODE == kE32Conv) {
-        const double* c = reinterpret_cast<const double*>(lds) + 3 * cl;
+        const double* c = reinterpret_cast<const double*>(lds + kJoinCoefOff) + 3 * cl;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           cf[i][0] = c[3 * i];
@@ -162,8 +162,7 @@ __device__ __forceinline__ void epilogue32(const ConvLaunch& a, const uint8_t* l
         for (int i = 0; i < 4; ++i) v[i] = acc[fm][fn][4 * b + i];
         if constexpr (MODE == kE32I32) {
           if (pl < bn && p0 + pl < a.m)
-            *reinterpret_cast<int4*>(reinterpret_cast<int32_t*>(a.y) +
-                                     (int64_t)(p0 + pl) * a.cout + co0 + cl) =
+            *reinterpret_cast<int4*>(y32 + (int64_t)(p0 + pl) * a.cout + co0 + cl) =
                 int4{v[0], v[1], v[2], v[3]};
           continue;
         }
@@ -171,7 +170,7 @@ __device__ __forceinline__ void epilogue32(const ConvLaunch& a, const uint8_t* l
         if constexpr (MODE == kE32Thr4) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int sv = tr[i].x * v[i];
+            const int sv = sgn(v[i], tr[i].x);
             code[i] = (sv > tr[i].y) + (sv > tr[i].z) + (sv > tr[i].w);
           }
         } else if constexpr (MODE == kE32Tab4) {
@@ -180,7 +179,7 @@ __device__ __forceinline__ void epilogue32(const ConvLaunch& a, const uint8_t* l
           for (int i = 0; i < 4; ++i) {
             const int x = (xs >> (2 * i)) & 3;
             const int4 t = *reinterpret_cast<const int4*>(prm + ((cl + i) * 4 + x) * 4);
-            const int sv = t.x * v[i];
+            const int sv = sgn(v[i], t.x);
             code[i] = (sv > t.y) + (sv > t.z) + (sv > t.w);
           }
         } else {
@@ -191,8 +190,9 @@ __device__ __forceinline__ void epilogue32(const ConvLaunch& a, const uint8_t* l
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const double z = fma(cf[i][0], (double)v[i], fma(cf[i][1], (double)dv[i], cf[i][2]));
+            const double* qt = reinterpret_cast<const double*>(lds);
             int c = 0;
-            for (int q = 0; q < a.nq; ++q) c += z > a.qthr[q];
+            for (int q = 0; q < a.nq; ++q) c += z > qt[q];
             code[i] = c;
           }
         }
@@ -286,9 +286,9 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void conv_mfma(ConvLaunch a) {
       const int pl = cb * 64 + lane;
       const int p = p0 + pl;
       if (pl < bn && p < a.m) {
-        const int nimg = p / howo;
+        const int nimg = fdiv(p, a.div_howo);
         const int rem = p - nimg * howo;
-        const int oy = rem / a.wo;
+        const int oy = fdiv(rem, a.div_wo);
         const int ox = rem - oy * a.wo;
         px_ok[i] = true;
         px_iy0[i] = oy * a.stride - a.pad;
@@ -298,9 +298,26 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void conv_mfma(ConvLaunch a) {
     }
   }
 
-  // Issue the loads of stage st into ring slot st % D. Chunk c covers K64
-  // step kk = st*SK + c / (CA1 + CB1) of the stage; within the step the
-  // first CA1 chunks are weights (row block, K32 half), the rest codes.
+  // Filter tap (r, s) and channel block g of K64 step kk, kept incrementally:
+  // kpos is the position of the first step of the next stage to issue.
+  struct KPos {
+    int g, s, r;
+  };
+  auto adv1 = [&](KPos& q) {
+    q.g += 1;
+    const bool wg = q.g == G;
+    q.g = wg ? 0 : q.g;
+    q.s += wg ? 1 : 0;
+    const bool ws = q.s == a.kw;
+    q.s = ws ? 0 : q.s;
+    q.r += ws ? 1 : 0;
+  };
+  KPos kpos{0, 0, 0};
+
+  // Issue the loads of stage st into ring slot st % D (stages are issued in
+  // order). Chunk c covers K64 step kk = st*SK + c / (CA1 + CB1) of the
+  // stage; within the step the first CA1 chunks are weights (row block, K32
+  // half), the rest codes.
   auto issue = [&](int st) {
     const uint32_t slot = lds0 + (uint32_t)((st % D) * STAGE);
 #pragma unroll
@@ -316,10 +333,9 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void conv_mfma(ConvLaunch a) {
         const int64_t off = ok ? ((int64_t)(rbw + rb) * nk32 + 2 * kk + t) * 1024 : a.wzero;
         dma16(wbase + off, dst);
       } else {
-        const int tap = kk / G;
-        const int g = kk - tap * G;
-        const int r = tap / a.kw;
-        const int s = tap - r * a.kw;
+        KPos q = kpos;
+        for (int u = 0; u < s_; ++u) adv1(q);
+        const int g = q.g, r = q.r, s = q.s;
         const int iy = px_iy0[i] + r;
         const int ix = px_ix0[i] + s;
         const bool ok = kk < nk && px_ok[i] && (unsigned)iy < (unsigned)a.h &&
@@ -329,6 +345,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void conv_mfma(ConvLaunch a) {
         dma16(src, dst);
       }
     }
+#pragma unroll
+    for (int u = 0; u < SK; ++u) adv1(kpos);
   };
 
   v16i acc[FM][FN];
@@ -424,19 +442,18 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void conv_mfma(ConvLaunch a) {
   if (kg == 0) {
     const bool fast = (a.cout & 31) == 0 && (a.out_mode == 0 || a.rec == 4);
     if (fast) {
-      if (a.acc_dump) {
-        ConvLaunch d = a;
-        d.y = a.acc_dump;
-        epilogue32<kE32I32, FM, FN>(d, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow);
-      }
+      int32_t* y32 = reinterpret_cast<int32_t*>(a.y);
+      if (a.acc_dump)
+        epilogue32<kE32I32, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow,
+                                    a.acc_dump);
       if (a.out_mode == 0)
-        epilogue32<kE32I32, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow);
+        epilogue32<kE32I32, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow, y32);
       else if (a.join_kind == IFQ_JOIN_IDENTITY)
-        epilogue32<kE32Tab4, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow);
+        epilogue32<kE32Tab4, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow, y32);
       else if (a.join_kind == IFQ_JOIN_CONV)
-        epilogue32<kE32Conv, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow);
+        epilogue32<kE32Conv, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow, y32);
       else
-        epilogue32<kE32Thr4, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow);
+        epilogue32<kE32Thr4, FM, FN>(a, lds, acc, wm, wn, h, l32, co0, p0, bn, otile, orow, y32);
     } else {
       epilogue_lane<FM * 4, FN>(
           a, lds, [&](int g, int fn, int i) { return acc[g >> 2][fn][4 * (g & 3) + i]; },
@@ -459,21 +476,26 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void conv_mfma(ConvLaunch a) {
 // ---------------------------------------------------------------------------
 struct Variant {
   int wm, wn, wk, fm, fn;
-  double eff;        // relative MFMA efficiency of the wave tile (measured)
+  double c0_us;      // fixed cost of one round of workgroups (measured)
+  double eff;        // MFMA efficiency of the main loop (measured)
   const char* name;
 };
 
-// Index order must match the switch in launch_conv_mfma.
+// Index order must match the switch in launch_conv_mfma. The two constants
+// of each variant are fitted to kernel times on the ResNet-18 layer shapes
+// (batch 64); the ones of the 64 x 256 tile are a conservative guess.
 const Variant kVariants[] = {
-    {2, 4, 1, 2, 4, 0.89, "conv_mfma<2, 4, 1, 2, 4, 1, 6>"},   // 128 x 512
-    {2, 4, 1, 2, 2, 0.83, "conv_mfma<2, 4, 1, 2, 2, 2, 4>"},   // 128 x 256
-    {1, 8, 1, 2, 2, 0.83, "conv_mfma<1, 8, 1, 2, 2, 2, 4>"},   //  64 x 512
-    {2, 4, 1, 1, 2, 0.70, "conv_mfma<2, 4, 1, 1, 2, 2, 6>"},   //  64 x 256
-    {2, 2, 2, 2, 2, 0.80, "conv_mfma<2, 2, 2, 2, 2, 2, 3>"},   // 128 x 128, K split 2
-    {2, 1, 4, 1, 4, 0.75, "conv_mfma<2, 1, 4, 1, 4, 1, 6>"},   //  64 x 128, K split 4
+    {2, 4, 1, 2, 4, 9.0, 0.45, "conv_mfma<2, 4, 1, 2, 4, 1, 6>"},    // 128 x 512
+    {2, 4, 1, 2, 2, 8.3, 0.443, "conv_mfma<2, 4, 1, 2, 2, 2, 4>"},   // 128 x 256
+    {1, 8, 1, 2, 2, 7.7, 0.415, "conv_mfma<1, 8, 1, 2, 2, 2, 4>"},   //  64 x 512
+    {2, 4, 1, 1, 2, 9.0, 0.30, "conv_mfma<2, 4, 1, 1, 2, 2, 6>"},    //  64 x 256
+    {2, 2, 2, 2, 2, 9.5, 0.309, "conv_mfma<2, 2, 2, 2, 2, 2, 3>"},   // 128 x 128, K split 2
+    {2, 1, 4, 1, 4, 6.7, 0.19, "conv_mfma<2, 1, 4, 1, 4, 1, 6>"},    //  64 x 128, K split 4
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 constexpr int kNumCUs = 256;
+// dense int8 MFMA ops per microsecond of one CU (2.4 GHz x 8192 per clock)
+constexpr double kCuOpsPerUs = 2.4e3 * 8192;
 
 struct Plan {
   int variant;
@@ -482,12 +504,12 @@ struct Plan {
 };
 
 // For each variant take the fewest rounds of one workgroup per CU that fit
-// the layer, spread the pixels evenly over the workgroups of those rounds
-// (in multiples of 32), and score useful MACs over issued MACs times the
-// variant's measured efficiency.
+// the layer and spread the pixels evenly over the workgroups of those rounds
+// (in multiples of 32). The predicted time is rounds x (fixed cost + the
+// tile's MFMA work at the variant's loop efficiency); the fastest wins.
 Plan plan_mfma(const ConvLaunch& a) {
   Plan best{0, 0, 0};
-  double best_score = -1.0;
+  double best_t = 1e30;
   for (int v = 0; v < kNumVariants; ++v) {
     const Variant& V = kVariants[v];
     const int bm = 32 * V.fm * V.wm;
@@ -501,10 +523,11 @@ Plan plan_mfma(const ConvLaunch& a) {
     bn = (bn + 31) / 32 * 32;
     if (bn > bnmax) bn = bnmax;
     const int64_t blocks = nco * ((a.m + bn - 1) / bn);
-    const double issued = (double)((blocks + kNumCUs - 1) / kNumCUs) * kNumCUs * bm * bnmax;
-    const double score = (double)a.m * a.cout / issued * V.eff;
-    if (score > best_score + 1e-9) {
-      best_score = score;
+    const double tile_ops = 2.0 * bm * bnmax * (double)a.kpad;
+    const double t = (double)((blocks + kNumCUs - 1) / kNumCUs) *
+                     (V.c0_us + tile_ops / (kCuOpsPerUs * V.eff));
+    if (t < best_t - 1e-9) {
+      best_t = t;
       best = Plan{v, (int)bn, (int)((a.m + bn - 1) / bn)};
     }
   }

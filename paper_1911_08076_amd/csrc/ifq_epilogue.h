@@ -22,17 +22,27 @@ namespace {
 // most (identity join tables of 4-bit codes: bm * 4 shortcut levels * 16).
 __host__ __device__ constexpr int epilogue_param_bytes(int bm) { return bm * 4 * 16 * 4; }
 
+// A conv join's parameters in LDS: the quantizer thresholds (16 doubles),
+// then {p, q, cc} per channel. Kernel-argument arrays are never indexed with
+// a runtime index (that would move the whole argument block to scratch).
+constexpr int kJoinCoefOff = 16 * 8;
+
 // Copies the per-channel epilogue parameters of output channels
 // [co0, co0 + bm) into LDS once per workgroup: threshold records
-// (bm * rec int32), identity join tables (bm * 4 * rec int32) or conv join
-// coefficients (bm * 3 doubles). The caller brackets it with barriers.
+// (bm * rec int32), identity join tables (bm * 4 * rec int32) or, for a
+// conv join, the quantizer thresholds and bm * 3 coefficients. The caller
+// brackets it with barriers.
 __device__ __forceinline__ void stage_epilogue(const ConvLaunch& a, uint8_t* lds,
                                                int co0, int bm) {
   if (a.out_mode == 0) return;
   const int tid = threadIdx.x;
   const int nch = a.cout - co0 < bm ? a.cout - co0 : bm;
   if (a.join_kind == IFQ_JOIN_CONV) {
-    double* dst = reinterpret_cast<double*>(lds);
+    double* qt = reinterpret_cast<double*>(lds);
+#pragma unroll
+    for (int q = 0; q < IFQ_MAX_THRESHOLDS; ++q)
+      if (tid == q) qt[q] = a.qthr[q];
+    double* dst = reinterpret_cast<double*>(lds + kJoinCoefOff);
     const double* src = a.coef + (int64_t)co0 * 3;
     for (int i = tid; i < bm * 3; i += blockDim.x) dst[i] = i < nch * 3 ? src[i] : 0.0;
     return;
@@ -44,10 +54,20 @@ __device__ __forceinline__ void stage_epilogue(const ConvLaunch& a, uint8_t* lds
   for (int i = tid; i < bm * per; i += blockDim.x) dst[i] = i < nch * per ? src[i] : 0;
 }
 
+// s * v for a record sign s in {+1, -1}, without a multiply
+__device__ __forceinline__ int sgn(int v, int s) {
+  const int m = s >> 31;
+  return (v ^ m) - m;
+}
+
+__device__ __forceinline__ int fdiv(int n, FastDiv d) {
+  return (int)((__umulhi((uint32_t)n, d.mul) + (uint32_t)n) >> d.shift);
+}
+
 // Byte offset of channel co of output pixel p in a BLOCK64 code tensor of
-// c channels over n images of howo pixels.
-__device__ __forceinline__ int64_t block64_byte(int p, int co, int howo, int c) {
-  const int nimg = p / howo;
+// c channels over n images of howo pixels (dh divides by howo).
+__device__ __forceinline__ int64_t block64_byte(int p, int co, int howo, FastDiv dh, int c) {
+  const int nimg = fdiv(p, dh);
   const int64_t cell = ((int64_t)nimg * (c >> 6) + (co >> 6)) * howo + (p - nimg * howo);
   return cell * 16 + ((co & 63) >> 2);
 }
@@ -58,7 +78,8 @@ __device__ __forceinline__ uint32_t shortcut_codes(const ConvLaunch& a, int p, i
   const uint8_t* sc8 = reinterpret_cast<const uint8_t*>(a.shortcut);
   const int64_t e = (int64_t)p * a.cout + co;
   if (a.sc_layout == IFQ_LAYOUT_U2_NHWC_PACKED) return sc8[e >> 2];
-  if (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64) return sc8[block64_byte(p, co, a.ho * a.wo, a.cout)];
+  if (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64)
+    return sc8[block64_byte(p, co, a.ho * a.wo, a.div_howo, a.cout)];
   uint32_t b = 0;  // byte per code
   if ((a.cout & 3) == 0) {
     const uint32_t w4 = *reinterpret_cast<const uint32_t*>(sc8 + e);
@@ -116,7 +137,7 @@ __device__ __forceinline__ void epilogue_mode(const ConvLaunch& a,
       for (int i = 0; i < 4; ++i) tr[i] = *reinterpret_cast<const int4*>(prm + (lc + i) * 4);
     }
     if constexpr (MODE == kEpiJoinConv) {
-      const double* c = reinterpret_cast<const double*>(lds) + 3 * lc;
+      const double* c = reinterpret_cast<const double*>(lds + kJoinCoefOff) + 3 * lc;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         cf[i][0] = c[3 * i];
@@ -147,14 +168,14 @@ __device__ __forceinline__ void epilogue_mode(const ConvLaunch& a,
       if constexpr (MODE == kEpiThr4) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int sv = tr[i].x * v[i];
+          const int sv = sgn(v[i], tr[i].x);
           code[i] = (sv > tr[i].y) + (sv > tr[i].z) + (sv > tr[i].w);
         }
       } else if constexpr (MODE == kEpiThr) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int32_t* t = prm + (lc + i) * a.rec;
-          const int sv = t[0] * v[i];
+          const int sv = sgn(v[i], t[0]);
           int c = 0;
           for (int q = 1; q <= a.nq; ++q) c += sv > t[q];
           code[i] = c;
@@ -166,11 +187,11 @@ __device__ __forceinline__ void epilogue_mode(const ConvLaunch& a,
           const int x = (xs >> (2 * i)) & 3;
           if constexpr (MODE == kEpiTab4) {
             const int4 t = *reinterpret_cast<const int4*>(prm + ((lc + i) * 4 + x) * 4);
-            const int sv = t.x * v[i];
+            const int sv = sgn(v[i], t.x);
             code[i] = (sv > t.y) + (sv > t.z) + (sv > t.w);
           } else {
             const int32_t* t = prm + ((lc + i) * 4 + x) * a.rec;
-            const int sv = t[0] * v[i];
+            const int sv = sgn(v[i], t[0]);
             int c = 0;
             for (int q = 1; q <= a.nq; ++q) c += sv > t[q];
             code[i] = c;
@@ -188,8 +209,9 @@ __device__ __forceinline__ void epilogue_mode(const ConvLaunch& a,
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const double z = fma(cf[i][0], (double)v[i], fma(cf[i][1], (double)d[i], cf[i][2]));
+          const double* qt = reinterpret_cast<const double*>(lds);
           int c = 0;
-          for (int q = 0; q < a.nq; ++q) c += z > a.qthr[q];
+          for (int q = 0; q < a.nq; ++q) c += z > qt[q];
           code[i] = c;
         }
       }
@@ -273,7 +295,7 @@ __device__ __forceinline__ void copy_out_tile(const ConvLaunch& a, const uint8_t
       for (int u = tid; u < npx * ng; u += blockDim.x) {
         const int pl = u / ng, gg = u - pl * ng;
         const int p = p0 + pl;
-        const int nimg = p / howo;
+        const int nimg = fdiv(p, a.div_howo);
         const int64_t cell =
             ((int64_t)nimg * G + (co0 >> 6) + gg) * howo + (p - nimg * howo);
         *reinterpret_cast<uint4*>(y8 + cell * 16) =
@@ -282,7 +304,7 @@ __device__ __forceinline__ void copy_out_tile(const ConvLaunch& a, const uint8_t
     } else {
       for (int u = tid; u < npx; u += blockDim.x) {
         const int p = p0 + u;
-        const int nimg = p / howo;
+        const int nimg = fdiv(p, a.div_howo);
         const int64_t cell = ((int64_t)nimg * G + (co0 >> 6)) * howo + (p - nimg * howo);
         *reinterpret_cast<uint2*>(y8 + cell * 16 + ((co0 & 63) >> 2)) =
             *reinterpret_cast<const uint2*>(otile + u * orow);

@@ -37,6 +37,22 @@ constexpr int kMfmaRows = 32;
 
 inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
+// Division of a non-negative int32 n < 2^31 by a fixed divisor d >= 1 as
+// (umulhi(n, mul) + n) >> shift, with shift = ceil(log2 d) and
+// mul = floor(2^32 * (2^shift - d) / d) + 1 (division by invariant integers,
+// Granlund and Montgomery); exact for every such n.
+struct FastDiv {
+  uint32_t mul;
+  uint32_t shift;
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  uint32_t l = 0;
+  while ((1ull << l) < d) ++l;
+  const uint64_t m = ((1ull << 32) * ((1ull << l) - d)) / d + 1;
+  return FastDiv{(uint32_t)m, l};
+}
+
 struct WeightGeom {
   int64_t k;         // kh*kw*c_in
   int64_t kpad;      // k rounded up to kKStep
@@ -89,6 +105,8 @@ struct ConvLaunch {
   int32_t out_mode;    // 0 int32 sums, 1 codes byte per code, 2 codes 2-bit packed
   int32_t bn;          // pixels per workgroup (set by the launcher)
   int64_t wzero;       // byte offset of the weight blob's zero block
+  FastDiv div_howo;    // division by ho*wo (output pixel -> image)
+  FastDiv div_wo;      // division by wo (pixel in image -> row)
 };
 
 hipError_t launch_conv(const ConvLaunch& a, hipStream_t stream);
