@@ -15,7 +15,8 @@ LIB = os.path.join(HERE, "libifq.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["ifq_api.cpp", "ifq_conv.hip", "ifq_conv_mfma.hip", "ifq_pool.hip"]
+SOURCES = ["ifq_api.cpp", "ifq_conv.hip", "ifq_conv_mfma.hip", "ifq_conv_halo.hip",
+           "ifq_pool.hip"]
 
 
 def build(verbose=False):

@@ -354,9 +354,10 @@ IFQ_API ifq_status ifq_pack_weights(const ifq_conv_desc* d,
           const int64_t tap = r * d->kw + s;
           int64_t pos;
           if (mfma) {
-            // K64 step kk = tap*G + c/64; channel c' = c%64 = 32h + 16t + 4i + q
-            // sits in K32 step 2*kk + t, lane 32h + co%32, byte 4q + i
-            const int64_t kk = tap * groups + c / 64, cp = c % 64;
+            // K64 step kk = (c/64)*T + tap (T = kh*kw taps); channel
+            // c' = c%64 = 32h + 16t + 4i + q sits in K32 step 2*kk + t,
+            // lane 32h + co%32, byte 4q + i
+            const int64_t kk = (c / 64) * (d->kh * d->kw) + tap, cp = c % 64;
             const int64_t h = cp / 32, t = (cp % 32) / 16, i = (cp % 16) / 4, q = cp % 4;
             const int64_t k32 = 2 * kk + t;
             const int64_t lane = 32 * h + co % 32;

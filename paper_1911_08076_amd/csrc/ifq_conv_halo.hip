@@ -1,0 +1,491 @@
+// Fast path of the integrated fixed-point quantized convolution for 3x3
+// filters (stride 1 or 2, zero padding 1) on 2-bit codes in the BLOCK64
+// layout, c_in a multiple of 64, on gfx950 (MI355X).
+//
+// The integer part of Eq. (1), a = W_b (x) X_q, is the implicit GEMM
+// D[co][pixel] = sum_k W[co][k] * X[pixel][k] on v_mfma_i32_32x32x32_i8, as in
+// ifq_conv_mfma.hip; what differs is how the operands reach the MFMA:
+//
+//  - Codes: a workgroup's output pixels are a run of consecutive (n, oy, ox)
+//    positions. Per image the input rows they touch (plus the filter halo)
+//    are one contiguous span of 16-byte cells per channel block g in the
+//    BLOCK64 layout, so the whole input window of the tile for block g is
+//    brought into LDS with a few 1 KB LDS-DMA chunks, once per g. The nine
+//    filter taps of that block then read it at fixed per-lane LDS addresses
+//    computed once per workgroup (out-of-image taps point at a zero cell), so
+//    the main loop spends no VALU on code addressing or bounds.
+//  - Weights stream through a ring of LDS stages, one K64 step per stage and
+//    wave group, with a wave-uniform SGPR base (no per-lane address math).
+//
+// K order: K64 step kk = g*9 + tap (channel block outermost, the weight blob's
+// order). The WK wave groups take the channel blocks g = gi*WK + kg, all at
+// the same tap, so stage st = 9*gi + tap covers WK K64 steps. The window of
+// block gi+1 is loaded into the second of two buffers per group while gi is
+// computed: its chunks ride along with the stage loads issued in the first
+// 11 - D iterations of gi, after the barrier that ends the use of that
+// buffer's previous contents, and before the loads of the first stage of
+// gi+1 (loads complete in issue order, so that stage's wait covers them).
+// Every wave issues exactly WK + 1 loads per stage (padding with dummy loads
+// into a scratch LDS area), which keeps the explicit vmcnt waits exact.
+//
+// Each of the 8 waves owns a 128-channel x 32-pixel tile (four 32x32
+// accumulators): every unpacked code fragment feeds four MFMAs. The WK
+// groups' sums are added through LDS; the fused epilogue of ifq_epilogue.h /
+// ifq_mfma_common.h produces codes, joins or int32 sums.
+#include <hip/hip_runtime.h>
+
+#include "ifq_epilogue.h"
+#include "ifq_internal.h"
+#include "ifq_mfma_common.h"
+
+namespace ifq {
+namespace {
+
+constexpr int kHaloNW = 8;     // waves per workgroup
+constexpr int kHaloFM = 4;     // 32-row blocks per wave
+constexpr int kHaloBM = 128;   // output channels per workgroup
+constexpr int kTaps = 9;
+
+// Cells of one halo buffer for WK wave groups (2 buffers per group).
+__host__ __device__ constexpr int halo_cap_cells(int wk) {
+  return wk == 1 ? 1280 : wk == 2 ? 512 : 192;
+}
+
+__host__ __device__ constexpr int round64(int v) { return (v + 63) & ~63; }
+
+template <int WN, int WK, int D>
+__global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
+  static_assert(WN * WK == kHaloNW, "8 waves");
+  constexpr int FM = kHaloFM, BM = kHaloBM, BN = 32 * WN;
+  constexpr int A_STEP = BM * 64;                 // one K64 step of weights
+  constexpr int STAGE = WK * A_STEP;
+  constexpr int CPW = WK + 1;                     // loads per wave per stage
+  static_assert((D - 3) * CPW <= 63, "vmcnt range");
+  static_assert(D >= 3 && D <= 10, "halo window");
+  constexpr int HCAP = halo_cap_cells(WK);
+  constexpr int HSTRIDE = HCAP * 16 + 16;         // buffer + its zero cell
+  constexpr int RING = D * STAGE;
+  constexpr int HALO0 = RING;
+  constexpr int DUMMY = HALO0 + 2 * WK * HSTRIDE;  // 1 KB sink of dummy loads
+  constexpr int LDS_MAIN = DUMMY + 1024;
+  constexpr int EPI_BYTES = epilogue_param_bytes(BM);
+  constexpr int OUT_BYTES = BN * BM;
+  constexpr int RED_BYTES = WK > 1 ? kHaloNW * FM * 4096 : 0;  // 32x32 partial blocks
+  constexpr int L1 = LDS_MAIN > RED_BYTES ? LDS_MAIN : RED_BYTES;
+  constexpr int LDS_BYTES = L1 > EPI_BYTES + OUT_BYTES ? L1 : EPI_BYTES + OUT_BYTES;
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS_BYTES];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kg = wave / WN;
+  const int wn = wave - kg * WN;
+  const int h = lane >> 5;
+  const int l32 = lane & 31;
+  const int bn = a.bn;
+  const int p0 = blockIdx.x * bn;
+  const int co0 = blockIdx.y * BM;
+  const int G = a.cin >> 6;
+  const int nG = G / WK;
+  const int nst = kTaps * nG;
+  const int H = a.h, W = a.w, Wo = a.wo, st = a.stride;
+  const int howo = a.ho * a.wo;
+  const int HW = H * W;
+  const uint32_t lds0 = lds_addr(lds);
+
+  // zero cells after every halo buffer
+  if (tid < 2 * WK)
+    *reinterpret_cast<uint4*>(lds + HALO0 + tid * HSTRIDE + HCAP * 16) = uint4{0, 0, 0, 0};
+
+  // ---- the tile's images (segments) and their input row spans ----------
+  const int pend = (p0 + bn < a.m ? p0 + bn : a.m) - 1;
+  const int n_first = fdiv(p0, a.div_howo);
+  const int n_last = fdiv(pend, a.div_howo);
+  const int nseg = n_last - n_first + 1;
+  const int oy_first = fdiv(p0 - n_first * howo, a.div_wo);
+  const int oy_last = fdiv(pend - n_last * howo, a.div_wo);
+  auto seg_rows = [&](int i, int& iya) {
+    const int oya = i == 0 ? oy_first : 0;
+    const int oyb = i == nseg - 1 ? oy_last : a.ho - 1;
+    iya = oya * st - 1;
+    iya = iya < 0 ? 0 : iya;
+    int iyb = oyb * st + 1;
+    iyb = iyb > H - 1 ? H - 1 : iyb;
+    return iyb - iya + 1;
+  };
+
+  // ---- per-lane LDS offsets of the nine taps (relative to buffer 0 of the
+  // lane's group); a tap outside the image reads the buffer's zero cell ----
+  int boff[kTaps];
+  {
+    const int pl = wn * 32 + l32;
+    const int p = p0 + pl;
+    const bool pok = pl < bn && p < a.m;
+    int my_off = 0, my_iya = 0, oy = 0, ox = 0;
+    if (pok) {
+      const int n = fdiv(p, a.div_howo);
+      const int rem = p - n * howo;
+      oy = fdiv(rem, a.div_wo);
+      ox = rem - oy * Wo;
+      int off = 0;
+      for (int i = 0; i < nseg; ++i) {
+        int iya;
+        const int rows = seg_rows(i, iya);
+        if (i == n - n_first) {
+          my_off = off;
+          my_iya = iya;
+        }
+        off += round64(rows * W);
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 3; ++r)
+#pragma unroll
+      for (int s = 0; s < 3; ++s) {
+        const int iy = oy * st - 1 + r;
+        const int ix = ox * st - 1 + s;
+        const bool ok = pok && (unsigned)iy < (unsigned)H && (unsigned)ix < (unsigned)W;
+        boff[r * 3 + s] = (ok ? (my_off + (iy - my_iya) * W + ix) * 16 : HCAP * 16) + 8 * h;
+      }
+  }
+
+  // ---- halo chunks: chunk j of a block's window is 64 cells of one image's
+  // span; q = kg'*C_h + j enumerates the WK groups' chunks ----------------
+  int C_h = 0;
+  for (int i = 0; i < nseg; ++i) {
+    int iya;
+    C_h += round64(seg_rows(i, iya) * W) >> 6;
+  }
+  const int nq = WK * C_h;
+  // source cell (without the channel-block term; -1: zero) and LDS
+  // destination (relative to buffer 0 of group 0) of chunk q for this lane
+  auto chunk = [&](int q, int& src_cell, int& dst) {
+    const int kq = q / C_h;
+    int j = q - kq * C_h;
+    int off = 0;
+    src_cell = -1;
+    dst = kq * 2 * HSTRIDE;
+    for (int i = 0; i < nseg; ++i) {
+      int iya;
+      const int cells = seg_rows(i, iya) * W;
+      const int nch = round64(cells) >> 6;
+      if (j >= 0 && j < nch) {
+        const int c = j * 64 + lane;
+        if (c < cells) src_cell = ((n_first + i) * G + kq) * HW + iya * W + c;
+        dst += (off + j * 64) * 16;
+      }
+      j -= nch;
+      off += round64(cells);
+    }
+  };
+  const uint8_t* zero_src = reinterpret_cast<const uint8_t*>(&g_zero_cell);
+  auto issue_halo = [&](int gi, int src_cell, int dst) {
+    // block g = gi*WK + kq: the chunk's group term kq is already in src_cell
+    const uint8_t* src =
+        src_cell >= 0 ? a.x + ((int64_t)src_cell + (int64_t)gi * WK * HW) * 16 : zero_src;
+    dma16(src, lds0 + HALO0 + (uint32_t)((gi & 1) * HSTRIDE + dst));
+  };
+  auto issue_dummy = [&]() { dma16(zero_src, lds0 + DUMMY); };
+
+  // chunks this wave adds to the stage loads of the first NR iterations of a
+  // block (see the loop below for why NR = 11 - D)
+  constexpr int NR = 11 - D < kTaps ? 11 - D : kTaps;
+  int hs_src[NR], hs_dst[NR];
+  bool hs_real[NR];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    const int q = r * kHaloNW + wave;
+    hs_real[r] = q < nq;
+    hs_src[r] = -1;
+    hs_dst[r] = 0;
+    if (hs_real[r]) chunk(q, hs_src[r], hs_dst[r]);
+  }
+
+  // ---- weights: wave w loads row block w/2, K32 half w%2 of each group's
+  // K64 step: 1 KB at ((rbw + rb) * nk32 + 2*kk + t) * 1024 ----------------
+  const int rb_w = wave >> 1, t_w = wave & 1;
+  const int nrb = a.cout_pad >> 5;
+  const int rbw = co0 >> 5;
+  const bool wrow_ok = rbw + rb_w < nrb;
+  const uint8_t* wbase = reinterpret_cast<const uint8_t*>(a.wgt);
+  const int nk32 = 2 * a.nk;
+  const uint32_t voff = (uint32_t)lane * 16;
+  auto issue_a = [&](int stg, int tap) {
+    const int gi = stg / kTaps;
+    const uint32_t slot = lds0 + (uint32_t)((stg % D) * STAGE);
+#pragma unroll
+    for (int i = 0; i < WK; ++i) {
+      const int kk = (gi * WK + i) * kTaps + tap;
+      const int64_t off =
+          wrow_ok ? ((int64_t)(rbw + rb_w) * nk32 + 2 * kk + t_w) * 1024 : a.wzero;
+      dma16s(wbase + off, voff, slot + (uint32_t)(i * A_STEP + (rb_w * 2 + t_w) * 1024));
+    }
+  };
+
+  // ---- prologue: block 0's windows, then stages 0 .. D-3 ------------------
+  for (int q = wave; q < nq; q += kHaloNW) {
+    int sc, dst;
+    chunk(q, sc, dst);
+    issue_halo(0, sc, dst);
+  }
+  const int pre = nst < D - 2 ? nst : D - 2;
+  for (int s_ = 0; s_ < pre; ++s_) {
+    issue_a(s_, s_ % kTaps);
+    issue_dummy();
+  }
+
+  v16i acc[FM];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) acc[fm] = v16i{0};
+
+  // Fragments of one stage in registers: A for both K32 halves and the raw
+  // 2-bit B words, unpacked only right before the MFMAs that use them (one
+  // iteration later), so no instruction waits on these reads in the
+  // iteration that issues them.
+  struct Frag {
+    v4i af[2][FM];
+    v2i braw;
+  };
+  auto read_frags = [&](int s_, int tap, Frag& F) {
+    const uint8_t* as = lds + (s_ % D) * STAGE + kg * A_STEP;
+    const int gi = s_ / kTaps;
+    F.braw = *reinterpret_cast<const v2i*>(
+        lds + HALO0 + kg * 2 * HSTRIDE + (gi & 1) * HSTRIDE + boff[tap]);
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+        F.af[t][fm] = *reinterpret_cast<const v4i*>(as + (fm * 2 + t) * 1024 + lane * 16);
+  };
+  auto mfmas = [&](const Frag& F) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const v4i bf = unpack2((uint32_t)F.braw[t]);
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+        acc[fm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(F.af[t][fm], bf, acc[fm], 0, 0, 0);
+    }
+  };
+
+  // Iteration s_: wait until stage s_ has landed, barrier, issue stage
+  // s_ + D - 2 into the slot of stage s_ - 2 (read in iteration s_ - 2 and
+  // consumed by the MFMAs of iteration s_ - 1, both before this barrier),
+  // read stage s_'s fragments into registers, then run the MFMAs of stage
+  // s_ - 1 while those reads are in flight. The window of block gi + 1 rides
+  // along with the loads issued in iterations 9*gi .. 9*gi + NR - 1: after
+  // the barrier of iteration 9*gi, which ends the reads of its buffer's
+  // previous block gi - 1, and before the loads of stage 9*(gi + 1), issued in
+  // iteration 9*gi + 11 - D, whose wait therefore covers them.
+  Frag fa, fb;   // even taps read into fa, odd taps into fb
+  for (int gi = 0; gi < nG; ++gi) {
+#pragma unroll
+    for (int tap = 0; tap < kTaps; ++tap) {
+      const int s_ = gi * kTaps + tap;
+      const int after = nst - 1 - s_;
+      wait_ahead<D - 3, CPW>(after < D - 3 ? after : D - 3);
+      // A bare barrier: no LDS fence is needed here (the slot reused below
+      // was read by fragments the previous iteration's MFMAs consumed, and
+      // the stage's LDS-DMA data is complete by the vmcnt wait above), and
+      // a fence would stall until this iteration's own fragment reads land.
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+      if (s_ + D - 2 < nst) {
+        issue_a(s_ + D - 2, (tap + D - 2) % kTaps);
+        if (tap < NR && gi + 1 < nG && hs_real[tap < NR ? tap : 0])
+          issue_halo(gi + 1, hs_src[tap < NR ? tap : 0], hs_dst[tap < NR ? tap : 0]);
+        else
+          issue_dummy();
+      }
+      if ((tap & 1) == 0) {
+        // tap 0 follows tap 8 of the previous block, which was read into fa
+        // and moved to fb at the end of that block
+        read_frags(s_, tap, fa);
+        if (s_ > 0) mfmas(fb);
+      } else {
+        read_frags(s_, tap, fb);
+        mfmas(fa);
+      }
+    }
+    // tap 8 (odd count of taps): its fragments move to fb
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) fb.af[t][fm] = fa.af[t][fm];
+    fb.braw = fa.braw;
+  }
+  mfmas(fb);
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  // ---- K groups: wave (kg, wn) keeps row blocks kg*OWN .. kg*OWN + OWN - 1
+  // of its pixel column; the other groups' sums of those blocks come through
+  // LDS (4 KB per 32x32 block) ------------------------------------------------
+  constexpr int OWN = FM / WK;
+  v16i own[OWN];
+  // (indices of acc stay compile-time: a runtime index would move it to
+  // scratch)
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+    if (fm / OWN == kg) own[fm % OWN] = acc[fm];
+  if constexpr (WK > 1) {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      if (fm / OWN == kg) continue;
+      uint8_t* dst = lds + ((kg * WN + wn) * FM + fm) * 4096;
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<v4i*>(dst + j * 1024 + lane * 16) =
+            v4i{acc[fm][4 * j], acc[fm][4 * j + 1], acc[fm][4 * j + 2], acc[fm][4 * j + 3]};
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k2 = 0; k2 < WK; ++k2) {
+      if (k2 == kg) continue;
+#pragma unroll
+      for (int j = 0; j < OWN; ++j) {
+        const uint8_t* src = lds + ((k2 * WN + wn) * FM + kg * OWN + j) * 4096;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const v4i v = *reinterpret_cast<const v4i*>(src + q * 1024 + lane * 16);
+          own[j][4 * q] += v.x;
+          own[j][4 * q + 1] += v.y;
+          own[j][4 * q + 2] += v.z;
+          own[j][4 * q + 3] += v.w;
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // 2-bit thresholds of a 3x3 layer fit packed 16-bit compares when
+  // 3 * 9 * c_in <= 32766 (sums and thresholds below 2^15 in magnitude)
+  const bool pk = a.out_mode == 2 && a.join_kind == IFQ_JOIN_NONE && a.rec == 4 &&
+                  (a.cout & 31) == 0 && 27 * a.cin <= 32766;
+  if (pk)
+    stage_thr_pk(a, lds, co0, BM);
+  else
+    stage_epilogue(a, lds, co0, BM);
+  __syncthreads();
+  const int orow = a.out_mode == 2 ? BM / 4 : BM;
+  uint8_t* otile = lds + EPI_BYTES;
+  const int pl = wn * 32 + l32;
+  {
+    v16i own2[OWN][1];
+#pragma unroll
+    for (int j = 0; j < OWN; ++j) own2[j][0] = own[j];
+    const bool fast = (a.cout & 31) == 0 && (a.out_mode == 0 || a.rec == 4);
+    int32_t* y32 = reinterpret_cast<int32_t*>(a.y);
+    if (a.acc_dump)
+      epilogue32<kE32I32, OWN, 1>(a, lds, own2, kg, wn, h, l32, co0, p0, bn, otile, orow,
+                                  a.acc_dump);
+    if (pk) {
+      epilogue_thr_pk<OWN>(a, lds, own, kg, h, co0, pl, otile, orow);
+    } else if (fast) {
+      if (a.out_mode == 0)
+        epilogue32<kE32I32, OWN, 1>(a, lds, own2, kg, wn, h, l32, co0, p0, bn, otile, orow, y32);
+      else if (a.join_kind == IFQ_JOIN_IDENTITY)
+        epilogue32<kE32Tab4, OWN, 1>(a, lds, own2, kg, wn, h, l32, co0, p0, bn, otile, orow, y32);
+      else if (a.join_kind == IFQ_JOIN_CONV)
+        epilogue32<kE32Conv, OWN, 1>(a, lds, own2, kg, wn, h, l32, co0, p0, bn, otile, orow, y32);
+      else
+        epilogue32<kE32Thr4, OWN, 1>(a, lds, own2, kg, wn, h, l32, co0, p0, bn, otile, orow, y32);
+    } else {
+      epilogue_lane<OWN * 4, 1>(
+          a, lds, [&](int g, int fn, int i) { return own2[g >> 2][fn][4 * (g & 3) + i]; },
+          [&](int g) { return co0 + (kg * OWN + (g >> 2)) * 32 + 8 * (g & 3) + 4 * h; }, co0,
+          p0, [&](int fn) { return (pl < bn && p0 + pl < a.m) ? pl : -1; }, otile, orow);
+    }
+  }
+  __syncthreads();
+  const int npx = a.m - p0 < bn ? a.m - p0 : bn;
+  copy_out_tile(a, otile, orow, co0, BM, p0, npx);
+}
+
+// ---------------------------------------------------------------------------
+// Variants and per-layer planning
+// ---------------------------------------------------------------------------
+struct HaloVariant {
+  int wn, wk, d;
+  double c0_us;   // fixed cost of one round of workgroups
+  double eff;     // MFMA efficiency of the main loop
+  const char* name;
+};
+
+// Index order must match the switch in launch_conv_halo.
+const HaloVariant kHaloVariants[] = {
+    {8, 1, 6, 4.0, 0.75, "conv_halo<8, 1, 6>"},   // 128 x 256
+    {4, 2, 4, 4.0, 0.75, "conv_halo<4, 2, 4>"},   // 128 x 128, K split 2
+    {2, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4>"},   // 128 x 64, K split 4
+};
+constexpr int kNumHalo = sizeof(kHaloVariants) / sizeof(kHaloVariants[0]);
+constexpr int kNumCUs = 256;
+constexpr double kCuOpsPerUs = 2.4e3 * 8192;
+
+// Upper bound of the halo cells (rounded per image to 64) one tile of bn
+// output pixels needs per channel block, over every tile of the layer.
+int64_t halo_cells_bound(const ConvLaunch& a, int64_t bn) {
+  const int64_t howo = (int64_t)a.ho * a.wo;
+  const int64_t nseg = (bn - 1) / howo + 2;              // images a tile touches
+  const int64_t rows_out = (bn - 1) / a.wo + 2;          // output rows it touches
+  int64_t rows_in = rows_out * a.stride + 3;
+  if (rows_in > a.h) rows_in = a.h;
+  return nseg * round64((int)(rows_in * a.w));
+}
+
+}  // namespace
+
+bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
+  if (!(a.in_layout == IFQ_LAYOUT_U2_BLOCK64 && a.in_bits == 2 && a.cin % 64 == 0 &&
+        a.kh == 3 && a.kw == 3 && a.pad == 1 && (a.stride == 1 || a.stride == 2)))
+    return false;
+  // 32-bit cell indices and offsets
+  if ((int64_t)a.n * a.h * a.w * (a.cin / 64) >= (int64_t)1 << 26) return false;
+  const int G = a.cin / 64;
+  double best_t = 1e30;
+  bool found = false;
+  for (int v = 0; v < kNumHalo; ++v) {
+    const HaloVariant& V = kHaloVariants[v];
+    if (G % V.wk) continue;
+    const int bnmax = 32 * V.wn;
+    const int64_t nco = (a.cout + kHaloBM - 1) / kHaloBM;
+    const int64_t nb_min = (a.m + bnmax - 1) / bnmax;
+    const int64_t rounds = (nco * nb_min + kNumCUs - 1) / kNumCUs;
+    int64_t nb = rounds * kNumCUs / nco;
+    if (nb < nb_min) nb = nb_min;
+    int64_t bn = (a.m + nb - 1) / nb;
+    bn = (bn + 31) / 32 * 32;
+    if (bn > bnmax) bn = bnmax;
+    const int64_t cells = halo_cells_bound(a, bn);
+    if (cells > halo_cap_cells(V.wk)) continue;
+    const int nr = 11 - V.d < kTaps ? 11 - V.d : kTaps;
+    if (V.wk * (cells / 64) > kHaloNW * nr) continue;
+    const int64_t blocks = nco * ((a.m + bn - 1) / bn);
+    const double tile_ops = 2.0 * kHaloBM * bnmax * (double)a.kpad;
+    const double t = (double)((blocks + kNumCUs - 1) / kNumCUs) *
+                     (V.c0_us + tile_ops / (kCuOpsPerUs * V.eff));
+    if (t < best_t) {
+      best_t = t;
+      *out = HaloPlan{v, (int)bn, (int)((a.m + bn - 1) / bn), t};
+      found = true;
+    }
+  }
+  return found;
+}
+
+const char* conv_halo_name(const HaloPlan& p) { return kHaloVariants[p.variant].name; }
+
+hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream) {
+  a.bn = p.bn;
+  const dim3 grid(p.blocks_m, (a.cout + kHaloBM - 1) / kHaloBM);
+  switch (p.variant) {
+    case 0: hipLaunchKernelGGL((conv_halo<8, 1, 6>), grid, dim3(512), 0, stream, a); break;
+    case 1: hipLaunchKernelGGL((conv_halo<4, 2, 4>), grid, dim3(512), 0, stream, a); break;
+    default: hipLaunchKernelGGL((conv_halo<2, 4, 4>), grid, dim3(512), 0, stream, a); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ifq

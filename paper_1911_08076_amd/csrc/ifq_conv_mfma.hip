@@ -7,7 +7,8 @@
 // A (rows = output channels) is the +-1 weight matrix in fragment order, B
 // (columns = output pixels) the input codes of one filter tap and 64 channels
 // per K64 step, unpacked from 2 bits to int8 in registers right before the
-// MFMA. K runs over K64 steps kk = (r*kw + s)*G + g (G = c_in/64).
+// MFMA. K runs over K64 steps kk = g*kh*kw + (r*kw + s) (G = c_in/64
+// channel blocks g, filter taps (r, s) fastest).
 //
 // A workgroup of WM x WN x WK waves computes a tile of 32*FM*WM output
 // channels x up to 32*FN*WN pixels (bn, chosen per layer on the host); the
@@ -33,187 +34,10 @@
 
 #include "ifq_epilogue.h"
 #include "ifq_internal.h"
+#include "ifq_mfma_common.h"
 
 namespace ifq {
 namespace {
-
-typedef int v2i __attribute__((ext_vector_type(2)));
-typedef int v4i __attribute__((ext_vector_type(4)));
-typedef int v16i __attribute__((ext_vector_type(16)));
-
-constexpr uint32_t kLow2 = 0x03030303u;
-
-// Sixteen zero bytes in device memory: code loads that fall outside the
-// image read them instead of branching around the load.
-__device__ uint4 g_zero_cell;
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
-}
-
-// One wave-wide LDS-DMA load: 16 bytes per lane from src to LDS dst + 16*lane.
-// M0 carries the LDS base; nothing else in these kernels uses M0.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void dma16(const void* src, uint32_t dst) {
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
-               :: "s"(dst), "v"(src) : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
-}
-
-// Waits until at most ahead*CPW of this wave's loads are outstanding
-// (0 <= ahead <= MAXA).
-template <int MAXA, int CPW>
-__device__ __forceinline__ void wait_ahead(int ahead) {
-  if constexpr (MAXA <= 0) {
-    wait_vmcnt<0>();
-  } else {
-    if (ahead >= MAXA) wait_vmcnt<MAXA * CPW>();
-    else wait_ahead<MAXA - 1, CPW>(ahead);
-  }
-}
-
-// Epilogue for the 32x32 accumulator layout when c_out % 32 == 0 and the
-// records have 4 entries (2-bit codes): every lane computes codes for all of
-// its accumulators without per-lane branches. A lane holds, per block
-// (fm, fn), output channels cb + 8b + 4h + i (b, i = 0..3) of one pixel; the
-// per-channel records of a 4-channel group are read from LDS once and used
-// for the FN pixel blocks. Codes go to the LDS output tile (rows past the
-// last pixel are never copied out); shortcut reads use a clamped pixel index.
-enum Epi32 { kE32I32 = 0, kE32Thr4 = 1, kE32Tab4 = 2, kE32Conv = 3 };
-
-template <int MODE, int FM, int FN>
-__device__ __forceinline__ void epilogue32(const ConvLaunch& a, const uint8_t* lds,
-                                           const v16i (&acc)[FM][FN], int wm, int wn,
-                                           int h, int l32, int co0, int p0, int bn,
-                                           uint8_t* otile, int orow, int32_t* y32) {
-  const int32_t* prm = reinterpret_cast<const int32_t*>(lds);
-  const bool u2 = a.out_mode == 2;
-  const int howo = a.ho * a.wo;
-  const uint8_t* sc8 = reinterpret_cast<const uint8_t*>(a.shortcut);
-  const int32_t* sc32 = reinterpret_cast<const int32_t*>(a.shortcut);
-#pragma unroll
-  for (int fm = 0; fm < FM; ++fm) {
-    const int cb = (wm * FM + fm) * 32;         // local first channel of the block
-    if (co0 + cb >= a.cout) continue;           // uniform: whole 32-channel block
-    // shortcut codes of the 32 channels of each pixel block (identity join):
-    // byte 2b + h of the 8 holds the lane's channels cb + 8b + 4h .. +3
-    uint32_t scw[FN][2];
-    if constexpr (MODE == kE32Tab4) {
-#pragma unroll
-      for (int fn = 0; fn < FN; ++fn) {
-        int p = p0 + wn * 32 * FN + fn * 32 + l32;
-        p = p < a.m ? p : a.m - 1;
-        const int co = co0 + cb;
-        if (a.sc_layout == IFQ_LAYOUT_I8_NHWC) {
-          const uint8_t* src = sc8 + (int64_t)p * a.cout + co;
-          uint32_t w[2] = {0u, 0u};
-#pragma unroll
-          for (int b = 0; b < 4; ++b) {
-            const uint32_t v = *reinterpret_cast<const uint32_t*>(src + 8 * b + 4 * h) & kLow2;
-            const uint32_t byte = v | (v >> 6) | (v >> 12) | (v >> 18);
-            w[b >> 1] |= (byte & 0xFFu) << (8 * (2 * (b & 1) + h));
-          }
-          scw[fn][0] = w[0];
-          scw[fn][1] = w[1];
-        } else {
-          int64_t off;
-          if (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64) {
-            const int nimg = fdiv(p, a.div_howo);
-            off = (((int64_t)nimg * (a.cout >> 6) + (co >> 6)) * howo + (p - nimg * howo)) * 16 +
-                  ((co & 63) >> 2);
-          } else {
-            off = ((int64_t)p * a.cout + co) >> 2;
-          }
-          const uint2 v = *reinterpret_cast<const uint2*>(sc8 + off);
-          scw[fn][0] = v.x;
-          scw[fn][1] = v.y;
-        }
-      }
-    }
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int cl = cb + 8 * b + 4 * h;        // local channel of value 4b + 0
-      int4 tr[4];
-      double cf[4][3];
-      if constexpr (MODE == kE32Thr4) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) tr[i] = *reinterpret_cast<const int4*>(prm + (cl + i) * 4);
-      }
-      if constexpr (MODE == kE32Conv) {
-        const double* c = reinterpret_cast<const double*>(lds + kJoinCoefOff) + 3 * cl;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          cf[i][0] = c[3 * i];
-          cf[i][1] = c[3 * i + 1];
-          cf[i][2] = c[3 * i + 2];
-        }
-      }
-#pragma unroll
-      for (int fn = 0; fn < FN; ++fn) {
-        const int pl = wn * 32 * FN + fn * 32 + l32;
-        int v[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) v[i] = acc[fm][fn][4 * b + i];
-        if constexpr (MODE == kE32I32) {
-          if (pl < bn && p0 + pl < a.m)
-            *reinterpret_cast<int4*>(y32 + (int64_t)(p0 + pl) * a.cout + co0 + cl) =
-                int4{v[0], v[1], v[2], v[3]};
-          continue;
-        }
-        int code[4];
-        if constexpr (MODE == kE32Thr4) {
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int sv = sgn(v[i], tr[i].x);
-            code[i] = (sv > tr[i].y) + (sv > tr[i].z) + (sv > tr[i].w);
-          }
-        } else if constexpr (MODE == kE32Tab4) {
-          const uint32_t xs = (scw[fn][b >> 1] >> (8 * (2 * (b & 1) + h))) & 0xFFu;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int x = (xs >> (2 * i)) & 3;
-            const int4 t = *reinterpret_cast<const int4*>(prm + ((cl + i) * 4 + x) * 4);
-            const int sv = sgn(v[i], t.x);
-            code[i] = (sv > t.y) + (sv > t.z) + (sv > t.w);
-          }
-        } else {
-          int p = p0 + pl;
-          p = p < a.m ? p : a.m - 1;
-          const int4 d = *reinterpret_cast<const int4*>(sc32 + (int64_t)p * a.cout + co0 + cl);
-          const int dv[4] = {d.x, d.y, d.z, d.w};
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const double z = fma(cf[i][0], (double)v[i], fma(cf[i][1], (double)dv[i], cf[i][2]));
-            const double* qt = reinterpret_cast<const double*>(lds);
-            int c = 0;
-            for (int q = 0; q < a.nq; ++q) c += z > qt[q];
-            code[i] = c;
-          }
-        }
-        if (u2) {
-          otile[pl * orow + (cl >> 2)] =
-              (uint8_t)(code[0] | (code[1] << 2) | (code[2] << 4) | (code[3] << 6));
-        } else {
-          *reinterpret_cast<uint32_t*>(otile + pl * orow + cl) =
-              (uint32_t)code[0] | ((uint32_t)code[1] << 8) | ((uint32_t)code[2] << 16) |
-              ((uint32_t)code[3] << 24);
-        }
-      }
-    }
-  }
-}
-
-// 16 two-bit codes (one 32-bit word of a cell) -> 16 int8 operand bytes.
-__device__ __forceinline__ v4i unpack2(uint32_t u) {
-  return v4i{(int)(u & kLow2), (int)((u >> 2) & kLow2), (int)((u >> 4) & kLow2),
-             (int)((u >> 6) & kLow2)};
-}
 
 template <int WM, int WN, int WK, int FM, int FN, int S, int D>
 __global__ __launch_bounds__(64 * WM * WN * WK) void conv_mfma(ConvLaunch a) {
@@ -298,19 +122,20 @@ __global__ __launch_bounds__(64 * WM * WN * WK) void conv_mfma(ConvLaunch a) {
     }
   }
 
-  // Filter tap (r, s) and channel block g of K64 step kk, kept incrementally:
-  // kpos is the position of the first step of the next stage to issue.
+  // Filter tap (r, s) and channel block g of K64 step kk, kept incrementally
+  // (taps fastest): kpos is the position of the first step of the next stage
+  // to issue.
   struct KPos {
     int g, s, r;
   };
   auto adv1 = [&](KPos& q) {
-    q.g += 1;
-    const bool wg = q.g == G;
-    q.g = wg ? 0 : q.g;
-    q.s += wg ? 1 : 0;
+    q.s += 1;
     const bool ws = q.s == a.kw;
     q.s = ws ? 0 : q.s;
     q.r += ws ? 1 : 0;
+    const bool wr = q.r == a.kh;
+    q.r = wr ? 0 : q.r;
+    q.g += wr ? 1 : 0;
   };
   KPos kpos{0, 0, 0};
 
@@ -501,6 +326,7 @@ struct Plan {
   int variant;
   int bn;        // pixels per workgroup
   int blocks_m;  // workgroups along pixels
+  double t_us;   // predicted time
 };
 
 // For each variant take the fewest rounds of one workgroup per CU that fit
@@ -508,7 +334,7 @@ struct Plan {
 // (in multiples of 32). The predicted time is rounds x (fixed cost + the
 // tile's MFMA work at the variant's loop efficiency); the fastest wins.
 Plan plan_mfma(const ConvLaunch& a) {
-  Plan best{0, 0, 0};
+  Plan best{0, 0, 0, 0.0};
   double best_t = 1e30;
   for (int v = 0; v < kNumVariants; ++v) {
     const Variant& V = kVariants[v];
@@ -528,7 +354,7 @@ Plan plan_mfma(const ConvLaunch& a) {
                      (V.c0_us + tile_ops / (kCuOpsPerUs * V.eff));
     if (t < best_t - 1e-9) {
       best_t = t;
-      best = Plan{v, (int)bn, (int)((a.m + bn - 1) / bn)};
+      best = Plan{v, (int)bn, (int)((a.m + bn - 1) / bn), t};
     }
   }
   return best;
@@ -550,10 +376,17 @@ bool mfma_eligible(const ConvLaunch& a) {
          (a.in_layout == IFQ_LAYOUT_U2_NHWC_PACKED || a.in_layout == IFQ_LAYOUT_U2_BLOCK64);
 }
 
-const char* conv_mfma_name(const ConvLaunch& a) { return kVariants[plan_mfma(a).variant].name; }
+const char* conv_mfma_name(const ConvLaunch& a) {
+  const Plan pl = plan_mfma(a);
+  HaloPlan hp;
+  if (plan_halo(a, &hp) && hp.t_us < pl.t_us) return conv_halo_name(hp);
+  return kVariants[pl.variant].name;
+}
 
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream) {
   const Plan pl = plan_mfma(a);
+  HaloPlan hp;
+  if (plan_halo(a, &hp) && hp.t_us < pl.t_us) return launch_conv_halo(a, hp, stream);
   switch (pl.variant) {
     case 0: return launch_variant<2, 4, 1, 2, 4, 1, 6>(a, pl, stream);
     case 1: return launch_variant<2, 4, 1, 2, 2, 2, 4>(a, pl, stream);

@@ -25,7 +25,8 @@ namespace ifq {
 //
 // Fast path (mfma_layout(d): 2-bit input, c_in % 64 == 0): W is in the A
 // fragment order of v_mfma_i32_32x32x32_i8. K runs over K64 steps
-// kk = (r*kw + s)*G + g, G = c_in/64, each split into two K32 steps
+// kk = g*kh*kw + (r*kw + s), G = c_in/64 channel blocks g with the filter
+// taps fastest, each split into two K32 steps
 // k32 = 2*kk + t. For each block of 32 rows rb and K32 step k32 one 1 KB
 // chunk at byte (rb*nk32 + k32)*1024 holds the 64 lanes' 16-byte fragments:
 // lane l = 32*h + r carries row 32*rb + r, and its byte 4*q + i is the weight
@@ -117,6 +118,19 @@ const char* conv_kernel_name(const ConvLaunch& a);
 // Fast path (MFMA 32x32x32 kernel): whether it takes the layer, its launch,
 // and the name of the variant it picks.
 bool mfma_eligible(const ConvLaunch& a);
+
+// 3x3 kernel with per-tile input windows in LDS (BLOCK64 input): the
+// variant, pixels per workgroup, workgroups along pixels and the predicted
+// time of the best variant that fits the layer, if any.
+struct HaloPlan {
+  int variant;
+  int bn;
+  int blocks_m;
+  double t_us;
+};
+bool plan_halo(const ConvLaunch& a, HaloPlan* out);
+hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream);
+const char* conv_halo_name(const HaloPlan& p);
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream);
 const char* conv_mfma_name(const ConvLaunch& a);
 

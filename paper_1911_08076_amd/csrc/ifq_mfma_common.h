@@ -1,0 +1,288 @@
+// Device helpers shared by the two MFMA conv kernels (included by each
+// kernel source): LDS-DMA loads with explicit vmcnt waits, the 2-bit code
+// unpack, and the fused epilogue for the 32x32 accumulator layout.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "ifq_epilogue.h"
+#include "ifq_internal.h"
+
+namespace ifq {
+namespace {
+
+typedef int v2i __attribute__((ext_vector_type(2)));
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+
+constexpr uint32_t kLow2 = 0x03030303u;
+
+// Sixteen zero bytes in device memory: code loads that fall outside the
+// image read them instead of branching around the load.
+__device__ uint4 g_zero_cell;
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
+}
+
+// One wave-wide LDS-DMA load: 16 bytes per lane from src to LDS dst + 16*lane.
+// M0 carries the LDS base; nothing else in these kernels uses M0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// dst must be wave-uniform (it is moved to SGPRs explicitly).
+__device__ __forceinline__ void dma16(const void* src, uint32_t dst) {
+  const uint32_t d = __builtin_amdgcn_readfirstlane(dst);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off"
+               :: "s"(d), "v"(src) : "memory", "m0");
+}
+
+// The same load with a wave-uniform 64-bit base in SGPRs and a per-lane
+// 32-bit byte offset: no per-lane address arithmetic.
+__device__ __forceinline__ void dma16s(const void* base, uint32_t voff, uint32_t dst) {
+  const uint32_t d = __builtin_amdgcn_readfirstlane(dst);
+  const uint64_t b = (uint64_t)(uintptr_t)base;
+  // readfirstlane yields a signed int: widen each half as unsigned, or a low
+  // half with bit 31 set would be sign-extended over the high half
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32));
+  const uint64_t bs = ((uint64_t)hi << 32) | (uint64_t)lo;
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :: "s"(d), "v"(voff), "s"(bs) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" :: "n"(N) : "memory");
+}
+
+// Waits until at most ahead*CPW of this wave's loads are outstanding
+// (0 <= ahead <= MAXA).
+template <int MAXA, int CPW>
+__device__ __forceinline__ void wait_ahead(int ahead) {
+  if constexpr (MAXA <= 0) {
+    wait_vmcnt<0>();
+  } else {
+    if (ahead >= MAXA) wait_vmcnt<MAXA * CPW>();
+    else wait_ahead<MAXA - 1, CPW>(ahead);
+  }
+}
+
+// Epilogue for the 32x32 accumulator layout when c_out % 32 == 0 and the
+// records have 4 entries (2-bit codes): every lane computes codes for all of
+// its accumulators without per-lane branches. A lane holds, per block
+// (fm, fn), output channels cb + 8b + 4h + i (b, i = 0..3) of one pixel; the
+// per-channel records of a 4-channel group are read from LDS once and used
+// for the FN pixel blocks. Codes go to the LDS output tile (rows past the
+// last pixel are never copied out); shortcut reads use a clamped pixel index.
+enum Epi32 { kE32I32 = 0, kE32Thr4 = 1, kE32Tab4 = 2, kE32Conv = 3 };
+
+template <int MODE, int FM, int FN>
+__device__ __forceinline__ void epilogue32(const ConvLaunch& a, const uint8_t* lds,
+                                           const v16i (&acc)[FM][FN], int wm, int wn,
+                                           int h, int l32, int co0, int p0, int bn,
+                                           uint8_t* otile, int orow, int32_t* y32) {
+  const int32_t* prm = reinterpret_cast<const int32_t*>(lds);
+  const bool u2 = a.out_mode == 2;
+  const int howo = a.ho * a.wo;
+  const uint8_t* sc8 = reinterpret_cast<const uint8_t*>(a.shortcut);
+  const int32_t* sc32 = reinterpret_cast<const int32_t*>(a.shortcut);
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    const int cb = (wm * FM + fm) * 32;         // local first channel of the block
+    if (co0 + cb >= a.cout) continue;           // uniform: whole 32-channel block
+    // shortcut codes of the 32 channels of each pixel block (identity join):
+    // byte 2b + h of the 8 holds the lane's channels cb + 8b + 4h .. +3
+    uint32_t scw[FN][2];
+    if constexpr (MODE == kE32Tab4) {
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        int p = p0 + wn * 32 * FN + fn * 32 + l32;
+        p = p < a.m ? p : a.m - 1;
+        const int co = co0 + cb;
+        if (a.sc_layout == IFQ_LAYOUT_I8_NHWC) {
+          const uint8_t* src = sc8 + (int64_t)p * a.cout + co;
+          uint32_t w[2] = {0u, 0u};
+#pragma unroll
+          for (int b = 0; b < 4; ++b) {
+            const uint32_t v = *reinterpret_cast<const uint32_t*>(src + 8 * b + 4 * h) & kLow2;
+            const uint32_t byte = v | (v >> 6) | (v >> 12) | (v >> 18);
+            w[b >> 1] |= (byte & 0xFFu) << (8 * (2 * (b & 1) + h));
+          }
+          scw[fn][0] = w[0];
+          scw[fn][1] = w[1];
+        } else {
+          int64_t off;
+          if (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64) {
+            const int nimg = fdiv(p, a.div_howo);
+            off = (((int64_t)nimg * (a.cout >> 6) + (co >> 6)) * howo + (p - nimg * howo)) * 16 +
+                  ((co & 63) >> 2);
+          } else {
+            off = ((int64_t)p * a.cout + co) >> 2;
+          }
+          const uint2 v = *reinterpret_cast<const uint2*>(sc8 + off);
+          scw[fn][0] = v.x;
+          scw[fn][1] = v.y;
+        }
+      }
+    }
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int cl = cb + 8 * b + 4 * h;        // local channel of value 4b + 0
+      int4 tr[4];
+      double cf[4][3];
+      if constexpr (MODE == kE32Thr4) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) tr[i] = *reinterpret_cast<const int4*>(prm + (cl + i) * 4);
+      }
+      if constexpr (MODE == kE32Conv) {
+        const double* c = reinterpret_cast<const double*>(lds + kJoinCoefOff) + 3 * cl;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          cf[i][0] = c[3 * i];
+          cf[i][1] = c[3 * i + 1];
+          cf[i][2] = c[3 * i + 2];
+        }
+      }
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        const int pl = wn * 32 * FN + fn * 32 + l32;
+        int v[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = acc[fm][fn][4 * b + i];
+        if constexpr (MODE == kE32I32) {
+          if (pl < bn && p0 + pl < a.m)
+            *reinterpret_cast<int4*>(y32 + (int64_t)(p0 + pl) * a.cout + co0 + cl) =
+                int4{v[0], v[1], v[2], v[3]};
+          continue;
+        }
+        int code[4];
+        if constexpr (MODE == kE32Thr4) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int sv = sgn(v[i], tr[i].x);
+            code[i] = (sv > tr[i].y) + (sv > tr[i].z) + (sv > tr[i].w);
+          }
+        } else if constexpr (MODE == kE32Tab4) {
+          const uint32_t xs = (scw[fn][b >> 1] >> (8 * (2 * (b & 1) + h))) & 0xFFu;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int x = (xs >> (2 * i)) & 3;
+            const int4 t = *reinterpret_cast<const int4*>(prm + ((cl + i) * 4 + x) * 4);
+            const int sv = sgn(v[i], t.x);
+            code[i] = (sv > t.y) + (sv > t.z) + (sv > t.w);
+          }
+        } else {
+          int p = p0 + pl;
+          p = p < a.m ? p : a.m - 1;
+          const int4 d = *reinterpret_cast<const int4*>(sc32 + (int64_t)p * a.cout + co0 + cl);
+          const int dv[4] = {d.x, d.y, d.z, d.w};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const double z = fma(cf[i][0], (double)v[i], fma(cf[i][1], (double)dv[i], cf[i][2]));
+            const double* qt = reinterpret_cast<const double*>(lds);
+            int c = 0;
+            for (int q = 0; q < a.nq; ++q) c += z > qt[q];
+            code[i] = c;
+          }
+        }
+        if (u2) {
+          otile[pl * orow + (cl >> 2)] =
+              (uint8_t)(code[0] | (code[1] << 2) | (code[2] << 4) | (code[3] << 6));
+        } else {
+          *reinterpret_cast<uint32_t*>(otile + pl * orow + cl) =
+              (uint32_t)code[0] | ((uint32_t)code[1] << 8) | ((uint32_t)code[2] << 16) |
+              ((uint32_t)code[3] << 24);
+        }
+      }
+    }
+  }
+}
+
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// Threshold records of 2-bit outputs laid out for packed 16-bit compares,
+// 32 bytes per group of four consecutive output channels c .. c+3:
+//   words 0..2  {T'_i(c), T'_i(c+1)} as int16 pairs, i = 1..3
+//   words 3..5  the same for (c+2, c+3)
+//   word  6     xor mask of the flipped channels, in the bit layout the codes
+//               are packed in by epilogue_thr_pk
+// with T' = T for s = +1 and T' = -T - 1 for s = -1. For an integer sum a,
+// -a > T holds exactly when a < -T, i.e. when a > -T - 1 is false, so a
+// flipped channel's code #{i : -a > T_i} is 3 - #{i : a > T'_i}, which is
+// that count xor 3. Needs |T| and |a| below 2^15 (3*K <= 32766).
+constexpr int kPkRecBytes = 32;
+
+__device__ __forceinline__ void stage_thr_pk(const ConvLaunch& a, uint8_t* lds, int co0, int bm) {
+  for (int gq = threadIdx.x; gq < bm / 4; gq += blockDim.x) {
+    uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = co0 + 4 * gq + i;
+      int4 r = int4{1, 0, 0, 0};
+      if (c < a.cout) r = *reinterpret_cast<const int4*>(a.thr + (int64_t)c * 4);
+      const bool flip = r.x < 0;
+      const int t[3] = {r.y, r.z, r.w};
+#pragma unroll
+      for (int k = 0; k < 3; ++k) {
+        const int v = flip ? -t[k] - 1 : t[k];
+        w[(i >> 1) * 3 + k] |= ((uint32_t)v & 0xFFFFu) << (16 * (i & 1));
+      }
+      if (flip) w[6] |= 3u << ((i & 1) * 16 + (i >> 1) * 4);
+    }
+    uint4* dst = reinterpret_cast<uint4*>(lds + gq * kPkRecBytes);
+    dst[0] = uint4{w[0], w[1], w[2], w[3]};
+    dst[1] = uint4{w[4], w[5], w[6], w[7]};
+  }
+}
+
+// #{i : a > T'_i} for both halves of a packed pair: T' - a is negative
+// exactly when a > T' (no overflow: both are below 2^15 in magnitude).
+__device__ __forceinline__ uint32_t count3_pk(s16x2 p, uint32_t w1, uint32_t w2, uint32_t w3) {
+  const s16x2 d1 = __builtin_bit_cast(s16x2, w1) - p;
+  const s16x2 d2 = __builtin_bit_cast(s16x2, w2) - p;
+  const s16x2 d3 = __builtin_bit_cast(s16x2, w3) - p;
+  const u16x2 s1 = __builtin_bit_cast(u16x2, d1) >> (unsigned short)15;
+  const u16x2 s2 = __builtin_bit_cast(u16x2, d2) >> (unsigned short)15;
+  const u16x2 s3 = __builtin_bit_cast(u16x2, d3) >> (unsigned short)15;
+  return __builtin_bit_cast(uint32_t, s1) + __builtin_bit_cast(uint32_t, s2) +
+         __builtin_bit_cast(uint32_t, s3);
+}
+
+// Threshold epilogue for 2-bit packed output from the records of
+// stage_thr_pk: per lane, accumulator blocks fm of rows (wm*NB + fm)*32 and
+// the pixel column pl of the output tile. Each group of four channels of a
+// pixel becomes one byte: codes packed two per 16-bit half, counted with
+// packed 16-bit subtracts, flipped channels xor'ed, then folded into a byte.
+template <int NB>
+__device__ __forceinline__ void epilogue_thr_pk(const ConvLaunch& a, const uint8_t* lds,
+                                                const v16i (&acc)[NB], int wm, int h, int co0,
+                                                int pl, uint8_t* otile, int orow) {
+#pragma unroll
+  for (int fm = 0; fm < NB; ++fm) {
+    const int cb = (wm * NB + fm) * 32;
+    if (co0 + cb >= a.cout) continue;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int cl = cb + 8 * b + 4 * h;
+      const uint4* rec = reinterpret_cast<const uint4*>(lds + (cl >> 2) * kPkRecBytes);
+      const uint4 r0 = rec[0], r1 = rec[1];
+      const s16x2 p01 = __builtin_amdgcn_cvt_pk_i16(acc[fm][4 * b], acc[fm][4 * b + 1]);
+      const s16x2 p23 = __builtin_amdgcn_cvt_pk_i16(acc[fm][4 * b + 2], acc[fm][4 * b + 3]);
+      const uint32_t c01 = count3_pk(p01, r0.x, r0.y, r0.z);
+      const uint32_t c23 = count3_pk(p23, r0.w, r1.x, r1.y);
+      const uint32_t t = (c01 | (c23 << 4)) ^ r1.z;
+      otile[pl * orow + (cl >> 2)] = (uint8_t)(t | (t >> 14));
+    }
+  }
+}
+
+// 16 two-bit codes (one 32-bit word of a cell) -> 16 int8 operand bytes.
+__device__ __forceinline__ v4i unpack2(uint32_t u) {
+  return v4i{(int)(u & kLow2), (int)((u >> 2) & kLow2), (int)((u >> 4) & kLow2),
+             (int)((u >> 6) & kLow2)};
+}
+
+}  // namespace
+}  // namespace ifq

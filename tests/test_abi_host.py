@@ -105,12 +105,12 @@ def unpack_blob(blob, cout, cin, kh, kw, u2, mfma):
     if mfma:
         # [row block of 32][K32 step][lane 32h + r][16 bytes]; byte 4q + i of
         # K32 step 2*kk + t is channel 64g + 32h + 16t + 4i + q of K64 step
-        # kk = tap*G + g
+        # kk = g*T + tap (T = kh*kw)
         G = cin // 64
         frag = rows.reshape(cpad // 32, kpad // 32, 2, 32, 4, 4)  # rb,k32,h,r,q,i
         for tap in range(kh * kw):
             for g in range(G):
-                kk = tap * G + g
+                kk = g * kh * kw + tap
                 for t in range(2):
                     blk = frag[:, 2 * kk + t]                     # rb,h,r,q,i
                     for h in range(2):

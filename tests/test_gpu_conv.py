@@ -112,6 +112,27 @@ def test_conv_block64_bit_exact(P, case, io):
     run_layout_case(P, case, io)
 
 
+# Workgroup tiles of the size the ResNet-18 layers of the benchmark run with
+# (256, 128 and 64 output pixels for the three variants of the 3x3 kernel
+# that keeps each tile's input window in LDS, and a stride-2 layer), at
+# batches the oracle finishes in about a second; the test also pins which
+# kernel variant the planner takes for each.
+HALO_TILES = [
+    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_halo<8, 1, 6>"),
+    ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_halo<4, 2, 4>"),
+    ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_halo<2, 4, 4>"),
+    ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_halo<8, 1, 6>"),
+]
+
+
+@pytest.mark.parametrize("case", HALO_TILES, ids=[c[0] for c in HALO_TILES])
+def test_conv_halo_tiles_bit_exact(P, case):
+    name, n, h, w, cin, cout, st, kernel = case
+    d = P.ConvDesc(n, h, w, cin, cout, 3, 3, st, 1, 2, 2, B64, B64)
+    assert P.ifq_conv_kernel_name(d) == kernel
+    run_layout_case(P, (name, n, h, w, cin, cout, 3, st, 1), (B64, B64))
+
+
 def test_conv_block64_int32_out(P):
     L = make_layer("b64_i32", 14, 14, 128, 256, 1, 2, 0, 2, 0)
     p = params_for(17, L)
