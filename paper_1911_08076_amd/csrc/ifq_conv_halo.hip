@@ -67,12 +67,16 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
   constexpr int RING = D * STAGE;
   constexpr int HALO0 = RING;
   constexpr int DUMMY = HALO0 + 2 * WK * HSTRIDE;  // 1 KB sink of dummy loads
-  constexpr int LDS_MAIN = DUMMY + 1024;
   constexpr int EPI_BYTES = epilogue_param_bytes(BM);
   constexpr int OUT_BYTES = BN * BM;
   constexpr int RED_BYTES = WK > 1 ? kHaloNW * FM * 4096 : 0;  // 32x32 partial blocks
-  constexpr int L1 = LDS_MAIN > RED_BYTES ? LDS_MAIN : RED_BYTES;
-  constexpr int LDS_BYTES = L1 > EPI_BYTES + OUT_BYTES ? L1 : EPI_BYTES + OUT_BYTES;
+  // Prefetched epilogue records, above everything the reduction and the
+  // epilogue reuse: BM threshold records of 16 B, or (where LDS allows) the
+  // identity-join records of BM channels (64 B each).
+  constexpr int TBL_BYTES = WK <= 2 ? BM * 64 : BM * 16;
+  constexpr int THR0 = DUMMY + 1024 > RED_BYTES ? DUMMY + 1024 : RED_BYTES;
+  constexpr int THR = THR0 > EPI_BYTES + OUT_BYTES ? THR0 : EPI_BYTES + OUT_BYTES;
+  constexpr int LDS_BYTES = THR + TBL_BYTES;
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 
   __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS_BYTES];
@@ -151,6 +155,17 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
       }
   }
 
+  // 2-bit thresholds of a 3x3 layer fit packed 16-bit compares when
+  // 3 * 9 * c_in <= 32766 (sums and thresholds below 2^15 in magnitude)
+  const bool pk16 = a.out_mode == 2 && a.rec == 4 && (a.cout & 31) == 0 && 27 * a.cin <= 32766;
+  const bool pk = pk16 && a.join_kind == IFQ_JOIN_NONE;
+  const bool pk_idj = pk16 && a.join_kind == IFQ_JOIN_IDENTITY &&
+                      (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64 ||
+                       a.sc_layout == IFQ_LAYOUT_U2_NHWC_PACKED);
+  const bool tbl_pre = pk_idj && WK <= 2;
+
+  constexpr int OWN = FM / WK;
+
   // ---- halo chunks: chunk j of a block's window is 64 cells of one image's
   // span; q = kg'*C_h + j enumerates the WK groups' chunks ----------------
   int C_h = 0;
@@ -224,7 +239,21 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
     }
   };
 
-  // ---- prologue: block 0's windows, then stages 0 .. D-3 ------------------
+
+  // ---- prologue: the tile's threshold records (read by the epilogue, so
+  // their latency hides behind the main loop), block 0's windows, then
+  // stages 0 .. D-3 ---------------------------------------------------------
+  if (pk && wave < BM / 64) {
+    const int c = co0 + wave * 64 + lane;
+    dma16(c < a.cout ? reinterpret_cast<const uint8_t*>(a.thr + (int64_t)c * 4) : zero_src,
+          lds0 + THR + wave * 1024);
+  }
+  if (tbl_pre) {   // 16 channels x 64 B per wave
+    const int c = co0 + wave * 16 + (lane >> 2);
+    dma16(c < a.cout ? reinterpret_cast<const uint8_t*>(a.table + (int64_t)c * 16 + (lane & 3) * 4)
+                     : zero_src,
+          lds0 + THR + wave * 1024);
+  }
   for (int q = wave; q < nq; q += kHaloNW) {
     int sc, dst;
     chunk(q, sc, dst);
@@ -323,7 +352,6 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
   // ---- K groups: wave (kg, wn) keeps row blocks kg*OWN .. kg*OWN + OWN - 1
   // of its pixel column; the other groups' sums of those blocks come through
   // LDS (4 KB per 32x32 block) ------------------------------------------------
-  constexpr int OWN = FM / WK;
   v16i own[OWN];
   // (indices of acc stay compile-time: a runtime index would move it to
   // scratch)
@@ -360,12 +388,11 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
     __syncthreads();
   }
 
-  // 2-bit thresholds of a 3x3 layer fit packed 16-bit compares when
-  // 3 * 9 * c_in <= 32766 (sums and thresholds below 2^15 in magnitude)
-  const bool pk = a.out_mode == 2 && a.join_kind == IFQ_JOIN_NONE && a.rec == 4 &&
-                  (a.cout & 31) == 0 && 27 * a.cin <= 32766;
   if (pk)
-    stage_thr_pk(a, lds, co0, BM);
+    stage_thr_pk(reinterpret_cast<const int4*>(lds + THR), lds, BM);
+  else if (pk_idj)
+    stage_idj_pk(tbl_pre ? reinterpret_cast<const int32_t*>(lds + THR) : a.table + co0 * 16,
+                 lds, BM, a.cout - co0 < BM ? a.cout - co0 : BM);
   else
     stage_epilogue(a, lds, co0, BM);
   __syncthreads();
@@ -383,6 +410,18 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
                                   a.acc_dump);
     if (pk) {
       epilogue_thr_pk<OWN>(a, lds, own, kg, h, co0, pl, otile, orow);
+    } else if (pk_idj) {
+      // shortcut codes of the row blocks this wave finishes (loading them
+      // before the main loop, as compiler-visible loads among the explicitly
+      // counted DMA, measured slower)
+      uint2 scw[OWN];
+      const int pc = p0 + pl < a.m ? p0 + pl : a.m - 1;
+#pragma unroll
+      for (int j = 0; j < OWN; ++j) {
+        const int co = co0 + (kg * OWN + j) * 32;
+        scw[j] = co < a.cout ? shortcut8(a, pc, co) : uint2{0, 0};
+      }
+      epilogue_idj_pk<OWN>(a, lds, own, scw, kg, h, co0, pl, otile, orow);
     } else if (fast) {
       if (a.out_mode == 0)
         epilogue32<kE32I32, OWN, 1>(a, lds, own2, kg, wn, h, l32, co0, p0, bn, otile, orow, y32);
@@ -408,7 +447,7 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
 // Variants and per-layer planning
 // ---------------------------------------------------------------------------
 struct HaloVariant {
-  int wn, wk, d;
+  int wn, wk, d;   // waves along pixels, K groups, ring stages
   double c0_us;   // fixed cost of one round of workgroups
   double eff;     // MFMA efficiency of the main loop
   const char* name;

@@ -214,14 +214,14 @@ typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 // that count xor 3. Needs |T| and |a| below 2^15 (3*K <= 32766).
 constexpr int kPkRecBytes = 32;
 
-__device__ __forceinline__ void stage_thr_pk(const ConvLaunch& a, uint8_t* lds, int co0, int bm) {
+// recs: the bm channels' {s, T1, T2, T3} records (already in LDS; records of
+// channels past c_out may hold anything, their codes are never stored).
+__device__ __forceinline__ void stage_thr_pk(const int4* recs, uint8_t* lds, int bm) {
   for (int gq = threadIdx.x; gq < bm / 4; gq += blockDim.x) {
     uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int c = co0 + 4 * gq + i;
-      int4 r = int4{1, 0, 0, 0};
-      if (c < a.cout) r = *reinterpret_cast<const int4*>(a.thr + (int64_t)c * 4);
+      const int4 r = recs[4 * gq + i];
       const bool flip = r.x < 0;
       const int t[3] = {r.y, r.z, r.w};
 #pragma unroll
@@ -273,6 +273,87 @@ __device__ __forceinline__ void epilogue_thr_pk(const ConvLaunch& a, const uint8
       const uint32_t c01 = count3_pk(p01, r0.x, r0.y, r0.z);
       const uint32_t c23 = count3_pk(p23, r0.w, r1.x, r1.y);
       const uint32_t t = (c01 | (c23 << 4)) ^ r1.z;
+      otile[pl * orow + (cl >> 2)] = (uint8_t)(t | (t >> 14));
+    }
+  }
+}
+
+// Identity-join records laid out for packed 16-bit compares. The shortcut
+// code x of each channel selects that channel's thresholds T_i(c, x) (the
+// records of ifq_fold_join_table; their sign s depends on the channel only).
+// Per group of four channels c .. c+3, 512 bytes: for the pair (c, c+1) 16
+// entries of 16 bytes, entry x0 | x1 << 2 holding {T'_i(c, x0), T'_i(c+1, x1)}
+// as int16 pairs (i = 1..3) and the pair's xor mask of flipped channels;
+// then the same for (c+2, c+3). T' as for stage_thr_pk.
+constexpr int kIdjGroupBytes = 512;
+
+// tbl: the bm channels' [4][4] int32 records (global or LDS); channels at or
+// past nch get plain records (their codes are never stored).
+__device__ __forceinline__ void stage_idj_pk(const int32_t* tbl, uint8_t* lds, int bm, int nch) {
+  for (int e = threadIdx.x; e < (bm / 4) * 32; e += blockDim.x) {
+    const int gq = e >> 5, pr = (e >> 4) & 1, combo = e & 15;
+    const int x[2] = {combo & 3, combo >> 2};
+    uint32_t w[4] = {0, 0, 0, 0};
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int c = 4 * gq + 2 * pr + j;
+      int4 r = int4{1, 0, 0, 0};
+      if (c < nch) r = *reinterpret_cast<const int4*>(tbl + (c * 4 + x[j]) * 4);
+      const bool flip = r.x < 0;
+      const int t[3] = {r.y, r.z, r.w};
+#pragma unroll
+      for (int k = 0; k < 3; ++k) {
+        const int v = flip ? -t[k] - 1 : t[k];
+        w[k] |= ((uint32_t)v & 0xFFFFu) << (16 * j);
+      }
+      if (flip) w[3] |= 3u << (16 * j);
+    }
+    *reinterpret_cast<uint4*>(lds + gq * kIdjGroupBytes + pr * 256 + combo * 16) =
+        uint4{w[0], w[1], w[2], w[3]};
+  }
+}
+
+// The 2-bit shortcut codes of output channels co .. co+31 of pixel p
+// (8 bytes, channel co + 4k + i in bits 2i of byte k), for shortcut layouts
+// U2_NHWC_PACKED and U2_BLOCK64 (co % 32 == 0).
+__device__ __forceinline__ uint2 shortcut8(const ConvLaunch& a, int p, int co) {
+  const uint8_t* sc8 = reinterpret_cast<const uint8_t*>(a.shortcut);
+  int64_t off;
+  if (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64) {
+    const int howo = a.ho * a.wo;
+    const int nimg = fdiv(p, a.div_howo);
+    off = (((int64_t)nimg * (a.cout >> 6) + (co >> 6)) * howo + (p - nimg * howo)) * 16 +
+          ((co & 63) >> 2);
+  } else {
+    off = ((int64_t)p * a.cout + co) >> 2;
+  }
+  return *reinterpret_cast<const uint2*>(sc8 + off);
+}
+
+// Identity-join epilogue for 2-bit packed output from the records of
+// stage_idj_pk; sc[fm]: shortcut8 of the lane's pixel for block fm.
+template <int NB>
+__device__ __forceinline__ void epilogue_idj_pk(const ConvLaunch& a, const uint8_t* lds,
+                                                const v16i (&acc)[NB], const uint2 (&sc)[NB],
+                                                int wm, int h, int co0, int pl,
+                                                uint8_t* otile, int orow) {
+#pragma unroll
+  for (int fm = 0; fm < NB; ++fm) {
+    const int cb = (wm * NB + fm) * 32;
+    if (co0 + cb >= a.cout) continue;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int cl = cb + 8 * b + 4 * h;
+      const uint32_t word = (b >> 1) ? sc[fm].y : sc[fm].x;
+      const uint32_t xs = word >> (8 * (2 * (b & 1) + h));
+      const uint8_t* g = lds + (cl >> 2) * kIdjGroupBytes;
+      const uint4 e01 = *reinterpret_cast<const uint4*>(g + (xs & 15u) * 16);
+      const uint4 e23 = *reinterpret_cast<const uint4*>(g + 256 + ((xs >> 4) & 15u) * 16);
+      const s16x2 p01 = __builtin_amdgcn_cvt_pk_i16(acc[fm][4 * b], acc[fm][4 * b + 1]);
+      const s16x2 p23 = __builtin_amdgcn_cvt_pk_i16(acc[fm][4 * b + 2], acc[fm][4 * b + 3]);
+      const uint32_t c01 = count3_pk(p01, e01.x, e01.y, e01.z) ^ e01.w;
+      const uint32_t c23 = count3_pk(p23, e23.x, e23.y, e23.z) ^ e23.w;
+      const uint32_t t = c01 | (c23 << 4);
       otile[pl * orow + (cl >> 2)] = (uint8_t)(t | (t >> 14));
     }
   }

@@ -244,6 +244,47 @@ class DeviceStack:
         return [conv_ops(L, self.batch) if _is_conv(L) else 0 for L in self.layers]
 
     # -- execution -------------------------------------------------------------
+    def _slot_ptr(self, k, x, y):
+        if k == 0:
+            return x.data_ptr()
+        if k == 1:
+            return y.data_ptr()
+        off, _ = api.ifq_stack_slot_info(self.stack, k)
+        return self.ws.data_ptr() + off
+
+    def layer_launcher(self, i, x, y, stream=None):
+        """A callable that launches layer i alone on the stack's buffers
+        (asynchronous), exactly as ifq_run_stack launches it: same
+        descriptor, weights, thresholds, join and slots. Valid once a full
+        run has filled the layer's input slots. The arguments are marshalled
+        once, so repeated calls cost one C call each."""
+        rec = self._layers[i]
+        lib = _ffi.load()
+        vp = ctypes.c_void_p
+        src = vp(self._slot_ptr(rec.src, x, y))
+        dst = vp(self._slot_ptr(rec.dst, x, y))
+        st = api._stream(stream)
+        if rec.kind == IFQ_LAYER_CONV:
+            desc = rec.conv
+            join = None
+            if rec.join.kind != 0:
+                join = _ffi.Join.from_buffer_copy(rec.join)
+                join.shortcut = self._slot_ptr(rec.join_src, x, y)
+            args = (ctypes.byref(desc), src, vp(rec.w_packed), vp(rec.thr),
+                    None if join is None else ctypes.byref(join), dst, None, None, 0, st)
+            fn = lib.ifq_conv_forward
+            what = "ifq_conv_forward"
+        else:
+            desc = rec.pool
+            args = (ctypes.byref(desc), src, dst, st)
+            fn = lib.ifq_maxpool_codes
+            what = "ifq_maxpool_codes"
+
+        def launch():
+            api._check(fn(*args), what)
+        launch.keep = (desc, join if rec.kind == IFQ_LAYER_CONV else None)
+        return launch
+
     def run(self, x, y, stream=None, events=None):
         """One forward pass (asynchronous on stream). events: optional ctypes
         array of n_layers + 1 hipEvent_t handles for per-layer timing."""

@@ -157,9 +157,9 @@ def run_layout_case(P, case, io):
 
 @pytest.mark.parametrize("io", [(I8, I8, I8), (I8, U2, I8), (U2, U2, U2),
                                 (U2, I8, U2), (B64, B64, B64), (B64, U2, I8),
-                                (U2, B64, B64)],
+                                (U2, B64, B64), (B64, U2, B64)],
                          ids=["i8", "sc_u2", "u2", "u2_sc_i8", "b64", "b64_sc_u2",
-                              "u2_sc_b64"])
+                              "u2_sc_b64", "b64_sc_u2_out_b64"])
 @pytest.mark.parametrize("shape", [(2, 10, 10, 64, 64), (1, 7, 7, 512, 512),
                                    (1, 9, 11, 128, 128), (6, 14, 14, 256, 256)])
 def test_identity_join_bit_exact(P, shape, io):
