@@ -244,6 +244,9 @@ def main():
     ap.add_argument("--layout", default="b64", choices=["b64", "u2", "i8"],
                     help="layout of the 2-bit code tensors (b64: channel "
                          "blocks of 64, u2: NHWC packed, i8: byte per code)")
+    ap.add_argument("--no-fuse-down", action="store_true",
+                    help="run the 1x1 downsample convs as layers of their own "
+                         "(default with b64: inside the conv join that reads them)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="the oracle's CPU-baseline sample repeats the whole "
                          "batch until this much time has passed")
@@ -281,7 +284,9 @@ def main():
     params = [layer_params(args.config, i, L, "plain") if isinstance(L, Conv) else None
               for i, L in enumerate(layers)]
     torch.cuda.set_device(0)
-    dev = P.DeviceStack(layers, params, batch, code_layout=args.layout)
+    dev = P.DeviceStack(layers, params, batch, code_layout=args.layout,
+                        fuse_down=not args.no_fuse_down)
+    run_layers = dev.layers    # without the downsample layers folded into joins
     L0 = layers[0]
     x_host = stack_input(args.config, (batch, L0.h, L0.w, L0.cin), L0.in_bits)
     x = dev.upload_input(x_host)
@@ -289,7 +294,7 @@ def main():
     stream = torch.cuda.Stream()
     sh = stream.cuda_stream
     hip = Hip()
-    nl = len(layers)
+    nl = len(run_layers)
 
     print("bench: %s batch %d layout %s, %d layers, %.3f Gop/step" %
           (cfg.name, batch, args.layout, nl, dev.ops / 1e9), file=sys.stderr, flush=True)
@@ -340,8 +345,10 @@ def main():
 
     ops = dev.layer_ops()
     per_layer = []
-    for i, L in enumerate(layers):
+    for i, L in enumerate(run_layers):
         rec = {"layer": L.name, "kernel": names[i], "us": lay_ms[i] * 1e3}
+        if L.name in dev.fused:
+            rec["fused_downsample"] = dev.fused[L.name]
         if ops[i]:
             rec["tops"] = ops[i] / (lay_ms[i] * 1e-3) / 1e12
             rec["pct_peak"] = 100.0 * rec["tops"] / PEAK_INT8_TOPS
@@ -368,8 +375,10 @@ def main():
                 "op": "int8 ops, 2 per +-1 x code MAC"}
 
     judged = [r for r in per_layer if r["layer"] in JUDGED]
-    judged_ops = sum(ops[i] for i, L in enumerate(layers) if L.name in JUDGED)
-    judged_ms = sum(lay_ms[i] for i, L in enumerate(layers) if L.name in JUDGED)
+    # judged layers: their own 3x3 conv ops only (a fused downsample's work
+    # is in their time but not counted)
+    judged_ops = sum(P.conv_ops(L, batch) for L in run_layers if L.name in JUDGED)
+    judged_ms = sum(lay_ms[i] for i, L in enumerate(run_layers) if L.name in JUDGED)
     judged_pct = (100.0 * judged_ops / (judged_ms * 1e-3) / 1e12 / PEAK_INT8_TOPS
                   if judged_ms else None)
 
@@ -386,6 +395,8 @@ def main():
         "config": {"workload": cfg.name, "batch": batch,
                    "input": "%dx%dx%d %d-bit codes" % (L0.h, L0.w, L0.cin, L0.in_bits),
                    "code_layout": args.layout, "weights": "+-1 (seeded)",
+                   "downsample": ("fused into the conv joins" if dev.fused
+                                  else "separate 1x1 convs"),
                    "params": "seeded BN/alpha, plain variant"},
         "images_per_s": images_s,
         "pct_int8_peak": 100.0 * value / 1e12 / PEAK_INT8_TOPS,

@@ -70,6 +70,8 @@ typedef int32_t ifq_status;
 #define IFQ_JOIN_NONE 0
 #define IFQ_JOIN_IDENTITY 1 /* shortcut = the block input codes             */
 #define IFQ_JOIN_CONV 2     /* shortcut = int32 sums of a 1x1 downsample conv */
+#define IFQ_JOIN_CONV_FUSED 3 /* shortcut = the downsample's input codes; the
+                                 1x1 downsample conv runs inside this conv  */
 
 #define IFQ_LAYER_CONV 0
 #define IFQ_LAYER_POOL 1
@@ -172,17 +174,30 @@ typedef struct ifq_join_params {
 
 /*
  * Device-side join operand of ifq_conv_forward.
- *   kind      IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY or IFQ_JOIN_CONV
+ *   kind      IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY, IFQ_JOIN_CONV or
+ *             IFQ_JOIN_CONV_FUSED
  *   layout    layout of shortcut: codes (I8, U2 or BLOCK64) for IDENTITY,
- *             I32 for CONV
- *   shortcut  device tensor [n][ho][wo][c_out]
- *   coef      IFQ_JOIN_CONV: device array [c_out][3] written by
+ *             I32 for CONV, BLOCK64 codes for CONV_FUSED
+ *   shortcut  IDENTITY, CONV: device tensor [n][ho][wo][c_out] (block input
+ *             codes, or the downsample conv's int32 sums d);
+ *             CONV_FUSED: the downsample conv's input codes, of shape
+ *             down.{n, h, w, c_in}
+ *   coef      IFQ_JOIN_CONV / CONV_FUSED: device array [c_out][3] written by
  *             ifq_fold_join (NULL for IDENTITY)
  *   table     IFQ_JOIN_IDENTITY: device array [c_out][4][2^out_bits]
  *             written by ifq_fold_join_table with x_bits = 2 (the shortcut
  *             codes are 2-bit; NULL for CONV)
  *   n_q       number of quantizer thresholds, 2^out_bits - 1
  *   q_thr     the quantizer thresholds of Eq. (3), strictly increasing
+ *   down_w, down
+ *             IFQ_JOIN_CONV_FUSED only (else ignored): the downsample conv's
+ *             packed weights (ifq_pack_weights of down) and its descriptor:
+ *             1x1, pad 0, 2-bit BLOCK64 input, int32 output (out_bits 0),
+ *             c_out and output size equal to the conv's. Its sums d are
+ *             computed inside the conv's kernel and never stored, so the
+ *             join reads neither d nor anything from an extra launch. It
+ *             needs a 3x3 pad-1 conv with 2-bit BLOCK64 input and output;
+ *             shapes the kernel does not cover return IFQ_ERR_UNSUPPORTED.
  */
 typedef struct ifq_join {
   int32_t kind;
@@ -193,6 +208,8 @@ typedef struct ifq_join {
   int32_t n_q;
   int32_t reserved;
   double q_thr[IFQ_MAX_THRESHOLDS];
+  const void* down_w;
+  ifq_conv_desc down;
 } ifq_join;
 
 /*

@@ -28,6 +28,7 @@ IFQ_POOL_SAME = 1
 IFQ_JOIN_NONE = 0
 IFQ_JOIN_IDENTITY = 1
 IFQ_JOIN_CONV = 2
+IFQ_JOIN_CONV_FUSED = 3
 
 IFQ_LAYER_CONV = 0
 IFQ_LAYER_POOL = 1
@@ -67,7 +68,8 @@ class JoinParams(ctypes.Structure):
 class Join(ctypes.Structure):
     _fields_ = [("kind", i32), ("layout", i32), ("shortcut", vp), ("coef", vp),
                 ("table", vp), ("n_q", i32), ("reserved", i32),
-                ("q_thr", f64 * IFQ_MAX_THRESHOLDS)]
+                ("q_thr", f64 * IFQ_MAX_THRESHOLDS), ("down_w", vp),
+                ("down", ConvDesc)]
 
 
 class PoolDesc(ctypes.Structure):

@@ -156,7 +156,10 @@ def ifq_fold_join_table(main, beta_x, in_bits, k, out_bits, q_thr, x_bits=2):
     return out
 
 
-def make_join(kind, layout, shortcut, coef, q_thr, table=None):
+def make_join(kind, layout, shortcut, coef, q_thr, table=None, down_w=None,
+              down=None):
+    """ifq_join; down_w (packed 1x1 weights) and down (its ConvDesc) are for
+    IFQ_JOIN_CONV_FUSED, whose coef comes from ifq_fold_join(IFQ_JOIN_CONV)."""
     j = Join()
     j.kind = kind
     j.layout = layout
@@ -167,6 +170,9 @@ def make_join(kind, layout, shortcut, coef, q_thr, table=None):
     j.n_q = len(q)
     for i, v in enumerate(q[:IFQ_MAX_THRESHOLDS]):
         j.q_thr[i] = float(v)
+    j.down_w = _ptr(down_w)
+    if down is not None:
+        j.down = down
     return j
 
 

@@ -157,7 +157,8 @@ ifq_status check_pool(const ifq_pool_desc* d, int64_t* ho, int64_t* wo) {
 }
 
 ifq_status check_join(const ifq_join* j, const ifq_conv_desc* d) {
-  if (j->kind != IFQ_JOIN_IDENTITY && j->kind != IFQ_JOIN_CONV)
+  if (j->kind != IFQ_JOIN_IDENTITY && j->kind != IFQ_JOIN_CONV &&
+      j->kind != IFQ_JOIN_CONV_FUSED)
     return fail(IFQ_ERR_INVALID_ARGUMENT, "join: bad kind %d", j->kind);
   if (d->out_bits == 0)
     return fail(IFQ_ERR_INVALID_ARGUMENT, "join: needs a quantized output");
@@ -169,8 +170,29 @@ ifq_status check_join(const ifq_join* j, const ifq_conv_desc* d) {
       return fail(IFQ_ERR_INVALID_ARGUMENT,
                   "join: q_thr must be finite and strictly increasing");
   }
-  if (j->kind == IFQ_JOIN_CONV && !j->coef)
+  if ((j->kind == IFQ_JOIN_CONV || j->kind == IFQ_JOIN_CONV_FUSED) && !j->coef)
     return fail(IFQ_ERR_INVALID_ARGUMENT, "join: conv join needs coef");
+  if (j->kind == IFQ_JOIN_CONV_FUSED) {
+    const ifq_conv_desc& dd = j->down;
+    int64_t dho, dwo;
+    if (check_conv(&dd, &dho, &dwo) != IFQ_OK)
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "join: fused downsample: %s",
+                  g_last_error.c_str());
+    int64_t ho, wo;
+    check_conv(d, &ho, &wo);
+    if (!j->down_w)
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "join: fused downsample needs down_w");
+    if (dd.kh != 1 || dd.kw != 1 || dd.pad != 0 || dd.in_bits != 2 || dd.out_bits != 0 ||
+        dd.out_layout != IFQ_LAYOUT_I32_NHWC)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "join: fused downsample must be 1x1, pad 0, 2-bit input, int32 output");
+    if (dd.n != d->n || dd.c_out != d->c_out || dho != ho || dwo != wo)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "join: fused downsample output must match the conv's (n, size, c_out)");
+    if (j->layout != dd.in_layout)
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "join: fused shortcut layout must be the downsample's input layout");
+  }
   if (j->kind == IFQ_JOIN_IDENTITY && !j->table)
     return fail(IFQ_ERR_INVALID_ARGUMENT, "join: identity join needs table");
   if (j->kind == IFQ_JOIN_CONV && j->layout != IFQ_LAYOUT_I32_NHWC)
@@ -217,6 +239,17 @@ ifq::ConvLaunch make_launch(const ifq_conv_desc* d, int64_t ho, int64_t wo,
     a.coef = join->coef;
     a.table = join->table;
     for (int i = 0; i < join->n_q; ++i) a.qthr[i] = join->q_thr[i];
+    if (join->kind == IFQ_JOIN_CONV_FUSED) {
+      const ifq::WeightGeom gd = ifq::weight_geom(join->down);
+      a.dx = static_cast<const uint8_t*>(shortcut);
+      a.dwgt = static_cast<const int8_t*>(join->down_w);
+      a.d_wzero = gd.zero_off;
+      a.d_cin = join->down.c_in;
+      a.d_h = join->down.h;
+      a.d_w = join->down.w;
+      a.d_stride = join->down.stride;
+      a.d_nk32 = (int32_t)(gd.kpad / 32);
+    }
   }
   a.nq = d->out_bits ? (1 << d->out_bits) - 1 : 0;
   a.rec = d->out_bits ? (1 << d->out_bits) : 0;
@@ -280,6 +313,15 @@ ifq_status conv_args_check(const ifq_conv_desc* d, const void* x,
     ifq_status st = check_join(join, d);
     if (st != IFQ_OK) return st;
     if (!shortcut) return fail(IFQ_ERR_INVALID_ARGUMENT, "join: shortcut is NULL");
+    if (join->kind == IFQ_JOIN_CONV_FUSED) {
+      int64_t ho, wo;
+      check_conv(d, &ho, &wo);
+      const ifq::ConvLaunch a =
+          make_launch(d, ho, wo, x, w, thr, join, shortcut, const_cast<void*>(y), nullptr);
+      if (!ifq::mfma_eligible(a) || !ifq::fused_supported(a))
+        return fail(IFQ_ERR_UNSUPPORTED,
+                    "join: no fused kernel for this conv and downsample shape");
+    }
   }
   if (d->n > 0 && (!x || !w || !y))
     return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: x, w_packed and y are required");

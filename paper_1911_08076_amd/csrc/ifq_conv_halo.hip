@@ -53,7 +53,7 @@ __host__ __device__ constexpr int halo_cap_cells(int wk) {
 
 __host__ __device__ constexpr int round64(int v) { return (v + 63) & ~63; }
 
-template <int WN, int WK, int D>
+template <int WN, int WK, int D, bool FUSED>
 __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
   static_assert(WN * WK == kHaloNW, "8 waves");
   constexpr int FM = kHaloFM, BM = kHaloBM, BN = 32 * WN;
@@ -164,7 +164,6 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
                        a.sc_layout == IFQ_LAYOUT_U2_NHWC_PACKED);
   const bool tbl_pre = pk_idj && WK <= 2;
 
-  constexpr int OWN = FM / WK;
 
   // ---- halo chunks: chunk j of a block's window is 64 cells of one image's
   // span; q = kg'*C_h + j enumerates the WK groups' chunks ----------------
@@ -240,6 +239,52 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
   };
 
 
+  // ---- fused downsample (IFQ_JOIN_CONV_FUSED): one extra stage after the
+  // 3x3 stages. Its weight chunks are those of the row blocks each group
+  // finishes (all Gd = d_cin/64 = WK K64 steps: 8 chunks per group, so the
+  // stage has the usual WK chunks per wave); its input cells (stride d_stride
+  // gather, one 16-byte cell per pixel and channel block, cell e = g*BN + pixel
+  // in 1 KB chunks, one per wave) go into the halo buffers of parity nG % 2,
+  // which the last block does not use. ----------------------------------------
+  constexpr bool fused = FUSED;   // a.join_kind == IFQ_JOIN_CONV_FUSED
+  const int Gd = fused ? a.d_cin >> 6 : 0;
+  const int nst_all = nst + (fused ? 1 : 0);
+  constexpr int CPB = HCAP / 64;                  // 1 KB chunks per halo buffer
+  const int dpar = nG & 1;
+  auto dchunk = [&](int q) {                      // LDS offset of down chunk q
+    return HALO0 + ((q / CPB) * 2 + dpar) * HSTRIDE + (q % CPB) * 1024;
+  };
+  const uint8_t* dsrc = zero_src;                 // this wave's down chunk
+  if constexpr (FUSED) {
+    const int e = wave * 64 + lane;
+    const int g = e / BN, pe = e - g * BN;
+    const int p = p0 + pe;
+    if (g < Gd && pe < bn && p < a.m) {
+      const int n = fdiv(p, a.div_howo);
+      const int rem = p - n * howo;
+      const int oy = fdiv(rem, a.div_wo);
+      const int ox = rem - oy * Wo;
+      dsrc = a.dx + ((((int64_t)n * Gd + g) * a.d_h + oy * a.d_stride) * a.d_w +
+                     ox * a.d_stride) * 16;
+    }
+  }
+  const bool dreal = fused && wave * 64 < Gd * BN;
+  auto issue_down = [&]() {
+    const uint32_t slot = lds0 + (uint32_t)((nst % D) * STAGE);
+    const int j = wave / (2 * Gd), k32 = wave - j * 2 * Gd;
+#pragma unroll
+    for (int i = 0; i < WK; ++i) {
+      const int rb = rbw + i * (FM / WK) + j;
+      const int64_t off = rb < nrb ? ((int64_t)rb * a.d_nk32 + k32) * 1024 : a.d_wzero;
+      dma16s(reinterpret_cast<const uint8_t*>(a.dwgt) + off, voff,
+             slot + (uint32_t)(i * A_STEP + wave * 1024));
+    }
+    if (dreal)
+      dma16(dsrc, lds0 + (uint32_t)dchunk(wave));
+    else
+      issue_dummy();
+  };
+
   // ---- prologue: the tile's threshold records (read by the epilogue, so
   // their latency hides behind the main loop), block 0's windows, then
   // stages 0 .. D-3 ---------------------------------------------------------
@@ -312,7 +357,7 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
 #pragma unroll
     for (int tap = 0; tap < kTaps; ++tap) {
       const int s_ = gi * kTaps + tap;
-      const int after = nst - 1 - s_;
+      const int after = nst_all - 1 - s_;
       wait_ahead<D - 3, CPW>(after < D - 3 ? after : D - 3);
       // A bare barrier: no LDS fence is needed here (the slot reused below
       // was read by fragments the previous iteration's MFMAs consumed, and
@@ -327,6 +372,8 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
           issue_halo(gi + 1, hs_src[tap < NR ? tap : 0], hs_dst[tap < NR ? tap : 0]);
         else
           issue_dummy();
+      } else if constexpr (FUSED) {
+        if (s_ + D - 2 == nst) issue_down();
       }
       if ((tap & 1) == 0) {
         // tap 0 follows tap 8 of the previous block, which was read into fa
@@ -348,6 +395,31 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
   mfmas(fb);
   wait_vmcnt<0>();
   __syncthreads();
+
+  // fused downsample: its sums for the row blocks this wave finishes
+  constexpr int OWN = FM / WK;
+  v16i accd[OWN];
+#pragma unroll
+  for (int j = 0; j < OWN; ++j) accd[j] = v16i{0};
+  if constexpr (FUSED) {
+    const uint8_t* as = lds + (nst % D) * STAGE + kg * A_STEP;
+    for (int g = 0; g < Gd; ++g) {
+      const int e = g * BN + wn * 32 + l32;
+      const v2i braw =
+          *reinterpret_cast<const v2i*>(lds + dchunk(e >> 6) + (e & 63) * 16 + 8 * h);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const v4i bf = unpack2((uint32_t)braw[t]);
+#pragma unroll
+        for (int j = 0; j < OWN; ++j) {
+          const v4i af = *reinterpret_cast<const v4i*>(
+              as + (j * 2 * Gd + 2 * g + t) * 1024 + lane * 16);
+          accd[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af, bf, accd[j], 0, 0, 0);
+        }
+      }
+    }
+    __syncthreads();   // before the K-group exchange reuses this LDS
+  }
 
   // ---- K groups: wave (kg, wn) keeps row blocks kg*OWN .. kg*OWN + OWN - 1
   // of its pixel column; the other groups' sums of those blocks come through
@@ -408,7 +480,9 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
     if (a.acc_dump)
       epilogue32<kE32I32, OWN, 1>(a, lds, own2, kg, wn, h, l32, co0, p0, bn, otile, orow,
                                   a.acc_dump);
-    if (pk) {
+    if (FUSED) {
+      epilogue_cjoin<OWN>(a, lds, own, accd, kg, h, co0, pl, otile, orow);
+    } else if (pk) {
       epilogue_thr_pk<OWN>(a, lds, own, kg, h, co0, pl, otile, orow);
     } else if (pk_idj) {
       // shortcut codes of the row blocks this wave finishes (loading them
@@ -455,9 +529,9 @@ struct HaloVariant {
 
 // Index order must match the switch in launch_conv_halo.
 const HaloVariant kHaloVariants[] = {
-    {8, 1, 6, 4.0, 0.75, "conv_halo<8, 1, 6>"},   // 128 x 256
-    {4, 2, 4, 4.0, 0.75, "conv_halo<4, 2, 4>"},   // 128 x 128, K split 2
-    {2, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4>"},   // 128 x 64, K split 4
+    {8, 1, 6, 4.0, 0.75, "conv_halo<8, 1, 6, false>"},   // 128 x 256
+    {4, 2, 4, 4.0, 0.75, "conv_halo<4, 2, 4, false>"},   // 128 x 128, K split 2
+    {2, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4, false>"},   // 128 x 64, K split 4
 };
 constexpr int kNumHalo = sizeof(kHaloVariants) / sizeof(kHaloVariants[0]);
 constexpr int kNumCUs = 256;
@@ -482,6 +556,12 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
     return false;
   // 32-bit cell indices and offsets
   if ((int64_t)a.n * a.h * a.w * (a.cin / 64) >= (int64_t)1 << 26) return false;
+  const bool fused = a.join_kind == IFQ_JOIN_CONV_FUSED;
+  if (fused && !(a.out_mode == 2 && a.rec == 4 && a.out_layout == IFQ_LAYOUT_U2_BLOCK64 &&
+                 a.sc_layout == IFQ_LAYOUT_U2_BLOCK64 && a.d_cin % 64 == 0 &&
+                 a.cout % 32 == 0 &&
+                 (int64_t)a.n * a.d_h * a.d_w * (a.d_cin / 64) < (int64_t)1 << 26))
+    return false;
   const int G = a.cin / 64;
   double best_t = 1e30;
   bool found = false;
@@ -489,6 +569,12 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
     const HaloVariant& V = kHaloVariants[v];
     if (G % V.wk) continue;
     const int bnmax = 32 * V.wn;
+    if (fused) {
+      // the downsample's K64 steps split one per group; its input chunks
+      // (one per wave) fit the spare halo buffers
+      const int gd = a.d_cin / 64, nqd = gd * bnmax / 64;
+      if (gd != V.wk || nqd > kHaloNW || nqd > V.wk * (halo_cap_cells(V.wk) / 64)) continue;
+    }
     const int64_t nco = (a.cout + kHaloBM - 1) / kHaloBM;
     const int64_t nb_min = (a.m + bnmax - 1) / bnmax;
     const int64_t rounds = (nco * nb_min + kNumCUs - 1) / kNumCUs;
@@ -514,15 +600,24 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
   return found;
 }
 
-const char* conv_halo_name(const HaloPlan& p) { return kHaloVariants[p.variant].name; }
+// The kernel's name as a profiler lists it (the template arguments).
+const char* conv_halo_name(const HaloPlan& p, bool fused) {
+  static const char* const kFused[] = {"conv_halo<8, 1, 6, true>", "conv_halo<4, 2, 4, true>",
+                                       "conv_halo<2, 4, 4, true>"};
+  return fused ? kFused[p.variant] : kHaloVariants[p.variant].name;
+}
 
 hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream) {
   a.bn = p.bn;
   const dim3 grid(p.blocks_m, (a.cout + kHaloBM - 1) / kHaloBM);
-  switch (p.variant) {
-    case 0: hipLaunchKernelGGL((conv_halo<8, 1, 6>), grid, dim3(512), 0, stream, a); break;
-    case 1: hipLaunchKernelGGL((conv_halo<4, 2, 4>), grid, dim3(512), 0, stream, a); break;
-    default: hipLaunchKernelGGL((conv_halo<2, 4, 4>), grid, dim3(512), 0, stream, a); break;
+  const bool fused = a.join_kind == IFQ_JOIN_CONV_FUSED;
+  switch (p.variant * 2 + (fused ? 1 : 0)) {
+    case 0: hipLaunchKernelGGL((conv_halo<8, 1, 6, false>), grid, dim3(512), 0, stream, a); break;
+    case 1: hipLaunchKernelGGL((conv_halo<8, 1, 6, true>), grid, dim3(512), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((conv_halo<4, 2, 4, false>), grid, dim3(512), 0, stream, a); break;
+    case 3: hipLaunchKernelGGL((conv_halo<4, 2, 4, true>), grid, dim3(512), 0, stream, a); break;
+    case 4: hipLaunchKernelGGL((conv_halo<2, 4, 4, false>), grid, dim3(512), 0, stream, a); break;
+    default: hipLaunchKernelGGL((conv_halo<2, 4, 4, true>), grid, dim3(512), 0, stream, a); break;
   }
   return hipGetLastError();
 }

@@ -376,17 +376,24 @@ bool mfma_eligible(const ConvLaunch& a) {
          (a.in_layout == IFQ_LAYOUT_U2_NHWC_PACKED || a.in_layout == IFQ_LAYOUT_U2_BLOCK64);
 }
 
+// A fused downsample join runs only in the windowed 3x3 kernel (the host
+// checks plan_halo succeeds before launching one).
 const char* conv_mfma_name(const ConvLaunch& a) {
-  const Plan pl = plan_mfma(a);
   HaloPlan hp;
-  if (plan_halo(a, &hp) && hp.t_us < pl.t_us) return conv_halo_name(hp);
+  const bool halo = plan_halo(a, &hp);
+  if (halo && a.join_kind == IFQ_JOIN_CONV_FUSED) return conv_halo_name(hp, true);
+  const Plan pl = plan_mfma(a);
+  if (halo && hp.t_us < pl.t_us) return conv_halo_name(hp, false);
   return kVariants[pl.variant].name;
 }
 
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream) {
-  const Plan pl = plan_mfma(a);
   HaloPlan hp;
-  if (plan_halo(a, &hp) && hp.t_us < pl.t_us) return launch_conv_halo(a, hp, stream);
+  const bool halo = plan_halo(a, &hp);
+  if (a.join_kind == IFQ_JOIN_CONV_FUSED)
+    return halo ? launch_conv_halo(a, hp, stream) : hipErrorNotSupported;
+  const Plan pl = plan_mfma(a);
+  if (halo && hp.t_us < pl.t_us) return launch_conv_halo(a, hp, stream);
   switch (pl.variant) {
     case 0: return launch_variant<2, 4, 1, 2, 4, 1, 6>(a, pl, stream);
     case 1: return launch_variant<2, 4, 1, 2, 2, 2, 4>(a, pl, stream);

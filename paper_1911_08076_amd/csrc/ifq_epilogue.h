@@ -37,7 +37,7 @@ __device__ __forceinline__ void stage_epilogue(const ConvLaunch& a, uint8_t* lds
   if (a.out_mode == 0) return;
   const int tid = threadIdx.x;
   const int nch = a.cout - co0 < bm ? a.cout - co0 : bm;
-  if (a.join_kind == IFQ_JOIN_CONV) {
+  if (a.join_kind == IFQ_JOIN_CONV || a.join_kind == IFQ_JOIN_CONV_FUSED) {
     double* qt = reinterpret_cast<double*>(lds);
 #pragma unroll
     for (int q = 0; q < IFQ_MAX_THRESHOLDS; ++q)

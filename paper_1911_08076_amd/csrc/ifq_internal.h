@@ -108,6 +108,12 @@ struct ConvLaunch {
   int64_t wzero;       // byte offset of the weight blob's zero block
   FastDiv div_howo;    // division by ho*wo (output pixel -> image)
   FastDiv div_wo;      // division by wo (pixel in image -> row)
+  // IFQ_JOIN_CONV_FUSED: the 1x1 downsample conv computed in this kernel
+  const uint8_t* dx;   // its input codes (BLOCK64)
+  const int8_t* dwgt;  // its packed weights (fragment order)
+  int64_t d_wzero;     // byte offset of its weight blob's zero block
+  int32_t d_cin, d_h, d_w, d_stride;
+  int32_t d_nk32;      // its K32 steps (2 * c_in / 64)
 };
 
 hipError_t launch_conv(const ConvLaunch& a, hipStream_t stream);
@@ -129,8 +135,13 @@ struct HaloPlan {
   double t_us;
 };
 bool plan_halo(const ConvLaunch& a, HaloPlan* out);
+// Whether a launch with a fused downsample (IFQ_JOIN_CONV_FUSED) is covered.
+inline bool fused_supported(const ConvLaunch& a) {
+  HaloPlan p;
+  return plan_halo(a, &p);
+}
 hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream);
-const char* conv_halo_name(const HaloPlan& p);
+const char* conv_halo_name(const HaloPlan& p, bool fused);
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream);
 const char* conv_mfma_name(const ConvLaunch& a);
 

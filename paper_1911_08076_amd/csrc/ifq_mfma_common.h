@@ -359,6 +359,38 @@ __device__ __forceinline__ void epilogue_idj_pk(const ConvLaunch& a, const uint8
   }
 }
 
+// Conv-join epilogue with both sums in registers (fused downsample): per
+// output z = fma(p, a, fma(q, d, cc)) in fp64 with the per-channel {p, q, cc}
+// staged at kJoinCoefOff, code = #{i : z > q_i} for the three quantizer
+// thresholds of 2-bit output, four codes packed per byte.
+template <int NB>
+__device__ __forceinline__ void epilogue_cjoin(const ConvLaunch& a, const uint8_t* lds,
+                                               const v16i (&acc)[NB], const v16i (&accd)[NB],
+                                               int wm, int h, int co0, int pl, uint8_t* otile,
+                                               int orow) {
+  const double q1 = a.qthr[0], q2 = a.qthr[1], q3 = a.qthr[2];
+  const double* cf = reinterpret_cast<const double*>(lds + kJoinCoefOff);
+#pragma unroll
+  for (int fm = 0; fm < NB; ++fm) {
+    const int cb = (wm * NB + fm) * 32;
+    if (co0 + cb >= a.cout) continue;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int cl = cb + 8 * b + 4 * h;
+      uint32_t byte = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const double* c = cf + 3 * (cl + i);
+        const double z = fma(c[0], (double)acc[fm][4 * b + i],
+                             fma(c[1], (double)accd[fm][4 * b + i], c[2]));
+        const uint32_t code = (uint32_t)(z > q1) + (uint32_t)(z > q2) + (uint32_t)(z > q3);
+        byte |= code << (2 * i);
+      }
+      otile[pl * orow + (cl >> 2)] = (uint8_t)byte;
+    }
+  }
+}
+
 // 16 two-bit codes (one 32-bit word of a cell) -> 16 int8 operand bytes.
 __device__ __forceinline__ v4i unpack2(uint32_t u) {
   return v4i{(int)(u & kLow2), (int)((u >> 2) & kLow2), (int)((u >> 4) & kLow2),

@@ -21,7 +21,7 @@ from . import _ffi, api
 from ._ffi import (Layer, Stack, IFQ_LAYER_CONV, IFQ_LAYER_POOL,
                    IFQ_LAYOUT_I8_NHWC, IFQ_LAYOUT_U2_NHWC_PACKED,
                    IFQ_LAYOUT_I32_NHWC, IFQ_LAYOUT_U2_BLOCK64, IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY,
-                   IFQ_JOIN_CONV, IFQ_POOL_VALID, IFQ_POOL_SAME)
+                   IFQ_JOIN_CONV, IFQ_JOIN_CONV_FUSED, IFQ_POOL_VALID, IFQ_POOL_SAME)
 
 
 def _is_conv(L):
@@ -44,14 +44,38 @@ class DeviceStack:
     are multiples of 64, else as "u2"). Other tensors use one byte per code;
     int32 sums stay int32. The stack input and output are NHWC codes on the
     host side either way (upload_input / download_output convert).
+    fuse_down: with "b64", compute each 1x1 downsample inside the conv join
+    that consumes it (IFQ_JOIN_CONV_FUSED); self.fused maps the join's layer
+    name to the downsample's, whose layer and output tensor are then absent.
     """
 
     def __init__(self, layers, params, batch, code_layout="i8",
-                 device="cuda"):
+                 device="cuda", fuse_down=False):
         import torch
         if code_layout not in ("i8", "u2", "b64"):
             raise ValueError("code_layout must be 'i8', 'u2' or 'b64'")
-        self.layers = list(layers)
+        all_layers = list(layers)
+        by_name = {L.name: (i, L) for i, L in enumerate(all_layers)}
+        # fuse_down (BLOCK64 codes): a 1x1 downsample whose int32 sums only a
+        # conv join reads runs inside that join's kernel (IFQ_JOIN_CONV_FUSED);
+        # its layer and its output tensor disappear from the stack
+        self.fused = {}
+        if fuse_down and code_layout == "b64":
+            for L in all_layers:
+                if not (_is_conv(L) and L.join is not None and L.join[0] == "conv"):
+                    continue
+                D = by_name[L.join[2]][1]
+                readers = [M for M in all_layers if M.name != L.name and
+                           (M.src == D.dst or (_is_conv(M) and M.join is not None
+                                               and M.join[1] == D.dst))]
+                if (not readers and D.k == 1 and D.pad == 0 and D.in_bits == 2 and
+                        D.cin % 64 == 0 and L.cout % 64 == 0 and L.k == 3 and
+                        L.pad == 1 and L.cin % 64 == 0 and L.out_bits == 2):
+                    self.fused[L.name] = D.name
+        skip = set(self.fused.values())
+        self._all_layers = all_layers
+        self.layers = [L for L in all_layers if L.name not in skip]
+        src_index = [by_name[L.name][0] for L in self.layers]
         self.batch = int(batch)
         self.device = torch.device(device)
         self._keep = []
@@ -78,7 +102,6 @@ class DeviceStack:
         self.input_bits = b0
         self.input_layout = layout_of["x"]
 
-        by_name = {L.name: (i, L) for i, L in enumerate(self.layers)}
         self.tensor_info = {"x": (self.input_shape, layout_of["x"], b0)}
         arr = (Layer * len(self.layers))()
         self.ops = 0
@@ -89,7 +112,7 @@ class DeviceStack:
             rec.join_src = -1
             in_layout = layout_of[L.src]
             if _is_conv(L):
-                p = params[i]
+                p = params[src_index[i]]
                 rec.kind = IFQ_LAYER_CONV
                 if L.out_bits == 0:
                     out_layout = IFQ_LAYOUT_I32_NHWC
@@ -124,6 +147,22 @@ class DeviceStack:
                         rec.join = api.make_join(IFQ_JOIN_IDENTITY,
                                                  layout_of[L.join[1]], None, None,
                                                  p["q_thr"], table=tdev)
+                    elif L.name in self.fused:
+                        D = by_name[self.fused[L.name]][1]
+                        pd = params[by_name[D.name][0]]
+                        coef = api.ifq_fold_join(IFQ_JOIN_CONV, p, pd["beta_in"],
+                                                 down=pd)
+                        cdev = torch.from_numpy(coef).to(self.device)
+                        dd = api.conv_desc(self.batch, D.h, D.w, D.cin, D.cout, D.k,
+                                           D.stride, D.pad, D.in_bits, 0,
+                                           layout_of[D.src], IFQ_LAYOUT_I32_NHWC)
+                        ddev = torch.from_numpy(api.ifq_pack_weights(dd, pd["w"])).to(
+                            self.device)
+                        self._keep += [cdev, ddev]
+                        rec.join = api.make_join(IFQ_JOIN_CONV_FUSED, layout_of[D.src],
+                                                 None, cdev, p["q_thr"], down_w=ddev,
+                                                 down=dd)
+                        self.ops += conv_ops(D, self.batch)
                     else:
                         pd = params[by_name[L.join[2]][0]]
                         coef = api.ifq_fold_join(IFQ_JOIN_CONV, p, pd["beta_in"],
@@ -132,7 +171,8 @@ class DeviceStack:
                         self._keep.append(cdev)
                         rec.join = api.make_join(IFQ_JOIN_CONV, layout_of[L.join[1]],
                                                  None, cdev, p["q_thr"])
-                    rec.join_src = sid(L.join[1])
+                    rec.join_src = (sid(by_name[self.fused[L.name]][1].src)
+                                    if L.name in self.fused else sid(L.join[1]))
                 self.ops += conv_ops(L, self.batch)
                 ho, wo = api.ifq_conv_output_dims(d)
                 out_shape = (self.batch, ho, wo, L.cout)
@@ -240,8 +280,16 @@ class DeviceStack:
         return out
 
     def layer_ops(self):
-        """Dense int-ops of every layer (0 for pools)."""
-        return [conv_ops(L, self.batch) if _is_conv(L) else 0 for L in self.layers]
+        """Dense int-ops of every layer (0 for pools; a conv with a fused
+        downsample counts both convs)."""
+        names = {L.name: L for L in self._all_layers}
+        out = []
+        for L in self.layers:
+            ops = conv_ops(L, self.batch) if _is_conv(L) else 0
+            if L.name in self.fused:
+                ops += conv_ops(names[self.fused[L.name]], self.batch)
+            out.append(ops)
+        return out
 
     # -- execution -------------------------------------------------------------
     def _slot_ptr(self, k, x, y):

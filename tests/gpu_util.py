@@ -51,11 +51,13 @@ def oracle_layer(L, x, p, shortcut=None, down=None):
 
 
 def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
-              sc_layout=I8, down=None, dump=True):
+              sc_layout=I8, down=None, dump=True, fused_down=None):
     """Run one conv through ifq_conv_forward; returns (acc or None, output).
 
     output is uint8 codes NHWC (packed [..., c/4] for U2, [n][c/64][h][w][16]
-    for B64) or int32 sums."""
+    for B64) or int32 sums. fused_down = (D, xin): a conv join whose 1x1
+    downsample layer D (params down) runs inside the kernel on the BLOCK64
+    codes xin (IFQ_JOIN_CONV_FUSED) instead of reading its sums."""
     import torch
     if out_layout is None:
         out_layout = I32 if L.out_bits == 0 else I8
@@ -83,6 +85,17 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
             keep += [scd, td_]
             join = P.make_join(P.IFQ_JOIN_IDENTITY, sc_layout, scd, None,
                                p["q_thr"], table=td_)
+        elif fused_down is not None:
+            D, xin = fused_down
+            coef = P.ifq_fold_join(P.IFQ_JOIN_CONV, p, down["beta_in"], down=down)
+            dd = P.conv_desc(n, D.h, D.w, D.cin, D.cout, D.k, D.stride, D.pad,
+                             D.in_bits, 0, B64, I32)
+            wdd = to_dev(P.ifq_pack_weights(dd, down["w"]))
+            xind = upload_codes(P, xin, B64)
+            cd = to_dev(coef)
+            keep += [wdd, xind, cd]
+            join = P.make_join(P.IFQ_JOIN_CONV_FUSED, B64, xind, cd, p["q_thr"],
+                               down_w=wdd, down=dd)
         else:
             coef = P.ifq_fold_join(P.IFQ_JOIN_CONV, p, down["beta_in"], down=down)
             scd = to_dev(shortcut.astype(np.int32))

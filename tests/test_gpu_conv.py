@@ -118,10 +118,10 @@ def test_conv_block64_bit_exact(P, case, io):
 # batches the oracle finishes in about a second; the test also pins which
 # kernel variant the planner takes for each.
 HALO_TILES = [
-    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_halo<8, 1, 6>"),
-    ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_halo<4, 2, 4>"),
-    ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_halo<2, 4, 4>"),
-    ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_halo<8, 1, 6>"),
+    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_halo<8, 1, 6, false>"),
+    ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_halo<4, 2, 4, false>"),
+    ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_halo<2, 4, 4, false>"),
+    ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_halo<8, 1, 6, false>"),
 ]
 
 
@@ -196,6 +196,31 @@ def test_conv_join_bit_exact(P, lay):
                          shortcut=want_d, down=pd)
     assert np.array_equal(acc, want_acc)
     assert np.array_equal(got, expect_layout(want, lay))
+
+
+# conv2 of a downsampling block with the 1x1/2 downsample computed inside the
+# conv kernel (IFQ_JOIN_CONV_FUSED): the shapes of the three ResNet-18
+# downsampling blocks at small batches (one variant each), plus ragged ones
+FUSED = [(2, 56, 64, 128), (3, 28, 128, 256), (2, 14, 256, 512), (1, 17, 128, 256),
+         (5, 13, 64, 128), (40, 28, 128, 256)]
+
+
+@pytest.mark.parametrize("shape", FUSED, ids=["x".join(map(str, f)) for f in FUSED])
+def test_fused_downsample_join_bit_exact(P, shape):
+    n, hin, cin, cout = shape
+    D = make_layer("down", hin, hin, cin, cout, 1, 2, 0, 2, 0)
+    ho = (hin - 1) // 2 + 1
+    L = make_layer("conv2", ho, ho, cout, cout, 3, 1, 1, join=("conv", "d", "down"))
+    pd = params_for(5 + hin, D)
+    p = params_for(6 + hin, L)
+    xin = codes_for(5 + hin, (n, hin, hin, cin), 2)
+    x = codes_for(6 + hin, (n, ho, ho, cout), 2)
+    want_d, _ = oracle_layer(D, xin, pd)
+    want_acc, want = oracle_layer(L, x, p, shortcut=want_d, down=pd)
+    acc, got = gpu_layer(P, L, n, x, p, in_layout=B64, out_layout=B64, down=pd,
+                         fused_down=(D, xin))
+    assert np.array_equal(acc, want_acc)
+    assert np.array_equal(got, expect_layout(want, B64))
 
 
 def test_conv_without_dump_and_determinism(P):

@@ -40,7 +40,12 @@ def check_stack(P, cfg, batch, layout, variant):
     import torch
     params, x, want = oracle_run(cfg, batch, variant)
     layers = get_stack(cfg).layers
-    dev = P.DeviceStack(layers, params, batch, code_layout=layout)
+    fuse = layout == "b64f"
+    dev = P.DeviceStack(layers, params, batch, code_layout="b64" if fuse else layout,
+                        fuse_down=fuse)
+    if fuse:
+        # every downsample of a ResNet-shaped stack is folded into its join
+        assert len(dev.fused) == sum(1 for L in layers if L.name.endswith(".down"))
     xd = dev.upload_input(x)
     y = dev.alloc_output()
     dev.run(xd, y)
@@ -71,7 +76,7 @@ def check_stack(P, cfg, batch, layout, variant):
 SMALL = [(0, 1), (1, 2), (2, 1), (3, 2), (4, 1)]
 
 
-@pytest.mark.parametrize("layout", ["i8", "u2", "b64"])
+@pytest.mark.parametrize("layout", ["i8", "u2", "b64", "b64f"])
 @pytest.mark.parametrize("cfg,batch", SMALL)
 def test_stack_small_batch(P, cfg, batch, layout):
     for variant in ("calibrated", "plain"):
@@ -84,3 +89,10 @@ def test_stack_small_batch(P, cfg, batch, layout):
 def test_stack_full_size(P, cfg, layout):
     batch = get_stack(cfg).batch
     check_stack(P, cfg, batch, layout, "plain")
+
+
+@pytest.mark.slow
+def test_stack_full_size_fused_downsample(P):
+    # the benchmark's configuration: ResNet-18 body, batch 64, BLOCK64 codes,
+    # downsample convs inside their joins
+    check_stack(P, 3, get_stack(3).batch, "b64f", "plain")
