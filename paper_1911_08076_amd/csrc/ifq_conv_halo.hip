@@ -42,27 +42,32 @@ namespace ifq {
 namespace {
 
 constexpr int kHaloNW = 8;     // waves per workgroup
-constexpr int kHaloFM = 4;     // 32-row blocks per wave
-constexpr int kHaloBM = 128;   // output channels per workgroup
 constexpr int kTaps = 9;
 
-// Cells of one halo buffer for WK wave groups (2 buffers per group).
-__host__ __device__ constexpr int halo_cap_cells(int wk) {
-  return wk == 1 ? 1280 : wk == 2 ? 512 : 192;
+// Cells of one halo buffer (2 buffers per wave group) for WK wave groups and
+// FM 32-row blocks per wave (FM = 2: two workgroups share a CU).
+__host__ __device__ constexpr int halo_cap_cells(int wk, int fm) {
+  return fm == 2 ? 1024 : wk == 1 ? 1280 : wk == 2 ? 512 : 192;
 }
 
 __host__ __device__ constexpr int round64(int v) { return (v + 63) & ~63; }
 
-template <int WN, int WK, int D, bool FUSED>
-__global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
+template <int WN, int WK, int D, bool FUSED, int FM>
+__global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) {
   static_assert(WN * WK == kHaloNW, "8 waves");
-  constexpr int FM = kHaloFM, BM = kHaloBM, BN = 32 * WN;
+  static_assert(FM == 4 || (FM == 2 && !FUSED), "fused downsample needs FM = 4");
+  constexpr int BM = 32 * FM, BN = 32 * WN;
   constexpr int A_STEP = BM * 64;                 // one K64 step of weights
   constexpr int STAGE = WK * A_STEP;
-  constexpr int CPW = WK + 1;                     // loads per wave per stage
+  // weight chunks (1 KB) per stage: 2*FM per group; wave w takes chunks
+  // w + 8k, k < CPWA (dummy loads where that runs past the stage)
+  constexpr int NCH = 2 * FM * WK;
+  constexpr int CPWA = NCH > kHaloNW ? NCH / kHaloNW : 1;
+  static_assert(NCH % kHaloNW == 0 || NCH < kHaloNW, "weight chunks per wave");
+  constexpr int CPW = CPWA + 1;                   // loads per wave per stage
   static_assert((D - 3) * CPW <= 63, "vmcnt range");
   static_assert(D >= 3 && D <= 10, "halo window");
-  constexpr int HCAP = halo_cap_cells(WK);
+  constexpr int HCAP = halo_cap_cells(WK, FM);
   constexpr int HSTRIDE = HCAP * 16 + 16;         // buffer + its zero cell
   constexpr int RING = D * STAGE;
   constexpr int HALO0 = RING;
@@ -217,12 +222,11 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
     if (hs_real[r]) chunk(q, hs_src[r], hs_dst[r]);
   }
 
-  // ---- weights: wave w loads row block w/2, K32 half w%2 of each group's
-  // K64 step: 1 KB at ((rbw + rb) * nk32 + 2*kk + t) * 1024 ----------------
-  const int rb_w = wave >> 1, t_w = wave & 1;
+  // ---- weights: chunk c of a stage is group c / (2*FM)'s row block
+  // (c % (2*FM)) / 2, K32 half c % 2 of its K64 step: 1 KB at
+  // ((rbw + rb) * nk32 + 2*kk + t) * 1024 -------------------------------------
   const int nrb = a.cout_pad >> 5;
   const int rbw = co0 >> 5;
-  const bool wrow_ok = rbw + rb_w < nrb;
   const uint8_t* wbase = reinterpret_cast<const uint8_t*>(a.wgt);
   const int nk32 = 2 * a.nk;
   const uint32_t voff = (uint32_t)lane * 16;
@@ -230,11 +234,18 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
     const int gi = stg / kTaps;
     const uint32_t slot = lds0 + (uint32_t)((stg % D) * STAGE);
 #pragma unroll
-    for (int i = 0; i < WK; ++i) {
-      const int kk = (gi * WK + i) * kTaps + tap;
-      const int64_t off =
-          wrow_ok ? ((int64_t)(rbw + rb_w) * nk32 + 2 * kk + t_w) * 1024 : a.wzero;
-      dma16s(wbase + off, voff, slot + (uint32_t)(i * A_STEP + (rb_w * 2 + t_w) * 1024));
+    for (int k = 0; k < CPWA; ++k) {
+      const int c = wave + kHaloNW * k;
+      if (NCH >= kHaloNW || c < NCH) {
+        const int i = c / (2 * FM), cc = c - i * 2 * FM;
+        const int rb = cc >> 1, t = cc & 1;
+        const int kk = (gi * WK + i) * kTaps + tap;
+        const int64_t off =
+            rbw + rb < nrb ? ((int64_t)(rbw + rb) * nk32 + 2 * kk + t) * 1024 : a.wzero;
+        dma16s(wbase + off, voff, slot + (uint32_t)(i * A_STEP + cc * 1024));
+      } else {
+        dma16(zero_src, lds0 + DUMMY);
+      }
     }
   };
 
@@ -293,7 +304,7 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
     dma16(c < a.cout ? reinterpret_cast<const uint8_t*>(a.thr + (int64_t)c * 4) : zero_src,
           lds0 + THR + wave * 1024);
   }
-  if (tbl_pre) {   // 16 channels x 64 B per wave
+  if (tbl_pre && wave < BM / 16) {   // 16 channels x 64 B per wave
     const int c = co0 + wave * 16 + (lane >> 2);
     dma16(c < a.cout ? reinterpret_cast<const uint8_t*>(a.table + (int64_t)c * 16 + (lane & 3) * 4)
                      : zero_src,
@@ -521,17 +532,20 @@ __global__ __launch_bounds__(512) void conv_halo(ConvLaunch a) {
 // Variants and per-layer planning
 // ---------------------------------------------------------------------------
 struct HaloVariant {
-  int wn, wk, d;   // waves along pixels, K groups, ring stages
-  double c0_us;   // fixed cost of one round of workgroups
-  double eff;     // MFMA efficiency of the main loop
-  const char* name;
+  int wn, wk, d, fm;   // waves along pixels, K groups, ring stages, row blocks per wave
+  double c0_us;        // fixed cost of one round of workgroups
+  double eff;          // MFMA efficiency of the main loop
+  const char* name;    // the unfused kernel, as a profiler lists it
+  const char* fused_name;
 };
 
-// Index order must match the switch in launch_conv_halo.
+// Index order must match the switch in launch_conv_halo. Variants with
+// fm = 2 (64 output channels) run two workgroups per CU.
 const HaloVariant kHaloVariants[] = {
-    {8, 1, 6, 4.0, 0.75, "conv_halo<8, 1, 6, false>"},   // 128 x 256
-    {4, 2, 4, 4.0, 0.75, "conv_halo<4, 2, 4, false>"},   // 128 x 128, K split 2
-    {2, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4, false>"},   // 128 x 64, K split 4
+    {8, 1, 6, 4, 4.0, 0.75, "conv_halo<8, 1, 6, false, 4>", "conv_halo<8, 1, 6, true, 4>"},
+    {4, 2, 4, 4, 4.0, 0.75, "conv_halo<4, 2, 4, false, 4>", "conv_halo<4, 2, 4, true, 4>"},
+    {2, 4, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4, false, 4>", "conv_halo<2, 4, 4, true, 4>"},
+    {8, 1, 6, 2, 4.0, 0.75, "conv_halo<8, 1, 6, false, 2>", nullptr},   // 64 x 256
 };
 constexpr int kNumHalo = sizeof(kHaloVariants) / sizeof(kHaloVariants[0]);
 constexpr int kNumCUs = 256;
@@ -568,29 +582,33 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
   for (int v = 0; v < kNumHalo; ++v) {
     const HaloVariant& V = kHaloVariants[v];
     if (G % V.wk) continue;
-    const int bnmax = 32 * V.wn;
+    const int bm = 32 * V.fm, bnmax = 32 * V.wn;
+    const int occ = V.fm == 2 ? 2 : 1;               // workgroups per CU
+    const int cap = halo_cap_cells(V.wk, V.fm);
     if (fused) {
       // the downsample's K64 steps split one per group; its input chunks
       // (one per wave) fit the spare halo buffers
       const int gd = a.d_cin / 64, nqd = gd * bnmax / 64;
-      if (gd != V.wk || nqd > kHaloNW || nqd > V.wk * (halo_cap_cells(V.wk) / 64)) continue;
+      if (!V.fused_name || gd != V.wk || nqd > kHaloNW || nqd > V.wk * (cap / 64)) continue;
     }
-    const int64_t nco = (a.cout + kHaloBM - 1) / kHaloBM;
+    const int64_t slots = (int64_t)kNumCUs * occ;
+    const int64_t nco = (a.cout + bm - 1) / bm;
     const int64_t nb_min = (a.m + bnmax - 1) / bnmax;
-    const int64_t rounds = (nco * nb_min + kNumCUs - 1) / kNumCUs;
-    int64_t nb = rounds * kNumCUs / nco;
+    const int64_t rounds = (nco * nb_min + slots - 1) / slots;
+    int64_t nb = rounds * slots / nco;
     if (nb < nb_min) nb = nb_min;
     int64_t bn = (a.m + nb - 1) / nb;
     bn = (bn + 31) / 32 * 32;
     if (bn > bnmax) bn = bnmax;
     const int64_t cells = halo_cells_bound(a, bn);
-    if (cells > halo_cap_cells(V.wk)) continue;
+    if (cells > cap) continue;
     const int nr = 11 - V.d < kTaps ? 11 - V.d : kTaps;
     if (V.wk * (cells / 64) > kHaloNW * nr) continue;
     const int64_t blocks = nco * ((a.m + bn - 1) / bn);
-    const double tile_ops = 2.0 * kHaloBM * bnmax * (double)a.kpad;
-    const double t = (double)((blocks + kNumCUs - 1) / kNumCUs) *
-                     (V.c0_us + tile_ops / (kCuOpsPerUs * V.eff));
+    // occ workgroups share a CU: each runs at 1/occ of its MFMA rate
+    const double tile_ops = 2.0 * bm * bnmax * (double)a.kpad;
+    const double t = (double)((blocks + slots - 1) / slots) *
+                     (V.c0_us + tile_ops * occ / (kCuOpsPerUs * V.eff));
     if (t < best_t) {
       best_t = t;
       *out = HaloPlan{v, (int)bn, (int)((a.m + bn - 1) / bn), t};
@@ -602,22 +620,23 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
 
 // The kernel's name as a profiler lists it (the template arguments).
 const char* conv_halo_name(const HaloPlan& p, bool fused) {
-  static const char* const kFused[] = {"conv_halo<8, 1, 6, true>", "conv_halo<4, 2, 4, true>",
-                                       "conv_halo<2, 4, 4, true>"};
-  return fused ? kFused[p.variant] : kHaloVariants[p.variant].name;
+  return fused ? kHaloVariants[p.variant].fused_name : kHaloVariants[p.variant].name;
 }
 
 hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream) {
   a.bn = p.bn;
-  const dim3 grid(p.blocks_m, (a.cout + kHaloBM - 1) / kHaloBM);
+  const int bm = 32 * kHaloVariants[p.variant].fm;
+  const dim3 grid(p.blocks_m, (a.cout + bm - 1) / bm);
   const bool fused = a.join_kind == IFQ_JOIN_CONV_FUSED;
   switch (p.variant * 2 + (fused ? 1 : 0)) {
-    case 0: hipLaunchKernelGGL((conv_halo<8, 1, 6, false>), grid, dim3(512), 0, stream, a); break;
-    case 1: hipLaunchKernelGGL((conv_halo<8, 1, 6, true>), grid, dim3(512), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((conv_halo<4, 2, 4, false>), grid, dim3(512), 0, stream, a); break;
-    case 3: hipLaunchKernelGGL((conv_halo<4, 2, 4, true>), grid, dim3(512), 0, stream, a); break;
-    case 4: hipLaunchKernelGGL((conv_halo<2, 4, 4, false>), grid, dim3(512), 0, stream, a); break;
-    default: hipLaunchKernelGGL((conv_halo<2, 4, 4, true>), grid, dim3(512), 0, stream, a); break;
+    case 0: hipLaunchKernelGGL((conv_halo<8, 1, 6, false, 4>), grid, dim3(512), 0, stream, a); break;
+    case 1: hipLaunchKernelGGL((conv_halo<8, 1, 6, true, 4>), grid, dim3(512), 0, stream, a); break;
+    case 2: hipLaunchKernelGGL((conv_halo<4, 2, 4, false, 4>), grid, dim3(512), 0, stream, a); break;
+    case 3: hipLaunchKernelGGL((conv_halo<4, 2, 4, true, 4>), grid, dim3(512), 0, stream, a); break;
+    case 4: hipLaunchKernelGGL((conv_halo<2, 4, 4, false, 4>), grid, dim3(512), 0, stream, a); break;
+    case 5: hipLaunchKernelGGL((conv_halo<2, 4, 4, true, 4>), grid, dim3(512), 0, stream, a); break;
+    case 6: hipLaunchKernelGGL((conv_halo<8, 1, 6, false, 2>), grid, dim3(512), 0, stream, a); break;
+    default: return hipErrorInvalidValue;   // no fused kernel for this variant
   }
   return hipGetLastError();
 }

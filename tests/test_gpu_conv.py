@@ -118,10 +118,11 @@ def test_conv_block64_bit_exact(P, case, io):
 # batches the oracle finishes in about a second; the test also pins which
 # kernel variant the planner takes for each.
 HALO_TILES = [
-    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_halo<8, 1, 6, false>"),
-    ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_halo<4, 2, 4, false>"),
-    ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_halo<2, 4, 4, false>"),
-    ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_halo<8, 1, 6, false>"),
+    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_halo<8, 1, 6, false, 4>"),
+    ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_halo<4, 2, 4, false, 4>"),
+    ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_halo<2, 4, 4, false, 4>"),
+    ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_halo<8, 1, 6, false, 4>"),
+    ("halo_l1_b24", 24, 56, 56, 64, 64, 1, "conv_halo<8, 1, 6, false, 2>"),
 ]
 
 
@@ -174,6 +175,23 @@ def test_identity_join_bit_exact(P, shape, io):
                          shortcut=sc, sc_layout=sc_l)
     assert np.array_equal(acc, want_acc)
     assert np.array_equal(got, expect_layout(want, out_l))
+
+
+def test_identity_join_64_channel_variant(P):
+    # the ResNet-18 l1 conv2 shape at batch 24 runs the 64-channel variant
+    # (two workgroups per CU) with an identity join
+    n, h, c = 24, 56, 64
+    d = P.conv_desc(n, h, h, c, c, 3, 1, 1, 2, 2, B64, B64)
+    assert P.ifq_conv_kernel_name(d) == "conv_halo<8, 1, 6, false, 2>"
+    L = make_layer("join_id", h, h, c, c, 3, 1, 1, join=("identity", "s"))
+    p = params_for(41, L)
+    x = codes_for(41, (n, h, h, c), 2)
+    sc = codes_for(42, (n, h, h, c), 2)
+    want_acc, want = oracle_layer(L, x, p, shortcut=sc)
+    acc, got = gpu_layer(P, L, n, x, p, in_layout=B64, out_layout=B64, shortcut=sc,
+                         sc_layout=B64)
+    assert np.array_equal(acc, want_acc)
+    assert np.array_equal(got, expect_layout(want, B64))
 
 
 @pytest.mark.parametrize("lay", [I8, U2, B64], ids=["i8", "u2", "b64"])
