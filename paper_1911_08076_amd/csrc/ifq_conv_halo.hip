@@ -282,7 +282,8 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
   const bool dreal = fused && wave * 64 < Gd * BN;
   auto issue_down = [&]() {
     const uint32_t slot = lds0 + (uint32_t)((nst % D) * STAGE);
-    const int j = wave / (2 * Gd), k32 = wave - j * 2 * Gd;
+    const int gd2 = fused ? 2 * Gd : 1;   // (Gd is 0 in the unfused kernels)
+    const int j = wave / gd2, k32 = wave - j * gd2;
 #pragma unroll
     for (int i = 0; i < WK; ++i) {
       const int rb = rbw + i * (FM / WK) + j;
