@@ -348,11 +348,12 @@ IFQ_API ifq_status ifq_fold_join_table(const ifq_join_params* p, int32_t in_bits
                                        const double* q_thr, int32_t* table_out);
 
 /*
- * Name of the kernel variant ifq_conv_forward launches for d (static string,
- * the kernel's symbol as a profiler lists it), or "" for an invalid desc.
- * Host; for profiling and benchmarks.
+ * Name of the kernel variant ifq_conv_forward launches for d with join
+ * (nullable: no join; only its kind and descriptors are read, no pointer is
+ * dereferenced), as a static string: the kernel's symbol as a profiler lists
+ * it, or "" for an invalid desc. Host; for profiling and benchmarks.
  */
-IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d);
+IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d, const ifq_join* join);
 
 /* Device workspace bytes ifq_conv_forward needs for d (may be 0). Host. */
 IFQ_API size_t ifq_conv_workspace_bytes(const ifq_conv_desc* d);

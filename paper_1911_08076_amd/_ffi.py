@@ -101,7 +101,7 @@ SIGNATURES = [
     ("ifq_fold_join", i32, [ctypes.POINTER(JoinParams), vp]),
     ("ifq_fold_join_table", i32, [ctypes.POINTER(JoinParams), i32, i64, i32, i32,
                                   vp, vp]),
-    ("ifq_conv_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc)]),
+    ("ifq_conv_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc), ctypes.POINTER(Join)]),
     ("ifq_conv_workspace_bytes", size_t, [ctypes.POINTER(ConvDesc)]),
     ("ifq_conv_forward", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp,
                                ctypes.POINTER(Join), vp, vp, vp, size_t, vp]),

@@ -176,8 +176,9 @@ def make_join(kind, layout, shortcut, coef, q_thr, table=None, down_w=None,
     return j
 
 
-def ifq_conv_kernel_name(desc):
-    return _lib().ifq_conv_kernel_name(ctypes.byref(desc)).decode()
+def ifq_conv_kernel_name(desc, join=None):
+    return _lib().ifq_conv_kernel_name(
+        ctypes.byref(desc), ctypes.byref(join) if join is not None else None).decode()
 
 
 def ifq_conv_workspace_bytes(desc):

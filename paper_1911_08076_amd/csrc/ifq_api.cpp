@@ -607,11 +607,11 @@ IFQ_API ifq_status ifq_fold_join_table(const ifq_join_params* p, int32_t in_bits
   return ok();
 }
 
-IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d) {
+IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d, const ifq_join* join) {
   int64_t ho, wo;
   if (check_conv(d, &ho, &wo) != IFQ_OK) return "";
-  const ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr,
-                                        nullptr, nullptr, nullptr, nullptr);
+  const ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, join,
+                                        nullptr, nullptr, nullptr);
   return ifq::conv_kernel_name(a);
 }
 

@@ -52,10 +52,15 @@ __host__ __device__ constexpr int halo_cap_cells(int wk, int fm) {
 
 __host__ __device__ constexpr int round64(int v) { return (v + 63) & ~63; }
 
-template <int WN, int WK, int D, bool FUSED, int FM>
+// SW: the MFMAs take the codes as A and the weights as B, so the sums come
+// out transposed (one channel per lane; see the transposed epilogues of
+// ifq_mfma_common.h). Those kernels serve the 2-bit threshold epilogue and
+// the fused downsample join only.
+template <int WN, int WK, int D, bool FUSED, int FM, bool SW>
 __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) {
   static_assert(WN * WK == kHaloNW, "8 waves");
   static_assert(FM == 4 || (FM == 2 && !FUSED), "fused downsample needs FM = 4");
+  static_assert(!FUSED || SW, "the fused join runs on the transposed layout");
   constexpr int BM = 32 * FM, BN = 32 * WN;
   constexpr int A_STEP = BM * 64;                 // one K64 step of weights
   constexpr int STAGE = WK * A_STEP;
@@ -350,8 +355,12 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
     for (int t = 0; t < 2; ++t) {
       const v4i bf = unpack2((uint32_t)F.braw[t]);
 #pragma unroll
-      for (int fm = 0; fm < FM; ++fm)
-        acc[fm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(F.af[t][fm], bf, acc[fm], 0, 0, 0);
+      for (int fm = 0; fm < FM; ++fm) {
+        if constexpr (SW)
+          acc[fm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(bf, F.af[t][fm], acc[fm], 0, 0, 0);
+        else
+          acc[fm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(F.af[t][fm], bf, acc[fm], 0, 0, 0);
+      }
     }
   };
 
@@ -426,7 +435,7 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
         for (int j = 0; j < OWN; ++j) {
           const v4i af = *reinterpret_cast<const v4i*>(
               as + (j * 2 * Gd + 2 * g + t) * 1024 + lane * 16);
-          accd[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af, bf, accd[j], 0, 0, 0);
+          accd[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(bf, af, accd[j], 0, 0, 0);
         }
       }
     }
@@ -472,7 +481,10 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
     __syncthreads();
   }
 
-  if (pk)
+  if constexpr (SW) {
+    // thresholds stay as raw records at THR; the join stages its coefficients
+    if (FUSED) stage_epilogue(a, lds, co0, BM);
+  } else if (pk)
     stage_thr_pk(reinterpret_cast<const int4*>(lds + THR), lds, BM);
   else if (pk_idj)
     stage_idj_pk(tbl_pre ? reinterpret_cast<const int32_t*>(lds + THR) : a.table + co0 * 16,
@@ -483,7 +495,14 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
   const int orow = a.out_mode == 2 ? BM / 4 : BM;
   uint8_t* otile = lds + EPI_BYTES;
   const int pl = wn * 32 + l32;
-  {
+  if constexpr (SW) {
+    if (a.acc_dump) dump_acc_t<OWN>(a, own, kg, h, l32, co0, p0, wn * 32, bn, a.acc_dump);
+    if constexpr (FUSED)
+      epilogue_cjoin_t<OWN>(a, lds, own, accd, kg, h, l32, co0, wn * 32, otile, orow);
+    else
+      epilogue_thr_pk_t<OWN>(a, reinterpret_cast<const int4*>(lds + THR), own, kg, h, l32, co0,
+                             wn * 32, otile, orow);
+  } else {
     v16i own2[OWN][1];
 #pragma unroll
     for (int j = 0; j < OWN; ++j) own2[j][0] = own[j];
@@ -492,9 +511,7 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
     if (a.acc_dump)
       epilogue32<kE32I32, OWN, 1>(a, lds, own2, kg, wn, h, l32, co0, p0, bn, otile, orow,
                                   a.acc_dump);
-    if (FUSED) {
-      epilogue_cjoin<OWN>(a, lds, own, accd, kg, h, co0, pl, otile, orow);
-    } else if (pk) {
+    if (pk) {
       epilogue_thr_pk<OWN>(a, lds, own, kg, h, co0, pl, otile, orow);
     } else if (pk_idj) {
       // shortcut codes of the row blocks this wave finishes (loading them
@@ -536,17 +553,22 @@ struct HaloVariant {
   int wn, wk, d, fm;   // waves along pixels, K groups, ring stages, row blocks per wave
   double c0_us;        // fixed cost of one round of workgroups
   double eff;          // MFMA efficiency of the main loop
-  const char* name;    // the unfused kernel, as a profiler lists it
-  const char* fused_name;
+  const char* name;    // the kernels as a profiler lists them: unfused,
+  const char* sw_name;       // unfused on the transposed layout,
+  const char* fused_name;    // fused downsample (transposed layout)
 };
 
 // Index order must match the switch in launch_conv_halo. Variants with
 // fm = 2 (64 output channels) run two workgroups per CU.
 const HaloVariant kHaloVariants[] = {
-    {8, 1, 6, 4, 4.0, 0.75, "conv_halo<8, 1, 6, false, 4>", "conv_halo<8, 1, 6, true, 4>"},
-    {4, 2, 4, 4, 4.0, 0.75, "conv_halo<4, 2, 4, false, 4>", "conv_halo<4, 2, 4, true, 4>"},
-    {2, 4, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4, false, 4>", "conv_halo<2, 4, 4, true, 4>"},
-    {8, 1, 6, 2, 4.0, 0.75, "conv_halo<8, 1, 6, false, 2>", nullptr},   // 64 x 256
+    {8, 1, 6, 4, 4.0, 0.75, "conv_halo<8, 1, 6, false, 4, false>", "conv_halo<8, 1, 6, false, 4, true>",
+     "conv_halo<8, 1, 6, true, 4, true>"},
+    {4, 2, 4, 4, 4.0, 0.75, "conv_halo<4, 2, 4, false, 4, false>", "conv_halo<4, 2, 4, false, 4, true>",
+     "conv_halo<4, 2, 4, true, 4, true>"},
+    {2, 4, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4, false, 4, false>", "conv_halo<2, 4, 4, false, 4, true>",
+     "conv_halo<2, 4, 4, true, 4, true>"},
+    {8, 1, 6, 2, 4.0, 0.75, "conv_halo<8, 1, 6, false, 2, false>", "conv_halo<8, 1, 6, false, 2, true>",
+     nullptr},   // 64 x 256
 };
 constexpr int kNumHalo = sizeof(kHaloVariants) / sizeof(kHaloVariants[0]);
 constexpr int kNumCUs = 256;
@@ -619,24 +641,42 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
   return found;
 }
 
+// Which instance of a variant runs: 0 = unfused, 1 = unfused on the
+// transposed layout (the 2-bit threshold epilogue with packed 16-bit
+// compares, the same condition as the kernel's pk), 2 = fused downsample.
+int halo_instance(const ConvLaunch& a) {
+  if (a.join_kind == IFQ_JOIN_CONV_FUSED) return 2;
+  const bool pk = a.out_mode == 2 && a.rec == 4 && (a.cout & 31) == 0 &&
+                  27 * a.cin <= 32766 && a.join_kind == IFQ_JOIN_NONE;
+  return pk ? 1 : 0;
+}
+
 // The kernel's name as a profiler lists it (the template arguments).
-const char* conv_halo_name(const HaloPlan& p, bool fused) {
-  return fused ? kHaloVariants[p.variant].fused_name : kHaloVariants[p.variant].name;
+const char* conv_halo_name(const HaloPlan& p, const ConvLaunch& a) {
+  const HaloVariant& V = kHaloVariants[p.variant];
+  const int inst = halo_instance(a);
+  return inst == 2 ? V.fused_name : inst == 1 ? V.sw_name : V.name;
 }
 
 hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream) {
   a.bn = p.bn;
   const int bm = 32 * kHaloVariants[p.variant].fm;
   const dim3 grid(p.blocks_m, (a.cout + bm - 1) / bm);
-  const bool fused = a.join_kind == IFQ_JOIN_CONV_FUSED;
-  switch (p.variant * 2 + (fused ? 1 : 0)) {
-    case 0: hipLaunchKernelGGL((conv_halo<8, 1, 6, false, 4>), grid, dim3(512), 0, stream, a); break;
-    case 1: hipLaunchKernelGGL((conv_halo<8, 1, 6, true, 4>), grid, dim3(512), 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((conv_halo<4, 2, 4, false, 4>), grid, dim3(512), 0, stream, a); break;
-    case 3: hipLaunchKernelGGL((conv_halo<4, 2, 4, true, 4>), grid, dim3(512), 0, stream, a); break;
-    case 4: hipLaunchKernelGGL((conv_halo<2, 4, 4, false, 4>), grid, dim3(512), 0, stream, a); break;
-    case 5: hipLaunchKernelGGL((conv_halo<2, 4, 4, true, 4>), grid, dim3(512), 0, stream, a); break;
-    case 6: hipLaunchKernelGGL((conv_halo<8, 1, 6, false, 2>), grid, dim3(512), 0, stream, a); break;
+  switch (p.variant * 3 + halo_instance(a)) {
+#define IFQ_HALO_CASE(k, wn, wk, d, fu, fm, sw) \
+    case k: hipLaunchKernelGGL((conv_halo<wn, wk, d, fu, fm, sw>), grid, dim3(512), 0, stream, a); break;
+    IFQ_HALO_CASE(0, 8, 1, 6, false, 4, false)
+    IFQ_HALO_CASE(1, 8, 1, 6, false, 4, true)
+    IFQ_HALO_CASE(2, 8, 1, 6, true, 4, true)
+    IFQ_HALO_CASE(3, 4, 2, 4, false, 4, false)
+    IFQ_HALO_CASE(4, 4, 2, 4, false, 4, true)
+    IFQ_HALO_CASE(5, 4, 2, 4, true, 4, true)
+    IFQ_HALO_CASE(6, 2, 4, 4, false, 4, false)
+    IFQ_HALO_CASE(7, 2, 4, 4, false, 4, true)
+    IFQ_HALO_CASE(8, 2, 4, 4, true, 4, true)
+    IFQ_HALO_CASE(9, 8, 1, 6, false, 2, false)
+    IFQ_HALO_CASE(10, 8, 1, 6, false, 2, true)
+#undef IFQ_HALO_CASE
     default: return hipErrorInvalidValue;   // no fused kernel for this variant
   }
   return hipGetLastError();

@@ -381,9 +381,9 @@ bool mfma_eligible(const ConvLaunch& a) {
 const char* conv_mfma_name(const ConvLaunch& a) {
   HaloPlan hp;
   const bool halo = plan_halo(a, &hp);
-  if (halo && a.join_kind == IFQ_JOIN_CONV_FUSED) return conv_halo_name(hp, true);
+  if (halo && a.join_kind == IFQ_JOIN_CONV_FUSED) return conv_halo_name(hp, a);
   const Plan pl = plan_mfma(a);
-  if (halo && hp.t_us < pl.t_us) return conv_halo_name(hp, false);
+  if (halo && hp.t_us < pl.t_us) return conv_halo_name(hp, a);
   return kVariants[pl.variant].name;
 }
 

@@ -141,7 +141,7 @@ inline bool fused_supported(const ConvLaunch& a) {
   return plan_halo(a, &p);
 }
 hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream);
-const char* conv_halo_name(const HaloPlan& p, bool fused);
+const char* conv_halo_name(const HaloPlan& p, const ConvLaunch& a);
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream);
 const char* conv_mfma_name(const ConvLaunch& a);
 

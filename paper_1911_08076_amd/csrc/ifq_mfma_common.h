@@ -391,6 +391,107 @@ __device__ __forceinline__ void epilogue_cjoin(const ConvLaunch& a, const uint8_
   }
 }
 
+// ---- Epilogues for the transposed accumulator layout --------------------
+// With the codes as the MFMA's A operand and the weights as B, a lane
+// (h, l32) holds per 32x32 block ONE output channel (column l32) for the 16
+// pixel rows 8b + 4h + i (register v = 4b + i) of its wave's 32-pixel column.
+// Its channel's thresholds or join coefficients are read once per block, not
+// once per output; the four channels of an output byte are the four lanes of
+// an aligned quad, merged with two DPP ORs, and lane t = l32 & 3 of the quad
+// stores the byte of pixel row 8b + 4h + t.
+
+// OR of w over the four lanes of the lane's quad (every lane gets it).
+__device__ __forceinline__ uint32_t quad_or(uint32_t w) {
+  w |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w, 0xB1, 0xF, 0xF, false);  // lane ^ 1
+  w |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)w, 0x4E, 0xF, 0xF, false);  // lane ^ 2
+  return w;
+}
+
+__device__ __forceinline__ uint32_t pk2_i16(int v) { return ((uint32_t)v & 0xFFFFu) * 0x10001u; }
+
+// Threshold epilogue (2-bit codes, c_out % 32 == 0, 27 * c_in <= 32766) from
+// the raw {s, T1, T2, T3} records of the tile's channels (recs[c - co0]),
+// with the same packed 16-bit compare and sign flip as epilogue_thr_pk.
+template <int NB>
+__device__ __forceinline__ void epilogue_thr_pk_t(const ConvLaunch& a, const int4* recs,
+                                                  const v16i (&acc)[NB], int wm, int h,
+                                                  int l32, int co0, int pl0, uint8_t* otile,
+                                                  int orow) {
+  const int t = l32 & 3;
+  const int bsel = ((t & 1) << 1) | (t >> 1);    // byte of pixel t in the merged word
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int cb = (wm * NB + j) * 32;
+    if (co0 + cb >= a.cout) continue;
+    const int cl = cb + l32;
+    const int4 r = recs[cl];
+    const bool flip = r.x < 0;
+    const uint32_t w1 = pk2_i16(flip ? -r.y - 1 : r.y);
+    const uint32_t w2 = pk2_i16(flip ? -r.z - 1 : r.z);
+    const uint32_t w3 = pk2_i16(flip ? -r.w - 1 : r.w);
+    const uint32_t xm = flip ? 0x03030303u : 0u;
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const s16x2 p01 = __builtin_amdgcn_cvt_pk_i16(acc[j][4 * b], acc[j][4 * b + 1]);
+      const s16x2 p23 = __builtin_amdgcn_cvt_pk_i16(acc[j][4 * b + 2], acc[j][4 * b + 3]);
+      // codes of pixels 0 and 1 in the halves of c01, 2 and 3 in c23: the
+      // word's bytes are pixels 0, 2, 1, 3
+      const uint32_t c01 = count3_pk(p01, w1, w2, w3);
+      const uint32_t c23 = count3_pk(p23, w1, w2, w3);
+      const uint32_t w = quad_or(((c01 | (c23 << 8)) ^ xm) << (2 * t));
+      otile[(pl0 + 8 * b + 4 * h + t) * orow + (cl >> 2)] = (uint8_t)(w >> (8 * bsel));
+    }
+  }
+}
+
+// Conv-join epilogue (fused downsample), the same fp64 evaluation as
+// epilogue_cjoin: z = fma(p, a, fma(q, d, cc)), code = #{i : z > q_i}.
+template <int NB>
+__device__ __forceinline__ void epilogue_cjoin_t(const ConvLaunch& a, const uint8_t* lds,
+                                                 const v16i (&acc)[NB], const v16i (&accd)[NB],
+                                                 int wm, int h, int l32, int co0, int pl0,
+                                                 uint8_t* otile, int orow) {
+  const double q1 = a.qthr[0], q2 = a.qthr[1], q3 = a.qthr[2];
+  const double* cf = reinterpret_cast<const double*>(lds + kJoinCoefOff);
+  const int t = l32 & 3;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int cb = (wm * NB + j) * 32;
+    if (co0 + cb >= a.cout) continue;
+    const int cl = cb + l32;
+    const double p = cf[3 * cl], q = cf[3 * cl + 1], cc = cf[3 * cl + 2];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      uint32_t w = 0;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const double z = fma(p, (double)acc[j][4 * b + i], fma(q, (double)accd[j][4 * b + i], cc));
+        const uint32_t code = (uint32_t)(z > q1) + (uint32_t)(z > q2) + (uint32_t)(z > q3);
+        w |= code << (8 * i);
+      }
+      w = quad_or(w << (2 * t));
+      otile[(pl0 + 8 * b + 4 * h + t) * orow + (cl >> 2)] = (uint8_t)(w >> (8 * t));
+    }
+  }
+}
+
+// int32 sums of the tile to dump[p * c_out + c] (diagnostic path).
+template <int NB>
+__device__ __forceinline__ void dump_acc_t(const ConvLaunch& a, const v16i (&acc)[NB], int wm,
+                                           int h, int l32, int co0, int p0, int pl0, int bn,
+                                           int32_t* dump) {
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int c = co0 + (wm * NB + j) * 32 + l32;
+    if (c >= a.cout) continue;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int pl = pl0 + 8 * (v >> 2) + 4 * h + (v & 3);
+      if (pl < bn && p0 + pl < a.m) dump[(int64_t)(p0 + pl) * a.cout + c] = acc[j][v];
+    }
+  }
+}
+
 // 16 two-bit codes (one 32-bit word of a cell) -> 16 int8 operand bytes.
 __device__ __forceinline__ v4i unpack2(uint32_t u) {
   return v4i{(int)(u & kLow2), (int)((u >> 2) & kLow2), (int)((u >> 4) & kLow2),

@@ -274,7 +274,9 @@ class DeviceStack:
         out = []
         for i, L in enumerate(self.layers):
             if _is_conv(L):
-                out.append(api.ifq_conv_kernel_name(self._layers[i].conv))
+                lay = self._layers[i]
+                join = lay.join if lay.join.kind != IFQ_JOIN_NONE else None
+                out.append(api.ifq_conv_kernel_name(lay.conv, join))
             else:
                 out.append("maxpool_codes")
         return out

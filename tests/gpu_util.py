@@ -96,6 +96,8 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
             keep += [wdd, xind, cd]
             join = P.make_join(P.IFQ_JOIN_CONV_FUSED, B64, xind, cd, p["q_thr"],
                                down_w=wdd, down=dd)
+            # the kernel name query sees the join: a fused kernel instance
+            assert ", true, " in P.ifq_conv_kernel_name(d, join)
         else:
             coef = P.ifq_fold_join(P.IFQ_JOIN_CONV, p, down["beta_in"], down=down)
             scd = to_dev(shortcut.astype(np.int32))

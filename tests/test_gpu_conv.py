@@ -116,13 +116,14 @@ def test_conv_block64_bit_exact(P, case, io):
 # (256, 128 and 64 output pixels for the three variants of the 3x3 kernel
 # that keeps each tile's input window in LDS, and a stride-2 layer), at
 # batches the oracle finishes in about a second; the test also pins which
-# kernel variant the planner takes for each.
+# kernel variant the planner takes for each. 2-bit threshold layers run the
+# instances with transposed sums (last template argument true).
 HALO_TILES = [
-    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_halo<8, 1, 6, false, 4>"),
-    ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_halo<4, 2, 4, false, 4>"),
-    ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_halo<2, 4, 4, false, 4>"),
-    ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_halo<8, 1, 6, false, 4>"),
-    ("halo_l1_b24", 24, 56, 56, 64, 64, 1, "conv_halo<8, 1, 6, false, 2>"),
+    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_halo<8, 1, 6, false, 4, true>"),
+    ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_halo<4, 2, 4, false, 4, true>"),
+    ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_halo<2, 4, 4, false, 4, true>"),
+    ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_halo<8, 1, 6, false, 4, true>"),
+    ("halo_l1_b24", 24, 56, 56, 64, 64, 1, "conv_halo<8, 1, 6, false, 2, true>"),
 ]
 
 
@@ -132,6 +133,20 @@ def test_conv_halo_tiles_bit_exact(P, case):
     d = P.ConvDesc(n, h, w, cin, cout, 3, 3, st, 1, 2, 2, B64, B64)
     assert P.ifq_conv_kernel_name(d) == kernel
     run_layout_case(P, (name, n, h, w, cin, cout, 3, st, 1), (B64, B64))
+
+
+@pytest.mark.parametrize("case", HALO_TILES[:1] + HALO_TILES[4:],
+                         ids=[c[0] for c in HALO_TILES[:1] + HALO_TILES[4:]])
+def test_conv_halo_tiles_no_dump(P, case):
+    # the same layers without the int32 dump, so only the code epilogue runs
+    name, n, h, w, cin, cout, st, _ = case
+    L = make_layer(name, h, w, cin, cout, 3, st, 1)
+    seed = zlib.crc32(name.encode()) % 991
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, w, cin), 2)
+    _, want = oracle_layer(L, x, p)
+    _, got = gpu_layer(P, L, n, x, p, in_layout=B64, out_layout=B64, dump=False)
+    assert np.array_equal(got, expect_layout(want, B64))
 
 
 def test_conv_block64_int32_out(P):
@@ -182,7 +197,7 @@ def test_identity_join_64_channel_variant(P):
     # (two workgroups per CU) with an identity join
     n, h, c = 24, 56, 64
     d = P.conv_desc(n, h, h, c, c, 3, 1, 1, 2, 2, B64, B64)
-    assert P.ifq_conv_kernel_name(d) == "conv_halo<8, 1, 6, false, 2>"
+    assert P.ifq_conv_kernel_name(d).startswith("conv_halo<8, 1, 6, false, 2, ")
     L = make_layer("join_id", h, h, c, c, 3, 1, 1, join=("identity", "s"))
     p = params_for(41, L)
     x = codes_for(41, (n, h, h, c), 2)
