@@ -78,8 +78,8 @@ class Hip:
 
 def source_hash():
     h = hashlib.sha256()
-    for f in ("ifq_conv.hip", "ifq_conv_mfma.hip", "ifq_conv_halo.hip", "ifq_epilogue.h",
-              "ifq_mfma_common.h", "ifq_pool.hip"):
+    for f in ("ifq_conv.hip", "ifq_conv_mfma.hip", "ifq_conv_halo.hip", "ifq_conv_small.hip",
+              "ifq_epilogue.h", "ifq_mfma_common.h", "ifq_pool.hip"):
         with open(os.path.join(ROOT, "paper_1911_08076_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

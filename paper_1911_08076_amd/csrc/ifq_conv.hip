@@ -317,6 +317,7 @@ hipError_t launch_gather(const ConvLaunch& a, hipStream_t stream) {
 
 const char* conv_kernel_name(const ConvLaunch& a) {
   if (mfma_eligible(a)) return conv_mfma_name(a);
+  if (small8_eligible(a)) return conv_small8_name(a);
   static const char* names[3][4] = {
       {"conv_igemm<16, 256, 1, 0>", "conv_igemm<32, 128, 1, 0>",
        "conv_igemm<64, 128, 2, 0>", "conv_igemm<128, 128, 2, 0>"},
@@ -330,6 +331,7 @@ const char* conv_kernel_name(const ConvLaunch& a) {
 hipError_t launch_conv(const ConvLaunch& a, hipStream_t stream) {
   if (a.m == 0) return hipSuccess;
   if (mfma_eligible(a)) return launch_conv_mfma(a, stream);
+  if (small8_eligible(a)) return launch_conv_small8(a, stream);
   switch (gather_kind(a)) {
     case kGatherU2: return launch_gather<kGatherU2>(a, stream);
     case kGatherI8: return launch_gather<kGatherI8>(a, stream);

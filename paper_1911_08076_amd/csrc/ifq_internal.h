@@ -143,6 +143,12 @@ inline bool fused_supported(const ConvLaunch& a) {
 hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream);
 const char* conv_halo_name(const HaloPlan& p, const ConvLaunch& a);
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream);
+
+// 8-bit input codes with c_in <= 4 (a detector's first layer): whether the
+// small-channel kernel takes the layer, its launch and its name.
+bool small8_eligible(const ConvLaunch& a);
+hipError_t launch_conv_small8(const ConvLaunch& a, hipStream_t stream);
+const char* conv_small8_name(const ConvLaunch& a);
 const char* conv_mfma_name(const ConvLaunch& a);
 
 struct PoolLaunch {

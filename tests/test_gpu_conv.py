@@ -61,6 +61,39 @@ def test_conv_layer_bit_exact(P, case):
         assert len(np.unique(want)) > 1
 
 
+# 8-bit input with c_in <= 4 (a detector's first layer) runs the small-channel
+# kernel: one YOLO-c1-sized layer (several output rows per workgroup, a
+# ragged last tile), and shapes across its parameters (c_in 1..4, stride 2,
+# 1x1 and 4x4 filters, 1..4 row blocks of 16 output channels, int32 output).
+# (name, n, h, w, cin, cout, k, stride, pad, out_bits)
+SMALL8 = [
+    ("s8_yolo_c1", 2, 415, 416, 3, 16, 3, 1, 1, 2),
+    ("s8_cin1_s2_c64", 3, 33, 31, 1, 64, 3, 2, 1, 2),
+    ("s8_cin4_1x1_c48", 2, 17, 19, 4, 48, 1, 1, 0, 2),
+    ("s8_cin2_c33_i32", 2, 21, 20, 2, 33, 3, 1, 1, 0),
+    ("s8_cin3_4x4_s2_pad0", 1, 23, 29, 3, 16, 4, 2, 0, 2),
+]
+
+
+@pytest.mark.parametrize("case", SMALL8, ids=[c[0] for c in SMALL8])
+def test_small8_bit_exact(P, case):
+    name, n, h, w, cin, cout, k, st, pad, ob = case
+    L = make_layer(name, h, w, cin, cout, k, st, pad, 8, ob)
+    d = P.conv_desc(n, h, w, cin, cout, k, st, pad, 8, ob, I8, I8 if ob else I32)
+    assert P.ifq_conv_kernel_name(d).startswith("conv_small8<")
+    seed = zlib.crc32(name.encode()) % 997
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, w, cin), 8)
+    want_acc, want = oracle_layer(L, x, p)
+    outs = [I8, U2] if ob else [I32]
+    for out_l in outs:
+        acc, got = gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=out_l)
+        assert np.array_equal(acc, want_acc), (name, out_l)
+        assert np.array_equal(got, expect_layout(want, out_l)), (name, out_l)
+    if ob:
+        assert len(np.unique(want)) > 1
+
+
 U2_LAYERS = [
     ("u2_3x3_64", 2, 14, 14, 64, 64, 3, 1, 1),
     ("u2_stride2_128", 2, 15, 15, 64, 128, 3, 2, 1),
