@@ -19,18 +19,21 @@
 //  - The +-1 weight fragments of all output channels stay in registers for
 //    the whole workgroup; the B fragment of 16 pixels is four LDS reads per
 //    lane, and one MFMA per 16 output channels follows.
-//  - The epilogue is the generic one (ifq_epilogue.h): thresholds (Eq. 7/8),
-//    int32 sums or the dump, codes through an LDS output tile copied out with
-//    wide stores.
+//  - 2-bit codes (the detector's case): each lane's four output channels
+//    are fixed for the whole workgroup, so their threshold records, signs
+//    and 128 * rowsum corrections sit in registers; the compares are packed
+//    16-bit (|sum| <= 255 * 64 < 2^15), and a lane's byte (or 4 bytes) of
+//    codes goes straight to HBM, the four lanes of a pixel writing adjacent
+//    bytes. Other outputs (int32 sums, wider codes) take the generic epilogue
+//    of ifq_epilogue.h through an LDS output tile.
 #include <hip/hip_runtime.h>
 
 #include "ifq_epilogue.h"
 #include "ifq_internal.h"
+#include "ifq_mfma_common.h"
 
 namespace ifq {
 namespace {
-
-typedef int v4i __attribute__((ext_vector_type(4)));
 
 constexpr int kSmallThreads = 256;
 constexpr int kSmallMaxPx = 4096;      // output pixels per workgroup
@@ -40,8 +43,11 @@ struct SmallGeom {
   int rows;        // output rows per workgroup
   int tiles;       // workgroups per image
   int rin, win;    // staged input rows and columns
+  FastDiv div_win; // division by win
   int out_off;     // LDS offsets: epilogue parameters at 0, output tile,
-  int in_off;      // then the staged input
+  int in_off;      // the staged input, then the raw input bytes
+  int raw_off;
+  int vec;         // input 16-byte aligned: rows staged with 16-byte loads
   int lds_bytes;
 };
 
@@ -72,19 +78,81 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
   uint8_t* tile = lds + sg.in_off;
   const int iy0 = oy0 * st - a.pad;
   const int nin = sg.rin * sg.win;
-  for (int e = tid; e < nin; e += kSmallThreads) {
-    const int r = e / sg.win;
-    const int c = e - r * sg.win;
-    const int iy = iy0 + r, ix = c - a.pad;
-    uint32_t word = 0x80808080u;
-    if ((unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w) {
-      const uint8_t* src = a.x + (((int64_t)nimg * a.h + iy) * a.w + ix) * a.cin;
-      for (int ch = 0; ch < a.cin; ++ch)
-        word ^= (uint32_t)src[ch] << (8 * ch);   // 0x80 ^ x in byte ch
+  if (sg.vec) {
+    // the input rows of the tile are one contiguous byte span of the NHWC
+    // tensor: 16-byte loads of it (plus a byte tail) into LDS, then each
+    // pixel's channels are picked from there
+    const int iy_lo = iy0 > 0 ? iy0 : 0;
+    const int iy_hi = iy0 + sg.rin - 1 < a.h - 1 ? iy0 + sg.rin - 1 : a.h - 1;
+    int lead = 0;
+    uint8_t* raw = lds + sg.raw_off;
+    if (iy_lo <= iy_hi) {
+      const int64_t gs = (((int64_t)nimg * a.h + iy_lo) * a.w) * a.cin;
+      const int64_t ge = (((int64_t)nimg * a.h + iy_hi + 1) * a.w) * a.cin;
+      const int64_t gs16 = gs & ~(int64_t)15;
+      lead = (int)(gs - gs16);
+      const int nb = (int)(ge - gs16);
+      const int nfull = nb >> 4;
+      const uint4* src = reinterpret_cast<const uint4*>(a.x + gs16);
+      constexpr int VB = 4;
+      for (int i0 = 0; i0 < nfull; i0 += VB * kSmallThreads) {
+        uint4 v[VB];
+#pragma unroll
+        for (int k = 0; k < VB; ++k) {   // unconditional (clamped) loads, all in flight
+          const int i = i0 + k * kSmallThreads + tid;
+          v[k] = src[i < nfull ? i : nfull - 1];
+        }
+#pragma unroll
+        for (int k = 0; k < VB; ++k) {
+          const int i = i0 + k * kSmallThreads + tid;
+          if (i < nfull) reinterpret_cast<uint4*>(raw)[i] = v[k];
+        }
+      }
+      for (int i = nfull * 16 + tid; i < nb; i += kSmallThreads) raw[i] = a.x[gs16 + i];
     }
-    *reinterpret_cast<uint32_t*>(tile + e * 4) = word;
+    __syncthreads();
+    for (int e = tid; e < nin; e += kSmallThreads) {
+      const int r = fdiv(e, sg.div_win);
+      const int iy = iy0 + r, ix = e - r * sg.win - a.pad;
+      uint32_t word = 0x80808080u;
+      if ((unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w) {
+        const uint8_t* px = raw + lead + ((iy - iy_lo) * a.w + ix) * a.cin;
+#pragma unroll
+        for (int ch = 0; ch < 4; ++ch)
+          if (ch < a.cin) word ^= (uint32_t)px[ch] << (8 * ch);   // 0x80 ^ x
+      }
+      *reinterpret_cast<uint32_t*>(tile + e * 4) = word;
+    }
   }
-  stage_epilogue(a, lds, 0, BM);
+  // otherwise batches of SB pixels per thread: every byte load of a batch is
+  // issued before the first is used
+  constexpr int SB = 8;
+  for (int e0 = 0; !sg.vec && e0 < nin; e0 += SB * kSmallThreads) {
+    uint32_t word[SB];
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const int e = e0 + k * kSmallThreads + tid;
+      const int r = fdiv(e, sg.div_win);
+      const int iy = iy0 + r, ix = e - r * sg.win - a.pad;
+      word[k] = 0x80808080u;
+      if (e < nin && (unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w) {
+        const uint8_t* src = a.x + (((int64_t)nimg * a.h + iy) * a.w + ix) * a.cin;
+#pragma unroll
+        for (int ch = 0; ch < 4; ++ch)
+          if (ch < a.cin) word[k] ^= (uint32_t)src[ch] << (8 * ch);   // 0x80 ^ x
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const int e = e0 + k * kSmallThreads + tid;
+      if (e < nin) *reinterpret_cast<uint32_t*>(tile + e * 4) = word[k];
+    }
+  }
+  // 2-bit codes into I8 or packed-U2 NHWC: the register epilogue below
+  const bool fast = a.out_mode != 0 && a.rec == 4 && a.join_kind == IFQ_JOIN_NONE &&
+                    (a.out_layout == IFQ_LAYOUT_I8_NHWC ||
+                     (a.out_layout == IFQ_LAYOUT_U2_NHWC_PACKED && (a.cout & 3) == 0));
+  if (!fast) stage_epilogue(a, lds, 0, BM);
 
   // ---- weight fragments (A: rows = output channels), K byte 4*j + c of
   // lane group kg = channel c of tap 4*kg + j -------------------------------
@@ -96,9 +164,12 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int tap = 4 * kg + j;
-      if (tap < ntaps && co < a.cout_pad)
-        for (int c = 0; c < a.cin; ++c)
-          w4[j] |= (uint32_t)(uint8_t)a.wgt[(int64_t)co * a.kpad + tap * a.cin + c] << (8 * c);
+      if (tap < ntaps && co < a.cout_pad) {
+        const int8_t* wr = a.wgt + (int64_t)co * a.kpad + tap * a.cin;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          if (c < a.cin) w4[j] |= (uint32_t)(uint8_t)wr[c] << (8 * c);
+      }
     }
     af[fm] = v4i{(int)w4[0], (int)w4[1], (int)w4[2], (int)w4[3]};
   }
@@ -112,34 +183,126 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
     const int ty = tval[j] ? tap / a.kw : 0, tx = tval[j] ? tap - ty * a.kw : 0;
     toff[j] = (ty * sg.win + tx) * 4;
   }
+  // register epilogue state: per row block, the lane's channels
+  // 16*fm + 4*kg + i: packed 16-bit thresholds T' (sign folded as in the
+  // transposed epilogues: T' = -T - 1 and the codes xor 3 for s = -1), the
+  // xor mask and the 128 * rowsum corrections
+  uint32_t tw[FM][2][3], txm[FM];
+  int corr[FM][4];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    uint32_t t16[4][3];
+    txm[fm] = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int co = fm * 16 + 4 * kg + i;
+      int4 r = int4{1, 0x7FFF, 0x7FFF, 0x7FFF};
+      corr[fm][i] = 0;
+      if (fast && co < a.cout) {
+        r = *reinterpret_cast<const int4*>(a.thr + (int64_t)co * 4);
+        corr[fm][i] = 128 * a.rowsum[co];
+      }
+      const bool flip = r.x < 0;
+      const int tt[3] = {r.y, r.z, r.w};
+#pragma unroll
+      for (int k = 0; k < 3; ++k) {
+        int v = flip ? -tt[k] - 1 : tt[k];
+        v = v > 32767 ? 32767 : v < -32768 ? -32768 : v;   // |sum| < 2^15 anyway
+        t16[i][k] = (uint32_t)v & 0xFFFFu;
+      }
+      if (flip) txm[fm] |= 3u << ((i & 1) * 16 + (i >> 1) * 4);
+    }
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      tw[fm][0][k] = t16[0][k] | t16[1][k] << 16;
+      tw[fm][1][k] = t16[2][k] | t16[3][k] << 16;
+    }
+  }
   __syncthreads();
 
   const int orow = small_orow(a, BM);
   uint8_t* otile = lds + sg.out_off;
+  uint8_t* y8 = reinterpret_cast<uint8_t*>(a.y);
   const int nblk = (npx + 15) / 16;
-  for (int blk = wave; blk < nblk; blk += kSmallThreads / 64) {
-    const int q = blk * 16 + l16;
-    const int qc = q < npx ? q : npx - 1;
-    const int r = fdiv(qc, a.div_wo);
-    const int ox = qc - r * a.wo;
-    const uint8_t* win = tile + ((r * st) * sg.win + ox * st) * 4;
-    uint32_t b4[4];
+  // UB independent blocks of 16 pixels per iteration, so the LDS reads, the
+  // MFMAs and the epilogues of different blocks overlap (one block at a time
+  // past 32 output channels, where four would not fit the registers)
+  constexpr int UB = FM <= 2 ? 4 : 1;
+  constexpr int NW = kSmallThreads / 64;
+  for (int blk0 = wave; blk0 < nblk; blk0 += NW * UB) {
+    v4i accu[UB][FM];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      b4[j] = tval[j] ? *reinterpret_cast<const uint32_t*>(win + toff[j]) : 0x80808080u;
-    const v4i bf = v4i{(int)b4[0], (int)b4[1], (int)b4[2], (int)b4[3]};
-    v4i acc[FM];
+    for (int u = 0; u < UB; ++u) {
+      const int q = (blk0 + NW * u) * 16 + l16;
+      const int qc = q < npx ? q : npx - 1;
+      const int r = fdiv(qc, a.div_wo);
+      const int ox = qc - r * a.wo;
+      const uint8_t* win = tile + ((r * st) * sg.win + ox * st) * 4;
+      uint32_t b4[4];
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm)
-      acc[fm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[fm], bf, v4i{0, 0, 0, 0}, 0, 0, 0);
-    // lane holds channels 16*g + 4*kg .. +3 of pixel q
-    epilogue_lane<FM, 1>(
-        a, lds, [&](int g, int, int i) { return acc[g][i]; },
-        [&](int g) { return g * 16 + 4 * kg; }, 0, p0,
-        [&](int) { return q < npx ? q : -1; }, otile, orow);
+      for (int j = 0; j < 4; ++j)
+        b4[j] = tval[j] ? *reinterpret_cast<const uint32_t*>(win + toff[j]) : 0x80808080u;
+      const v4i bf = v4i{(int)b4[0], (int)b4[1], (int)b4[2], (int)b4[3]};
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+        accu[u][fm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[fm], bf, v4i{0, 0, 0, 0}, 0, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < UB; ++u) {
+      const int q = (blk0 + NW * u) * 16 + l16;
+      v4i acc[FM];
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) acc[fm] = accu[u][fm];
+      // lane holds channels 16*g + 4*kg .. +3 of pixel q
+      if (fast) {
+        const int64_t p = (int64_t)p0 + q;
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm) {
+          const int co = fm * 16 + 4 * kg;
+          const int v0 = acc[fm][0] + corr[fm][0], v1 = acc[fm][1] + corr[fm][1];
+          const int v2 = acc[fm][2] + corr[fm][2], v3 = acc[fm][3] + corr[fm][3];
+          if (a.acc_dump && q < npx) {
+            int32_t* dp = a.acc_dump + p * a.cout + co;
+            const int vv[4] = {v0, v1, v2, v3};
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (co + i < a.cout) dp[i] = vv[i];
+          }
+          const s16x2 p01 = __builtin_amdgcn_cvt_pk_i16(v0, v1);
+          const s16x2 p23 = __builtin_amdgcn_cvt_pk_i16(v2, v3);
+          const uint32_t c01 = count3_pk(p01, tw[fm][0][0], tw[fm][0][1], tw[fm][0][2]);
+          const uint32_t c23 = count3_pk(p23, tw[fm][1][0], tw[fm][1][1], tw[fm][1][2]);
+          // codes of channels i = 0..3: c01 bits 0 and 16, c23 bits 0 and 16
+          const uint32_t t = (c01 | (c23 << 4)) ^ txm[fm];
+          if (q < npx && co < a.cout) {
+            if (a.out_layout == IFQ_LAYOUT_U2_NHWC_PACKED) {
+              y8[(p * a.cout + co) >> 2] = (uint8_t)(t | (t >> 14));
+            } else {
+              const uint32_t b4 = (t & 3u) | ((t >> 16) & 3u) << 8 | ((t >> 4) & 3u) << 16 |
+                                  ((t >> 20) & 3u) << 24;
+              uint8_t* dst = y8 + p * a.cout + co;
+              if (co + 4 <= a.cout && ((p * a.cout + co) & 3) == 0) {
+                *reinterpret_cast<uint32_t*>(dst) = b4;
+              } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                  if (co + i < a.cout) dst[i] = (uint8_t)(b4 >> (8 * i));
+              }
+            }
+          }
+        }
+      } else {
+        epilogue_lane<FM, 1>(
+            a, lds, [&](int g, int, int i) { return acc[g][i]; },
+            [&](int g) { return g * 16 + 4 * kg; }, 0, p0,
+            [&](int) { return q < npx ? q : -1; }, otile, orow);
+      }
+    }
   }
-  __syncthreads();
-  copy_out_tile(a, otile, orow, 0, BM, p0, npx);
+  if (!fast) {
+    __syncthreads();
+    copy_out_tile(a, otile, orow, 0, BM, p0, npx);
+  }
 }
 
 bool small_geom(const ConvLaunch& a, SmallGeom* g) {
@@ -157,14 +320,19 @@ bool small_geom(const ConvLaunch& a, SmallGeom* g) {
     const int rin = (rows - 1) * a.stride + a.kh;
     const int epi = epilogue_param_bytes(bm);
     const int out = (npx * small_orow(a, bm) + 15) & ~15;
-    const int64_t total = (int64_t)epi + out + (int64_t)rin * win * 4;
+    const int64_t in = ((int64_t)rin * win * 4 + 15) & ~(int64_t)15;   // raw buffer 16-aligned
+    const int64_t rawb = ((int64_t)rin * a.w * a.cin + 16 + 15) & ~(int64_t)15;
+    const int64_t total = (int64_t)epi + out + in + rawb;
     if (npx <= kSmallMaxPx && total <= kSmallMaxLds) {
       g->rows = rows;
       g->tiles = (a.ho + rows - 1) / rows;
       g->rin = rin;
       g->win = win;
+      g->div_win = make_fastdiv((uint32_t)win);
       g->out_off = epi;
       g->in_off = epi + out;
+      g->raw_off = (int)(epi + out + in);
+      g->vec = ((uintptr_t)a.x & 15) == 0;
       g->lds_bytes = (int)total;
       return true;
     }
