@@ -47,7 +47,7 @@ constexpr int kTaps = 9;
 // Cells of one halo buffer (2 buffers per wave group) for WK wave groups and
 // FM 32-row blocks per wave (FM = 2: two workgroups share a CU).
 __host__ __device__ constexpr int halo_cap_cells(int wk, int fm) {
-  return fm == 2 ? 1024 : wk == 1 ? 1280 : wk == 2 ? 512 : 192;
+  return fm == 2 ? 1024 : wk == 1 ? 2560 : wk == 2 ? 1024 : 192;
 }
 
 __host__ __device__ constexpr int round64(int v) { return (v + 63) & ~63; }
