@@ -278,6 +278,10 @@ def main():
     ap.add_argument("--no-fuse-down", action="store_true",
                     help="run the 1x1 downsample convs as layers of their own "
                          "(default with b64: inside the conv join that reads them)")
+    ap.add_argument("--no-fuse-pool", action="store_true",
+                    help="run every max-pool as a layer of its own (default: a "
+                         "2x2/2 pool inside the conv that feeds it, where a "
+                         "fused kernel covers the pair)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="the oracle's CPU-baseline sample repeats the whole "
                          "batch until this much time has passed")
@@ -316,7 +320,7 @@ def main():
               for i, L in enumerate(layers)]
     torch.cuda.set_device(0)
     dev = P.DeviceStack(layers, params, batch, code_layout=args.layout,
-                        fuse_down=not args.no_fuse_down)
+                        fuse_down=not args.no_fuse_down, fuse_pool=not args.no_fuse_pool)
     run_layers = dev.layers    # without the downsample layers folded into joins
     L0 = layers[0]
     x_host = stack_input(args.config, (batch, L0.h, L0.w, L0.cin), L0.in_bits)
@@ -428,6 +432,10 @@ def main():
                    "code_layout": args.layout, "weights": "+-1 (seeded)",
                    "downsample": ("fused into the conv joins" if dev.fused
                                   else "separate 1x1 convs"),
+                   "pools": ("%d of %d fused into their convs" %
+                             (len(dev.fused_pool),
+                              len(dev.fused_pool) + sum(1 for L in run_layers
+                                                        if not hasattr(L, "cin")))),
                    "params": "seeded BN/alpha, plain variant"},
         "images_per_s": images_s,
         "pct_int8_peak": 100.0 * value / 1e12 / PEAK_INT8_TOPS,

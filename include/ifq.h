@@ -75,6 +75,7 @@ typedef int32_t ifq_status;
 
 #define IFQ_LAYER_CONV 0
 #define IFQ_LAYER_POOL 1
+#define IFQ_LAYER_CONV_POOL 2 /* conv with its max-pool fused (see ifq_conv_pool_forward) */
 
 #define IFQ_MAX_THRESHOLDS 15 /* 2^4 - 1: codes of up to 4 bits */
 
@@ -229,13 +230,16 @@ typedef struct ifq_pool_desc {
 
 /*
  * One layer of a stack (Sec. 3.1: a network is a chain of substructures).
- *   kind        IFQ_LAYER_CONV or IFQ_LAYER_POOL
+ *   kind        IFQ_LAYER_CONV, IFQ_LAYER_POOL or IFQ_LAYER_CONV_POOL (conv
+ *               without join whose codes go through pool before dst; its
+ *               pool desc describes the conv's output as for
+ *               ifq_conv_pool_forward)
  *   src, dst    tensor slots: 0 is the stack input x, 1 the stack output y,
  *               2 .. n_slots-1 live in the caller's workspace
  *   join_src    slot of the join shortcut (conv layers with join.kind != 0),
  *               else -1; join.shortcut is ignored inside a stack
  *   conv        shape of a conv layer; w_packed/thr as for ifq_conv_forward
- *   pool        shape of a pool layer
+ *   pool        shape of a pool layer, or the fused pool of a CONV_POOL layer
  */
 typedef struct ifq_layer {
   int32_t kind;
@@ -376,6 +380,35 @@ IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
                                     const ifq_join* join, void* y,
                                     int32_t* acc_dump, void* ws,
                                     size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Conv (Eq. 1, thresholds of Eq. 7-8) and max-pool (Eq. 4) in one kernel: the
+ * codes of each output tile are pooled in the conv's epilogue and only the
+ * pooled tensor reaches HBM. The paper pools the conv output before BN and
+ * the quantizer; the code of a channel is monotone in its integer sum
+ * (non-increasing where the sign s is -1), so pooling the codes gives the
+ * same result as pooling the sums with max (s = +1) or min (s = -1) and
+ * thresholding once. Asynchronous on stream.
+ *   d          conv as for ifq_conv_forward, codes out (out_bits 1..8), no join
+ *   p          the pool over the conv's output: n, h, w, c equal to the conv's
+ *              n, ho, wo, c_out; bits = d->out_bits; layout = d->out_layout;
+ *              mode IFQ_POOL_VALID with k == stride, ho and wo multiples of k
+ *   x, w_packed, thr   as for ifq_conv_forward
+ *   y          device [n][ho/k][wo/k][c_out] codes in d->out_layout
+ * Errors: INVALID_ARGUMENT (a desc invalid or the two inconsistent),
+ * UNSUPPORTED (no fused kernel covers the shape: ifq_conv_pool_kernel_name
+ * returns ""; run ifq_conv_forward and ifq_maxpool_codes instead), HIP.
+ */
+IFQ_API ifq_status ifq_conv_pool_forward(const ifq_conv_desc* d, const ifq_pool_desc* p,
+                                         const void* x, const void* w_packed,
+                                         const int32_t* thr, void* y, hipStream_t stream);
+
+/*
+ * Name of the kernel ifq_conv_pool_forward launches for d and p, as
+ * ifq_conv_kernel_name; "" when the pair is invalid or not covered. Host.
+ */
+IFQ_API const char* ifq_conv_pool_kernel_name(const ifq_conv_desc* d,
+                                              const ifq_pool_desc* p);
 
 /*
  * Max-pool on codes (Eq. 4), asynchronous on stream. x, y device tensors in

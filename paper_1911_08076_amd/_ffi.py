@@ -32,6 +32,7 @@ IFQ_JOIN_CONV_FUSED = 3
 
 IFQ_LAYER_CONV = 0
 IFQ_LAYER_POOL = 1
+IFQ_LAYER_CONV_POOL = 2
 
 IFQ_MAX_THRESHOLDS = 15
 
@@ -105,6 +106,10 @@ SIGNATURES = [
     ("ifq_conv_workspace_bytes", size_t, [ctypes.POINTER(ConvDesc)]),
     ("ifq_conv_forward", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp,
                                ctypes.POINTER(Join), vp, vp, vp, size_t, vp]),
+    ("ifq_conv_pool_forward", i32, [ctypes.POINTER(ConvDesc), ctypes.POINTER(PoolDesc),
+                                    vp, vp, vp, vp, vp]),
+    ("ifq_conv_pool_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc),
+                                                    ctypes.POINTER(PoolDesc)]),
     ("ifq_maxpool_codes", i32, [ctypes.POINTER(PoolDesc), vp, vp, vp]),
     ("ifq_convert_codes", i32, [i64, i64, i64, i32, i32, i32, vp, vp, vp]),
     ("ifq_stack_workspace_bytes", size_t, [ctypes.POINTER(Stack)]),

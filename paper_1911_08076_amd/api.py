@@ -194,6 +194,16 @@ def ifq_conv_forward(desc, x, w_packed, thr, y, join=None, acc_dump=None,
         _ptr(ws), ws_bytes, _stream(stream)), "ifq_conv_forward")
 
 
+def ifq_conv_pool_forward(desc, pool, x, w_packed, thr, y, stream=None):
+    _check(_lib().ifq_conv_pool_forward(
+        ctypes.byref(desc), ctypes.byref(pool), _ptr(x), _ptr(w_packed), _ptr(thr),
+        _ptr(y), _stream(stream)), "ifq_conv_pool_forward")
+
+
+def ifq_conv_pool_kernel_name(desc, pool):
+    return _lib().ifq_conv_pool_kernel_name(ctypes.byref(desc), ctypes.byref(pool)).decode()
+
+
 def ifq_maxpool_codes(desc, x, y, stream=None):
     _check(_lib().ifq_maxpool_codes(ctypes.byref(desc), _ptr(x), _ptr(y),
                                     _stream(stream)), "ifq_maxpool_codes")

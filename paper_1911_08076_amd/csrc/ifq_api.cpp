@@ -277,6 +277,35 @@ ifq::ConvLaunch make_launch(const ifq_conv_desc* d, int64_t ho, int64_t wo,
   return a;
 }
 
+// A conv with a fused pool: both descs valid, the pool over the conv's own
+// output (shape, code width, layout), non-overlapping valid windows that
+// tile it exactly, codes out and no join.
+ifq_status check_conv_pool(const ifq_conv_desc* d, const ifq_pool_desc* p, int64_t* ho,
+                           int64_t* wo) {
+  ifq_status st = check_conv(d, ho, wo);
+  if (st != IFQ_OK) return st;
+  int64_t pho, pwo;
+  st = check_pool(p, &pho, &pwo);
+  if (st != IFQ_OK) return st;
+  if (p->n != d->n || p->h != *ho || p->w != *wo || p->c != d->c_out)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "conv+pool: pool input is not the conv output");
+  if (d->out_bits == 0 || p->bits != d->out_bits || p->layout != d->out_layout)
+    return fail(IFQ_ERR_INVALID_ARGUMENT,
+                "conv+pool: codes out, with the pool's bits and layout the conv's");
+  if (p->mode != IFQ_POOL_VALID || p->k != p->stride || *ho % p->k || *wo % p->k)
+    return fail(IFQ_ERR_UNSUPPORTED,
+                "conv+pool: needs valid windows with k == stride dividing ho and wo");
+  return IFQ_OK;
+}
+
+void add_pool(ifq::ConvLaunch& a, const ifq_pool_desc& p) {
+  a.pool_k = p.k;
+  a.pho = a.ho / p.k;
+  a.pwo = a.wo / p.k;
+  a.div_pwo = ifq::make_fastdiv((uint32_t)(a.pwo > 0 ? a.pwo : 1));
+  a.div_phowo = ifq::make_fastdiv((uint32_t)(a.pho * a.pwo > 0 ? a.pho * a.pwo : 1));
+}
+
 // A BLOCK64 tensor of n images and c channels is pooled as the NHWC packed
 // tensor of n*c/64 images of 64 channels it is laid out as.
 ifq::PoolLaunch make_pool(const ifq_pool_desc& d, int64_t ho, int64_t wo,
@@ -639,6 +668,34 @@ IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
   return ok();
 }
 
+IFQ_API const char* ifq_conv_pool_kernel_name(const ifq_conv_desc* d,
+                                              const ifq_pool_desc* p) {
+  int64_t ho, wo;
+  if (check_conv_pool(d, p, &ho, &wo) != IFQ_OK) return "";
+  ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                  nullptr, nullptr);
+  add_pool(a, *p);
+  return ifq::conv_kernel_name(a);
+}
+
+IFQ_API ifq_status ifq_conv_pool_forward(const ifq_conv_desc* d, const ifq_pool_desc* p,
+                                         const void* x, const void* w_packed,
+                                         const int32_t* thr, void* y, hipStream_t stream) {
+  int64_t ho, wo;
+  ifq_status st = check_conv_pool(d, p, &ho, &wo);
+  if (st != IFQ_OK) return st;
+  st = conv_args_check(d, x, w_packed, thr, nullptr, nullptr, y);
+  if (st != IFQ_OK) return st;
+  if (d->n == 0) return ok();
+  ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_packed, thr, nullptr, nullptr, y, nullptr);
+  add_pool(a, *p);
+  if (!*ifq::conv_kernel_name(a))
+    return fail(IFQ_ERR_UNSUPPORTED, "conv+pool: no fused kernel covers this shape");
+  st = hip_status(ifq::launch_conv(a, stream), "conv+pool launch");
+  if (st != IFQ_OK) return st;
+  return ok();
+}
+
 IFQ_API ifq_status ifq_maxpool_codes(const ifq_pool_desc* d, const void* x,
                                      void* y, hipStream_t stream) {
   int64_t ho, wo;
@@ -692,6 +749,12 @@ struct SlotPlan {
 };
 
 int64_t layer_out_bytes(const ifq_layer& L) {
+  if (L.kind == IFQ_LAYER_CONV_POOL) {
+    const int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);
+    const int64_t wo = out_extent(L.conv.w, L.conv.kw, L.conv.stride, L.conv.pad);
+    const int64_t k = L.pool.k > 0 ? L.pool.k : 1;
+    return tensor_bytes(L.conv.n, ho / k, wo / k, L.conv.c_out, L.conv.out_layout);
+  }
   if (L.kind == IFQ_LAYER_CONV) {
     const int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);
     const int64_t wo = out_extent(L.conv.w, L.conv.kw, L.conv.stride, L.conv.pad);
@@ -709,7 +772,7 @@ int64_t layer_out_bytes(const ifq_layer& L) {
 }
 
 int64_t layer_in_bytes(const ifq_layer& L) {
-  if (L.kind == IFQ_LAYER_CONV)
+  if (L.kind == IFQ_LAYER_CONV || L.kind == IFQ_LAYER_CONV_POOL)
     return tensor_bytes(L.conv.n, L.conv.h, L.conv.w, L.conv.c_in, L.conv.in_layout);
   return tensor_bytes(L.pool.n, L.pool.h, L.pool.w, L.pool.c, L.pool.layout);
 }
@@ -745,6 +808,15 @@ ifq_status plan_stack(const ifq_stack* s, SlotPlan* plan) {
       int64_t ho, wo;
       st = check_pool(&L.pool, &ho, &wo);
       if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+    } else if (L.kind == IFQ_LAYER_CONV_POOL) {
+      int64_t ho, wo;
+      st = check_conv_pool(&L.conv, &L.pool, &ho, &wo);
+      if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+      st = conv_args_check(&L.conv, (const void*)1, L.w_packed, L.thr, nullptr, nullptr,
+                           (const void*)1);
+      if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+      if (L.conv.n > 0 && !*ifq_conv_pool_kernel_name(&L.conv, &L.pool))
+        return fail(IFQ_ERR_UNSUPPORTED, "layer %d: no fused conv+pool kernel covers it", i);
     } else {
       return fail(IFQ_ERR_INVALID_ARGUMENT, "layer %d: bad kind %d", i, L.kind);
     }
@@ -825,6 +897,13 @@ IFQ_API ifq_status ifq_run_stack(const ifq_stack* s, const void* x, void* y,
                                             L.thr, &j, sc, slot(L.dst), nullptr);
       (void)conv_ws;
       st = hip_status(ifq::launch_conv(a, stream), "conv launch");
+    } else if (L.kind == IFQ_LAYER_CONV_POOL) {
+      int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);
+      int64_t wo = out_extent(L.conv.w, L.conv.kw, L.conv.stride, L.conv.pad);
+      ifq::ConvLaunch a = make_launch(&L.conv, ho, wo, slot(L.src), L.w_packed, L.thr,
+                                      nullptr, nullptr, slot(L.dst), nullptr);
+      add_pool(a, L.pool);
+      st = hip_status(ifq::launch_conv(a, stream), "conv+pool launch");
     } else {
       int64_t ho, wo;
       check_pool(&L.pool, &ho, &wo);

@@ -315,7 +315,16 @@ hipError_t launch_gather(const ConvLaunch& a, hipStream_t stream) {
 
 }  // namespace
 
+// A fused pool (a.pool_k) runs in the windowed 3x3 kernel or the
+// small-channel 8-bit kernel, where their planners fit whole rows of pooling
+// windows into a tile; no other kernel takes it.
 const char* conv_kernel_name(const ConvLaunch& a) {
+  if (a.pool_k) {
+    HaloPlan hp;
+    if (mfma_eligible(a) && plan_halo(a, &hp)) return conv_halo_name(hp, a);
+    if (small8_eligible(a)) return conv_small8_name(a);
+    return "";
+  }
   if (mfma_eligible(a)) return conv_mfma_name(a);
   if (small8_eligible(a)) return conv_small8_name(a);
   static const char* names[3][4] = {
@@ -330,6 +339,12 @@ const char* conv_kernel_name(const ConvLaunch& a) {
 
 hipError_t launch_conv(const ConvLaunch& a, hipStream_t stream) {
   if (a.m == 0) return hipSuccess;
+  if (a.pool_k) {
+    HaloPlan hp;
+    if (mfma_eligible(a) && plan_halo(a, &hp)) return launch_conv_halo(a, hp, stream);
+    if (small8_eligible(a)) return launch_conv_small8(a, stream);
+    return hipErrorNotSupported;
+  }
   if (mfma_eligible(a)) return launch_conv_mfma(a, stream);
   if (small8_eligible(a)) return launch_conv_small8(a, stream);
   switch (gather_kind(a)) {

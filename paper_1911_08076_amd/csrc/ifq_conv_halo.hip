@@ -543,7 +543,10 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
   }
   __syncthreads();
   const int npx = a.m - p0 < bn ? a.m - p0 : bn;
-  copy_out_tile(a, otile, orow, co0, BM, p0, npx);
+  if (a.pool_k)
+    pool_out_tile(a, otile, orow, co0, BM, p0, npx);
+  else
+    copy_out_tile(a, otile, orow, co0, BM, p0, npx);
 }
 
 // ---------------------------------------------------------------------------
@@ -599,6 +602,7 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
                  a.cout % 32 == 0 &&
                  (int64_t)a.n * a.d_h * a.d_w * (a.d_cin / 64) < (int64_t)1 << 26))
     return false;
+  if (a.pool_k && !pool_epilogue_ok(a)) return false;
   const int G = a.cin / 64;
   double best_t = 1e30;
   bool found = false;
@@ -623,6 +627,13 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
     int64_t bn = (a.m + nb - 1) / nb;
     bn = (bn + 31) / 32 * 32;
     if (bn > bnmax) bn = bnmax;
+    if (a.pool_k) {
+      // a fused pool needs whole rows of pooling windows per tile
+      const int64_t unit = (int64_t)a.pool_k * a.wo;
+      bn = (bn + unit - 1) / unit * unit;
+      if (bn > bnmax) bn = bnmax / unit * unit;
+      if (bn == 0) continue;
+    }
     const int64_t cells = halo_cells_bound(a, bn);
     if (cells > cap) continue;
     const int nr = 11 - V.d < kTaps ? 11 - V.d : kTaps;

@@ -222,6 +222,7 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
 
   const int orow = small_orow(a, BM);
   uint8_t* otile = lds + sg.out_off;
+  const bool pooled = a.pool_k > 0;
   uint8_t* y8 = reinterpret_cast<uint8_t*>(a.y);
   const int nblk = (npx + 15) / 16;
   // UB independent blocks of 16 pixels per iteration, so the LDS reads, the
@@ -274,7 +275,15 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
           const uint32_t c23 = count3_pk(p23, tw[fm][1][0], tw[fm][1][1], tw[fm][1][2]);
           // codes of channels i = 0..3: c01 bits 0 and 16, c23 bits 0 and 16
           const uint32_t t = (c01 | (c23 << 4)) ^ txm[fm];
-          if (q < npx && co < a.cout) {
+          if (q < npx && co < a.cout && pooled) {
+            // into the LDS tile for the pooled copy-out (cout % 16 == 0 for
+            // packed codes, % 4 for bytes)
+            if (a.out_mode == 2)
+              otile[q * orow + (co >> 2)] = (uint8_t)(t | (t >> 14));
+            else
+              *reinterpret_cast<uint32_t*>(otile + q * orow + co) =
+                  (t & 3u) | ((t >> 16) & 3u) << 8 | ((t >> 4) & 3u) << 16 | ((t >> 20) & 3u) << 24;
+          } else if (q < npx && co < a.cout) {
             if (a.out_layout == IFQ_LAYOUT_U2_NHWC_PACKED) {
               y8[(p * a.cout + co) >> 2] = (uint8_t)(t | (t >> 14));
             } else {
@@ -299,9 +308,12 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
       }
     }
   }
-  if (!fast) {
+  if (!fast || pooled) {
     __syncthreads();
-    copy_out_tile(a, otile, orow, 0, BM, p0, npx);
+    if (pooled)
+      pool_out_tile(a, otile, orow, 0, BM, p0, npx);
+    else
+      copy_out_tile(a, otile, orow, 0, BM, p0, npx);
   }
 }
 
@@ -314,7 +326,11 @@ bool small_geom(const ConvLaunch& a, SmallGeom* g) {
   int rows = (int)((rows_total + 1023) / 1024);
   if (rows < 1) rows = 1;
   if (rows > a.ho) rows = a.ho;
-  for (;; --rows) {
+  // a fused pool needs whole rows of pooling windows per workgroup
+  const int rstep = a.pool_k > 0 ? a.pool_k : 1;
+  rows = (rows + rstep - 1) / rstep * rstep;
+  if (rows > a.ho) rows = a.ho / rstep * rstep;
+  for (;; rows -= rstep) {
     if (rows < 1) return false;
     const int npx = rows * a.wo;
     const int rin = (rows - 1) * a.stride + a.kh;
@@ -346,6 +362,7 @@ bool small8_eligible(const ConvLaunch& a) {
         a.kh * a.kw <= 16 && a.cout <= 64 && a.join_kind == IFQ_JOIN_NONE && a.m > 0))
     return false;
   if ((int64_t)a.n * a.h * a.w * a.cin >= ((int64_t)1 << 31)) return false;
+  if (a.pool_k && !pool_epilogue_ok(a)) return false;
   SmallGeom g;
   return small_geom(a, &g);
 }

@@ -337,5 +337,65 @@ __device__ __forceinline__ void copy_out_tile(const ConvLaunch& a, const uint8_t
   }
 }
 
+// Max of two words of codes, field by field (Eq. 4 on codes): 2-bit fields
+// (bit 1 of a field decides, then bit 0 among equals), or bytes below 128
+// (a per-byte a >= b from the top bit of (a | 0x80) - b, which never
+// borrows across bytes).
+__device__ __forceinline__ uint32_t max_codes_u2(uint32_t a, uint32_t b) {
+  constexpr uint32_t M = 0x55555555u;
+  const uint32_t ha = (a >> 1) & M, la = a & M, hb = (b >> 1) & M, lb = b & M;
+  const uint32_t lo = (ha & ~hb & la) | (hb & ~ha & lb) | (~(ha ^ hb) & (la | lb));
+  return ((ha | hb) << 1) | (lo & M);
+}
+__device__ __forceinline__ uint32_t max_codes_u8(uint32_t a, uint32_t b) {
+  const uint32_t ge = (((a | 0x80808080u) - b) & 0x80808080u) >> 7;   // 1 per byte a >= b
+  const uint32_t mask = ge * 0xFFu;
+  return (a & mask) | (b & ~mask);
+}
+
+// copy_out_tile with the max-pool of Eq. 4 fused (a.pool_k x a.pool_k
+// windows at stride a.pool_k, valid): the tile's npx pixels are whole rows
+// of whole windows, starting at a window row (p0 a multiple of pool_k * wo),
+// so its pooled pixels start at p0 / pool_k^2 of the pooled tensor. One
+// 32-bit word of a pixel's channel row per thread and step, the max taken
+// over the window's words in the LDS tile.
+__device__ __forceinline__ void pool_out_tile(const ConvLaunch& a, const uint8_t* otile,
+                                              int orow, int co0, int bm, int p0, int npx) {
+  if (npx <= 0) return;
+  const int k = a.pool_k;
+  const bool u2 = a.out_mode == 2;
+  const int ch = a.cout - co0 < bm ? a.cout - co0 : bm;
+  const int words = (u2 ? ch >> 2 : ch) >> 2;
+  const int npo = npx / (k * k);
+  const int P0 = p0 / (k * k);
+  const int pstride = u2 ? a.cout >> 2 : a.cout;
+  const int cofs = u2 ? co0 >> 2 : co0;
+  const int phowo = a.pho * a.pwo;
+  const bool b64 = a.out_layout == IFQ_LAYOUT_U2_BLOCK64;
+  uint8_t* y8 = reinterpret_cast<uint8_t*>(a.y);
+  for (int u = threadIdx.x; u < npo * words; u += blockDim.x) {
+    const int po = u / words, wi = u - po * words;
+    const int r = fdiv(po, a.div_pwo), c = po - r * a.pwo;
+    const uint8_t* src = otile + ((r * k) * a.wo + c * k) * orow + 4 * wi;
+    uint32_t m = 0;
+    for (int dy = 0; dy < k; ++dy)
+      for (int dx = 0; dx < k; ++dx) {
+        const uint32_t v = *reinterpret_cast<const uint32_t*>(src + (dy * a.wo + dx) * orow);
+        m = u2 ? max_codes_u2(m, v) : max_codes_u8(m, v);
+      }
+    const int P = P0 + po;
+    int64_t off;
+    if (b64) {
+      const int nimg = fdiv(P, a.div_phowo);
+      const int gb = cofs + 4 * wi;   // byte of the pixel's 2-bit channel row
+      off = (((int64_t)nimg * (a.cout >> 6) + (gb >> 4)) * phowo + (P - nimg * phowo)) * 16 +
+            (gb & 15);
+    } else {
+      off = (int64_t)P * pstride + cofs + 4 * wi;
+    }
+    *reinterpret_cast<uint32_t*>(y8 + off) = m;
+  }
+}
+
 }  // namespace
 }  // namespace ifq

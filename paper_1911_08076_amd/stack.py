@@ -18,7 +18,7 @@ import ctypes
 import numpy as np
 
 from . import _ffi, api
-from ._ffi import (Layer, Stack, IFQ_LAYER_CONV, IFQ_LAYER_POOL,
+from ._ffi import (Layer, Stack, IFQ_LAYER_CONV, IFQ_LAYER_POOL, IFQ_LAYER_CONV_POOL,
                    IFQ_LAYOUT_I8_NHWC, IFQ_LAYOUT_U2_NHWC_PACKED,
                    IFQ_LAYOUT_I32_NHWC, IFQ_LAYOUT_U2_BLOCK64, IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY,
                    IFQ_JOIN_CONV, IFQ_JOIN_CONV_FUSED, IFQ_POOL_VALID, IFQ_POOL_SAME)
@@ -47,10 +47,15 @@ class DeviceStack:
     fuse_down: with "b64", compute each 1x1 downsample inside the conv join
     that consumes it (IFQ_JOIN_CONV_FUSED); self.fused maps the join's layer
     name to the downsample's, whose layer and output tensor are then absent.
+    fuse_pool: a conv whose codes only a following valid max-pool with
+    k == stride reads runs as one IFQ_LAYER_CONV_POOL layer where a fused
+    kernel covers the pair (ifq_conv_pool_kernel_name); self.fused_pool maps
+    the conv's name to the pool's, whose layer and the conv's output tensor
+    are then absent.
     """
 
     def __init__(self, layers, params, batch, code_layout="i8",
-                 device="cuda", fuse_down=False):
+                 device="cuda", fuse_down=False, fuse_pool=False):
         import torch
         if code_layout not in ("i8", "u2", "b64"):
             raise ValueError("code_layout must be 'i8', 'u2' or 'b64'")
@@ -75,8 +80,14 @@ class DeviceStack:
         skip = set(self.fused.values())
         self._all_layers = all_layers
         self.layers = [L for L in all_layers if L.name not in skip]
-        src_index = [by_name[L.name][0] for L in self.layers]
         self.batch = int(batch)
+        self.fused_pool = {}
+        if fuse_pool:
+            self.fused_pool = self._pool_fusions(code_layout)
+            drop = set(self.fused_pool.values())
+            self.layers = [L for L in self.layers if L.name not in drop]
+        pool_of = {c: by_name[p][1] for c, p in self.fused_pool.items()}
+        src_index = [by_name[L.name][0] for L in self.layers]
         self.device = torch.device(device)
         self._keep = []
         slots = {"x": 0, "y": 1}
@@ -103,14 +114,35 @@ class DeviceStack:
         self.input_layout = layout_of["x"]
 
         self.tensor_info = {"x": (self.input_shape, layout_of["x"], b0)}
+        # slot -> (the layer specs' name of the tensor it holds last, the spec
+        # layer that computed it: a fused pool's name for a fused conv + pool)
+        self.slot_origin = {"x": ("x", None)}
+        alias = {}
+
+        def cur(name):
+            return alias.get(name, name)
         arr = (Layer * len(self.layers))()
         self.ops = 0
         for i, L in enumerate(self.layers):
             rec = arr[i]
-            rec.src = sid(L.src)
-            rec.dst = sid(L.dst)
+            # slot names: a fused conv + pool that would read and write the
+            # same slot (slots ping-pong along the chain) writes a slot of its
+            # own, which stands for that name until the name is written again
+            src_name = cur(L.src)
+            if L.name in pool_of:
+                dst_name = pool_of[L.name].dst
+                if cur(dst_name) == src_name:
+                    alias[dst_name] = "%s@%s" % (dst_name, L.name)
+                else:
+                    alias.pop(dst_name, None)
+                dst_name, orig_dst, writer = cur(dst_name), dst_name, pool_of[L.name].name
+            else:
+                alias.pop(L.dst, None)
+                dst_name, orig_dst, writer = L.dst, L.dst, L.name
+            rec.src = sid(src_name)
+            rec.dst = sid(dst_name)
             rec.join_src = -1
-            in_layout = layout_of[L.src]
+            in_layout = layout_of[src_name]
             if _is_conv(L):
                 p = params[src_index[i]]
                 rec.kind = IFQ_LAYER_CONV
@@ -122,6 +154,12 @@ class DeviceStack:
                                   L.stride, L.pad, L.in_bits, L.out_bits,
                                   in_layout, out_layout)
                 rec.conv = d
+                if L.name in pool_of:
+                    Pl = pool_of[L.name]
+                    rec.kind = IFQ_LAYER_CONV_POOL
+                    ho, wo = api.ifq_conv_output_dims(d)
+                    rec.pool = api.pool_desc(self.batch, ho, wo, L.cout, Pl.k, Pl.stride,
+                                             IFQ_POOL_VALID, L.out_bits, out_layout)
                 blob = api.ifq_pack_weights(d, p["w"])
                 wdev = torch.from_numpy(blob).to(self.device)
                 self._keep.append(wdev)
@@ -145,7 +183,7 @@ class DeviceStack:
                         tdev = torch.from_numpy(table).to(self.device)
                         self._keep.append(tdev)
                         rec.join = api.make_join(IFQ_JOIN_IDENTITY,
-                                                 layout_of[L.join[1]], None, None,
+                                                 layout_of[cur(L.join[1])], None, None,
                                                  p["q_thr"], table=tdev)
                     elif L.name in self.fused:
                         D = by_name[self.fused[L.name]][1]
@@ -155,11 +193,11 @@ class DeviceStack:
                         cdev = torch.from_numpy(coef).to(self.device)
                         dd = api.conv_desc(self.batch, D.h, D.w, D.cin, D.cout, D.k,
                                            D.stride, D.pad, D.in_bits, 0,
-                                           layout_of[D.src], IFQ_LAYOUT_I32_NHWC)
+                                           layout_of[cur(D.src)], IFQ_LAYOUT_I32_NHWC)
                         ddev = torch.from_numpy(api.ifq_pack_weights(dd, pd["w"])).to(
                             self.device)
                         self._keep += [cdev, ddev]
-                        rec.join = api.make_join(IFQ_JOIN_CONV_FUSED, layout_of[D.src],
+                        rec.join = api.make_join(IFQ_JOIN_CONV_FUSED, layout_of[cur(D.src)],
                                                  None, cdev, p["q_thr"], down_w=ddev,
                                                  down=dd)
                         self.ops += conv_ops(D, self.batch)
@@ -169,14 +207,17 @@ class DeviceStack:
                                                  down=pd)
                         cdev = torch.from_numpy(coef).to(self.device)
                         self._keep.append(cdev)
-                        rec.join = api.make_join(IFQ_JOIN_CONV, layout_of[L.join[1]],
+                        rec.join = api.make_join(IFQ_JOIN_CONV, layout_of[cur(L.join[1])],
                                                  None, cdev, p["q_thr"])
-                    rec.join_src = (sid(by_name[self.fused[L.name]][1].src)
-                                    if L.name in self.fused else sid(L.join[1]))
+                    rec.join_src = (sid(cur(by_name[self.fused[L.name]][1].src))
+                                    if L.name in self.fused else sid(cur(L.join[1])))
                 self.ops += conv_ops(L, self.batch)
                 ho, wo = api.ifq_conv_output_dims(d)
                 out_shape = (self.batch, ho, wo, L.cout)
                 out_bits = L.out_bits
+                if L.name in pool_of:
+                    k = pool_of[L.name].k
+                    out_shape = (self.batch, ho // k, wo // k, L.cout)
             else:
                 rec.kind = IFQ_LAYER_POOL
                 mode = {"valid": IFQ_POOL_VALID, "same": IFQ_POOL_SAME}[L.mode]
@@ -189,9 +230,10 @@ class DeviceStack:
                     ho, wo = -(-L.h // L.stride), -(-L.w // L.stride)
                 out_shape = (self.batch, ho, wo, L.c)
                 out_bits = L.bits
-            layout_of[L.dst] = out_layout
-            self.tensor_info[L.dst] = (out_shape, out_layout, out_bits)
-            if L.dst == "y":
+            layout_of[dst_name] = out_layout
+            self.tensor_info[dst_name] = (out_shape, out_layout, out_bits)
+            self.slot_origin[dst_name] = (orig_dst, writer)
+            if dst_name == "y":
                 self.output_shape = out_shape
                 self.output_layout = out_layout
                 self.output_bits = out_bits
@@ -206,6 +248,56 @@ class DeviceStack:
                                api.ifq_last_error())
         self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8,
                               device=self.device)
+
+    def _pool_fusions(self, code_layout):
+        """conv name -> pool name for every conv whose codes only a following
+        valid k == stride max-pool reads and whose pair a fused kernel covers
+        (layouts as the stack would give them)."""
+        layout_of = {}
+
+        def code_layout_for(bits, channels):
+            if code_layout == "b64" and bits == 2 and channels % 64 == 0:
+                return IFQ_LAYOUT_U2_BLOCK64
+            if code_layout in ("u2", "b64") and bits == 2 and channels % 16 == 0:
+                return IFQ_LAYOUT_U2_NHWC_PACKED
+            return IFQ_LAYOUT_I8_NHWC
+
+        L0 = self.layers[0]
+        layout_of[L0.src] = code_layout_for(L0.in_bits if _is_conv(L0) else L0.bits,
+                                            L0.cin if _is_conv(L0) else L0.c)
+        out = {}
+        for i, L in enumerate(self.layers):
+            if not _is_conv(L):
+                layout_of[L.dst] = layout_of[L.src]
+                continue
+            out_layout = (IFQ_LAYOUT_I32_NHWC if L.out_bits == 0
+                          else code_layout_for(L.out_bits, L.cout))
+            layout_of[L.dst] = out_layout
+            nxt = self.layers[i + 1] if i + 1 < len(self.layers) else None
+            if (nxt is None or _is_conv(nxt) or nxt.src != L.dst or L.join is not None
+                    or L.out_bits == 0 or L.dst == "y" or nxt.mode != "valid"
+                    or nxt.k != nxt.stride):
+                continue
+            # anything reading the conv's tensor before its slot is written
+            # again (slots are reused along the chain)
+            read_later = False
+            for M in self.layers[i + 2:]:
+                if M.src == L.dst or (_is_conv(M) and M.join is not None
+                                      and M.join[1] == L.dst):
+                    read_later = True
+                    break
+                if M.dst == L.dst:
+                    break
+            if read_later:
+                continue
+            d = api.conv_desc(self.batch, L.h, L.w, L.cin, L.cout, L.k, L.stride, L.pad,
+                              L.in_bits, L.out_bits, layout_of[L.src], out_layout)
+            ho, wo = api.ifq_conv_output_dims(d)
+            pd = api.pool_desc(self.batch, ho, wo, L.cout, nxt.k, nxt.stride,
+                               IFQ_POOL_VALID, L.out_bits, out_layout)
+            if api.ifq_conv_pool_kernel_name(d, pd):
+                out[L.name] = nxt.name
+        return out
 
     # -- buffers ---------------------------------------------------------------
     def _bytes(self, shape, layout):
@@ -273,8 +365,10 @@ class DeviceStack:
         maxpool_codes)."""
         out = []
         for i, L in enumerate(self.layers):
-            if _is_conv(L):
-                lay = self._layers[i]
+            lay = self._layers[i]
+            if lay.kind == IFQ_LAYER_CONV_POOL:
+                out.append(api.ifq_conv_pool_kernel_name(lay.conv, lay.pool))
+            elif _is_conv(L):
                 join = lay.join if lay.join.kind != IFQ_JOIN_NONE else None
                 out.append(api.ifq_conv_kernel_name(lay.conv, join))
             else:
@@ -324,6 +418,13 @@ class DeviceStack:
                     None if join is None else ctypes.byref(join), dst, None, None, 0, st)
             fn = lib.ifq_conv_forward
             what = "ifq_conv_forward"
+        elif rec.kind == IFQ_LAYER_CONV_POOL:
+            desc = (rec.conv, rec.pool)
+            join = None
+            args = (ctypes.byref(rec.conv), ctypes.byref(rec.pool), src, vp(rec.w_packed),
+                    vp(rec.thr), dst, st)
+            fn = lib.ifq_conv_pool_forward
+            what = "ifq_conv_pool_forward"
         else:
             desc = rec.pool
             args = (ctypes.byref(desc), src, dst, st)
@@ -332,7 +433,7 @@ class DeviceStack:
 
         def launch():
             api._check(fn(*args), what)
-        launch.keep = (desc, join if rec.kind == IFQ_LAYER_CONV else None)
+        launch.keep = (desc, join if rec.kind != IFQ_LAYER_POOL else None)
         return launch
 
     def run(self, x, y, stream=None, events=None):

@@ -490,6 +490,44 @@ def test_maxpool_rejects_bad_desc(pool, want):
     assert st == want
 
 
+@pytest.mark.parametrize("pool,want", [
+    (dict(h=14), EINVAL),                     # not the conv's output
+    (dict(c=32), EINVAL),
+    (dict(n=3), EINVAL),
+    (dict(layout=U2), EINVAL),                # not the conv's layout
+    (dict(bits=4), EINVAL),
+    (dict(k=3, stride=2), EUNSUP),            # overlapping windows
+    (dict(mode=1), EUNSUP),                   # same mode
+    (dict(k=3, stride=3), EUNSUP),            # 16 is no multiple of 3
+    (dict(k=0), EINVAL)])
+def test_conv_pool_rejects_inconsistent_pair(pool, want):
+    d = P.conv_desc(2, 16, 16, 64, 64, 3, 1, 1, 2, 2, B64, B64)
+    base = dict(n=2, h=16, w=16, c=64, k=2, stride=2, mode=0, bits=2, layout=B64)
+    base.update(pool)
+    pd = _ffi.PoolDesc(**base)
+    assert P.ifq_conv_pool_kernel_name(d, pd) == ""
+    st = status_of("ifq_conv_pool_forward", ctypes.byref(d), ctypes.byref(pd), FAKE,
+                   FAKE, FAKE, FAKE, None)
+    assert st == want
+
+
+def test_conv_pool_kernel_choice():
+    # the pair fuses in the windowed 3x3 kernel (BLOCK64 input) and in the
+    # 8-bit first-layer kernel; other inputs have no fused kernel
+    pd = lambda n, h, c, lay: _ffi.PoolDesc(n, h, h, c, 2, 2, 0, 2, lay)
+    d = P.conv_desc(2, 28, 28, 256, 256, 3, 1, 1, 2, 2, B64, B64)
+    assert P.ifq_conv_pool_kernel_name(d, pd(2, 28, 256, B64)).startswith("conv_halo<")
+    d = P.conv_desc(2, 64, 64, 3, 16, 3, 1, 1, 8, 2, I8, U2)
+    assert P.ifq_conv_pool_kernel_name(d, pd(2, 64, 16, U2)).startswith("conv_small8<")
+    d = P.conv_desc(2, 28, 28, 256, 256, 3, 1, 1, 2, 2, U2, U2)
+    assert P.ifq_conv_pool_kernel_name(d, pd(2, 28, 256, U2)) == ""
+    assert status_of("ifq_conv_pool_forward", ctypes.byref(d),
+                     ctypes.byref(pd(2, 28, 256, U2)), FAKE, FAKE, FAKE, FAKE, None) == EUNSUP
+    # a tile cannot hold two rows of 224 pixels: not covered
+    d = P.conv_desc(1, 224, 224, 64, 64, 3, 1, 1, 2, 2, B64, B64)
+    assert P.ifq_conv_pool_kernel_name(d, pd(1, 224, 64, B64)) == ""
+
+
 def test_convert_rejects_bad_args():
     cv = lambda *a: status_of("ifq_convert_codes", *a)
     assert cv(1, 1, 10, 6, I8, U2, FAKE, FAKE, None) == EINVAL     # C % 4

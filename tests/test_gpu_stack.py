@@ -40,12 +40,21 @@ def check_stack(P, cfg, batch, layout, variant):
     import torch
     params, x, want = oracle_run(cfg, batch, variant)
     layers = get_stack(cfg).layers
-    fuse = layout == "b64f"
-    dev = P.DeviceStack(layers, params, batch, code_layout="b64" if fuse else layout,
-                        fuse_down=fuse)
+    # "b64f": downsamples inside their joins; "...p": pools inside the convs
+    # that feed them, where a fused kernel covers the pair
+    fuse = layout in ("b64f", "b64p")
+    fpool = layout.endswith("p")
+    base = {"b64f": "b64", "b64p": "b64", "i8p": "i8"}.get(layout, layout)
+    dev = P.DeviceStack(layers, params, batch, code_layout=base, fuse_down=fuse,
+                        fuse_pool=fpool)
     if fuse:
         # every downsample of a ResNet-shaped stack is folded into its join
         assert len(dev.fused) == sum(1 for L in layers if L.name.endswith(".down"))
+    if fpool:
+        names = dev.layer_kernel_names()
+        for i, L in enumerate(dev.layers):
+            if L.name in dev.fused_pool:
+                assert dev._layers[i].kind == P.IFQ_LAYER_CONV_POOL and names[i]
     xd = dev.upload_input(x)
     y = dev.alloc_output()
     dev.run(xd, y)
@@ -54,11 +63,18 @@ def check_stack(P, cfg, batch, layout, variant):
     assert got.shape == want["y"].shape
     assert np.array_equal(got, want["y"]), "stack output differs"
     checked = 1
+    # the oracle keeps the last tensor written under each slot name; a slot
+    # is compared where the same layer wrote it last on both sides (fusions
+    # leave some names to other writers, or move a tensor to a slot of its own)
+    last_writer = {L.dst: L.name for L in layers}
     for name, (shape, lay, bits) in dev.tensor_info.items():
         if name in ("x", "y"):
             continue
+        orig, writer = dev.slot_origin[name]
+        if last_writer.get(orig) != writer:
+            continue
         g = dev.read_slot(name)
-        w = want[name]
+        w = want[orig]
         if lay == P.IFQ_LAYOUT_U2_NHWC_PACKED:
             w = olayout.pack2(w)
         elif lay == P.IFQ_LAYOUT_U2_BLOCK64:
@@ -76,7 +92,7 @@ def check_stack(P, cfg, batch, layout, variant):
 SMALL = [(0, 1), (1, 2), (2, 1), (3, 2), (4, 1)]
 
 
-@pytest.mark.parametrize("layout", ["i8", "u2", "b64", "b64f"])
+@pytest.mark.parametrize("layout", ["i8", "u2", "b64", "b64f", "b64p", "i8p"])
 @pytest.mark.parametrize("cfg,batch", SMALL)
 def test_stack_small_batch(P, cfg, batch, layout):
     for variant in ("calibrated", "plain"):
@@ -89,6 +105,14 @@ def test_stack_small_batch(P, cfg, batch, layout):
 def test_stack_full_size(P, cfg, layout):
     batch = get_stack(cfg).batch
     check_stack(P, cfg, batch, layout, "plain")
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("cfg", [4, 2])
+def test_stack_full_size_fused_pools(P, cfg):
+    # the benchmark's configuration of the stacks with pools: BLOCK64 codes,
+    # the 2x2/2 pools inside the convs that feed them
+    check_stack(P, cfg, get_stack(cfg).batch, "b64p", "plain")
 
 
 @pytest.mark.slow
