@@ -320,6 +320,49 @@ IFQ_API ifq_status ifq_fold_thresholds(const ifq_fold_params* p,
                                        int32_t* thr_out);
 
 /*
+ * Compact thresholds of a uniform quantizer (Sec. 3.3, Eq. 8): with
+ * q_i = i*base + offset for i = 1 .. 2^out_bits - 1, the moved thresholds of
+ * a channel are t_i = i*base' + offset', so one record per channel serves
+ * every bit width. In fp64, in exactly this order (sd = sqrt(var + eps),
+ * ab = alpha*beta_in):
+ *   base'   = ((base * sd) / gamma) / ab
+ *   offset' = ((((offset - bn_beta) * sd) / gamma + mean) - bias) / ab
+ *   s       = +1 (gamma > 0), -1 (gamma < 0), or 0 (gamma == 0: every code is
+ *             cstar = #{i : bn_beta > i*base + offset})
+ */
+typedef struct ifq_thr_compact {
+  double base;
+  double offset;
+  int32_t s;
+  int32_t cstar;
+} ifq_thr_compact;
+
+/*
+ * Fold one layer into compact records (host). p as for ifq_fold_thresholds,
+ * except that p->q_thr is not read: base > 0 and offset define the
+ * quantizer. out: host array of p->c_out records.
+ * Errors: INVALID_ARGUMENT as ifq_fold_thresholds, and base <= 0 or a
+ * non-finite base or offset.
+ */
+IFQ_API ifq_status ifq_fold_thresholds_compact(const ifq_fold_params* p, double base,
+                                               double offset, ifq_thr_compact* out);
+
+/*
+ * Expand compact records into the records ifq_conv_forward takes (Eq. 8 with
+ * a floor per threshold; the floor of i*base' + offset' is not affine in i,
+ * so it is taken for each i). Asynchronous on stream, device memory:
+ *   recs   c_out records (ifq_fold_thresholds_compact)
+ *   thr    c_out * 2^out_bits int32: {s, T_1 .. T_{R-1}} per channel with
+ *          T_i = clamp(floor(s * (i*base' + offset')), -B-1, B), the product
+ *          i*base' rounded before the sum; s = 0 becomes s = +1 with
+ *          T_i = -B-1 for i <= cstar and B above, B = k*(2^in_bits - 1)
+ * Errors: INVALID_ARGUMENT (NULL, c_out < 1, bits or k out of range), HIP.
+ */
+IFQ_API ifq_status ifq_expand_thresholds(const ifq_thr_compact* recs, int32_t c_out,
+                                         int32_t in_bits, int64_t k, int32_t out_bits,
+                                         int32_t* thr, hipStream_t stream);
+
+/*
  * Join coefficients (see ifq_join_params), fp64 in this order:
  *   p  = (gamma * (alpha*beta_in)) / sd
  *   c2 = (gamma * (bias - mean)) / sd + bn_beta

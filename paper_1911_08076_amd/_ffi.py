@@ -99,6 +99,8 @@ SIGNATURES = [
     ("ifq_packed_weight_bytes", size_t, [ctypes.POINTER(ConvDesc)]),
     ("ifq_pack_weights", i32, [ctypes.POINTER(ConvDesc), vp, vp, size_t]),
     ("ifq_fold_thresholds", i32, [ctypes.POINTER(FoldParams), vp]),
+    ("ifq_fold_thresholds_compact", i32, [ctypes.POINTER(FoldParams), f64, f64, vp]),
+    ("ifq_expand_thresholds", i32, [vp, i32, i32, i64, i32, vp, vp]),
     ("ifq_fold_join", i32, [ctypes.POINTER(JoinParams), vp]),
     ("ifq_fold_join_table", i32, [ctypes.POINTER(JoinParams), i32, i64, i32, i32,
                                   vp, vp]),

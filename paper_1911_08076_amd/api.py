@@ -114,6 +114,32 @@ def ifq_fold_thresholds(c_out, in_bits, out_bits, k, alpha, beta_in, q_thr,
     return out
 
 
+# One compact threshold record (ifq_thr_compact): base', offset', s, cstar.
+THR_COMPACT = np.dtype([("base", "<f8"), ("offset", "<f8"), ("s", "<i4"), ("cstar", "<i4")])
+
+
+def ifq_fold_thresholds_compact(c_out, in_bits, out_bits, k, alpha, beta_in, base, offset,
+                                bias=None, mean=None, var=None, gamma=None,
+                                bn_beta=None, eps=0.0):
+    """Compact records (THR_COMPACT, c_out of them) of a uniform quantizer
+    q_i = i*base + offset."""
+    arrs = [_f64(a) for a in (alpha, bias, mean, var, gamma, bn_beta)]
+    p = FoldParams(c_out, in_bits, out_bits, 0, int(k), _ptr(arrs[0]),
+                   float(beta_in), _ptr(arrs[1]), _ptr(arrs[2]), _ptr(arrs[3]),
+                   _ptr(arrs[4]), _ptr(arrs[5]), float(eps), None)
+    out = np.zeros(c_out, dtype=THR_COMPACT)
+    _check(_lib().ifq_fold_thresholds_compact(ctypes.byref(p), float(base), float(offset),
+                                              _ptr(out)), "ifq_fold_thresholds_compact")
+    return out
+
+
+def ifq_expand_thresholds(recs, c_out, in_bits, k, out_bits, thr, stream=None):
+    """Device: compact records -> int32 records [c_out][2^out_bits] in thr."""
+    _check(_lib().ifq_expand_thresholds(_ptr(recs), int(c_out), int(in_bits), int(k),
+                                        int(out_bits), _ptr(thr), _stream(stream)),
+           "ifq_expand_thresholds")
+
+
 def _join_params(kind, main, beta_x, down=None):
     m = {k: _f64(main.get(k)) for k in ("alpha", "bias", "mean", "var", "gamma",
                                           "bn_beta")}

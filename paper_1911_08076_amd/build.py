@@ -16,7 +16,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 SOURCES = ["ifq_api.cpp", "ifq_conv.hip", "ifq_conv_mfma.hip", "ifq_conv_halo.hip",
-           "ifq_conv_small.hip", "ifq_pool.hip"]
+           "ifq_conv_small.hip", "ifq_pool.hip", "ifq_thresholds.hip"]
 
 
 def build(verbose=False):

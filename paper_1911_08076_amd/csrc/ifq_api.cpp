@@ -363,6 +363,43 @@ ifq_status conv_args_check(const ifq_conv_desc* d, const void* x,
   return IFQ_OK;
 }
 
+// Checks of a fold's parameters shared by the table and the compact folds
+// (the quantizer thresholds only where need_q), before anything is written.
+ifq_status check_fold_params(const ifq_fold_params* p, bool need_q) {
+  if (p->c_out < 1) return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: c_out < 1");
+  if (p->in_bits < 1 || p->in_bits > 8)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: in_bits must be 1..8");
+  if (p->out_bits < 1 || p->out_bits > 4)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: out_bits must be 1..4");
+  if (p->k < 1 || p->k * ((1 << p->in_bits) - 1) >= kMaxIndex / 2)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: bad contraction length");
+  if (!p->alpha || (need_q && !p->q_thr))
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: alpha and q_thr are required");
+  if (!(p->beta_in > 0.0) || !is_finite(p->beta_in))
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: beta_in must be > 0");
+  if (!is_finite(p->eps)) return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: eps not finite");
+  const int nq = (1 << p->out_bits) - 1;
+  for (int i = 0; need_q && i < nq; ++i)
+    if (!is_finite(p->q_thr[i]) || (i > 0 && !(p->q_thr[i] > p->q_thr[i - 1])))
+      return fail(IFQ_ERR_INVALID_ARGUMENT,
+                  "fold: q_thr must be finite and strictly increasing");
+  for (int c = 0; c < p->c_out; ++c) {
+    const double al = p->alpha[c];
+    const double bi = p->bias ? p->bias[c] : 0.0;
+    const double mu = p->mean ? p->mean[c] : 0.0;
+    const double va = p->var ? p->var[c] : 1.0;
+    const double ga = p->gamma ? p->gamma[c] : 1.0;
+    const double be = p->bn_beta ? p->bn_beta[c] : 0.0;
+    if (!(al > 0.0) || !is_finite(al))
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: alpha[%d] must be > 0", c);
+    if (!is_finite(bi) || !is_finite(mu) || !is_finite(va) || !is_finite(ga) || !is_finite(be))
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: channel %d not finite", c);
+    if (!(va + p->eps > 0.0))
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: var[%d] + eps must be > 0", c);
+  }
+  return IFQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -452,40 +489,11 @@ IFQ_API ifq_status ifq_pack_weights(const ifq_conv_desc* d,
 IFQ_API ifq_status ifq_fold_thresholds(const ifq_fold_params* p,
                                        int32_t* thr_out) {
   if (!p || !thr_out) return fail(IFQ_ERR_INVALID_ARGUMENT, "NULL pointer");
-  if (p->c_out < 1) return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: c_out < 1");
-  if (p->in_bits < 1 || p->in_bits > 8)
-    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: in_bits must be 1..8");
-  if (p->out_bits < 1 || p->out_bits > 4)
-    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: out_bits must be 1..4");
-  if (p->k < 1 || p->k * ((1 << p->in_bits) - 1) >= kMaxIndex / 2)
-    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: bad contraction length");
-  if (!p->alpha || !p->q_thr)
-    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: alpha and q_thr are required");
-  if (!(p->beta_in > 0.0) || !is_finite(p->beta_in))
-    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: beta_in must be > 0");
-  if (!is_finite(p->eps)) return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: eps not finite");
+  ifq_status st = check_fold_params(p, true);
+  if (st != IFQ_OK) return st;
   const int nq = (1 << p->out_bits) - 1;
   const int rec = nq + 1;
-  for (int i = 0; i < nq; ++i)
-    if (!is_finite(p->q_thr[i]) || (i > 0 && !(p->q_thr[i] > p->q_thr[i - 1])))
-      return fail(IFQ_ERR_INVALID_ARGUMENT,
-                  "fold: q_thr must be finite and strictly increasing");
   const double bound = (double)p->k * (double)((1 << p->in_bits) - 1);
-  // validate every channel before writing anything
-  for (int c = 0; c < p->c_out; ++c) {
-    const double al = p->alpha[c];
-    const double bi = p->bias ? p->bias[c] : 0.0;
-    const double mu = p->mean ? p->mean[c] : 0.0;
-    const double va = p->var ? p->var[c] : 1.0;
-    const double ga = p->gamma ? p->gamma[c] : 1.0;
-    const double be = p->bn_beta ? p->bn_beta[c] : 0.0;
-    if (!(al > 0.0) || !is_finite(al))
-      return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: alpha[%d] must be > 0", c);
-    if (!is_finite(bi) || !is_finite(mu) || !is_finite(va) || !is_finite(ga) || !is_finite(be))
-      return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: channel %d not finite", c);
-    if (!(va + p->eps > 0.0))
-      return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: var[%d] + eps must be > 0", c);
-  }
   for (int c = 0; c < p->c_out; ++c) {
     const double alpha = p->alpha[c];
     const double bias = p->bias ? p->bias[c] : 0.0;
@@ -522,6 +530,65 @@ IFQ_API ifq_status ifq_fold_thresholds(const ifq_fold_params* p,
       rec_c[1 + i] = (int32_t)f;
     }
   }
+  return ok();
+}
+
+IFQ_API ifq_status ifq_fold_thresholds_compact(const ifq_fold_params* p, double base,
+                                               double offset, ifq_thr_compact* out) {
+  if (!p || !out) return fail(IFQ_ERR_INVALID_ARGUMENT, "NULL pointer");
+  ifq_status st = check_fold_params(p, false);
+  if (st != IFQ_OK) return st;
+  if (!(base > 0.0) || !is_finite(base) || !is_finite(offset))
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "fold: base must be > 0 and offset finite");
+  const int nq = (1 << p->out_bits) - 1;
+  for (int c = 0; c < p->c_out; ++c) {
+    const double alpha = p->alpha[c];
+    const double bias = p->bias ? p->bias[c] : 0.0;
+    const double mean = p->mean ? p->mean[c] : 0.0;
+    const double var = p->var ? p->var[c] : 1.0;
+    const double gamma = p->gamma ? p->gamma[c] : 1.0;
+    const double bn_beta = p->bn_beta ? p->bn_beta[c] : 0.0;
+    ifq_thr_compact& r = out[c];
+    r.base = 0.0;
+    r.offset = 0.0;
+    r.cstar = 0;
+    if (gamma == 0.0) {
+      r.s = 0;
+      for (int i = 1; i <= nq; ++i) {
+        double q = (double)i * base;
+        q = q + offset;
+        r.cstar += bn_beta > q ? 1 : 0;
+      }
+      continue;
+    }
+    r.s = gamma > 0.0 ? 1 : -1;
+    const double sd = std::sqrt(var + p->eps);
+    const double ab = alpha * p->beta_in;
+    double b = base * sd;
+    b = b / gamma;
+    r.base = b / ab;
+    double o = offset - bn_beta;
+    o = o * sd;
+    o = o / gamma;
+    o = o + mean;
+    o = o - bias;
+    r.offset = o / ab;
+  }
+  return ok();
+}
+
+IFQ_API ifq_status ifq_expand_thresholds(const ifq_thr_compact* recs, int32_t c_out,
+                                         int32_t in_bits, int64_t k, int32_t out_bits,
+                                         int32_t* thr, hipStream_t stream) {
+  if (!recs || !thr) return fail(IFQ_ERR_INVALID_ARGUMENT, "expand: NULL pointer");
+  if (c_out < 1 || in_bits < 1 || in_bits > 8 || out_bits < 1 || out_bits > 4 || k < 1 ||
+      k * ((1 << in_bits) - 1) >= kMaxIndex / 2)
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "expand: bad c_out, bits or k");
+  const double bound = (double)k * (double)((1 << in_bits) - 1);
+  ifq_status st = hip_status(ifq::launch_expand_thresholds(recs, c_out, out_bits, bound, thr,
+                                                           stream),
+                             "expand launch");
+  if (st != IFQ_OK) return st;
   return ok();
 }
 

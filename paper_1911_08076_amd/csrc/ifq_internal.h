@@ -178,6 +178,10 @@ struct PoolLaunch {
 
 hipError_t launch_pool(const PoolLaunch& a, hipStream_t stream);
 
+// Compact thresholds (Eq. 8) -> {s, T_1..T_nq} records of c_out channels.
+hipError_t launch_expand_thresholds(const ifq_thr_compact* recs, int c_out, int out_bits,
+                                    double bound, int32_t* thr, hipStream_t stream);
+
 hipError_t launch_convert(int64_t n, int64_t hw, int32_t c, int32_t src_layout,
                           int32_t dst_layout, const void* src, void* dst,
                           hipStream_t stream);

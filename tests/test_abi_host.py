@@ -624,3 +624,35 @@ def test_stack_rejects_bad_layer_kind_and_slots():
     st.layers[0].dst = 0          # writing the input slot
     assert lib.ifq_run_stack(ctypes.byref(st), FAKE, FAKE, FAKE, 1 << 20,
                              None) == EINVAL
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_compact_fold_matches_oracle(bits):
+    # the library's host fold of the compact records (Eq. 8) and the
+    # oracle's, written separately, agree to the last bit
+    from oracle import compact
+    from workloads import Conv, layer_params
+    from workloads.gen import STEP
+    L = Conv("cf", "x", "y", 9, 9, 64, 96, 3, 1, 1, 2, bits, None)
+    p = dict(layer_params(77, 0, L, "calibrated"))
+    p["gamma"] = np.array(p["gamma"], dtype=np.float64)
+    p["gamma"][5] = 0.0                      # the constant-code case
+    got = P.ifq_fold_thresholds_compact(L.cout, 2, bits, 9 * L.cin, p["alpha"], p["beta_in"],
+                                        STEP, -STEP / 2, bias=p["bias"], mean=p["mean"],
+                                        var=p["var"], gamma=p["gamma"], bn_beta=p["bn_beta"],
+                                        eps=p["eps"])
+    want = compact.fold_compact(p, STEP, -STEP / 2, bits)
+    for f in ("base", "offset", "s", "cstar"):
+        assert np.array_equal(got[f], want[f]), f
+    assert (got["s"] == -1).any() and got["s"][5] == 0
+
+
+def test_compact_fold_rejects_bad_quantizer():
+    a = np.ones(4)
+    for base, offset in ((0.0, 0.0), (-0.5, 0.0), (float("nan"), 0.0), (0.5, float("inf"))):
+        with pytest.raises(P.IfqError):
+            P.ifq_fold_thresholds_compact(4, 2, 2, 9, a, 0.5, base, offset)
+    st = status_of("ifq_expand_thresholds", FAKE, 0, 2, 9, 2, FAKE, None)
+    assert st == EINVAL
+    st = status_of("ifq_expand_thresholds", FAKE, 4, 2, 9, 5, FAKE, None)
+    assert st == EINVAL

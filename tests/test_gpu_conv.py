@@ -42,6 +42,15 @@ LAYERS = [
     ("cout384_cin384", 1, 13, 13, 384, 384, 3, 1, 1, 2, 2),
     ("valid_no_pad", 1, 10, 10, 64, 64, 3, 1, 0, 2, 2),
     ("8bit_cin16", 1, 10, 10, 16, 32, 3, 2, 1, 8, 2),
+    # k-bit activations (Table 2/3 variants: 3 and 4 bits, 7 and 15 thresholds)
+    ("in3_out3", 2, 11, 9, 64, 96, 3, 1, 1, 3, 3),
+    ("in2_out3", 1, 9, 9, 128, 64, 3, 1, 1, 2, 3),
+    ("in3_out4_5x5", 1, 9, 9, 96, 64, 5, 1, 2, 3, 4),
+    ("in4_out2_s2", 2, 12, 12, 64, 64, 3, 2, 1, 4, 2),
+    # AlexNet's fully connected layers as convs over the 6x6x256 pool5 output
+    # (FC6: one 6x6 window) and over FC6's 1x1x4096 output (FC7), batch 32
+    ("fc6_as_6x6_conv", 32, 6, 6, 256, 4096, 6, 1, 0, 2, 2),
+    ("fc7_as_1x1_conv", 32, 1, 1, 4096, 4096, 1, 1, 0, 2, 2),
 ]
 
 
@@ -59,6 +68,26 @@ def test_conv_layer_bit_exact(P, case):
     if ob:
         # the codes use more than one level (the comparison has teeth)
         assert len(np.unique(want)) > 1
+
+
+FC_U2 = [("fc6_u2", 32, 6, 6, 256, 4096, 6), ("fc7_u2", 32, 1, 1, 4096, 4096, 1)]
+
+
+@pytest.mark.parametrize("case", FC_U2, ids=[c[0] for c in FC_U2])
+def test_fc_as_conv_on_mfma_path(P, case):
+    # the same layers from 2-bit packed codes: the MFMA kernel takes any kh x kw
+    name, n, h, w, cin, cout, k = case
+    L = make_layer(name, h, w, cin, cout, k, 1, 0, 2, 2)
+    d = P.conv_desc(n, h, w, cin, cout, k, 1, 0, 2, 2, U2, U2)
+    assert P.ifq_conv_kernel_name(d).startswith("conv_mfma<")
+    seed = zlib.crc32(name.encode()) % 997
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, w, cin), 2)
+    want_acc, want = oracle_layer(L, x, p)
+    acc, got = gpu_layer(P, L, n, x, p, in_layout=U2, out_layout=U2)
+    assert np.array_equal(acc, want_acc), name
+    assert np.array_equal(got, expect_layout(want, U2)), name
+    assert len(np.unique(want)) > 1
 
 
 # 8-bit input with c_in <= 4 (a detector's first layer) runs the small-channel

@@ -120,3 +120,37 @@ def test_stack_full_size_fused_downsample(P):
     # the benchmark's configuration: ResNet-18 body, batch 64, BLOCK64 codes,
     # downsample convs inside their joins
     check_stack(P, 3, get_stack(3).batch, "b64f", "plain")
+
+
+@pytest.mark.parametrize("bits", [3, 4])
+def test_kbit_alexnet_body(P, bits):
+    # the AlexNet body with k-bit activations (the k = 3, 4 networks of
+    # Tables 2-3): every conv takes and gives k-bit codes (one byte each), the
+    # pools run on them; the generic path and the k-bit folds, end to end
+    import dataclasses
+    import torch
+    from oracle import core
+    from oracle.stack import conv_layer
+    from workloads import Conv, layer_params, stack_input
+    cfg = get_stack(1)
+    layers = [dataclasses.replace(L, in_bits=bits, out_bits=bits) if isinstance(L, Conv)
+              else dataclasses.replace(L, bits=bits) for L in cfg.layers]
+    batch = 2
+    params = [layer_params(1, i, L, "calibrated") if isinstance(L, Conv) else None
+              for i, L in enumerate(layers)]
+    L0 = layers[0]
+    x = stack_input(1, (batch, L0.h, L0.w, L0.cin), bits)
+    slots = {"x": x}
+    for i, L in enumerate(layers):
+        if isinstance(L, Conv):
+            slots[L.dst], _ = conv_layer(L, slots[L.src], params[i])
+        else:
+            slots[L.dst] = core.maxpool(slots[L.src], L.k, L.stride, L.mode)
+    dev = P.DeviceStack(layers, params, batch, code_layout="i8")
+    xd = dev.upload_input(x)
+    y = dev.alloc_output()
+    dev.run(xd, y)
+    torch.cuda.synchronize()
+    got = dev.download_output(y)
+    assert np.array_equal(got, slots["y"])
+    assert got.max() > 3   # codes beyond the 2-bit range occur
