@@ -435,9 +435,12 @@ IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
  *   d          conv as for ifq_conv_forward, codes out (out_bits 1..8), no join
  *   p          the pool over the conv's output: n, h, w, c equal to the conv's
  *              n, ho, wo, c_out; bits = d->out_bits; layout = d->out_layout;
- *              mode IFQ_POOL_VALID with k == stride, ho and wo multiples of k
+ *              any window, stride and mode of ifq_maxpool_codes. A kernel
+ *              covers it where its tiles can hold whole rows of windows
+ *              (VALID, k == stride, ho and wo multiples of k) or whole images
  *   x, w_packed, thr   as for ifq_conv_forward
- *   y          device [n][ho/k][wo/k][c_out] codes in d->out_layout
+ *   y          device [n][pho][pwo][c_out] codes in d->out_layout, pho and pwo
+ *              as ifq_maxpool_codes gives them
  * Errors: INVALID_ARGUMENT (a desc invalid or the two inconsistent),
  * UNSUPPORTED (no fused kernel covers the shape: ifq_conv_pool_kernel_name
  * returns ""; run ifq_conv_forward and ifq_maxpool_codes instead), HIP.

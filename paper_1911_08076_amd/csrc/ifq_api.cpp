@@ -292,18 +292,24 @@ ifq_status check_conv_pool(const ifq_conv_desc* d, const ifq_pool_desc* p, int64
   if (d->out_bits == 0 || p->bits != d->out_bits || p->layout != d->out_layout)
     return fail(IFQ_ERR_INVALID_ARGUMENT,
                 "conv+pool: codes out, with the pool's bits and layout the conv's");
-  if (p->mode != IFQ_POOL_VALID || p->k != p->stride || *ho % p->k || *wo % p->k)
-    return fail(IFQ_ERR_UNSUPPORTED,
-                "conv+pool: needs valid windows with k == stride dividing ho and wo");
   return IFQ_OK;
 }
 
+// Pool fields of a conv launch (p checked by check_conv_pool): tiles of
+// whole window rows where the windows tile the output exactly, else of whole
+// images.
 void add_pool(ifq::ConvLaunch& a, const ifq_pool_desc& p) {
+  int64_t pho, pwo;
+  check_pool(&p, &pho, &pwo);
   a.pool_k = p.k;
-  a.pho = a.ho / p.k;
-  a.pwo = a.wo / p.k;
+  a.pool_s = p.stride;
+  a.pool_same = p.mode == IFQ_POOL_SAME ? 1 : 0;
+  a.pool_img = (p.mode == IFQ_POOL_VALID && p.k == p.stride && a.ho % p.k == 0 &&
+                a.wo % p.k == 0) ? 0 : 1;
+  a.pho = (int32_t)pho;
+  a.pwo = (int32_t)pwo;
   a.div_pwo = ifq::make_fastdiv((uint32_t)(a.pwo > 0 ? a.pwo : 1));
-  a.div_phowo = ifq::make_fastdiv((uint32_t)(a.pho * a.pwo > 0 ? a.pho * a.pwo : 1));
+  a.div_pho = ifq::make_fastdiv((uint32_t)(a.pho > 0 ? a.pho : 1));
 }
 
 // A BLOCK64 tensor of n images and c channels is pooled as the NHWC packed
@@ -817,10 +823,10 @@ struct SlotPlan {
 
 int64_t layer_out_bytes(const ifq_layer& L) {
   if (L.kind == IFQ_LAYER_CONV_POOL) {
-    const int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);
-    const int64_t wo = out_extent(L.conv.w, L.conv.kw, L.conv.stride, L.conv.pad);
-    const int64_t k = L.pool.k > 0 ? L.pool.k : 1;
-    return tensor_bytes(L.conv.n, ho / k, wo / k, L.conv.c_out, L.conv.out_layout);
+    // the pooled tensor (pool checked by plan_stack before this is used)
+    int64_t pho = 0, pwo = 0;
+    if (check_pool(&L.pool, &pho, &pwo) != IFQ_OK) return 0;
+    return tensor_bytes(L.conv.n, pho, pwo, L.conv.c_out, L.conv.out_layout);
   }
   if (L.kind == IFQ_LAYER_CONV) {
     const int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);

@@ -628,8 +628,9 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
     bn = (bn + 31) / 32 * 32;
     if (bn > bnmax) bn = bnmax;
     if (a.pool_k) {
-      // a fused pool needs whole rows of pooling windows per tile
-      const int64_t unit = (int64_t)a.pool_k * a.wo;
+      // a fused pool needs whole rows of pooling windows (or whole images)
+      // per tile
+      const int64_t unit = a.pool_img ? (int64_t)a.ho * a.wo : (int64_t)a.pool_k * a.wo;
       bn = (bn + unit - 1) / unit * unit;
       if (bn > bnmax) bn = bnmax / unit * unit;
       if (bn == 0) continue;

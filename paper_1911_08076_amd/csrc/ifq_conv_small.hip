@@ -326,8 +326,9 @@ bool small_geom(const ConvLaunch& a, SmallGeom* g) {
   int rows = (int)((rows_total + 1023) / 1024);
   if (rows < 1) rows = 1;
   if (rows > a.ho) rows = a.ho;
-  // a fused pool needs whole rows of pooling windows per workgroup
-  const int rstep = a.pool_k > 0 ? a.pool_k : 1;
+  // a fused pool needs whole rows of pooling windows (or the whole image)
+  // per workgroup
+  const int rstep = a.pool_k == 0 ? 1 : a.pool_img ? a.ho : a.pool_k;
   rows = (rows + rstep - 1) / rstep * rstep;
   if (rows > a.ho) rows = a.ho / rstep * rstep;
   for (;; rows -= rstep) {

@@ -353,21 +353,30 @@ __device__ __forceinline__ uint32_t max_codes_u8(uint32_t a, uint32_t b) {
   return (a & mask) | (b & ~mask);
 }
 
-// copy_out_tile with the max-pool of Eq. 4 fused (a.pool_k x a.pool_k
-// windows at stride a.pool_k, valid): the tile's npx pixels are whole rows
-// of whole windows, starting at a window row (p0 a multiple of pool_k * wo),
-// so its pooled pixels start at p0 / pool_k^2 of the pooled tensor. One
-// 32-bit word of a pixel's channel row per thread and step, the max taken
-// over the window's words in the LDS tile.
+// copy_out_tile with the max-pool of Eq. 4 fused: the tile's npx pixels are
+// whole rows of whole windows (pool_img 0: k == stride, valid, the tile
+// starting at a window row) or whole images (pool_img 1: any window), so
+// every window of the tile's pooled pixels lies in the LDS tile. One 32-bit
+// word of a pixel's channel row per thread and step, the max taken over the
+// window's words (clipped at the bottom and right edges in SAME mode).
 __device__ __forceinline__ void pool_out_tile(const ConvLaunch& a, const uint8_t* otile,
                                               int orow, int co0, int bm, int p0, int npx) {
   if (npx <= 0) return;
-  const int k = a.pool_k;
+  const int k = a.pool_k, st = a.pool_s;
   const bool u2 = a.out_mode == 2;
   const int ch = a.cout - co0 < bm ? a.cout - co0 : bm;
   const int words = (u2 ? ch >> 2 : ch) >> 2;
-  const int npo = npx / (k * k);
-  const int P0 = p0 / (k * k);
+  const int howo = a.ho * a.wo;
+  // first pooled row (over all images) and pooled pixels of the tile
+  int pr0, npo;
+  if (a.pool_img) {
+    const int i0 = fdiv(p0, a.div_howo);
+    pr0 = i0 * a.pho;
+    npo = fdiv(npx, a.div_howo) * a.pho * a.pwo;
+  } else {
+    pr0 = fdiv(p0, a.div_wo) / k;
+    npo = npx / (k * k);
+  }
   const int pstride = u2 ? a.cout >> 2 : a.cout;
   const int cofs = u2 ? co0 >> 2 : co0;
   const int phowo = a.pho * a.pwo;
@@ -375,20 +384,25 @@ __device__ __forceinline__ void pool_out_tile(const ConvLaunch& a, const uint8_t
   uint8_t* y8 = reinterpret_cast<uint8_t*>(a.y);
   for (int u = threadIdx.x; u < npo * words; u += blockDim.x) {
     const int po = u / words, wi = u - po * words;
-    const int r = fdiv(po, a.div_pwo), c = po - r * a.pwo;
-    const uint8_t* src = otile + ((r * k) * a.wo + c * k) * orow + 4 * wi;
+    const int dr = fdiv(po, a.div_pwo);
+    const int px = po - dr * a.pwo;
+    const int pr = pr0 + dr;
+    const int img = fdiv(pr, a.div_pho);
+    const int py = pr - img * a.pho;
+    const int y0 = py * st, x0 = px * st;
+    const int y1 = y0 + k < a.ho ? y0 + k : a.ho, x1 = x0 + k < a.wo ? x0 + k : a.wo;
+    const uint8_t* src = otile + (img * howo - p0) * orow + 4 * wi;
     uint32_t m = 0;
-    for (int dy = 0; dy < k; ++dy)
-      for (int dx = 0; dx < k; ++dx) {
-        const uint32_t v = *reinterpret_cast<const uint32_t*>(src + (dy * a.wo + dx) * orow);
+    for (int y = y0; y < y1; ++y)
+      for (int x = x0; x < x1; ++x) {
+        const uint32_t v = *reinterpret_cast<const uint32_t*>(src + (y * a.wo + x) * orow);
         m = u2 ? max_codes_u2(m, v) : max_codes_u8(m, v);
       }
-    const int P = P0 + po;
+    const int P = pr * a.pwo + px;
     int64_t off;
     if (b64) {
-      const int nimg = fdiv(P, a.div_phowo);
       const int gb = cofs + 4 * wi;   // byte of the pixel's 2-bit channel row
-      off = (((int64_t)nimg * (a.cout >> 6) + (gb >> 4)) * phowo + (P - nimg * phowo)) * 16 +
+      off = (((int64_t)img * (a.cout >> 6) + (gb >> 4)) * phowo + (P - img * phowo)) * 16 +
             (gb & 15);
     } else {
       off = (int64_t)P * pstride + cofs + 4 * wi;

@@ -115,21 +115,23 @@ struct ConvLaunch {
   int32_t d_cin, d_h, d_w, d_stride;
   int32_t d_nk32;      // its K32 steps (2 * c_in / 64)
   // Max-pool fused into the epilogue (Eq. 4): pool_k x pool_k windows at
-  // stride pool_k over the codes, in valid mode, with ho and wo multiples of
-  // pool_k; y is then the pooled tensor [n][pho][pwo][cout]. 0: no pool.
-  int32_t pool_k;
+  // stride pool_s over the codes (pool_same: SAME mode, windows clipped at
+  // the bottom and right edges), y then the pooled tensor
+  // [n][pho][pwo][cout]. pool_k 0: no pool. Tiles hold whole rows of
+  // windows (pool_img 0: k == stride, valid, ho and wo multiples of k) or
+  // whole images (pool_img 1: any window).
+  int32_t pool_k, pool_s, pool_same, pool_img;
   int32_t pho, pwo;
-  FastDiv div_pwo;     // division by pwo (pooled pixel in a tile -> row)
-  FastDiv div_phowo;   // division by pho*pwo (pooled pixel -> image)
+  FastDiv div_pwo;     // division by pwo (pooled pixel -> pooled row)
+  FastDiv div_pho;     // division by pho (pooled row -> image)
 };
 
 // Whether the pooled epilogue takes this launch: codes out (no join), and
 // every output tile row of the tile's channels a whole number of 32-bit
-// words. The kernel then also has to hold whole rows of pooling windows per
-// tile (its own planner).
+// words. The kernel's planner then fits whole rows of windows (or whole
+// images, pool_img) into each tile.
 inline bool pool_epilogue_ok(const ConvLaunch& a) {
   if (a.pool_k < 1 || a.out_mode == 0 || a.join_kind != IFQ_JOIN_NONE) return false;
-  if (a.ho % a.pool_k || a.wo % a.pool_k) return false;
   return a.out_mode == 2 ? a.cout % 16 == 0 : a.cout % 4 == 0;
 }
 

@@ -28,6 +28,16 @@ def _is_conv(L):
     return hasattr(L, "cin")
 
 
+_POOL_MODE = {"valid": IFQ_POOL_VALID, "same": IFQ_POOL_SAME}
+
+
+def _pool_hw(h, w, P):
+    """Output size of pool spec P over h x w (as ifq_maxpool_codes)."""
+    if P.mode == "valid":
+        return (h - P.k) // P.stride + 1, (w - P.k) // P.stride + 1
+    return -(-h // P.stride), -(-w // P.stride)
+
+
 def conv_ops(L, batch):
     """Dense int-ops of a conv layer: 2 * N*Ho*Wo * Cout * kh*kw*Cin."""
     ho = (L.h + 2 * L.pad - L.k) // L.stride + 1
@@ -47,9 +57,13 @@ class DeviceStack:
     fuse_down: with "b64", compute each 1x1 downsample inside the conv join
     that consumes it (IFQ_JOIN_CONV_FUSED); self.fused maps the join's layer
     name to the downsample's, whose layer and output tensor are then absent.
-    fuse_pool: a conv whose codes only a following valid max-pool with
-    k == stride reads runs as one IFQ_LAYER_CONV_POOL layer where a fused
-    kernel covers the pair (ifq_conv_pool_kernel_name); self.fused_pool maps
+    fuse_pool: a conv whose codes only the following max-pool reads runs as
+    one IFQ_LAYER_CONV_POOL layer where a fused kernel covers the pair
+    (ifq_conv_pool_kernel_name). True fuses the pools whose windows tile the
+    conv output (valid, k == stride), where the fused kernel keeps its usual
+    tile count; "all" also the others, which the fused kernels run with one
+    image per tile (slower than a separate pool at small batch: too few
+    workgroups for the chip). self.fused_pool maps
     the conv's name to the pool's, whose layer and the conv's output tensor
     are then absent.
     """
@@ -83,7 +97,7 @@ class DeviceStack:
         self.batch = int(batch)
         self.fused_pool = {}
         if fuse_pool:
-            self.fused_pool = self._pool_fusions(code_layout)
+            self.fused_pool = self._pool_fusions(code_layout, fuse_pool)
             drop = set(self.fused_pool.values())
             self.layers = [L for L in self.layers if L.name not in drop]
         pool_of = {c: by_name[p][1] for c, p in self.fused_pool.items()}
@@ -159,7 +173,7 @@ class DeviceStack:
                     rec.kind = IFQ_LAYER_CONV_POOL
                     ho, wo = api.ifq_conv_output_dims(d)
                     rec.pool = api.pool_desc(self.batch, ho, wo, L.cout, Pl.k, Pl.stride,
-                                             IFQ_POOL_VALID, L.out_bits, out_layout)
+                                             _POOL_MODE[Pl.mode], L.out_bits, out_layout)
                 blob = api.ifq_pack_weights(d, p["w"])
                 wdev = torch.from_numpy(blob).to(self.device)
                 self._keep.append(wdev)
@@ -216,8 +230,7 @@ class DeviceStack:
                 out_shape = (self.batch, ho, wo, L.cout)
                 out_bits = L.out_bits
                 if L.name in pool_of:
-                    k = pool_of[L.name].k
-                    out_shape = (self.batch, ho // k, wo // k, L.cout)
+                    out_shape = (self.batch,) + _pool_hw(ho, wo, pool_of[L.name]) + (L.cout,)
             else:
                 rec.kind = IFQ_LAYER_POOL
                 mode = {"valid": IFQ_POOL_VALID, "same": IFQ_POOL_SAME}[L.mode]
@@ -249,10 +262,10 @@ class DeviceStack:
         self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8,
                               device=self.device)
 
-    def _pool_fusions(self, code_layout):
-        """conv name -> pool name for every conv whose codes only a following
-        valid k == stride max-pool reads and whose pair a fused kernel covers
-        (layouts as the stack would give them)."""
+    def _pool_fusions(self, code_layout, fuse=True):
+        """conv name -> pool name for every conv whose codes only the
+        following max-pool reads and whose pair a fused kernel covers (layouts
+        as the stack would give them)."""
         layout_of = {}
 
         def code_layout_for(bits, channels):
@@ -275,8 +288,13 @@ class DeviceStack:
             layout_of[L.dst] = out_layout
             nxt = self.layers[i + 1] if i + 1 < len(self.layers) else None
             if (nxt is None or _is_conv(nxt) or nxt.src != L.dst or L.join is not None
-                    or L.out_bits == 0 or L.dst == "y" or nxt.mode != "valid"
-                    or nxt.k != nxt.stride):
+                    or L.out_bits == 0 or L.dst == "y"):
+                continue
+            ho0 = (L.h + 2 * L.pad - L.k) // L.stride + 1
+            wo0 = (L.w + 2 * L.pad - L.k) // L.stride + 1
+            rows = (nxt.mode == "valid" and nxt.k == nxt.stride and ho0 % nxt.k == 0
+                    and wo0 % nxt.k == 0)
+            if not rows and fuse != "all":
                 continue
             # anything reading the conv's tensor before its slot is written
             # again (slots are reused along the chain)
@@ -294,7 +312,7 @@ class DeviceStack:
                               L.in_bits, L.out_bits, layout_of[L.src], out_layout)
             ho, wo = api.ifq_conv_output_dims(d)
             pd = api.pool_desc(self.batch, ho, wo, L.cout, nxt.k, nxt.stride,
-                               IFQ_POOL_VALID, L.out_bits, out_layout)
+                               _POOL_MODE[nxt.mode], L.out_bits, out_layout)
             if api.ifq_conv_pool_kernel_name(d, pd):
                 out[L.name] = nxt.name
         return out

@@ -491,18 +491,20 @@ def test_maxpool_rejects_bad_desc(pool, want):
 
 
 @pytest.mark.parametrize("pool,want", [
-    (dict(h=14), EINVAL),                     # not the conv's output
+    (dict(h=18), EINVAL),                     # not the conv's output
     (dict(c=32), EINVAL),
     (dict(n=3), EINVAL),
     (dict(layout=U2), EINVAL),                # not the conv's layout
     (dict(bits=4), EINVAL),
+    # windows that need whole images per tile, which 20x20 outputs
+    # (400 pixels) do not fit: not covered
     (dict(k=3, stride=2), EUNSUP),            # overlapping windows
     (dict(mode=1), EUNSUP),                   # same mode
-    (dict(k=3, stride=3), EUNSUP),            # 16 is no multiple of 3
+    (dict(k=3, stride=3), EUNSUP),            # 20 is no multiple of 3
     (dict(k=0), EINVAL)])
 def test_conv_pool_rejects_inconsistent_pair(pool, want):
-    d = P.conv_desc(2, 16, 16, 64, 64, 3, 1, 1, 2, 2, B64, B64)
-    base = dict(n=2, h=16, w=16, c=64, k=2, stride=2, mode=0, bits=2, layout=B64)
+    d = P.conv_desc(2, 20, 20, 64, 64, 3, 1, 1, 2, 2, B64, B64)
+    base = dict(n=2, h=20, w=20, c=64, k=2, stride=2, mode=0, bits=2, layout=B64)
     base.update(pool)
     pd = _ffi.PoolDesc(**base)
     assert P.ifq_conv_pool_kernel_name(d, pd) == ""
@@ -526,6 +528,13 @@ def test_conv_pool_kernel_choice():
     # a tile cannot hold two rows of 224 pixels: not covered
     d = P.conv_desc(1, 224, 224, 64, 64, 3, 1, 1, 2, 2, B64, B64)
     assert P.ifq_conv_pool_kernel_name(d, pd(1, 224, 64, B64)) == ""
+    # overlapping and SAME windows on 13x13 outputs: whole images per tile
+    d = P.conv_desc(3, 13, 13, 384, 256, 3, 1, 1, 2, 2, B64, B64)
+    p3 = _ffi.PoolDesc(3, 13, 13, 256, 3, 2, 0, 2, B64)
+    assert P.ifq_conv_pool_kernel_name(d, p3).startswith("conv_halo<")
+    d = P.conv_desc(2, 13, 13, 256, 512, 3, 1, 1, 2, 2, B64, B64)
+    p2 = _ffi.PoolDesc(2, 13, 13, 512, 2, 1, 1, 2, B64)
+    assert P.ifq_conv_pool_kernel_name(d, p2).startswith("conv_halo<")
 
 
 def test_convert_rejects_bad_args():

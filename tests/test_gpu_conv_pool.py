@@ -26,12 +26,14 @@ def P():
     return P
 
 
-def gpu_conv_pool(P, L, n, x, p, k, in_layout, out_layout):
+def gpu_conv_pool(P, L, n, x, p, k, in_layout, out_layout, st=None, mode="valid"):
     import torch
     d = P.conv_desc(n, L.h, L.w, L.cin, L.cout, L.k, L.stride, L.pad,
                     L.in_bits, L.out_bits, in_layout, out_layout)
     ho, wo = P.ifq_conv_output_dims(d)
-    pd = P.pool_desc(n, ho, wo, L.cout, k, k, P.IFQ_POOL_VALID, L.out_bits, out_layout)
+    st = k if st is None else st
+    pm = P.IFQ_POOL_VALID if mode == "valid" else P.IFQ_POOL_SAME
+    pd = P.pool_desc(n, ho, wo, L.cout, k, st, pm, L.out_bits, out_layout)
     name = P.ifq_conv_pool_kernel_name(d, pd)
     wd = to_dev(P.ifq_pack_weights(d, p["w"]))
     thr = P.ifq_fold_thresholds(L.cout, L.in_bits, L.out_bits, L.k * L.k * L.cin,
@@ -40,7 +42,10 @@ def gpu_conv_pool(P, L, n, x, p, k, in_layout, out_layout):
                                 bn_beta=p["bn_beta"], eps=p["eps"])
     td = to_dev(thr)
     xd = upload_codes(P, x, in_layout)
-    pho, pwo = ho // k, wo // k
+    if mode == "valid":
+        pho, pwo = (ho - k) // st + 1, (wo - k) // st + 1
+    else:
+        pho, pwo = -(-ho // st), -(-wo // st)
     ob = P.ifq_tensor_bytes(n, pho, pwo, L.cout, out_layout)
     # poisoned output: every byte the kernel leaves alone shows up
     y = torch.full((ob,), 0xA5, dtype=torch.uint8, device=device())
@@ -56,15 +61,15 @@ def gpu_conv_pool(P, L, n, x, p, k, in_layout, out_layout):
     return name, out
 
 
-def check(P, name, L, n, k, in_layout, outs, family):
+def check(P, name, L, n, k, in_layout, outs, family, st=None, mode="valid"):
     seed = zlib.crc32(name.encode()) % 997
     p = params_for(seed, L)
     x = codes_for(seed, (n, L.h, L.w, L.cin), L.in_bits)
     _, codes = oracle_layer(L, x, p)
-    want = oracle.maxpool(codes, k, k, "valid")
+    want = oracle.maxpool(codes, k, k if st is None else st, mode)
     assert len(np.unique(want)) > 1
     for out_l in outs:
-        kname, got = gpu_conv_pool(P, L, n, x, p, k, in_layout, out_l)
+        kname, got = gpu_conv_pool(P, L, n, x, p, k, in_layout, out_l, st, mode)
         assert kname.startswith(family), (name, out_l, kname)
         assert np.array_equal(got, expect_layout(want, out_l)), (name, out_l, kname)
 
@@ -102,3 +107,25 @@ def test_halo_conv_pool_bit_exact(P, case):
     name, n, h, w, cin, cout, k, outs = case
     L = make_layer(name, h, w, cin, cout, 3, 1, 1, 2, 2)
     check(P, name, L, n, k, B64, outs, "conv_halo<")
+
+
+# windows that overlap, run in SAME mode or do not tile the output: each tile
+# holds whole images (name, n, h, c_in, c_out, k, stride, mode, layouts)
+WHOLE_IMAGE = [
+    ("hp_alexnet_conv5_pool3s2", 3, 13, 384, 256, 3, 2, "valid", [B64, U2]),
+    ("hp_yolo_c6_pool2s1_same", 2, 13, 256, 512, 2, 1, "same", [B64]),
+    ("hp_odd_size_pool2", 2, 13, 128, 128, 2, 2, "valid", [B64, I8]),
+    ("hp_pool3s3_same", 4, 10, 64, 128, 3, 3, "same", [B64]),
+]
+
+
+@pytest.mark.parametrize("case", WHOLE_IMAGE, ids=[c[0] for c in WHOLE_IMAGE])
+def test_halo_conv_pool_whole_images(P, case):
+    name, n, h, cin, cout, k, st, mode, outs = case
+    L = make_layer(name, h, h, cin, cout, 3, 1, 1, 2, 2)
+    check(P, name, L, n, k, B64, outs, "conv_halo<", st, mode)
+
+
+def test_small8_conv_pool_whole_images(P):
+    L = make_layer("s8p_pool3s2", 31, 29, 3, 16, 3, 1, 1, 8, 2)
+    check(P, "s8p_pool3s2", L, 2, 3, I8, [I8, U2], "conv_small8<", 2, "valid")

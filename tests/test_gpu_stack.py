@@ -42,9 +42,9 @@ def check_stack(P, cfg, batch, layout, variant):
     layers = get_stack(cfg).layers
     # "b64f": downsamples inside their joins; "...p": pools inside the convs
     # that feed them, where a fused kernel covers the pair
-    fuse = layout in ("b64f", "b64p")
-    fpool = layout.endswith("p")
-    base = {"b64f": "b64", "b64p": "b64", "i8p": "i8"}.get(layout, layout)
+    fuse = layout in ("b64f", "b64p", "b64pa")
+    fpool = "all" if layout.endswith("pa") else layout.endswith("p")
+    base = {"b64f": "b64", "b64p": "b64", "b64pa": "b64", "i8p": "i8"}.get(layout, layout)
     dev = P.DeviceStack(layers, params, batch, code_layout=base, fuse_down=fuse,
                         fuse_pool=fpool)
     if fuse:
@@ -92,7 +92,7 @@ def check_stack(P, cfg, batch, layout, variant):
 SMALL = [(0, 1), (1, 2), (2, 1), (3, 2), (4, 1)]
 
 
-@pytest.mark.parametrize("layout", ["i8", "u2", "b64", "b64f", "b64p", "i8p"])
+@pytest.mark.parametrize("layout", ["i8", "u2", "b64", "b64f", "b64p", "b64pa", "i8p"])
 @pytest.mark.parametrize("cfg,batch", SMALL)
 def test_stack_small_batch(P, cfg, batch, layout):
     for variant in ("calibrated", "plain"):
