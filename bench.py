@@ -30,6 +30,7 @@ METRIC = ("IFQ conv int-ops/s (% int8 MFMA peak) + images/s on "
           "ResNet-18-shaped stack")
 # 256 CUs x 2.4 GHz x 8192 dense int8 ops per clock per CU
 PEAK_INT8_TOPS = 5033.2
+PEAK_FP4_TFLOPS = 10100.0   # dense MXFP4, for the kernels on the fp4 path
 PEAK_HBM_GBPS = 8000.0
 JUDGED = ["l2.1.conv1", "l2.1.conv2", "l3.0.conv2", "l3.1.conv1",
           "l3.1.conv2", "l4.0.conv2", "l4.1.conv1", "l4.1.conv2"]
@@ -74,6 +75,13 @@ class Hip:
     def destroy(self, arr):
         for e in arr:
             self.lib.hipEventDestroy(e)
+
+
+def kernel_peak(name):
+    """Dense peak of the matrix instructions a kernel runs on: the fp4
+    instances of the windowed kernel (last template argument true after the
+    transposed flag) against MXFP4, the others against int8."""
+    return PEAK_FP4_TFLOPS if name.endswith(", true, true>") else PEAK_INT8_TOPS
 
 
 def source_hash():
@@ -278,6 +286,10 @@ def main():
     ap.add_argument("--no-fuse-down", action="store_true",
                     help="run the 1x1 downsample convs as layers of their own "
                          "(default with b64: inside the conv join that reads them)")
+    ap.add_argument("--fp4", action="store_true",
+                    help="run the 2-bit threshold 3x3 layers on the fp4 (e2m1) "
+                         "scaled MFMA (same codes; the default is int8 MFMA "
+                         "throughout)")
     ap.add_argument("--no-fuse-pool", action="store_true",
                     help="run every max-pool as a layer of its own (default: a "
                          "2x2/2 pool inside the conv that feeds it, where a "
@@ -320,7 +332,8 @@ def main():
               for i, L in enumerate(layers)]
     torch.cuda.set_device(0)
     dev = P.DeviceStack(layers, params, batch, code_layout=args.layout,
-                        fuse_down=not args.no_fuse_down, fuse_pool=not args.no_fuse_pool)
+                        fuse_down=not args.no_fuse_down, fuse_pool=not args.no_fuse_pool,
+                        fp4=args.fp4)
     run_layers = dev.layers    # without the downsample layers folded into joins
     L0 = layers[0]
     x_host = stack_input(args.config, (batch, L0.h, L0.w, L0.cin), L0.in_bits)
@@ -386,7 +399,7 @@ def main():
             rec["fused_downsample"] = dev.fused[L.name]
         if ops[i]:
             rec["tops"] = ops[i] / (lay_ms[i] * 1e-3) / 1e12
-            rec["pct_peak"] = 100.0 * rec["tops"] / PEAK_INT8_TOPS
+            rec["pct_peak"] = 100.0 * rec["tops"] / kernel_peak(names[i])
         per_layer.append(rec)
 
     # dominant kernel: most total time; its achieved rate over its launches
@@ -401,13 +414,15 @@ def main():
     avg_us = gd["ms"] / gd["n"] * 1e3
     achieved = gd["ops"] / (gd["ms"] * 1e-3) / 1e12 if gd["ops"] else 0.0
     traffic = load_traffic(dom, cfg.name + ":" + args.layout)
+    peak = kernel_peak(dom)
     roofline = {"bound": "mfma", "achieved": round(achieved, 2),
-                "peak": PEAK_INT8_TOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_INT8_TOPS, 4),
+                "peak": peak, "unit": "TFLOP/s",
+                "frac": round(achieved / peak, 4),
                 "traffic": traffic, "kernel": dom, "launches_per_step": gd["n"],
                 "avg_launch_us": round(avg_us, 3),
                 "ops_per_launch": gd["ops"] // gd["n"],
-                "op": "int8 ops, 2 per +-1 x code MAC"}
+                "op": ("fp4 ops" if peak == PEAK_FP4_TFLOPS else "int8 ops") +
+                      ", 2 per +-1 x code MAC"}
 
     judged = [r for r in per_layer if r["layer"] in JUDGED]
     # judged layers: their own 3x3 conv ops only (a fused downsample's work
@@ -436,7 +451,9 @@ def main():
                              (len(dev.fused_pool),
                               len(dev.fused_pool) + sum(1 for L in run_layers
                                                         if not hasattr(L, "cin")))),
-                   "params": "seeded BN/alpha, plain variant"},
+                   "params": "seeded BN/alpha, plain variant",
+                   "contraction": ("fp4 scaled MFMA on %d layers, int8 MFMA elsewhere" %
+                                   len(dev.fp4_layers) if dev.fp4_layers else "int8 MFMA")},
         "images_per_s": images_s,
         "pct_int8_peak": 100.0 * value / 1e12 / PEAK_INT8_TOPS,
         "judged_layers_pct_peak": judged_pct,

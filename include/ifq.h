@@ -76,6 +76,7 @@ typedef int32_t ifq_status;
 #define IFQ_LAYER_CONV 0
 #define IFQ_LAYER_POOL 1
 #define IFQ_LAYER_CONV_POOL 2 /* conv with its max-pool fused (see ifq_conv_pool_forward) */
+#define IFQ_LAYER_CONV_FP4 3  /* conv on the fp4 path (see ifq_conv_forward_fp4) */
 
 #define IFQ_MAX_THRESHOLDS 15 /* 2^4 - 1: codes of up to 4 bits */
 
@@ -230,10 +231,12 @@ typedef struct ifq_pool_desc {
 
 /*
  * One layer of a stack (Sec. 3.1: a network is a chain of substructures).
- *   kind        IFQ_LAYER_CONV, IFQ_LAYER_POOL or IFQ_LAYER_CONV_POOL (conv
+ *   kind        IFQ_LAYER_CONV, IFQ_LAYER_POOL, IFQ_LAYER_CONV_POOL (conv
  *               without join whose codes go through pool before dst; its
  *               pool desc describes the conv's output as for
- *               ifq_conv_pool_forward)
+ *               ifq_conv_pool_forward) or IFQ_LAYER_CONV_FP4 (conv without
+ *               join on the fp4 path; w_packed is its ifq_pack_weights_fp4
+ *               blob)
  *   src, dst    tensor slots: 0 is the stack input x, 1 the stack output y,
  *               2 .. n_slots-1 live in the caller's workspace
  *   join_src    slot of the join shortcut (conv layers with join.kind != 0),
@@ -423,6 +426,37 @@ IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
                                     const ifq_join* join, void* y,
                                     int32_t* acc_dump, void* ws,
                                     size_t ws_bytes, hipStream_t stream);
+
+/*
+ * The conv of ifq_conv_forward with its contraction (Eq. 1, integer part) on
+ * the fp4 (e2m1) scaled matrix instructions, for the 3x3 layers of the
+ * windowed kernel with the 2-bit threshold epilogue. The codes 0..3 are the
+ * e2m1 values c/2 and the weights +-2.0, so every product and partial sum is
+ * an exact integer in fp32, and the output is bit-identical to
+ * ifq_conv_forward's. Weights come from ifq_pack_weights_fp4.
+ * Covered: in_layout BLOCK64, in_bits 2, 3x3, pad 1, stride 1 or 2,
+ * c_in % 64 == 0, out_bits 2 in a 2-bit layout, c_out % 32 == 0, no join;
+ * otherwise UNSUPPORTED (ifq_conv_fp4_kernel_name returns ""). Asynchronous.
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
+ */
+IFQ_API ifq_status ifq_conv_forward_fp4(const ifq_conv_desc* d, const void* x,
+                                        const void* w_fp4, const int32_t* thr, void* y,
+                                        hipStream_t stream);
+
+/* Name of the kernel ifq_conv_forward_fp4 launches for d, "" if none. Host. */
+IFQ_API const char* ifq_conv_fp4_kernel_name(const ifq_conv_desc* d);
+
+/*
+ * Bytes of the fp4 weight blob of a layer (0 unless in_bits 2, c_in % 64 == 0
+ * and a 2-bit packed input layout), and its packing from the same OIHW +-1
+ * int8 weights as ifq_pack_weights: per 32-row block and K64 step, 1 KB of
+ * 64 lanes x 32 nibbles (+-2.0 as 0x4 / 0xC), in the order the kernel's
+ * nibble expansion of the codes gives K; a zero block of 1 KB at the end.
+ * Host only. Errors as ifq_pack_weights.
+ */
+IFQ_API size_t ifq_packed_weight_bytes_fp4(const ifq_conv_desc* d);
+IFQ_API ifq_status ifq_pack_weights_fp4(const ifq_conv_desc* d, const int8_t* w_oihw,
+                                        void* dst, size_t dst_bytes);
 
 /*
  * Conv (Eq. 1, thresholds of Eq. 7-8) and max-pool (Eq. 4) in one kernel: the

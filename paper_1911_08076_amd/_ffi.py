@@ -33,6 +33,7 @@ IFQ_JOIN_CONV_FUSED = 3
 IFQ_LAYER_CONV = 0
 IFQ_LAYER_POOL = 1
 IFQ_LAYER_CONV_POOL = 2
+IFQ_LAYER_CONV_FP4 = 3
 
 IFQ_MAX_THRESHOLDS = 15
 
@@ -108,6 +109,10 @@ SIGNATURES = [
     ("ifq_conv_workspace_bytes", size_t, [ctypes.POINTER(ConvDesc)]),
     ("ifq_conv_forward", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp,
                                ctypes.POINTER(Join), vp, vp, vp, size_t, vp]),
+    ("ifq_conv_forward_fp4", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp, vp, vp]),
+    ("ifq_conv_fp4_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc)]),
+    ("ifq_packed_weight_bytes_fp4", size_t, [ctypes.POINTER(ConvDesc)]),
+    ("ifq_pack_weights_fp4", i32, [ctypes.POINTER(ConvDesc), vp, vp, size_t]),
     ("ifq_conv_pool_forward", i32, [ctypes.POINTER(ConvDesc), ctypes.POINTER(PoolDesc),
                                     vp, vp, vp, vp, vp]),
     ("ifq_conv_pool_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc),

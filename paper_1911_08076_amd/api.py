@@ -220,6 +220,27 @@ def ifq_conv_forward(desc, x, w_packed, thr, y, join=None, acc_dump=None,
         _ptr(ws), ws_bytes, _stream(stream)), "ifq_conv_forward")
 
 
+def ifq_pack_weights_fp4(desc, w_oihw):
+    """The fp4 weight blob (uint8) of OIHW +-1 weights."""
+    w = np.ascontiguousarray(w_oihw, dtype=np.int8)
+    n = int(_lib().ifq_packed_weight_bytes_fp4(ctypes.byref(desc)))
+    if n == 0:
+        raise IfqError(-1, "ifq_packed_weight_bytes_fp4", "no fp4 layout for this layer")
+    out = np.zeros(n, dtype=np.uint8)
+    _check(_lib().ifq_pack_weights_fp4(ctypes.byref(desc), _ptr(w), _ptr(out), n),
+           "ifq_pack_weights_fp4")
+    return out
+
+
+def ifq_conv_fp4_kernel_name(desc):
+    return _lib().ifq_conv_fp4_kernel_name(ctypes.byref(desc)).decode()
+
+
+def ifq_conv_forward_fp4(desc, x, w_fp4, thr, y, stream=None):
+    _check(_lib().ifq_conv_forward_fp4(ctypes.byref(desc), _ptr(x), _ptr(w_fp4), _ptr(thr),
+                                       _ptr(y), _stream(stream)), "ifq_conv_forward_fp4")
+
+
 def ifq_conv_pool_forward(desc, pool, x, w_packed, thr, y, stream=None):
     _check(_lib().ifq_conv_pool_forward(
         ctypes.byref(desc), ctypes.byref(pool), _ptr(x), _ptr(w_packed), _ptr(thr),

@@ -406,6 +406,27 @@ ifq_status check_fold_params(const ifq_fold_params* p, bool need_q) {
   return IFQ_OK;
 }
 
+// fp4 weight blob: 1 KB per 32-row block and K64 step, then a zero block.
+int64_t fp4_zero_off(const ifq::WeightGeom& g) { return (g.cout_pad / 32) * (g.kpad / 64) * 1024; }
+
+// The fp4 kernels: the windowed kernel's 2-bit threshold epilogue on the
+// transposed layout (the conditions of its packed 16-bit compares), no join,
+// no pool, and a plan of the windowed kernel.
+bool fp4_plan(const ifq::ConvLaunch& a, ifq::HaloPlan* hp) {
+  if (!(a.out_mode == 2 && a.rec == 4 && a.cout % 32 == 0 && 27 * a.cin <= 32766 &&
+        a.join_kind == IFQ_JOIN_NONE && a.pool_k == 0 && a.m > 0))
+    return false;
+  // only where the int8 plan's variant has an fp4 instance: the
+  // 64-channel layers, whose two-workgroups-per-CU variant has none, measured
+  // 16 -> 24 us on the 128-channel fp4 tiles (half their rows padding)
+  ifq::HaloPlan h8;
+  if (!ifq::plan_halo(a, &h8)) return false;
+  ifq::ConvLaunch f = a;
+  f.f4 = 1;   // the variants with an fp4 instance
+  if (!ifq::plan_halo(f, hp)) return false;
+  return hp->variant == h8.variant;
+}
+
 }  // namespace
 
 extern "C" {
@@ -741,6 +762,83 @@ IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
   return ok();
 }
 
+IFQ_API size_t ifq_packed_weight_bytes_fp4(const ifq_conv_desc* d) {
+  if (check_conv(d) != IFQ_OK || !ifq::mfma_layout(*d)) return 0;
+  const ifq::WeightGeom g = ifq::weight_geom(*d);
+  return (size_t)(fp4_zero_off(g) + 1024);
+}
+
+IFQ_API ifq_status ifq_pack_weights_fp4(const ifq_conv_desc* d, const int8_t* w_oihw,
+                                        void* dst, size_t dst_bytes) {
+  ifq_status st = check_conv(d);
+  if (st != IFQ_OK) return st;
+  if (!w_oihw || !dst) return fail(IFQ_ERR_INVALID_ARGUMENT, "NULL pointer");
+  if (!ifq::mfma_layout(*d))
+    return fail(IFQ_ERR_INVALID_ARGUMENT,
+                "pack fp4: needs in_bits 2, c_in %% 64 == 0 and a 2-bit packed input");
+  const ifq::WeightGeom g = ifq::weight_geom(*d);
+  const int64_t bytes = fp4_zero_off(g) + 1024;
+  if (dst_bytes < (size_t)bytes)
+    return fail(IFQ_ERR_INSUFFICIENT_BUFFER, "pack fp4: need %lld bytes, got %zu",
+                (long long)bytes, dst_bytes);
+  const int64_t total = (int64_t)d->c_out * d->c_in * d->kh * d->kw;
+  for (int64_t i = 0; i < total; ++i)
+    if (w_oihw[i] != 1 && w_oihw[i] != -1)
+      return fail(IFQ_ERR_INVALID_ARGUMENT, "pack fp4: weight %lld is %d, must be +1 or -1",
+                  (long long)i, (int)w_oihw[i]);
+  uint8_t* out = static_cast<uint8_t*>(dst);
+  std::memset(dst, 0, (size_t)bytes);
+  const int64_t nk = g.kpad / 64;
+  for (int64_t co = 0; co < d->c_out; ++co)
+    for (int64_t r = 0; r < d->kh; ++r)
+      for (int64_t s = 0; s < d->kw; ++s)
+        for (int64_t c = 0; c < d->c_in; ++c) {
+          const int8_t v = w_oihw[((co * d->c_in + c) * d->kh + r) * d->kw + s];
+          // K64 step kk = (c/64)*T + tap; channel c' = c%64 = 32h + m sits in
+          // lane 32h + co%32 at nibble 8*qw + j, where the kernel expands
+          // code m = 16*(qw/2) + 2*j + qw%2 of the lane's half cell
+          const int64_t kk = (c / 64) * (d->kh * d->kw) + r * d->kw + s, cp = c % 64;
+          const int64_t h = cp / 32, m = cp % 32;
+          const int64_t qw = 2 * (m / 16) + (m % 2), j = (m % 16) / 2;
+          const int64_t lane = 32 * h + co % 32, nib = 8 * qw + j;
+          const int64_t pos = (((co / 32) * nk + kk) * 64 + lane) * 16 + nib / 2;
+          out[pos] |= (uint8_t)((v > 0 ? 0x4 : 0xC) << (4 * (nib % 2)));
+        }
+  return ok();
+}
+
+IFQ_API const char* ifq_conv_fp4_kernel_name(const ifq_conv_desc* d) {
+  int64_t ho, wo;
+  if (check_conv(d, &ho, &wo) != IFQ_OK) return "";
+  ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                  nullptr, nullptr);
+  ifq::HaloPlan hp;
+  if (!fp4_plan(a, &hp)) return "";
+  a.f4 = 1;
+  return ifq::conv_halo_name(hp, a);
+}
+
+IFQ_API ifq_status ifq_conv_forward_fp4(const ifq_conv_desc* d, const void* x,
+                                        const void* w_fp4, const int32_t* thr, void* y,
+                                        hipStream_t stream) {
+  int64_t ho, wo;
+  ifq_status st = check_conv(d, &ho, &wo);
+  if (st != IFQ_OK) return st;
+  st = conv_args_check(d, x, w_fp4, thr, nullptr, nullptr, y);
+  if (st != IFQ_OK) return st;
+  ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_fp4, thr, nullptr, nullptr, y, nullptr);
+  if (d->n == 0) return ok();
+  ifq::HaloPlan hp;
+  if (!fp4_plan(a, &hp))
+    return fail(IFQ_ERR_UNSUPPORTED, "conv fp4: no fp4 kernel covers this layer");
+  a.f4 = 1;
+  a.rowsum = nullptr;
+  a.wzero = fp4_zero_off(ifq::weight_geom(*d));
+  st = hip_status(ifq::launch_conv_halo(a, hp, stream), "conv fp4 launch");
+  if (st != IFQ_OK) return st;
+  return ok();
+}
+
 IFQ_API const char* ifq_conv_pool_kernel_name(const ifq_conv_desc* d,
                                               const ifq_pool_desc* p) {
   int64_t ho, wo;
@@ -828,7 +926,7 @@ int64_t layer_out_bytes(const ifq_layer& L) {
     if (check_pool(&L.pool, &pho, &pwo) != IFQ_OK) return 0;
     return tensor_bytes(L.conv.n, pho, pwo, L.conv.c_out, L.conv.out_layout);
   }
-  if (L.kind == IFQ_LAYER_CONV) {
+  if (L.kind == IFQ_LAYER_CONV || L.kind == IFQ_LAYER_CONV_FP4) {
     const int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);
     const int64_t wo = out_extent(L.conv.w, L.conv.kw, L.conv.stride, L.conv.pad);
     return tensor_bytes(L.conv.n, ho, wo, L.conv.c_out, L.conv.out_layout);
@@ -845,7 +943,7 @@ int64_t layer_out_bytes(const ifq_layer& L) {
 }
 
 int64_t layer_in_bytes(const ifq_layer& L) {
-  if (L.kind == IFQ_LAYER_CONV || L.kind == IFQ_LAYER_CONV_POOL)
+  if (L.kind == IFQ_LAYER_CONV || L.kind == IFQ_LAYER_CONV_POOL || L.kind == IFQ_LAYER_CONV_FP4)
     return tensor_bytes(L.conv.n, L.conv.h, L.conv.w, L.conv.c_in, L.conv.in_layout);
   return tensor_bytes(L.pool.n, L.pool.h, L.pool.w, L.pool.c, L.pool.layout);
 }
@@ -881,6 +979,14 @@ ifq_status plan_stack(const ifq_stack* s, SlotPlan* plan) {
       int64_t ho, wo;
       st = check_pool(&L.pool, &ho, &wo);
       if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+    } else if (L.kind == IFQ_LAYER_CONV_FP4) {
+      st = check_conv(&L.conv);
+      if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+      st = conv_args_check(&L.conv, (const void*)1, L.w_packed, L.thr, nullptr, nullptr,
+                           (const void*)1);
+      if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+      if (L.conv.n > 0 && !*ifq_conv_fp4_kernel_name(&L.conv))
+        return fail(IFQ_ERR_UNSUPPORTED, "layer %d: no fp4 kernel covers it", i);
     } else if (L.kind == IFQ_LAYER_CONV_POOL) {
       int64_t ho, wo;
       st = check_conv_pool(&L.conv, &L.pool, &ho, &wo);
@@ -970,6 +1076,8 @@ IFQ_API ifq_status ifq_run_stack(const ifq_stack* s, const void* x, void* y,
                                             L.thr, &j, sc, slot(L.dst), nullptr);
       (void)conv_ws;
       st = hip_status(ifq::launch_conv(a, stream), "conv launch");
+    } else if (L.kind == IFQ_LAYER_CONV_FP4) {
+      st = ifq_conv_forward_fp4(&L.conv, slot(L.src), L.w_packed, L.thr, slot(L.dst), stream);
     } else if (L.kind == IFQ_LAYER_CONV_POOL) {
       int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);
       int64_t wo = out_extent(L.conv.w, L.conv.kw, L.conv.stride, L.conv.pad);

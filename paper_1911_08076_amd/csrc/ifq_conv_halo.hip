@@ -56,17 +56,25 @@ __host__ __device__ constexpr int round64(int v) { return (v + 63) & ~63; }
 // out transposed (one channel per lane; see the transposed epilogues of
 // ifq_mfma_common.h). Those kernels serve the 2-bit threshold epilogue and
 // the fused downsample join only.
-template <int WN, int WK, int D, bool FUSED, int FM, bool SW>
+// F4: the contraction on the fp4 (e2m1) scaled MFMA, 32x32x64 with unit
+// scales. A code c is the nibble c, the e2m1 value c/2; a weight is +-2.0, so
+// every product is +-c and every partial sum an integer far below 2^24: the
+// fp32 accumulators hold the int8 kernel's sums exactly. The weight blob
+// holds 32 nibbles per lane and K64 step (half the int8 bytes), and one
+// MFMA covers what two int8 ones do.
+template <int WN, int WK, int D, bool FUSED, int FM, bool SW, bool F4 = false>
 __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) {
   static_assert(WN * WK == kHaloNW, "8 waves");
   static_assert(FM == 4 || (FM == 2 && !FUSED), "fused downsample needs FM = 4");
   static_assert(!FUSED || SW, "the fused join runs on the transposed layout");
+  static_assert(!F4 || (SW && !FUSED), "the fp4 kernels serve the threshold epilogue");
   constexpr int BM = 32 * FM, BN = 32 * WN;
-  constexpr int A_STEP = BM * 64;                 // one K64 step of weights
+  constexpr int KH = F4 ? 1 : 2;                  // 1 KB chunks per row block and K64 step
+  constexpr int A_STEP = BM * 32 * KH;            // one K64 step of weights
   constexpr int STAGE = WK * A_STEP;
-  // weight chunks (1 KB) per stage: 2*FM per group; wave w takes chunks
+  // weight chunks (1 KB) per stage: KH*FM per group; wave w takes chunks
   // w + 8k, k < CPWA (dummy loads where that runs past the stage)
-  constexpr int NCH = 2 * FM * WK;
+  constexpr int NCH = KH * FM * WK;
   constexpr int CPWA = NCH > kHaloNW ? NCH / kHaloNW : 1;
   static_assert(NCH % kHaloNW == 0 || NCH < kHaloNW, "weight chunks per wave");
   constexpr int CPW = CPWA + 1;                   // loads per wave per stage
@@ -229,11 +237,10 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
 
   // ---- weights: chunk c of a stage is group c / (2*FM)'s row block
   // (c % (2*FM)) / 2, K32 half c % 2 of its K64 step: 1 KB at
-  // ((rbw + rb) * nk32 + 2*kk + t) * 1024 -------------------------------------
+  // ((rbw + rb) * KH*nk + KH*kk + t) * 1024 (KH = 1, t = 0 for fp4) ------------
   const int nrb = a.cout_pad >> 5;
   const int rbw = co0 >> 5;
   const uint8_t* wbase = reinterpret_cast<const uint8_t*>(a.wgt);
-  const int nk32 = 2 * a.nk;
   const uint32_t voff = (uint32_t)lane * 16;
   auto issue_a = [&](int stg, int tap) {
     const int gi = stg / kTaps;
@@ -242,11 +249,11 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
     for (int k = 0; k < CPWA; ++k) {
       const int c = wave + kHaloNW * k;
       if (NCH >= kHaloNW || c < NCH) {
-        const int i = c / (2 * FM), cc = c - i * 2 * FM;
-        const int rb = cc >> 1, t = cc & 1;
+        const int i = c / (KH * FM), cc = c - i * KH * FM;
+        const int rb = F4 ? cc : cc >> 1, t = F4 ? 0 : cc & 1;
         const int kk = (gi * WK + i) * kTaps + tap;
         const int64_t off =
-            rbw + rb < nrb ? ((int64_t)(rbw + rb) * nk32 + 2 * kk + t) * 1024 : a.wzero;
+            rbw + rb < nrb ? ((int64_t)(rbw + rb) * (KH * a.nk) + KH * kk + t) * 1024 : a.wzero;
         dma16s(wbase + off, voff, slot + (uint32_t)(i * A_STEP + cc * 1024));
       } else {
         dma16(zero_src, lds0 + DUMMY);
@@ -330,13 +337,16 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
   v16i acc[FM];
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) acc[fm] = v16i{0};
+  v16f accf[F4 ? FM : 1];
+#pragma unroll
+  for (int fm = 0; fm < (F4 ? FM : 1); ++fm) accf[fm] = v16f{0.0f};
 
   // Fragments of one stage in registers: A for both K32 halves and the raw
   // 2-bit B words, unpacked only right before the MFMAs that use them (one
   // iteration later), so no instruction waits on these reads in the
   // iteration that issues them.
   struct Frag {
-    v4i af[2][FM];
+    v4i af[KH][FM];
     v2i braw;
   };
   auto read_frags = [&](int s_, int tap, Frag& F) {
@@ -345,12 +355,28 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
     F.braw = *reinterpret_cast<const v2i*>(
         lds + HALO0 + kg * 2 * HSTRIDE + (gi & 1) * HSTRIDE + boff[tap]);
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < KH; ++t)
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
-        F.af[t][fm] = *reinterpret_cast<const v4i*>(as + (fm * 2 + t) * 1024 + lane * 16);
+        F.af[t][fm] = *reinterpret_cast<const v4i*>(as + (fm * KH + t) * 1024 + lane * 16);
   };
   auto mfmas = [&](const Frag& F) {
+    if constexpr (F4) {
+      // the 32 codes of the lane's half of the cell as nibbles: word 0 holds
+      // codes 0, 2, .., 14 of braw.x, word 1 codes 1, 3, .., 15, words 2 and
+      // 3 the same of braw.y (the weight blob follows that order)
+      const uint32_t w0 = (uint32_t)F.braw[0], w1 = (uint32_t)F.braw[1];
+      const v8i bf = v8i{(int)(w0 & 0x33333333u), (int)((w0 >> 2) & 0x33333333u),
+                         (int)(w1 & 0x33333333u), (int)((w1 >> 2) & 0x33333333u), 0, 0, 0, 0};
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) {
+        const v4i w = F.af[0][fm];
+        const v8i af = v8i{w.x, w.y, w.z, w.w, 0, 0, 0, 0};
+        accf[fm] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bf, af, accf[fm], 4, 4, 0,
+                                                                   127, 0, 127);
+      }
+      return;
+    }
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const v4i bf = unpack2((uint32_t)F.braw[t]);
@@ -408,12 +434,19 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
     }
     // tap 8 (odd count of taps): its fragments move to fb
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < KH; ++t)
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm) fb.af[t][fm] = fa.af[t][fm];
     fb.braw = fa.braw;
   }
   mfmas(fb);
+  if constexpr (F4) {
+    // exact integers (see above)
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[fm][i] = (int)accf[fm][i];
+  }
   wait_vmcnt<0>();
   __syncthreads();
 
@@ -558,20 +591,21 @@ struct HaloVariant {
   double eff;          // MFMA efficiency of the main loop
   const char* name;    // the kernels as a profiler lists them: unfused,
   const char* sw_name;       // unfused on the transposed layout,
-  const char* fused_name;    // fused downsample (transposed layout)
+  const char* fused_name;    // fused downsample (transposed layout),
+  const char* f4_name;       // fp4 contraction (transposed layout)
 };
 
 // Index order must match the switch in launch_conv_halo. Variants with
 // fm = 2 (64 output channels) run two workgroups per CU.
 const HaloVariant kHaloVariants[] = {
     {8, 1, 6, 4, 4.0, 0.75, "conv_halo<8, 1, 6, false, 4, false>", "conv_halo<8, 1, 6, false, 4, true>",
-     "conv_halo<8, 1, 6, true, 4, true>"},
+     "conv_halo<8, 1, 6, true, 4, true>", "conv_halo<8, 1, 6, false, 4, true, true>"},
     {4, 2, 4, 4, 4.0, 0.75, "conv_halo<4, 2, 4, false, 4, false>", "conv_halo<4, 2, 4, false, 4, true>",
-     "conv_halo<4, 2, 4, true, 4, true>"},
+     "conv_halo<4, 2, 4, true, 4, true>", "conv_halo<4, 2, 4, false, 4, true, true>"},
     {2, 4, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4, false, 4, false>", "conv_halo<2, 4, 4, false, 4, true>",
-     "conv_halo<2, 4, 4, true, 4, true>"},
+     "conv_halo<2, 4, 4, true, 4, true>", "conv_halo<2, 4, 4, false, 4, true, true>"},
     {8, 1, 6, 2, 4.0, 0.75, "conv_halo<8, 1, 6, false, 2, false>", "conv_halo<8, 1, 6, false, 2, true>",
-     nullptr},   // 64 x 256
+     nullptr, nullptr},   // 64 x 256
 };
 constexpr int kNumHalo = sizeof(kHaloVariants) / sizeof(kHaloVariants[0]);
 constexpr int kNumCUs = 256;
@@ -609,6 +643,9 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
   for (int v = 0; v < kNumHalo; ++v) {
     const HaloVariant& V = kHaloVariants[v];
     if (G % V.wk) continue;
+    // the fp4 instance of the two-workgroups-per-CU variant needs more than
+    // its 128 VGPRs (spills): fp4 layers take the 128-channel tiles instead
+    if (a.f4 && !V.f4_name) continue;
     const int bm = 32 * V.fm, bnmax = 32 * V.wn;
     const int occ = V.fm == 2 ? 2 : 1;               // workgroups per CU
     const int cap = halo_cap_cells(V.wk, V.fm);
@@ -655,8 +692,10 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
 
 // Which instance of a variant runs: 0 = unfused, 1 = unfused on the
 // transposed layout (the 2-bit threshold epilogue with packed 16-bit
-// compares, the same condition as the kernel's pk), 2 = fused downsample.
+// compares, the same condition as the kernel's pk), 2 = fused downsample,
+// 3 = the fp4 contraction (a.f4; the same epilogue as 1, checked by the host).
 int halo_instance(const ConvLaunch& a) {
+  if (a.f4) return 3;
   if (a.join_kind == IFQ_JOIN_CONV_FUSED) return 2;
   const bool pk = a.out_mode == 2 && a.rec == 4 && (a.cout & 31) == 0 &&
                   27 * a.cin <= 32766 && a.join_kind == IFQ_JOIN_NONE;
@@ -667,16 +706,19 @@ int halo_instance(const ConvLaunch& a) {
 const char* conv_halo_name(const HaloPlan& p, const ConvLaunch& a) {
   const HaloVariant& V = kHaloVariants[p.variant];
   const int inst = halo_instance(a);
-  return inst == 2 ? V.fused_name : inst == 1 ? V.sw_name : V.name;
+  return inst == 3 ? V.f4_name : inst == 2 ? V.fused_name : inst == 1 ? V.sw_name : V.name;
 }
 
 hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream) {
   a.bn = p.bn;
   const int bm = 32 * kHaloVariants[p.variant].fm;
   const dim3 grid(p.blocks_m, (a.cout + bm - 1) / bm);
-  switch (p.variant * 3 + halo_instance(a)) {
+  const int inst = halo_instance(a);
+  switch (inst == 3 ? 12 + p.variant : p.variant * 3 + inst) {
 #define IFQ_HALO_CASE(k, wn, wk, d, fu, fm, sw) \
     case k: hipLaunchKernelGGL((conv_halo<wn, wk, d, fu, fm, sw>), grid, dim3(512), 0, stream, a); break;
+#define IFQ_HALO_F4(k, wn, wk, d, fm) \
+    case k: hipLaunchKernelGGL((conv_halo<wn, wk, d, false, fm, true, true>), grid, dim3(512), 0, stream, a); break;
     IFQ_HALO_CASE(0, 8, 1, 6, false, 4, false)
     IFQ_HALO_CASE(1, 8, 1, 6, false, 4, true)
     IFQ_HALO_CASE(2, 8, 1, 6, true, 4, true)
@@ -688,7 +730,11 @@ hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream)
     IFQ_HALO_CASE(8, 2, 4, 4, true, 4, true)
     IFQ_HALO_CASE(9, 8, 1, 6, false, 2, false)
     IFQ_HALO_CASE(10, 8, 1, 6, false, 2, true)
+    IFQ_HALO_F4(12, 8, 1, 6, 4)
+    IFQ_HALO_F4(13, 4, 2, 4, 4)
+    IFQ_HALO_F4(14, 2, 4, 4, 4)
 #undef IFQ_HALO_CASE
+#undef IFQ_HALO_F4
     default: return hipErrorInvalidValue;   // no fused kernel for this variant
   }
   return hipGetLastError();

@@ -121,6 +121,10 @@ struct ConvLaunch {
   // windows (pool_img 0: k == stride, valid, ho and wo multiples of k) or
   // whole images (pool_img 1: any window).
   int32_t pool_k, pool_s, pool_same, pool_img;
+  // The contraction on the fp4 scaled MFMA (windowed 3x3 kernel, 2-bit
+  // threshold epilogue): wgt is then the fp4 weight blob, wzero its zero
+  // block.
+  int32_t f4;
   int32_t pho, pwo;
   FastDiv div_pwo;     // division by pwo (pooled pixel -> pooled row)
   FastDiv div_pho;     // division by pho (pooled row -> image)

@@ -19,6 +19,7 @@ import numpy as np
 
 from . import _ffi, api
 from ._ffi import (Layer, Stack, IFQ_LAYER_CONV, IFQ_LAYER_POOL, IFQ_LAYER_CONV_POOL,
+                   IFQ_LAYER_CONV_FP4,
                    IFQ_LAYOUT_I8_NHWC, IFQ_LAYOUT_U2_NHWC_PACKED,
                    IFQ_LAYOUT_I32_NHWC, IFQ_LAYOUT_U2_BLOCK64, IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY,
                    IFQ_JOIN_CONV, IFQ_JOIN_CONV_FUSED, IFQ_POOL_VALID, IFQ_POOL_SAME)
@@ -63,13 +64,15 @@ class DeviceStack:
     conv output (valid, k == stride), where the fused kernel keeps its usual
     tile count; "all" also the others, which the fused kernels run with one
     image per tile (slower than a separate pool at small batch: too few
-    workgroups for the chip). self.fused_pool maps
+    workgroups for the chip). fp4: the convs an fp4 kernel covers (the
+    windowed kernel's 2-bit threshold layers) run on it (IFQ_LAYER_CONV_FP4,
+    the same codes); self.fp4_layers names them. self.fused_pool maps
     the conv's name to the pool's, whose layer and the conv's output tensor
     are then absent.
     """
 
     def __init__(self, layers, params, batch, code_layout="i8",
-                 device="cuda", fuse_down=False, fuse_pool=False):
+                 device="cuda", fuse_down=False, fuse_pool=False, fp4=False):
         import torch
         if code_layout not in ("i8", "u2", "b64"):
             raise ValueError("code_layout must be 'i8', 'u2' or 'b64'")
@@ -95,6 +98,7 @@ class DeviceStack:
         self._all_layers = all_layers
         self.layers = [L for L in all_layers if L.name not in skip]
         self.batch = int(batch)
+        self.fp4_layers = []
         self.fused_pool = {}
         if fuse_pool:
             self.fused_pool = self._pool_fusions(code_layout, fuse_pool)
@@ -174,7 +178,12 @@ class DeviceStack:
                     ho, wo = api.ifq_conv_output_dims(d)
                     rec.pool = api.pool_desc(self.batch, ho, wo, L.cout, Pl.k, Pl.stride,
                                              _POOL_MODE[Pl.mode], L.out_bits, out_layout)
-                blob = api.ifq_pack_weights(d, p["w"])
+                if (fp4 and rec.kind == IFQ_LAYER_CONV and L.join is None
+                        and api.ifq_conv_fp4_kernel_name(d)):
+                    rec.kind = IFQ_LAYER_CONV_FP4
+                    self.fp4_layers.append(L.name)
+                blob = (api.ifq_pack_weights_fp4(d, p["w"]) if rec.kind == IFQ_LAYER_CONV_FP4
+                        else api.ifq_pack_weights(d, p["w"]))
                 wdev = torch.from_numpy(blob).to(self.device)
                 self._keep.append(wdev)
                 rec.w_packed = wdev.data_ptr()
@@ -386,6 +395,8 @@ class DeviceStack:
             lay = self._layers[i]
             if lay.kind == IFQ_LAYER_CONV_POOL:
                 out.append(api.ifq_conv_pool_kernel_name(lay.conv, lay.pool))
+            elif lay.kind == IFQ_LAYER_CONV_FP4:
+                out.append(api.ifq_conv_fp4_kernel_name(lay.conv))
             elif _is_conv(L):
                 join = lay.join if lay.join.kind != IFQ_JOIN_NONE else None
                 out.append(api.ifq_conv_kernel_name(lay.conv, join))
@@ -436,6 +447,12 @@ class DeviceStack:
                     None if join is None else ctypes.byref(join), dst, None, None, 0, st)
             fn = lib.ifq_conv_forward
             what = "ifq_conv_forward"
+        elif rec.kind == IFQ_LAYER_CONV_FP4:
+            desc = rec.conv
+            join = None
+            args = (ctypes.byref(desc), src, vp(rec.w_packed), vp(rec.thr), dst, st)
+            fn = lib.ifq_conv_forward_fp4
+            what = "ifq_conv_forward_fp4"
         elif rec.kind == IFQ_LAYER_CONV_POOL:
             desc = (rec.conv, rec.pool)
             join = None

@@ -665,3 +665,25 @@ def test_compact_fold_rejects_bad_quantizer():
     assert st == EINVAL
     st = status_of("ifq_expand_thresholds", FAKE, 4, 2, 9, 5, FAKE, None)
     assert st == EINVAL
+
+
+def test_fp4_entry_points_host_side():
+    # the fp4 path covers the windowed kernel's threshold layers only
+    d = P.conv_desc(2, 28, 28, 128, 128, 3, 1, 1, 2, 2, B64, B64)
+    assert P.ifq_conv_fp4_kernel_name(d).endswith(", true, true>")
+    k = 9 * 128
+    assert P._ffi.load().ifq_packed_weight_bytes_fp4(ctypes.byref(d)) == (128 // 32) * (k // 64) * 1024 + 1024
+    w = np.ones((128, 128, 3, 3), dtype=np.int8)
+    blob = P.ifq_pack_weights_fp4(d, w)
+    # +2.0 is the e2m1 nibble 0x4 in every used position, the zero block stays 0
+    assert set(np.unique(blob[:-1024])) == {0x44} and not blob[-1024:].any()
+    w[0, 0, 0, 0] = 3
+    with pytest.raises(P.IfqError):
+        P.ifq_pack_weights_fp4(d, w)
+    # int32 output, byte-code input, 8-bit input: no fp4 kernel
+    for dd in (P.conv_desc(2, 28, 28, 128, 128, 3, 1, 1, 2, 0, B64, I32),
+               P.conv_desc(2, 28, 28, 128, 128, 3, 1, 1, 2, 2, I8, I8)):
+        assert P.ifq_conv_fp4_kernel_name(dd) == ""
+    d8 = P.conv_desc(2, 28, 28, 128, 128, 3, 1, 1, 2, 2, I8, I8)
+    assert status_of("ifq_conv_forward_fp4", ctypes.byref(d8), FAKE, FAKE, FAKE, FAKE,
+                     None) == EUNSUP

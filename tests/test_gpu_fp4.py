@@ -1,0 +1,77 @@
+"""GPU parity of the fp4 contraction (ifq_conv_forward_fp4): the 3x3 layers
+of the ResNet-18 stack with the 2-bit threshold epilogue, on every variant
+of the windowed kernel (64, 128, 256 and 512 channels, a stride-2 layer),
+must give the oracle's codes bit for bit (the fp32 sums of +-2 x c/2 are
+exact integers)."""
+import zlib
+
+import numpy as np
+import pytest
+
+from gpu_util import (U2, B64, oracle_layer, expect_layout, make_layer, params_for, codes_for,
+                      upload_codes, to_dev, device)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def P():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1911_08076_amd as P
+    return P
+
+
+# name, n, h, c_in, c_out, stride, expected variant (every variant with an
+# fp4 instance)
+FP4 = [
+    ("f4_c64_small_batch", 2, 56, 64, 64, 1, "conv_halo<8, 1, 6, false, 4, true, true>"),
+    ("f4_l2", 3, 28, 128, 128, 1, "conv_halo<4, 2, 4, false, 4, true, true>"),
+    ("f4_l2_0_s2", 2, 56, 64, 128, 2, None),
+    ("f4_l3", 4, 14, 256, 256, 1, None),
+    ("f4_l4", 6, 7, 512, 512, 1, "conv_halo<2, 4, 4, false, 4, true, true>"),
+]
+
+
+@pytest.mark.parametrize("case", FP4, ids=[c[0] for c in FP4])
+def test_fp4_conv_bit_exact(P, case):
+    import torch
+    name, n, h, cin, cout, st, variant = case
+    L = make_layer(name, h, h, cin, cout, 3, st, 1, 2, 2)
+    seed = zlib.crc32(name.encode()) % 997
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, h, cin), 2)
+    _, want = oracle_layer(L, x, p)
+    assert len(np.unique(want)) > 1
+    thr = P.ifq_fold_thresholds(cout, 2, 2, 9 * cin, p["alpha"], p["beta_in"], p["q_thr"],
+                                bias=p["bias"], mean=p["mean"], var=p["var"], gamma=p["gamma"],
+                                bn_beta=p["bn_beta"], eps=p["eps"])
+    td = to_dev(thr)
+    xd = upload_codes(P, x, B64)
+    for out_l in (B64, U2):
+        d = P.conv_desc(n, h, h, cin, cout, 3, st, 1, 2, 2, B64, out_l)
+        kname = P.ifq_conv_fp4_kernel_name(d)
+        assert kname.endswith(", true, true>"), kname
+        if variant:
+            assert kname == variant
+        wd = to_dev(P.ifq_pack_weights_fp4(d, p["w"]))
+        ho, wo = P.ifq_conv_output_dims(d)
+        ob = P.ifq_tensor_bytes(n, ho, wo, cout, out_l)
+        y = torch.full((ob,), 0xA5, dtype=torch.uint8, device=device())
+        P.ifq_conv_forward_fp4(d, xd, wd, td, y)
+        torch.cuda.synchronize()
+        got = y.cpu().numpy()
+        got = (got.reshape(n, cout // 64, ho, wo, 16) if out_l == B64
+               else got.reshape(n, ho, wo, cout // 4))
+        assert np.array_equal(got, expect_layout(want, out_l)), (name, out_l, kname)
+
+
+def test_fp4_not_offered_for_the_64_channel_tiles(P):
+    # the full-batch 64-channel layers plan the two-workgroups-per-CU variant,
+    # which has no fp4 instance: the fp4 entry point declines them
+    d = P.conv_desc(64, 56, 56, 64, 64, 3, 1, 1, 2, 2, B64, B64)
+    assert P.ifq_conv_kernel_name(d) == "conv_halo<8, 1, 6, false, 2, true>"
+    assert P.ifq_conv_fp4_kernel_name(d) == ""
+    with pytest.raises(P.IfqError):
+        P.ifq_conv_forward_fp4(d, None, None, None, None)

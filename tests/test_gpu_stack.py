@@ -42,11 +42,17 @@ def check_stack(P, cfg, batch, layout, variant):
     layers = get_stack(cfg).layers
     # "b64f": downsamples inside their joins; "...p": pools inside the convs
     # that feed them, where a fused kernel covers the pair
-    fuse = layout in ("b64f", "b64p", "b64pa")
+    fuse = layout in ("b64f", "b64p", "b64pa", "b64fp4")
     fpool = "all" if layout.endswith("pa") else layout.endswith("p")
-    base = {"b64f": "b64", "b64p": "b64", "b64pa": "b64", "i8p": "i8"}.get(layout, layout)
+    fp4 = layout.endswith("fp4")
+    base = {"b64f": "b64", "b64p": "b64", "b64pa": "b64", "i8p": "i8",
+            "b64fp4": "b64"}.get(layout, layout)
     dev = P.DeviceStack(layers, params, batch, code_layout=base, fuse_down=fuse,
-                        fuse_pool=fpool)
+                        fuse_pool=fpool, fp4=fp4)
+    if fp4 and base == "b64" and cfg == 3:
+        # the 3x3 threshold layers of the ResNet-shaped stack are on fp4 (at
+        # full batch all but the 64-channel ones)
+        assert dev.fp4_layers and all(n.endswith(".conv1") for n in dev.fp4_layers)
     if fuse:
         # every downsample of a ResNet-shaped stack is folded into its join
         assert len(dev.fused) == sum(1 for L in layers if L.name.endswith(".down"))
@@ -92,7 +98,8 @@ def check_stack(P, cfg, batch, layout, variant):
 SMALL = [(0, 1), (1, 2), (2, 1), (3, 2), (4, 1)]
 
 
-@pytest.mark.parametrize("layout", ["i8", "u2", "b64", "b64f", "b64p", "b64pa", "i8p"])
+@pytest.mark.parametrize("layout", ["i8", "u2", "b64", "b64f", "b64p", "b64pa", "i8p",
+                                    "b64fp4"])
 @pytest.mark.parametrize("cfg,batch", SMALL)
 def test_stack_small_batch(P, cfg, batch, layout):
     for variant in ("calibrated", "plain"):
@@ -113,6 +120,12 @@ def test_stack_full_size_fused_pools(P, cfg):
     # the benchmark's configuration of the stacks with pools: BLOCK64 codes,
     # the 2x2/2 pools inside the convs that feed them
     check_stack(P, cfg, get_stack(cfg).batch, "b64p", "plain")
+
+
+@pytest.mark.slow
+def test_stack_full_size_fp4(P):
+    # the ResNet-18 body at batch 64 with its threshold layers on fp4
+    check_stack(P, 3, get_stack(3).batch, "b64fp4", "plain")
 
 
 @pytest.mark.slow
