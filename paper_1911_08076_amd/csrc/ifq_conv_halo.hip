@@ -598,13 +598,13 @@ struct HaloVariant {
 // Index order must match the switch in launch_conv_halo. Variants with
 // fm = 2 (64 output channels) run two workgroups per CU.
 const HaloVariant kHaloVariants[] = {
-    {8, 1, 6, 4, 4.0, 0.75, "conv_halo<8, 1, 6, false, 4, false>", "conv_halo<8, 1, 6, false, 4, true>",
-     "conv_halo<8, 1, 6, true, 4, true>", "conv_halo<8, 1, 6, false, 4, true, true>"},
-    {4, 2, 4, 4, 4.0, 0.75, "conv_halo<4, 2, 4, false, 4, false>", "conv_halo<4, 2, 4, false, 4, true>",
-     "conv_halo<4, 2, 4, true, 4, true>", "conv_halo<4, 2, 4, false, 4, true, true>"},
-    {2, 4, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4, false, 4, false>", "conv_halo<2, 4, 4, false, 4, true>",
-     "conv_halo<2, 4, 4, true, 4, true>", "conv_halo<2, 4, 4, false, 4, true, true>"},
-    {8, 1, 6, 2, 4.0, 0.75, "conv_halo<8, 1, 6, false, 2, false>", "conv_halo<8, 1, 6, false, 2, true>",
+    {8, 1, 6, 4, 4.0, 0.75, "conv_halo<8, 1, 6, false, 4, false, false>", "conv_halo<8, 1, 6, false, 4, true, false>",
+     "conv_halo<8, 1, 6, true, 4, true, false>", "conv_halo<8, 1, 6, false, 4, true, true>"},
+    {4, 2, 4, 4, 4.0, 0.75, "conv_halo<4, 2, 4, false, 4, false, false>", "conv_halo<4, 2, 4, false, 4, true, false>",
+     "conv_halo<4, 2, 4, true, 4, true, false>", "conv_halo<4, 2, 4, false, 4, true, true>"},
+    {2, 4, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4, false, 4, false, false>", "conv_halo<2, 4, 4, false, 4, true, false>",
+     "conv_halo<2, 4, 4, true, 4, true, false>", "conv_halo<2, 4, 4, false, 4, true, true>"},
+    {8, 1, 6, 2, 4.0, 0.75, "conv_halo<8, 1, 6, false, 2, false, false>", "conv_halo<8, 1, 6, false, 2, true, false>",
      nullptr, nullptr},   // 64 x 256
 };
 constexpr int kNumHalo = sizeof(kHaloVariants) / sizeof(kHaloVariants[0]);

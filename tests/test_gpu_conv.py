@@ -181,14 +181,14 @@ def test_conv_block64_bit_exact(P, case, io):
 # kernel variant the planner takes for each. 2-bit threshold layers run the
 # instances with transposed sums (last template argument true).
 HALO_TILES = [
-    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_halo<8, 1, 6, false, 4, true>"),
-    ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_halo<4, 2, 4, false, 4, true>"),
-    ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_halo<2, 4, 4, false, 4, true>"),
-    ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_halo<4, 2, 4, false, 4, true>"),
-    ("halo_l1_b24", 24, 56, 56, 64, 64, 1, "conv_halo<8, 1, 6, false, 2, true>"),
+    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_halo<8, 1, 6, false, 4, true, false>"),
+    ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_halo<4, 2, 4, false, 4, true, false>"),
+    ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_halo<2, 4, 4, false, 4, true, false>"),
+    ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_halo<4, 2, 4, false, 4, true, false>"),
+    ("halo_l1_b24", 24, 56, 56, 64, 64, 1, "conv_halo<8, 1, 6, false, 2, true, false>"),
     # the stride-2 layers at the full batch of 64, with the largest windows
-    ("halo_l2s2_b64", 64, 56, 56, 64, 128, 2, "conv_halo<8, 1, 6, false, 4, true>"),
-    ("halo_l4s2_b64", 64, 14, 14, 256, 512, 2, "conv_halo<4, 2, 4, false, 4, true>"),
+    ("halo_l2s2_b64", 64, 56, 56, 64, 128, 2, "conv_halo<8, 1, 6, false, 4, true, false>"),
+    ("halo_l4s2_b64", 64, 14, 14, 256, 512, 2, "conv_halo<4, 2, 4, false, 4, true, false>"),
 ]
 
 

@@ -71,7 +71,7 @@ def test_fp4_not_offered_for_the_64_channel_tiles(P):
     # the full-batch 64-channel layers plan the two-workgroups-per-CU variant,
     # which has no fp4 instance: the fp4 entry point declines them
     d = P.conv_desc(64, 56, 56, 64, 64, 3, 1, 1, 2, 2, B64, B64)
-    assert P.ifq_conv_kernel_name(d) == "conv_halo<8, 1, 6, false, 2, true>"
+    assert P.ifq_conv_kernel_name(d) == "conv_halo<8, 1, 6, false, 2, true, false>"
     assert P.ifq_conv_fp4_kernel_name(d) == ""
     with pytest.raises(P.IfqError):
         P.ifq_conv_forward_fp4(d, None, None, None, None)
