@@ -687,3 +687,18 @@ def test_fp4_entry_points_host_side():
     d8 = P.conv_desc(2, 28, 28, 128, 128, 3, 1, 1, 2, 2, I8, I8)
     assert status_of("ifq_conv_forward_fp4", ctypes.byref(d8), FAKE, FAKE, FAKE, FAKE,
                      None) == EUNSUP
+
+
+def test_new_entry_points_accept_an_empty_batch():
+    # n = 0: validated, then nothing to launch (no tensor pointer is needed;
+    # the thresholds are, as for ifq_conv_forward, and never dereferenced)
+    d = P.conv_desc(0, 28, 28, 128, 128, 3, 1, 1, 2, 2, B64, B64)
+    pd = _ffi.PoolDesc(0, 28, 28, 128, 2, 2, 0, 2, B64)
+    assert status_of("ifq_conv_pool_forward", ctypes.byref(d), ctypes.byref(pd), None, None,
+                     FAKE, None, None) == OK
+    assert status_of("ifq_conv_forward_fp4", ctypes.byref(d), None, None, FAKE, None,
+                     None) == OK
+    # the pool must still describe the conv's output
+    bad = _ffi.PoolDesc(0, 27, 28, 128, 2, 2, 0, 2, B64)
+    assert status_of("ifq_conv_pool_forward", ctypes.byref(d), ctypes.byref(bad), None, None,
+                     FAKE, None, None) == EINVAL
