@@ -430,21 +430,24 @@ IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
 /*
  * The conv of ifq_conv_forward with its contraction (Eq. 1, integer part) on
  * the fp4 (e2m1) scaled matrix instructions, for the 3x3 layers of the
- * windowed kernel with the 2-bit threshold epilogue. The codes 0..3 are the
+ * windowed kernel with the 2-bit threshold or identity-join epilogue. The codes 0..3 are the
  * e2m1 values c/2 and the weights +-2.0, so every product and partial sum is
  * an exact integer in fp32, and the output is bit-identical to
  * ifq_conv_forward's. Weights come from ifq_pack_weights_fp4.
  * Covered: in_layout BLOCK64, in_bits 2, 3x3, pad 1, stride 1 or 2,
- * c_in % 64 == 0, out_bits 2 in a 2-bit layout, c_out % 32 == 0, no join;
- * otherwise UNSUPPORTED (ifq_conv_fp4_kernel_name returns ""). Asynchronous.
+ * c_in % 64 == 0, out_bits 2 in a 2-bit layout, c_out % 32 == 0, and no join
+ * (thr as for ifq_conv_forward) or an identity join with a 2-bit packed
+ * shortcut (join as for ifq_conv_forward, thr NULL); otherwise UNSUPPORTED
+ * (ifq_conv_fp4_kernel_name returns ""). Asynchronous.
  * Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
  */
 IFQ_API ifq_status ifq_conv_forward_fp4(const ifq_conv_desc* d, const void* x,
-                                        const void* w_fp4, const int32_t* thr, void* y,
-                                        hipStream_t stream);
+                                        const void* w_fp4, const int32_t* thr,
+                                        const ifq_join* join, void* y, hipStream_t stream);
 
-/* Name of the kernel ifq_conv_forward_fp4 launches for d, "" if none. Host. */
-IFQ_API const char* ifq_conv_fp4_kernel_name(const ifq_conv_desc* d);
+/* Name of the kernel ifq_conv_forward_fp4 launches for d and join (nullable),
+ * "" if none. Host. */
+IFQ_API const char* ifq_conv_fp4_kernel_name(const ifq_conv_desc* d, const ifq_join* join);
 
 /*
  * Bytes of the fp4 weight blob of a layer (0 unless in_bits 2, c_in % 64 == 0

@@ -109,8 +109,10 @@ SIGNATURES = [
     ("ifq_conv_workspace_bytes", size_t, [ctypes.POINTER(ConvDesc)]),
     ("ifq_conv_forward", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp,
                                ctypes.POINTER(Join), vp, vp, vp, size_t, vp]),
-    ("ifq_conv_forward_fp4", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp, vp, vp]),
-    ("ifq_conv_fp4_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc)]),
+    ("ifq_conv_forward_fp4", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp,
+                                   ctypes.POINTER(Join), vp, vp]),
+    ("ifq_conv_fp4_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc),
+                                                   ctypes.POINTER(Join)]),
     ("ifq_packed_weight_bytes_fp4", size_t, [ctypes.POINTER(ConvDesc)]),
     ("ifq_pack_weights_fp4", i32, [ctypes.POINTER(ConvDesc), vp, vp, size_t]),
     ("ifq_conv_pool_forward", i32, [ctypes.POINTER(ConvDesc), ctypes.POINTER(PoolDesc),

@@ -232,13 +232,16 @@ def ifq_pack_weights_fp4(desc, w_oihw):
     return out
 
 
-def ifq_conv_fp4_kernel_name(desc):
-    return _lib().ifq_conv_fp4_kernel_name(ctypes.byref(desc)).decode()
+def ifq_conv_fp4_kernel_name(desc, join=None):
+    return _lib().ifq_conv_fp4_kernel_name(
+        ctypes.byref(desc), ctypes.byref(join) if join is not None else None).decode()
 
 
-def ifq_conv_forward_fp4(desc, x, w_fp4, thr, y, stream=None):
-    _check(_lib().ifq_conv_forward_fp4(ctypes.byref(desc), _ptr(x), _ptr(w_fp4), _ptr(thr),
-                                       _ptr(y), _stream(stream)), "ifq_conv_forward_fp4")
+def ifq_conv_forward_fp4(desc, x, w_fp4, thr, y, join=None, stream=None):
+    _check(_lib().ifq_conv_forward_fp4(
+        ctypes.byref(desc), _ptr(x), _ptr(w_fp4), _ptr(thr),
+        None if join is None else ctypes.byref(join), _ptr(y), _stream(stream)),
+        "ifq_conv_forward_fp4")
 
 
 def ifq_conv_pool_forward(desc, pool, x, w_packed, thr, y, stream=None):

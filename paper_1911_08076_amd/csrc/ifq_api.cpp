@@ -413,8 +413,12 @@ int64_t fp4_zero_off(const ifq::WeightGeom& g) { return (g.cout_pad / 32) * (g.k
 // transposed layout (the conditions of its packed 16-bit compares), no join,
 // no pool, and a plan of the windowed kernel.
 bool fp4_plan(const ifq::ConvLaunch& a, ifq::HaloPlan* hp) {
-  if (!(a.out_mode == 2 && a.rec == 4 && a.cout % 32 == 0 && 27 * a.cin <= 32766 &&
-        a.join_kind == IFQ_JOIN_NONE && a.pool_k == 0 && a.m > 0))
+  const bool join_ok =
+      a.join_kind == IFQ_JOIN_NONE ||
+      (a.join_kind == IFQ_JOIN_IDENTITY && (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64 ||
+                                            a.sc_layout == IFQ_LAYOUT_U2_NHWC_PACKED));
+  if (!(a.out_mode == 2 && a.rec == 4 && a.cout % 32 == 0 && 27 * a.cin <= 32766 && join_ok &&
+        a.pool_k == 0 && a.m > 0))
     return false;
   // only where the int8 plan's variant has an fp4 instance: the
   // 64-channel layers, whose two-workgroups-per-CU variant has none, measured
@@ -807,10 +811,10 @@ IFQ_API ifq_status ifq_pack_weights_fp4(const ifq_conv_desc* d, const int8_t* w_
   return ok();
 }
 
-IFQ_API const char* ifq_conv_fp4_kernel_name(const ifq_conv_desc* d) {
+IFQ_API const char* ifq_conv_fp4_kernel_name(const ifq_conv_desc* d, const ifq_join* join) {
   int64_t ho, wo;
   if (check_conv(d, &ho, &wo) != IFQ_OK) return "";
-  ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, nullptr, nullptr,
+  ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, join, nullptr,
                                   nullptr, nullptr);
   ifq::HaloPlan hp;
   if (!fp4_plan(a, &hp)) return "";
@@ -819,14 +823,15 @@ IFQ_API const char* ifq_conv_fp4_kernel_name(const ifq_conv_desc* d) {
 }
 
 IFQ_API ifq_status ifq_conv_forward_fp4(const ifq_conv_desc* d, const void* x,
-                                        const void* w_fp4, const int32_t* thr, void* y,
-                                        hipStream_t stream) {
+                                        const void* w_fp4, const int32_t* thr,
+                                        const ifq_join* join, void* y, hipStream_t stream) {
   int64_t ho, wo;
   ifq_status st = check_conv(d, &ho, &wo);
   if (st != IFQ_OK) return st;
-  st = conv_args_check(d, x, w_fp4, thr, nullptr, nullptr, y);
+  const void* sc = (join && join->kind != IFQ_JOIN_NONE) ? join->shortcut : nullptr;
+  st = conv_args_check(d, x, w_fp4, thr, join, sc, y);
   if (st != IFQ_OK) return st;
-  ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_fp4, thr, nullptr, nullptr, y, nullptr);
+  ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_fp4, thr, join, sc, y, nullptr);
   if (d->n == 0) return ok();
   ifq::HaloPlan hp;
   if (!fp4_plan(a, &hp))
@@ -982,10 +987,15 @@ ifq_status plan_stack(const ifq_stack* s, SlotPlan* plan) {
     } else if (L.kind == IFQ_LAYER_CONV_FP4) {
       st = check_conv(&L.conv);
       if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
-      st = conv_args_check(&L.conv, (const void*)1, L.w_packed, L.thr, nullptr, nullptr,
-                           (const void*)1);
+      const bool joined = L.join.kind != IFQ_JOIN_NONE;
+      st = conv_args_check(&L.conv, (const void*)1, L.w_packed, L.thr, &L.join,
+                           joined ? (const void*)1 : nullptr, (const void*)1);
       if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
-      if (L.conv.n > 0 && !*ifq_conv_fp4_kernel_name(&L.conv))
+      if (joined && (L.join_src < 0 || L.join_src >= s->n_slots || !written[L.join_src] ||
+                     L.join_src == L.dst))
+        return fail(IFQ_ERR_INVALID_ARGUMENT, "layer %d: join slot %d not written before", i,
+                    L.join_src);
+      if (L.conv.n > 0 && !*ifq_conv_fp4_kernel_name(&L.conv, &L.join))
         return fail(IFQ_ERR_UNSUPPORTED, "layer %d: no fp4 kernel covers it", i);
     } else if (L.kind == IFQ_LAYER_CONV_POOL) {
       int64_t ho, wo;
@@ -1077,7 +1087,10 @@ IFQ_API ifq_status ifq_run_stack(const ifq_stack* s, const void* x, void* y,
       (void)conv_ws;
       st = hip_status(ifq::launch_conv(a, stream), "conv launch");
     } else if (L.kind == IFQ_LAYER_CONV_FP4) {
-      st = ifq_conv_forward_fp4(&L.conv, slot(L.src), L.w_packed, L.thr, slot(L.dst), stream);
+      ifq_join j = L.join;
+      if (j.kind != IFQ_JOIN_NONE) j.shortcut = slot(L.join_src);
+      st = ifq_conv_forward_fp4(&L.conv, slot(L.src), L.w_packed, L.thr, &j, slot(L.dst),
+                                stream);
     } else if (L.kind == IFQ_LAYER_CONV_POOL) {
       int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);
       int64_t wo = out_extent(L.conv.w, L.conv.kw, L.conv.stride, L.conv.pad);

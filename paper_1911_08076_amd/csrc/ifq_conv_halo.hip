@@ -67,7 +67,7 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
   static_assert(WN * WK == kHaloNW, "8 waves");
   static_assert(FM == 4 || (FM == 2 && !FUSED), "fused downsample needs FM = 4");
   static_assert(!FUSED || SW, "the fused join runs on the transposed layout");
-  static_assert(!F4 || (SW && !FUSED), "the fp4 kernels serve the threshold epilogue");
+  static_assert(!F4 || !FUSED, "the fp4 kernels serve the threshold and identity-join epilogues");
   constexpr int BM = 32 * FM, BN = 32 * WN;
   constexpr int KH = F4 ? 1 : 2;                  // 1 KB chunks per row block and K64 step
   constexpr int A_STEP = BM * 32 * KH;            // one K64 step of weights
@@ -372,8 +372,12 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
       for (int fm = 0; fm < FM; ++fm) {
         const v4i w = F.af[0][fm];
         const v8i af = v8i{w.x, w.y, w.z, w.w, 0, 0, 0, 0};
-        accf[fm] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bf, af, accf[fm], 4, 4, 0,
-                                                                   127, 0, 127);
+        if constexpr (SW)
+          accf[fm] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bf, af, accf[fm], 4, 4, 0,
+                                                                     127, 0, 127);
+        else
+          accf[fm] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af, bf, accf[fm], 4, 4, 0,
+                                                                     127, 0, 127);
       }
       return;
     }
@@ -592,20 +596,24 @@ struct HaloVariant {
   const char* name;    // the kernels as a profiler lists them: unfused,
   const char* sw_name;       // unfused on the transposed layout,
   const char* fused_name;    // fused downsample (transposed layout),
-  const char* f4_name;       // fp4 contraction (transposed layout)
+  const char* f4_name;       // fp4 contraction (transposed layout),
+  const char* f4_idj_name;   // fp4 contraction, identity join (untransposed)
 };
 
 // Index order must match the switch in launch_conv_halo. Variants with
 // fm = 2 (64 output channels) run two workgroups per CU.
 const HaloVariant kHaloVariants[] = {
     {8, 1, 6, 4, 4.0, 0.75, "conv_halo<8, 1, 6, false, 4, false, false>", "conv_halo<8, 1, 6, false, 4, true, false>",
-     "conv_halo<8, 1, 6, true, 4, true, false>", "conv_halo<8, 1, 6, false, 4, true, true>"},
+     "conv_halo<8, 1, 6, true, 4, true, false>", "conv_halo<8, 1, 6, false, 4, true, true>",
+     "conv_halo<8, 1, 6, false, 4, false, true>"},
     {4, 2, 4, 4, 4.0, 0.75, "conv_halo<4, 2, 4, false, 4, false, false>", "conv_halo<4, 2, 4, false, 4, true, false>",
-     "conv_halo<4, 2, 4, true, 4, true, false>", "conv_halo<4, 2, 4, false, 4, true, true>"},
+     "conv_halo<4, 2, 4, true, 4, true, false>", "conv_halo<4, 2, 4, false, 4, true, true>",
+     "conv_halo<4, 2, 4, false, 4, false, true>"},
     {2, 4, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4, false, 4, false, false>", "conv_halo<2, 4, 4, false, 4, true, false>",
-     "conv_halo<2, 4, 4, true, 4, true, false>", "conv_halo<2, 4, 4, false, 4, true, true>"},
+     "conv_halo<2, 4, 4, true, 4, true, false>", "conv_halo<2, 4, 4, false, 4, true, true>",
+     "conv_halo<2, 4, 4, false, 4, false, true>"},
     {8, 1, 6, 2, 4.0, 0.75, "conv_halo<8, 1, 6, false, 2, false, false>", "conv_halo<8, 1, 6, false, 2, true, false>",
-     nullptr, nullptr},   // 64 x 256
+     nullptr, nullptr, nullptr},   // 64 x 256
 };
 constexpr int kNumHalo = sizeof(kHaloVariants) / sizeof(kHaloVariants[0]);
 constexpr int kNumCUs = 256;
@@ -693,9 +701,10 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
 // Which instance of a variant runs: 0 = unfused, 1 = unfused on the
 // transposed layout (the 2-bit threshold epilogue with packed 16-bit
 // compares, the same condition as the kernel's pk), 2 = fused downsample,
-// 3 = the fp4 contraction (a.f4; the same epilogue as 1, checked by the host).
+// 3 = the fp4 contraction (a.f4; the same epilogue as 1, checked by the host),
+// 4 = the fp4 contraction with the identity join (untransposed, as 0).
 int halo_instance(const ConvLaunch& a) {
-  if (a.f4) return 3;
+  if (a.f4) return a.join_kind == IFQ_JOIN_IDENTITY ? 4 : 3;
   if (a.join_kind == IFQ_JOIN_CONV_FUSED) return 2;
   const bool pk = a.out_mode == 2 && a.rec == 4 && (a.cout & 31) == 0 &&
                   27 * a.cin <= 32766 && a.join_kind == IFQ_JOIN_NONE;
@@ -706,7 +715,11 @@ int halo_instance(const ConvLaunch& a) {
 const char* conv_halo_name(const HaloPlan& p, const ConvLaunch& a) {
   const HaloVariant& V = kHaloVariants[p.variant];
   const int inst = halo_instance(a);
-  return inst == 3 ? V.f4_name : inst == 2 ? V.fused_name : inst == 1 ? V.sw_name : V.name;
+  return inst == 4   ? V.f4_idj_name
+         : inst == 3 ? V.f4_name
+         : inst == 2 ? V.fused_name
+         : inst == 1 ? V.sw_name
+                     : V.name;
 }
 
 hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream) {
@@ -714,11 +727,11 @@ hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream)
   const int bm = 32 * kHaloVariants[p.variant].fm;
   const dim3 grid(p.blocks_m, (a.cout + bm - 1) / bm);
   const int inst = halo_instance(a);
-  switch (inst == 3 ? 12 + p.variant : p.variant * 3 + inst) {
+  switch (inst == 4 ? 16 + p.variant : inst == 3 ? 12 + p.variant : p.variant * 3 + inst) {
 #define IFQ_HALO_CASE(k, wn, wk, d, fu, fm, sw) \
     case k: hipLaunchKernelGGL((conv_halo<wn, wk, d, fu, fm, sw>), grid, dim3(512), 0, stream, a); break;
-#define IFQ_HALO_F4(k, wn, wk, d, fm) \
-    case k: hipLaunchKernelGGL((conv_halo<wn, wk, d, false, fm, true, true>), grid, dim3(512), 0, stream, a); break;
+#define IFQ_HALO_F4(k, wn, wk, d, fm, sw) \
+    case k: hipLaunchKernelGGL((conv_halo<wn, wk, d, false, fm, sw, true>), grid, dim3(512), 0, stream, a); break;
     IFQ_HALO_CASE(0, 8, 1, 6, false, 4, false)
     IFQ_HALO_CASE(1, 8, 1, 6, false, 4, true)
     IFQ_HALO_CASE(2, 8, 1, 6, true, 4, true)
@@ -730,9 +743,12 @@ hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream)
     IFQ_HALO_CASE(8, 2, 4, 4, true, 4, true)
     IFQ_HALO_CASE(9, 8, 1, 6, false, 2, false)
     IFQ_HALO_CASE(10, 8, 1, 6, false, 2, true)
-    IFQ_HALO_F4(12, 8, 1, 6, 4)
-    IFQ_HALO_F4(13, 4, 2, 4, 4)
-    IFQ_HALO_F4(14, 2, 4, 4, 4)
+    IFQ_HALO_F4(12, 8, 1, 6, 4, true)
+    IFQ_HALO_F4(13, 4, 2, 4, 4, true)
+    IFQ_HALO_F4(14, 2, 4, 4, 4, true)
+    IFQ_HALO_F4(16, 8, 1, 6, 4, false)
+    IFQ_HALO_F4(17, 4, 2, 4, 4, false)
+    IFQ_HALO_F4(18, 2, 4, 4, 4, false)
 #undef IFQ_HALO_CASE
 #undef IFQ_HALO_F4
     default: return hipErrorInvalidValue;   // no fused kernel for this variant

@@ -178,12 +178,7 @@ class DeviceStack:
                     ho, wo = api.ifq_conv_output_dims(d)
                     rec.pool = api.pool_desc(self.batch, ho, wo, L.cout, Pl.k, Pl.stride,
                                              _POOL_MODE[Pl.mode], L.out_bits, out_layout)
-                if (fp4 and rec.kind == IFQ_LAYER_CONV and L.join is None
-                        and api.ifq_conv_fp4_kernel_name(d)):
-                    rec.kind = IFQ_LAYER_CONV_FP4
-                    self.fp4_layers.append(L.name)
-                blob = (api.ifq_pack_weights_fp4(d, p["w"]) if rec.kind == IFQ_LAYER_CONV_FP4
-                        else api.ifq_pack_weights(d, p["w"]))
+                blob = api.ifq_pack_weights(d, p["w"])
                 wdev = torch.from_numpy(blob).to(self.device)
                 self._keep.append(wdev)
                 rec.w_packed = wdev.data_ptr()
@@ -234,6 +229,15 @@ class DeviceStack:
                                                  None, cdev, p["q_thr"])
                     rec.join_src = (sid(cur(by_name[self.fused[L.name]][1].src))
                                     if L.name in self.fused else sid(cur(L.join[1])))
+                if (fp4 and rec.kind == IFQ_LAYER_CONV and
+                        (L.join is None or L.join[0] == "identity") and
+                        api.ifq_conv_fp4_kernel_name(d, rec.join if L.join else None)):
+                    # the same layer on the fp4 path: its own weight blob
+                    rec.kind = IFQ_LAYER_CONV_FP4
+                    self.fp4_layers.append(L.name)
+                    w4 = torch.from_numpy(api.ifq_pack_weights_fp4(d, p["w"])).to(self.device)
+                    self._keep.append(w4)
+                    rec.w_packed = w4.data_ptr()
                 self.ops += conv_ops(L, self.batch)
                 ho, wo = api.ifq_conv_output_dims(d)
                 out_shape = (self.batch, ho, wo, L.cout)
@@ -396,7 +400,8 @@ class DeviceStack:
             if lay.kind == IFQ_LAYER_CONV_POOL:
                 out.append(api.ifq_conv_pool_kernel_name(lay.conv, lay.pool))
             elif lay.kind == IFQ_LAYER_CONV_FP4:
-                out.append(api.ifq_conv_fp4_kernel_name(lay.conv))
+                join = lay.join if lay.join.kind != IFQ_JOIN_NONE else None
+                out.append(api.ifq_conv_fp4_kernel_name(lay.conv, join))
             elif _is_conv(L):
                 join = lay.join if lay.join.kind != IFQ_JOIN_NONE else None
                 out.append(api.ifq_conv_kernel_name(lay.conv, join))
@@ -450,7 +455,11 @@ class DeviceStack:
         elif rec.kind == IFQ_LAYER_CONV_FP4:
             desc = rec.conv
             join = None
-            args = (ctypes.byref(desc), src, vp(rec.w_packed), vp(rec.thr), dst, st)
+            if rec.join.kind != 0:
+                join = _ffi.Join.from_buffer_copy(rec.join)
+                join.shortcut = self._slot_ptr(rec.join_src, x, y)
+            args = (ctypes.byref(desc), src, vp(rec.w_packed), vp(rec.thr),
+                    None if join is None else ctypes.byref(join), dst, st)
             fn = lib.ifq_conv_forward_fp4
             what = "ifq_conv_forward_fp4"
         elif rec.kind == IFQ_LAYER_CONV_POOL:

@@ -685,7 +685,7 @@ def test_fp4_entry_points_host_side():
                P.conv_desc(2, 28, 28, 128, 128, 3, 1, 1, 2, 2, I8, I8)):
         assert P.ifq_conv_fp4_kernel_name(dd) == ""
     d8 = P.conv_desc(2, 28, 28, 128, 128, 3, 1, 1, 2, 2, I8, I8)
-    assert status_of("ifq_conv_forward_fp4", ctypes.byref(d8), FAKE, FAKE, FAKE, FAKE,
+    assert status_of("ifq_conv_forward_fp4", ctypes.byref(d8), FAKE, FAKE, FAKE, None, FAKE,
                      None) == EUNSUP
 
 
@@ -696,7 +696,7 @@ def test_new_entry_points_accept_an_empty_batch():
     pd = _ffi.PoolDesc(0, 28, 28, 128, 2, 2, 0, 2, B64)
     assert status_of("ifq_conv_pool_forward", ctypes.byref(d), ctypes.byref(pd), None, None,
                      FAKE, None, None) == OK
-    assert status_of("ifq_conv_forward_fp4", ctypes.byref(d), None, None, FAKE, None,
+    assert status_of("ifq_conv_forward_fp4", ctypes.byref(d), None, None, FAKE, None, None,
                      None) == OK
     # the pool must still describe the conv's output
     bad = _ffi.PoolDesc(0, 27, 28, 128, 2, 2, 0, 2, B64)

@@ -75,3 +75,35 @@ def test_fp4_not_offered_for_the_64_channel_tiles(P):
     assert P.ifq_conv_fp4_kernel_name(d) == ""
     with pytest.raises(P.IfqError):
         P.ifq_conv_forward_fp4(d, None, None, None, None)
+
+
+# identity join (the blocks' second convs): name, n, h, channels
+FP4_IDJ = [("f4j_l1_small_batch", 2, 56, 64), ("f4j_l2", 3, 28, 128),
+           ("f4j_l3", 4, 14, 256), ("f4j_l4", 6, 7, 512)]
+
+
+@pytest.mark.parametrize("case", FP4_IDJ, ids=[c[0] for c in FP4_IDJ])
+def test_fp4_identity_join_bit_exact(P, case):
+    import torch
+    name, n, h, c = case
+    L = make_layer(name, h, h, c, c, 3, 1, 1, 2, 2, join=("identity", "x"))
+    seed = zlib.crc32(name.encode()) % 997
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, h, c), 2)
+    sc = codes_for(seed + 1, (n, h, h, c), 2)
+    _, want = oracle_layer(L, x, p, shortcut=sc)
+    assert len(np.unique(want)) > 1
+    table = to_dev(P.ifq_fold_join_table(p, p["beta_in"], 2, 9 * c, 2, p["q_thr"]))
+    scd = upload_codes(P, sc, B64)
+    join = P.make_join(P.IFQ_JOIN_IDENTITY, B64, scd, None, p["q_thr"], table=table)
+    xd = upload_codes(P, x, B64)
+    d = P.conv_desc(n, h, h, c, c, 3, 1, 1, 2, 2, B64, B64)
+    kname = P.ifq_conv_fp4_kernel_name(d, join)
+    assert kname.endswith(", false, true>"), kname
+    wd = to_dev(P.ifq_pack_weights_fp4(d, p["w"]))
+    ob = P.ifq_tensor_bytes(n, h, h, c, B64)
+    y = torch.full((ob,), 0xA5, dtype=torch.uint8, device=device())
+    P.ifq_conv_forward_fp4(d, xd, wd, None, y, join=join)
+    torch.cuda.synchronize()
+    got = y.cpu().numpy().reshape(n, c // 64, h, h, 16)
+    assert np.array_equal(got, expect_layout(want, B64)), (name, kname)

@@ -50,9 +50,12 @@ def check_stack(P, cfg, batch, layout, variant):
     dev = P.DeviceStack(layers, params, batch, code_layout=base, fuse_down=fuse,
                         fuse_pool=fpool, fp4=fp4)
     if fp4 and base == "b64" and cfg == 3:
-        # the 3x3 threshold layers of the ResNet-shaped stack are on fp4 (at
-        # full batch all but the 64-channel ones)
-        assert dev.fp4_layers and all(n.endswith(".conv1") for n in dev.fp4_layers)
+        # the 3x3 threshold and identity-join layers of the ResNet-shaped
+        # stack are on fp4 (at full batch all but the 64-channel ones); the
+        # fused downsample joins stay on int8
+        covered = {L.name for L in layers if hasattr(L, "cin") and
+                   (L.join is None or L.join[0] == "identity")}
+        assert dev.fp4_layers and set(dev.fp4_layers) <= covered
     if fuse:
         # every downsample of a ResNet-shaped stack is folded into its join
         assert len(dev.fused) == sum(1 for L in layers if L.name.endswith(".down"))
