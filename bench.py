@@ -290,6 +290,8 @@ def main():
                     help="run the 2-bit threshold 3x3 layers on the fp4 (e2m1) "
                          "scaled MFMA (same codes; the default is int8 MFMA "
                          "throughout)")
+    ap.add_argument("--no-fp4-compare", action="store_true",
+                    help="skip the extra timing of the same stack on the fp4 path")
     ap.add_argument("--no-fuse-pool", action="store_true",
                     help="run every max-pool as a layer of its own (default: a "
                          "2x2/2 pool inside the conv that feeds it, where a "
@@ -460,6 +462,35 @@ def main():
         "wall_s_timed": wall,
         "roofline": roofline,
     }
+
+    # the same stack with its fp4-covered layers on the fp4 path, timed the
+    # same way after the headline measurement (which stays int8): its output
+    # must be the same bytes
+    if not args.fp4 and not args.no_fp4_compare:
+        dev4 = P.DeviceStack(layers, params, batch, code_layout=args.layout,
+                             fuse_down=not args.no_fuse_down,
+                             fuse_pool=not args.no_fuse_pool, fp4=True)
+        if dev4.fp4_layers:
+            y4 = dev4.alloc_output()
+            with torch.cuda.stream(stream):
+                for _ in range(args.warmup):
+                    dev4.run(x, y4, stream=sh)
+            torch.cuda.synchronize()
+            s4, e4 = hip.events(2)
+            hip.record(s4, sh)
+            for k in range(args.steps):
+                dev4.run(x, y4, stream=sh)
+            hip.record(e4, sh)
+            hip.sync(e4)
+            torch.cuda.synchronize()
+            ms4 = hip.ms(s4, e4) / args.steps
+            out["fp4_variant"] = {
+                "ms_per_step": ms4, "images_per_s": batch / (ms4 * 1e-3),
+                "layers_on_fp4": len(dev4.fp4_layers),
+                "same_output_bytes": bool(torch.equal(y, y4)),
+                "note": "not the headline: int8 MFMA is; fp4 (e2m1) scaled MFMA on the "
+                        "covered 3x3 layers, exact integer sums"}
+            del dev4, y4
 
     if not args.no_cpu_baseline:
         import oracle
