@@ -436,8 +436,10 @@ IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
  * ifq_conv_forward's. Weights come from ifq_pack_weights_fp4.
  * Covered: in_layout BLOCK64, in_bits 2, 3x3, pad 1, stride 1 or 2,
  * c_in % 64 == 0, out_bits 2 in a 2-bit layout, c_out % 32 == 0, and no join
- * (thr as for ifq_conv_forward) or an identity join with a 2-bit packed
- * shortcut (join as for ifq_conv_forward, thr NULL); otherwise UNSUPPORTED
+ * (thr as for ifq_conv_forward), an identity join with a 2-bit packed
+ * shortcut, or a fused downsample join whose down_w is the 1x1 conv's
+ * ifq_pack_weights_fp4 blob (join as for ifq_conv_forward, thr NULL); the
+ * 128-channel tiles of the windowed kernel only; otherwise UNSUPPORTED
  * (ifq_conv_fp4_kernel_name returns ""). Asynchronous.
  * Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
  */

@@ -414,7 +414,7 @@ int64_t fp4_zero_off(const ifq::WeightGeom& g) { return (g.cout_pad / 32) * (g.k
 // no pool, and a plan of the windowed kernel.
 bool fp4_plan(const ifq::ConvLaunch& a, ifq::HaloPlan* hp) {
   const bool join_ok =
-      a.join_kind == IFQ_JOIN_NONE ||
+      a.join_kind == IFQ_JOIN_NONE || a.join_kind == IFQ_JOIN_CONV_FUSED ||
       (a.join_kind == IFQ_JOIN_IDENTITY && (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64 ||
                                             a.sc_layout == IFQ_LAYOUT_U2_NHWC_PACKED));
   if (!(a.out_mode == 2 && a.rec == 4 && a.cout % 32 == 0 && 27 * a.cin <= 32766 && join_ok &&
@@ -839,6 +839,8 @@ IFQ_API ifq_status ifq_conv_forward_fp4(const ifq_conv_desc* d, const void* x,
   a.f4 = 1;
   a.rowsum = nullptr;
   a.wzero = fp4_zero_off(ifq::weight_geom(*d));
+  if (a.join_kind == IFQ_JOIN_CONV_FUSED)   // join->down_w is the down conv's fp4 blob
+    a.d_wzero = fp4_zero_off(ifq::weight_geom(join->down));
   st = hip_status(ifq::launch_conv_halo(a, hp, stream), "conv fp4 launch");
   if (st != IFQ_OK) return st;
   return ok();

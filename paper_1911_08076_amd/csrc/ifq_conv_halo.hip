@@ -67,7 +67,7 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
   static_assert(WN * WK == kHaloNW, "8 waves");
   static_assert(FM == 4 || (FM == 2 && !FUSED), "fused downsample needs FM = 4");
   static_assert(!FUSED || SW, "the fused join runs on the transposed layout");
-  static_assert(!F4 || !FUSED, "the fp4 kernels serve the threshold and identity-join epilogues");
+  static_assert(!F4 || FM == 4, "fp4 kernels: 128-channel tiles");
   constexpr int BM = 32 * FM, BN = 32 * WN;
   constexpr int KH = F4 ? 1 : 2;                  // 1 KB chunks per row block and K64 step
   constexpr int A_STEP = BM * 32 * KH;            // one K64 step of weights
@@ -294,14 +294,33 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
   const bool dreal = fused && wave * 64 < Gd * BN;
   auto issue_down = [&]() {
     const uint32_t slot = lds0 + (uint32_t)((nst % D) * STAGE);
-    const int gd2 = fused ? 2 * Gd : 1;   // (Gd is 0 in the unfused kernels)
-    const int j = wave / gd2, k32 = wave - j * gd2;
+    if constexpr (F4) {
+      // fp4: FM chunks (FM/WK row blocks x Gd = WK K64 steps) per group,
+      // chunk c = wave + 8k as in issue_a (the same loads per wave)
 #pragma unroll
-    for (int i = 0; i < WK; ++i) {
-      const int rb = rbw + i * (FM / WK) + j;
-      const int64_t off = rb < nrb ? ((int64_t)rb * a.d_nk32 + k32) * 1024 : a.d_wzero;
-      dma16s(reinterpret_cast<const uint8_t*>(a.dwgt) + off, voff,
-             slot + (uint32_t)(i * A_STEP + wave * 1024));
+      for (int k = 0; k < CPWA; ++k) {
+        const int c = wave + kHaloNW * k;
+        if (NCH >= kHaloNW || c < NCH) {
+          const int i = c / FM, cc = c - i * FM;
+          const int j = cc / WK, g = cc - j * WK;
+          const int rb = rbw + i * (FM / WK) + j;
+          const int64_t off = rb < nrb ? ((int64_t)rb * WK + g) * 1024 : a.d_wzero;
+          dma16s(reinterpret_cast<const uint8_t*>(a.dwgt) + off, voff,
+                 slot + (uint32_t)(i * A_STEP + cc * 1024));
+        } else {
+          issue_dummy();
+        }
+      }
+    } else {
+      const int gd2 = fused ? 2 * Gd : 1;   // (Gd is 0 in the unfused kernels)
+      const int j = wave / gd2, k32 = wave - j * gd2;
+#pragma unroll
+      for (int i = 0; i < WK; ++i) {
+        const int rb = rbw + i * (FM / WK) + j;
+        const int64_t off = rb < nrb ? ((int64_t)rb * a.d_nk32 + k32) * 1024 : a.d_wzero;
+        dma16s(reinterpret_cast<const uint8_t*>(a.dwgt) + off, voff,
+               slot + (uint32_t)(i * A_STEP + wave * 1024));
+      }
     }
     if (dreal)
       dma16(dsrc, lds0 + (uint32_t)dchunk(wave));
@@ -459,7 +478,32 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
   v16i accd[OWN];
 #pragma unroll
   for (int j = 0; j < OWN; ++j) accd[j] = v16i{0};
-  if constexpr (FUSED) {
+  if constexpr (FUSED && F4) {
+    const uint8_t* as = lds + (nst % D) * STAGE + kg * A_STEP;
+    v16f accdf[OWN];
+#pragma unroll
+    for (int j = 0; j < OWN; ++j) accdf[j] = v16f{0.0f};
+    for (int g = 0; g < Gd; ++g) {
+      const int e = g * BN + wn * 32 + l32;
+      const v2i braw =
+          *reinterpret_cast<const v2i*>(lds + dchunk(e >> 6) + (e & 63) * 16 + 8 * h);
+      const uint32_t w0 = (uint32_t)braw[0], w1 = (uint32_t)braw[1];
+      const v8i bf = v8i{(int)(w0 & 0x33333333u), (int)((w0 >> 2) & 0x33333333u),
+                         (int)(w1 & 0x33333333u), (int)((w1 >> 2) & 0x33333333u), 0, 0, 0, 0};
+#pragma unroll
+      for (int j = 0; j < OWN; ++j) {
+        const v4i w = *reinterpret_cast<const v4i*>(as + (j * Gd + g) * 1024 + lane * 16);
+        const v8i af = v8i{w.x, w.y, w.z, w.w, 0, 0, 0, 0};
+        accdf[j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bf, af, accdf[j], 4, 4, 0,
+                                                                   127, 0, 127);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < OWN; ++j)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) accd[j][i] = (int)accdf[j][i];
+    __syncthreads();   // before the K-group exchange reuses this LDS
+  } else if constexpr (FUSED) {
     const uint8_t* as = lds + (nst % D) * STAGE + kg * A_STEP;
     for (int g = 0; g < Gd; ++g) {
       const int e = g * BN + wn * 32 + l32;
@@ -597,7 +641,8 @@ struct HaloVariant {
   const char* sw_name;       // unfused on the transposed layout,
   const char* fused_name;    // fused downsample (transposed layout),
   const char* f4_name;       // fp4 contraction (transposed layout),
-  const char* f4_idj_name;   // fp4 contraction, identity join (untransposed)
+  const char* f4_idj_name;   // fp4 contraction, identity join (untransposed),
+  const char* f4_fused_name; // fp4 contraction, fused downsample (transposed)
 };
 
 // Index order must match the switch in launch_conv_halo. Variants with
@@ -605,15 +650,15 @@ struct HaloVariant {
 const HaloVariant kHaloVariants[] = {
     {8, 1, 6, 4, 4.0, 0.75, "conv_halo<8, 1, 6, false, 4, false, false>", "conv_halo<8, 1, 6, false, 4, true, false>",
      "conv_halo<8, 1, 6, true, 4, true, false>", "conv_halo<8, 1, 6, false, 4, true, true>",
-     "conv_halo<8, 1, 6, false, 4, false, true>"},
+     "conv_halo<8, 1, 6, false, 4, false, true>", "conv_halo<8, 1, 6, true, 4, true, true>"},
     {4, 2, 4, 4, 4.0, 0.75, "conv_halo<4, 2, 4, false, 4, false, false>", "conv_halo<4, 2, 4, false, 4, true, false>",
      "conv_halo<4, 2, 4, true, 4, true, false>", "conv_halo<4, 2, 4, false, 4, true, true>",
-     "conv_halo<4, 2, 4, false, 4, false, true>"},
+     "conv_halo<4, 2, 4, false, 4, false, true>", "conv_halo<4, 2, 4, true, 4, true, true>"},
     {2, 4, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4, false, 4, false, false>", "conv_halo<2, 4, 4, false, 4, true, false>",
      "conv_halo<2, 4, 4, true, 4, true, false>", "conv_halo<2, 4, 4, false, 4, true, true>",
-     "conv_halo<2, 4, 4, false, 4, false, true>"},
+     "conv_halo<2, 4, 4, false, 4, false, true>", "conv_halo<2, 4, 4, true, 4, true, true>"},
     {8, 1, 6, 2, 4.0, 0.75, "conv_halo<8, 1, 6, false, 2, false, false>", "conv_halo<8, 1, 6, false, 2, true, false>",
-     nullptr, nullptr, nullptr},   // 64 x 256
+     nullptr, nullptr, nullptr, nullptr},   // 64 x 256
 };
 constexpr int kNumHalo = sizeof(kHaloVariants) / sizeof(kHaloVariants[0]);
 constexpr int kNumCUs = 256;
@@ -702,9 +747,11 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
 // transposed layout (the 2-bit threshold epilogue with packed 16-bit
 // compares, the same condition as the kernel's pk), 2 = fused downsample,
 // 3 = the fp4 contraction (a.f4; the same epilogue as 1, checked by the host),
-// 4 = the fp4 contraction with the identity join (untransposed, as 0).
+// 4 = the fp4 contraction with the identity join (untransposed, as 0),
+// 5 = the fp4 contraction with the fused downsample (as 2).
 int halo_instance(const ConvLaunch& a) {
-  if (a.f4) return a.join_kind == IFQ_JOIN_IDENTITY ? 4 : 3;
+  if (a.f4)
+    return a.join_kind == IFQ_JOIN_IDENTITY ? 4 : a.join_kind == IFQ_JOIN_CONV_FUSED ? 5 : 3;
   if (a.join_kind == IFQ_JOIN_CONV_FUSED) return 2;
   const bool pk = a.out_mode == 2 && a.rec == 4 && (a.cout & 31) == 0 &&
                   27 * a.cin <= 32766 && a.join_kind == IFQ_JOIN_NONE;
@@ -715,7 +762,8 @@ int halo_instance(const ConvLaunch& a) {
 const char* conv_halo_name(const HaloPlan& p, const ConvLaunch& a) {
   const HaloVariant& V = kHaloVariants[p.variant];
   const int inst = halo_instance(a);
-  return inst == 4   ? V.f4_idj_name
+  return inst == 5   ? V.f4_fused_name
+         : inst == 4 ? V.f4_idj_name
          : inst == 3 ? V.f4_name
          : inst == 2 ? V.fused_name
          : inst == 1 ? V.sw_name
@@ -727,11 +775,14 @@ hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream)
   const int bm = 32 * kHaloVariants[p.variant].fm;
   const dim3 grid(p.blocks_m, (a.cout + bm - 1) / bm);
   const int inst = halo_instance(a);
-  switch (inst == 4 ? 16 + p.variant : inst == 3 ? 12 + p.variant : p.variant * 3 + inst) {
+  switch (inst == 5   ? 20 + p.variant
+          : inst == 4 ? 16 + p.variant
+          : inst == 3 ? 12 + p.variant
+                      : p.variant * 3 + inst) {
 #define IFQ_HALO_CASE(k, wn, wk, d, fu, fm, sw) \
     case k: hipLaunchKernelGGL((conv_halo<wn, wk, d, fu, fm, sw>), grid, dim3(512), 0, stream, a); break;
-#define IFQ_HALO_F4(k, wn, wk, d, fm, sw) \
-    case k: hipLaunchKernelGGL((conv_halo<wn, wk, d, false, fm, sw, true>), grid, dim3(512), 0, stream, a); break;
+#define IFQ_HALO_F4(k, wn, wk, d, fu, fm, sw) \
+    case k: hipLaunchKernelGGL((conv_halo<wn, wk, d, fu, fm, sw, true>), grid, dim3(512), 0, stream, a); break;
     IFQ_HALO_CASE(0, 8, 1, 6, false, 4, false)
     IFQ_HALO_CASE(1, 8, 1, 6, false, 4, true)
     IFQ_HALO_CASE(2, 8, 1, 6, true, 4, true)
@@ -743,12 +794,15 @@ hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream)
     IFQ_HALO_CASE(8, 2, 4, 4, true, 4, true)
     IFQ_HALO_CASE(9, 8, 1, 6, false, 2, false)
     IFQ_HALO_CASE(10, 8, 1, 6, false, 2, true)
-    IFQ_HALO_F4(12, 8, 1, 6, 4, true)
-    IFQ_HALO_F4(13, 4, 2, 4, 4, true)
-    IFQ_HALO_F4(14, 2, 4, 4, 4, true)
-    IFQ_HALO_F4(16, 8, 1, 6, 4, false)
-    IFQ_HALO_F4(17, 4, 2, 4, 4, false)
-    IFQ_HALO_F4(18, 2, 4, 4, 4, false)
+    IFQ_HALO_F4(12, 8, 1, 6, false, 4, true)
+    IFQ_HALO_F4(13, 4, 2, 4, false, 4, true)
+    IFQ_HALO_F4(14, 2, 4, 4, false, 4, true)
+    IFQ_HALO_F4(16, 8, 1, 6, false, 4, false)
+    IFQ_HALO_F4(17, 4, 2, 4, false, 4, false)
+    IFQ_HALO_F4(18, 2, 4, 4, false, 4, false)
+    IFQ_HALO_F4(20, 8, 1, 6, true, 4, true)
+    IFQ_HALO_F4(21, 4, 2, 4, true, 4, true)
+    IFQ_HALO_F4(22, 2, 4, 4, true, 4, true)
 #undef IFQ_HALO_CASE
 #undef IFQ_HALO_F4
     default: return hipErrorInvalidValue;   // no fused kernel for this variant

@@ -230,14 +230,22 @@ class DeviceStack:
                     rec.join_src = (sid(cur(by_name[self.fused[L.name]][1].src))
                                     if L.name in self.fused else sid(cur(L.join[1])))
                 if (fp4 and rec.kind == IFQ_LAYER_CONV and
-                        (L.join is None or L.join[0] == "identity") and
-                        api.ifq_conv_fp4_kernel_name(d, rec.join if L.join else None)):
-                    # the same layer on the fp4 path: its own weight blob
+                        (L.join is None or L.join[0] == "identity" or L.name in self.fused)
+                        and api.ifq_conv_fp4_kernel_name(d, rec.join if L.join else None)):
+                    # the same layer on the fp4 path: its own weight blob (and
+                    # the fused downsample's)
                     rec.kind = IFQ_LAYER_CONV_FP4
                     self.fp4_layers.append(L.name)
                     w4 = torch.from_numpy(api.ifq_pack_weights_fp4(d, p["w"])).to(self.device)
                     self._keep.append(w4)
                     rec.w_packed = w4.data_ptr()
+                    if L.name in self.fused:
+                        D = by_name[self.fused[L.name]][1]
+                        pd = params[by_name[D.name][0]]
+                        d4 = torch.from_numpy(api.ifq_pack_weights_fp4(
+                            rec.join.down, pd["w"])).to(self.device)
+                        self._keep.append(d4)
+                        rec.join.down_w = d4.data_ptr()
                 self.ops += conv_ops(L, self.batch)
                 ho, wo = api.ifq_conv_output_dims(d)
                 out_shape = (self.batch, ho, wo, L.cout)

@@ -50,11 +50,10 @@ def check_stack(P, cfg, batch, layout, variant):
     dev = P.DeviceStack(layers, params, batch, code_layout=base, fuse_down=fuse,
                         fuse_pool=fpool, fp4=fp4)
     if fp4 and base == "b64" and cfg == 3:
-        # the 3x3 threshold and identity-join layers of the ResNet-shaped
-        # stack are on fp4 (at full batch all but the 64-channel ones); the
-        # fused downsample joins stay on int8
+        # the 3x3 layers of the ResNet-shaped stack are on fp4 (at full batch
+        # all but the 64-channel ones), the fused downsample joins included
         covered = {L.name for L in layers if hasattr(L, "cin") and
-                   (L.join is None or L.join[0] == "identity")}
+                   (L.join is None or L.join[0] == "identity" or L.name in dev.fused)}
         assert dev.fp4_layers and set(dev.fp4_layers) <= covered
     if fuse:
         # every downsample of a ResNet-shaped stack is folded into its join
