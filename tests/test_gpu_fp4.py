@@ -107,3 +107,40 @@ def test_fp4_identity_join_bit_exact(P, case):
     torch.cuda.synchronize()
     got = y.cpu().numpy().reshape(n, c // 64, h, h, 16)
     assert np.array_equal(got, expect_layout(want, B64)), (name, kname)
+
+
+# conv2 of a downsampling block with the 1x1/2 downsample inside the kernel
+# (IFQ_JOIN_CONV_FUSED), both convs on fp4: the three ResNet-18 shapes at
+# small batch, one ragged
+FP4_FUSED = [(2, 56, 64, 128), (3, 28, 128, 256), (2, 14, 256, 512), (5, 13, 64, 128)]
+
+
+@pytest.mark.parametrize("shape", FP4_FUSED, ids=["x".join(map(str, f)) for f in FP4_FUSED])
+def test_fp4_fused_downsample_bit_exact(P, shape):
+    import torch
+    n, hin, cin, cout = shape
+    D = make_layer("down", hin, hin, cin, cout, 1, 2, 0, 2, 0)
+    ho = (hin - 1) // 2 + 1
+    L = make_layer("conv2", ho, ho, cout, cout, 3, 1, 1, join=("conv", "d", "down"))
+    pd = params_for(15 + hin, D)
+    p = params_for(16 + hin, L)
+    xin = codes_for(15 + hin, (n, hin, hin, cin), 2)
+    x = codes_for(16 + hin, (n, ho, ho, cout), 2)
+    want_d, _ = oracle_layer(D, xin, pd)
+    _, want = oracle_layer(L, x, p, shortcut=want_d, down=pd)
+    d = P.conv_desc(n, ho, ho, cout, cout, 3, 1, 1, 2, 2, B64, B64)
+    dd = P.conv_desc(n, hin, hin, cin, cout, 1, 2, 0, 2, 0, B64, P.IFQ_LAYOUT_I32_NHWC)
+    coef = to_dev(P.ifq_fold_join(P.IFQ_JOIN_CONV, p, pd["beta_in"], down=pd))
+    w4 = to_dev(P.ifq_pack_weights_fp4(d, p["w"]))
+    dw4 = to_dev(P.ifq_pack_weights_fp4(dd, pd["w"]))
+    xind = upload_codes(P, xin, B64)
+    xd = upload_codes(P, x, B64)
+    join = P.make_join(P.IFQ_JOIN_CONV_FUSED, B64, xind, coef, p["q_thr"], down_w=dw4, down=dd)
+    kname = P.ifq_conv_fp4_kernel_name(d, join)
+    assert kname.endswith(", true, 4, true, true>"), kname
+    ob = P.ifq_tensor_bytes(n, ho, ho, cout, B64)
+    y = torch.full((ob,), 0xA5, dtype=torch.uint8, device=device())
+    P.ifq_conv_forward_fp4(d, xd, w4, None, y, join=join)
+    torch.cuda.synchronize()
+    got = y.cpu().numpy().reshape(n, cout // 64, ho, ho, 16)
+    assert np.array_equal(got, expect_layout(want, B64)), (shape, kname)
