@@ -77,6 +77,7 @@ typedef int32_t ifq_status;
 #define IFQ_LAYER_POOL 1
 #define IFQ_LAYER_CONV_POOL 2 /* conv with its max-pool fused (see ifq_conv_pool_forward) */
 #define IFQ_LAYER_CONV_FP4 3  /* conv on the fp4 path (see ifq_conv_forward_fp4) */
+#define IFQ_LAYER_CONV_POOL_FP4 4 /* CONV_POOL on the fp4 path (ifq_conv_pool_forward_fp4) */
 
 #define IFQ_MAX_THRESHOLDS 15 /* 2^4 - 1: codes of up to 4 bits */
 
@@ -234,9 +235,10 @@ typedef struct ifq_pool_desc {
  *   kind        IFQ_LAYER_CONV, IFQ_LAYER_POOL, IFQ_LAYER_CONV_POOL (conv
  *               without join whose codes go through pool before dst; its
  *               pool desc describes the conv's output as for
- *               ifq_conv_pool_forward) or IFQ_LAYER_CONV_FP4 (conv without
- *               join on the fp4 path; w_packed is its ifq_pack_weights_fp4
- *               blob)
+ *               ifq_conv_pool_forward), IFQ_LAYER_CONV_FP4 (conv on the fp4
+ *               path; w_packed is its ifq_pack_weights_fp4 blob, a fused
+ *               join's down_w the down conv's) or IFQ_LAYER_CONV_POOL_FP4
+ *               (CONV_POOL on the fp4 path)
  *   src, dst    tensor slots: 0 is the stack input x, 1 the stack output y,
  *               2 .. n_slots-1 live in the caller's workspace
  *   join_src    slot of the join shortcut (conv layers with join.kind != 0),
@@ -450,6 +452,19 @@ IFQ_API ifq_status ifq_conv_forward_fp4(const ifq_conv_desc* d, const void* x,
 /* Name of the kernel ifq_conv_forward_fp4 launches for d and join (nullable),
  * "" if none. Host. */
 IFQ_API const char* ifq_conv_fp4_kernel_name(const ifq_conv_desc* d, const ifq_join* join);
+
+/*
+ * ifq_conv_pool_forward with the contraction on the fp4 path (as
+ * ifq_conv_forward_fp4; w_fp4 from ifq_pack_weights_fp4): the same pooled
+ * codes. Covered where both a fused-pool plan and an fp4 instance of the
+ * windowed kernel exist; otherwise UNSUPPORTED (the name query returns "").
+ * Errors: INVALID_ARGUMENT, UNSUPPORTED, HIP.
+ */
+IFQ_API ifq_status ifq_conv_pool_forward_fp4(const ifq_conv_desc* d, const ifq_pool_desc* p,
+                                             const void* x, const void* w_fp4,
+                                             const int32_t* thr, void* y, hipStream_t stream);
+IFQ_API const char* ifq_conv_pool_fp4_kernel_name(const ifq_conv_desc* d,
+                                                  const ifq_pool_desc* p);
 
 /*
  * Bytes of the fp4 weight blob of a layer (0 unless in_bits 2, c_in % 64 == 0

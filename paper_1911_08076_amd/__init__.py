@@ -21,4 +21,4 @@ from ._ffi import (IFQ_LAYOUT_I8_NHWC, IFQ_LAYOUT_U2_NHWC_PACKED,  # noqa: E402,
                    IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY, IFQ_JOIN_CONV,
                    IFQ_JOIN_CONV_FUSED,
                    IFQ_LAYER_CONV, IFQ_LAYER_POOL, IFQ_LAYER_CONV_POOL,
-                   IFQ_LAYER_CONV_FP4)
+                   IFQ_LAYER_CONV_FP4, IFQ_LAYER_CONV_POOL_FP4)

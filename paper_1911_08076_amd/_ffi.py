@@ -34,6 +34,7 @@ IFQ_LAYER_CONV = 0
 IFQ_LAYER_POOL = 1
 IFQ_LAYER_CONV_POOL = 2
 IFQ_LAYER_CONV_FP4 = 3
+IFQ_LAYER_CONV_POOL_FP4 = 4
 
 IFQ_MAX_THRESHOLDS = 15
 
@@ -115,6 +116,10 @@ SIGNATURES = [
                                                    ctypes.POINTER(Join)]),
     ("ifq_packed_weight_bytes_fp4", size_t, [ctypes.POINTER(ConvDesc)]),
     ("ifq_pack_weights_fp4", i32, [ctypes.POINTER(ConvDesc), vp, vp, size_t]),
+    ("ifq_conv_pool_forward_fp4", i32, [ctypes.POINTER(ConvDesc), ctypes.POINTER(PoolDesc),
+                                        vp, vp, vp, vp, vp]),
+    ("ifq_conv_pool_fp4_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc),
+                                                        ctypes.POINTER(PoolDesc)]),
     ("ifq_conv_pool_forward", i32, [ctypes.POINTER(ConvDesc), ctypes.POINTER(PoolDesc),
                                     vp, vp, vp, vp, vp]),
     ("ifq_conv_pool_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc),

@@ -250,6 +250,16 @@ def ifq_conv_pool_forward(desc, pool, x, w_packed, thr, y, stream=None):
         _ptr(y), _stream(stream)), "ifq_conv_pool_forward")
 
 
+def ifq_conv_pool_forward_fp4(desc, pool, x, w_fp4, thr, y, stream=None):
+    _check(_lib().ifq_conv_pool_forward_fp4(
+        ctypes.byref(desc), ctypes.byref(pool), _ptr(x), _ptr(w_fp4), _ptr(thr), _ptr(y),
+        _stream(stream)), "ifq_conv_pool_forward_fp4")
+
+
+def ifq_conv_pool_fp4_kernel_name(desc, pool):
+    return _lib().ifq_conv_pool_fp4_kernel_name(ctypes.byref(desc), ctypes.byref(pool)).decode()
+
+
 def ifq_conv_pool_kernel_name(desc, pool):
     return _lib().ifq_conv_pool_kernel_name(ctypes.byref(desc), ctypes.byref(pool)).decode()
 

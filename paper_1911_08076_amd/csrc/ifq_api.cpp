@@ -418,7 +418,7 @@ bool fp4_plan(const ifq::ConvLaunch& a, ifq::HaloPlan* hp) {
       (a.join_kind == IFQ_JOIN_IDENTITY && (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64 ||
                                             a.sc_layout == IFQ_LAYOUT_U2_NHWC_PACKED));
   if (!(a.out_mode == 2 && a.rec == 4 && a.cout % 32 == 0 && 27 * a.cin <= 32766 && join_ok &&
-        a.pool_k == 0 && a.m > 0))
+        (a.pool_k == 0 || a.join_kind == IFQ_JOIN_NONE) && a.m > 0))
     return false;
   // only where the int8 plan's variant has an fp4 instance: the
   // 64-channel layers, whose two-workgroups-per-CU variant has none, measured
@@ -874,6 +874,41 @@ IFQ_API ifq_status ifq_conv_pool_forward(const ifq_conv_desc* d, const ifq_pool_
   return ok();
 }
 
+IFQ_API const char* ifq_conv_pool_fp4_kernel_name(const ifq_conv_desc* d,
+                                                  const ifq_pool_desc* p) {
+  int64_t ho, wo;
+  if (check_conv_pool(d, p, &ho, &wo) != IFQ_OK) return "";
+  ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                  nullptr, nullptr);
+  add_pool(a, *p);
+  ifq::HaloPlan hp;
+  if (!ifq::mfma_eligible(a) || !fp4_plan(a, &hp)) return "";
+  a.f4 = 1;
+  return ifq::conv_halo_name(hp, a);
+}
+
+IFQ_API ifq_status ifq_conv_pool_forward_fp4(const ifq_conv_desc* d, const ifq_pool_desc* p,
+                                             const void* x, const void* w_fp4,
+                                             const int32_t* thr, void* y, hipStream_t stream) {
+  int64_t ho, wo;
+  ifq_status st = check_conv_pool(d, p, &ho, &wo);
+  if (st != IFQ_OK) return st;
+  st = conv_args_check(d, x, w_fp4, thr, nullptr, nullptr, y);
+  if (st != IFQ_OK) return st;
+  if (d->n == 0) return ok();
+  ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_fp4, thr, nullptr, nullptr, y, nullptr);
+  add_pool(a, *p);
+  ifq::HaloPlan hp;
+  if (!ifq::mfma_eligible(a) || !fp4_plan(a, &hp))
+    return fail(IFQ_ERR_UNSUPPORTED, "conv+pool fp4: no fp4 kernel covers this pair");
+  a.f4 = 1;
+  a.rowsum = nullptr;
+  a.wzero = fp4_zero_off(ifq::weight_geom(*d));
+  st = hip_status(ifq::launch_conv_halo(a, hp, stream), "conv+pool fp4 launch");
+  if (st != IFQ_OK) return st;
+  return ok();
+}
+
 IFQ_API ifq_status ifq_maxpool_codes(const ifq_pool_desc* d, const void* x,
                                      void* y, hipStream_t stream) {
   int64_t ho, wo;
@@ -927,7 +962,7 @@ struct SlotPlan {
 };
 
 int64_t layer_out_bytes(const ifq_layer& L) {
-  if (L.kind == IFQ_LAYER_CONV_POOL) {
+  if (L.kind == IFQ_LAYER_CONV_POOL || L.kind == IFQ_LAYER_CONV_POOL_FP4) {
     // the pooled tensor (pool checked by plan_stack before this is used)
     int64_t pho = 0, pwo = 0;
     if (check_pool(&L.pool, &pho, &pwo) != IFQ_OK) return 0;
@@ -950,7 +985,8 @@ int64_t layer_out_bytes(const ifq_layer& L) {
 }
 
 int64_t layer_in_bytes(const ifq_layer& L) {
-  if (L.kind == IFQ_LAYER_CONV || L.kind == IFQ_LAYER_CONV_POOL || L.kind == IFQ_LAYER_CONV_FP4)
+  if (L.kind == IFQ_LAYER_CONV || L.kind == IFQ_LAYER_CONV_POOL || L.kind == IFQ_LAYER_CONV_FP4 ||
+      L.kind == IFQ_LAYER_CONV_POOL_FP4)
     return tensor_bytes(L.conv.n, L.conv.h, L.conv.w, L.conv.c_in, L.conv.in_layout);
   return tensor_bytes(L.pool.n, L.pool.h, L.pool.w, L.pool.c, L.pool.layout);
 }
@@ -999,6 +1035,15 @@ ifq_status plan_stack(const ifq_stack* s, SlotPlan* plan) {
                     L.join_src);
       if (L.conv.n > 0 && !*ifq_conv_fp4_kernel_name(&L.conv, &L.join))
         return fail(IFQ_ERR_UNSUPPORTED, "layer %d: no fp4 kernel covers it", i);
+    } else if (L.kind == IFQ_LAYER_CONV_POOL_FP4) {
+      int64_t ho, wo;
+      st = check_conv_pool(&L.conv, &L.pool, &ho, &wo);
+      if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+      st = conv_args_check(&L.conv, (const void*)1, L.w_packed, L.thr, nullptr, nullptr,
+                           (const void*)1);
+      if (st != IFQ_OK) return fail(st, "layer %d: %s", i, g_last_error.c_str());
+      if (L.conv.n > 0 && !*ifq_conv_pool_fp4_kernel_name(&L.conv, &L.pool))
+        return fail(IFQ_ERR_UNSUPPORTED, "layer %d: no fp4 conv+pool kernel covers it", i);
     } else if (L.kind == IFQ_LAYER_CONV_POOL) {
       int64_t ho, wo;
       st = check_conv_pool(&L.conv, &L.pool, &ho, &wo);
@@ -1088,6 +1133,9 @@ IFQ_API ifq_status ifq_run_stack(const ifq_stack* s, const void* x, void* y,
                                             L.thr, &j, sc, slot(L.dst), nullptr);
       (void)conv_ws;
       st = hip_status(ifq::launch_conv(a, stream), "conv launch");
+    } else if (L.kind == IFQ_LAYER_CONV_POOL_FP4) {
+      st = ifq_conv_pool_forward_fp4(&L.conv, &L.pool, slot(L.src), L.w_packed, L.thr,
+                                     slot(L.dst), stream);
     } else if (L.kind == IFQ_LAYER_CONV_FP4) {
       ifq_join j = L.join;
       if (j.kind != IFQ_JOIN_NONE) j.shortcut = slot(L.join_src);

@@ -19,7 +19,7 @@ import numpy as np
 
 from . import _ffi, api
 from ._ffi import (Layer, Stack, IFQ_LAYER_CONV, IFQ_LAYER_POOL, IFQ_LAYER_CONV_POOL,
-                   IFQ_LAYER_CONV_FP4,
+                   IFQ_LAYER_CONV_FP4, IFQ_LAYER_CONV_POOL_FP4,
                    IFQ_LAYOUT_I8_NHWC, IFQ_LAYOUT_U2_NHWC_PACKED,
                    IFQ_LAYOUT_I32_NHWC, IFQ_LAYOUT_U2_BLOCK64, IFQ_JOIN_NONE, IFQ_JOIN_IDENTITY,
                    IFQ_JOIN_CONV, IFQ_JOIN_CONV_FUSED, IFQ_POOL_VALID, IFQ_POOL_SAME)
@@ -246,6 +246,13 @@ class DeviceStack:
                             rec.join.down, pd["w"])).to(self.device)
                         self._keep.append(d4)
                         rec.join.down_w = d4.data_ptr()
+                elif (fp4 and rec.kind == IFQ_LAYER_CONV_POOL and
+                      api.ifq_conv_pool_fp4_kernel_name(d, rec.pool)):
+                    rec.kind = IFQ_LAYER_CONV_POOL_FP4
+                    self.fp4_layers.append(L.name)
+                    w4 = torch.from_numpy(api.ifq_pack_weights_fp4(d, p["w"])).to(self.device)
+                    self._keep.append(w4)
+                    rec.w_packed = w4.data_ptr()
                 self.ops += conv_ops(L, self.batch)
                 ho, wo = api.ifq_conv_output_dims(d)
                 out_shape = (self.batch, ho, wo, L.cout)
@@ -410,6 +417,8 @@ class DeviceStack:
             elif lay.kind == IFQ_LAYER_CONV_FP4:
                 join = lay.join if lay.join.kind != IFQ_JOIN_NONE else None
                 out.append(api.ifq_conv_fp4_kernel_name(lay.conv, join))
+            elif lay.kind == IFQ_LAYER_CONV_POOL_FP4:
+                out.append(api.ifq_conv_pool_fp4_kernel_name(lay.conv, lay.pool))
             elif _is_conv(L):
                 join = lay.join if lay.join.kind != IFQ_JOIN_NONE else None
                 out.append(api.ifq_conv_kernel_name(lay.conv, join))
@@ -470,13 +479,14 @@ class DeviceStack:
                     None if join is None else ctypes.byref(join), dst, st)
             fn = lib.ifq_conv_forward_fp4
             what = "ifq_conv_forward_fp4"
-        elif rec.kind == IFQ_LAYER_CONV_POOL:
+        elif rec.kind in (IFQ_LAYER_CONV_POOL, IFQ_LAYER_CONV_POOL_FP4):
             desc = (rec.conv, rec.pool)
             join = None
             args = (ctypes.byref(rec.conv), ctypes.byref(rec.pool), src, vp(rec.w_packed),
                     vp(rec.thr), dst, st)
-            fn = lib.ifq_conv_pool_forward
-            what = "ifq_conv_pool_forward"
+            f4 = rec.kind == IFQ_LAYER_CONV_POOL_FP4
+            fn = lib.ifq_conv_pool_forward_fp4 if f4 else lib.ifq_conv_pool_forward
+            what = "ifq_conv_pool_forward_fp4" if f4 else "ifq_conv_pool_forward"
         else:
             desc = rec.pool
             args = (ctypes.byref(desc), src, dst, st)

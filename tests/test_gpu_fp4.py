@@ -144,3 +144,37 @@ def test_fp4_fused_downsample_bit_exact(P, shape):
     torch.cuda.synchronize()
     got = y.cpu().numpy().reshape(n, cout // 64, ho, ho, 16)
     assert np.array_equal(got, expect_layout(want, B64)), (shape, kname)
+
+
+# conv + fused max-pool on the fp4 path (the VGG and YOLO shapes of the
+# window-row pools): name, n, h, c_in, c_out
+FP4_POOL = [("f4p_vgg_conv4_3", 2, 28, 512, 512), ("f4p_yolo_c5", 2, 26, 128, 256),
+            ("f4p_vgg_conv2_2", 1, 112, 128, 128)]
+
+
+@pytest.mark.parametrize("case", FP4_POOL, ids=[c[0] for c in FP4_POOL])
+def test_fp4_conv_pool_bit_exact(P, case):
+    import torch
+    import oracle
+    name, n, h, cin, cout = case
+    L = make_layer(name, h, h, cin, cout, 3, 1, 1, 2, 2)
+    seed = zlib.crc32(name.encode()) % 997
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, h, cin), 2)
+    _, codes = oracle_layer(L, x, p)
+    want = oracle.maxpool(codes, 2, 2, "valid")
+    thr = to_dev(P.ifq_fold_thresholds(cout, 2, 2, 9 * cin, p["alpha"], p["beta_in"],
+                                       p["q_thr"], bias=p["bias"], mean=p["mean"], var=p["var"],
+                                       gamma=p["gamma"], bn_beta=p["bn_beta"], eps=p["eps"]))
+    d = P.conv_desc(n, h, h, cin, cout, 3, 1, 1, 2, 2, B64, B64)
+    pd = P.pool_desc(n, h, h, cout, 2, 2, P.IFQ_POOL_VALID, 2, B64)
+    kname = P.ifq_conv_pool_fp4_kernel_name(d, pd)
+    assert kname.endswith(", true, true>"), kname
+    w4 = to_dev(P.ifq_pack_weights_fp4(d, p["w"]))
+    xd = upload_codes(P, x, B64)
+    ob = P.ifq_tensor_bytes(n, h // 2, h // 2, cout, B64)
+    y = torch.full((ob,), 0xA5, dtype=torch.uint8, device=device())
+    P.ifq_conv_pool_forward_fp4(d, pd, xd, w4, thr, y)
+    torch.cuda.synchronize()
+    got = y.cpu().numpy().reshape(n, cout // 64, h // 2, h // 2, 16)
+    assert np.array_equal(got, expect_layout(want, B64)), (name, kname)

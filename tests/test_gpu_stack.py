@@ -42,11 +42,11 @@ def check_stack(P, cfg, batch, layout, variant):
     layers = get_stack(cfg).layers
     # "b64f": downsamples inside their joins; "...p": pools inside the convs
     # that feed them, where a fused kernel covers the pair
-    fuse = layout in ("b64f", "b64p", "b64pa", "b64fp4")
-    fpool = "all" if layout.endswith("pa") else layout.endswith("p")
+    fuse = layout in ("b64f", "b64p", "b64pa", "b64fp4", "b64pfp4")
+    fpool = "all" if layout.endswith("pa") else (layout.endswith("p") or layout == "b64pfp4")
     fp4 = layout.endswith("fp4")
     base = {"b64f": "b64", "b64p": "b64", "b64pa": "b64", "i8p": "i8",
-            "b64fp4": "b64"}.get(layout, layout)
+            "b64fp4": "b64", "b64pfp4": "b64"}.get(layout, layout)
     dev = P.DeviceStack(layers, params, batch, code_layout=base, fuse_down=fuse,
                         fuse_pool=fpool, fp4=fp4)
     if fp4 and base == "b64" and cfg == 3:
@@ -62,7 +62,8 @@ def check_stack(P, cfg, batch, layout, variant):
         names = dev.layer_kernel_names()
         for i, L in enumerate(dev.layers):
             if L.name in dev.fused_pool:
-                assert dev._layers[i].kind == P.IFQ_LAYER_CONV_POOL and names[i]
+                assert dev._layers[i].kind in (P.IFQ_LAYER_CONV_POOL,
+                                               P.IFQ_LAYER_CONV_POOL_FP4) and names[i]
     xd = dev.upload_input(x)
     y = dev.alloc_output()
     dev.run(xd, y)
@@ -101,7 +102,7 @@ SMALL = [(0, 1), (1, 2), (2, 1), (3, 2), (4, 1)]
 
 
 @pytest.mark.parametrize("layout", ["i8", "u2", "b64", "b64f", "b64p", "b64pa", "i8p",
-                                    "b64fp4"])
+                                    "b64fp4", "b64pfp4"])
 @pytest.mark.parametrize("cfg,batch", SMALL)
 def test_stack_small_batch(P, cfg, batch, layout):
     for variant in ("calibrated", "plain"):
