@@ -79,9 +79,10 @@ class Hip:
 
 def kernel_peak(name):
     """Dense peak of the matrix instructions a kernel runs on: the fp4
-    instances of the windowed kernel (last template argument true after the
-    transposed flag) against MXFP4, the others against int8."""
-    return PEAK_FP4_TFLOPS if name.endswith(", true, true>") else PEAK_INT8_TOPS
+    instances of the windowed kernel (its last template argument, the fp4
+    flag, true) against MXFP4, the others against int8."""
+    fp4 = name.startswith("conv_halo<") and name.endswith(", true>")
+    return PEAK_FP4_TFLOPS if fp4 else PEAK_INT8_TOPS
 
 
 def source_hash():

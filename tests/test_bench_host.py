@@ -1,0 +1,40 @@
+"""Host-side logic of bench.py (no GPU): which peak a kernel is priced
+against, the GPU-count guard and the traffic table's format."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+
+
+def test_fp4_kernels_priced_against_the_fp4_peak():
+    assert bench.kernel_peak("conv_halo<4, 2, 4, false, 4, true, true>") == bench.PEAK_FP4_TFLOPS
+    assert bench.kernel_peak("conv_halo<2, 4, 4, true, 4, true, true>") == bench.PEAK_FP4_TFLOPS
+    assert bench.kernel_peak("conv_halo<8, 1, 6, false, 4, false, true>") == bench.PEAK_FP4_TFLOPS
+    for int8 in ("conv_halo<8, 1, 6, false, 2, false, false>",
+                 "conv_halo<8, 1, 6, true, 4, true, false>",
+                 "conv_mfma<2, 1, 4, 1, 4, 1, 6>", "conv_small8<1>", "conv_igemm<32, 128, 1, 1>"):
+        assert bench.kernel_peak(int8) == bench.PEAK_INT8_TOPS
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_traffic_table_lines_parse():
+    path = os.path.join(ROOT, "profiles", "traffic.txt")
+    n = 0
+    for line in open(path):
+        if line.startswith("#") or not line.strip():
+            continue
+        parts = dict(kv.split("=", 1) for kv in line.split())
+        assert set(parts) == {"kernel", "workload", "src", "bytes_per_launch"}
+        assert float(parts["bytes_per_launch"]) > 0 and len(parts["src"]) == 16
+        n += 1
+    assert n > 0
