@@ -191,6 +191,14 @@ typedef struct ifq_join_params {
  *             written by ifq_fold_join_table with x_bits = 2 (the shortcut
  *             codes are 2-bit; NULL for CONV)
  *   n_q       number of quantizer thresholds, 2^out_bits - 1
+ *   sc_bits   IFQ_JOIN_IDENTITY: bit width of the shortcut codes, 0 meaning
+ *             2. Only 2-bit shortcut codes are supported (the table holds 4
+ *             shortcut levels and the kernels read 2 bits per code): any
+ *             other width returns IFQ_ERR_UNSUPPORTED. With an I8_NHWC
+ *             shortcut every code must be below 4; larger values are not
+ *             detected on the device. In a stack, a shortcut slot written
+ *             by a layer whose out_bits is not 2 is rejected the same way.
+ *             Ignored for the other kinds.
  *   q_thr     the quantizer thresholds of Eq. (3), strictly increasing
  *   down_w, down
  *             IFQ_JOIN_CONV_FUSED only (else ignored): the downsample conv's
@@ -209,7 +217,7 @@ typedef struct ifq_join {
   const double* coef;
   const int32_t* table;
   int32_t n_q;
-  int32_t reserved;
+  int32_t sc_bits;
   double q_thr[IFQ_MAX_THRESHOLDS];
   const void* down_w;
   ifq_conv_desc down;
@@ -325,7 +333,7 @@ IFQ_API ifq_status ifq_fold_thresholds(const ifq_fold_params* p,
                                        int32_t* thr_out);
 
 /*
- * Compact thresholds of a uniform quantizer (Sec. 3.3, Eq. 8): with
+ * Compact thresholds of a uniform quantizer (Sec. 3.2, Eq. 8): with
  * q_i = i*base + offset for i = 1 .. 2^out_bits - 1, the moved thresholds of
  * a channel are t_i = i*base' + offset', so one record per channel serves
  * every bit width. In fp64, in exactly this order (sd = sqrt(var + eps),

@@ -1,4 +1,4 @@
-"""Compact thresholds of a uniform quantizer (Sec. 3.3, Eq. 8). Test
+"""Compact thresholds of a uniform quantizer (Sec. 3.2, Eq. 8). Test
 infrastructure, host only.
 
 For thresholds q_i = i*base + offset (i = 1 .. 2^k - 1), moving the quantizer

@@ -70,7 +70,7 @@ class JoinParams(ctypes.Structure):
 
 class Join(ctypes.Structure):
     _fields_ = [("kind", i32), ("layout", i32), ("shortcut", vp), ("coef", vp),
-                ("table", vp), ("n_q", i32), ("reserved", i32),
+                ("table", vp), ("n_q", i32), ("sc_bits", i32),
                 ("q_thr", f64 * IFQ_MAX_THRESHOLDS), ("down_w", vp),
                 ("down", ConvDesc)]
 

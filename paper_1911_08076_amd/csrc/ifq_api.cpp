@@ -195,6 +195,9 @@ ifq_status check_join(const ifq_join* j, const ifq_conv_desc* d) {
   }
   if (j->kind == IFQ_JOIN_IDENTITY && !j->table)
     return fail(IFQ_ERR_INVALID_ARGUMENT, "join: identity join needs table");
+  if (j->kind == IFQ_JOIN_IDENTITY && j->sc_bits != 0 && j->sc_bits != 2)
+    return fail(IFQ_ERR_UNSUPPORTED,
+                "join: identity shortcut codes must be 2-bit (sc_bits %d)", j->sc_bits);
   if (j->kind == IFQ_JOIN_CONV && j->layout != IFQ_LAYOUT_I32_NHWC)
     return fail(IFQ_ERR_INVALID_ARGUMENT, "join: conv shortcut must be I32_NHWC");
   if (j->kind == IFQ_JOIN_IDENTITY) {
@@ -991,6 +994,29 @@ int64_t layer_in_bytes(const ifq_layer& L) {
   return tensor_bytes(L.pool.n, L.pool.h, L.pool.w, L.pool.c, L.pool.layout);
 }
 
+// Bytes the join of a conv layer reads from its join_src slot: the block
+// input codes [n][ho][wo][c_out] (identity), the downsample's int32 sums
+// (conv) or the downsample's input codes (fused downsample); 0 without a join.
+int64_t join_in_bytes(const ifq_layer& L) {
+  if (L.kind != IFQ_LAYER_CONV && L.kind != IFQ_LAYER_CONV_FP4) return 0;
+  const ifq_join& j = L.join;
+  const int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);
+  const int64_t wo = out_extent(L.conv.w, L.conv.kw, L.conv.stride, L.conv.pad);
+  switch (j.kind) {
+    case IFQ_JOIN_IDENTITY: return tensor_bytes(L.conv.n, ho, wo, L.conv.c_out, j.layout);
+    case IFQ_JOIN_CONV:
+      return tensor_bytes(L.conv.n, ho, wo, L.conv.c_out, IFQ_LAYOUT_I32_NHWC);
+    case IFQ_JOIN_CONV_FUSED:
+      return tensor_bytes(j.down.n, j.down.h, j.down.w, j.down.c_in, j.down.in_layout);
+    default: return 0;
+  }
+}
+
+// Code width a layer writes into its dst slot (0: int32 sums).
+int layer_out_bits(const ifq_layer& L) {
+  return L.kind == IFQ_LAYER_POOL ? L.pool.bits : L.conv.out_bits;
+}
+
 ifq_status plan_stack(const ifq_stack* s, SlotPlan* plan) {
   if (!s) return fail(IFQ_ERR_INVALID_ARGUMENT, "stack is NULL");
   if (s->n_layers < 0 || (s->n_layers > 0 && !s->layers))
@@ -1000,6 +1026,10 @@ ifq_status plan_stack(const ifq_stack* s, SlotPlan* plan) {
   plan->bytes.assign(s->n_slots, 0);
   std::vector<char> written(s->n_slots, 0);
   written[0] = 1;
+  // bytes and code width of the last write of each slot (the caller's x
+  // and y have no size known here; their bits are unknown, -1)
+  std::vector<int64_t> last_bytes(s->n_slots, 0);
+  std::vector<int> last_bits(s->n_slots, -1);
   for (int i = 0; i < s->n_layers; ++i) {
     const ifq_layer& L = s->layers[i];
     ifq_status st;
@@ -1061,12 +1091,28 @@ ifq_status plan_stack(const ifq_stack* s, SlotPlan* plan) {
                   i, L.src);
     if (L.dst < 1 || L.dst >= s->n_slots || L.dst == L.src)
       return fail(IFQ_ERR_INVALID_ARGUMENT, "layer %d: bad dst slot %d", i, L.dst);
-    if (L.src >= 2 && layer_in_bytes(L) > plan->bytes[L.src])
+    if (L.src >= 2 && layer_in_bytes(L) > last_bytes[L.src])
       return fail(IFQ_ERR_INVALID_ARGUMENT,
                   "layer %d: reads %lld bytes from slot %d holding %lld", i,
-                  (long long)layer_in_bytes(L), L.src, (long long)plan->bytes[L.src]);
+                  (long long)layer_in_bytes(L), L.src, (long long)last_bytes[L.src]);
+    const bool joins = (L.kind == IFQ_LAYER_CONV || L.kind == IFQ_LAYER_CONV_FP4) &&
+                       L.join.kind != IFQ_JOIN_NONE;
+    if (joins) {
+      const int64_t jb = join_in_bytes(L);
+      if (jb < 0 || (L.join_src >= 2 && jb > last_bytes[L.join_src]))
+        return fail(IFQ_ERR_INVALID_ARGUMENT,
+                    "layer %d: the join reads %lld bytes from slot %d holding %lld", i,
+                    (long long)jb, L.join_src, (long long)last_bytes[L.join_src]);
+      if (L.join.kind == IFQ_JOIN_IDENTITY && last_bits[L.join_src] >= 0 &&
+          last_bits[L.join_src] != 2)
+        return fail(IFQ_ERR_UNSUPPORTED,
+                    "layer %d: identity shortcut slot %d holds %d-bit codes (2-bit only)", i,
+                    L.join_src, last_bits[L.join_src]);
+    }
     const int64_t ob = layer_out_bytes(L);
     if (ob > plan->bytes[L.dst]) plan->bytes[L.dst] = ob;
+    last_bytes[L.dst] = ob;
+    last_bits[L.dst] = layer_out_bits(L);
     written[L.dst] = 1;
   }
   int64_t off = 0;

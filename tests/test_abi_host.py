@@ -635,6 +635,59 @@ def test_stack_rejects_bad_layer_kind_and_slots():
                              None) == EINVAL
 
 
+def test_identity_join_needs_2bit_shortcut_codes():
+    # the identity join's table has 4 shortcut levels and the kernels read 2
+    # bits per shortcut code: wider shortcut codes are refused, not misread
+    d = P.conv_desc(1, 8, 8, 64, 64, 3, 1, 1, 2, 2)
+    table = np.zeros((64, 4, 4), dtype=np.int32)
+    for sc_bits, want in ((0, None), (2, None), (1, EUNSUP), (3, EUNSUP), (4, EUNSUP),
+                          (8, EUNSUP)):
+        j = P.make_join(P.IFQ_JOIN_IDENTITY, I8, None, None, [0.25, 0.75, 1.25], table=table)
+        j.shortcut = 0x1000
+        j.sc_bits = sc_bits
+        name = P.ifq_conv_kernel_name(d, j)
+        st = status_of("ifq_conv_forward", ctypes.byref(P.conv_desc(0, 8, 8, 64, 64, 3, 1, 1,
+                                                                    2, 2)),
+                       FAKE, FAKE, None, ctypes.byref(j), FAKE, None, None, 0, None)
+        if want is None:
+            assert st == 0 and name
+        else:
+            assert st == want, sc_bits
+
+
+def test_stack_rejects_a_join_slot_smaller_than_the_join_reads():
+    # s2 holds a 4x4 map (a stride-2 conv's output); the identity join of the
+    # last layer reads an 8x8 map of the same channels from it
+    layers = [Conv("a", "x", "s2", 8, 8, 64, 64, 3, 2, 1, 2, 2),
+              Conv("b", "x", "s3", 8, 8, 64, 64, 3, 1, 1, 2, 2),
+              Conv("c", "s3", "y", 8, 8, 64, 64, 3, 1, 1, 2, 2, ("identity", "s2"))]
+    st, slots = make_stack(layers, 2)
+    lib = _ffi.load()
+    assert P.ifq_stack_workspace_bytes(st) == 0
+    assert lib.ifq_run_stack(ctypes.byref(st), FAKE, FAKE, FAKE, 1 << 30, None) == EINVAL
+    assert "join reads" in P.ifq_last_error()
+    # the same stack with the join on the 8x8 map plans
+    layers[2] = Conv("c", "s3", "y", 8, 8, 64, 64, 3, 1, 1, 2, 2, ("identity", "s3"))
+    st, slots = make_stack(layers[1:], 2)
+    assert P.ifq_stack_workspace_bytes(st) > 0
+
+
+def test_stack_rejects_identity_shortcut_of_wider_codes():
+    # s2 holds 3-bit codes (byte per code); an identity join reading it would
+    # see only their low 2 bits, so the stack is refused
+    def layers(bits):
+        return [Conv("a", "x", "s2", 8, 8, 64, 64, 3, 1, 1, 2, bits),
+                Conv("b", "s2", "s3", 8, 8, 64, 64, 3, 1, 1, bits, 2),
+                Conv("c", "s3", "y", 8, 8, 64, 64, 3, 1, 1, 2, 2, ("identity", "s2"))]
+    lib = _ffi.load()
+    st, _ = make_stack(layers(2), 2)
+    assert P.ifq_stack_workspace_bytes(st) > 0
+    st, _ = make_stack(layers(3), 2)
+    assert P.ifq_stack_workspace_bytes(st) == 0
+    assert lib.ifq_run_stack(ctypes.byref(st), FAKE, FAKE, FAKE, 1 << 30, None) == EUNSUP
+    assert "2-bit only" in P.ifq_last_error()
+
+
 @pytest.mark.parametrize("bits", [2, 3, 4])
 def test_compact_fold_matches_oracle(bits):
     # the library's host fold of the compact records (Eq. 8) and the

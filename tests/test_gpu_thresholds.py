@@ -1,4 +1,4 @@
-"""GPU parity of the compact thresholds (Sec. 3.3, Eq. 8): records expanded
+"""GPU parity of the compact thresholds (Sec. 3.2, Eq. 8): records expanded
 on the device equal the oracle's expansion, and a conv that reads them gives
 the oracle's codes, for 2-, 3- and 4-bit outputs (the 2-bit case on the
 windowed kernel, BLOCK64 codes; the others on the generic path)."""

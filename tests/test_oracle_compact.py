@@ -1,4 +1,4 @@
-"""Pins of the compact thresholds (Sec. 3.3, Eq. 8): a hand-worked channel
+"""Pins of the compact thresholds (Sec. 3.2, Eq. 8): a hand-worked channel
 for each sign of gamma and for gamma = 0, exact agreement with the table fold
 where the arithmetic is exact, the true floor of the exact rational t_i away
 from integers, and the float chain's codes on seeded k-bit layers."""

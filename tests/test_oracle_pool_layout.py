@@ -95,3 +95,45 @@ def test_alexnet_parameter_count_supports_dense_convs():
     shapes = [(L.cout, L.cin, L.k) for L in convs]
     want = [(L["cout"], L["cin"], L["k"]) for L in g["layers"][1:5]]
     assert shapes == want
+
+
+@pytest.mark.parametrize("shape", [(2, 3, 5, 128), (1, 4, 2, 64), (3, 2, 3, 192)])
+def test_pack_block64_places_every_code_by_the_layout_formula(shape):
+    # IFQ_LAYOUT_U2_BLOCK64 (the k-bit feature maps of Table 4 at 2 bits,
+    # regrouped in 64-channel blocks): code (n, y, x, c) sits in byte
+    # (((n*C/64 + c/64)*H + y)*W + x)*16 + (c%64)/4, bits 2*(c%4) .. +1.
+    # Every position is checked from that formula with explicit loops, on
+    # codes that differ between any two axes, so a swapped axis of the
+    # packer's transpose fails.
+    n, h, w, c = shape
+    idx = np.indices(shape)
+    codes = ((idx[0] * 7 + idx[1] * 5 + idx[2] * 3 + idx[3] + idx[3] // 64) % 4).astype(np.uint8)
+    flat = layout.pack_block64(codes).reshape(-1)
+    assert flat.size == n * h * w * c // 4
+    for ni in range(n):
+        for y in range(h):
+            for x in range(w):
+                for ch in range(c):
+                    byte = (((ni * (c // 64) + ch // 64) * h + y) * w + x) * 16 + (ch % 64) // 4
+                    got = (int(flat[byte]) >> (2 * (ch % 4))) & 3
+                    assert got == codes[ni, y, x, ch], (ni, y, x, ch)
+
+
+def test_pack_block64_one_hot_cells():
+    # a single nonzero code lands in exactly one byte, at the formula's place
+    n, h, w, c = 2, 3, 4, 128
+    for (ni, y, x, ch) in [(0, 0, 0, 0), (1, 2, 3, 127), (0, 1, 2, 64), (1, 0, 3, 5),
+                           (0, 2, 0, 70)]:
+        codes = np.zeros((n, h, w, c), np.uint8)
+        codes[ni, y, x, ch] = 2
+        flat = layout.pack_block64(codes).reshape(-1)
+        byte = (((ni * (c // 64) + ch // 64) * h + y) * w + x) * 16 + (ch % 64) // 4
+        assert np.flatnonzero(flat).tolist() == [byte]
+        assert flat[byte] == 2 << (2 * (ch % 4))
+
+
+def test_block64_round_trip(rng):
+    codes = rng.integers(0, 4, size=(2, 3, 5, 192), dtype=np.uint8)
+    packed = layout.pack_block64(codes)
+    assert packed.shape == (2, 3, 3, 5, 16)
+    assert np.array_equal(layout.unpack_block64(packed, 192), codes)
