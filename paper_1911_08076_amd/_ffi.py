@@ -7,9 +7,8 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-# IFQ_LIBRARY may point at another build of the same library (e.g. an
-# instrumented one); by default the in-tree build next to this file is used.
-LIB_PATH = os.environ.get("IFQ_LIBRARY", os.path.join(HERE, "libifq.so"))
+# always the in-tree build next to this file
+LIB_PATH = os.path.join(HERE, "libifq.so")
 
 IFQ_OK = 0
 IFQ_ERR_INVALID_ARGUMENT = -1
