@@ -559,6 +559,27 @@ IFQ_API ifq_status ifq_run_stack(const ifq_stack* s, const void* x, void* y,
                                  void* ws, size_t ws_bytes,
                                  hipStream_t stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): ifq_run_stack
+ * with the work slots in a workspace of ifq_static_workspace_bytes() bytes
+ * (64 MiB) that the library keeps in a device array, one per GPU, for the
+ * life of the process. The caller still passes x and y (device pointers, as
+ * for ifq_run_stack). Calls nothing that allocates or frees device memory.
+ * Every call on one GPU shares that GPU's array and leaves the last call's
+ * slot contents in it (nothing in it needs clearing: every slot is written
+ * before it is read), so calls that overlap on one GPU (two streams, two
+ * threads) race and must be serialised by the caller. Errors: as
+ * ifq_run_stack, INSUFFICIENT_BUFFER when ifq_stack_workspace_bytes(s)
+ * exceeds the static workspace (nothing is launched), HIP_ERROR when the
+ * array's device address cannot be looked up on the current device.
+ */
+IFQ_API ifq_status ifq_run_stack_static(const ifq_stack* s, const void* x, void* y,
+                                        hipStream_t stream);
+
+/* Bytes of the static workspace of ifq_run_stack_static. Host. */
+IFQ_API size_t ifq_static_workspace_bytes(void);
+
 #ifdef __cplusplus
 }
 #endif

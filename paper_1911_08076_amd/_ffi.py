@@ -129,6 +129,8 @@ SIGNATURES = [
     ("ifq_stack_slot_info", i32, [ctypes.POINTER(Stack), i32,
                                   ctypes.POINTER(size_t), ctypes.POINTER(size_t)]),
     ("ifq_run_stack", i32, [ctypes.POINTER(Stack), vp, vp, vp, size_t, vp]),
+    ("ifq_run_stack_static", i32, [ctypes.POINTER(Stack), vp, vp, vp]),
+    ("ifq_static_workspace_bytes", size_t, []),
 ]
 
 _lib = None

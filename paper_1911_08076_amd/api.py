@@ -293,3 +293,12 @@ def ifq_run_stack(stack, x, y, ws, stream=None):
     _check(_lib().ifq_run_stack(ctypes.byref(stack), _ptr(x), _ptr(y),
                                 _ptr(ws), ws_bytes, _stream(stream)),
            "ifq_run_stack")
+
+
+def ifq_run_stack_static(stack, x, y, stream=None):
+    _check(_lib().ifq_run_stack_static(ctypes.byref(stack), _ptr(x), _ptr(y), _stream(stream)),
+           "ifq_run_stack_static")
+
+
+def ifq_static_workspace_bytes():
+    return int(_lib().ifq_static_workspace_bytes())

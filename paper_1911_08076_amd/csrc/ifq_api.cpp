@@ -33,6 +33,17 @@ ifq_status ok() {
   return IFQ_OK;
 }
 
+}  // namespace
+
+namespace ifq {
+ifq_status set_error(ifq_status st, const char* msg) {
+  g_last_error = msg;
+  return st;
+}
+}  // namespace ifq
+
+namespace {
+
 constexpr int64_t kMaxIndex = (int64_t)1 << 31;  // byte offsets kept below 2^31
 
 bool is_finite(double v) { return std::isfinite(v); }

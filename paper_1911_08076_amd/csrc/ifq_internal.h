@@ -188,6 +188,9 @@ hipError_t launch_pool(const PoolLaunch& a, hipStream_t stream);
 hipError_t launch_expand_thresholds(const ifq_thr_compact* recs, int c_out, int out_bits,
                                     double bound, int32_t* thr, hipStream_t stream);
 
+// Sets the thread's last-error text (ifq_last_error) and returns st.
+ifq_status set_error(ifq_status st, const char* msg);
+
 hipError_t launch_convert(int64_t n, int64_t hw, int32_t c, int32_t src_layout,
                           int32_t dst_layout, const void* src, void* dst,
                           hipStream_t stream);

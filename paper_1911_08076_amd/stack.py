@@ -498,6 +498,12 @@ class DeviceStack:
         launch.keep = (desc, join if rec.kind != IFQ_LAYER_POOL else None)
         return launch
 
+    def run_static(self, x, y, stream=None):
+        """One forward pass on the library's static workspace
+        (ifq_run_stack_static) instead of self.ws."""
+        self.stack.events = None
+        api.ifq_run_stack_static(self.stack, x, y, stream)
+
     def run(self, x, y, stream=None, events=None):
         """One forward pass (asynchronous on stream). events: optional ctypes
         array of n_layers + 1 hipEvent_t handles for per-layer timing."""

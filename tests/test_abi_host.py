@@ -755,3 +755,16 @@ def test_new_entry_points_accept_an_empty_batch():
     bad = _ffi.PoolDesc(0, 27, 28, 128, 2, 2, 0, 2, B64)
     assert status_of("ifq_conv_pool_forward", ctypes.byref(d), ctypes.byref(bad), None, None,
                      FAKE, None, None) == EINVAL
+
+
+def test_run_stack_static_host_side():
+    # the static-workspace driver validates before touching the GPU: a NULL
+    # stack and a stack needing more than the static workspace are refused
+    lib = _ffi.load()
+    cap = P.ifq_static_workspace_bytes()
+    assert cap == 64 << 20
+    assert lib.ifq_run_stack_static(None, FAKE, FAKE, None) == EINVAL
+    st, _ = make_stack(list(get_stack(3).layers), 64, "i8")
+    assert P.ifq_stack_workspace_bytes(st) > cap
+    assert lib.ifq_run_stack_static(ctypes.byref(st), FAKE, FAKE, None) == EBUF
+    assert "static workspace" in P.ifq_last_error()
