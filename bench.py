@@ -79,9 +79,14 @@ class Hip:
 
 def kernel_peak(name):
     """Dense peak of the matrix instructions a kernel runs on: the fp4
-    instances of the windowed kernel (its last template argument, the fp4
-    flag, true) against MXFP4, the others against int8."""
-    fp4 = name.startswith("conv_halo<") and name.endswith(", true>")
+    instances (the windowed kernel's last template argument, the fp4 flag,
+    true; the register-blocked kernel's ninth) against MXFP4, the others
+    against int8."""
+    fp4 = False
+    if name.startswith("conv_halo<"):
+        fp4 = name.endswith(", true>")
+    elif name.startswith("conv_w2<"):
+        fp4 = name[len("conv_w2<"):-1].split(", ")[8] == "true"
     return PEAK_FP4_TFLOPS if fp4 else PEAK_INT8_TOPS
 
 

@@ -415,6 +415,34 @@ IFQ_API ifq_status ifq_fold_join_table(const ifq_join_params* p, int32_t in_bits
  */
 IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d, const ifq_join* join);
 
+/*
+ * Kernel variants of the register-blocked 3x3 conv kernel, for autotuning
+ * and per-variant parity tests (the same contraction, Eq. 1, and the same
+ * epilogues as ifq_conv_forward). The kernel takes 3x3 pad-1 convs of
+ * stride 1 or 2 on 2-bit BLOCK64 codes with c_in % 64 == 0, 2-bit output
+ * (U2 or BLOCK64, c_out % 32 == 0, 27 * c_in <= 32766), no pool, and either
+ * thresholds or an identity join with a 2-bit shortcut.
+ *   ifq_conv_variant_count   number of variants (host)
+ *   ifq_conv_variant_name    the kernel variant `variant` would launch for
+ *                            d and join (join nullable; no pointer in it is
+ *                            dereferenced), or "" if it cannot take the
+ *                            layer or d has no pixels (host)
+ *   ifq_conv_forward_variant ifq_conv_forward (same arguments, no
+ *                            workspace) on that variant, asynchronous on
+ *                            stream; IFQ_ERR_UNSUPPORTED where it cannot
+ *                            take the layer. Errors as ifq_conv_forward.
+ * Variants whose name has the fp4 flag (the ninth template argument) true
+ * compute the sums exactly on the fp4 scaled MFMA, as ifq_conv_forward_fp4:
+ * their w_packed is the ifq_pack_weights_fp4 blob.
+ */
+IFQ_API int32_t ifq_conv_variant_count(void);
+IFQ_API const char* ifq_conv_variant_name(const ifq_conv_desc* d, const ifq_join* join,
+                                          int32_t variant);
+IFQ_API ifq_status ifq_conv_forward_variant(const ifq_conv_desc* d, const void* x,
+                                            const void* w_packed, const int32_t* thr,
+                                            const ifq_join* join, void* y, int32_t* acc_dump,
+                                            int32_t variant, hipStream_t stream);
+
 /* Device workspace bytes ifq_conv_forward needs for d (may be 0). Host. */
 IFQ_API size_t ifq_conv_workspace_bytes(const ifq_conv_desc* d);
 

@@ -302,3 +302,21 @@ def ifq_run_stack_static(stack, x, y, stream=None):
 
 def ifq_static_workspace_bytes():
     return int(_lib().ifq_static_workspace_bytes())
+
+
+def ifq_conv_variant_count():
+    return int(_lib().ifq_conv_variant_count())
+
+
+def ifq_conv_variant_name(desc, join, variant):
+    return _lib().ifq_conv_variant_name(
+        ctypes.byref(desc), ctypes.byref(join) if join is not None else None,
+        int(variant)).decode()
+
+
+def ifq_conv_forward_variant(desc, x, w_packed, thr, y, variant, join=None, acc_dump=None,
+                             stream=None):
+    _check(_lib().ifq_conv_forward_variant(
+        ctypes.byref(desc), _ptr(x), _ptr(w_packed), _ptr(thr),
+        ctypes.byref(join) if join is not None else None, _ptr(y), _ptr(acc_dump),
+        int(variant), _stream(stream)), "ifq_conv_forward_variant")

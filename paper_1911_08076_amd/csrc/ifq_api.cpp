@@ -756,6 +756,45 @@ IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d, const ifq_join*
   return ifq::conv_kernel_name(a);
 }
 
+IFQ_API int32_t ifq_conv_variant_count(void) { return ifq::w2_variant_count(); }
+
+IFQ_API const char* ifq_conv_variant_name(const ifq_conv_desc* d, const ifq_join* join,
+                                          int32_t variant) {
+  int64_t ho, wo;
+  if (check_conv(d, &ho, &wo) != IFQ_OK) return "";
+  ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, join, nullptr,
+                                  nullptr, nullptr);
+  a.f4 = ifq::w2_variant_fp4(variant) ? 1 : 0;
+  ifq::W2Plan p;
+  if (variant < 0 || !ifq::plan_w2(a, variant, &p)) return "";
+  return ifq::conv_w2_name(p, a);
+}
+
+IFQ_API ifq_status ifq_conv_forward_variant(const ifq_conv_desc* d, const void* x,
+                                            const void* w_packed, const int32_t* thr,
+                                            const ifq_join* join, void* y, int32_t* acc_dump,
+                                            int32_t variant, hipStream_t stream) {
+  int64_t ho, wo;
+  ifq_status st = check_conv(d, &ho, &wo);
+  if (st != IFQ_OK) return st;
+  const void* sc = (join && join->kind != IFQ_JOIN_NONE) ? join->shortcut : nullptr;
+  st = conv_args_check(d, x, w_packed, thr, join, sc, y);
+  if (st != IFQ_OK) return st;
+  if (d->n == 0) return ok();
+  ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_packed, thr, join, sc, y, acc_dump);
+  if (ifq::w2_variant_fp4(variant)) {   // w_packed is the fp4 blob
+    a.f4 = 1;
+    a.rowsum = nullptr;
+    a.wzero = fp4_zero_off(ifq::weight_geom(*d));
+  }
+  ifq::W2Plan p;
+  if (variant < 0 || !ifq::plan_w2(a, variant, &p))
+    return fail(IFQ_ERR_UNSUPPORTED, "conv variant %d: cannot take this layer", variant);
+  st = hip_status(ifq::launch_conv_w2(a, p, stream), "conv variant launch");
+  if (st != IFQ_OK) return st;
+  return ok();
+}
+
 IFQ_API size_t ifq_conv_workspace_bytes(const ifq_conv_desc* d) {
   (void)d;
   return 0;
@@ -830,6 +869,10 @@ IFQ_API const char* ifq_conv_fp4_kernel_name(const ifq_conv_desc* d, const ifq_j
   if (check_conv(d, &ho, &wo) != IFQ_OK) return "";
   ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, join, nullptr,
                                   nullptr, nullptr);
+  a.f4 = 1;
+  ifq::W2Plan wp;
+  if (ifq::plan_w2(a, -1, &wp)) return ifq::conv_w2_name(wp, a);
+  a.f4 = 0;
   ifq::HaloPlan hp;
   if (!fp4_plan(a, &hp)) return "";
   a.f4 = 1;
@@ -847,6 +890,20 @@ IFQ_API ifq_status ifq_conv_forward_fp4(const ifq_conv_desc* d, const void* x,
   if (st != IFQ_OK) return st;
   ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_fp4, thr, join, sc, y, nullptr);
   if (d->n == 0) return ok();
+  // the register-blocked kernel's fp4 instances where they take the layer
+  // (thresholds or an identity join), else the windowed kernel's
+  ifq::W2Plan wp;
+  {
+    ifq::ConvLaunch f = a;
+    f.f4 = 1;
+    if (ifq::plan_w2(f, -1, &wp)) {
+      f.rowsum = nullptr;
+      f.wzero = fp4_zero_off(ifq::weight_geom(*d));
+      st = hip_status(ifq::launch_conv_w2(f, wp, stream), "conv fp4 launch");
+      if (st != IFQ_OK) return st;
+      return ok();
+    }
+  }
   ifq::HaloPlan hp;
   if (!fp4_plan(a, &hp))
     return fail(IFQ_ERR_UNSUPPORTED, "conv fp4: no fp4 kernel covers this layer");

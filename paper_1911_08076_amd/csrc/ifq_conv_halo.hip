@@ -635,8 +635,8 @@ __global__ __launch_bounds__(512, FM == 2 ? 4 : 2) void conv_halo(ConvLaunch a) 
 // ---------------------------------------------------------------------------
 struct HaloVariant {
   int wn, wk, d, fm;   // waves along pixels, K groups, ring stages, row blocks per wave
-  double c0_us;        // fixed cost of one round of workgroups
-  double eff;          // MFMA efficiency of the main loop
+  double c0_us;        // fixed cost per round of workgroups on a CU (plan_time)
+  double eff;          // MFMA efficiency of a tile's main loop (plan_time)
   const char* name;    // the kernels as a profiler lists them: unfused,
   const char* sw_name;       // unfused on the transposed layout,
   const char* fused_name;    // fused downsample (transposed layout),
@@ -647,22 +647,23 @@ struct HaloVariant {
 
 // Index order must match the switch in launch_conv_halo. Variants with
 // fm = 2 (64 output channels) run two workgroups per CU.
+// (c0_us, eff) fitted to measured MI355X kernel times (ResNet-18, AlexNet,
+// VGG-16, Tiny-YOLOv2 layer shapes).
 const HaloVariant kHaloVariants[] = {
-    {8, 1, 6, 4, 4.0, 0.75, "conv_halo<8, 1, 6, false, 4, false, false>", "conv_halo<8, 1, 6, false, 4, true, false>",
+    {8, 1, 6, 4, 4.0, 0.55, "conv_halo<8, 1, 6, false, 4, false, false>", "conv_halo<8, 1, 6, false, 4, true, false>",
      "conv_halo<8, 1, 6, true, 4, true, false>", "conv_halo<8, 1, 6, false, 4, true, true>",
      "conv_halo<8, 1, 6, false, 4, false, true>", "conv_halo<8, 1, 6, true, 4, true, true>"},
-    {4, 2, 4, 4, 4.0, 0.75, "conv_halo<4, 2, 4, false, 4, false, false>", "conv_halo<4, 2, 4, false, 4, true, false>",
+    {4, 2, 4, 4, 3.5, 0.55, "conv_halo<4, 2, 4, false, 4, false, false>", "conv_halo<4, 2, 4, false, 4, true, false>",
      "conv_halo<4, 2, 4, true, 4, true, false>", "conv_halo<4, 2, 4, false, 4, true, true>",
      "conv_halo<4, 2, 4, false, 4, false, true>", "conv_halo<4, 2, 4, true, 4, true, true>"},
-    {2, 4, 4, 4, 4.0, 0.75, "conv_halo<2, 4, 4, false, 4, false, false>", "conv_halo<2, 4, 4, false, 4, true, false>",
+    {2, 4, 4, 4, 5.7, 0.55, "conv_halo<2, 4, 4, false, 4, false, false>", "conv_halo<2, 4, 4, false, 4, true, false>",
      "conv_halo<2, 4, 4, true, 4, true, false>", "conv_halo<2, 4, 4, false, 4, true, true>",
      "conv_halo<2, 4, 4, false, 4, false, true>", "conv_halo<2, 4, 4, true, 4, true, true>"},
-    {8, 1, 6, 2, 4.0, 0.75, "conv_halo<8, 1, 6, false, 2, false, false>", "conv_halo<8, 1, 6, false, 2, true, false>",
+    {8, 1, 6, 2, 2.0, 0.33, "conv_halo<8, 1, 6, false, 2, false, false>", "conv_halo<8, 1, 6, false, 2, true, false>",
      nullptr, nullptr, nullptr, nullptr},   // 64 x 256
 };
 constexpr int kNumHalo = sizeof(kHaloVariants) / sizeof(kHaloVariants[0]);
 constexpr int kNumCUs = 256;
-constexpr double kCuOpsPerUs = 2.4e3 * 8192;
 
 // Upper bound of the halo cells (rounded per image to 64) one tile of bn
 // output pixels needs per channel block, over every tile of the layer.
@@ -731,9 +732,7 @@ bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
     if (V.wk * (cells / 64) > kHaloNW * nr) continue;
     const int64_t blocks = nco * ((a.m + bn - 1) / bn);
     // occ workgroups share a CU: each runs at 1/occ of its MFMA rate
-    const double tile_ops = 2.0 * bm * bnmax * (double)a.kpad;
-    const double t = (double)((blocks + slots - 1) / slots) *
-                     (V.c0_us + tile_ops * occ / (kCuOpsPerUs * V.eff));
+    const double t = plan_time(blocks, 2.0 * bm * bnmax * (double)a.kpad, occ, V.c0_us, V.eff);
     if (t < best_t) {
       best_t = t;
       *out = HaloPlan{v, (int)bn, (int)((a.m + bn - 1) / bn), t};

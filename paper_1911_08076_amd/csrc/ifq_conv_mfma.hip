@@ -319,8 +319,6 @@ const Variant kVariants[] = {
 };
 constexpr int kNumVariants = sizeof(kVariants) / sizeof(kVariants[0]);
 constexpr int kNumCUs = 256;
-// dense int8 MFMA ops per microsecond of one CU (2.4 GHz x 8192 per clock)
-constexpr double kCuOpsPerUs = 2.4e3 * 8192;
 
 struct Plan {
   int variant;
@@ -349,9 +347,7 @@ Plan plan_mfma(const ConvLaunch& a) {
     bn = (bn + 31) / 32 * 32;
     if (bn > bnmax) bn = bnmax;
     const int64_t blocks = nco * ((a.m + bn - 1) / bn);
-    const double tile_ops = 2.0 * bm * bnmax * (double)a.kpad;
-    const double t = (double)((blocks + kNumCUs - 1) / kNumCUs) *
-                     (V.c0_us + tile_ops / (kCuOpsPerUs * V.eff));
+    const double t = plan_time(blocks, 2.0 * bm * bnmax * (double)a.kpad, 1, V.c0_us, V.eff);
     if (t < best_t - 1e-9) {
       best_t = t;
       best = Plan{v, (int)bn, (int)((a.m + bn - 1) / bn), t};
@@ -378,11 +374,18 @@ bool mfma_eligible(const ConvLaunch& a) {
 
 // A fused downsample join runs only in the windowed 3x3 kernel (the host
 // checks plan_halo succeeds before launching one).
+// The fast path picks the kernel with the lowest predicted time (plan_time)
+// among the register-blocked 3x3 kernel, the windowed 3x3 kernel and the
+// tiled kernel. A fused downsample join runs only in the windowed kernel
+// (the host checks plan_halo succeeds before launching one).
 const char* conv_mfma_name(const ConvLaunch& a) {
   HaloPlan hp;
   const bool halo = plan_halo(a, &hp);
   if (halo && a.join_kind == IFQ_JOIN_CONV_FUSED) return conv_halo_name(hp, a);
+  W2Plan wp;
+  const bool w2 = plan_w2(a, -1, &wp);
   const Plan pl = plan_mfma(a);
+  if (w2 && wp.t_us <= pl.t_us && (!halo || wp.t_us <= hp.t_us)) return conv_w2_name(wp, a);
   if (halo && hp.t_us < pl.t_us) return conv_halo_name(hp, a);
   return kVariants[pl.variant].name;
 }
@@ -392,7 +395,11 @@ hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream) {
   const bool halo = plan_halo(a, &hp);
   if (a.join_kind == IFQ_JOIN_CONV_FUSED)
     return halo ? launch_conv_halo(a, hp, stream) : hipErrorNotSupported;
+  W2Plan wp;
+  const bool w2 = plan_w2(a, -1, &wp);
   const Plan pl = plan_mfma(a);
+  if (w2 && wp.t_us <= pl.t_us && (!halo || wp.t_us <= hp.t_us))
+    return launch_conv_w2(a, wp, stream);
   if (halo && hp.t_us < pl.t_us) return launch_conv_halo(a, hp, stream);
   switch (pl.variant) {
     case 0: return launch_variant<2, 4, 1, 2, 4, 1, 6>(a, pl, stream);

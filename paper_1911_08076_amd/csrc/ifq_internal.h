@@ -128,6 +128,7 @@ struct ConvLaunch {
   int32_t pho, pwo;
   FastDiv div_pwo;     // division by pwo (pooled pixel -> pooled row)
   FastDiv div_pho;     // division by pho (pooled row -> image)
+  int32_t wcells;      // register-blocked 3x3 kernel: window cells per channel block
 };
 
 // Whether the pooled epilogue takes this launch: codes out (no join), and
@@ -151,6 +152,22 @@ bool mfma_eligible(const ConvLaunch& a);
 // 3x3 kernel with per-tile input windows in LDS (BLOCK64 input): the
 // variant, pixels per workgroup, workgroups along pixels and the predicted
 // time of the best variant that fits the layer, if any.
+// Predicted time (us) of a conv launch of `tiles` workgroup tiles of
+// tile_ops dense int8 ops each, occ of them sharing a CU: the launch, the
+// MFMA work of the busiest CU at a fitted efficiency eff, and a fitted fixed
+// cost c0_us per round of occ tiles on a CU (prologue latency, epilogue,
+// drain). One form for every kernel, so that the planners' predictions
+// compare.
+constexpr double kLaunchUs = 2.0;
+constexpr int kPlanCUs = 256;
+constexpr double kCuOpsPerUsInt8 = 2.4e3 * 8192;   // dense int8 ops per us of one CU
+inline double plan_time(int64_t tiles, double tile_ops, int occ, double c0_us, double eff) {
+  const int64_t per_cu = (tiles + kPlanCUs - 1) / kPlanCUs;
+  const int64_t rounds = (per_cu + occ - 1) / occ;
+  return kLaunchUs + (double)per_cu * tile_ops / (kCuOpsPerUsInt8 * eff) +
+         (double)rounds * c0_us;
+}
+
 struct HaloPlan {
   int variant;
   int bn;
@@ -166,6 +183,24 @@ inline bool fused_supported(const ConvLaunch& a) {
 hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream);
 const char* conv_halo_name(const HaloPlan& p, const ConvLaunch& a);
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream);
+
+// 3x3 kernel with register-blocked waves and every channel block's window
+// resident in LDS (BLOCK64 input, 2-bit threshold or identity-join
+// epilogue): the variant, pixels per workgroup, workgroups along pixels,
+// window cells per channel block and the predicted time. forced >= 0 plans
+// that variant only (false if it cannot take the layer).
+struct W2Plan {
+  int variant;
+  int bn;
+  int blocks_m;
+  int wcells;
+  double t_us;
+};
+int w2_variant_count();
+bool w2_variant_fp4(int v);   // variant v runs the fp4 contraction (fp4 weight blob)
+bool plan_w2(const ConvLaunch& a, int forced, W2Plan* out);
+hipError_t launch_conv_w2(ConvLaunch a, const W2Plan& p, hipStream_t stream);
+const char* conv_w2_name(const W2Plan& p, const ConvLaunch& a);
 
 // 8-bit input codes with c_in <= 4 (a detector's first layer): whether the
 // small-channel kernel takes the layer, its launch and its name.

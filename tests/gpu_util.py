@@ -51,20 +51,24 @@ def oracle_layer(L, x, p, shortcut=None, down=None):
 
 
 def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
-              sc_layout=I8, down=None, dump=True, fused_down=None):
+              sc_layout=I8, down=None, dump=True, fused_down=None, variant=None):
     """Run one conv through ifq_conv_forward; returns (acc or None, output).
 
     output is uint8 codes NHWC (packed [..., c/4] for U2, [n][c/64][h][w][16]
     for B64) or int32 sums. fused_down = (D, xin): a conv join whose 1x1
     downsample layer D (params down) runs inside the kernel on the BLOCK64
-    codes xin (IFQ_JOIN_CONV_FUSED) instead of reading its sums."""
+    codes xin (IFQ_JOIN_CONV_FUSED) instead of reading its sums. variant:
+    run that variant of the register-blocked 3x3 kernel
+    (ifq_conv_forward_variant) instead of the kernel ifq_conv_forward picks."""
     import torch
     if out_layout is None:
         out_layout = I32 if L.out_bits == 0 else I8
     d = P.conv_desc(n, L.h, L.w, L.cin, L.cout, L.k, L.stride, L.pad,
                     L.in_bits, L.out_bits, in_layout, out_layout)
     ho, wo = P.ifq_conv_output_dims(d)
-    blob = P.ifq_pack_weights(d, p["w"])
+    fp4 = variant is not None and \
+        P.ifq_conv_variant_name(d, None, variant)[len("conv_w2<"):-1].split(", ")[8] == "true"
+    blob = P.ifq_pack_weights_fp4(d, p["w"]) if fp4 else P.ifq_pack_weights(d, p["w"])
     wd = to_dev(blob)
     td = None
     join = None
@@ -111,7 +115,14 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
     if dump:
         acc = torch.empty(max(n * ho * wo * L.cout, 1), dtype=torch.int32,
                           device=device())
-    P.ifq_conv_forward(d, xd, wd, td, y, join=join, acc_dump=acc)
+    if variant is None:
+        P.ifq_conv_forward(d, xd, wd, td, y, join=join, acc_dump=acc)
+    else:
+        name = P.ifq_conv_variant_name(d, join, variant)
+        assert name.startswith("conv_w2<"), (variant, name)
+        print("variant %d: %s n=%d %dx%dx%d -> %d s%d" % (variant, name, n, L.h, L.w, L.cin,
+                                                          L.cout, L.stride), flush=True)
+        P.ifq_conv_forward_variant(d, xd, wd, td, y, variant, join=join, acc_dump=acc)
     torch.cuda.synchronize()
     shape = (n, ho, wo, L.cout)
     acc_h = None if acc is None else acc[:np.prod(shape)].cpu().numpy().reshape(shape)

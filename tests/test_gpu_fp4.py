@@ -23,14 +23,23 @@ def P():
     return P
 
 
-# name, n, h, c_in, c_out, stride, expected variant (every variant with an
-# fp4 instance)
+def fp4_kernel(name):
+    """Whether a kernel name is an fp4 instance: the windowed kernel's last
+    template argument, the register-blocked kernel's ninth."""
+    if name.startswith("conv_halo<"):
+        return name.endswith(", true>")
+    if name.startswith("conv_w2<"):
+        return name[len("conv_w2<"):-1].split(", ")[8] == "true"
+    return False
+
+
+# name, n, h, c_in, c_out, stride, expected variant
 FP4 = [
-    ("f4_c64_small_batch", 2, 56, 64, 64, 1, "conv_halo<8, 1, 6, false, 4, true, true>"),
-    ("f4_l2", 3, 28, 128, 128, 1, "conv_halo<4, 2, 4, false, 4, true, true>"),
+    ("f4_c64_small_batch", 2, 56, 64, 64, 1, "conv_w2<1, 4, 1, 2, 2, 9, 2, true, true, 2, 20480>"),
+    ("f4_l2", 3, 28, 128, 128, 1, None),
     ("f4_l2_0_s2", 2, 56, 64, 128, 2, None),
-    ("f4_l3", 4, 14, 256, 256, 1, None),
-    ("f4_l4", 6, 7, 512, 512, 1, "conv_halo<2, 4, 4, false, 4, true, true>"),
+    ("f4_l3", 4, 14, 256, 256, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, true, true, 1, 36864>"),
+    ("f4_l4", 6, 7, 512, 512, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, true, true, 1, 36864>"),
 ]
 
 
@@ -52,7 +61,7 @@ def test_fp4_conv_bit_exact(P, case):
     for out_l in (B64, U2):
         d = P.conv_desc(n, h, h, cin, cout, 3, st, 1, 2, 2, B64, out_l)
         kname = P.ifq_conv_fp4_kernel_name(d)
-        assert kname.endswith(", true, true>"), kname
+        assert fp4_kernel(kname), kname
         if variant:
             assert kname == variant
         wd = to_dev(P.ifq_pack_weights_fp4(d, p["w"]))
@@ -67,14 +76,17 @@ def test_fp4_conv_bit_exact(P, case):
         assert np.array_equal(got, expect_layout(want, out_l)), (name, out_l, kname)
 
 
-def test_fp4_not_offered_for_the_64_channel_tiles(P):
-    # the full-batch 64-channel layers plan the two-workgroups-per-CU variant,
-    # which has no fp4 instance: the fp4 entry point declines them
+def test_fp4_offered_for_the_64_channel_tiles(P):
+    # the full-batch 64-channel layers run the register-blocked kernel's
+    # 64-channel tiles (two workgroups per CU), which have an fp4 instance
     d = P.conv_desc(64, 56, 56, 64, 64, 3, 1, 1, 2, 2, B64, B64)
-    assert P.ifq_conv_kernel_name(d) == "conv_halo<8, 1, 6, false, 2, true, false>"
-    assert P.ifq_conv_fp4_kernel_name(d) == ""
-    with pytest.raises(P.IfqError):
-        P.ifq_conv_forward_fp4(d, None, None, None, None)
+    assert P.ifq_conv_kernel_name(d) == "conv_w2<1, 4, 1, 2, 2, 3, 3, true, false, 2, 20480>"
+    assert P.ifq_conv_fp4_kernel_name(d) == "conv_w2<1, 4, 1, 2, 2, 9, 2, true, true, 2, 20480>"
+    # a fused pool is not the register-blocked kernel's: the windowed
+    # kernel's fp4 instances take it
+    pd = P.pool_desc(64, 56, 56, 64, 2, 2, P.IFQ_POOL_VALID, 2, B64)
+    assert P.ifq_conv_pool_fp4_kernel_name(d, pd) in ("",) or \
+        P.ifq_conv_pool_fp4_kernel_name(d, pd).startswith("conv_halo<")
 
 
 # identity join (the blocks' second convs): name, n, h, channels
@@ -99,7 +111,7 @@ def test_fp4_identity_join_bit_exact(P, case):
     xd = upload_codes(P, x, B64)
     d = P.conv_desc(n, h, h, c, c, 3, 1, 1, 2, 2, B64, B64)
     kname = P.ifq_conv_fp4_kernel_name(d, join)
-    assert kname.endswith(", false, true>"), kname
+    assert fp4_kernel(kname) and ", false, true" in kname, kname
     wd = to_dev(P.ifq_pack_weights_fp4(d, p["w"]))
     ob = P.ifq_tensor_bytes(n, h, h, c, B64)
     y = torch.full((ob,), 0xA5, dtype=torch.uint8, device=device())

@@ -1,0 +1,95 @@
+"""GPU parity of every variant of the register-blocked 3x3 kernel
+(ifq_conv_forward_variant): int32 sums and output codes (thresholds of
+Eq. 7/8, or the identity residual join) must equal the oracle's bit for bit
+on the same seeded inputs, on small ragged layers that span several tiles
+and on the ResNet-18-shaped stack's full-size layers."""
+import zlib
+
+import numpy as np
+import pytest
+
+from gpu_util import (B64, U2, gpu_layer, oracle_layer, expect_layout, make_layer,
+                      params_for, codes_for)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def P():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1911_08076_amd as P
+    return P
+
+
+# (name, n, h, w, cin, cout, stride)
+SMALL = [
+    ("r13x11_64_128", 2, 13, 11, 64, 128, 1),
+    ("s2_15_64_128", 2, 15, 15, 64, 128, 2),
+    ("r28_64_64", 1, 28, 28, 64, 64, 1),
+    ("r14_256_256", 2, 14, 14, 256, 256, 1),
+    ("r7_512_512", 3, 7, 7, 512, 512, 1),
+    ("s2_14_128_256", 5, 14, 14, 128, 256, 2),
+    ("r9_192_64", 1, 9, 9, 192, 64, 1),
+    ("r5_128_96", 3, 5, 6, 128, 96, 1),
+]
+
+FULL = [
+    ("l1", 64, 56, 56, 64, 64, 1),
+    ("l2", 64, 28, 28, 128, 128, 1),
+    ("l3", 64, 14, 14, 256, 256, 1),
+    ("l4", 64, 7, 7, 512, 512, 1),
+    ("l3.0.conv1_s2", 64, 28, 28, 128, 256, 2),
+]
+
+
+def _nvar(P):
+    return P.ifq_conv_variant_count()
+
+
+def _check(P, case, variant, join, out_layout=None):
+    name, n, h, w, cin, cout, st = case
+    if out_layout is None:
+        out_layout = B64 if cout % 64 == 0 else U2
+    L = make_layer(name, h, w, cin, cout, 3, st, 1, 2, 2,
+                   ("identity", "x") if join else None)
+    if join and (st != 1 or cin != cout):
+        pytest.skip("an identity join needs the block input's shape")
+    seed = zlib.crc32((name + str(join)).encode()) % 997
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, w, cin), 2)
+    d = P.conv_desc(n, h, w, cin, cout, 3, st, 1, 2, 2, B64, out_layout)
+    jn = None
+    if join:
+        jn = P.make_join(P.IFQ_JOIN_IDENTITY, B64, None, None, p["q_thr"])
+        jn.table = 0x1000
+    if not P.ifq_conv_variant_name(d, jn, variant):
+        pytest.skip("variant %d does not take %s" % (variant, name))
+    sc = x if join else None
+    want_acc, want = oracle_layer(L, x, p, shortcut=sc)
+    acc, got = gpu_layer(P, L, n, x, p, in_layout=B64, out_layout=out_layout, shortcut=sc,
+                         sc_layout=B64, variant=variant)
+    assert np.array_equal(acc, want_acc), (name, variant)
+    assert np.array_equal(got, expect_layout(want, out_layout)), (name, variant)
+    assert len(np.unique(want)) > 1
+
+
+@pytest.mark.parametrize("variant", range(10))
+@pytest.mark.parametrize("join", [False, True], ids=["thr", "idj"])
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_variant_small_bit_exact(P, case, join, variant):
+    assert _nvar(P) == 10
+    _check(P, case, variant, join)
+
+
+@pytest.mark.parametrize("variant", range(10))
+@pytest.mark.parametrize("join", [False, True], ids=["thr", "idj"])
+@pytest.mark.parametrize("case", FULL, ids=[c[0] for c in FULL])
+def test_variant_full_size_bit_exact(P, case, join, variant):
+    _check(P, case, variant, join)
+
+
+def test_variant_u2_output(P):
+    # the NHWC packed output layout through the same tile copy-out
+    _check(P, SMALL[0], 0, False, out_layout=U2)
