@@ -420,8 +420,9 @@ IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d, const ifq_join*
  * and per-variant parity tests (the same contraction, Eq. 1, and the same
  * epilogues as ifq_conv_forward). The kernel takes 3x3 pad-1 convs of
  * stride 1 or 2 on 2-bit BLOCK64 codes with c_in % 64 == 0, 2-bit output
- * (U2 or BLOCK64, c_out % 32 == 0, 27 * c_in <= 32766), no pool, and either
- * thresholds or an identity join with a 2-bit shortcut.
+ * (U2 or BLOCK64, c_out % 32 == 0, 27 * c_in <= 32766), no pool, and
+ * thresholds, an identity join with a 2-bit shortcut (c_out % 64 == 0), or a
+ * join with a fused 1x1 downsample on BLOCK64 codes of at most 256 channels.
  *   ifq_conv_variant_count   number of variants (host)
  *   ifq_conv_variant_name    the kernel variant `variant` would launch for
  *                            d and join (join nullable; no pointer in it is

@@ -782,10 +782,11 @@ IFQ_API ifq_status ifq_conv_forward_variant(const ifq_conv_desc* d, const void* 
   if (st != IFQ_OK) return st;
   if (d->n == 0) return ok();
   ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_packed, thr, join, sc, y, acc_dump);
-  if (ifq::w2_variant_fp4(variant)) {   // w_packed is the fp4 blob
+  if (ifq::w2_variant_fp4(variant)) {   // w_packed (and a fused join's down_w): fp4 blobs
     a.f4 = 1;
     a.rowsum = nullptr;
     a.wzero = fp4_zero_off(ifq::weight_geom(*d));
+    if (a.join_kind == IFQ_JOIN_CONV_FUSED) a.d_wzero = fp4_zero_off(ifq::weight_geom(join->down));
   }
   ifq::W2Plan p;
   if (variant < 0 || !ifq::plan_w2(a, variant, &p))
@@ -899,6 +900,8 @@ IFQ_API ifq_status ifq_conv_forward_fp4(const ifq_conv_desc* d, const void* x,
     if (ifq::plan_w2(f, -1, &wp)) {
       f.rowsum = nullptr;
       f.wzero = fp4_zero_off(ifq::weight_geom(*d));
+      if (f.join_kind == IFQ_JOIN_CONV_FUSED)   // join->down_w is the down conv's fp4 blob
+        f.d_wzero = fp4_zero_off(ifq::weight_geom(join->down));
       st = hip_status(ifq::launch_conv_w2(f, wp, stream), "conv fp4 launch");
       if (st != IFQ_OK) return st;
       return ok();

@@ -381,9 +381,12 @@ bool mfma_eligible(const ConvLaunch& a) {
 const char* conv_mfma_name(const ConvLaunch& a) {
   HaloPlan hp;
   const bool halo = plan_halo(a, &hp);
-  if (halo && a.join_kind == IFQ_JOIN_CONV_FUSED) return conv_halo_name(hp, a);
   W2Plan wp;
   const bool w2 = plan_w2(a, -1, &wp);
+  if (a.join_kind == IFQ_JOIN_CONV_FUSED) {
+    if (w2 && (!halo || wp.t_us <= hp.t_us)) return conv_w2_name(wp, a);
+    return halo ? conv_halo_name(hp, a) : "";
+  }
   const Plan pl = plan_mfma(a);
   if (w2 && wp.t_us <= pl.t_us && (!halo || wp.t_us <= hp.t_us)) return conv_w2_name(wp, a);
   if (halo && hp.t_us < pl.t_us) return conv_halo_name(hp, a);
@@ -393,10 +396,12 @@ const char* conv_mfma_name(const ConvLaunch& a) {
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream) {
   HaloPlan hp;
   const bool halo = plan_halo(a, &hp);
-  if (a.join_kind == IFQ_JOIN_CONV_FUSED)
-    return halo ? launch_conv_halo(a, hp, stream) : hipErrorNotSupported;
   W2Plan wp;
   const bool w2 = plan_w2(a, -1, &wp);
+  if (a.join_kind == IFQ_JOIN_CONV_FUSED) {
+    if (w2 && (!halo || wp.t_us <= hp.t_us)) return launch_conv_w2(a, wp, stream);
+    return halo ? launch_conv_halo(a, hp, stream) : hipErrorNotSupported;
+  }
   const Plan pl = plan_mfma(a);
   if (w2 && wp.t_us <= pl.t_us && (!halo || wp.t_us <= hp.t_us))
     return launch_conv_w2(a, wp, stream);

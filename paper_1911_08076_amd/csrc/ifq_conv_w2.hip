@@ -21,10 +21,13 @@
 //    fewer LDS bytes and VALU unpacks are spent per MFMA than with one
 //    32-pixel column per wave. The K groups add their sums through LDS.
 //
-// Epilogues: the 2-bit threshold epilogue of Eq. (7)/(8) on the transposed
-// layout (SW: codes as the MFMA's A operand, one output channel per lane), or
-// the identity residual join on the untransposed layout, with the packed
-// 16-bit compares of ifq_mfma_common.h; optional int32 dump of the sums.
+// Epilogues (MODE): 0, the 2-bit threshold epilogue of Eq. (7)/(8) on the
+// transposed layout (codes as the MFMA's A operand, one output channel per
+// lane); 1, the identity residual join on the untransposed layout, both with
+// the packed 16-bit compares of ifq_mfma_common.h; 2, the join with a 1x1
+// downsample computed in the kernel (its weights arrive as one extra stage of
+// the ring, its strided input cells in the prologue) and the fp64 join of
+// ifq_epilogue.h on the transposed layout. Optional int32 dump of the sums.
 #include <hip/hip_runtime.h>
 
 #include "ifq_epilogue.h"
@@ -39,11 +42,13 @@ constexpr int kW2Taps = 9;
 __host__ __device__ constexpr int w2_round64(int v) { return (v + 63) & ~63; }
 __host__ __device__ constexpr int w2_max(int a, int b) { return a > b ? a : b; }
 
-// SW: transposed sums (threshold epilogue); otherwise the identity join.
-template <int WM, int WN, int WK, int FM, int FN, int T, int D, bool SW, bool F4, int OCC,
+template <int WM, int WN, int WK, int FM, int FN, int T, int D, int MODE, bool F4, int OCC,
           int WINB>
 __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void conv_w2(
     ConvLaunch a) {
+  constexpr bool SW = MODE != 1;                 // transposed sums
+  constexpr bool FUSED = MODE == 2;
+  constexpr int GDM = 4;                         // downsample channel blocks at most
   constexpr int NW = WM * WN * WK;
   constexpr int NT = 64 * NW;
   constexpr int BM = 32 * FM * WM;
@@ -65,13 +70,17 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
   constexpr int DUMMY = WIN0 + WINB;             // 1 KB sink of padding loads
   constexpr int NOK = FM * FN - NB;              // blocks a wave hands to the others
   constexpr int RED_BYTES = WK > 1 ? NW * NOK * 4096 : 0;
-  constexpr int EPI_BYTES = SW ? 0 : BM * 128;    // stage_idj_pk's records
+  // staged epilogue parameters: the identity join's records, or the
+  // downsample join's {p, q, cc} per channel (at kJoinCoefOff)
+  constexpr int EPI_BYTES = MODE == 1 ? BM * 128 : MODE == 2 ? (kJoinCoefOff + BM * 24 + 15) / 16 * 16 : 0;
   constexpr int OUT_BYTES = BN * BM / 4;         // 2-bit output tile
-  constexpr int TBL_BYTES = SW ? BM * 16 : BM * 64;
+  // prefetched per-channel records: thresholds, join records or coefficients
+  constexpr int TBL_BYTES = MODE == 0 ? BM * 16 : MODE == 1 ? BM * 64 : (BM * 24 + 1023) / 1024 * 1024;
   constexpr int THR = w2_max(w2_max(DUMMY + 1024, RED_BYTES), EPI_BYTES + OUT_BYTES);
-  // identity join: the tile's shortcut cells, [BM/64 blocks][BN pixels] x 16 B
+  // the tile's shortcut cells [BM/64 blocks][BN pixels] (identity join) or
+  // the downsample's strided input cells [GDM blocks][BN pixels], 16 B each
   constexpr int SCB = THR + TBL_BYTES;
-  constexpr int SC_BYTES = SW ? 0 : (BM / 64) * BN * 16;
+  constexpr int SC_BYTES = MODE == 1 ? (BM / 64) * BN * 16 : MODE == 2 ? GDM * BN * 16 : 0;
   constexpr int LDS_BYTES = SCB + SC_BYTES;
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 
@@ -122,11 +131,39 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
 
   // ---- prologue: the epilogue's per-channel records, the windows of all
   // channel blocks, then stages 0 .. D-2 of the weight ring --------------------
-  if constexpr (SW) {
+  if constexpr (MODE == 0) {
     for (int q = wave; q < BM / 64; q += NW) {
       const int c = co0 + q * 64 + lane;
       dma16(c < a.cout ? reinterpret_cast<const uint8_t*>(a.thr + (int64_t)c * 4) : zero_src,
             lds0 + THR + q * 1024);
+    }
+  } else if constexpr (MODE == 2) {
+    // the join coefficients of the tile's channels (24 bytes each, as 16-byte
+    // pieces; c_out % 32 == 0 keeps every piece inside the array or past it)
+    const uint8_t* cf8 = reinterpret_cast<const uint8_t*>(a.coef);
+    const int nch = a.cout - co0 < BM ? a.cout - co0 : BM;
+    for (int q = wave; q < TBL_BYTES / 1024; q += NW) {
+      const int e = q * 64 + lane;               // 16-byte piece of the slice
+      dma16(e * 16 < nch * 24 ? cf8 + (int64_t)co0 * 24 + e * 16 : zero_src,
+            lds0 + THR + q * 1024);
+    }
+    // the downsample's input cells of the tile's pixels: pixel (n, oy, ox)
+    // reads cell (n, gd, oy*d_stride, ox*d_stride) of its BLOCK64 input
+    const int Gd = a.d_cin >> 6;
+    const int ncx = (bn + 63) >> 6;
+    for (int q = wave; q < Gd * ncx; q += NW) {
+      const int gd = q / ncx, j = q - gd * ncx;
+      const int pl = j * 64 + lane, p = p0 + pl;
+      const uint8_t* src = zero_src;
+      if (pl < bn && p < a.m) {
+        const int n = fdiv(p, a.div_howo);
+        const int rem = p - n * howo;
+        const int oy = fdiv(rem, a.div_wo);
+        const int ox = rem - oy * Wo;
+        src = a.dx + ((((int64_t)n * Gd + gd) * a.d_h + oy * a.d_stride) * a.d_w +
+                      ox * a.d_stride) * 16;
+      }
+      dma16(src, lds0 + SCB + (uint32_t)((gd * BN + j * 64) * 16));
     }
   } else {
     for (int q = wave; q < BM / 16; q += NW) {   // 16 channels x 64 B per chunk
@@ -205,8 +242,38 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
       }
     }
   };
-  const int pre = nst < D - 1 ? nst : D - 1;
-  for (int s = 0; s < pre; ++s) issue_stage(s);
+  // the downsample's weights: one extra stage after the 3x3 stages, chunk
+  // c = (gd*RB + rb)*KH + t (Gd * RB * KH <= NCH, checked by the host)
+  const int nst_all = nst + (FUSED ? 1 : 0);
+  auto issue_down = [&]() {
+    const uint32_t slot = lds0 + (uint32_t)((nst % D) * STAGE);
+    const int Gd = a.d_cin >> 6;
+#pragma unroll
+    for (int k = 0; k < CPW; ++k) {
+      const int c = wave + NW * k;
+      if (c < Gd * RB * KH) {
+        const int t = c % KH;
+        const int rb = (c / KH) % RB;
+        const int gd = c / (KH * RB);
+        const int64_t off =
+            rbw + rb < nrb
+                ? ((int64_t)(rbw + rb) * (KH == 2 ? a.d_nk32 : Gd) + (KH == 2 ? 2 * gd + t : gd)) *
+                      1024
+                : a.d_wzero;
+        dma16s(reinterpret_cast<const uint8_t*>(a.dwgt) + off, voff, slot + (uint32_t)(c * 1024));
+      } else {
+        dma16(zero_src, lds0 + DUMMY);
+      }
+    }
+  };
+  auto issue_any = [&](int s) {
+    if (s < nst)
+      issue_stage(s);
+    else
+      issue_down();
+  };
+  const int pre = nst_all < D - 1 ? nst_all : D - 1;
+  for (int s = 0; s < pre; ++s) issue_any(s);
 
   // ---- per-lane LDS offsets of the nine taps of each pixel column block,
   // relative to a block window (computed while the prologue's loads are in
@@ -329,12 +396,12 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
 #pragma unroll
     for (int ts = 0; ts < TSTEPS; ++ts) {
       const int s = gi * TSTEPS + ts;
-      const int after = nst - 1 - s;
+      const int after = nst_all - 1 - s;
       wait_ahead<D - 2, CPW>(after < D - 2 ? after : D - 2);
       asm volatile("" ::: "memory");
       __builtin_amdgcn_s_barrier();
       asm volatile("" ::: "memory");
-      if (s + D - 1 < nst) issue_stage(s + D - 1);
+      if (s + D - 1 < nst_all) issue_any(s + D - 1);
       Frag f0, f1;
       read_frags(slot, 0, ts * T, win, f0);
 #pragma unroll
@@ -356,6 +423,48 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
   }
   wait_vmcnt<0>();
   __syncthreads();
+
+  // ---- the downsample's sums of the blocks this wave keeps after the K
+  // sum (its weights in the extra stage's slot, its cells at SCB) ------------
+  v16i accd[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) accd[j] = v16i{0};
+  if constexpr (FUSED) {
+    const uint8_t* ds = lds + (nst % D) * STAGE;
+    const int Gd = a.d_cin >> 6;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int b = kg * NB + j;
+      const int fm = b / FN, fn = b - fm * FN;
+      const int pl = (wn * FN + fn) * 32 + l32;
+      const int rbl = wm * FM + fm;
+      v16f df = v16f{0.0f};
+      for (int gd = 0; gd < Gd; ++gd) {
+        const v2i braw = *reinterpret_cast<const v2i*>(lds + SCB + (gd * BN + pl) * 16 + 8 * h);
+        if constexpr (F4) {
+          const uint32_t w0 = (uint32_t)braw[0], w1 = (uint32_t)braw[1];
+          const v8i bf = v8i{(int)(w0 & 0x33333333u), (int)((w0 >> 2) & 0x33333333u),
+                             (int)(w1 & 0x33333333u), (int)((w1 >> 2) & 0x33333333u), 0, 0, 0, 0};
+          const v4i w = *reinterpret_cast<const v4i*>(ds + (gd * RB + rbl) * 1024 + lane * 16);
+          const v8i af = v8i{w.x, w.y, w.z, w.w, 0, 0, 0, 0};
+          df = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(bf, af, df, 4, 4, 0, 127, 0, 127);
+        } else {
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            const v4i af =
+                *reinterpret_cast<const v4i*>(ds + ((gd * RB + rbl) * 2 + t) * 1024 + lane * 16);
+            accd[j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(unpack2((uint32_t)braw[t]), af,
+                                                            accd[j], 0, 0, 0);
+          }
+        }
+      }
+      if constexpr (F4) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i) accd[j][i] = (int)df[i];
+      }
+    }
+    __syncthreads();   // before the K-group exchange reuses the ring
+  }
 
   // ---- K groups: wave (wm, wn, kg) keeps blocks b = fm*FN + fn in
   // [kg*NB, kg*NB + NB); the other groups' sums of those blocks come through
@@ -400,9 +509,14 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
   }
 
   // ---- epilogue -------------------------------------------------------------
-  if constexpr (!SW)
+  if constexpr (MODE == 1)
     stage_idj_pk(reinterpret_cast<const int32_t*>(lds + THR), lds, BM,
                  a.cout - co0 < BM ? a.cout - co0 : BM);
+  if constexpr (MODE == 2) {
+    const double* src = reinterpret_cast<const double*>(lds + THR);
+    double* dst = reinterpret_cast<double*>(lds + kJoinCoefOff);
+    for (int i = tid; i < BM * 3; i += NT) dst[i] = src[i];
+  }
   __syncthreads();
   constexpr int orow = BM / 4;
   uint8_t* otile = lds + EPI_BYTES;
@@ -412,10 +526,14 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
     const int rbl = wm * FM + b / FN;            // row block in the tile
     const int pcb = wn * FN + b % FN;            // pixel column block in the tile
     const v16i one[1] = {own[j]};
-    if constexpr (SW) {
+    if constexpr (MODE == 0) {
       if (a.acc_dump) dump_acc_t<1>(a, one, rbl, h, l32, co0, p0, pcb * 32, bn, a.acc_dump);
       epilogue_thr_pk_t<1>(a, reinterpret_cast<const int4*>(lds + THR), one, rbl, h, l32, co0,
                            pcb * 32, otile, orow);
+    } else if constexpr (MODE == 2) {
+      if (a.acc_dump) dump_acc_t<1>(a, one, rbl, h, l32, co0, p0, pcb * 32, bn, a.acc_dump);
+      const v16i oned[1] = {accd[j]};
+      epilogue_cjoin_t<1>(a, lds, one, oned, rbl, h, l32, co0, pcb * 32, otile, orow);
     } else {
       const v16i one2[1][1] = {{own[j]}};
       if (a.acc_dump)
@@ -442,14 +560,17 @@ struct W2Variant {
   double c0_us;        // fixed cost per round of occ workgroups on a CU
   double eff;          // MFMA efficiency of a tile's main loop
   const char* thr_name;   // the kernels as a profiler lists them: threshold
-  const char* idj_name;   // epilogue (transposed), identity join
+  const char* idj_name;   // epilogue, identity join, fused downsample join
+  const char* fused_name;
 };
 
-#define IFQ_W2_NAMES(wm, wn, wk, fm, fn, t, d, f4, occ, winb)                             \
-  "conv_w2<" #wm ", " #wn ", " #wk ", " #fm ", " #fn ", " #t ", " #d ", true, " #f4 ", " #occ \
-  ", " #winb ">",                                                                           \
-      "conv_w2<" #wm ", " #wn ", " #wk ", " #fm ", " #fn ", " #t ", " #d ", false, " #f4     \
-      ", " #occ ", " #winb ">"
+#define IFQ_W2_NAME(wm, wn, wk, fm, fn, t, d, mode, f4, occ, winb)                          \
+  "conv_w2<" #wm ", " #wn ", " #wk ", " #fm ", " #fn ", " #t ", " #d ", " #mode ", " #f4 ", " \
+  #occ ", " #winb ">"
+#define IFQ_W2_NAMES(wm, wn, wk, fm, fn, t, d, f4, occ, winb)      \
+  IFQ_W2_NAME(wm, wn, wk, fm, fn, t, d, 0, f4, occ, winb),         \
+      IFQ_W2_NAME(wm, wn, wk, fm, fn, t, d, 1, f4, occ, winb),     \
+      IFQ_W2_NAME(wm, wn, wk, fm, fn, t, d, 2, f4, occ, winb)
 
 // Index order must match the switch in launch_conv_w2.
 // (c0_us, eff) are fitted to kernel times measured on MI355X over the
@@ -491,8 +612,13 @@ bool w2_mode_ok(const ConvLaunch& a) {
     return false;
   if (a.join_kind == IFQ_JOIN_NONE) return true;
   // identity join: the shortcut is prefetched as whole 16-byte cells
-  return a.join_kind == IFQ_JOIN_IDENTITY && a.cout % 64 == 0 &&
-         (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64 || a.sc_layout == IFQ_LAYOUT_U2_NHWC_PACKED);
+  if (a.join_kind == IFQ_JOIN_IDENTITY)
+    return a.cout % 64 == 0 &&
+           (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64 || a.sc_layout == IFQ_LAYOUT_U2_NHWC_PACKED);
+  // downsample join: 1x1 conv on BLOCK64 codes with at most 4 channel blocks
+  return a.join_kind == IFQ_JOIN_CONV_FUSED && a.sc_layout == IFQ_LAYOUT_U2_BLOCK64 &&
+         a.d_cin % 64 == 0 && a.d_cin / 64 <= 4 &&
+         (int64_t)a.n * a.d_h * a.d_w * (a.d_cin / 64) < (int64_t)1 << 26;
 }
 
 // Pixels per workgroup and the predicted time of variant v on layer a, or
@@ -502,6 +628,11 @@ bool w2_fit(const ConvLaunch& a, int v, W2Plan* out) {
   if (V.f4 != (a.f4 != 0)) return false;
   const int G = a.cin / 64;
   if (G % V.wk) return false;
+  // the downsample's weights fit one stage; the two-per-CU eight-wave tiles'
+  // join instance needs more than their 128 VGPRs
+  if (a.join_kind == IFQ_JOIN_CONV_FUSED &&
+      (a.d_cin / 64 > V.wk * V.t || (V.occ == 2 && V.wm * V.wn * V.wk == 8 && V.fn == 2)))
+    return false;
   const int bm = 32 * V.fm * V.wm, bnmax = 32 * V.fn * V.wn;
   const int64_t slots = (int64_t)kW2CUs * V.occ;
   const int64_t nco = (a.cout + bm - 1) / bm;
@@ -547,7 +678,9 @@ bool plan_w2(const ConvLaunch& a, int forced, W2Plan* out) {
 
 const char* conv_w2_name(const W2Plan& p, const ConvLaunch& a) {
   const W2Variant& V = kW2Variants[p.variant];
-  return a.join_kind == IFQ_JOIN_IDENTITY ? V.idj_name : V.thr_name;
+  return a.join_kind == IFQ_JOIN_IDENTITY    ? V.idj_name
+         : a.join_kind == IFQ_JOIN_CONV_FUSED ? V.fused_name
+                                              : V.thr_name;
 }
 
 hipError_t launch_conv_w2(ConvLaunch a, const W2Plan& p, hipStream_t stream) {
@@ -557,16 +690,20 @@ hipError_t launch_conv_w2(ConvLaunch a, const W2Plan& p, hipStream_t stream) {
   const int bm = 32 * V.fm * V.wm;
   const dim3 grid(p.blocks_m, (a.cout + bm - 1) / bm);
   const dim3 block(64 * V.wm * V.wn * V.wk);
-  const bool sw = a.join_kind != IFQ_JOIN_IDENTITY;
-  switch (p.variant * 2 + (sw ? 0 : 1)) {
-#define IFQ_W2_CASE(k, wm, wn, wk, fm, fn, t, d, f4, occ, winb)                              \
-  case 2 * k:                                                                                \
-    hipLaunchKernelGGL((conv_w2<wm, wn, wk, fm, fn, t, d, true, f4, occ, winb>), grid, block, \
-                       0, stream, a);                                                        \
-    break;                                                                                   \
-  case 2 * k + 1:                                                                            \
-    hipLaunchKernelGGL((conv_w2<wm, wn, wk, fm, fn, t, d, false, f4, occ, winb>), grid,      \
-                       block, 0, stream, a);                                                 \
+  const int mode = a.join_kind == IFQ_JOIN_IDENTITY ? 1 : a.join_kind == IFQ_JOIN_CONV_FUSED ? 2 : 0;
+  switch (p.variant * 3 + mode) {
+#define IFQ_W2_CASE(k, wm, wn, wk, fm, fn, t, d, f4, occ, winb)                                 \
+  case 3 * k:                                                                                   \
+    hipLaunchKernelGGL((conv_w2<wm, wn, wk, fm, fn, t, d, 0, f4, occ, winb>), grid, block, 0,   \
+                       stream, a);                                                              \
+    break;                                                                                      \
+  case 3 * k + 1:                                                                               \
+    hipLaunchKernelGGL((conv_w2<wm, wn, wk, fm, fn, t, d, 1, f4, occ, winb>), grid, block, 0,   \
+                       stream, a);                                                              \
+    break;                                                                                      \
+  case 3 * k + 2:                                                                               \
+    hipLaunchKernelGGL((conv_w2<wm, wn, wk, fm, fn, t, d, 2, f4, occ, winb>), grid, block, 0,   \
+                       stream, a);                                                              \
     break;
     IFQ_W2_CASE(0, 2, 4, 1, 2, 2, 3, 3, false, 1, 49152)
     IFQ_W2_CASE(1, 1, 4, 2, 2, 2, 3, 2, false, 1, 53248)

@@ -175,11 +175,6 @@ struct HaloPlan {
   double t_us;
 };
 bool plan_halo(const ConvLaunch& a, HaloPlan* out);
-// Whether a launch with a fused downsample (IFQ_JOIN_CONV_FUSED) is covered.
-inline bool fused_supported(const ConvLaunch& a) {
-  HaloPlan p;
-  return plan_halo(a, &p);
-}
 hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream);
 const char* conv_halo_name(const HaloPlan& p, const ConvLaunch& a);
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream);
@@ -201,6 +196,14 @@ bool w2_variant_fp4(int v);   // variant v runs the fp4 contraction (fp4 weight 
 bool plan_w2(const ConvLaunch& a, int forced, W2Plan* out);
 hipError_t launch_conv_w2(ConvLaunch a, const W2Plan& p, hipStream_t stream);
 const char* conv_w2_name(const W2Plan& p, const ConvLaunch& a);
+
+// Whether a launch with a fused downsample (IFQ_JOIN_CONV_FUSED) is covered
+// by one of the 3x3 kernels.
+inline bool fused_supported(const ConvLaunch& a) {
+  HaloPlan p;
+  W2Plan w;
+  return plan_halo(a, &p) || plan_w2(a, -1, &w);
+}
 
 // 8-bit input codes with c_in <= 4 (a detector's first layer): whether the
 // small-channel kernel takes the layer, its launch and its name.

@@ -66,8 +66,8 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
     d = P.conv_desc(n, L.h, L.w, L.cin, L.cout, L.k, L.stride, L.pad,
                     L.in_bits, L.out_bits, in_layout, out_layout)
     ho, wo = P.ifq_conv_output_dims(d)
-    fp4 = variant is not None and \
-        P.ifq_conv_variant_name(d, None, variant)[len("conv_w2<"):-1].split(", ")[8] == "true"
+    vname = P.ifq_conv_variant_name(d, None, variant) if variant is not None else ""
+    fp4 = bool(vname) and vname[len("conv_w2<"):-1].split(", ")[8] == "true"
     blob = P.ifq_pack_weights_fp4(d, p["w"]) if fp4 else P.ifq_pack_weights(d, p["w"])
     wd = to_dev(blob)
     td = None
@@ -94,14 +94,19 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
             coef = P.ifq_fold_join(P.IFQ_JOIN_CONV, p, down["beta_in"], down=down)
             dd = P.conv_desc(n, D.h, D.w, D.cin, D.cout, D.k, D.stride, D.pad,
                              D.in_bits, 0, B64, I32)
-            wdd = to_dev(P.ifq_pack_weights(dd, down["w"]))
+            wdd = to_dev(P.ifq_pack_weights_fp4(dd, down["w"]) if fp4 else
+                         P.ifq_pack_weights(dd, down["w"]))
             xind = upload_codes(P, xin, B64)
             cd = to_dev(coef)
             keep += [wdd, xind, cd]
             join = P.make_join(P.IFQ_JOIN_CONV_FUSED, B64, xind, cd, p["q_thr"],
                                down_w=wdd, down=dd)
             # the kernel name query sees the join: a fused kernel instance
-            assert ", true, " in P.ifq_conv_kernel_name(d, join)
+            # (the windowed kernel's fused flag, or the register-blocked
+            # kernel's epilogue mode 2)
+            kn = P.ifq_conv_kernel_name(d, join)
+            assert ", true, " in kn or (kn.startswith("conv_w2<") and
+                                        kn[8:-1].split(", ")[7] == "2"), kn
         else:
             coef = P.ifq_fold_join(P.IFQ_JOIN_CONV, p, down["beta_in"], down=down)
             scd = to_dev(shortcut.astype(np.int32))

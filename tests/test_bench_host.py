@@ -15,12 +15,12 @@ def test_fp4_kernels_priced_against_the_fp4_peak():
     assert bench.kernel_peak("conv_halo<4, 2, 4, false, 4, true, true>") == bench.PEAK_FP4_TFLOPS
     assert bench.kernel_peak("conv_halo<2, 4, 4, true, 4, true, true>") == bench.PEAK_FP4_TFLOPS
     assert bench.kernel_peak("conv_halo<8, 1, 6, false, 4, false, true>") == bench.PEAK_FP4_TFLOPS
-    assert bench.kernel_peak("conv_w2<1, 2, 4, 2, 2, 3, 2, true, true, 1, 36864>") == \
+    assert bench.kernel_peak("conv_w2<1, 2, 4, 2, 2, 3, 2, 0, true, 1, 36864>") == \
         bench.PEAK_FP4_TFLOPS
-    assert bench.kernel_peak("conv_w2<1, 4, 1, 2, 2, 9, 2, false, true, 2, 20480>") == \
+    assert bench.kernel_peak("conv_w2<1, 4, 1, 2, 2, 9, 2, 1, true, 2, 20480>") == \
         bench.PEAK_FP4_TFLOPS
-    for int8 in ("conv_w2<2, 4, 1, 2, 2, 3, 3, true, false, 1, 49152>",
-                 "conv_w2<1, 4, 1, 2, 2, 3, 3, false, false, 2, 20480>",
+    for int8 in ("conv_w2<2, 4, 1, 2, 2, 3, 3, 0, false, 1, 49152>",
+                 "conv_w2<1, 4, 1, 2, 2, 3, 3, 1, false, 2, 20480>",
                  "conv_halo<8, 1, 6, false, 2, false, false>",
                  "conv_halo<8, 1, 6, true, 4, true, false>",
                  "conv_mfma<2, 1, 4, 1, 4, 1, 6>", "conv_small8<1>", "conv_igemm<32, 128, 1, 1>"):

@@ -35,11 +35,11 @@ def fp4_kernel(name):
 
 # name, n, h, c_in, c_out, stride, expected variant
 FP4 = [
-    ("f4_c64_small_batch", 2, 56, 64, 64, 1, "conv_w2<1, 4, 1, 2, 2, 9, 2, true, true, 2, 20480>"),
+    ("f4_c64_small_batch", 2, 56, 64, 64, 1, "conv_w2<1, 4, 1, 2, 2, 9, 2, 0, true, 2, 20480>"),
     ("f4_l2", 3, 28, 128, 128, 1, None),
     ("f4_l2_0_s2", 2, 56, 64, 128, 2, None),
-    ("f4_l3", 4, 14, 256, 256, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, true, true, 1, 36864>"),
-    ("f4_l4", 6, 7, 512, 512, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, true, true, 1, 36864>"),
+    ("f4_l3", 4, 14, 256, 256, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, 0, true, 1, 36864>"),
+    ("f4_l4", 6, 7, 512, 512, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, 0, true, 1, 36864>"),
 ]
 
 
@@ -80,8 +80,8 @@ def test_fp4_offered_for_the_64_channel_tiles(P):
     # the full-batch 64-channel layers run the register-blocked kernel's
     # 64-channel tiles (two workgroups per CU), which have an fp4 instance
     d = P.conv_desc(64, 56, 56, 64, 64, 3, 1, 1, 2, 2, B64, B64)
-    assert P.ifq_conv_kernel_name(d) == "conv_w2<1, 4, 1, 2, 2, 3, 3, true, false, 2, 20480>"
-    assert P.ifq_conv_fp4_kernel_name(d) == "conv_w2<1, 4, 1, 2, 2, 9, 2, true, true, 2, 20480>"
+    assert P.ifq_conv_kernel_name(d) == "conv_w2<1, 4, 1, 2, 2, 3, 3, 0, false, 2, 20480>"
+    assert P.ifq_conv_fp4_kernel_name(d) == "conv_w2<1, 4, 1, 2, 2, 9, 2, 0, true, 2, 20480>"
     # a fused pool is not the register-blocked kernel's: the windowed
     # kernel's fp4 instances take it
     pd = P.pool_desc(64, 56, 56, 64, 2, 2, P.IFQ_POOL_VALID, 2, B64)
@@ -111,7 +111,7 @@ def test_fp4_identity_join_bit_exact(P, case):
     xd = upload_codes(P, x, B64)
     d = P.conv_desc(n, h, h, c, c, 3, 1, 1, 2, 2, B64, B64)
     kname = P.ifq_conv_fp4_kernel_name(d, join)
-    assert fp4_kernel(kname) and ", false, true" in kname, kname
+    assert fp4_kernel(kname) and kname[8:-1].split(", ")[7] == "1", kname
     wd = to_dev(P.ifq_pack_weights_fp4(d, p["w"]))
     ob = P.ifq_tensor_bytes(n, h, h, c, B64)
     y = torch.full((ob,), 0xA5, dtype=torch.uint8, device=device())
@@ -149,7 +149,10 @@ def test_fp4_fused_downsample_bit_exact(P, shape):
     xd = upload_codes(P, x, B64)
     join = P.make_join(P.IFQ_JOIN_CONV_FUSED, B64, xind, coef, p["q_thr"], down_w=dw4, down=dd)
     kname = P.ifq_conv_fp4_kernel_name(d, join)
-    assert kname.endswith(", true, 4, true, true>"), kname
+    # a fused join instance on fp4: the windowed kernel's (fused flag true)
+    # or the register-blocked kernel's (epilogue mode 2)
+    assert fp4_kernel(kname) and (kname.endswith(", true, 4, true, true>") or
+                                  kname[8:-1].split(", ")[7] == "2"), kname
     ob = P.ifq_tensor_bytes(n, ho, ho, cout, B64)
     y = torch.full((ob,), 0xA5, dtype=torch.uint8, device=device())
     P.ifq_conv_forward_fp4(d, xd, w4, None, y, join=join)

@@ -1,8 +1,9 @@
 """GPU parity of every variant of the register-blocked 3x3 kernel
-(ifq_conv_forward_variant): int32 sums and output codes (thresholds of
-Eq. 7/8, or the identity residual join) must equal the oracle's bit for bit
-on the same seeded inputs, on small ragged layers that span several tiles
-and on the ResNet-18-shaped stack's full-size layers."""
+(ifq_conv_forward_variant), int8 and fp4 instances: int32 sums and output
+codes (thresholds of Eq. 7/8, the identity residual join, or the join with
+a 1x1 downsample computed in the kernel) must equal the oracle's bit for
+bit on the same seeded inputs, on small ragged layers that span several
+tiles and on the ResNet-18-shaped stack's full-size layers."""
 import zlib
 
 import numpy as np
@@ -93,3 +94,37 @@ def test_variant_full_size_bit_exact(P, case, join, variant):
 def test_variant_u2_output(P):
     # the NHWC packed output layout through the same tile copy-out
     _check(P, SMALL[0], 0, False, out_layout=U2)
+
+
+# downsampling blocks' second conv with the 1x1 stride-2 downsample fused:
+# (n, h_in, c_in, c_out); ragged, small and the full ResNet-18 shapes
+FUSED = [(2, 56, 64, 128), (3, 28, 128, 256), (2, 14, 256, 512), (5, 13, 64, 128),
+         (64, 56, 64, 128), (64, 28, 128, 256), (64, 14, 256, 512)]
+
+
+@pytest.mark.parametrize("variant", range(10))
+@pytest.mark.parametrize("shape", FUSED, ids=["x".join(map(str, f)) for f in FUSED])
+def test_variant_fused_downsample_bit_exact(P, shape, variant):
+    n, hin, cin, cout = shape
+    D = make_layer("down", hin, hin, cin, cout, 1, 2, 0, 2, 0)
+    ho = (hin - 1) // 2 + 1
+    L = make_layer("conv2", ho, ho, cout, cout, 3, 1, 1, join=("conv", "d", "down"))
+    d = P.conv_desc(n, ho, ho, cout, cout, 3, 1, 1, 2, 2, B64, B64)
+    dd = P.conv_desc(n, hin, hin, cin, cout, 1, 2, 0, 2, 0, B64, P.IFQ_LAYOUT_I32_NHWC)
+    jn = P.make_join(P.IFQ_JOIN_CONV_FUSED, B64, None, None, [0.25, 0.75, 1.25], down=dd)
+    jn.coef = 0x1000
+    jn.down_w = 0x1000
+    if not P.ifq_conv_variant_name(d, jn, variant):
+        pytest.skip("variant %d does not take %s" % (variant, shape))
+    seed = 31 + hin + n
+    pd = params_for(seed, D)
+    p = params_for(seed + 1, L)
+    xin = codes_for(seed, (n, hin, hin, cin), 2)
+    x = codes_for(seed + 1, (n, ho, ho, cout), 2)
+    want_d, _ = oracle_layer(D, xin, pd)
+    want_acc, want = oracle_layer(L, x, p, shortcut=want_d, down=pd)
+    acc, got = gpu_layer(P, L, n, x, p, in_layout=B64, out_layout=B64, down=pd,
+                         fused_down=(D, xin), variant=variant)
+    assert np.array_equal(acc, want_acc), (shape, variant)
+    assert np.array_equal(got, expect_layout(want, B64)), (shape, variant)
+    assert len(np.unique(want)) > 1
