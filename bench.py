@@ -79,21 +79,24 @@ class Hip:
 
 def kernel_peak(name):
     """Dense peak of the matrix instructions a kernel runs on: the fp4
-    instances (the windowed kernel's last template argument, the fp4 flag,
-    true; the register-blocked kernel's ninth) against MXFP4, the others
+    instances (the fp4 flag true: the windowed kernel's last template
+    argument, conv_w2's ninth, conv_wp's fifth) against MXFP4, the others
     against int8."""
     fp4 = False
     if name.startswith("conv_halo<"):
         fp4 = name.endswith(", true>")
     elif name.startswith("conv_w2<"):
         fp4 = name[len("conv_w2<"):-1].split(", ")[8] == "true"
+    elif name.startswith("conv_wp<"):
+        fp4 = name[len("conv_wp<"):-1].split(", ")[4] == "true"
     return PEAK_FP4_TFLOPS if fp4 else PEAK_INT8_TOPS
 
 
 def source_hash():
     h = hashlib.sha256()
     for f in ("ifq_conv.hip", "ifq_conv_mfma.hip", "ifq_conv_halo.hip", "ifq_conv_small.hip",
-              "ifq_epilogue.h", "ifq_mfma_common.h", "ifq_pool.hip"):
+              "ifq_conv_w2.hip", "ifq_conv_wp.hip", "ifq_epilogue.h", "ifq_mfma_common.h",
+              "ifq_pool.hip"):
         with open(os.path.join(ROOT, "paper_1911_08076_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

@@ -416,14 +416,23 @@ IFQ_API ifq_status ifq_fold_join_table(const ifq_join_params* p, int32_t in_bits
 IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d, const ifq_join* join);
 
 /*
- * Kernel variants of the register-blocked 3x3 conv kernel, for autotuning
+ * Kernel variants of the register-blocked 3x3 conv kernels, for autotuning
  * and per-variant parity tests (the same contraction, Eq. 1, and the same
- * epilogues as ifq_conv_forward). The kernel takes 3x3 pad-1 convs of
- * stride 1 or 2 on 2-bit BLOCK64 codes with c_in % 64 == 0, 2-bit output
+ * epilogues as ifq_conv_forward): conv_w2 (one output tile per workgroup)
+ * and conv_wp (persistent: a workgroup keeps the weights of its 64 output
+ * channels in LDS and runs a range of pixel tiles). Both take 3x3 pad-1 convs
+ * of stride 1 or 2 on 2-bit BLOCK64 codes with c_in % 64 == 0, 2-bit output
  * (U2 or BLOCK64, c_out % 32 == 0, 27 * c_in <= 32766), no pool, and
- * thresholds, an identity join with a 2-bit shortcut (c_out % 64 == 0), or a
- * join with a fused 1x1 downsample on BLOCK64 codes of at most 256 channels.
+ * thresholds or an identity join with a 2-bit shortcut (c_out % 64 == 0);
+ * conv_w2 also a join with a fused 1x1 downsample on BLOCK64 codes of at
+ * most 256 channels. Each variant further needs its weights and input
+ * windows to fit its LDS budget.
  *   ifq_conv_variant_count   number of variants (host)
+ *   ifq_conv_variant_fp4     1 if variant computes the sums exactly on the
+ *                            fp4 scaled MFMA, as ifq_conv_forward_fp4 (its
+ *                            w_packed, and a fused join's down_w, are then
+ *                            ifq_pack_weights_fp4 blobs), 0 if on the int8
+ *                            MFMA, -1 if variant is out of range (host)
  *   ifq_conv_variant_name    the kernel variant `variant` would launch for
  *                            d and join (join nullable; no pointer in it is
  *                            dereferenced), or "" if it cannot take the
@@ -432,11 +441,9 @@ IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d, const ifq_join*
  *                            workspace) on that variant, asynchronous on
  *                            stream; IFQ_ERR_UNSUPPORTED where it cannot
  *                            take the layer. Errors as ifq_conv_forward.
- * Variants whose name has the fp4 flag (the ninth template argument) true
- * compute the sums exactly on the fp4 scaled MFMA, as ifq_conv_forward_fp4:
- * their w_packed is the ifq_pack_weights_fp4 blob.
  */
 IFQ_API int32_t ifq_conv_variant_count(void);
+IFQ_API int32_t ifq_conv_variant_fp4(int32_t variant);
 IFQ_API const char* ifq_conv_variant_name(const ifq_conv_desc* d, const ifq_join* join,
                                           int32_t variant);
 IFQ_API ifq_status ifq_conv_forward_variant(const ifq_conv_desc* d, const void* x,

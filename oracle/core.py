@@ -97,6 +97,8 @@ def fold(alpha, beta_in, mean, var, gamma, bn_beta, eps, q_thr, k, in_bits,
 
 def codes(acc, s, t):
     acc = np.ascontiguousarray(acc, dtype=np.int32)
+    s = np.ascontiguousarray(s, dtype=np.int32)
+    t = np.ascontiguousarray(t, dtype=np.int32)
     c_out = acc.shape[-1]
     out = np.empty(acc.shape, dtype=np.uint8)
     _load().oracle_codes(_p(acc), acc.size // c_out, c_out, _p(s), _p(t),

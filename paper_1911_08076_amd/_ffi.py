@@ -108,6 +108,7 @@ SIGNATURES = [
     ("ifq_conv_kernel_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc), ctypes.POINTER(Join)]),
     ("ifq_conv_workspace_bytes", size_t, [ctypes.POINTER(ConvDesc)]),
     ("ifq_conv_variant_count", i32, []),
+    ("ifq_conv_variant_fp4", i32, [i32]),
     ("ifq_conv_variant_name", ctypes.c_char_p, [ctypes.POINTER(ConvDesc), ctypes.POINTER(Join),
                                                i32]),
     ("ifq_conv_forward_variant", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp,

@@ -308,6 +308,24 @@ def ifq_conv_variant_count():
     return int(_lib().ifq_conv_variant_count())
 
 
+def ifq_conv_variant_fp4(variant):
+    """1: the variant runs on the fp4 scaled MFMA (takes the fp4 weight
+    blob); 0: int8 MFMA; -1: no such variant."""
+    return int(_lib().ifq_conv_variant_fp4(int(variant)))
+
+
+def kernel_is_fp4(name):
+    """Whether a kernel name (as ifq_conv_kernel_name returns it) is an fp4
+    instance: the fp4 flag true (the windowed kernel's last template
+    argument, conv_w2's ninth, conv_wp's fifth)."""
+    if name.startswith("conv_halo<"):
+        return name.endswith(", true>")
+    for kern, pos in (("conv_w2<", 8), ("conv_wp<", 4)):
+        if name.startswith(kern):
+            return name[len(kern):-1].split(", ")[pos] == "true"
+    return False
+
+
 def ifq_conv_variant_name(desc, join, variant):
     return _lib().ifq_conv_variant_name(
         ctypes.byref(desc), ctypes.byref(join) if join is not None else None,

@@ -15,7 +15,7 @@ LIB = os.path.join(HERE, "libifq.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["ifq_api.cpp", "ifq_conv.hip", "ifq_conv_mfma.hip", "ifq_conv_halo.hip", "ifq_conv_w2.hip", "ifq_noalloc.hip",
+SOURCES = ["ifq_api.cpp", "ifq_conv.hip", "ifq_conv_mfma.hip", "ifq_conv_halo.hip", "ifq_conv_w2.hip", "ifq_conv_wp.hip", "ifq_noalloc.hip",
            "ifq_conv_small.hip", "ifq_pool.hip", "ifq_thresholds.hip"]
 
 

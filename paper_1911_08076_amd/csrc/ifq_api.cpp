@@ -756,7 +756,12 @@ IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d, const ifq_join*
   return ifq::conv_kernel_name(a);
 }
 
-IFQ_API int32_t ifq_conv_variant_count(void) { return ifq::w2_variant_count(); }
+IFQ_API int32_t ifq_conv_variant_count(void) { return ifq::reg3_variant_count(); }
+
+IFQ_API int32_t ifq_conv_variant_fp4(int32_t variant) {
+  if (variant < 0 || variant >= ifq::reg3_variant_count()) return -1;
+  return ifq::reg3_variant_fp4(variant) ? 1 : 0;
+}
 
 IFQ_API const char* ifq_conv_variant_name(const ifq_conv_desc* d, const ifq_join* join,
                                           int32_t variant) {
@@ -764,10 +769,10 @@ IFQ_API const char* ifq_conv_variant_name(const ifq_conv_desc* d, const ifq_join
   if (check_conv(d, &ho, &wo) != IFQ_OK) return "";
   ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, join, nullptr,
                                   nullptr, nullptr);
-  a.f4 = ifq::w2_variant_fp4(variant) ? 1 : 0;
-  ifq::W2Plan p;
-  if (variant < 0 || !ifq::plan_w2(a, variant, &p)) return "";
-  return ifq::conv_w2_name(p, a);
+  a.f4 = ifq::reg3_variant_fp4(variant) ? 1 : 0;
+  ifq::Reg3Plan p;
+  if (variant < 0 || !ifq::plan_reg3(a, variant, &p)) return "";
+  return ifq::reg3_name(p, a);
 }
 
 IFQ_API ifq_status ifq_conv_forward_variant(const ifq_conv_desc* d, const void* x,
@@ -782,16 +787,16 @@ IFQ_API ifq_status ifq_conv_forward_variant(const ifq_conv_desc* d, const void* 
   if (st != IFQ_OK) return st;
   if (d->n == 0) return ok();
   ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_packed, thr, join, sc, y, acc_dump);
-  if (ifq::w2_variant_fp4(variant)) {   // w_packed (and a fused join's down_w): fp4 blobs
+  if (ifq::reg3_variant_fp4(variant)) {   // w_packed (and a fused join's down_w): fp4 blobs
     a.f4 = 1;
     a.rowsum = nullptr;
     a.wzero = fp4_zero_off(ifq::weight_geom(*d));
     if (a.join_kind == IFQ_JOIN_CONV_FUSED) a.d_wzero = fp4_zero_off(ifq::weight_geom(join->down));
   }
-  ifq::W2Plan p;
-  if (variant < 0 || !ifq::plan_w2(a, variant, &p))
+  ifq::Reg3Plan p;
+  if (variant < 0 || !ifq::plan_reg3(a, variant, &p))
     return fail(IFQ_ERR_UNSUPPORTED, "conv variant %d: cannot take this layer", variant);
-  st = hip_status(ifq::launch_conv_w2(a, p, stream), "conv variant launch");
+  st = hip_status(ifq::launch_reg3(a, p, stream), "conv variant launch");
   if (st != IFQ_OK) return st;
   return ok();
 }
@@ -871,8 +876,8 @@ IFQ_API const char* ifq_conv_fp4_kernel_name(const ifq_conv_desc* d, const ifq_j
   ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, join, nullptr,
                                   nullptr, nullptr);
   a.f4 = 1;
-  ifq::W2Plan wp;
-  if (ifq::plan_w2(a, -1, &wp)) return ifq::conv_w2_name(wp, a);
+  ifq::Reg3Plan wp;
+  if (ifq::plan_reg3(a, -1, &wp)) return ifq::reg3_name(wp, a);
   a.f4 = 0;
   ifq::HaloPlan hp;
   if (!fp4_plan(a, &hp)) return "";
@@ -891,18 +896,18 @@ IFQ_API ifq_status ifq_conv_forward_fp4(const ifq_conv_desc* d, const void* x,
   if (st != IFQ_OK) return st;
   ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_fp4, thr, join, sc, y, nullptr);
   if (d->n == 0) return ok();
-  // the register-blocked kernel's fp4 instances where they take the layer
+  // the register-blocked kernels' fp4 instances where they take the layer
   // (thresholds or an identity join), else the windowed kernel's
-  ifq::W2Plan wp;
+  ifq::Reg3Plan wp;
   {
     ifq::ConvLaunch f = a;
     f.f4 = 1;
-    if (ifq::plan_w2(f, -1, &wp)) {
+    if (ifq::plan_reg3(f, -1, &wp)) {
       f.rowsum = nullptr;
       f.wzero = fp4_zero_off(ifq::weight_geom(*d));
       if (f.join_kind == IFQ_JOIN_CONV_FUSED)   // join->down_w is the down conv's fp4 blob
         f.d_wzero = fp4_zero_off(ifq::weight_geom(join->down));
-      st = hip_status(ifq::launch_conv_w2(f, wp, stream), "conv fp4 launch");
+      st = hip_status(ifq::launch_reg3(f, wp, stream), "conv fp4 launch");
       if (st != IFQ_OK) return st;
       return ok();
     }

@@ -375,20 +375,20 @@ bool mfma_eligible(const ConvLaunch& a) {
 // A fused downsample join runs only in the windowed 3x3 kernel (the host
 // checks plan_halo succeeds before launching one).
 // The fast path picks the kernel with the lowest predicted time (plan_time)
-// among the register-blocked 3x3 kernel, the windowed 3x3 kernel and the
-// tiled kernel. A fused downsample join runs only in the windowed kernel
+// among the register-blocked 3x3 kernels (one tile per workgroup or
+// persistent), the windowed 3x3 kernel and the tiled kernel. A fused downsample join runs only in the windowed kernel
 // (the host checks plan_halo succeeds before launching one).
 const char* conv_mfma_name(const ConvLaunch& a) {
   HaloPlan hp;
   const bool halo = plan_halo(a, &hp);
-  W2Plan wp;
-  const bool w2 = plan_w2(a, -1, &wp);
+  Reg3Plan rp;
+  const bool r3 = plan_reg3(a, -1, &rp);
   if (a.join_kind == IFQ_JOIN_CONV_FUSED) {
-    if (w2 && (!halo || wp.t_us <= hp.t_us)) return conv_w2_name(wp, a);
+    if (r3 && (!halo || rp.t_us <= hp.t_us)) return reg3_name(rp, a);
     return halo ? conv_halo_name(hp, a) : "";
   }
   const Plan pl = plan_mfma(a);
-  if (w2 && wp.t_us <= pl.t_us && (!halo || wp.t_us <= hp.t_us)) return conv_w2_name(wp, a);
+  if (r3 && rp.t_us <= pl.t_us && (!halo || rp.t_us <= hp.t_us)) return reg3_name(rp, a);
   if (halo && hp.t_us < pl.t_us) return conv_halo_name(hp, a);
   return kVariants[pl.variant].name;
 }
@@ -396,15 +396,15 @@ const char* conv_mfma_name(const ConvLaunch& a) {
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream) {
   HaloPlan hp;
   const bool halo = plan_halo(a, &hp);
-  W2Plan wp;
-  const bool w2 = plan_w2(a, -1, &wp);
+  Reg3Plan rp;
+  const bool r3 = plan_reg3(a, -1, &rp);
   if (a.join_kind == IFQ_JOIN_CONV_FUSED) {
-    if (w2 && (!halo || wp.t_us <= hp.t_us)) return launch_conv_w2(a, wp, stream);
+    if (r3 && (!halo || rp.t_us <= hp.t_us)) return launch_reg3(a, rp, stream);
     return halo ? launch_conv_halo(a, hp, stream) : hipErrorNotSupported;
   }
   const Plan pl = plan_mfma(a);
-  if (w2 && wp.t_us <= pl.t_us && (!halo || wp.t_us <= hp.t_us))
-    return launch_conv_w2(a, wp, stream);
+  if (r3 && rp.t_us <= pl.t_us && (!halo || rp.t_us <= hp.t_us))
+    return launch_reg3(a, rp, stream);
   if (halo && hp.t_us < pl.t_us) return launch_conv_halo(a, hp, stream);
   switch (pl.variant) {
     case 0: return launch_variant<2, 4, 1, 2, 4, 1, 6>(a, pl, stream);

@@ -583,13 +583,15 @@ const W2Variant kW2Variants[] = {
     {1, 8, 1, 2, 1, 3, 3, 2, 20480, false, 0.23, 0.27, IFQ_W2_NAMES(1, 8, 1, 2, 1, 3, 3, false, 2, 20480)},
     {2, 4, 1, 2, 2, 1, 3, 2, 24576, false, 2.0, 0.475, IFQ_W2_NAMES(2, 4, 1, 2, 2, 1, 3, false, 2, 24576)},
     // the same tiles on the fp4 scaled MFMA (half the weight bytes per K64
-    // step: a stage holds three times the taps)
-    {2, 4, 1, 2, 2, 9, 2, 1, 49152, true, 4.4, 0.69, IFQ_W2_NAMES(2, 4, 1, 2, 2, 9, 2, true, 1, 49152)},
-    {1, 4, 2, 2, 2, 9, 2, 1, 53248, true, 3.8, 0.73, IFQ_W2_NAMES(1, 4, 2, 2, 2, 9, 2, true, 1, 53248)},
-    {1, 2, 4, 2, 2, 3, 2, 1, 36864, true, 3.5, 0.60, IFQ_W2_NAMES(1, 2, 4, 2, 2, 3, 2, true, 1, 36864)},
-    {1, 4, 1, 2, 2, 9, 2, 2, 20480, true, 1.0, 0.335, IFQ_W2_NAMES(1, 4, 1, 2, 2, 9, 2, true, 2, 20480)},
+    // step: a stage holds three times the taps); eff against twice the int8
+    // rate
+    {2, 4, 1, 2, 2, 9, 2, 1, 49152, true, 4.4, 0.67, IFQ_W2_NAMES(2, 4, 1, 2, 2, 9, 2, true, 1, 49152)},
+    {1, 4, 2, 2, 2, 9, 2, 1, 53248, true, 3.8, 0.61, IFQ_W2_NAMES(1, 4, 2, 2, 2, 9, 2, true, 1, 53248)},
+    {1, 2, 4, 2, 2, 3, 2, 1, 36864, true, 3.5, 0.46, IFQ_W2_NAMES(1, 2, 4, 2, 2, 3, 2, true, 1, 36864)},
+    {1, 4, 1, 2, 2, 9, 2, 2, 20480, true, 1.0, 0.21, IFQ_W2_NAMES(1, 4, 1, 2, 2, 9, 2, true, 2, 20480)},
 };
 constexpr int kNumW2 = sizeof(kW2Variants) / sizeof(kW2Variants[0]);
+constexpr double kW2IdjRoundUs = 1.0;
 constexpr int kW2CUs = 256;
 
 // Upper bound of the window cells (rounded per image to 64) one tile of bn
@@ -646,8 +648,11 @@ bool w2_fit(const ConvLaunch& a, int v, W2Plan* out) {
   const int64_t cells = w2_cells_bound(a, bn);
   if ((int64_t)G * (cells + 1) * 16 > V.winb) return false;
   const int64_t blocks = nco * ((a.m + bn - 1) / bn);
+  // the identity join's table epilogue and shortcut cells: about 1 us more
+  // per round of tiles (measured on the ResNet-18-shaped stack's blocks)
+  const double c0 = V.c0_us + (a.join_kind == IFQ_JOIN_IDENTITY ? kW2IdjRoundUs : 0.0);
   const double t = plan_time(blocks, (V.f4 ? 1.0 : 2.0) * bm * bnmax * (double)a.kpad, V.occ,
-                             V.c0_us, V.eff);
+                             c0, V.eff);
   *out = W2Plan{v, (int)bn, (int)((a.m + bn - 1) / bn), (int)cells, t};
   return true;
 }

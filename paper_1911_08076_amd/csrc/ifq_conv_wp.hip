@@ -1,0 +1,584 @@
+// Persistent 3x3 kernel for layers whose weight slab of one 64-channel
+// output slice fits in LDS (3x3, stride 1 or 2, pad 1, 2-bit BLOCK64 codes,
+// c_in a multiple of 64), on gfx950 (MI355X). The contraction and epilogues
+// are those of the register-blocked kernel in ifq_conv_w2.hip: the integer
+// part of Eq. (1) on v_mfma_i32_32x32x32_i8 (or exactly on the fp4 scaled
+// MFMA, F4), then the 2-bit threshold epilogue of Eq. (7)/(8) (MODE 0) or the
+// identity residual join (MODE 1).
+//
+// Layers with many output pixels and a short K (the 56x56 64-channel layers
+// of a ResNet-18 body: K = 576, about three 64x256 tiles per CU) spend most
+// of a one-tile-per-workgroup kernel in each tile's prologue and epilogue.
+// Here a workgroup loads the weights of its channel slice into LDS once and
+// then runs a contiguous range of pixel tiles:
+//  - a tile's main loop reads weights and input window from LDS only: no
+//    waits and no barriers inside it;
+//  - the window (and the identity join's shortcut cells) of the next tile
+//    load into the other half of a double buffer while the current tile's
+//    main loop and epilogue run;
+//  - the output tile is double-buffered too, so one barrier per tile
+//    separates every producer from its consumer;
+//  - two workgroups share a CU, so one's epilogue (VALU) can overlap the
+//    other's MFMAs.
+#include <hip/hip_runtime.h>
+
+#include "ifq_epilogue.h"
+#include "ifq_internal.h"
+#include "ifq_mfma_common.h"
+
+namespace ifq {
+namespace {
+
+constexpr int kWpTaps = 9;
+
+__host__ __device__ constexpr int wp_round64(int v) { return (v + 63) & ~63; }
+
+// The images (segments) the output pixels [p0, p0 + bn) of a tile touch and
+// the input row span of each (the window layout of ifq_conv_w2.hip: per
+// channel block, each segment's rows of cells rounded up to 64 cells).
+struct WpTile {
+  int n_first, nseg, oy_first, oy_last;
+  __device__ void init(const ConvLaunch& a, int p0, int bn) {
+    const int howo = a.ho * a.wo;
+    const int pend = (p0 + bn < a.m ? p0 + bn : a.m) - 1;
+    n_first = fdiv(p0, a.div_howo);
+    const int n_last = fdiv(pend, a.div_howo);
+    nseg = n_last - n_first + 1;
+    oy_first = fdiv(p0 - n_first * howo, a.div_wo);
+    oy_last = fdiv(pend - n_last * howo, a.div_wo);
+  }
+  __device__ int rows(const ConvLaunch& a, int i, int& iya) const {
+    const int oya = i == 0 ? oy_first : 0;
+    const int oyb = i == nseg - 1 ? oy_last : a.ho - 1;
+    iya = oya * a.stride - 1;
+    iya = iya < 0 ? 0 : iya;
+    int iyb = oyb * a.stride + 1;
+    iyb = iyb > a.h - 1 ? a.h - 1 : iyb;
+    return iyb - iya + 1;
+  }
+};
+
+template <int WN, int FM, int FN, int MODE, bool F4, int OCC, int WGTB, int WINB>
+__global__ __launch_bounds__(64 * WN, (WN / 4) * OCC) void conv_wp(ConvLaunch a) {
+  constexpr bool SW = MODE == 0;                 // transposed sums
+  constexpr int NW = WN;
+  constexpr int BM = 32 * FM;
+  constexpr int BN = 32 * FN * WN;
+  constexpr int KH = F4 ? 1 : 2;                 // 1 KB chunks per row block and K64 step
+  constexpr int RB = FM;
+  static_assert(NW % 4 == 0 && BM == 64, "waves; one 64-channel slice per workgroup");
+  // LDS: the slice's weights, two windows, the per-channel records, two
+  // shortcut buffers (identity join), two output tiles. The identity join's
+  // raw records are only read while the packed ones are staged, before the
+  // second window is first written: they sit in that window.
+  constexpr int WGT = 0;
+  constexpr int WIN = WGTB;
+  constexpr int TBL = SW ? WIN + 2 * WINB : WIN + WINB;
+  constexpr int TBL_BYTES = SW ? BM * 16 : 0;
+  static_assert(SW || BM * 64 <= WINB, "raw join records inside the second window");
+  constexpr int EPI = WIN + 2 * WINB + TBL_BYTES;   // past both windows
+  constexpr int EPI_BYTES = SW ? 0 : BM * 128;
+  constexpr int SCB = EPI + EPI_BYTES;
+  constexpr int SC_BYTES = SW ? 0 : (BM / 64) * BN * 16;
+  constexpr int OTL = SCB + 2 * SC_BYTES;
+  constexpr int OUT_BYTES = BN * BM / 4;
+  constexpr int LDS_BYTES = OTL + 2 * OUT_BYTES;
+  static_assert(LDS_BYTES <= 160 * 1024 / OCC, "LDS");
+
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS_BYTES];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wn = wave;
+  const int h = lane >> 5;
+  const int l32 = lane & 31;
+  const int bn = a.bn;
+  const int co0 = blockIdx.y * BM;
+  const int G = a.cin >> 6;
+  const int H = a.h, W = a.w, Wo = a.wo, st = a.stride;
+  const int howo = a.ho * a.wo;
+  const int HW = H * W;
+  const int wcells = a.wcells;                   // host: the largest tile window
+  const int wstr = (wcells + 1) * 16;            // block window + its zero cell
+  const int ntm = (a.m + bn - 1) / bn;
+  const int t_begin = blockIdx.x * a.tiles_wg;
+  const int t_end = t_begin + a.tiles_wg < ntm ? t_begin + a.tiles_wg : ntm;
+  const uint32_t lds0 = lds_addr(lds);
+  const uint8_t* zero_src = reinterpret_cast<const uint8_t*>(&g_zero_cell);
+  constexpr int orow = BM / 4;
+
+  // the window of tile tt into window buffer b: chunk j of segment i is 64
+  // cells of that image's input rows, the same chunk for every channel block;
+  // wave w takes the chunks w, w + NW, .. of the segments' chunk list
+  auto load_window = [&](int tt, int b) {
+    WpTile tl;
+    tl.init(a, tt * bn, bn);
+    const uint32_t dst0 = lds0 + WIN + b * WINB;
+    int off = 0, jbase = 0;
+    for (int i = 0; i < tl.nseg; ++i) {
+      int iya;
+      const int cells = tl.rows(a, i, iya) * W;
+      const int nch = wp_round64(cells) >> 6;
+      int j = wave - jbase;
+      j += j < 0 ? ((-j + NW - 1) / NW) * NW : 0;
+      for (; j < nch; j += NW) {
+        const int c = j * 64 + lane;
+        const int64_t src = ((int64_t)(tl.n_first + i) * G * HW + iya * W + c) * 16;
+        for (int g = 0; g < G; ++g)
+          dma16(c < cells ? a.x + src + (int64_t)g * HW * 16 : zero_src,
+                dst0 + (uint32_t)(g * wstr + (off + j * 64) * 16));
+      }
+      jbase += nch;
+      off += wp_round64(cells);
+    }
+  };
+  // the shortcut cells of tile tt's pixels (identity join) into buffer b
+  auto load_shortcut = [&](int tt, int b) {
+    const int p0 = tt * bn;
+    const uint8_t* sc8 = reinterpret_cast<const uint8_t*>(a.shortcut);
+    const int ncx = (bn + 63) >> 6;
+    for (int q = wave; q < (BM / 64) * ncx; q += NW) {
+      const int gbl = q / ncx, j = q - gbl * ncx;
+      const int pl = j * 64 + lane, p = p0 + pl, gb = (co0 >> 6) + gbl;
+      const uint8_t* src = zero_src;
+      if (pl < bn && p < a.m && gb * 64 < a.cout) {
+        if (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64) {
+          const int nimg = fdiv(p, a.div_howo);
+          src = sc8 + (((int64_t)nimg * (a.cout >> 6) + gb) * howo + (p - nimg * howo)) * 16;
+        } else {
+          src = sc8 + ((int64_t)p * a.cout + gb * 64) / 4;
+        }
+      }
+      dma16(src, lds0 + SCB + (uint32_t)(b * SC_BYTES + (gbl * BN + j * 64) * 16));
+    }
+  };
+
+  // ---- prologue: records, weights, the first tile's window and shortcut ---
+  if constexpr (SW) {
+    for (int q = wave; q < BM / 64; q += NW) {
+      const int c = co0 + q * 64 + lane;
+      dma16(c < a.cout ? reinterpret_cast<const uint8_t*>(a.thr + (int64_t)c * 4) : zero_src,
+            lds0 + TBL + q * 1024);
+    }
+  } else {
+    for (int q = wave; q < BM / 16; q += NW) {   // 16 channels x 64 B per chunk
+      const int c = co0 + q * 16 + (lane >> 2);
+      dma16(c < a.cout ? reinterpret_cast<const uint8_t*>(a.table + (int64_t)c * 16 + (lane & 3) * 4)
+                       : zero_src,
+            lds0 + TBL + q * 1024);
+    }
+  }
+  {
+    // weight chunk c = (kk*RB + rb)*KH + t of K64 step kk = g*9 + tap
+    const int nrb = a.cout_pad >> 5;
+    const int rbw = co0 >> 5;
+    const uint8_t* wbase = reinterpret_cast<const uint8_t*>(a.wgt);
+    const uint32_t voff = (uint32_t)lane * 16;
+    const int nch = G * kWpTaps * RB * KH;
+    for (int c = wave; c < nch; c += NW) {
+      const int t = c % KH, rb = (c / KH) % RB, kk = c / (KH * RB);
+      const int64_t off =
+          rbw + rb < nrb ? ((int64_t)(rbw + rb) * (KH * a.nk) + KH * kk + t) * 1024 : a.wzero;
+      dma16s(wbase + off, voff, lds0 + WGT + (uint32_t)(c * 1024));
+    }
+  }
+  if (t_begin < t_end) {
+    load_window(t_begin, 0);
+    if constexpr (!SW) load_shortcut(t_begin, 0);
+  }
+  // zero cell after every block window (the second window's, for the
+  // identity join, once its raw records are staged)
+  for (int g = tid; g < G * (SW ? 2 : 1); g += 64 * NW) {
+    const int b = g / G, gg = g - b * G;
+    *reinterpret_cast<uint4*>(lds + WIN + b * WINB + gg * wstr + wcells * 16) = uint4{0, 0, 0, 0};
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+  if constexpr (!SW) {
+    stage_idj_pk(reinterpret_cast<const int32_t*>(lds + TBL), lds + EPI, BM,
+                 a.cout - co0 < BM ? a.cout - co0 : BM);
+    __syncthreads();
+    // ordered before the second window's first read by the first tile's
+    // barrier
+    for (int g = tid; g < G; g += 64 * NW)
+      *reinterpret_cast<uint4*>(lds + WIN + WINB + g * wstr + wcells * 16) = uint4{0, 0, 0, 0};
+  }
+
+  struct Frag {
+    v4i af[KH][FM];
+    v2i braw[FN];
+  };
+  // Tile i (buffer b = i & 1): issue the next tile's window and shortcut
+  // into buffer b ^ 1 (last read by tile i - 1, before its barrier), run the
+  // main loop on window b, the epilogue into output tile b, wait for this
+  // wave's loads, barrier, then write output tile b to HBM (output tile b is
+  // next written by tile i + 2, after tile i + 1's barrier).
+  int b = 0;
+  for (int tile = t_begin; tile < t_end; ++tile, b ^= 1) {
+    const int p0 = tile * bn;
+    if (tile + 1 < t_end) {
+      load_window(tile + 1, b ^ 1);
+      if constexpr (!SW) load_shortcut(tile + 1, b ^ 1);
+    }
+    // ---- per-lane LDS offsets of the nine taps of each pixel block -------
+    int boff[FN][kWpTaps];
+    {
+      WpTile tl;
+      tl.init(a, p0, bn);
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) {
+        const int pl = (wn * FN + fn) * 32 + l32;
+        const int p = p0 + pl;
+        const bool pok = pl < bn && p < a.m;
+        int my_off = 0, my_iya = 0, oy = 0, ox = 0;
+        if (pok) {
+          const int n = fdiv(p, a.div_howo);
+          const int rem = p - n * howo;
+          oy = fdiv(rem, a.div_wo);
+          ox = rem - oy * Wo;
+          int off = 0;
+          for (int i = 0; i < tl.nseg; ++i) {
+            int iya;
+            const int rows = tl.rows(a, i, iya);
+            if (i == n - tl.n_first) {
+              my_off = off;
+              my_iya = iya;
+            }
+            off += wp_round64(rows * W);
+          }
+        }
+#pragma unroll
+        for (int r = 0; r < 3; ++r)
+#pragma unroll
+          for (int s = 0; s < 3; ++s) {
+            const int iy = oy * st - 1 + r;
+            const int ix = ox * st - 1 + s;
+            const bool ok = pok && (unsigned)iy < (unsigned)H && (unsigned)ix < (unsigned)W;
+            boff[fn][r * 3 + s] =
+                (ok ? (my_off + (iy - my_iya) * W + ix) * 16 : wcells * 16) + 8 * h;
+          }
+      }
+    }
+
+    // ---- main loop: every tap of every channel block, operands in LDS ----
+    v16i acc[FM][FN];
+    v16f accf[F4 ? FM : 1][F4 ? FN : 1];
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn) acc[fm][fn] = v16i{0};
+#pragma unroll
+    for (int fm = 0; fm < (F4 ? FM : 1); ++fm)
+#pragma unroll
+      for (int fn = 0; fn < (F4 ? FN : 1); ++fn) accf[fm][fn] = v16f{0.0f};
+    const uint8_t* winb = lds + WIN + b * WINB;
+    auto read_frags = [&](int g, int tap, Frag& F) {
+      const uint8_t* as = lds + WGT + (g * kWpTaps + tap) * RB * KH * 1024;
+      const uint8_t* win = winb + g * wstr;
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int t = 0; t < KH; ++t)
+          F.af[t][fm] = *reinterpret_cast<const v4i*>(as + (fm * KH + t) * 1024 + lane * 16);
+#pragma unroll
+      for (int fn = 0; fn < FN; ++fn)
+        F.braw[fn] = *reinterpret_cast<const v2i*>(win + boff[fn][tap]);
+    };
+    // B operands: int8 bytes of the 2-bit codes per K32 half and pixel
+    // block, or the codes as fp4 nibbles (the order of the fp4 weight blob)
+    struct Unp {
+      v4i b4[F4 ? 1 : 2][FN];
+      v8i b8[F4 ? FN : 1];
+    };
+    constexpr int kGroups = KH * FN;   // MFMA groups of a tap: one B operand, FM MFMAs
+    // piece k of the unpack: group k's B operand
+    auto unpack_piece = [&](const Frag& F, Unp& U, int k) {
+      const int t = k / FN, fn = k % FN;
+      if constexpr (F4) {
+        const uint32_t w0 = (uint32_t)F.braw[fn][0], w1 = (uint32_t)F.braw[fn][1];
+        U.b8[fn] = v8i{(int)(w0 & 0x33333333u), (int)((w0 >> 2) & 0x33333333u),
+                       (int)(w1 & 0x33333333u), (int)((w1 >> 2) & 0x33333333u), 0, 0, 0, 0};
+      } else {
+        U.b4[t][fn] = unpack2((uint32_t)F.braw[fn][t]);
+      }
+    };
+    auto mfma_group = [&](const Frag& F, const Unp& U, int k) {
+      const int t = k / FN, fn = k % FN;
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) {
+        if constexpr (F4) {
+          const v4i w = F.af[0][fm];
+          const v8i af = v8i{w.x, w.y, w.z, w.w, 0, 0, 0, 0};
+          if constexpr (SW)
+            accf[fm][fn] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                U.b8[fn], af, accf[fm][fn], 4, 4, 0, 127, 0, 127);
+          else
+            accf[fm][fn] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                af, U.b8[fn], accf[fm][fn], 4, 4, 0, 127, 0, 127);
+        } else {
+          if constexpr (SW)
+            acc[fm][fn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(U.b4[t][fn], F.af[t][fm],
+                                                                acc[fm][fn], 0, 0, 0);
+          else
+            acc[fm][fn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(F.af[t][fm], U.b4[t][fn],
+                                                                acc[fm][fn], 0, 0, 0);
+        }
+      }
+    };
+    // Software pipeline over the taps: during tap i's MFMA groups the
+    // fragments of tap i + 1 arrive from LDS and their B operands are
+    // unpacked, one piece after each group from the second on, so the VALU
+    // work runs while the MFMAs queued before it execute. Scheduling
+    // barriers keep that order (the scheduler would otherwise sink each read
+    // and unpack to its first use and expose the LDS latency).
+    // MFMA phases run at raised wave priority: where the other workgroup on
+    // the CU is in its epilogue, its VALU work fills the issue slots this
+    // loop leaves and the two drift into complementary phases.
+    __builtin_amdgcn_s_setprio(1);
+    for (int g = 0; g < G; ++g) {
+      Frag f[2];
+      Unp u[2];
+      read_frags(g, 0, f[0]);
+#pragma unroll
+      for (int k = 0; k < kGroups; ++k) unpack_piece(f[0], u[0], k);
+#pragma unroll
+      for (int tap = 0; tap < kWpTaps; ++tap) {
+        const int c = tap & 1;
+        const bool nxt = tap + 1 < kWpTaps;
+        if (nxt) read_frags(g, tap + 1, f[c ^ 1]);
+#pragma unroll
+        for (int k = 0; k < kGroups; ++k) {
+          __builtin_amdgcn_sched_barrier(0);
+          mfma_group(f[c], u[c], k);
+          __builtin_amdgcn_sched_barrier(0);
+          if (nxt && k >= 1) unpack_piece(f[c ^ 1], u[c ^ 1], k - 1);
+        }
+        if (nxt) unpack_piece(f[c ^ 1], u[c ^ 1], kGroups - 1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    __builtin_amdgcn_s_setprio(0);
+    if constexpr (F4) {
+      // exact integers (every partial sum is an integer below 2^24)
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < FN; ++fn)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) acc[fm][fn][i] = (int)accf[fm][fn][i];
+    }
+
+    // ---- epilogue into output tile b --------------------------------------
+    uint8_t* otile = lds + OTL + b * OUT_BYTES;
+#pragma unroll
+    for (int q = 0; q < FM * FN; ++q) {
+      const int fm = q / FN, fn = q % FN;
+      const int pcb = wn * FN + fn;
+      const v16i one[1] = {acc[fm][fn]};
+      if constexpr (SW) {
+        if (a.acc_dump) dump_acc_t<1>(a, one, fm, h, l32, co0, p0, pcb * 32, bn, a.acc_dump);
+        epilogue_thr_pk_t<1>(a, reinterpret_cast<const int4*>(lds + TBL), one, fm, h, l32, co0,
+                             pcb * 32, otile, orow);
+      } else {
+        if (a.acc_dump) {
+          const v16i one2[1][1] = {{acc[fm][fn]}};
+          epilogue32<kE32I32, 1, 1>(a, lds + EPI, one2, fm, pcb, h, l32, co0, p0, bn, otile,
+                                    orow, a.acc_dump);
+        }
+        const int pl = pcb * 32 + l32;
+        const int cl = fm * 32;
+        const uint2 sc[1] = {*reinterpret_cast<const uint2*>(
+            lds + SCB + b * SC_BYTES + (((cl >> 6) * BN + pl) * 16) + ((cl & 63) >> 2))};
+        epilogue_idj_pk<1>(a, lds + EPI, one, sc, fm, h, co0, pl, otile, orow);
+      }
+    }
+    wait_vmcnt<0>();
+    __syncthreads();
+    copy_out_tile(a, otile, orow, co0, BM, p0, a.m - p0 < bn ? a.m - p0 : bn);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Variants and planning
+// ---------------------------------------------------------------------------
+struct WpVariant {
+  int wn, fm, fn, occ, wgtb, winb_thr, winb_idj;
+  bool f4;
+  const char* thr_name;
+  const char* idj_name;
+};
+// Fitted to kernel times measured on MI355X (the ResNet-18-shaped stack's
+// 64-channel layers, int8 and fp4, and its 128-channel layers on fp4): a
+// fixed cost per workgroup (prologue, launch ramp), per tile (window and
+// tap offsets, epilogue, copy-out; more for the identity join's table
+// epilogue) and the main loop's MFMA efficiency.
+constexpr double kWpWgUs = 1.3;
+constexpr double kWpTileUs = 3.6;
+constexpr double kWpTileIdjUs = 4.7;
+constexpr double kWpEff = 0.95;
+
+#define IFQ_WP_NAME(wn, fm, fn, mode, f4, occ, wgtb, winb) \
+  "conv_wp<" #wn ", " #fm ", " #fn ", " #mode ", " #f4 ", " #occ ", " #wgtb ", " #winb ">"
+
+// Index order must match the switch in launch_conv_wp.
+const WpVariant kWpVariants[] = {
+    {4, 2, 2, 2, 36864, 16384, 10240, false,
+     IFQ_WP_NAME(4, 2, 2, 0, false, 2, 36864, 16384),
+     IFQ_WP_NAME(4, 2, 2, 1, false, 2, 36864, 10240)},
+    {4, 2, 2, 2, 36864, 16384, 10240, true,
+     IFQ_WP_NAME(4, 2, 2, 0, true, 2, 36864, 16384),
+     IFQ_WP_NAME(4, 2, 2, 1, true, 2, 36864, 10240)},
+};
+constexpr int kNumWp = sizeof(kWpVariants) / sizeof(kWpVariants[0]);
+
+// The largest window (cells per channel block, each image's rows rounded up
+// to 64 cells) over the layer's tiles of bn pixels, or -1 past `limit`.
+int64_t wp_cells_max(const ConvLaunch& a, int64_t bn, int64_t limit) {
+  const int64_t howo = (int64_t)a.ho * a.wo;
+  int64_t mx = 0;
+  for (int64_t p0 = 0; p0 < a.m; p0 += bn) {
+    const int64_t pend = (p0 + bn < a.m ? p0 + bn : a.m) - 1;
+    const int64_t nf = p0 / howo, nl = pend / howo;
+    const int64_t oyf = (p0 - nf * howo) / a.wo, oyl = (pend - nl * howo) / a.wo;
+    int64_t tot = 0;
+    for (int64_t i = 0; i <= nl - nf; ++i) {
+      const int64_t oya = i == 0 ? oyf : 0, oyb = i == nl - nf ? oyl : a.ho - 1;
+      int64_t iya = oya * a.stride - 1, iyb = oyb * a.stride + 1;
+      if (iya < 0) iya = 0;
+      if (iyb > a.h - 1) iyb = a.h - 1;
+      tot += wp_round64((int)((iyb - iya + 1) * a.w));
+    }
+    if (tot > mx) mx = tot;
+    if (mx > limit) return -1;
+  }
+  return mx;
+}
+
+bool wp_fit(const ConvLaunch& a, int v, WpPlan* out) {
+  const WpVariant& V = kWpVariants[v];
+  if (V.f4 != (a.f4 != 0)) return false;
+  const int G = a.cin / 64;
+  const int bm = 32 * V.fm, bn = 32 * V.fn * V.wn;
+  const int kh = V.f4 ? 1 : 2;
+  if ((int64_t)G * kWpTaps * (bm / 32) * kh * 1024 > V.wgtb) return false;
+  const int winb = a.join_kind == IFQ_JOIN_IDENTITY ? V.winb_idj : V.winb_thr;
+  const int64_t cells = wp_cells_max(a, bn, (int64_t)winb / 16);
+  if (cells < 0 || (int64_t)G * (cells + 1) * 16 > winb) return false;
+  const int64_t nco = (a.cout + bm - 1) / bm;
+  const int64_t ntm = (a.m + bn - 1) / bn;
+  const int64_t slots = (int64_t)kPlanCUs * V.occ;
+  const int64_t per = (nco * ntm + slots - 1) / slots;     // tiles per workgroup
+  const int64_t gx = (ntm + per - 1) / per;
+  // the busiest CU: up to occ workgroups of per tiles each
+  int64_t wgs_cu = (nco * gx + kPlanCUs - 1) / kPlanCUs;
+  if (wgs_cu > V.occ) wgs_cu = V.occ;
+  const double tile_us = (V.f4 ? 1.0 : 2.0) * bm * bn * (double)a.kpad / kCuOpsPerUsInt8;
+  const double c_tile = a.join_kind == IFQ_JOIN_IDENTITY ? kWpTileIdjUs : kWpTileUs;
+  const double t = kLaunchUs + kWpWgUs + (double)per * ((double)wgs_cu * tile_us / kWpEff + c_tile);
+  *out = WpPlan{v, bn, (int)gx, (int)per, (int)cells, t};
+  return true;
+}
+
+bool wp_mode_ok(const ConvLaunch& a) {
+  if (!(a.out_mode == 2 && a.rec == 4 && (a.cout & 31) == 0 && 27 * a.cin <= 32766 &&
+        a.pool_k == 0))
+    return false;
+  if (a.join_kind == IFQ_JOIN_NONE) return true;
+  return a.join_kind == IFQ_JOIN_IDENTITY && a.cout % 64 == 0 &&
+         (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64 || a.sc_layout == IFQ_LAYOUT_U2_NHWC_PACKED);
+}
+
+}  // namespace
+
+int wp_variant_count() { return kNumWp; }
+bool wp_variant_fp4(int v) { return v >= 0 && v < kNumWp && kWpVariants[v].f4; }
+
+bool plan_wp(const ConvLaunch& a, int forced, WpPlan* out) {
+  if (!(a.in_layout == IFQ_LAYOUT_U2_BLOCK64 && a.in_bits == 2 && a.cin % 64 == 0 &&
+        a.kh == 3 && a.kw == 3 && a.pad == 1 && (a.stride == 1 || a.stride == 2) && a.m > 0))
+    return false;
+  if (!wp_mode_ok(a)) return false;
+  // 32-bit cell indices and offsets
+  if ((int64_t)a.n * a.h * a.w * (a.cin / 64) >= (int64_t)1 << 26) return false;
+  if (forced >= 0) return forced < kNumWp && wp_fit(a, forced, out);
+  bool found = false;
+  for (int v = 0; v < kNumWp; ++v) {
+    WpPlan p;
+    if (wp_fit(a, v, &p) && (!found || p.t_us < out->t_us)) {
+      *out = p;
+      found = true;
+    }
+  }
+  return found;
+}
+
+const char* conv_wp_name(const WpPlan& p, const ConvLaunch& a) {
+  const WpVariant& V = kWpVariants[p.variant];
+  return a.join_kind == IFQ_JOIN_IDENTITY ? V.idj_name : V.thr_name;
+}
+
+hipError_t launch_conv_wp(ConvLaunch a, const WpPlan& p, hipStream_t stream) {
+  a.bn = p.bn;
+  a.wcells = p.wcells;
+  a.tiles_wg = p.per;
+  const WpVariant& V = kWpVariants[p.variant];
+  const int bm = 32 * V.fm;
+  const dim3 grid(p.gx, (a.cout + bm - 1) / bm);
+  const dim3 block(64 * V.wn);
+  const int mode = a.join_kind == IFQ_JOIN_IDENTITY ? 1 : 0;
+  switch (p.variant * 2 + mode) {
+#define IFQ_WP_CASE(k, wn, fm, fn, f4, occ, wgtb, winbt, winbi)                             \
+  case 2 * k:                                                                               \
+    hipLaunchKernelGGL((conv_wp<wn, fm, fn, 0, f4, occ, wgtb, winbt>), grid, block, 0,      \
+                       stream, a);                                                          \
+    break;                                                                                  \
+  case 2 * k + 1:                                                                           \
+    hipLaunchKernelGGL((conv_wp<wn, fm, fn, 1, f4, occ, wgtb, winbi>), grid, block, 0,      \
+                       stream, a);                                                          \
+    break;
+    IFQ_WP_CASE(0, 4, 2, 2, false, 2, 36864, 16384, 10240)
+    IFQ_WP_CASE(1, 4, 2, 2, true, 2, 36864, 16384, 10240)
+#undef IFQ_WP_CASE
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// ---- the register-blocked family ------------------------------------------
+int reg3_variant_count() { return w2_variant_count() + wp_variant_count(); }
+
+bool reg3_variant_fp4(int v) {
+  return v < w2_variant_count() ? w2_variant_fp4(v) : wp_variant_fp4(v - w2_variant_count());
+}
+
+bool plan_reg3(const ConvLaunch& a, int forced, Reg3Plan* out) {
+  const int n2 = w2_variant_count();
+  if (forced >= 0) {
+    out->persistent = forced >= n2;
+    if (forced < n2) {
+      if (!plan_w2(a, forced, &out->w2)) return false;
+      out->t_us = out->w2.t_us;
+    } else {
+      if (!plan_wp(a, forced - n2, &out->wp)) return false;
+      out->t_us = out->wp.t_us;
+    }
+    return true;
+  }
+  const bool w2 = plan_w2(a, -1, &out->w2);
+  const bool wp = plan_wp(a, -1, &out->wp);
+  if (!w2 && !wp) return false;
+  out->persistent = wp && (!w2 || out->wp.t_us < out->w2.t_us);
+  out->t_us = out->persistent ? out->wp.t_us : out->w2.t_us;
+  return true;
+}
+
+hipError_t launch_reg3(const ConvLaunch& a, const Reg3Plan& p, hipStream_t stream) {
+  return p.persistent ? launch_conv_wp(a, p.wp, stream) : launch_conv_w2(a, p.w2, stream);
+}
+
+const char* reg3_name(const Reg3Plan& p, const ConvLaunch& a) {
+  return p.persistent ? conv_wp_name(p.wp, a) : conv_w2_name(p.w2, a);
+}
+
+}  // namespace ifq

@@ -128,7 +128,8 @@ struct ConvLaunch {
   int32_t pho, pwo;
   FastDiv div_pwo;     // division by pwo (pooled pixel -> pooled row)
   FastDiv div_pho;     // division by pho (pooled row -> image)
-  int32_t wcells;      // register-blocked 3x3 kernel: window cells per channel block
+  int32_t wcells;      // register-blocked 3x3 kernels: window cells per channel block
+  int32_t tiles_wg;    // persistent 3x3 kernel: consecutive pixel tiles per workgroup
 };
 
 // Whether the pooled epilogue takes this launch: codes out (no join), and
@@ -196,6 +197,39 @@ bool w2_variant_fp4(int v);   // variant v runs the fp4 contraction (fp4 weight 
 bool plan_w2(const ConvLaunch& a, int forced, W2Plan* out);
 hipError_t launch_conv_w2(ConvLaunch a, const W2Plan& p, hipStream_t stream);
 const char* conv_w2_name(const W2Plan& p, const ConvLaunch& a);
+
+// Persistent 3x3 kernel (BLOCK64 input, every weight of a 64-channel slice
+// resident in LDS, 2-bit threshold or identity-join epilogue): the variant,
+// pixels per tile, workgroups along pixels, tiles per workgroup, window cells
+// per channel block and the predicted time.
+struct WpPlan {
+  int variant;
+  int bn;
+  int gx;
+  int per;
+  int wcells;
+  double t_us;
+};
+int wp_variant_count();
+bool wp_variant_fp4(int v);
+bool plan_wp(const ConvLaunch& a, int forced, WpPlan* out);
+hipError_t launch_conv_wp(ConvLaunch a, const WpPlan& p, hipStream_t stream);
+const char* conv_wp_name(const WpPlan& p, const ConvLaunch& a);
+
+// The register-blocked 3x3 kernels as one family: variants 0 ..
+// w2_variant_count()-1 are conv_w2's, the rest conv_wp's. plan_reg3 with
+// forced < 0 takes the faster prediction of the two planners.
+struct Reg3Plan {
+  bool persistent;
+  W2Plan w2;
+  WpPlan wp;
+  double t_us;
+};
+int reg3_variant_count();
+bool reg3_variant_fp4(int v);
+bool plan_reg3(const ConvLaunch& a, int forced, Reg3Plan* out);
+hipError_t launch_reg3(const ConvLaunch& a, const Reg3Plan& p, hipStream_t stream);
+const char* reg3_name(const Reg3Plan& p, const ConvLaunch& a);
 
 // Whether a launch with a fused downsample (IFQ_JOIN_CONV_FUSED) is covered
 // by one of the 3x3 kernels.

@@ -213,7 +213,8 @@ typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
 // with T' = T for s = +1 and T' = -T - 1 for s = -1. For an integer sum a,
 // -a > T holds exactly when a < -T, i.e. when a > -T - 1 is false, so a
 // flipped channel's code #{i : -a > T_i} is 3 - #{i : a > T'_i}, which is
-// that count xor 3. Needs |T| and |a| below 2^15 (3*K <= 32766).
+// that count xor 3. Needs |T| and |a| below 2^15 (3*K <= 32766); their
+// difference can reach 2^16 and is taken with a saturating subtract.
 constexpr int kPkRecBytes = 32;
 
 // recs: the bm channels' {s, T1, T2, T3} records (already in LDS; records of
@@ -240,11 +241,13 @@ __device__ __forceinline__ void stage_thr_pk(const int4* recs, uint8_t* lds, int
 }
 
 // #{i : a > T'_i} for both halves of a packed pair: T' - a is negative
-// exactly when a > T' (no overflow: both are below 2^15 in magnitude).
+// exactly when a > T'. With T' and a in [-2^15, 2^15) the difference spans
+// twice the int16 range: the subtract saturates (v_pk_sub_i16 with clamp),
+// which keeps its sign, where a wrapping one would flip it.
 __device__ __forceinline__ uint32_t count3_pk(s16x2 p, uint32_t w1, uint32_t w2, uint32_t w3) {
-  const s16x2 d1 = __builtin_bit_cast(s16x2, w1) - p;
-  const s16x2 d2 = __builtin_bit_cast(s16x2, w2) - p;
-  const s16x2 d3 = __builtin_bit_cast(s16x2, w3) - p;
+  const s16x2 d1 = __builtin_elementwise_sub_sat(__builtin_bit_cast(s16x2, w1), p);
+  const s16x2 d2 = __builtin_elementwise_sub_sat(__builtin_bit_cast(s16x2, w2), p);
+  const s16x2 d3 = __builtin_elementwise_sub_sat(__builtin_bit_cast(s16x2, w3), p);
   const u16x2 s1 = __builtin_bit_cast(u16x2, d1) >> (unsigned short)15;
   const u16x2 s2 = __builtin_bit_cast(u16x2, d2) >> (unsigned short)15;
   const u16x2 s3 = __builtin_bit_cast(u16x2, d3) >> (unsigned short)15;

@@ -66,8 +66,7 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
     d = P.conv_desc(n, L.h, L.w, L.cin, L.cout, L.k, L.stride, L.pad,
                     L.in_bits, L.out_bits, in_layout, out_layout)
     ho, wo = P.ifq_conv_output_dims(d)
-    vname = P.ifq_conv_variant_name(d, None, variant) if variant is not None else ""
-    fp4 = bool(vname) and vname[len("conv_w2<"):-1].split(", ")[8] == "true"
+    fp4 = variant is not None and P.ifq_conv_variant_fp4(variant) == 1
     blob = P.ifq_pack_weights_fp4(d, p["w"]) if fp4 else P.ifq_pack_weights(d, p["w"])
     wd = to_dev(blob)
     td = None
@@ -124,7 +123,8 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
         P.ifq_conv_forward(d, xd, wd, td, y, join=join, acc_dump=acc)
     else:
         name = P.ifq_conv_variant_name(d, join, variant)
-        assert name.startswith("conv_w2<"), (variant, name)
+        assert name.startswith(("conv_w2<", "conv_wp<")), (variant, name)
+        assert P.kernel_is_fp4(name) == fp4, (variant, name)
         print("variant %d: %s n=%d %dx%dx%d -> %d s%d" % (variant, name, n, L.h, L.w, L.cin,
                                                           L.cout, L.stride), flush=True)
         P.ifq_conv_forward_variant(d, xd, wd, td, y, variant, join=join, acc_dump=acc)

@@ -19,7 +19,10 @@ def test_fp4_kernels_priced_against_the_fp4_peak():
         bench.PEAK_FP4_TFLOPS
     assert bench.kernel_peak("conv_w2<1, 4, 1, 2, 2, 9, 2, 1, true, 2, 20480>") == \
         bench.PEAK_FP4_TFLOPS
+    assert bench.kernel_peak("conv_wp<4, 2, 2, 0, true, 2, 36864, 16384>") == \
+        bench.PEAK_FP4_TFLOPS
     for int8 in ("conv_w2<2, 4, 1, 2, 2, 3, 3, 0, false, 1, 49152>",
+                 "conv_wp<4, 2, 2, 1, false, 2, 36864, 10240>",
                  "conv_w2<1, 4, 1, 2, 2, 3, 3, 1, false, 2, 20480>",
                  "conv_halo<8, 1, 6, false, 2, false, false>",
                  "conv_halo<8, 1, 6, true, 4, true, false>",

@@ -24,13 +24,9 @@ def P():
 
 
 def fp4_kernel(name):
-    """Whether a kernel name is an fp4 instance: the windowed kernel's last
-    template argument, the register-blocked kernel's ninth."""
-    if name.startswith("conv_halo<"):
-        return name.endswith(", true>")
-    if name.startswith("conv_w2<"):
-        return name[len("conv_w2<"):-1].split(", ")[8] == "true"
-    return False
+    """Whether a kernel name is an fp4 instance (the fp4 template flag)."""
+    import paper_1911_08076_amd as P
+    return P.kernel_is_fp4(name)
 
 
 # name, n, h, c_in, c_out, stride, expected variant
@@ -77,11 +73,12 @@ def test_fp4_conv_bit_exact(P, case):
 
 
 def test_fp4_offered_for_the_64_channel_tiles(P):
-    # the full-batch 64-channel layers run the register-blocked kernel's
-    # 64-channel tiles (two workgroups per CU), which have an fp4 instance
+    # the full-batch 64-channel layers run the persistent kernel (the slice's
+    # weights resident in LDS, two workgroups per CU), which has an fp4
+    # instance
     d = P.conv_desc(64, 56, 56, 64, 64, 3, 1, 1, 2, 2, B64, B64)
-    assert P.ifq_conv_kernel_name(d) == "conv_w2<1, 4, 1, 2, 2, 3, 3, 0, false, 2, 20480>"
-    assert P.ifq_conv_fp4_kernel_name(d) == "conv_w2<1, 4, 1, 2, 2, 9, 2, 0, true, 2, 20480>"
+    assert P.ifq_conv_kernel_name(d) == "conv_wp<4, 2, 2, 0, false, 2, 36864, 16384>"
+    assert P.ifq_conv_fp4_kernel_name(d) == "conv_wp<4, 2, 2, 0, true, 2, 36864, 16384>"
     # a fused pool is not the register-blocked kernel's: the windowed
     # kernel's fp4 instances take it
     pd = P.pool_desc(64, 56, 56, 64, 2, 2, P.IFQ_POOL_VALID, 2, B64)

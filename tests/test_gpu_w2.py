@@ -1,5 +1,6 @@
-"""GPU parity of every variant of the register-blocked 3x3 kernel
-(ifq_conv_forward_variant), int8 and fp4 instances: int32 sums and output
+"""GPU parity of every variant of the register-blocked 3x3 kernels, conv_w2
+and the persistent conv_wp (ifq_conv_forward_variant), int8 and fp4
+instances: int32 sums and output
 codes (thresholds of Eq. 7/8, the identity residual join, or the join with
 a 1x1 downsample computed in the kernel) must equal the oracle's bit for
 bit on the same seeded inputs, on small ragged layers that span several
@@ -38,11 +39,19 @@ SMALL = [
 
 FULL = [
     ("l1", 64, 56, 56, 64, 64, 1),
+    # more tiles than two workgroups per CU take at once: the persistent
+    # kernel runs 3 (ragged: the last workgroup's one tile is partial) and 4
+    # tiles per workgroup through its double buffers
+    ("l1_n97", 97, 56, 56, 64, 64, 1),
+    ("l1_n160", 160, 56, 56, 64, 64, 1),
     ("l2", 64, 28, 28, 128, 128, 1),
     ("l3", 64, 14, 14, 256, 256, 1),
     ("l4", 64, 7, 7, 512, 512, 1),
     ("l3.0.conv1_s2", 64, 28, 28, 128, 256, 2),
 ]
+
+
+NVAR = 12   # conv_w2's ten, then conv_wp's two
 
 
 def _nvar(P):
@@ -76,18 +85,20 @@ def _check(P, case, variant, join, out_layout=None):
     assert len(np.unique(want)) > 1
 
 
-@pytest.mark.parametrize("variant", range(10))
+@pytest.mark.parametrize("variant", range(NVAR))
 @pytest.mark.parametrize("join", [False, True], ids=["thr", "idj"])
 @pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
 def test_variant_small_bit_exact(P, case, join, variant):
-    assert _nvar(P) == 10
+    assert _nvar(P) == NVAR
     _check(P, case, variant, join)
 
 
-@pytest.mark.parametrize("variant", range(10))
+@pytest.mark.parametrize("variant", range(NVAR))
 @pytest.mark.parametrize("join", [False, True], ids=["thr", "idj"])
 @pytest.mark.parametrize("case", FULL, ids=[c[0] for c in FULL])
 def test_variant_full_size_bit_exact(P, case, join, variant):
+    if case[0] in ("l1_n97", "l1_n160") and variant < NVAR - 2:
+        pytest.skip("one tile per workgroup: covered by the batch-64 case")
     _check(P, case, variant, join)
 
 
@@ -102,7 +113,7 @@ FUSED = [(2, 56, 64, 128), (3, 28, 128, 256), (2, 14, 256, 512), (5, 13, 64, 128
          (64, 56, 64, 128), (64, 28, 128, 256), (64, 14, 256, 512)]
 
 
-@pytest.mark.parametrize("variant", range(10))
+@pytest.mark.parametrize("variant", range(NVAR))
 @pytest.mark.parametrize("shape", FUSED, ids=["x".join(map(str, f)) for f in FUSED])
 def test_variant_fused_downsample_bit_exact(P, shape, variant):
     n, hin, cin, cout = shape
