@@ -411,7 +411,8 @@ IFQ_API ifq_status ifq_fold_join_table(const ifq_join_params* p, int32_t in_bits
  * Name of the kernel variant ifq_conv_forward launches for d with join
  * (nullable: no join; only its kind and descriptors are read, no pointer is
  * dereferenced), as a static string: the kernel's symbol as a profiler lists
- * it, or "" for an invalid desc. Host; for profiling and benchmarks.
+ * it, or "" for an invalid desc or one with no output pixels (nothing is
+ * launched). Host; for profiling and benchmarks.
  */
 IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d, const ifq_join* join);
 

@@ -319,6 +319,7 @@ hipError_t launch_gather(const ConvLaunch& a, hipStream_t stream) {
 // small-channel 8-bit kernel, where their planners fit whole rows of pooling
 // windows into a tile; no other kernel takes it.
 const char* conv_kernel_name(const ConvLaunch& a) {
+  if (a.m == 0) return "";   // nothing is launched
   if (a.pool_k) {
     HaloPlan hp;
     if (mfma_eligible(a) && plan_halo(a, &hp)) return conv_halo_name(hp, a);

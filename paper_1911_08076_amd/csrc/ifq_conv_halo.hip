@@ -680,7 +680,7 @@ int64_t halo_cells_bound(const ConvLaunch& a, int64_t bn) {
 
 bool plan_halo(const ConvLaunch& a, HaloPlan* out) {
   if (!(a.in_layout == IFQ_LAYOUT_U2_BLOCK64 && a.in_bits == 2 && a.cin % 64 == 0 &&
-        a.kh == 3 && a.kw == 3 && a.pad == 1 && (a.stride == 1 || a.stride == 2)))
+        a.kh == 3 && a.kw == 3 && a.pad == 1 && (a.stride == 1 || a.stride == 2) && a.m > 0))
     return false;
   // 32-bit cell indices and offsets
   if ((int64_t)a.n * a.h * a.w * (a.cin / 64) >= (int64_t)1 << 26) return false;

@@ -278,23 +278,21 @@ __device__ __forceinline__ void epilogue_lane(const ConvLaunch& a,
 // (else 8-, 4- or 1-byte) stores. In NHWC layouts each pixel's channel range
 // is one contiguous row; in BLOCK64 each 64-channel block of a pixel is a
 // 16-byte cell and consecutive pixels of an image are consecutive cells.
-// tid0, nthr: the threads that do the copy (default: the whole workgroup).
 __device__ __forceinline__ void copy_out_tile(const ConvLaunch& a, const uint8_t* otile,
                                               int orow, int co0, int bm, int p0,
-                                              int npx, int tid0 = -1, int nthr = 0) {
+                                              int npx) {
   if (a.out_mode == 0 || npx <= 0) return;
   const bool u2 = a.out_mode == 2;
   const int ch = a.cout - co0 < bm ? a.cout - co0 : bm;
   uint8_t* y8 = reinterpret_cast<uint8_t*>(a.y);
-  const int tid = tid0 < 0 ? (int)threadIdx.x : tid0;
-  const int nth = tid0 < 0 ? (int)blockDim.x : nthr;
+  const int tid = threadIdx.x;
   if (a.out_layout == IFQ_LAYOUT_U2_BLOCK64) {
     // cells of 64 channels (a tile of 32 channels fills half a cell)
     const int howo = a.ho * a.wo;
     const int G = a.cout >> 6;
     if (ch >= 64) {
       const int ng = ch >> 6;
-      for (int u = tid; u < npx * ng; u += nth) {
+      for (int u = tid; u < npx * ng; u += blockDim.x) {
         const int pl = u / ng, gg = u - pl * ng;
         const int p = p0 + pl;
         const int nimg = fdiv(p, a.div_howo);
@@ -304,7 +302,7 @@ __device__ __forceinline__ void copy_out_tile(const ConvLaunch& a, const uint8_t
             *reinterpret_cast<const uint4*>(otile + pl * orow + gg * 16);
       }
     } else {
-      for (int u = tid; u < npx; u += nth) {
+      for (int u = tid; u < npx; u += blockDim.x) {
         const int p = p0 + u;
         const int nimg = fdiv(p, a.div_howo);
         const int64_t cell = ((int64_t)nimg * G + (co0 >> 6)) * howo + (p - nimg * howo);
@@ -319,20 +317,20 @@ __device__ __forceinline__ void copy_out_tile(const ConvLaunch& a, const uint8_t
   const int cofs = u2 ? co0 >> 2 : co0;
   if ((rbytes & 15) == 0 && (pstride & 15) == 0 && (cofs & 15) == 0) {
     const int per = rbytes >> 4;
-    for (int u = tid; u < npx * per; u += nth) {
+    for (int u = tid; u < npx * per; u += blockDim.x) {
       const int pl = u / per, q = u - pl * per;
       *reinterpret_cast<uint4*>(y8 + (int64_t)(p0 + pl) * pstride + cofs + q * 16) =
           *reinterpret_cast<const uint4*>(otile + pl * orow + q * 16);
     }
   } else if ((rbytes & 3) == 0 && (pstride & 3) == 0 && (cofs & 3) == 0) {
     const int per = rbytes >> 2;
-    for (int u = tid; u < npx * per; u += nth) {
+    for (int u = tid; u < npx * per; u += blockDim.x) {
       const int pl = u / per, q = u - pl * per;
       *reinterpret_cast<uint32_t*>(y8 + (int64_t)(p0 + pl) * pstride + cofs + q * 4) =
           *reinterpret_cast<const uint32_t*>(otile + pl * orow + q * 4);
     }
   } else {
-    for (int u = tid; u < npx * rbytes; u += nth) {
+    for (int u = tid; u < npx * rbytes; u += blockDim.x) {
       const int pl = u / rbytes, q = u - pl * rbytes;
       y8[(int64_t)(p0 + pl) * pstride + cofs + q] = otile[pl * orow + q];
     }
