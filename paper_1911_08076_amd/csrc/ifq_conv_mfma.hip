@@ -372,19 +372,19 @@ bool mfma_eligible(const ConvLaunch& a) {
          (a.in_layout == IFQ_LAYOUT_U2_NHWC_PACKED || a.in_layout == IFQ_LAYOUT_U2_BLOCK64);
 }
 
-// A fused downsample join runs only in the windowed 3x3 kernel (the host
-// checks plan_halo succeeds before launching one).
-// The fast path picks the kernel with the lowest predicted time (plan_time)
-// among the register-blocked 3x3 kernels (one tile per workgroup or
-// persistent), the windowed 3x3 kernel and the tiled kernel. A fused downsample join runs only in the windowed kernel
-// (the host checks plan_halo succeeds before launching one).
+// The fast path picks the kernel with the lowest predicted time among the
+// register-blocked 3x3 kernels (one tile per workgroup or persistent), the
+// windowed 3x3 kernel and the tiled kernel. A fused downsample join runs on
+// the register-blocked kernel wherever it takes the layer (faster on every
+// downsampling block of the ResNet-18-shaped stack as measured), else on the
+// windowed kernel (the host checks fused_supported before launching one).
 const char* conv_mfma_name(const ConvLaunch& a) {
   HaloPlan hp;
   const bool halo = plan_halo(a, &hp);
   Reg3Plan rp;
   const bool r3 = plan_reg3(a, -1, &rp);
   if (a.join_kind == IFQ_JOIN_CONV_FUSED) {
-    if (r3 && (!halo || rp.t_us <= hp.t_us)) return reg3_name(rp, a);
+    if (r3) return reg3_name(rp, a);
     return halo ? conv_halo_name(hp, a) : "";
   }
   const Plan pl = plan_mfma(a);
@@ -399,7 +399,7 @@ hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream) {
   Reg3Plan rp;
   const bool r3 = plan_reg3(a, -1, &rp);
   if (a.join_kind == IFQ_JOIN_CONV_FUSED) {
-    if (r3 && (!halo || rp.t_us <= hp.t_us)) return launch_reg3(a, rp, stream);
+    if (r3) return launch_reg3(a, rp, stream);
     return halo ? launch_conv_halo(a, hp, stream) : hipErrorNotSupported;
   }
   const Plan pl = plan_mfma(a);

@@ -558,7 +558,8 @@ struct W2Variant {
   int wm, wn, wk, fm, fn, t, d, occ, winb;
   bool f4;
   double c0_us;        // fixed cost per round of occ workgroups on a CU
-  double eff;          // MFMA efficiency of a tile's main loop
+  double cj_us;        // more per round with a join epilogue
+  double cs_us;        // cost of one weight stage (T taps of the tile's MFMAs)
   const char* thr_name;   // the kernels as a profiler lists them: threshold
   const char* idj_name;   // epilogue, identity join, fused downsample join
   const char* fused_name;
@@ -573,37 +574,27 @@ struct W2Variant {
       IFQ_W2_NAME(wm, wn, wk, fm, fn, t, d, 2, f4, occ, winb)
 
 // Index order must match the switch in launch_conv_w2.
-// (c0_us, eff) are fitted to kernel times measured on MI355X over the
-// ResNet-18, AlexNet, VGG-16 and Tiny-YOLOv2 layer shapes (see plan_time).
+// (c0_us, cj_us, cs_us) are least-squares fits to kernel times measured on
+// MI355X for every variant on every 3x3 layer of the ResNet-18, AlexNet,
+// VGG-16 and Tiny-YOLOv2 stacks it takes (rms error 2-4%, 7% for the
+// one-tap-stage tiles): a stage's cost holds its MFMAs at the efficiency the
+// tile reaches and the barrier and DMA issue that bracket it.
 const W2Variant kW2Variants[] = {
-    {2, 4, 1, 2, 2, 3, 3, 1, 49152, false, 4.4, 0.69, IFQ_W2_NAMES(2, 4, 1, 2, 2, 3, 3, false, 1, 49152)},
-    {1, 4, 2, 2, 2, 3, 2, 1, 53248, false, 3.8, 0.73, IFQ_W2_NAMES(1, 4, 2, 2, 2, 3, 2, false, 1, 53248)},
-    {1, 2, 4, 2, 2, 3, 2, 1, 36864, false, 3.5, 0.60, IFQ_W2_NAMES(1, 2, 4, 2, 2, 3, 2, false, 1, 36864)},
-    {1, 4, 1, 2, 2, 3, 3, 2, 20480, false, 1.0, 0.335, IFQ_W2_NAMES(1, 4, 1, 2, 2, 3, 3, false, 2, 20480)},
-    {1, 8, 1, 2, 1, 3, 3, 2, 20480, false, 0.23, 0.27, IFQ_W2_NAMES(1, 8, 1, 2, 1, 3, 3, false, 2, 20480)},
-    {2, 4, 1, 2, 2, 1, 3, 2, 24576, false, 2.0, 0.475, IFQ_W2_NAMES(2, 4, 1, 2, 2, 1, 3, false, 2, 24576)},
+    {2, 4, 1, 2, 2, 3, 3, 1, 49152, false, 4.14, 0.75, 0.927, IFQ_W2_NAMES(2, 4, 1, 2, 2, 3, 3, false, 1, 49152)},
+    {1, 4, 2, 2, 2, 3, 2, 1, 53248, false, 3.64, 0.68, 0.919, IFQ_W2_NAMES(1, 4, 2, 2, 2, 3, 2, false, 1, 53248)},
+    {1, 2, 4, 2, 2, 3, 2, 1, 36864, false, 4.05, 0.75, 0.917, IFQ_W2_NAMES(1, 2, 4, 2, 2, 3, 2, false, 1, 36864)},
+    {1, 4, 1, 2, 2, 3, 3, 2, 20480, false, 3.46, 1.71, 0.457, IFQ_W2_NAMES(1, 4, 1, 2, 2, 3, 3, false, 2, 20480)},
+    {1, 8, 1, 2, 1, 3, 3, 2, 20480, false, 3.52, 0.90, 0.477, IFQ_W2_NAMES(1, 8, 1, 2, 1, 3, 3, false, 2, 20480)},
+    {2, 4, 1, 2, 2, 1, 3, 2, 24576, false, 3.33, 2.11, 0.298, IFQ_W2_NAMES(2, 4, 1, 2, 2, 1, 3, false, 2, 24576)},
     // the same tiles on the fp4 scaled MFMA (half the weight bytes per K64
-    // step: a stage holds three times the taps); eff against twice the int8
-    // rate
-    {2, 4, 1, 2, 2, 9, 2, 1, 49152, true, 4.4, 0.67, IFQ_W2_NAMES(2, 4, 1, 2, 2, 9, 2, true, 1, 49152)},
-    {1, 4, 2, 2, 2, 9, 2, 1, 53248, true, 3.8, 0.61, IFQ_W2_NAMES(1, 4, 2, 2, 2, 9, 2, true, 1, 53248)},
-    {1, 2, 4, 2, 2, 3, 2, 1, 36864, true, 3.5, 0.46, IFQ_W2_NAMES(1, 2, 4, 2, 2, 3, 2, true, 1, 36864)},
-    {1, 4, 1, 2, 2, 9, 2, 2, 20480, true, 1.0, 0.21, IFQ_W2_NAMES(1, 4, 1, 2, 2, 9, 2, true, 2, 20480)},
+    // step: a stage holds three times the taps)
+    {2, 4, 1, 2, 2, 9, 2, 1, 49152, true, 3.68, 1.14, 1.656, IFQ_W2_NAMES(2, 4, 1, 2, 2, 9, 2, true, 1, 49152)},
+    {1, 4, 2, 2, 2, 9, 2, 1, 53248, true, 3.84, 0.62, 1.645, IFQ_W2_NAMES(1, 4, 2, 2, 2, 9, 2, true, 1, 53248)},
+    {1, 2, 4, 2, 2, 3, 2, 1, 36864, true, 3.91, 0.70, 0.569, IFQ_W2_NAMES(1, 2, 4, 2, 2, 3, 2, true, 1, 36864)},
+    {1, 4, 1, 2, 2, 9, 2, 2, 20480, true, 3.60, 1.59, 0.782, IFQ_W2_NAMES(1, 4, 1, 2, 2, 9, 2, true, 2, 20480)},
 };
 constexpr int kNumW2 = sizeof(kW2Variants) / sizeof(kW2Variants[0]);
-constexpr double kW2IdjRoundUs = 1.0;
 constexpr int kW2CUs = 256;
-
-// Upper bound of the window cells (rounded per image to 64) one tile of bn
-// output pixels needs per channel block, over every tile of the layer.
-int64_t w2_cells_bound(const ConvLaunch& a, int64_t bn) {
-  const int64_t howo = (int64_t)a.ho * a.wo;
-  const int64_t nseg = (bn - 1) / howo + 2;              // images a tile touches
-  const int64_t rows_out = (bn - 1) / a.wo + 2;          // output rows it touches
-  int64_t rows_in = rows_out * a.stride + 3;
-  if (rows_in > a.h) rows_in = a.h;
-  return nseg * w2_round64((int)(rows_in * a.w));
-}
 
 // The epilogues this kernel has: 2-bit codes with the packed 16-bit compares
 // (sums and thresholds below 2^15), no pool, and either thresholds or an
@@ -645,14 +636,16 @@ bool w2_fit(const ConvLaunch& a, int v, W2Plan* out) {
   int64_t bn = (a.m + nb - 1) / nb;
   bn = (bn + 31) / 32 * 32;
   if (bn > bnmax) bn = bnmax;
-  const int64_t cells = w2_cells_bound(a, bn);
-  if ((int64_t)G * (cells + 1) * 16 > V.winb) return false;
+  const int64_t cells = window_cells_max(a, bn, (int64_t)V.winb / 16 / G);
+  if (cells < 0 || (int64_t)G * (cells + 1) * 16 > V.winb) return false;
   const int64_t blocks = nco * ((a.m + bn - 1) / bn);
-  // the identity join's table epilogue and shortcut cells: about 1 us more
-  // per round of tiles (measured on the ResNet-18-shaped stack's blocks)
-  const double c0 = V.c0_us + (a.join_kind == IFQ_JOIN_IDENTITY ? kW2IdjRoundUs : 0.0);
-  const double t = plan_time(blocks, (V.f4 ? 1.0 : 2.0) * bm * bnmax * (double)a.kpad, V.occ,
-                             c0, V.eff);
+  // the busiest CU's tiles and rounds of occ tiles, each tile's weight
+  // stages (the fused downsample's weights are one more)
+  const int64_t per_cu = (blocks + kW2CUs - 1) / kW2CUs;
+  const int64_t cu_rounds = (per_cu + V.occ - 1) / V.occ;
+  const int64_t stages = (G / V.wk) * (kW2Taps / V.t) + (a.join_kind == IFQ_JOIN_CONV_FUSED);
+  const double c_round = V.c0_us + (a.join_kind != IFQ_JOIN_NONE ? V.cj_us : 0.0);
+  const double t = kLaunchUs + (double)cu_rounds * c_round + (double)(per_cu * stages) * V.cs_us;
   *out = W2Plan{v, (int)bn, (int)((a.m + bn - 1) / bn), (int)cells, t};
   return true;
 }

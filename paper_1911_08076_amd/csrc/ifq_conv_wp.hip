@@ -405,55 +405,33 @@ __global__ __launch_bounds__(64 * WN, (WN / 4) * OCC) void conv_wp(ConvLaunch a)
 struct WpVariant {
   int wn, fm, fn, occ, wgtb, winb_thr, winb_idj;
   bool f4;
+  double c_tile_us;    // fixed cost of a tile (window and tap offsets, epilogue, copy-out)
+  double c_blk_us;     // a tile's main loop per 64-channel input block
   const char* thr_name;
   const char* idj_name;
 };
 // Fitted to kernel times measured on MI355X (the ResNet-18-shaped stack's
-// 64-channel layers, int8 and fp4, and its 128-channel layers on fp4): a
-// fixed cost per workgroup (prologue, launch ramp), per tile (window and
-// tap offsets, epilogue, copy-out; more for the identity join's table
-// epilogue) and the main loop's MFMA efficiency.
-constexpr double kWpWgUs = 1.3;
-constexpr double kWpTileUs = 3.6;
-constexpr double kWpTileIdjUs = 4.7;
-constexpr double kWpEff = 0.95;
+// 64-channel layers and VGG-16's conv1_2, int8 and fp4, and the ResNet
+// 128-channel layers on fp4), with two workgroups on every busy CU: a fixed
+// cost per workgroup (prologue, launch ramp), then per tile the variant's
+// fixed and per-channel-block costs, more for the identity join's table
+// epilogue.
+constexpr double kWpWgUs = 1.27;
+constexpr double kWpIdjUs = 1.1;
 
 #define IFQ_WP_NAME(wn, fm, fn, mode, f4, occ, wgtb, winb) \
   "conv_wp<" #wn ", " #fm ", " #fn ", " #mode ", " #f4 ", " #occ ", " #wgtb ", " #winb ">"
 
 // Index order must match the switch in launch_conv_wp.
 const WpVariant kWpVariants[] = {
-    {4, 2, 2, 2, 36864, 16384, 10240, false,
+    {4, 2, 2, 2, 36864, 16384, 10240, false, 2.91, 2.34,
      IFQ_WP_NAME(4, 2, 2, 0, false, 2, 36864, 16384),
      IFQ_WP_NAME(4, 2, 2, 1, false, 2, 36864, 10240)},
-    {4, 2, 2, 2, 36864, 16384, 10240, true,
+    {4, 2, 2, 2, 36864, 16384, 10240, true, 3.34, 1.17,
      IFQ_WP_NAME(4, 2, 2, 0, true, 2, 36864, 16384),
      IFQ_WP_NAME(4, 2, 2, 1, true, 2, 36864, 10240)},
 };
 constexpr int kNumWp = sizeof(kWpVariants) / sizeof(kWpVariants[0]);
-
-// The largest window (cells per channel block, each image's rows rounded up
-// to 64 cells) over the layer's tiles of bn pixels, or -1 past `limit`.
-int64_t wp_cells_max(const ConvLaunch& a, int64_t bn, int64_t limit) {
-  const int64_t howo = (int64_t)a.ho * a.wo;
-  int64_t mx = 0;
-  for (int64_t p0 = 0; p0 < a.m; p0 += bn) {
-    const int64_t pend = (p0 + bn < a.m ? p0 + bn : a.m) - 1;
-    const int64_t nf = p0 / howo, nl = pend / howo;
-    const int64_t oyf = (p0 - nf * howo) / a.wo, oyl = (pend - nl * howo) / a.wo;
-    int64_t tot = 0;
-    for (int64_t i = 0; i <= nl - nf; ++i) {
-      const int64_t oya = i == 0 ? oyf : 0, oyb = i == nl - nf ? oyl : a.ho - 1;
-      int64_t iya = oya * a.stride - 1, iyb = oyb * a.stride + 1;
-      if (iya < 0) iya = 0;
-      if (iyb > a.h - 1) iyb = a.h - 1;
-      tot += wp_round64((int)((iyb - iya + 1) * a.w));
-    }
-    if (tot > mx) mx = tot;
-    if (mx > limit) return -1;
-  }
-  return mx;
-}
 
 bool wp_fit(const ConvLaunch& a, int v, WpPlan* out) {
   const WpVariant& V = kWpVariants[v];
@@ -463,19 +441,16 @@ bool wp_fit(const ConvLaunch& a, int v, WpPlan* out) {
   const int kh = V.f4 ? 1 : 2;
   if ((int64_t)G * kWpTaps * (bm / 32) * kh * 1024 > V.wgtb) return false;
   const int winb = a.join_kind == IFQ_JOIN_IDENTITY ? V.winb_idj : V.winb_thr;
-  const int64_t cells = wp_cells_max(a, bn, (int64_t)winb / 16);
+  const int64_t cells = window_cells_max(a, bn, (int64_t)winb / 16 / G);
   if (cells < 0 || (int64_t)G * (cells + 1) * 16 > winb) return false;
   const int64_t nco = (a.cout + bm - 1) / bm;
   const int64_t ntm = (a.m + bn - 1) / bn;
   const int64_t slots = (int64_t)kPlanCUs * V.occ;
   const int64_t per = (nco * ntm + slots - 1) / slots;     // tiles per workgroup
   const int64_t gx = (ntm + per - 1) / per;
-  // the busiest CU: up to occ workgroups of per tiles each
-  int64_t wgs_cu = (nco * gx + kPlanCUs - 1) / kPlanCUs;
-  if (wgs_cu > V.occ) wgs_cu = V.occ;
-  const double tile_us = (V.f4 ? 1.0 : 2.0) * bm * bn * (double)a.kpad / kCuOpsPerUsInt8;
-  const double c_tile = a.join_kind == IFQ_JOIN_IDENTITY ? kWpTileIdjUs : kWpTileUs;
-  const double t = kLaunchUs + kWpWgUs + (double)per * ((double)wgs_cu * tile_us / kWpEff + c_tile);
+  const double c_tile = V.c_tile_us + G * V.c_blk_us +
+                        (a.join_kind == IFQ_JOIN_IDENTITY ? kWpIdjUs : 0.0);
+  const double t = kLaunchUs + kWpWgUs + (double)per * c_tile;
   *out = WpPlan{v, bn, (int)gx, (int)per, (int)cells, t};
   return true;
 }

@@ -180,6 +180,42 @@ hipError_t launch_conv_halo(ConvLaunch a, const HaloPlan& p, hipStream_t stream)
 const char* conv_halo_name(const HaloPlan& p, const ConvLaunch& a);
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream);
 
+// The largest input window (cells per channel block, each image's rows of
+// cells rounded up to 64) that a tile of bn consecutive output pixels of a
+// 3x3 pad-1 conv needs, over the layer's tiles, or -1 once it exceeds limit.
+// Tile starts repeat modulo ho*wo with period ho*wo / gcd(bn, ho*wo), so one
+// period and the layer's last (partial) tile cover every distinct tile.
+inline int64_t window_cells_max(const ConvLaunch& a, int64_t bn, int64_t limit) {
+  const int64_t howo = (int64_t)a.ho * a.wo;
+  int64_t g = bn, r = howo;
+  while (r) {
+    const int64_t t = g % r;
+    g = r;
+    r = t;
+  }
+  const int64_t ntm = (a.m + bn - 1) / bn;
+  const int64_t period = howo / g;
+  int64_t mx = 0;
+  for (int64_t t = 0; t < ntm; ++t) {
+    if (t == period && ntm > period) t = ntm - 1;   // then only the last tile
+    const int64_t p0 = t * bn;
+    const int64_t pend = (p0 + bn < a.m ? p0 + bn : a.m) - 1;
+    const int64_t nf = p0 / howo, nl = pend / howo;
+    const int64_t oyf = (p0 - nf * howo) / a.wo, oyl = (pend - nl * howo) / a.wo;
+    int64_t tot = 0;
+    for (int64_t i = 0; i <= nl - nf; ++i) {
+      const int64_t oya = i == 0 ? oyf : 0, oyb = i == nl - nf ? oyl : a.ho - 1;
+      int64_t iya = oya * a.stride - 1, iyb = oyb * a.stride + 1;
+      if (iya < 0) iya = 0;
+      if (iyb > a.h - 1) iyb = a.h - 1;
+      tot += ((iyb - iya + 1) * a.w + 63) / 64 * 64;
+    }
+    if (tot > mx) mx = tot;
+    if (mx > limit) return -1;
+  }
+  return mx;
+}
+
 // 3x3 kernel with register-blocked waves and every channel block's window
 // resident in LDS (BLOCK64 input, 2-bit threshold or identity-join
 // epilogue): the variant, pixels per workgroup, workgroups along pixels,

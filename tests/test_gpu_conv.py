@@ -177,18 +177,17 @@ def test_conv_block64_bit_exact(P, case, io):
 # Workgroup tiles of the size the ResNet-18 layers of the benchmark run with
 # (the 3x3 kernels' tiles of 256, 128 and 64 output pixels, stride-2 layers),
 # at batches the oracle finishes in about a second; the test also pins which
-# kernel variant the planner takes for each: the register-blocked kernel
-# (conv_w2; the eighth template argument is its epilogue: 0 thresholds) and,
-# where its window does not fit, the windowed kernel (conv_halo).
+# kernel variant the planner takes for each (conv_w2; the eighth template
+# argument is its epilogue: 0 thresholds).
 HALO_TILES = [
-    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_w2<2, 4, 1, 2, 2, 3, 3, 0, false, 1, 49152>"),
+    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_w2<1, 4, 1, 2, 2, 3, 3, 0, false, 2, 20480>"),
     ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_w2<1, 4, 2, 2, 2, 3, 2, 0, false, 1, 53248>"),
     ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, 0, false, 1, 36864>"),
     ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_w2<1, 4, 2, 2, 2, 3, 2, 0, false, 1, 53248>"),
     ("halo_l1_b24", 24, 56, 56, 64, 64, 1, "conv_w2<1, 4, 1, 2, 2, 3, 3, 0, false, 2, 20480>"),
     # the stride-2 layers at the full batch of 64, with the largest windows
-    ("halo_l2s2_b64", 64, 56, 56, 64, 128, 2, "conv_w2<2, 4, 1, 2, 2, 3, 3, 0, false, 1, 49152>"),
-    ("halo_l4s2_b64", 64, 14, 14, 256, 512, 2, "conv_halo<4, 2, 4, false, 4, true, false>"),
+    ("halo_l2s2_b64", 64, 56, 56, 64, 128, 2, "conv_w2<1, 4, 1, 2, 2, 3, 3, 0, false, 2, 20480>"),
+    ("halo_l4s2_b64", 64, 14, 14, 256, 512, 2, "conv_w2<1, 4, 2, 2, 2, 3, 2, 0, false, 1, 53248>"),
 ]
 
 
@@ -264,7 +263,7 @@ def test_identity_join_64_channel_variant(P):
     d = P.conv_desc(n, h, h, c, c, 3, 1, 1, 2, 2, B64, B64)
     jn = P.make_join(P.IFQ_JOIN_IDENTITY, B64, None, None, [0.25, 0.75, 1.25])
     jn.table = 0x1000
-    assert P.ifq_conv_kernel_name(d, jn).startswith("conv_w2<1, 4, 1, 2, 2, ")
+    assert P.ifq_conv_kernel_name(d, jn) == "conv_w2<1, 8, 1, 2, 1, 3, 3, 1, false, 2, 20480>"
     L = make_layer("join_id", h, h, c, c, 3, 1, 1, join=("identity", "s"))
     p = params_for(41, L)
     x = codes_for(41, (n, h, h, c), 2)
