@@ -315,8 +315,8 @@ hipError_t launch_gather(const ConvLaunch& a, hipStream_t stream) {
 
 }  // namespace
 
-// A fused pool (a.pool_k) runs in the windowed 3x3 kernel or the
-// small-channel 8-bit kernel, where their planners fit whole rows of pooling
+// A fused pool (a.pool_k) runs in the windowed 3x3 kernel or one of the
+// small-channel kernels, where their planners fit whole rows of pooling
 // windows into a tile; no other kernel takes it.
 const char* conv_kernel_name(const ConvLaunch& a) {
   if (a.m == 0) return "";   // nothing is launched
@@ -324,10 +324,12 @@ const char* conv_kernel_name(const ConvLaunch& a) {
     HaloPlan hp;
     if (mfma_eligible(a) && plan_halo(a, &hp)) return conv_halo_name(hp, a);
     if (small8_eligible(a)) return conv_small8_name(a);
+    if (small2_eligible(a)) return conv_small2_name(a);
     return "";
   }
   if (mfma_eligible(a)) return conv_mfma_name(a);
   if (small8_eligible(a)) return conv_small8_name(a);
+  if (small2_eligible(a)) return conv_small2_name(a);
   static const char* names[3][4] = {
       {"conv_igemm<16, 256, 1, 0>", "conv_igemm<32, 128, 1, 0>",
        "conv_igemm<64, 128, 2, 0>", "conv_igemm<128, 128, 2, 0>"},
@@ -344,10 +346,12 @@ hipError_t launch_conv(const ConvLaunch& a, hipStream_t stream) {
     HaloPlan hp;
     if (mfma_eligible(a) && plan_halo(a, &hp)) return launch_conv_halo(a, hp, stream);
     if (small8_eligible(a)) return launch_conv_small8(a, stream);
+    if (small2_eligible(a)) return launch_conv_small2(a, stream);
     return hipErrorNotSupported;
   }
   if (mfma_eligible(a)) return launch_conv_mfma(a, stream);
   if (small8_eligible(a)) return launch_conv_small8(a, stream);
+  if (small2_eligible(a)) return launch_conv_small2(a, stream);
   switch (gather_kind(a)) {
     case kGatherU2: return launch_gather<kGatherU2>(a, stream);
     case kGatherI8: return launch_gather<kGatherI8>(a, stream);

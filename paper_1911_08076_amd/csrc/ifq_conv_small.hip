@@ -356,6 +356,187 @@ bool small_geom(const ConvLaunch& a, SmallGeom* g) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// 2-bit input codes with 16 or 32 input channels (a detector's second and
+// third layers): 3x3, stride 1, pad 1, 2-bit output codes with thresholds,
+// optionally with the following max-pool fused. The implicit GEMM runs on
+// v_mfma_i32_32x32x32_i8 with K in the weight blob's order (tap-major, the
+// 16 channels of a group transposed as 4x4, which is the order in which a
+// lane unpacks the 16 codes of a packed 32-bit word): K32 step s covers the
+// two taps 2s, 2s+1 (c_in 16) or the one tap s (c_in 32), and the half h of
+// the lanes takes the 16 K values 32s + 16h .. +15, i.e. one packed 32-bit
+// word of the input window per lane and step.
+//  - A workgroup computes whole output rows of one image; the input rows they
+//    need are staged once in LDS as packed pixels of c_in/4 bytes with a
+//    column of zero codes on either side, rows outside the image zero.
+//  - The weight fragments of all K steps and output channels stay in
+//    registers for the whole workgroup (K <= 288, c_out <= 64).
+//  - Epilogue: the packed 16-bit threshold compare from LDS records, codes
+//    into the LDS output tile, then the tile (or its pooled form) to HBM.
+template <int FM, int CIN>
+__global__ __launch_bounds__(kSmallThreads) void conv_small2(ConvLaunch a, SmallGeom sg) {
+  constexpr int BM = 32 * FM;
+  constexpr int KS = (9 * CIN + 31) / 32;        // K32 steps
+  constexpr int BPP = CIN / 4;                   // bytes per packed pixel (4 or 8)
+  constexpr int WPP = CIN / 16;                  // 32-bit words per pixel (1 or 2)
+  extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int h = lane >> 5;
+  const int l32 = lane & 31;
+
+  const int nimg = blockIdx.x / sg.tiles;
+  const int oy0 = (blockIdx.x - nimg * sg.tiles) * sg.rows;
+  const int rows = a.ho - oy0 < sg.rows ? a.ho - oy0 : sg.rows;
+  const int npx = rows * a.wo;
+  const int p0 = (nimg * a.ho + oy0) * a.wo;
+
+  // ---- stage the input rows (1 or 2 words per pixel) ------------------------
+  uint32_t* tile = reinterpret_cast<uint32_t*>(lds + sg.in_off);
+  const int iy0 = oy0 - 1;
+  const int nwords = sg.rin * sg.win * WPP;
+  const uint32_t* x32 = reinterpret_cast<const uint32_t*>(a.x);
+  constexpr int SB = 8;
+  for (int e0 = 0; e0 < nwords; e0 += SB * kSmallThreads) {
+    uint32_t v[SB];
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const int e = e0 + k * kSmallThreads + tid;
+      const int px = e / WPP, wd = e - px * WPP;
+      const int r = fdiv(px, sg.div_win);
+      const int iy = iy0 + r, ix = px - r * sg.win - 1;
+      v[k] = 0u;
+      if (e < nwords && (unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w)
+        v[k] = x32[(((int64_t)nimg * a.h + iy) * a.w + ix) * WPP + wd];
+    }
+#pragma unroll
+    for (int k = 0; k < SB; ++k) {
+      const int e = e0 + k * kSmallThreads + tid;
+      if (e < nwords) tile[e] = v[k];
+    }
+  }
+  // ---- threshold records (stage_thr_pk's layout; channels past c_out get
+  // records whose codes are never stored) and weight fragments --------------
+  if (tid < BM / 4) {
+    uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = 4 * tid + i;
+      int4 r = int4{1, 0, 0, 0};
+      if (c < a.cout) r = *reinterpret_cast<const int4*>(a.thr + (int64_t)c * 4);
+      const bool flip = r.x < 0;
+      const int t[3] = {r.y, r.z, r.w};
+#pragma unroll
+      for (int k = 0; k < 3; ++k) {
+        int vv = flip ? -t[k] - 1 : t[k];
+        vv = vv > 32767 ? 32767 : vv < -32768 ? -32768 : vv;   // |sum| <= 3 * 288
+        w[(i >> 1) * 3 + k] |= ((uint32_t)vv & 0xFFFFu) << (16 * (i & 1));
+      }
+      if (flip) w[6] |= 3u << ((i & 1) * 16 + (i >> 1) * 4);
+    }
+    uint4* dst = reinterpret_cast<uint4*>(lds + tid * kPkRecBytes);
+    dst[0] = uint4{w[0], w[1], w[2], w[3]};
+    dst[1] = uint4{w[4], w[5], w[6], w[7]};
+  }
+  v4i af[KS][FM];
+#pragma unroll
+  for (int s = 0; s < KS; ++s)
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      const int row = fm * 32 + l32;
+      const int k0 = 32 * s + 16 * h;
+      af[s][fm] = v4i{0, 0, 0, 0};
+      if (row < a.cout_pad && k0 < a.kpad)
+        af[s][fm] = *reinterpret_cast<const v4i*>(a.wgt + (int64_t)row * a.kpad + k0);
+    }
+  // LDS byte offset of this lane's word of K step s from a pixel's window corner
+  int toff[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const int k0 = 32 * s + 16 * h;
+    const int tap = k0 / CIN, c0 = k0 - tap * CIN;
+    const int ty = tap / 3, tx = tap - ty * 3;
+    toff[s] = tap < 9 ? ((ty * sg.win + tx) * BPP + (c0 >> 2)) : -1;
+  }
+  __syncthreads();
+
+  const int orow = small_orow(a, BM);
+  uint8_t* otile = lds + sg.out_off;
+  const int nblk = (npx + 31) / 32;
+  constexpr int NW = kSmallThreads / 64;
+  for (int blk = wave; blk < nblk; blk += NW) {
+    const int q = blk * 32 + l32;
+    const int qc = q < npx ? q : npx - 1;
+    const int r = fdiv(qc, a.div_wo);
+    const int ox = qc - r * a.wo;
+    const uint8_t* win = lds + sg.in_off + (r * sg.win + ox) * BPP;
+    v16i acc[FM];
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) acc[fm] = v16i{0};
+    uint32_t u[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+      u[s] = toff[s] >= 0 ? *reinterpret_cast<const uint32_t*>(win + toff[s]) : 0u;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      const v4i bf = unpack2(u[s]);
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+        acc[fm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[s][fm], bf, acc[fm], 0, 0, 0);
+    }
+    if (a.acc_dump && q < npx) {
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int c = fm * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+          if (c < a.cout) a.acc_dump[(int64_t)(p0 + q) * a.cout + c] = acc[fm][v];
+        }
+    }
+    if (q < npx) epilogue_thr_pk<FM>(a, lds, acc, 0, h, 0, q, otile, orow);
+  }
+  __syncthreads();
+  if (a.pool_k)
+    pool_out_tile(a, otile, orow, 0, BM, p0, npx);
+  else
+    copy_out_tile(a, otile, orow, 0, BM, p0, npx);
+}
+
+bool small2_geom(const ConvLaunch& a, SmallGeom* g) {
+  const int bm = 32 * ((a.cout + 31) / 32);
+  const int win = a.wo + 2;
+  const int64_t rows_total = (int64_t)a.n * a.ho;
+  int rows = (int)((rows_total + 1023) / 1024);
+  if (rows < 1) rows = 1;
+  if (rows > a.ho) rows = a.ho;
+  const int rstep = a.pool_k == 0 ? 1 : a.pool_img ? a.ho : a.pool_k;
+  rows = (rows + rstep - 1) / rstep * rstep;
+  if (rows > a.ho) rows = a.ho / rstep * rstep;
+  for (;; rows -= rstep) {
+    if (rows < 1) return false;
+    const int npx = rows * a.wo;
+    const int rin = rows + 2;
+    const int rec = bm / 4 * kPkRecBytes;
+    const int out = (npx * small_orow(a, bm) + 15) & ~15;
+    const int64_t in = ((int64_t)rin * win * (a.cin / 4) + 15) & ~(int64_t)15;
+    const int64_t total = (int64_t)rec + out + in;
+    if (npx <= kSmallMaxPx && total <= kSmallMaxLds) {
+      g->rows = rows;
+      g->tiles = (a.ho + rows - 1) / rows;
+      g->rin = rin;
+      g->win = win;
+      g->div_win = make_fastdiv((uint32_t)win);
+      g->out_off = rec;
+      g->in_off = (int)(rec + out);
+      g->raw_off = 0;
+      g->vec = 0;
+      g->lds_bytes = (int)total;
+      return true;
+    }
+  }
+}
+
 }  // namespace
 
 bool small8_eligible(const ConvLaunch& a) {
@@ -383,6 +564,39 @@ hipError_t launch_conv_small8(const ConvLaunch& a, hipStream_t stream) {
     case 2: hipLaunchKernelGGL((conv_small8<2>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
     case 3: hipLaunchKernelGGL((conv_small8<3>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
     case 4: hipLaunchKernelGGL((conv_small8<4>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+bool small2_eligible(const ConvLaunch& a) {
+  if (!(a.in_bits == 2 && a.in_layout == IFQ_LAYOUT_U2_NHWC_PACKED &&
+        (a.cin == 16 || a.cin == 32) && a.kh == 3 && a.kw == 3 && a.stride == 1 &&
+        a.pad == 1 && a.cout <= 64 && a.out_mode == 2 && a.rec == 4 &&
+        a.join_kind == IFQ_JOIN_NONE && a.m > 0))
+    return false;
+  if (((uintptr_t)a.x & 3) != 0) return false;   // staged as 32-bit words
+  if (a.pool_k && !pool_epilogue_ok(a)) return false;
+  SmallGeom g;
+  return small2_geom(a, &g);
+}
+
+const char* conv_small2_name(const ConvLaunch& a) {
+  const bool two = a.cout > 32;
+  if (a.cin == 16) return two ? "conv_small2<2, 16>" : "conv_small2<1, 16>";
+  return two ? "conv_small2<2, 32>" : "conv_small2<1, 32>";
+}
+
+hipError_t launch_conv_small2(const ConvLaunch& a, hipStream_t stream) {
+  SmallGeom g;
+  if (!small2_geom(a, &g)) return hipErrorInvalidValue;
+  const dim3 grid(a.n * g.tiles);
+  const int key = (a.cout > 32 ? 2 : 0) + (a.cin == 32 ? 1 : 0);
+  switch (key) {
+    case 0: hipLaunchKernelGGL((conv_small2<1, 16>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
+    case 1: hipLaunchKernelGGL((conv_small2<1, 32>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
+    case 2: hipLaunchKernelGGL((conv_small2<2, 16>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
+    case 3: hipLaunchKernelGGL((conv_small2<2, 32>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -280,6 +280,11 @@ inline bool fused_supported(const ConvLaunch& a) {
 bool small8_eligible(const ConvLaunch& a);
 hipError_t launch_conv_small8(const ConvLaunch& a, hipStream_t stream);
 const char* conv_small8_name(const ConvLaunch& a);
+// 2-bit packed NHWC input codes with c_in 16 or 32, 3x3 s1 p1, 2-bit output
+// codes with thresholds (a detector's second and third layers).
+bool small2_eligible(const ConvLaunch& a);
+hipError_t launch_conv_small2(const ConvLaunch& a, hipStream_t stream);
+const char* conv_small2_name(const ConvLaunch& a);
 const char* conv_mfma_name(const ConvLaunch& a);
 
 struct PoolLaunch {

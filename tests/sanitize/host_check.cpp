@@ -45,6 +45,8 @@ static void conv_shapes(std::mt19937& rng) {
       desc(2, 6, 6, 1024, 64, 3, 1, 1, 2, 2, B64, B64),
       desc(8, 416, 416, 3, 16, 3, 1, 1, 8, 2, I8, U2),
       desc(8, 208, 208, 16, 32, 3, 1, 1, 2, 2, U2, U2),
+      desc(8, 104, 104, 32, 64, 3, 1, 1, 2, 2, U2, B64),
+      desc(3, 1, 1, 32, 36, 3, 1, 1, 2, 2, U2, U2),
       desc(32, 27, 27, 96, 256, 5, 1, 2, 2, 2, I8, I8),
       desc(8, 13, 13, 512, 30, 1, 1, 0, 2, 0, B64, I32),
       desc(2, 9, 9, 32, 200, 3, 1, 1, 2, 4, I8, I8),

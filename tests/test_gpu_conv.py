@@ -123,6 +123,46 @@ def test_small8_bit_exact(P, case):
         assert len(np.unique(want)) > 1
 
 
+
+# 2-bit packed input with c_in 16 or 32 (a detector's second and third
+# layers) runs the small-channel 2-bit kernel: the YOLO c2 and c3 shapes,
+# and shapes across its parameters (one and two blocks of 32 output channels,
+# half-used blocks, 1-pixel-wide and 1-row images where every tap but the
+# centre column or row is padding, a ragged last row tile).
+# (name, n, h, w, cin, cout)
+SMALL2 = [
+    ("s2_yolo_c2", 2, 208, 208, 16, 32),
+    ("s2_yolo_c3", 2, 104, 104, 32, 64),
+    ("s2_cin16_c48_ragged", 3, 37, 29, 16, 48),
+    ("s2_cin32_c4", 2, 9, 11, 32, 4),
+    ("s2_cin32_c36_1x1_image", 5, 1, 1, 32, 36),
+    ("s2_cin16_one_row", 2, 1, 57, 16, 16),
+    ("s2_cin16_one_column", 1, 67, 1, 16, 64),
+    ("s2_cin32_c20", 3, 23, 17, 32, 20),
+]
+
+
+@pytest.mark.parametrize("case", SMALL2, ids=[c[0] for c in SMALL2])
+def test_small2_bit_exact(P, case):
+    name, n, h, w, cin, cout = case
+    L = make_layer(name, h, w, cin, cout, 3, 1, 1, 2, 2)
+    seed = zlib.crc32(name.encode()) % 997
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, w, cin), 2)
+    want_acc, want = oracle_layer(L, x, p)
+    outs = [U2, B64] if cout % 64 == 0 else [U2]
+    for out_l in outs:
+        d = P.conv_desc(n, h, w, cin, cout, 3, 1, 1, 2, 2, U2, out_l)
+        assert P.ifq_conv_kernel_name(d).startswith("conv_small2<"), (name, out_l)
+        acc, got = gpu_layer(P, L, n, x, p, in_layout=U2, out_layout=out_l)
+        assert np.array_equal(acc, want_acc), (name, out_l)
+        assert np.array_equal(got, expect_layout(want, out_l)), (name, out_l)
+        # without the sums dumped (the launch the stacks make)
+        _, got = gpu_layer(P, L, n, x, p, in_layout=U2, out_layout=out_l, dump=False)
+        assert np.array_equal(got, expect_layout(want, out_l)), (name, out_l)
+    assert len(np.unique(want)) > 1
+
+
 U2_LAYERS = [
     ("u2_3x3_64", 2, 14, 14, 64, 64, 3, 1, 1),
     ("u2_stride2_128", 2, 15, 15, 64, 128, 3, 2, 1),

@@ -1,8 +1,8 @@
 """GPU parity of the fused conv + max-pool (ifq_conv_pool_forward): the
 pooled codes must equal the oracle's conv -> thresholds -> max-pool on codes
 (Eq. 1, Eq. 7-8, Eq. 4) bit for bit, for the two kernels that fuse the pool
-(the small-channel 8-bit first layer and the windowed 3x3 kernel on BLOCK64
-input), every code layout they write, pool sizes 2..4, tiles that span
+(the small-channel 8-bit first layer, the small-channel 2-bit kernel for
+c_in 16 and 32, and the windowed 3x3 kernel on BLOCK64 input), every code layout they write, pool sizes 2..4, tiles that span
 images, and channels with a negative BN scale (the calibrated parameters
 flip about a tenth of them)."""
 import zlib
@@ -90,6 +90,24 @@ def test_small8_conv_pool_bit_exact(P, case):
     check(P, name, L, n, k, I8, [I8, U2], "conv_small8<")
 
 
+
+# name, n, h, w, c_in, c_out, pool k, output layouts
+SMALL2_POOL = [
+    ("s2p_yolo_c2", 2, 208, 208, 16, 32, 2, [U2]),
+    ("s2p_yolo_c3", 2, 104, 104, 32, 64, 2, [B64, U2]),
+    ("s2p_c48_ragged_rows", 3, 37, 29, 16, 48, 2, [U2]),
+    ("s2p_pool3_c16", 2, 33, 27, 32, 16, 3, [U2]),
+    ("s2p_pool4_c64", 1, 40, 44, 16, 64, 4, [B64]),
+]
+
+
+@pytest.mark.parametrize("case", SMALL2_POOL, ids=[c[0] for c in SMALL2_POOL])
+def test_small2_conv_pool_bit_exact(P, case):
+    name, n, h, w, cin, cout, k, outs = case
+    L = make_layer(name, h, w, cin, cout, 3, 1, 1, 2, 2)
+    check(P, name, L, n, k, U2, outs, "conv_small2<")
+
+
 # name, n, h, w, c_in, c_out, pool k, output layouts
 HALO_POOL = [
     ("hp_yolo_c4", 2, 52, 52, 64, 128, 2, [B64, U2, I8]),
@@ -129,3 +147,11 @@ def test_halo_conv_pool_whole_images(P, case):
 def test_small8_conv_pool_whole_images(P):
     L = make_layer("s8p_pool3s2", 31, 29, 3, 16, 3, 1, 1, 8, 2)
     check(P, "s8p_pool3s2", L, 2, 3, I8, [I8, U2], "conv_small8<", 2, "valid")
+
+
+def test_small2_conv_pool_whole_images(P):
+    # overlapping 3/2 windows and a SAME pool: each workgroup holds whole images
+    L = make_layer("s2p_pool3s2", 31, 29, 32, 32, 3, 1, 1, 2, 2)
+    check(P, "s2p_pool3s2", L, 2, 3, U2, [U2], "conv_small2<", 2, "valid")
+    L = make_layer("s2p_pool2s1_same", 13, 13, 16, 64, 3, 1, 1, 2, 2)
+    check(P, "s2p_pool2s1_same", L, 3, 2, U2, [B64, U2], "conv_small2<", 1, "same")
