@@ -458,9 +458,10 @@ IFQ_API size_t ifq_conv_workspace_bytes(const ifq_conv_desc* d);
 /*
  * One quantized substructure on the GPU, asynchronous on stream.
  *   x          device input [n][h][w][c_in] in d->in_layout
- *   w_packed   device copy of ifq_pack_weights(d, ...)
- *   thr        device copy of ifq_fold_thresholds(...) for this layer; must
- *              be NULL iff out_bits == 0 or join->kind != IFQ_JOIN_NONE
+ *   w_packed   device copy of ifq_pack_weights(d, ...), 16-byte aligned
+ *   thr        device copy of ifq_fold_thresholds(...) for this layer,
+ *              16-byte aligned; must be NULL iff out_bits == 0 or
+ *              join->kind != IFQ_JOIN_NONE
  *   join       nullable; residual join in place of the thresholds
  *   y          device output [n][ho][wo][c_out] in d->out_layout
  *   acc_dump   nullable device int32 [n][ho][wo][c_out]: also receives the

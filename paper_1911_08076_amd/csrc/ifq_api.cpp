@@ -374,6 +374,9 @@ ifq_status conv_args_check(const ifq_conv_desc* d, const void* x,
   }
   if (d->n > 0 && (!x || !w || !y))
     return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: x, w_packed and y are required");
+  // the kernels read the blob and the records with 16-byte loads
+  if ((reinterpret_cast<uintptr_t>(w) & 15) || (reinterpret_cast<uintptr_t>(thr) & 15))
+    return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: w_packed and thr must be 16-byte aligned");
   const bool want_thr = d->out_bits != 0 && !joined;
   if (want_thr && !thr)
     return fail(IFQ_ERR_INVALID_ARGUMENT, "conv: thresholds required");

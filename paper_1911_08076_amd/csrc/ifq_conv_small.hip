@@ -49,13 +49,30 @@ struct SmallGeom {
   int raw_off;
   int vec;         // input 16-byte aligned: rows staged with 16-byte loads
   int lds_bytes;
+  int ncg;         // register-pooled epilogue: groups of 4 pooled columns per
+  FastDiv div_ncg; // row pair, and the division by it
 };
 
 __host__ __device__ inline int small_orow(const ConvLaunch& a, int bm) {
   return a.out_mode == 2 ? bm / 4 : bm;
 }
 
-template <int FM>
+// EPI: the epilogue, fixed per launch by small8_epi: 0 the generic one
+// through the LDS output tile, 1 the register epilogue of 2-bit codes
+// stored straight to HBM, 2 the register epilogue into the LDS tile for the
+// fused pool, 3 a 2x2/2 max-pool taken on the sums in registers before the
+// threshold compare.
+//
+// EPI 3. The code #{i : s*a > T_i} does not decrease as s*a grows, so the
+// largest code of a window is the code of the window's largest s*a (the
+// order of Eq. 4 and Eq. 7 swapped: pool the sums, max where s = +1 and min
+// where s = -1). Rows of the weights with s = -1 are negated in registers,
+// which makes every sum s*a and the pool a plain max. A 16-pixel block is
+// four 2x2 windows, the four pixels of a window in one lane quad; four
+// blocks are in flight, and two DPP exchanges inside each quad leave lane e
+// of a quad with block e's pooled window (a reduce-scatter), so the compare
+// and packing run once per pooled pixel instead of once per pixel.
+template <int FM, int EPI>
 __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, SmallGeom sg) {
   constexpr int BM = 16 * FM;
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
@@ -72,6 +89,44 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
   const int p0 = (nimg * a.ho + oy0) * a.wo;
   const int st = a.stride;
   const int ntaps = a.kh * a.kw;
+  constexpr bool fast = EPI != 0;
+
+  // ---- operands kept in registers, loaded before the input rows so that
+  // their latency overlaps the staging loads: from clamped addresses, the
+  // lanes out of range masked afterwards. A lane group's 4*c_in weight bytes
+  // (taps 4*kg .. 4*kg+3) are one 4-aligned span of its row, inside the row's
+  // kpad >= 64 bytes.
+  uint32_t wraw[FM][4];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) {
+    const int co = fm * 16 + l16;
+    const int coc = co < a.cout_pad ? co : a.cout_pad - 1;
+    const uint32_t* wr =
+        reinterpret_cast<const uint32_t*>(a.wgt + (int64_t)coc * a.kpad + 4 * kg * a.cin);
+#pragma unroll
+    for (int d = 0; d < 4; ++d) wraw[fm][d] = wr[d];
+  }
+  int asgn[FM];   // EPI 3: s of the lane's weight row fm*16 + l16
+  if constexpr (EPI == 3) {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      const int co = fm * 16 + l16;
+      asgn[fm] = a.thr[(int64_t)(co < a.cout ? co : a.cout - 1) * 4];
+    }
+  }
+  int4 rrec[FM][4];
+  int rsum[FM][4];
+  if constexpr (fast) {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int co = fm * 16 + 4 * kg + i;
+        const int coc = co < a.cout ? co : a.cout - 1;
+        rrec[fm][i] = *reinterpret_cast<const int4*>(a.thr + (int64_t)coc * 4);
+        rsum[fm][i] = a.rowsum[coc];
+      }
+  }
 
   // ---- stage the input rows: 4 bytes per pixel, x ^ 0x80, zero code
   // (0x80) outside the image and past c_in ---------------------------------
@@ -95,31 +150,41 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
       const int nfull = nb >> 4;
       const uint4* src = reinterpret_cast<const uint4*>(a.x + gs16);
       constexpr int VB = 4;
-      for (int i0 = 0; i0 < nfull; i0 += VB * kSmallThreads) {
+      // unconditional loads and stores at clamped indices (the lanes past the
+      // end store the last cell's value again), so that every load of a
+      // batch is in flight before the first store waits
+      auto batch = [&](int i0) {
         uint4 v[VB];
 #pragma unroll
-        for (int k = 0; k < VB; ++k) {   // unconditional (clamped) loads, all in flight
+        for (int k = 0; k < VB; ++k) {
           const int i = i0 + k * kSmallThreads + tid;
           v[k] = src[i < nfull ? i : nfull - 1];
         }
 #pragma unroll
         for (int k = 0; k < VB; ++k) {
           const int i = i0 + k * kSmallThreads + tid;
-          if (i < nfull) reinterpret_cast<uint4*>(raw)[i] = v[k];
+          reinterpret_cast<uint4*>(raw)[i < nfull ? i : nfull - 1] = v[k];
         }
-      }
+      };
+      if (nfull > 0) batch(0);   // outside the loop: no loop-header wait
+      for (int i0 = VB * kSmallThreads; i0 < nfull; i0 += VB * kSmallThreads) batch(i0);
       for (int i = nfull * 16 + tid; i < nb; i += kSmallThreads) raw[i] = a.x[gs16 + i];
     }
     __syncthreads();
+    // a pixel's c_in bytes from the two aligned words that hold them (the
+    // raw buffer has 16 bytes of slack past its end), the channels past c_in
+    // masked to the zero code
+    const uint32_t keep = a.cin >= 4 ? 0xFFFFFFFFu : (1u << (8 * a.cin)) - 1u;
     for (int e = tid; e < nin; e += kSmallThreads) {
       const int r = fdiv(e, sg.div_win);
       const int iy = iy0 + r, ix = e - r * sg.win - a.pad;
       uint32_t word = 0x80808080u;
       if ((unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w) {
-        const uint8_t* px = raw + lead + ((iy - iy_lo) * a.w + ix) * a.cin;
-#pragma unroll
-        for (int ch = 0; ch < 4; ++ch)
-          if (ch < a.cin) word ^= (uint32_t)px[ch] << (8 * ch);   // 0x80 ^ x
+        const int b = lead + ((iy - iy_lo) * a.w + ix) * a.cin;
+        const uint32_t* w32 = reinterpret_cast<const uint32_t*>(raw + (b & ~3));
+        const uint32_t lo = w32[0], hi = w32[1];
+        const uint32_t v = __builtin_amdgcn_alignbyte(hi, lo, (uint32_t)(b & 3));
+        word ^= v & keep;                                         // 0x80 ^ x
       }
       *reinterpret_cast<uint32_t*>(tile + e * 4) = word;
     }
@@ -149,38 +214,42 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
     }
   }
   // 2-bit codes into I8 or packed-U2 NHWC: the register epilogue below
-  const bool fast = a.out_mode != 0 && a.rec == 4 && a.join_kind == IFQ_JOIN_NONE &&
-                    (a.out_layout == IFQ_LAYOUT_I8_NHWC ||
-                     (a.out_layout == IFQ_LAYOUT_U2_NHWC_PACKED && (a.cout & 3) == 0));
   if (!fast) stage_epilogue(a, lds, 0, BM);
 
   // ---- weight fragments (A: rows = output channels), K byte 4*j + c of
-  // lane group kg = channel c of tap 4*kg + j -------------------------------
+  // lane group kg = channel c of tap 4*kg + j: tap j's c_in bytes start at
+  // byte j*c_in of the lane group's span -------------------------------------
   v4i af[FM];
+  const uint32_t keep = a.cin >= 4 ? 0xFFFFFFFFu : (1u << (8 * a.cin)) - 1u;
 #pragma unroll
   for (int fm = 0; fm < FM; ++fm) {
-    const int co = fm * 16 + l16;
-    uint32_t w4[4] = {0u, 0u, 0u, 0u};
+    const bool row_ok = fm * 16 + l16 < a.cout_pad;
+    uint32_t w4[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int tap = 4 * kg + j;
-      if (tap < ntaps && co < a.cout_pad) {
-        const int8_t* wr = a.wgt + (int64_t)co * a.kpad + tap * a.cin;
+      const int o = j * a.cin, q = o >> 2;
+      const uint32_t lo = q == 0 ? wraw[fm][0] : q == 1 ? wraw[fm][1] : q == 2 ? wraw[fm][2] : wraw[fm][3];
+      const uint32_t hi = q == 0 ? wraw[fm][1] : q == 1 ? wraw[fm][2] : q == 2 ? wraw[fm][3] : 0u;
+      const uint32_t v = __builtin_amdgcn_alignbyte(hi, lo, (uint32_t)(o & 3)) & keep;
+      w4[j] = (row_ok && 4 * kg + j < ntaps) ? v : 0u;
+      if (EPI == 3 && asgn[fm] < 0) {   // bytes in {-1, 0, 1}: negate each
+        uint32_t nv = 0;
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-          if (c < a.cin) w4[j] |= (uint32_t)(uint8_t)wr[c] << (8 * c);
+        for (int b = 0; b < 4; ++b)
+          nv |= (uint32_t)(uint8_t)(-(int8_t)(w4[j] >> (8 * b))) << (8 * b);
+        w4[j] = nv;
       }
     }
     af[fm] = v4i{(int)w4[0], (int)w4[1], (int)w4[2], (int)w4[3]};
   }
   // LDS byte offsets of this lane's four taps from a pixel's window corner
+  // (taps past kh*kw read the corner: their weights are zero)
   int toff[4];
-  bool tval[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int tap = 4 * kg + j;
-    tval[j] = tap < ntaps;
-    const int ty = tval[j] ? tap / a.kw : 0, tx = tval[j] ? tap - ty * a.kw : 0;
+    const bool valid = tap < ntaps;
+    const int ty = valid ? tap / a.kw : 0, tx = valid ? tap - ty * a.kw : 0;
     toff[j] = (ty * sg.win + tx) * 4;
   }
   // register epilogue state: per row block, the lane's channels
@@ -199,18 +268,30 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
       int4 r = int4{1, 0x7FFF, 0x7FFF, 0x7FFF};
       corr[fm][i] = 0;
       if (fast && co < a.cout) {
-        r = *reinterpret_cast<const int4*>(a.thr + (int64_t)co * 4);
-        corr[fm][i] = 128 * a.rowsum[co];
+        r = rrec[fm][i];
+        corr[fm][i] = 128 * rsum[fm][i];
       }
       const bool flip = r.x < 0;
       const int tt[3] = {r.y, r.z, r.w};
+      if constexpr (EPI == 3) {
+        // the sums are s*a - s*128*rowsum (negated rows): compare them with
+        // T - s*128*rowsum; |sum| <= 128*64, so the clamp keeps every answer
+        if (flip) corr[fm][i] = -corr[fm][i];
 #pragma unroll
-      for (int k = 0; k < 3; ++k) {
-        int v = flip ? -tt[k] - 1 : tt[k];
-        v = v > 32767 ? 32767 : v < -32768 ? -32768 : v;   // |sum| < 2^15 anyway
-        t16[i][k] = (uint32_t)v & 0xFFFFu;
+        for (int k = 0; k < 3; ++k) {
+          int64_t v = (int64_t)tt[k] - corr[fm][i];
+          v = v > 32767 ? 32767 : v < -32768 ? -32768 : v;
+          t16[i][k] = (uint32_t)v & 0xFFFFu;
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+          int v = flip ? -tt[k] - 1 : tt[k];
+          v = v > 32767 ? 32767 : v < -32768 ? -32768 : v;   // |sum| < 2^15 anyway
+          t16[i][k] = (uint32_t)v & 0xFFFFu;
+        }
+        if (flip) txm[fm] |= 3u << ((i & 1) * 16 + (i >> 1) * 4);
       }
-      if (flip) txm[fm] |= 3u << ((i & 1) * 16 + (i >> 1) * 4);
     }
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
@@ -222,7 +303,7 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
 
   const int orow = small_orow(a, BM);
   uint8_t* otile = lds + sg.out_off;
-  const bool pooled = a.pool_k > 0;
+  const bool pooled = EPI == 2 || (EPI == 0 && a.pool_k > 0);
   uint8_t* y8 = reinterpret_cast<uint8_t*>(a.y);
   const int nblk = (npx + 15) / 16;
   // UB independent blocks of 16 pixels per iteration, so the LDS reads, the
@@ -230,6 +311,82 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
   // past 32 output channels, where four would not fit the registers)
   constexpr int UB = FM <= 2 ? 4 : 1;
   constexpr int NW = kSmallThreads / 64;
+  if constexpr (EPI == 3) {
+    static_assert(FM <= 2, "four blocks in flight");
+    // block b: row pair b / ncg, pooled columns 4*(b % ncg) .. +3; lane
+    // l16 = 4*w + e: window w, pixel (e >> 1, e & 1) of it
+    const int w = l16 >> 2, e = l16 & 3;
+    const int pwo = a.wo >> 1;
+    const int nb3 = (rows >> 1) * sg.ncg;
+    const int prow = pwo * orow;   // pooled tile bytes per row pair
+    for (int blk0 = wave; blk0 < nb3; blk0 += NW * 4) {
+      v4i accu[4][FM];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int b = blk0 + NW * u;
+        const int bc = b < nb3 ? b : nb3 - 1;
+        const int rp = fdiv(bc, sg.div_ncg);
+        const int pc = 4 * (bc - rp * sg.ncg) + w;
+        const int pcc = pc < pwo ? pc : pwo - 1;
+        const int r = 2 * rp + (e >> 1), ox = 2 * pcc + (e & 1);
+        const uint8_t* win = tile + ((r * st) * sg.win + ox * st) * 4;
+        uint32_t b4[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) b4[j] = *reinterpret_cast<const uint32_t*>(win + toff[j]);
+        const v4i bf = v4i{(int)b4[0], (int)b4[1], (int)b4[2], (int)b4[3]};
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+          accu[u][fm] = __builtin_amdgcn_mfma_i32_16x16x64_i8(af[fm], bf, v4i{0, 0, 0, 0}, 0, 0, 0);
+      }   // (a pooled launch carries no sum dump)
+      // int16 pairs (|sum| <= 128*64), then the reduce-scatter over the quad
+      s16x2 pk[4][FM][2];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm) {
+          pk[u][fm][0] = __builtin_amdgcn_cvt_pk_i16(accu[u][fm][0], accu[u][fm][1]);
+          pk[u][fm][1] = __builtin_amdgcn_cvt_pk_i16(accu[u][fm][2], accu[u][fm][3]);
+        }
+      const bool odd = (e & 1) != 0, high = (e & 2) != 0;
+      auto xchg = [](s16x2 v, int ctrl) {
+        const int iv = __builtin_bit_cast(int, v);
+        const int r = ctrl == 0xB1 ? __builtin_amdgcn_mov_dpp(iv, 0xB1, 0xF, 0xF, false)
+                                   : __builtin_amdgcn_mov_dpp(iv, 0x4E, 0xF, 0xF, false);
+        return __builtin_bit_cast(s16x2, r);
+      };
+      s16x2 red[FM][2];
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          // lanes e ^ 1: the even lane keeps blocks 0, 2, the odd lane 1, 3
+          s16x2 k1[2];
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const s16x2 send = odd ? pk[2 * j][fm][hf] : pk[2 * j + 1][fm][hf];
+            const s16x2 keep = odd ? pk[2 * j + 1][fm][hf] : pk[2 * j][fm][hf];
+            k1[j] = __builtin_elementwise_max(keep, xchg(send, 0xB1));
+          }
+          // lanes e ^ 2: lane e keeps block e
+          const s16x2 send = high ? k1[0] : k1[1];
+          const s16x2 keep = high ? k1[1] : k1[0];
+          red[fm][hf] = __builtin_elementwise_max(keep, xchg(send, 0x4E));
+        }
+      // lane e: block blk0 + NW*e, pooled pixel (row pair, 4*group + w)
+      const int be = blk0 + NW * e;
+      const int bec = be < nb3 ? be : nb3 - 1;
+      const int rpe = fdiv(bec, sg.div_ncg);
+      const int pce = 4 * (bec - rpe * sg.ncg) + w;
+      const bool store = be < nb3 && pce < pwo;
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) {
+        const uint32_t c01 = count3_pk(red[fm][0], tw[fm][0][0], tw[fm][0][1], tw[fm][0][2]);
+        const uint32_t c23 = count3_pk(red[fm][1], tw[fm][1][0], tw[fm][1][1], tw[fm][1][2]);
+        const uint32_t t = c01 | (c23 << 4);
+        if (store) otile[rpe * prow + pce * orow + fm * 4 + kg] = (uint8_t)(t | (t >> 14));
+      }
+    }
+  } else
   for (int blk0 = wave; blk0 < nblk; blk0 += NW * UB) {
     v4i accu[UB][FM];
 #pragma unroll
@@ -242,7 +399,7 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
       uint32_t b4[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        b4[j] = tval[j] ? *reinterpret_cast<const uint32_t*>(win + toff[j]) : 0x80808080u;
+        b4[j] = *reinterpret_cast<const uint32_t*>(win + toff[j]);
       const v4i bf = v4i{(int)b4[0], (int)b4[1], (int)b4[2], (int)b4[3]};
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm)
@@ -308,7 +465,16 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
       }
     }
   }
-  if (!fast || pooled) {
+  if constexpr (EPI == 3) {
+    // the pooled rows are one contiguous span of the packed NHWC output
+    // (c_out == BM, 4-byte rows of 16 channels)
+    __syncthreads();
+    const int nw = (rows >> 1) * (a.wo >> 1) * orow / 4;
+    const int64_t pp0 = ((int64_t)nimg * a.pho + (oy0 >> 1)) * a.pwo;
+    uint32_t* dst = reinterpret_cast<uint32_t*>(y8 + pp0 * orow);
+    const uint32_t* srcw = reinterpret_cast<const uint32_t*>(otile);
+    for (int i = tid; i < nw; i += kSmallThreads) dst[i] = srcw[i];
+  } else if (!fast || pooled) {
     __syncthreads();
     if (pooled)
       pool_out_tile(a, otile, orow, 0, BM, p0, npx);
@@ -338,7 +504,8 @@ bool small_geom(const ConvLaunch& a, SmallGeom* g) {
     const int epi = epilogue_param_bytes(bm);
     const int out = (npx * small_orow(a, bm) + 15) & ~15;
     const int64_t in = ((int64_t)rin * win * 4 + 15) & ~(int64_t)15;   // raw buffer 16-aligned
-    const int64_t rawb = ((int64_t)rin * a.w * a.cin + 16 + 15) & ~(int64_t)15;
+    // 16 bytes of alignment lead plus 8 of slack for the two-word pixel reads
+    const int64_t rawb = ((int64_t)rin * a.w * a.cin + 24 + 15) & ~(int64_t)15;
     const int64_t total = (int64_t)epi + out + in + rawb;
     if (npx <= kSmallMaxPx && total <= kSmallMaxLds) {
       g->rows = rows;
@@ -351,6 +518,8 @@ bool small_geom(const ConvLaunch& a, SmallGeom* g) {
       g->raw_off = (int)(epi + out + in);
       g->vec = ((uintptr_t)a.x & 15) == 0;
       g->lds_bytes = (int)total;
+      g->ncg = ((a.wo >> 1) + 3) / 4;
+      g->div_ncg = make_fastdiv((uint32_t)(g->ncg > 0 ? g->ncg : 1));
       return true;
     }
   }
@@ -392,13 +561,35 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small2(ConvLaunch a, Small
   const int npx = rows * a.wo;
   const int p0 = (nimg * a.ho + oy0) * a.wo;
 
+  // ---- weight fragments and threshold records into registers first, so
+  // that their latency overlaps the staging loads (clamped addresses; rows
+  // past cout_pad are zeroed once loaded, records past c_out never used) ----
+  v4i af[KS][FM];
+#pragma unroll
+  for (int s = 0; s < KS; ++s)
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      const int row = fm * 32 + l32;
+      const int rowc = row < a.cout_pad ? row : a.cout_pad - 1;
+      af[s][fm] = *reinterpret_cast<const v4i*>(a.wgt + (int64_t)rowc * a.kpad + 32 * s + 16 * h);
+    }
+  int4 rrec[4];
+  if (tid < BM / 4) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = 4 * tid + i;
+      const int cc = c < a.cout ? c : a.cout - 1;
+      rrec[i] = *reinterpret_cast<const int4*>(a.thr + (int64_t)cc * 4);
+    }
+  }
+
   // ---- stage the input rows (1 or 2 words per pixel) ------------------------
   uint32_t* tile = reinterpret_cast<uint32_t*>(lds + sg.in_off);
   const int iy0 = oy0 - 1;
   const int nwords = sg.rin * sg.win * WPP;
   const uint32_t* x32 = reinterpret_cast<const uint32_t*>(a.x);
   constexpr int SB = 8;
-  for (int e0 = 0; e0 < nwords; e0 += SB * kSmallThreads) {
+  auto stage = [&](int e0) {
     uint32_t v[SB];
 #pragma unroll
     for (int k = 0; k < SB; ++k) {
@@ -415,16 +606,20 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small2(ConvLaunch a, Small
       const int e = e0 + k * kSmallThreads + tid;
       if (e < nwords) tile[e] = v[k];
     }
-  }
+  };
+  // the first batch outside the loop: a loop header would wait for every
+  // load in flight, the register operands' included
+  stage(0);
+  for (int e0 = SB * kSmallThreads; e0 < nwords; e0 += SB * kSmallThreads) stage(e0);
   // ---- threshold records (stage_thr_pk's layout; channels past c_out get
   // records whose codes are never stored) and weight fragments --------------
   if (tid < BM / 4) {
     uint32_t w[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int c = 4 * tid + i;
-      int4 r = int4{1, 0, 0, 0};
-      if (c < a.cout) r = *reinterpret_cast<const int4*>(a.thr + (int64_t)c * 4);
+      // opaque here, so that no use of the record moves above the staging
+      asm volatile("" : "+v"(rrec[i].x), "+v"(rrec[i].y), "+v"(rrec[i].z), "+v"(rrec[i].w));
+      const int4 r = rrec[i];
       const bool flip = r.x < 0;
       const int t[3] = {r.y, r.z, r.w};
 #pragma unroll
@@ -439,25 +634,20 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small2(ConvLaunch a, Small
     dst[0] = uint4{w[0], w[1], w[2], w[3]};
     dst[1] = uint4{w[4], w[5], w[6], w[7]};
   }
-  v4i af[KS][FM];
 #pragma unroll
-  for (int s = 0; s < KS; ++s)
+  for (int fm = 0; fm < FM; ++fm)
+    if (fm * 32 + l32 >= a.cout_pad)
 #pragma unroll
-    for (int fm = 0; fm < FM; ++fm) {
-      const int row = fm * 32 + l32;
-      const int k0 = 32 * s + 16 * h;
-      af[s][fm] = v4i{0, 0, 0, 0};
-      if (row < a.cout_pad && k0 < a.kpad)
-        af[s][fm] = *reinterpret_cast<const v4i*>(a.wgt + (int64_t)row * a.kpad + k0);
-    }
-  // LDS byte offset of this lane's word of K step s from a pixel's window corner
+      for (int s = 0; s < KS; ++s) af[s][fm] = v4i{0, 0, 0, 0};
+  // LDS byte offset of this lane's word of K step s from a pixel's window
+  // corner (K past 9*c_in reads the corner: its weights are zero)
   int toff[KS];
 #pragma unroll
   for (int s = 0; s < KS; ++s) {
     const int k0 = 32 * s + 16 * h;
     const int tap = k0 / CIN, c0 = k0 - tap * CIN;
     const int ty = tap / 3, tx = tap - ty * 3;
-    toff[s] = tap < 9 ? ((ty * sg.win + tx) * BPP + (c0 >> 2)) : -1;
+    toff[s] = tap < 9 ? ((ty * sg.win + tx) * BPP + (c0 >> 2)) : 0;
   }
   __syncthreads();
 
@@ -477,7 +667,7 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small2(ConvLaunch a, Small
     uint32_t u[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s)
-      u[s] = toff[s] >= 0 ? *reinterpret_cast<const uint32_t*>(win + toff[s]) : 0u;
+      u[s] = *reinterpret_cast<const uint32_t*>(win + toff[s]);
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const v4i bf = unpack2(u[s]);
@@ -549,24 +739,58 @@ bool small8_eligible(const ConvLaunch& a) {
   return small_geom(a, &g);
 }
 
+// The epilogue kind of a small8 launch (the EPI template argument).
+static int small8_epi(const ConvLaunch& a) {
+  const bool fast = a.out_mode != 0 && a.rec == 4 && a.join_kind == IFQ_JOIN_NONE &&
+                    (a.out_layout == IFQ_LAYOUT_I8_NHWC ||
+                     (a.out_layout == IFQ_LAYOUT_U2_NHWC_PACKED && (a.cout & 3) == 0));
+  if (!fast) return 0;
+  if (a.pool_k == 0) return 1;
+  // the register pool: 2x2/2 windows in whole row pairs, packed NHWC codes,
+  // c_out 16 or 32 (one or two row blocks, the whole tile row)
+  const bool reg_pool = a.pool_k == 2 && a.pool_s == 2 && !a.pool_same && !a.pool_img &&
+                        a.out_layout == IFQ_LAYOUT_U2_NHWC_PACKED &&
+                        (a.cout == 16 || a.cout == 32) && ((uintptr_t)a.y & 3) == 0;
+  return reg_pool ? 3 : 2;
+}
+
 const char* conv_small8_name(const ConvLaunch& a) {
-  static const char* names[4] = {"conv_small8<1>", "conv_small8<2>", "conv_small8<3>",
-                                 "conv_small8<4>"};
-  return names[(a.cout + 15) / 16 - 1];
+  static const char* names[4][4] = {
+      {"conv_small8<1, 0>", "conv_small8<1, 1>", "conv_small8<1, 2>", "conv_small8<1, 3>"},
+      {"conv_small8<2, 0>", "conv_small8<2, 1>", "conv_small8<2, 2>", "conv_small8<2, 3>"},
+      {"conv_small8<3, 0>", "conv_small8<3, 1>", "conv_small8<3, 2>", ""},
+      {"conv_small8<4, 0>", "conv_small8<4, 1>", "conv_small8<4, 2>", ""}};
+  return names[(a.cout + 15) / 16 - 1][small8_epi(a)];
+}
+
+template <int FM>
+static hipError_t launch_small8_fm(const ConvLaunch& a, const SmallGeom& g, hipStream_t stream) {
+  const dim3 grid(a.n * g.tiles);
+  switch (small8_epi(a)) {
+    case 0: hipLaunchKernelGGL((conv_small8<FM, 0>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
+    case 1: hipLaunchKernelGGL((conv_small8<FM, 1>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
+    case 2: hipLaunchKernelGGL((conv_small8<FM, 2>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
+    default:
+      if constexpr (FM <= 2) {
+        hipLaunchKernelGGL((conv_small8<FM, 3>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g);
+      } else {
+        return hipErrorInvalidValue;
+      }
+      break;
+  }
+  return hipGetLastError();
 }
 
 hipError_t launch_conv_small8(const ConvLaunch& a, hipStream_t stream) {
   SmallGeom g;
   if (!small_geom(a, &g)) return hipErrorInvalidValue;
-  const dim3 grid(a.n * g.tiles);
   switch ((a.cout + 15) / 16) {
-    case 1: hipLaunchKernelGGL((conv_small8<1>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
-    case 2: hipLaunchKernelGGL((conv_small8<2>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
-    case 3: hipLaunchKernelGGL((conv_small8<3>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
-    case 4: hipLaunchKernelGGL((conv_small8<4>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
+    case 1: return launch_small8_fm<1>(a, g, stream);
+    case 2: return launch_small8_fm<2>(a, g, stream);
+    case 3: return launch_small8_fm<3>(a, g, stream);
+    case 4: return launch_small8_fm<4>(a, g, stream);
     default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 bool small2_eligible(const ConvLaunch& a) {

@@ -26,7 +26,7 @@ def test_fp4_kernels_priced_against_the_fp4_peak():
                  "conv_w2<1, 4, 1, 2, 2, 3, 3, 1, false, 2, 20480>",
                  "conv_halo<8, 1, 6, false, 2, false, false>",
                  "conv_halo<8, 1, 6, true, 4, true, false>",
-                 "conv_mfma<2, 1, 4, 1, 4, 1, 6>", "conv_small8<1>", "conv_igemm<32, 128, 1, 1>"):
+                 "conv_mfma<2, 1, 4, 1, 4, 1, 6>", "conv_small8<1, 2>", "conv_small2<2, 32>", "conv_igemm<32, 128, 1, 1>"):
         assert bench.kernel_peak(int8) == bench.PEAK_INT8_TOPS
 
 

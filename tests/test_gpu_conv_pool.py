@@ -80,6 +80,9 @@ SMALL8_POOL = [
     ("s8p_c32_ragged_rows", 3, 50, 38, 3, 32, 2),
     ("s8p_c64_cin4", 1, 36, 44, 4, 64, 2),
     ("s8p_pool3", 2, 39, 45, 3, 16, 3),
+    # 4 rows per workgroup with a last tile of 2, and a ragged last group of
+    # pooled columns (pwo = 11) in the register pool
+    ("s8p_rows4_ragged_tile", 8, 290, 22, 3, 16, 2),
 ]
 
 
