@@ -327,6 +327,7 @@ const char* conv_kernel_name(const ConvLaunch& a) {
     if (small2_eligible(a)) return conv_small2_name(a);
     return "";
   }
+  if (head_eligible(a)) return conv_head_name(a);
   if (mfma_eligible(a)) return conv_mfma_name(a);
   if (small8_eligible(a)) return conv_small8_name(a);
   if (small2_eligible(a)) return conv_small2_name(a);
@@ -349,6 +350,7 @@ hipError_t launch_conv(const ConvLaunch& a, hipStream_t stream) {
     if (small2_eligible(a)) return launch_conv_small2(a, stream);
     return hipErrorNotSupported;
   }
+  if (head_eligible(a)) return launch_conv_head(a, stream);
   if (mfma_eligible(a)) return launch_conv_mfma(a, stream);
   if (small8_eligible(a)) return launch_conv_small8(a, stream);
   if (small2_eligible(a)) return launch_conv_small2(a, stream);

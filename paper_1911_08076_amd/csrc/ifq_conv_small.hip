@@ -727,6 +727,89 @@ bool small2_geom(const ConvLaunch& a, SmallGeom* g) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// 1x1 convolutions with int32 sums out and at most 64 output channels (a
+// detector's head: c_in 512 -> 30 channels), on 2-bit codes in BLOCK64 or
+// packed NHWC with c_in a multiple of 64. M is small (the head of Tiny-YOLOv2
+// at batch 8 has 1352 pixels), so the kernel is built for latency: one wave
+// per 32 pixels, no LDS and no barrier. Each lane loads its pixel's 16-byte
+// cells (one per 64-channel block) and its A fragments (the weight blob's
+// fragment order) straight into registers, all loads of a chunk of eight
+// channel blocks in flight at once; K32 step 2g + t takes the 32-bit word
+// 2h + t of cell g (the 16 channels 32h + 16t .. +15 the blob's K order puts
+// in that half of the step) through unpack2, then v_mfma_i32_32x32x32_i8.
+template <int FM>
+__global__ __launch_bounds__(64, 1) void conv_head(ConvLaunch a) {
+  constexpr int GC = 8;                            // channel blocks per chunk
+  const int lane = threadIdx.x;
+  const int h = lane >> 5;
+  const int l32 = lane & 31;
+  const int G = a.cin >> 6;
+  const int nk32 = 2 * G;                          // kpad = c_in for 1x1
+  const int p0 = blockIdx.x * 32;
+  const int p = p0 + l32;
+  const int pc = p < a.m ? p : a.m - 1;
+  // byte offset of the pixel's cell g: g * gstride + cbase
+  int64_t cbase, gstride;
+  if (a.in_layout == IFQ_LAYOUT_U2_BLOCK64) {
+    const int howo = a.h * a.w;
+    const int n = fdiv(pc, a.div_howo);
+    cbase = ((int64_t)n * G * howo + (pc - n * howo)) * 16;
+    gstride = (int64_t)howo * 16;
+  } else {
+    cbase = (int64_t)pc * G * 16;
+    gstride = 16;
+  }
+  const uint8_t* x8 = reinterpret_cast<const uint8_t*>(a.x);
+  const uint8_t* w8 = reinterpret_cast<const uint8_t*>(a.wgt);
+  v16i acc[FM];
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm) acc[fm] = v16i{0};
+  for (int g0 = 0; g0 < G; g0 += GC) {
+    uint2 cw[GC];                                  // words 2h, 2h+1 of each cell
+    v4i af[GC][2][FM];
+#pragma unroll
+    for (int j = 0; j < GC; ++j) {
+      const int g = g0 + j < G ? g0 + j : G - 1;
+      cw[j] = *reinterpret_cast<const uint2*>(x8 + cbase + g * gstride + 8 * h);
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+          af[j][t][fm] = *reinterpret_cast<const v4i*>(
+              w8 + (((int64_t)fm * nk32 + 2 * g + t) * 64 + lane) * 16);
+    }
+    // blocks past G (the last chunk) multiply zero codes: no branch, and no
+    // instruction scheduled across this point, so that every load of the
+    // chunk is issued before the first MFMA
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < GC; ++j) {
+      const bool in = g0 + j < G;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const v4i bf = unpack2(in ? (t == 0 ? cw[j].x : cw[j].y) : 0u);
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+          acc[fm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[j][t][fm], bf, acc[fm], 0, 0, 0);
+      }
+    }
+  }
+  if (p >= a.m) return;
+  // lane: pixel p, channels fm*32 + 8b + 4h + i (b = v >> 2, i = v & 3)
+  int32_t* y32 = reinterpret_cast<int32_t*>(a.y);
+#pragma unroll
+  for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int c = fm * 32 + 8 * (v >> 2) + 4 * h + (v & 3);
+      if (c < a.cout) {
+        y32[(int64_t)p * a.cout + c] = acc[fm][v];
+        if (a.acc_dump) a.acc_dump[(int64_t)p * a.cout + c] = acc[fm][v];
+      }
+    }
+}
+
 }  // namespace
 
 bool small8_eligible(const ConvLaunch& a) {
@@ -823,6 +906,27 @@ hipError_t launch_conv_small2(const ConvLaunch& a, hipStream_t stream) {
     case 3: hipLaunchKernelGGL((conv_small2<2, 32>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+bool head_eligible(const ConvLaunch& a) {
+  return a.in_bits == 2 && a.cin % 64 == 0 &&
+         (a.in_layout == IFQ_LAYOUT_U2_BLOCK64 || a.in_layout == IFQ_LAYOUT_U2_NHWC_PACKED) &&
+         a.kh == 1 && a.kw == 1 && a.stride == 1 && a.pad == 0 && a.cout <= 64 &&
+         a.out_mode == 0 && a.join_kind == IFQ_JOIN_NONE && a.m > 0 &&
+         ((uintptr_t)a.x & 7) == 0 && (int64_t)a.n * a.h * a.w * (a.cin / 4) < ((int64_t)1 << 40);
+}
+
+const char* conv_head_name(const ConvLaunch& a) {
+  return a.cout > 32 ? "conv_head<2>" : "conv_head<1>";
+}
+
+hipError_t launch_conv_head(const ConvLaunch& a, hipStream_t stream) {
+  const dim3 grid((a.m + 31) / 32);
+  if (a.cout > 32)
+    hipLaunchKernelGGL((conv_head<2>), grid, dim3(64), 0, stream, a);
+  else
+    hipLaunchKernelGGL((conv_head<1>), grid, dim3(64), 0, stream, a);
   return hipGetLastError();
 }
 

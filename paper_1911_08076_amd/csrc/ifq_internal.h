@@ -285,6 +285,11 @@ const char* conv_small8_name(const ConvLaunch& a);
 bool small2_eligible(const ConvLaunch& a);
 hipError_t launch_conv_small2(const ConvLaunch& a, hipStream_t stream);
 const char* conv_small2_name(const ConvLaunch& a);
+// 1x1, stride 1, c_in a multiple of 64 on 2-bit codes, c_out <= 64, int32
+// sums out (a detector's head): a latency-bound kernel without LDS.
+bool head_eligible(const ConvLaunch& a);
+hipError_t launch_conv_head(const ConvLaunch& a, hipStream_t stream);
+const char* conv_head_name(const ConvLaunch& a);
 const char* conv_mfma_name(const ConvLaunch& a);
 
 struct PoolLaunch {

@@ -163,6 +163,37 @@ def test_small2_bit_exact(P, case):
     assert len(np.unique(want)) > 1
 
 
+
+# 1x1 convolutions with int32 sums out and c_out <= 64 on 2-bit codes (a
+# detector's head) run the latency-bound head kernel: the YOLO head, both
+# code layouts, ragged channel counts, c_in past one chunk of eight channel
+# blocks (1024) and a last chunk of one block (576).
+# (name, n, h, w, cin, cout, in_layout)
+HEAD = [
+    ("head_yolo", 8, 13, 13, 512, 30, "b64"),
+    ("head_u2_c64", 3, 9, 7, 128, 64, "u2"),
+    ("head_c33", 2, 5, 11, 64, 33, "b64"),
+    ("head_cin1024", 1, 6, 6, 1024, 30, "u2"),
+    ("head_cin576_c8", 2, 7, 7, 576, 8, "b64"),
+]
+
+
+@pytest.mark.parametrize("case", HEAD, ids=[c[0] for c in HEAD])
+def test_head_bit_exact(P, case):
+    name, n, h, w, cin, cout, lay = case
+    in_l = B64 if lay == "b64" else U2
+    L = make_layer(name, h, w, cin, cout, 1, 1, 0, 2, 0)
+    d = P.conv_desc(n, h, w, cin, cout, 1, 1, 0, 2, 0, in_l, I32)
+    assert P.ifq_conv_kernel_name(d).startswith("conv_head<"), name
+    seed = zlib.crc32(name.encode()) % 997
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, w, cin), 2)
+    want_acc, want = oracle_layer(L, x, p)
+    acc, got = gpu_layer(P, L, n, x, p, in_layout=in_l, out_layout=I32)
+    assert np.array_equal(acc, want_acc), name
+    assert np.array_equal(got, want), name
+
+
 U2_LAYERS = [
     ("u2_3x3_64", 2, 14, 14, 64, 64, 3, 1, 1),
     ("u2_stride2_128", 2, 15, 15, 64, 128, 3, 2, 1),
