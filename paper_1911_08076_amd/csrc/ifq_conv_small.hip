@@ -49,8 +49,9 @@ struct SmallGeom {
   int raw_off;
   int vec;         // input 16-byte aligned: rows staged with 16-byte loads
   int lds_bytes;
-  int ncg;         // register-pooled epilogue: groups of 4 pooled columns per
-  FastDiv div_ncg; // row pair, and the division by it
+  int ncg;         // register-pooled epilogues: groups of pooled columns per
+  FastDiv div_ncg; // row pair (4 in small8, 8 in small2), the division by it
+  FastDiv div_phowo;  // small2: division by pho * pwo (pooled copy-out)
 };
 
 __host__ __device__ inline int small_orow(const ConvLaunch& a, int bm) {
@@ -542,7 +543,12 @@ bool small_geom(const ConvLaunch& a, SmallGeom* g) {
 //    registers for the whole workgroup (K <= 288, c_out <= 64).
 //  - Epilogue: the packed 16-bit threshold compare from LDS records, codes
 //    into the LDS output tile, then the tile (or its pooled form) to HBM.
-template <int FM, int CIN>
+// RP: the 2x2/2 max-pool taken on the sums in registers, as in conv_small8's
+// EPI 3: weight rows with s = -1 negated, a 32-pixel block is eight 2x2
+// windows (lane l32 = 4*w + e), UB blocks in flight, a reduce-scatter over
+// each lane quad (UB = 4: lane e ends with block e; UB = 2: a scatter over
+// e ^ 1 and a butterfly over e ^ 2), and the compare once per pooled pixel.
+template <int FM, int CIN, bool RP>
 __global__ __launch_bounds__(kSmallThreads) void conv_small2(ConvLaunch a, SmallGeom sg) {
   constexpr int BM = 32 * FM;
   constexpr int KS = (9 * CIN + 31) / 32;        // K32 steps
@@ -620,7 +626,7 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small2(ConvLaunch a, Small
       // opaque here, so that no use of the record moves above the staging
       asm volatile("" : "+v"(rrec[i].x), "+v"(rrec[i].y), "+v"(rrec[i].z), "+v"(rrec[i].w));
       const int4 r = rrec[i];
-      const bool flip = r.x < 0;
+      const bool flip = !RP && r.x < 0;   // RP: the sums are s*a already
       const int t[3] = {r.y, r.z, r.w};
 #pragma unroll
       for (int k = 0; k < 3; ++k) {
@@ -639,6 +645,25 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small2(ConvLaunch a, Small
     if (fm * 32 + l32 >= a.cout_pad)
 #pragma unroll
       for (int s = 0; s < KS; ++s) af[s][fm] = v4i{0, 0, 0, 0};
+  if constexpr (RP) {
+    // s of the lane's weight row: rows with s = -1 negated (bytes in {-1, 0, 1})
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm) {
+      const int row = fm * 32 + l32;
+      if (row < a.cout && a.thr[(int64_t)row * 4] < 0)
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const uint32_t w4 = (uint32_t)af[s][fm][k];
+            uint32_t nv = 0;
+#pragma unroll
+            for (int b = 0; b < 4; ++b)
+              nv |= (uint32_t)(uint8_t)(-(int8_t)(w4 >> (8 * b))) << (8 * b);
+            af[s][fm][k] = (int)nv;
+          }
+    }
+  }
   // LDS byte offset of this lane's word of K step s from a pixel's window
   // corner (K past 9*c_in reads the corner: its weights are zero)
   int toff[KS];
@@ -655,6 +680,105 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small2(ConvLaunch a, Small
   uint8_t* otile = lds + sg.out_off;
   const int nblk = (npx + 31) / 32;
   constexpr int NW = kSmallThreads / 64;
+  if constexpr (RP) {
+    constexpr int UB = FM == 1 ? 4 : 2;
+    const int w = l32 >> 2, e = l32 & 3;
+    const int pwo = a.wo >> 1;
+    const int nb = (rows >> 1) * sg.ncg;
+    const int prow = pwo * orow;
+    auto xchg = [](s16x2 v, int ctrl) {
+      const int iv = __builtin_bit_cast(int, v);
+      const int r = ctrl == 0xB1 ? __builtin_amdgcn_mov_dpp(iv, 0xB1, 0xF, 0xF, false)
+                                 : __builtin_amdgcn_mov_dpp(iv, 0x4E, 0xF, 0xF, false);
+      return __builtin_bit_cast(s16x2, r);
+    };
+    for (int blk0 = wave; blk0 < nb; blk0 += NW * UB) {
+      s16x2 pk[UB][FM][8];
+#pragma unroll
+      for (int u = 0; u < UB; ++u) {
+        const int b = blk0 + NW * u;
+        const int bc = b < nb ? b : nb - 1;
+        const int rp = fdiv(bc, sg.div_ncg);
+        const int pc = 8 * (bc - rp * sg.ncg) + w;
+        const int pcc = pc < pwo ? pc : pwo - 1;
+        const int r = 2 * rp + (e >> 1), ox = 2 * pcc + (e & 1);
+        const uint8_t* win = lds + sg.in_off + (r * sg.win + ox) * BPP;
+        v16i acc[FM];
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm) acc[fm] = v16i{0};
+        uint32_t uw[KS];
+#pragma unroll
+        for (int s = 0; s < KS; ++s) uw[s] = *reinterpret_cast<const uint32_t*>(win + toff[s]);
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+          const v4i bf = unpack2(uw[s]);
+#pragma unroll
+          for (int fm = 0; fm < FM; ++fm)
+            acc[fm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[s][fm], bf, acc[fm], 0, 0, 0);
+        }
+        // int16 pairs: |sum| <= 3 * 288
+#pragma unroll
+        for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+          for (int v2 = 0; v2 < 8; ++v2)
+            pk[u][fm][v2] = __builtin_amdgcn_cvt_pk_i16(acc[fm][2 * v2], acc[fm][2 * v2 + 1]);
+      }   // (a pooled launch carries no sum dump)
+      const bool odd = (e & 1) != 0, high = (e & 2) != 0;
+      s16x2 red[FM][8];
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int v2 = 0; v2 < 8; ++v2) {
+          if constexpr (UB == 4) {
+            s16x2 k1[2];
+#pragma unroll
+            for (int j = 0; j < 2; ++j) {
+              const s16x2 send = odd ? pk[2 * j][fm][v2] : pk[2 * j + 1][fm][v2];
+              const s16x2 keep = odd ? pk[2 * j + 1][fm][v2] : pk[2 * j][fm][v2];
+              k1[j] = __builtin_elementwise_max(keep, xchg(send, 0xB1));
+            }
+            const s16x2 send = high ? k1[0] : k1[1];
+            const s16x2 keep = high ? k1[1] : k1[0];
+            red[fm][v2] = __builtin_elementwise_max(keep, xchg(send, 0x4E));
+          } else {
+            const s16x2 send = odd ? pk[0][fm][v2] : pk[1][fm][v2];
+            const s16x2 keep = odd ? pk[1][fm][v2] : pk[0][fm][v2];
+            const s16x2 k1 = __builtin_elementwise_max(keep, xchg(send, 0xB1));
+            red[fm][v2] = __builtin_elementwise_max(k1, xchg(k1, 0x4E));
+          }
+        }
+      // lane e: block blk0 + NW*ub (ub = e, or e & 1 for two blocks)
+      const int ub = UB == 4 ? e : (e & 1);
+      const int be = blk0 + NW * ub;
+      const int bec = be < nb ? be : nb - 1;
+      const int rpe = fdiv(bec, sg.div_ncg);
+      const int pce = 8 * (bec - rpe * sg.ncg) + w;
+      const bool store = be < nb && pce < pwo && (UB == 4 || e < 2);
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) {
+        if (fm * 32 >= a.cout) continue;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int cl = fm * 32 + 8 * b + 4 * h;
+          const uint4* rec = reinterpret_cast<const uint4*>(lds + (cl >> 2) * kPkRecBytes);
+          const uint4 r0 = rec[0], r1 = rec[1];
+          const uint32_t c01 = count3_pk(red[fm][2 * b], r0.x, r0.y, r0.z);
+          const uint32_t c23 = count3_pk(red[fm][2 * b + 1], r0.w, r1.x, r1.y);
+          const uint32_t t = c01 | (c23 << 4);
+          if (store) otile[rpe * prow + pce * orow + (cl >> 2)] = (uint8_t)(t | (t >> 14));
+        }
+      }
+    }
+    __syncthreads();
+    // the pooled rows of the tile, as an output of pho x pwo pixels
+    ConvLaunch ap = a;
+    ap.ho = a.pho;
+    ap.wo = a.pwo;
+    ap.div_howo = sg.div_phowo;
+    copy_out_tile(ap, otile, orow, 0, BM, (nimg * a.pho + (oy0 >> 1)) * a.pwo,
+                  (rows >> 1) * a.pwo);
+    return;
+  }
   for (int blk = wave; blk < nblk; blk += NW) {
     const int q = blk * 32 + l32;
     const int qc = q < npx ? q : npx - 1;
@@ -722,6 +846,9 @@ bool small2_geom(const ConvLaunch& a, SmallGeom* g) {
       g->raw_off = 0;
       g->vec = 0;
       g->lds_bytes = (int)total;
+      g->ncg = ((a.wo >> 1) + 7) / 8;
+      g->div_ncg = make_fastdiv((uint32_t)(g->ncg > 0 ? g->ncg : 1));
+      g->div_phowo = make_fastdiv((uint32_t)(a.pool_k ? (a.pho * a.pwo > 0 ? a.pho * a.pwo : 1) : 1));
       return true;
     }
   }
@@ -888,22 +1015,41 @@ bool small2_eligible(const ConvLaunch& a) {
   return small2_geom(a, &g);
 }
 
+// The register pool: 2x2/2 windows in whole row pairs (even ho and wo),
+// one row block of 32 output channels (four blocks in flight; with two row
+// blocks and two blocks in flight it measured slower than the LDS pool on
+// the detector's third layer: 10.4 against 9.8 us).
+static bool small2_reg_pool(const ConvLaunch& a) {
+  return a.pool_k == 2 && a.pool_s == 2 && !a.pool_same && !a.pool_img && a.cout <= 32;
+}
+
 const char* conv_small2_name(const ConvLaunch& a) {
-  const bool two = a.cout > 32;
-  if (a.cin == 16) return two ? "conv_small2<2, 16>" : "conv_small2<1, 16>";
-  return two ? "conv_small2<2, 32>" : "conv_small2<1, 32>";
+  static const char* names[2][2][2] = {
+      {{"conv_small2<1, 16, false>", "conv_small2<1, 16, true>"},
+       {"conv_small2<1, 32, false>", "conv_small2<1, 32, true>"}},
+      {{"conv_small2<2, 16, false>", "conv_small2<2, 16, true>"},
+       {"conv_small2<2, 32, false>", "conv_small2<2, 32, true>"}}};
+  return names[a.cout > 32][a.cin == 32][small2_reg_pool(a)];
+}
+
+template <int FM, int CIN>
+static void launch_small2_rp(const ConvLaunch& a, const SmallGeom& g, hipStream_t stream) {
+  const dim3 grid(a.n * g.tiles);
+  if (small2_reg_pool(a))
+    hipLaunchKernelGGL((conv_small2<FM, CIN, true>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g);
+  else
+    hipLaunchKernelGGL((conv_small2<FM, CIN, false>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g);
 }
 
 hipError_t launch_conv_small2(const ConvLaunch& a, hipStream_t stream) {
   SmallGeom g;
   if (!small2_geom(a, &g)) return hipErrorInvalidValue;
-  const dim3 grid(a.n * g.tiles);
   const int key = (a.cout > 32 ? 2 : 0) + (a.cin == 32 ? 1 : 0);
   switch (key) {
-    case 0: hipLaunchKernelGGL((conv_small2<1, 16>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
-    case 1: hipLaunchKernelGGL((conv_small2<1, 32>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
-    case 2: hipLaunchKernelGGL((conv_small2<2, 16>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
-    case 3: hipLaunchKernelGGL((conv_small2<2, 32>), grid, dim3(kSmallThreads), g.lds_bytes, stream, a, g); break;
+    case 0: launch_small2_rp<1, 16>(a, g, stream); break;
+    case 1: launch_small2_rp<1, 32>(a, g, stream); break;
+    case 2: launch_small2_rp<2, 16>(a, g, stream); break;
+    case 3: launch_small2_rp<2, 32>(a, g, stream); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

@@ -101,6 +101,10 @@ SMALL2_POOL = [
     ("s2p_c48_ragged_rows", 3, 37, 29, 16, 48, 2, [U2]),
     ("s2p_pool3_c16", 2, 33, 27, 32, 16, 3, [U2]),
     ("s2p_pool4_c64", 1, 40, 44, 16, 64, 4, [B64]),
+    # the register pool (2x2/2, c_out <= 32): a ragged last group of pooled
+    # columns, and 4 rows per workgroup with a last tile of 2
+    ("s2p_rp_c16_cin32_ragged", 3, 38, 42, 32, 16, 2, [U2]),
+    ("s2p_rp_rows4_ragged_tile", 8, 290, 14, 16, 32, 2, [U2]),
 ]
 
 
