@@ -176,18 +176,31 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
     // raw buffer has 16 bytes of slack past its end), the channels past c_in
     // masked to the zero code
     const uint32_t keep = a.cin >= 4 ? 0xFFFFFFFFu : (1u << (8 * a.cin)) - 1u;
-    for (int e = tid; e < nin; e += kSmallThreads) {
-      const int r = fdiv(e, sg.div_win);
-      const int iy = iy0 + r, ix = e - r * sg.win - a.pad;
-      uint32_t word = 0x80808080u;
-      if ((unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w) {
-        const int b = lead + ((iy - iy_lo) * a.w + ix) * a.cin;
+    // EB pixels per thread and pass, their LDS reads all issued before the
+    // first is used (positions outside the image read byte 0 and are masked)
+    constexpr int EB = 4;
+    for (int e0 = tid; e0 < nin; e0 += EB * kSmallThreads) {
+      uint32_t lo[EB], hi[EB];
+      int sh[EB];
+      bool in[EB];
+#pragma unroll
+      for (int k = 0; k < EB; ++k) {
+        const int e = e0 + k * kSmallThreads;
+        const int r = fdiv(e, sg.div_win);
+        const int iy = iy0 + r, ix = e - r * sg.win - a.pad;
+        in[k] = e < nin && (unsigned)iy < (unsigned)a.h && (unsigned)ix < (unsigned)a.w;
+        const int b = in[k] ? lead + ((iy - iy_lo) * a.w + ix) * a.cin : 0;
         const uint32_t* w32 = reinterpret_cast<const uint32_t*>(raw + (b & ~3));
-        const uint32_t lo = w32[0], hi = w32[1];
-        const uint32_t v = __builtin_amdgcn_alignbyte(hi, lo, (uint32_t)(b & 3));
-        word ^= v & keep;                                         // 0x80 ^ x
+        lo[k] = w32[0];
+        hi[k] = w32[1];
+        sh[k] = b & 3;
       }
-      *reinterpret_cast<uint32_t*>(tile + e * 4) = word;
+#pragma unroll
+      for (int k = 0; k < EB; ++k) {
+        const int e = e0 + k * kSmallThreads;
+        const uint32_t v = __builtin_amdgcn_alignbyte(hi[k], lo[k], (uint32_t)sh[k]) & keep;
+        if (e < nin) *reinterpret_cast<uint32_t*>(tile + e * 4) = 0x80808080u ^ (in[k] ? v : 0u);
+      }
     }
   }
   // otherwise batches of SB pixels per thread: every byte load of a batch is
