@@ -58,6 +58,50 @@ def _nvar(P):
     return P.ifq_conv_variant_count()
 
 
+def _host_lib():
+    """The library for host-side queries at collection (no GPU needed), or
+    None where it is not built: then every combination is collected and the
+    test itself skips the ones no variant takes."""
+    try:
+        import paper_1911_08076_amd as P
+        P.ifq_conv_variant_count()
+        return P
+    except Exception:
+        return None
+
+
+def _thr_join(P, join, q=(0.25, 0.75, 1.25)):
+    if not join:
+        return None
+    jn = P.make_join(P.IFQ_JOIN_IDENTITY, B64, None, None, list(q))
+    jn.table = 0x1000
+    return jn
+
+
+def _combos(cases, full=False):
+    """(case, join, variant) for the variants that take the layer (the planner's
+    host-side answer), identity joins only on shape-preserving layers, and the
+    multi-tile batches only on the persistent kernel."""
+    P = _host_lib()
+    out = []
+    for c in cases:
+        name, n, h, w, cin, cout, st = c
+        for join in (False, True):
+            if join and (st != 1 or cin != cout):
+                continue
+            for v in range(NVAR):
+                if full and name in ("l1_n97", "l1_n160") and v < NVAR - 2:
+                    continue   # one tile per workgroup: the batch-64 case covers it
+                if P is not None:
+                    ob = B64 if cout % 64 == 0 else U2
+                    d = P.conv_desc(n, h, w, cin, cout, 3, st, 1, 2, 2, B64, ob)
+                    if not P.ifq_conv_variant_name(d, _thr_join(P, join), v):
+                        continue
+                out.append(pytest.param(c, join, v, id="%s-%s-v%d" % (
+                    name, "idj" if join else "thr", v)))
+    return out
+
+
 def _check(P, case, variant, join, out_layout=None):
     name, n, h, w, cin, cout, st = case
     if out_layout is None:
@@ -70,10 +114,7 @@ def _check(P, case, variant, join, out_layout=None):
     p = params_for(seed, L)
     x = codes_for(seed, (n, h, w, cin), 2)
     d = P.conv_desc(n, h, w, cin, cout, 3, st, 1, 2, 2, B64, out_layout)
-    jn = None
-    if join:
-        jn = P.make_join(P.IFQ_JOIN_IDENTITY, B64, None, None, p["q_thr"])
-        jn.table = 0x1000
+    jn = _thr_join(P, join, p["q_thr"])
     if not P.ifq_conv_variant_name(d, jn, variant):
         pytest.skip("variant %d does not take %s" % (variant, name))
     sc = x if join else None
@@ -85,20 +126,17 @@ def _check(P, case, variant, join, out_layout=None):
     assert len(np.unique(want)) > 1
 
 
-@pytest.mark.parametrize("variant", range(NVAR))
-@pytest.mark.parametrize("join", [False, True], ids=["thr", "idj"])
-@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
-def test_variant_small_bit_exact(P, case, join, variant):
+def test_variant_count(P):
     assert _nvar(P) == NVAR
+
+
+@pytest.mark.parametrize("case,join,variant", _combos(SMALL))
+def test_variant_small_bit_exact(P, case, join, variant):
     _check(P, case, variant, join)
 
 
-@pytest.mark.parametrize("variant", range(NVAR))
-@pytest.mark.parametrize("join", [False, True], ids=["thr", "idj"])
-@pytest.mark.parametrize("case", FULL, ids=[c[0] for c in FULL])
+@pytest.mark.parametrize("case,join,variant", _combos(FULL, full=True))
 def test_variant_full_size_bit_exact(P, case, join, variant):
-    if case[0] in ("l1_n97", "l1_n160") and variant < NVAR - 2:
-        pytest.skip("one tile per workgroup: covered by the batch-64 case")
     _check(P, case, variant, join)
 
 
@@ -113,18 +151,37 @@ FUSED = [(2, 56, 64, 128), (3, 28, 128, 256), (2, 14, 256, 512), (5, 13, 64, 128
          (64, 56, 64, 128), (64, 28, 128, 256), (64, 14, 256, 512)]
 
 
-@pytest.mark.parametrize("variant", range(NVAR))
-@pytest.mark.parametrize("shape", FUSED, ids=["x".join(map(str, f)) for f in FUSED])
-def test_variant_fused_downsample_bit_exact(P, shape, variant):
+def _fused_join(P, shape):
     n, hin, cin, cout = shape
-    D = make_layer("down", hin, hin, cin, cout, 1, 2, 0, 2, 0)
     ho = (hin - 1) // 2 + 1
-    L = make_layer("conv2", ho, ho, cout, cout, 3, 1, 1, join=("conv", "d", "down"))
     d = P.conv_desc(n, ho, ho, cout, cout, 3, 1, 1, 2, 2, B64, B64)
     dd = P.conv_desc(n, hin, hin, cin, cout, 1, 2, 0, 2, 0, B64, P.IFQ_LAYOUT_I32_NHWC)
     jn = P.make_join(P.IFQ_JOIN_CONV_FUSED, B64, None, None, [0.25, 0.75, 1.25], down=dd)
     jn.coef = 0x1000
     jn.down_w = 0x1000
+    return d, jn
+
+
+def _fused_combos():
+    P = _host_lib()
+    out = []
+    for f in FUSED:
+        for v in range(NVAR):
+            if P is not None:
+                d, jn = _fused_join(P, f)
+                if not P.ifq_conv_variant_name(d, jn, v):
+                    continue
+            out.append(pytest.param(f, v, id="%s-v%d" % ("x".join(map(str, f)), v)))
+    return out
+
+
+@pytest.mark.parametrize("shape,variant", _fused_combos())
+def test_variant_fused_downsample_bit_exact(P, shape, variant):
+    n, hin, cin, cout = shape
+    D = make_layer("down", hin, hin, cin, cout, 1, 2, 0, 2, 0)
+    ho = (hin - 1) // 2 + 1
+    L = make_layer("conv2", ho, ho, cout, cout, 3, 1, 1, join=("conv", "d", "down"))
+    d, jn = _fused_join(P, shape)
     if not P.ifq_conv_variant_name(d, jn, variant):
         pytest.skip("variant %d does not take %s" % (variant, shape))
     seed = 31 + hin + n
