@@ -452,7 +452,43 @@ IFQ_API ifq_status ifq_conv_forward_variant(const ifq_conv_desc* d, const void* 
                                             const ifq_join* join, void* y, int32_t* acc_dump,
                                             int32_t variant, hipStream_t stream);
 
-/* Device workspace bytes ifq_conv_forward needs for d (may be 0). Host. */
+/*
+ * The contraction of Eq. (1) split over K across workgroups, on one int8
+ * variant of the register-blocked kernel (conv_w2, variants below
+ * ifq_conv_variant_count() - 2 with ifq_conv_variant_fp4 0), for tests and
+ * tuning: ksplit workgroups per output tile, each over c_in/64/ksplit of the
+ * channel blocks, their int32 partial tiles added by the last to arrive,
+ * which runs the threshold epilogue (Eq. 7/8; no join). ifq_conv_forward
+ * takes such a split where its planner predicts one faster.
+ *   ifq_conv_split_workspace_bytes  workspace bytes of that launch, or 0 if
+ *                                   the variant cannot take the layer with
+ *                                   that split (ksplit 2 or 4 dividing the
+ *                                   variant's K groups into c_in/64) (host)
+ *   ifq_conv_forward_split          the launch, asynchronous on stream; ws
+ *                                   as for ifq_conv_forward (zero-filled
+ *                                   before its first use). Errors:
+ *                                   UNSUPPORTED where the variant cannot take
+ *                                   the layer with that split, else as
+ *                                   ifq_conv_forward.
+ */
+IFQ_API size_t ifq_conv_split_workspace_bytes(const ifq_conv_desc* d, int32_t variant,
+                                              int32_t ksplit);
+IFQ_API ifq_status ifq_conv_forward_split(const ifq_conv_desc* d, const void* x,
+                                          const void* w_packed, const int32_t* thr, void* y,
+                                          int32_t* acc_dump, int32_t variant, int32_t ksplit,
+                                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * Device workspace bytes ifq_conv_forward needs for d (may be 0). Host.
+ * Non-zero where the planner splits the contraction of Eq. (1) over K
+ * across workgroups (3x3 layers with the threshold epilogue that fill too
+ * few workgroups): the workspace holds one int32 partial tile per split and
+ * tile, and at its start a 64 KiB region of per-tile arrival counters. That
+ * region must be zero before the workspace's first use (hipMemset once);
+ * every call leaves it zero again, so a workspace serves any number of
+ * calls (on one stream at a time). The sums stay exact: integer addition
+ * is associative.
+ */
 IFQ_API size_t ifq_conv_workspace_bytes(const ifq_conv_desc* d);
 
 /*
@@ -466,7 +502,8 @@ IFQ_API size_t ifq_conv_workspace_bytes(const ifq_conv_desc* d);
  *   y          device output [n][ho][wo][c_out] in d->out_layout
  *   acc_dump   nullable device int32 [n][ho][wo][c_out]: also receives the
  *              raw sums a
- *   ws         device workspace of ws_bytes >= ifq_conv_workspace_bytes(d)
+ *   ws         device workspace of ws_bytes >= ifq_conv_workspace_bytes(d),
+ *              zero-filled before its first use (see there)
  * Errors: INVALID_ARGUMENT, UNSUPPORTED, INSUFFICIENT_BUFFER, HIP.
  */
 IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
@@ -575,7 +612,13 @@ IFQ_API ifq_status ifq_convert_codes(int64_t n, int64_t h, int64_t w, int32_t c,
                                      const void* src, void* dst,
                                      hipStream_t stream);
 
-/* Device workspace bytes of a stack (its work slots, 256-byte aligned). */
+/*
+ * Device workspace bytes of a stack: at its start the conv workspace shared
+ * by the layers (the K-split counters and partial tiles, as for
+ * ifq_conv_workspace_bytes; at least the 64 KiB counter region), then the
+ * work slots (256-byte aligned). Zero-fill it before its first use; runs
+ * leave the counter region zero, so one workspace serves any stacks.
+ */
 IFQ_API size_t ifq_stack_workspace_bytes(const ifq_stack* s);
 
 /*
@@ -606,7 +649,9 @@ IFQ_API ifq_status ifq_run_stack(const ifq_stack* s, const void* x, void* y,
  * for ifq_run_stack). Calls nothing that allocates or frees device memory.
  * Every call on one GPU shares that GPU's array and leaves the last call's
  * slot contents in it (nothing in it needs clearing: every slot is written
- * before it is read), so calls that overlap on one GPU (two streams, two
+ * before it is read, and the K-split counter region at its start is zero
+ * from the library's load and again after every run), so calls that
+ * overlap on one GPU (two streams, two
  * threads) race and must be serialised by the caller. Errors: as
  * ifq_run_stack, INSUFFICIENT_BUFFER when ifq_stack_workspace_bytes(s)
  * exceeds the static workspace (nothing is launched), HIP_ERROR when the

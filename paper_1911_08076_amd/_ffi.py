@@ -113,6 +113,9 @@ SIGNATURES = [
                                                i32]),
     ("ifq_conv_forward_variant", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp,
                                        ctypes.POINTER(Join), vp, vp, i32, vp]),
+    ("ifq_conv_split_workspace_bytes", size_t, [ctypes.POINTER(ConvDesc), i32, i32]),
+    ("ifq_conv_forward_split", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp, vp, vp, i32, i32,
+                                     vp, size_t, vp]),
     ("ifq_conv_forward", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp,
                                ctypes.POINTER(Join), vp, vp, vp, size_t, vp]),
     ("ifq_conv_forward_fp4", i32, [ctypes.POINTER(ConvDesc), vp, vp, vp,

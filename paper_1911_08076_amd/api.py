@@ -213,6 +213,13 @@ def ifq_conv_workspace_bytes(desc):
 
 def ifq_conv_forward(desc, x, w_packed, thr, y, join=None, acc_dump=None,
                      ws=None, stream=None):
+    """ws None: a zero-filled device workspace of ifq_conv_workspace_bytes
+    bytes is made for this call where the layer needs one (a K split)."""
+    if ws is None:
+        need = ifq_conv_workspace_bytes(desc)
+        if need:
+            import torch
+            ws = torch.zeros(need, dtype=torch.uint8, device=y.device)
     ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(_lib().ifq_conv_forward(
         ctypes.byref(desc), _ptr(x), _ptr(w_packed), _ptr(thr),
@@ -330,6 +337,20 @@ def ifq_conv_variant_name(desc, join, variant):
     return _lib().ifq_conv_variant_name(
         ctypes.byref(desc), ctypes.byref(join) if join is not None else None,
         int(variant)).decode()
+
+
+def ifq_conv_split_workspace_bytes(desc, variant, ksplit):
+    return int(_lib().ifq_conv_split_workspace_bytes(ctypes.byref(desc), int(variant),
+                                                     int(ksplit)))
+
+
+def ifq_conv_forward_split(desc, x, w_packed, thr, y, variant, ksplit, ws, acc_dump=None,
+                           stream=None):
+    ws_bytes = 0 if ws is None else ws.numel() * ws.element_size()
+    _check(_lib().ifq_conv_forward_split(
+        ctypes.byref(desc), _ptr(x), _ptr(w_packed), _ptr(thr), _ptr(y), _ptr(acc_dump),
+        int(variant), int(ksplit), _ptr(ws), ws_bytes, _stream(stream)),
+        "ifq_conv_forward_split")
 
 
 def ifq_conv_forward_variant(desc, x, w_packed, thr, y, variant, join=None, acc_dump=None,

@@ -288,6 +288,7 @@ ifq::ConvLaunch make_launch(const ifq_conv_desc* d, int64_t ho, int64_t wo,
   a.out_mode = d->out_bits == 0 ? 0 : d->out_layout == IFQ_LAYOUT_I8_NHWC ? 1 : 2;
   a.div_howo = ifq::make_fastdiv((uint32_t)(ho * wo > 0 ? ho * wo : 1));
   a.div_wo = ifq::make_fastdiv((uint32_t)(wo > 0 ? wo : 1));
+  a.ksplit = 1;
   return a;
 }
 
@@ -804,9 +805,61 @@ IFQ_API ifq_status ifq_conv_forward_variant(const ifq_conv_desc* d, const void* 
   return ok();
 }
 
+namespace {
+// The plan of a forced K split (int8 register-blocked variant, thresholds).
+bool split_plan(const ifq_conv_desc* d, int32_t variant, int32_t ksplit, ifq::ConvLaunch* a,
+                ifq::W2Plan* p) {
+  if (variant < 0 || variant >= ifq::w2_variant_count() || ifq::w2_variant_fp4(variant) ||
+      ksplit < 2 || ksplit > 4 || d->out_bits == 0)
+    return false;
+  a->split_ok = 1;
+  return ifq::plan_w2(*a, variant, p, ksplit) && p->ksplit == ksplit;
+}
+}  // namespace
+
+IFQ_API size_t ifq_conv_split_workspace_bytes(const ifq_conv_desc* d, int32_t variant,
+                                              int32_t ksplit) {
+  int64_t ho, wo;
+  if (!d || check_conv(d, &ho, &wo) != IFQ_OK || d->n == 0) return 0;
+  ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                  nullptr, nullptr);
+  ifq::W2Plan p;
+  if (!split_plan(d, variant, ksplit, &a, &p)) return 0;
+  return (size_t)ifq::w2_split_bytes(a, p);
+}
+
+IFQ_API ifq_status ifq_conv_forward_split(const ifq_conv_desc* d, const void* x,
+                                          const void* w_packed, const int32_t* thr, void* y,
+                                          int32_t* acc_dump, int32_t variant, int32_t ksplit,
+                                          void* ws, size_t ws_bytes, hipStream_t stream) {
+  int64_t ho, wo;
+  ifq_status st = check_conv(d, &ho, &wo);
+  if (st != IFQ_OK) return st;
+  st = conv_args_check(d, x, w_packed, thr, nullptr, nullptr, y);
+  if (st != IFQ_OK) return st;
+  if (d->n == 0) return ok();
+  ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_packed, thr, nullptr, nullptr, y, acc_dump);
+  ifq::W2Plan p;
+  if (!split_plan(d, variant, ksplit, &a, &p))
+    return fail(IFQ_ERR_UNSUPPORTED, "conv split: variant %d cannot take this layer in %d",
+                variant, ksplit);
+  const int64_t need = ifq::w2_split_bytes(a, p);
+  if ((int64_t)ws_bytes < need || !ws)
+    return fail(IFQ_ERR_INSUFFICIENT_BUFFER, "conv split: workspace needs %lld bytes",
+                (long long)need);
+  a.ws_cnt = static_cast<uint32_t*>(ws);
+  st = hip_status(ifq::launch_conv_w2(a, p, stream), "conv split launch");
+  if (st != IFQ_OK) return st;
+  return ok();
+}
+
 IFQ_API size_t ifq_conv_workspace_bytes(const ifq_conv_desc* d) {
-  (void)d;
-  return 0;
+  int64_t ho, wo;
+  if (!d || check_conv(d, &ho, &wo) != IFQ_OK) return 0;
+  ifq::ConvLaunch a = make_launch(d, ho, wo, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                  nullptr, nullptr);
+  a.split_ok = 1;
+  return (size_t)ifq::conv_workspace_bytes(a);
 }
 
 IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
@@ -820,9 +873,14 @@ IFQ_API ifq_status ifq_conv_forward(const ifq_conv_desc* d, const void* x,
   const void* sc = (join && join->kind != IFQ_JOIN_NONE) ? join->shortcut : nullptr;
   st = conv_args_check(d, x, w_packed, thr, join, sc, y);
   if (st != IFQ_OK) return st;
-  if (ws_bytes < ifq_conv_workspace_bytes(d) || (ifq_conv_workspace_bytes(d) && !ws))
-    return fail(IFQ_ERR_INSUFFICIENT_BUFFER, "conv: workspace too small");
-  const ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_packed, thr, join, sc, y, acc_dump);
+  const size_t need = ifq_conv_workspace_bytes(d);
+  if (ws_bytes < need || (need && !ws))
+    return fail(IFQ_ERR_INSUFFICIENT_BUFFER, "conv: workspace needs %zu bytes", need);
+  ifq::ConvLaunch a = make_launch(d, ho, wo, x, w_packed, thr, join, sc, y, acc_dump);
+  if (need) {   // the K split the workspace was sized for
+    a.split_ok = 1;
+    a.ws_cnt = static_cast<uint32_t*>(ws);
+  }
   st = hip_status(ifq::launch_conv(a, stream), "conv launch");
   if (st != IFQ_OK) return st;
   return ok();
@@ -1194,13 +1252,17 @@ ifq_status plan_stack(const ifq_stack* s, SlotPlan* plan) {
     last_bits[L.dst] = layer_out_bits(L);
     written[L.dst] = 1;
   }
-  int64_t off = 0;
+  // the conv workspace first, its K-split counters at offset 0 for every
+  // stack (at least the counter region, so that no stack's slots overwrite
+  // another's counters in a shared workspace), then the slots
+  plan->conv_ws = ifq::round_up(std::max<int64_t>(plan->conv_ws, ifq::kSplitCounterBytes), 256);
+  int64_t off = plan->conv_ws;
   for (int k = 2; k < s->n_slots; ++k) {
     plan->offset[k] = off;
     off += ifq::round_up(plan->bytes[k], 256);
   }
   plan->slots_bytes = off;
-  plan->total = off + ifq::round_up(plan->conv_ws, 256);
+  plan->total = off;
   return IFQ_OK;
 }
 
@@ -1241,7 +1303,7 @@ IFQ_API ifq_status ifq_run_stack(const ifq_stack* s, const void* x, void* y,
     if (k == 1) return y;
     return base + plan.offset[k];
   };
-  void* conv_ws = base ? base + plan.slots_bytes : nullptr;
+  void* conv_ws = base;   // offset 0: the K-split counters, then partials
   for (int i = 0; i < s->n_layers; ++i) {
     const ifq_layer& L = s->layers[i];
     if (s->events) {
@@ -1254,9 +1316,12 @@ IFQ_API ifq_status ifq_run_stack(const ifq_stack* s, const void* x, void* y,
       if (j.kind != IFQ_JOIN_NONE) sc = slot(L.join_src);
       int64_t ho = out_extent(L.conv.h, L.conv.kh, L.conv.stride, L.conv.pad);
       int64_t wo = out_extent(L.conv.w, L.conv.kw, L.conv.stride, L.conv.pad);
-      const ifq::ConvLaunch a = make_launch(&L.conv, ho, wo, slot(L.src), L.w_packed,
-                                            L.thr, &j, sc, slot(L.dst), nullptr);
-      (void)conv_ws;
+      ifq::ConvLaunch a = make_launch(&L.conv, ho, wo, slot(L.src), L.w_packed,
+                                      L.thr, &j, sc, slot(L.dst), nullptr);
+      if (ifq_conv_workspace_bytes(&L.conv) > 0) {   // sized into plan.conv_ws
+        a.split_ok = 1;
+        a.ws_cnt = static_cast<uint32_t*>(conv_ws);
+      }
       st = hip_status(ifq::launch_conv(a, stream), "conv launch");
     } else if (L.kind == IFQ_LAYER_CONV_POOL_FP4) {
       st = ifq_conv_pool_forward_fp4(&L.conv, &L.pool, slot(L.src), L.w_packed, L.thr,

@@ -341,6 +341,11 @@ const char* conv_kernel_name(const ConvLaunch& a) {
   return names[gather_kind(a)][tile_variant(a)];
 }
 
+int64_t conv_workspace_bytes(const ConvLaunch& a) {
+  if (a.m == 0 || a.pool_k || head_eligible(a)) return 0;
+  return mfma_eligible(a) ? conv_mfma_workspace_bytes(a) : 0;
+}
+
 hipError_t launch_conv(const ConvLaunch& a, hipStream_t stream) {
   if (a.m == 0) return hipSuccess;
   if (a.pool_k) {

@@ -393,6 +393,19 @@ const char* conv_mfma_name(const ConvLaunch& a) {
   return kVariants[pl.variant].name;
 }
 
+// The workspace of the kernel launch_conv_mfma picks (the same choice).
+int64_t conv_mfma_workspace_bytes(const ConvLaunch& a) {
+  HaloPlan hp;
+  const bool halo = plan_halo(a, &hp);
+  Reg3Plan rp;
+  const bool r3 = plan_reg3(a, -1, &rp);
+  if (!r3 || rp.persistent) return 0;
+  if (a.join_kind == IFQ_JOIN_CONV_FUSED) return w2_split_bytes(a, rp.w2);
+  const Plan pl = plan_mfma(a);
+  if (rp.t_us <= pl.t_us && (!halo || rp.t_us <= hp.t_us)) return w2_split_bytes(a, rp.w2);
+  return 0;
+}
+
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream) {
   HaloPlan hp;
   const bool halo = plan_halo(a, &hp);

@@ -28,6 +28,14 @@
 // downsample computed in the kernel (its weights arrive as one extra stage of
 // the ring, its strided input cells in the prologue) and the fp64 join of
 // ifq_epilogue.h on the transposed layout. Optional int32 dump of the sums.
+//
+// K split across workgroups (threshold epilogue only, a.ksplit > 1): the
+// grid's z index picks a range of c_in/64/ksplit channel blocks. Each
+// workgroup of a tile writes its int32 partial tile to the workspace,
+// fences, and counts its arrival on the tile's counter; the one that
+// arrives last adds the other partials to its own (integer addition is
+// associative, so the sums are exact) and runs the epilogue. No workgroup
+// waits for another, and the counter returns to zero with the last arrival.
 #include <hip/hip_runtime.h>
 
 #include "ifq_epilogue.h"
@@ -98,8 +106,10 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
   const int bn = a.bn;
   const int p0 = blockIdx.x * bn;
   const int co0 = blockIdx.y * BM;
-  const int G = a.cin >> 6;
-  const int nst = (G / WK) * TSTEPS;
+  const int G = a.cin >> 6;                      // channel blocks of the layer
+  const int Gs = G / a.ksplit;                   // of this workgroup's K range
+  const int gbase = blockIdx.z * Gs;
+  const int nst = (Gs / WK) * TSTEPS;
   const int H = a.h, W = a.w, Wo = a.wo, st = a.stride;
   const int howo = a.ho * a.wo;
   const int HW = H * W;
@@ -109,7 +119,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
   const uint8_t* zero_src = reinterpret_cast<const uint8_t*>(&g_zero_cell);
 
   // zero cell after every block window
-  for (int g = tid; g < G; g += NT)
+  for (int g = tid; g < Gs; g += NT)
     *reinterpret_cast<uint4*>(lds + WIN0 + g * wstr + wcells * 16) = uint4{0, 0, 0, 0};
 
   // ---- the tile's images (segments) and their input row spans ------------
@@ -206,8 +216,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
       for (; j < nch; j += NW) {
         const int c = j * 64 + lane;
         const int64_t src = ((int64_t)(n_first + i) * G * HW + iya * W + c) * 16;
-        for (int g = 0; g < G; ++g)
-          dma16(c < cells ? a.x + src + (int64_t)g * HW * 16 : zero_src,
+        for (int g = 0; g < Gs; ++g)
+          dma16(c < cells ? a.x + src + (int64_t)(gbase + g) * HW * 16 : zero_src,
                 lds0 + WIN0 + (uint32_t)(g * wstr + (off + j * 64) * 16));
       }
       jbase += nch;
@@ -233,7 +243,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
         const int rb = (c / KH) % RB;
         const int kt = c / (KH * RB);
         const int tau = kt % T, kq = kt / T;
-        const int kk = (gi * WK + kq) * kW2Taps + tap0 + tau;
+        const int kk = (gbase + gi * WK + kq) * kW2Taps + tap0 + tau;
         const int64_t off =
             rbw + rb < nrb ? ((int64_t)(rbw + rb) * (KH * a.nk) + KH * kk + t) * 1024 : a.wzero;
         dma16s(wbase + off, voff, slot + (uint32_t)(c * 1024));
@@ -389,7 +399,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
   // MFMAs of tap tau. The first wait also covers the windows and records,
   // issued before stage 0. Taps are compile-time indices (the stage loop is
   // unrolled per block), so boff stays in registers.
-  const int nG = G / WK;
+  const int nG = Gs / WK;
   int slot = 0;
   for (int gi = 0; gi < nG; ++gi) {
     const uint8_t* win = lds + WIN0 + (gi * WK + kg) * wstr;
@@ -508,6 +518,52 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
     __syncthreads();
   }
 
+  // ---- K split across workgroups: partial tiles through the workspace ------
+  if (MODE == 0 && a.ksplit > 1) {
+    const int S = a.ksplit;
+    const int tile = blockIdx.y * gridDim.x + blockIdx.x;
+    constexpr int PER = NB * 16;                 // int32 per thread
+    int32_t* part = a.ws_part + (int64_t)tile * S * (NT * PER);
+    int32_t* mine = part + (int64_t)blockIdx.z * (NT * PER) + tid * PER;
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        *reinterpret_cast<v4i*>(mine + j * 16 + 4 * q) =
+            v4i{own[j][4 * q], own[j][4 * q + 1], own[j][4 * q + 2], own[j][4 * q + 3]};
+    // every wave's stores have reached the L2 before the barrier; then one
+    // device-scope fence (an L2 write-back for the whole workgroup) and the
+    // arrival, whose count wraps to zero at the last of the S arrivals; the
+    // last arrival's fence invalidates the caches the partials are read
+    // through (one per workgroup: the waves share them)
+    wait_vmcnt<0>();
+    __syncthreads();
+    volatile int* flag = reinterpret_cast<volatile int*>(lds);
+    if (tid == 0) {
+      __threadfence();
+      const bool last = atomicInc(a.ws_cnt + tile, (unsigned)(S - 1)) == (unsigned)(S - 1);
+      if (last) __threadfence();
+      *flag = last;
+    }
+    __syncthreads();
+    if (!*flag) return;
+    for (int z = 0; z < S; ++z) {
+      if (z == (int)blockIdx.z) continue;
+      const int32_t* src = part + (int64_t)z * (NT * PER) + tid * PER;
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const v4i v = *reinterpret_cast<const v4i*>(src + j * 16 + 4 * q);
+          own[j][4 * q] += v.x;
+          own[j][4 * q + 1] += v.y;
+          own[j][4 * q + 2] += v.z;
+          own[j][4 * q + 3] += v.w;
+        }
+    }
+    __syncthreads();   // the flag word before the epilogue's tile writes
+  }
+
   // ---- epilogue -------------------------------------------------------------
   if constexpr (MODE == 1)
     stage_idj_pk(reinterpret_cast<const int32_t*>(lds + THR), lds, BM,
@@ -595,6 +651,17 @@ const W2Variant kW2Variants[] = {
 };
 constexpr int kNumW2 = sizeof(kW2Variants) / sizeof(kW2Variants[0]);
 constexpr int kW2CUs = 256;
+// K split across workgroups: at most 4 ways; per round of a split tile, the
+// partial's write, fence and arrival, and each other partial the last
+// arrival adds. Measured on MI355X (Tiny-YOLOv2 c7, 13x13x512 -> 512 at
+// batch 8, split 2 on 2 x 88 workgroups): 26-30 us against 11.5 us
+// unsplit. The device-scope fence that publishes a partial is an L2
+// write-back of the whole XCD's L2, one per workgroup, and those serialise;
+// so the fixed cost below keeps the planner from splitting any layer of
+// the benchmark stacks, and ifq_conv_forward_split runs it on request.
+constexpr int kW2MaxSplit = 4;
+constexpr double kW2SplitUs = 19.0;
+constexpr double kW2SplitAddUs = 0.3;
 
 // The epilogues this kernel has: 2-bit codes with the packed 16-bit compares
 // (sums and thresholds below 2^15), no pool, and either thresholds or an
@@ -616,7 +683,7 @@ bool w2_mode_ok(const ConvLaunch& a) {
 
 // Pixels per workgroup and the predicted time of variant v on layer a, or
 // false if v cannot take it.
-bool w2_fit(const ConvLaunch& a, int v, W2Plan* out) {
+bool w2_fit(const ConvLaunch& a, int v, W2Plan* out, int want_split) {
   const W2Variant& V = kW2Variants[v];
   if (V.f4 != (a.f4 != 0)) return false;
   const int G = a.cin / 64;
@@ -627,46 +694,76 @@ bool w2_fit(const ConvLaunch& a, int v, W2Plan* out) {
       (a.d_cin / 64 > V.wk * V.t || (V.occ == 2 && V.wm * V.wn * V.wk == 8 && V.fn == 2)))
     return false;
   const int bm = 32 * V.fm * V.wm, bnmax = 32 * V.fn * V.wn;
-  const int64_t slots = (int64_t)kW2CUs * V.occ;
   const int64_t nco = (a.cout + bm - 1) / bm;
   const int64_t nb_min = (a.m + bnmax - 1) / bnmax;
-  const int64_t rounds = (nco * nb_min + slots - 1) / slots;
-  int64_t nb = rounds * slots / nco;
-  if (nb < nb_min) nb = nb_min;
-  int64_t bn = (a.m + nb - 1) / nb;
-  bn = (bn + 31) / 32 * 32;
-  if (bn > bnmax) bn = bnmax;
-  const int64_t cells = window_cells_max(a, bn, (int64_t)V.winb / 16 / G);
-  if (cells < 0 || (int64_t)G * (cells + 1) * 16 > V.winb) return false;
-  const int64_t blocks = nco * ((a.m + bn - 1) / bn);
-  // the busiest CU's tiles and rounds of occ tiles, each tile's weight
-  // stages (the fused downsample's weights are one more)
-  const int64_t per_cu = (blocks + kW2CUs - 1) / kW2CUs;
-  const int64_t cu_rounds = (per_cu + V.occ - 1) / V.occ;
-  const int64_t stages = (G / V.wk) * (kW2Taps / V.t) + (a.join_kind == IFQ_JOIN_CONV_FUSED);
+  // per K split S (S workgroups per tile, each over 1/S of the channel
+  // blocks): pixel tiles sized so that the S * tiles workgroups fill whole
+  // rounds of occ per CU; the busiest CU's rounds and weight stages (the
+  // fused downsample's weights are one more stage), and for S > 1 the
+  // partial tile's round trip through the workspace per round
   const double c_round = V.c0_us + (a.join_kind != IFQ_JOIN_NONE ? V.cj_us : 0.0);
-  const double t = kLaunchUs + (double)cu_rounds * c_round + (double)(per_cu * stages) * V.cs_us;
-  *out = W2Plan{v, (int)bn, (int)((a.m + bn - 1) / bn), (int)cells, t};
+  W2Plan best{};
+  bool have = false;
+  for (int S = 1; S <= kW2MaxSplit; S *= 2) {
+    if (S > 1 && !(a.split_ok && a.join_kind == IFQ_JOIN_NONE && !V.f4 && G % (S * V.wk) == 0))
+      break;
+    if (want_split > 0 && S != want_split) continue;
+    const int64_t slots = (int64_t)kW2CUs * V.occ / S;
+    const int64_t rounds = (nco * nb_min + slots - 1) / slots;
+    int64_t nb = rounds * slots / nco;
+    if (nb < nb_min) nb = nb_min;
+    int64_t bn = (a.m + nb - 1) / nb;
+    bn = (bn + 31) / 32 * 32;
+    if (bn > bnmax) bn = bnmax;
+    // a workgroup holds the windows of its own G / S channel blocks
+    const int64_t gs = G / S;
+    const int64_t cells = window_cells_max(a, bn, (int64_t)V.winb / 16 / gs);
+    if (cells < 0 || gs * (cells + 1) * 16 > V.winb) continue;
+    const int64_t blocks = nco * ((a.m + bn - 1) / bn);
+    if (S > 1 && blocks > kSplitMaxTiles) continue;
+    const int64_t wgs = blocks * S;
+    const int64_t per_cu = (wgs + kW2CUs - 1) / kW2CUs;
+    const int64_t cu_rounds = (per_cu + V.occ - 1) / V.occ;
+    const int64_t stages =
+        (G / S / V.wk) * (kW2Taps / V.t) + (a.join_kind == IFQ_JOIN_CONV_FUSED);
+    const double split_us = S > 1 ? kW2SplitUs + kW2SplitAddUs * (S - 1) : 0.0;
+    const double t = kLaunchUs + (double)cu_rounds * (c_round + split_us) +
+                     (double)(per_cu * stages) * V.cs_us;
+    if (!have || t < best.t_us) {
+      best = W2Plan{v, (int)bn, (int)((a.m + bn - 1) / bn), (int)cells, t, S};
+      have = true;
+    }
+  }
+  if (!have) return false;
+  *out = best;
   return true;
 }
 
 }  // namespace
 
 int w2_variant_count() { return kNumW2; }
+
+int64_t w2_split_bytes(const ConvLaunch& a, const W2Plan& p) {
+  if (p.ksplit <= 1) return 0;
+  const W2Variant& V = kW2Variants[p.variant];
+  const int64_t bm = 32 * V.fm * V.wm, bn = 32 * V.fn * V.wn;
+  const int64_t tiles = (int64_t)p.blocks_m * ((a.cout + bm - 1) / bm);
+  return kSplitCounterBytes + tiles * p.ksplit * bm * bn * 4;
+}
 bool w2_variant_fp4(int v) { return v >= 0 && v < kNumW2 && kW2Variants[v].f4; }
 
-bool plan_w2(const ConvLaunch& a, int forced, W2Plan* out) {
+bool plan_w2(const ConvLaunch& a, int forced, W2Plan* out, int want_split) {
   if (!(a.in_layout == IFQ_LAYOUT_U2_BLOCK64 && a.in_bits == 2 && a.cin % 64 == 0 &&
         a.kh == 3 && a.kw == 3 && a.pad == 1 && (a.stride == 1 || a.stride == 2) && a.m > 0))
     return false;
   if (!w2_mode_ok(a)) return false;
   // 32-bit cell indices and offsets
   if ((int64_t)a.n * a.h * a.w * (a.cin / 64) >= (int64_t)1 << 26) return false;
-  if (forced >= 0) return forced < kNumW2 && w2_fit(a, forced, out);
+  if (forced >= 0) return forced < kNumW2 && w2_fit(a, forced, out, want_split);
   bool found = false;
   for (int v = 0; v < kNumW2; ++v) {
     W2Plan p;
-    if (w2_fit(a, v, &p) && (!found || p.t_us < out->t_us)) {
+    if (w2_fit(a, v, &p, want_split) && (!found || p.t_us < out->t_us)) {
       *out = p;
       found = true;
     }
@@ -686,7 +783,13 @@ hipError_t launch_conv_w2(ConvLaunch a, const W2Plan& p, hipStream_t stream) {
   a.wcells = p.wcells;
   const W2Variant& V = kW2Variants[p.variant];
   const int bm = 32 * V.fm * V.wm;
-  const dim3 grid(p.blocks_m, (a.cout + bm - 1) / bm);
+  a.ksplit = p.ksplit > 1 ? p.ksplit : 1;
+  if (a.ksplit > 1) {
+    if (!a.ws_cnt) return hipErrorInvalidValue;   // the caller's workspace
+    a.ws_part = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(a.ws_cnt) +
+                                           kSplitCounterBytes);
+  }
+  const dim3 grid(p.blocks_m, (a.cout + bm - 1) / bm, a.ksplit);
   const dim3 block(64 * V.wm * V.wn * V.wk);
   const int mode = a.join_kind == IFQ_JOIN_IDENTITY ? 1 : a.join_kind == IFQ_JOIN_CONV_FUSED ? 2 : 0;
   switch (p.variant * 3 + mode) {

@@ -130,6 +130,15 @@ struct ConvLaunch {
   FastDiv div_pho;     // division by pho (pooled row -> image)
   int32_t wcells;      // register-blocked 3x3 kernels: window cells per channel block
   int32_t tiles_wg;    // persistent 3x3 kernel: consecutive pixel tiles per workgroup
+  // K split across workgroups (register-blocked 3x3 kernel, threshold
+  // epilogue): split_ok lets the planner split (a workspace is at hand);
+  // ksplit workgroups per tile, each over c_in/64/ksplit channel blocks,
+  // their int32 partial tiles in ws_part and one arrival counter per tile in
+  // ws_cnt (zero before the launch, zero again after it)
+  int32_t split_ok;
+  int32_t ksplit;
+  uint32_t* ws_cnt;
+  int32_t* ws_part;
 };
 
 // Whether the pooled epilogue takes this launch: codes out (no join), and
@@ -142,6 +151,11 @@ inline bool pool_epilogue_ok(const ConvLaunch& a) {
 }
 
 hipError_t launch_conv(const ConvLaunch& a, hipStream_t stream);
+
+// Workspace bytes launch_conv needs for these arguments (a K split planned
+// with a.split_ok set), 0 if none.
+int64_t conv_workspace_bytes(const ConvLaunch& a);
+int64_t conv_mfma_workspace_bytes(const ConvLaunch& a);
 
 // Name of the kernel launch_conv would pick for these arguments.
 const char* conv_kernel_name(const ConvLaunch& a);
@@ -227,10 +241,22 @@ struct W2Plan {
   int blocks_m;
   int wcells;
   double t_us;
+  int ksplit;     // workgroups per tile along K (1: no split)
 };
+// Workspace of a K-split conv: a fixed region of arrival counters (one per
+// tile, at most kSplitMaxTiles) at offset 0, which must be zero before the
+// first use and is zero again after every launch, then the partial tiles.
+// The region sits at the same place for every layer and every stack, so no
+// layer's partials or slots ever land on another layer's counters.
+constexpr int64_t kSplitCounterBytes = 64 << 10;
+constexpr int64_t kSplitMaxTiles = kSplitCounterBytes / 4;
+// Workspace bytes of a K-split launch of plan p (0 without a split).
+int64_t w2_split_bytes(const ConvLaunch& a, const W2Plan& p);
 int w2_variant_count();
 bool w2_variant_fp4(int v);   // variant v runs the fp4 contraction (fp4 weight blob)
-bool plan_w2(const ConvLaunch& a, int forced, W2Plan* out);
+// want_split > 0: only plans with that K split (a.split_ok must be set for
+// any split above 1).
+bool plan_w2(const ConvLaunch& a, int forced, W2Plan* out, int want_split = 0);
 hipError_t launch_conv_w2(ConvLaunch a, const W2Plan& p, hipStream_t stream);
 const char* conv_w2_name(const W2Plan& p, const ConvLaunch& a);
 

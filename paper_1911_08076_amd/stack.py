@@ -287,7 +287,9 @@ class DeviceStack:
         if nbytes == 0 and self.n_slots > 2:
             raise api.IfqError(-1, "ifq_stack_workspace_bytes",
                                api.ifq_last_error())
-        self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8,
+        # zero-filled once: the K-split arrival counters at its start must
+        # be zero before the first run (every run leaves them zero)
+        self.ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8,
                               device=self.device)
 
     def _pool_fusions(self, code_layout, fuse=True):
@@ -465,8 +467,11 @@ class DeviceStack:
             if rec.join.kind != 0:
                 join = _ffi.Join.from_buffer_copy(rec.join)
                 join.shortcut = self._slot_ptr(rec.join_src, x, y)
+            # the stack workspace: its conv region (offset 0) is what
+            # ifq_run_stack hands a K-split layer
             args = (ctypes.byref(desc), src, vp(rec.w_packed), vp(rec.thr),
-                    None if join is None else ctypes.byref(join), dst, None, None, 0, st)
+                    None if join is None else ctypes.byref(join), dst, None,
+                    vp(self.ws.data_ptr()), self.ws.numel(), st)
             fn = lib.ifq_conv_forward
             what = "ifq_conv_forward"
         elif rec.kind == IFQ_LAYER_CONV_FP4:

@@ -51,7 +51,8 @@ def oracle_layer(L, x, p, shortcut=None, down=None):
 
 
 def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
-              sc_layout=I8, down=None, dump=True, fused_down=None, variant=None):
+              sc_layout=I8, down=None, dump=True, fused_down=None, variant=None,
+              split=None):
     """Run one conv through ifq_conv_forward; returns (acc or None, output).
 
     output is uint8 codes NHWC (packed [..., c/4] for U2, [n][c/64][h][w][16]
@@ -59,7 +60,10 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
     downsample layer D (params down) runs inside the kernel on the BLOCK64
     codes xin (IFQ_JOIN_CONV_FUSED) instead of reading its sums. variant:
     run that variant of the register-blocked 3x3 kernel
-    (ifq_conv_forward_variant) instead of the kernel ifq_conv_forward picks."""
+    (ifq_conv_forward_variant) instead of the kernel ifq_conv_forward picks.
+    split = (variant, ksplit, ws): that int8 variant with its contraction
+    split over ksplit workgroups (ifq_conv_forward_split) on workspace ws
+    (None: a fresh zero-filled one)."""
     import torch
     if out_layout is None:
         out_layout = I32 if L.out_bits == 0 else I8
@@ -119,8 +123,17 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
     if dump:
         acc = torch.empty(max(n * ho * wo * L.cout, 1), dtype=torch.int32,
                           device=device())
-    if variant is None:
-        P.ifq_conv_forward(d, xd, wd, td, y, join=join, acc_dump=acc)
+    if split is not None:
+        sv, ks, ws = split
+        if ws is None:
+            ws = torch.zeros(P.ifq_conv_split_workspace_bytes(d, sv, ks), dtype=torch.uint8,
+                             device=device())
+        P.ifq_conv_forward_split(d, xd, wd, td, y, sv, ks, ws, acc_dump=acc)
+    elif variant is None:
+        # a K-split launch needs its workspace, zero-filled before first use
+        wsb = P.ifq_conv_workspace_bytes(d)
+        ws = torch.zeros(wsb, dtype=torch.uint8, device=device()) if wsb else None
+        P.ifq_conv_forward(d, xd, wd, td, y, join=join, acc_dump=acc, ws=ws)
     else:
         name = P.ifq_conv_variant_name(d, join, variant)
         assert name.startswith(("conv_w2<", "conv_wp<")), (variant, name)

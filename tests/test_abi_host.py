@@ -771,3 +771,53 @@ def test_run_stack_static_host_side():
     assert P.ifq_stack_workspace_bytes(st) > cap
     assert lib.ifq_run_stack_static(ctypes.byref(st), FAKE, FAKE, None) == EBUF
     assert "static workspace" in P.ifq_last_error()
+
+
+# ---------------------------------------------------------------------------
+# K split across workgroups: workspace sizing and host-side checks (the
+# launches themselves are GPU tests)
+B64L = P.IFQ_LAYOUT_U2_BLOCK64
+
+
+def test_split_workspace_sizes():
+    # the planner prices a split with its measured cost (a device-scope
+    # fence per workgroup), above the unsplit launch of every benchmark
+    # layer, even the detector's 13x13 512->512 layers that fill 88 of 256
+    # CUs: no workspace is asked for
+    for shape in ((8, 13, 13, 512, 512), (64, 56, 56, 64, 64), (1, 13, 13, 512, 512)):
+        d = P.conv_desc(*shape, 3, 1, 1, 2, 2, B64L, B64L)
+        assert P.ifq_conv_workspace_bytes(d) == 0, shape
+    # forced splits: 64 KiB of counters, then ksplit partial tiles of
+    # BM x BN int32 per tile (variant 0: 128 x 256 tiles, one K group)
+    l4 = P.conv_desc(64, 7, 7, 512, 512, 3, 1, 1, 2, 2, B64L, B64L)
+    for s in (2, 4):
+        b = P.ifq_conv_split_workspace_bytes(l4, 0, s)
+        assert b > 64 << 10 and (b - (64 << 10)) % (s * 128 * 256 * 4) == 0
+    assert P.ifq_conv_split_workspace_bytes(l4, 0, 1) == 0   # not a split
+    assert P.ifq_conv_split_workspace_bytes(l4, 0, 3) == 0   # 3 does not divide 8 blocks
+    assert P.ifq_conv_split_workspace_bytes(l4, 2, 4) == 0   # 4 K groups x 4 > 8 blocks
+    fp4 = [v for v in range(P.ifq_conv_variant_count()) if P.ifq_conv_variant_fp4(v) == 1]
+    assert fp4 and all(P.ifq_conv_split_workspace_bytes(l4, v, 2) == 0 for v in fp4)
+    i32 = P.conv_desc(64, 7, 7, 512, 512, 3, 1, 1, 2, 0, B64L, P.IFQ_LAYOUT_I32_NHWC)
+    assert P.ifq_conv_split_workspace_bytes(i32, 0, 2) == 0  # threshold epilogue only
+
+
+def test_split_rejects_small_workspace():
+    lib = _ffi.load()
+    l4 = P.conv_desc(64, 7, 7, 512, 512, 3, 1, 1, 2, 2, B64L, B64L)
+    need = P.ifq_conv_split_workspace_bytes(l4, 0, 2)
+    assert lib.ifq_conv_forward_split(ctypes.byref(l4), FAKE, FAKE, FAKE, FAKE, None, 0, 2,
+                                      FAKE, need - 1, None) == EBUF
+    assert lib.ifq_conv_forward_split(ctypes.byref(l4), FAKE, FAKE, FAKE, FAKE, None, 0, 3,
+                                      FAKE, 1 << 30, None) == EUNSUP
+
+
+@pytest.mark.parametrize("cfg", [0, 3, 4])
+def test_stack_slots_follow_the_counter_region(cfg):
+    # every stack's conv workspace, with the split counters at offset 0,
+    # comes first, so that no stack's slots land on another's counters
+    st, slots = make_stack(get_stack(cfg).layers, 2, "i8" if cfg == 4 else "b64")
+    for name, k in slots.items():
+        if k >= 2:
+            off, nb = P.ifq_stack_slot_info(st, k)
+            assert off >= 64 << 10
