@@ -29,7 +29,7 @@
 // the ring, its strided input cells in the prologue) and the fp64 join of
 // ifq_epilogue.h on the transposed layout. Optional int32 dump of the sums.
 //
-// K split across workgroups (threshold epilogue only, a.ksplit > 1): the
+// K split across workgroups (MODE 3: the threshold epilogue, a.ksplit > 1): the
 // grid's z index picks a range of c_in/64/ksplit channel blocks. Each
 // workgroup of a tile writes its int32 partial tile to the workspace,
 // fences, and counts its arrival on the tile's counter; the one that
@@ -54,8 +54,11 @@ template <int WM, int WN, int WK, int FM, int FN, int T, int D, int MODE, bool F
           int WINB>
 __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void conv_w2(
     ConvLaunch a) {
-  constexpr bool SW = MODE != 1;                 // transposed sums
-  constexpr bool FUSED = MODE == 2;
+  // MODE 3: the threshold epilogue (0) with the K split across workgroups
+  constexpr bool SPLIT = MODE == 3;
+  constexpr int EM = SPLIT ? 0 : MODE;           // the epilogue
+  constexpr bool SW = EM != 1;                 // transposed sums
+  constexpr bool FUSED = EM == 2;
   constexpr int GDM = 4;                         // downsample channel blocks at most
   constexpr int NW = WM * WN * WK;
   constexpr int NT = 64 * NW;
@@ -80,15 +83,15 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
   constexpr int RED_BYTES = WK > 1 ? NW * NOK * 4096 : 0;
   // staged epilogue parameters: the identity join's records, or the
   // downsample join's {p, q, cc} per channel (at kJoinCoefOff)
-  constexpr int EPI_BYTES = MODE == 1 ? BM * 128 : MODE == 2 ? (kJoinCoefOff + BM * 24 + 15) / 16 * 16 : 0;
+  constexpr int EPI_BYTES = EM == 1 ? BM * 128 : EM == 2 ? (kJoinCoefOff + BM * 24 + 15) / 16 * 16 : 0;
   constexpr int OUT_BYTES = BN * BM / 4;         // 2-bit output tile
   // prefetched per-channel records: thresholds, join records or coefficients
-  constexpr int TBL_BYTES = MODE == 0 ? BM * 16 : MODE == 1 ? BM * 64 : (BM * 24 + 1023) / 1024 * 1024;
+  constexpr int TBL_BYTES = EM == 0 ? BM * 16 : EM == 1 ? BM * 64 : (BM * 24 + 1023) / 1024 * 1024;
   constexpr int THR = w2_max(w2_max(DUMMY + 1024, RED_BYTES), EPI_BYTES + OUT_BYTES);
   // the tile's shortcut cells [BM/64 blocks][BN pixels] (identity join) or
   // the downsample's strided input cells [GDM blocks][BN pixels], 16 B each
   constexpr int SCB = THR + TBL_BYTES;
-  constexpr int SC_BYTES = MODE == 1 ? (BM / 64) * BN * 16 : MODE == 2 ? GDM * BN * 16 : 0;
+  constexpr int SC_BYTES = EM == 1 ? (BM / 64) * BN * 16 : EM == 2 ? GDM * BN * 16 : 0;
   constexpr int LDS_BYTES = SCB + SC_BYTES;
   static_assert(LDS_BYTES <= 160 * 1024, "LDS");
 
@@ -107,8 +110,8 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
   const int p0 = blockIdx.x * bn;
   const int co0 = blockIdx.y * BM;
   const int G = a.cin >> 6;                      // channel blocks of the layer
-  const int Gs = G / a.ksplit;                   // of this workgroup's K range
-  const int gbase = blockIdx.z * Gs;
+  const int Gs = SPLIT ? G / a.ksplit : G;       // of this workgroup's K range
+  const int gbase = SPLIT ? (int)blockIdx.z * Gs : 0;
   const int nst = (Gs / WK) * TSTEPS;
   const int H = a.h, W = a.w, Wo = a.wo, st = a.stride;
   const int howo = a.ho * a.wo;
@@ -141,13 +144,13 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
 
   // ---- prologue: the epilogue's per-channel records, the windows of all
   // channel blocks, then stages 0 .. D-2 of the weight ring --------------------
-  if constexpr (MODE == 0) {
+  if constexpr (EM == 0) {
     for (int q = wave; q < BM / 64; q += NW) {
       const int c = co0 + q * 64 + lane;
       dma16(c < a.cout ? reinterpret_cast<const uint8_t*>(a.thr + (int64_t)c * 4) : zero_src,
             lds0 + THR + q * 1024);
     }
-  } else if constexpr (MODE == 2) {
+  } else if constexpr (EM == 2) {
     // the join coefficients of the tile's channels (24 bytes each, as 16-byte
     // pieces; c_out % 32 == 0 keeps every piece inside the array or past it)
     const uint8_t* cf8 = reinterpret_cast<const uint8_t*>(a.coef);
@@ -519,7 +522,7 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
   }
 
   // ---- K split across workgroups: partial tiles through the workspace ------
-  if (MODE == 0 && a.ksplit > 1) {
+  if constexpr (SPLIT) {
     const int S = a.ksplit;
     const int tile = blockIdx.y * gridDim.x + blockIdx.x;
     constexpr int PER = NB * 16;                 // int32 per thread
@@ -565,10 +568,10 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
   }
 
   // ---- epilogue -------------------------------------------------------------
-  if constexpr (MODE == 1)
+  if constexpr (EM == 1)
     stage_idj_pk(reinterpret_cast<const int32_t*>(lds + THR), lds, BM,
                  a.cout - co0 < BM ? a.cout - co0 : BM);
-  if constexpr (MODE == 2) {
+  if constexpr (EM == 2) {
     const double* src = reinterpret_cast<const double*>(lds + THR);
     double* dst = reinterpret_cast<double*>(lds + kJoinCoefOff);
     for (int i = tid; i < BM * 3; i += NT) dst[i] = src[i];
@@ -582,11 +585,11 @@ __global__ __launch_bounds__(64 * WM * WN * WK, (WM * WN * WK / 4) * OCC) void c
     const int rbl = wm * FM + b / FN;            // row block in the tile
     const int pcb = wn * FN + b % FN;            // pixel column block in the tile
     const v16i one[1] = {own[j]};
-    if constexpr (MODE == 0) {
+    if constexpr (EM == 0) {
       if (a.acc_dump) dump_acc_t<1>(a, one, rbl, h, l32, co0, p0, pcb * 32, bn, a.acc_dump);
       epilogue_thr_pk_t<1>(a, reinterpret_cast<const int4*>(lds + THR), one, rbl, h, l32, co0,
                            pcb * 32, otile, orow);
-    } else if constexpr (MODE == 2) {
+    } else if constexpr (EM == 2) {
       if (a.acc_dump) dump_acc_t<1>(a, one, rbl, h, l32, co0, p0, pcb * 32, bn, a.acc_dump);
       const v16i oned[1] = {accd[j]};
       epilogue_cjoin_t<1>(a, lds, one, oned, rbl, h, l32, co0, pcb * 32, otile, orow);
@@ -791,21 +794,36 @@ hipError_t launch_conv_w2(ConvLaunch a, const W2Plan& p, hipStream_t stream) {
   }
   const dim3 grid(p.blocks_m, (a.cout + bm - 1) / bm, a.ksplit);
   const dim3 block(64 * V.wm * V.wn * V.wk);
-  const int mode = a.join_kind == IFQ_JOIN_IDENTITY ? 1 : a.join_kind == IFQ_JOIN_CONV_FUSED ? 2 : 0;
-  switch (p.variant * 3 + mode) {
+  const int mode = a.ksplit > 1                            ? 3
+                   : a.join_kind == IFQ_JOIN_IDENTITY    ? 1
+                   : a.join_kind == IFQ_JOIN_CONV_FUSED ? 2
+                                                         : 0;
+  switch (p.variant * 4 + mode) {
+// the K-split instances (int8 variants only)
+#define IFQ_W2_SPLIT(k, wm, wn, wk, fm, fn, t, d, f4, occ, winb)                                \
+  case 4 * k + 3:                                                                               \
+    hipLaunchKernelGGL((conv_w2<wm, wn, wk, fm, fn, t, d, 3, f4, occ, winb>), grid, block, 0,   \
+                       stream, a);                                                              \
+    break;
 #define IFQ_W2_CASE(k, wm, wn, wk, fm, fn, t, d, f4, occ, winb)                                 \
-  case 3 * k:                                                                                   \
+  case 4 * k:                                                                                   \
     hipLaunchKernelGGL((conv_w2<wm, wn, wk, fm, fn, t, d, 0, f4, occ, winb>), grid, block, 0,   \
                        stream, a);                                                              \
     break;                                                                                      \
-  case 3 * k + 1:                                                                               \
+  case 4 * k + 1:                                                                               \
     hipLaunchKernelGGL((conv_w2<wm, wn, wk, fm, fn, t, d, 1, f4, occ, winb>), grid, block, 0,   \
                        stream, a);                                                              \
     break;                                                                                      \
-  case 3 * k + 2:                                                                               \
+  case 4 * k + 2:                                                                               \
     hipLaunchKernelGGL((conv_w2<wm, wn, wk, fm, fn, t, d, 2, f4, occ, winb>), grid, block, 0,   \
                        stream, a);                                                              \
     break;
+    IFQ_W2_SPLIT(0, 2, 4, 1, 2, 2, 3, 3, false, 1, 49152)
+    IFQ_W2_SPLIT(1, 1, 4, 2, 2, 2, 3, 2, false, 1, 53248)
+    IFQ_W2_SPLIT(2, 1, 2, 4, 2, 2, 3, 2, false, 1, 36864)
+    IFQ_W2_SPLIT(3, 1, 4, 1, 2, 2, 3, 3, false, 2, 20480)
+    IFQ_W2_SPLIT(4, 1, 8, 1, 2, 1, 3, 3, false, 2, 20480)
+    IFQ_W2_SPLIT(5, 2, 4, 1, 2, 2, 1, 3, false, 2, 24576)
     IFQ_W2_CASE(0, 2, 4, 1, 2, 2, 3, 3, false, 1, 49152)
     IFQ_W2_CASE(1, 1, 4, 2, 2, 2, 3, 2, false, 1, 53248)
     IFQ_W2_CASE(2, 1, 2, 4, 2, 2, 3, 2, false, 1, 36864)
@@ -817,6 +835,7 @@ hipError_t launch_conv_w2(ConvLaunch a, const W2Plan& p, hipStream_t stream) {
     IFQ_W2_CASE(8, 1, 2, 4, 2, 2, 3, 2, true, 1, 36864)
     IFQ_W2_CASE(9, 1, 4, 1, 2, 2, 9, 2, true, 2, 20480)
 #undef IFQ_W2_CASE
+#undef IFQ_W2_SPLIT
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
