@@ -79,7 +79,7 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int kg = lane >> 4;     // K bytes 16*kg .. 16*kg+15: taps 4*kg .. 4*kg+3
   const int l16 = lane & 15;
 
@@ -333,17 +333,24 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
     const int pwo = a.wo >> 1;
     const int nb3 = (rows >> 1) * sg.ncg;
     const int prow = pwo * orow;   // pooled tile bytes per row pair
+    // the lane's fixed offset inside a block: pixel (e >> 1, e & 1) of
+    // window w (columns 2w, 2w + 1 of the block's 8)
+    const int lane_off = ((e >> 1) * st * sg.win + (2 * w + (e & 1)) * st) * 4;
+    const int last_off = ((e >> 1) * st * sg.win + (2 * (pwo - 1) + (e & 1)) * st) * 4;
     for (int blk0 = wave; blk0 < nb3; blk0 += NW * 4) {
       v4i accu[4][FM];
+      int rps[4], cgs[4];   // wave-uniform block coordinates (scalar)
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int b = blk0 + NW * u;
         const int bc = b < nb3 ? b : nb3 - 1;
-        const int rp = fdiv(bc, sg.div_ncg);
-        const int pc = 4 * (bc - rp * sg.ncg) + w;
-        const int pcc = pc < pwo ? pc : pwo - 1;
-        const int r = 2 * rp + (e >> 1), ox = 2 * pcc + (e & 1);
-        const uint8_t* win = tile + ((r * st) * sg.win + ox * st) * 4;
+        rps[u] = fdiv(bc, sg.div_ncg);
+        cgs[u] = bc - rps[u] * sg.ncg;
+        // window w of the block's group, or the row's last window past pwo
+        const int pc = 4 * cgs[u] + w;
+        const int base = (2 * rps[u] * st * sg.win + 8 * cgs[u] * st) * 4;
+        const uint8_t* win =
+            tile + (pc < pwo ? base + lane_off : (2 * rps[u] * st * sg.win) * 4 + last_off);
         uint32_t b4[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) b4[j] = *reinterpret_cast<const uint32_t*>(win + toff[j]);
@@ -388,9 +395,8 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small8(ConvLaunch a, Small
         }
       // lane e: block blk0 + NW*e, pooled pixel (row pair, 4*group + w)
       const int be = blk0 + NW * e;
-      const int bec = be < nb3 ? be : nb3 - 1;
-      const int rpe = fdiv(bec, sg.div_ncg);
-      const int pce = 4 * (bec - rpe * sg.ncg) + w;
+      const int rpe = e == 0 ? rps[0] : e == 1 ? rps[1] : e == 2 ? rps[2] : rps[3];
+      const int pce = 4 * (e == 0 ? cgs[0] : e == 1 ? cgs[1] : e == 2 ? cgs[2] : cgs[3]) + w;
       const bool store = be < nb3 && pce < pwo;
 #pragma unroll
       for (int fm = 0; fm < FM; ++fm) {
@@ -570,7 +576,7 @@ __global__ __launch_bounds__(kSmallThreads) void conv_small2(ConvLaunch a, Small
   extern __shared__ __attribute__((aligned(16))) uint8_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform
   const int h = lane >> 5;
   const int l32 = lane & 31;
 
