@@ -80,8 +80,8 @@ class Hip:
 def kernel_peak(name):
     """Dense peak of the matrix instructions a kernel runs on: the fp4
     instances (the fp4 flag true: the windowed kernel's last template
-    argument, conv_w2's ninth, conv_wp's fifth) against MXFP4, the others
-    against int8."""
+    argument, conv_w2's ninth, conv_wp's fifth, conv_wv's second) against
+    MXFP4, the others against int8."""
     fp4 = False
     if name.startswith("conv_halo<"):
         fp4 = name.endswith(", true>")
@@ -89,6 +89,8 @@ def kernel_peak(name):
         fp4 = name[len("conv_w2<"):-1].split(", ")[8] == "true"
     elif name.startswith("conv_wp<"):
         fp4 = name[len("conv_wp<"):-1].split(", ")[4] == "true"
+    elif name.startswith("conv_wv<"):
+        fp4 = name[len("conv_wv<"):-1].split(", ")[1] == "true"
     return PEAK_FP4_TFLOPS if fp4 else PEAK_INT8_TOPS
 
 

@@ -419,15 +419,17 @@ IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d, const ifq_join*
 /*
  * Kernel variants of the register-blocked 3x3 conv kernels, for autotuning
  * and per-variant parity tests (the same contraction, Eq. 1, and the same
- * epilogues as ifq_conv_forward): conv_w2 (one output tile per workgroup)
- * and conv_wp (persistent: a workgroup keeps the weights of its 64 output
- * channels in LDS and runs a range of pixel tiles). Both take 3x3 pad-1 convs
- * of stride 1 or 2 on 2-bit BLOCK64 codes with c_in % 64 == 0, 2-bit output
- * (U2 or BLOCK64, c_out % 32 == 0, 27 * c_in <= 32766), no pool, and
- * thresholds or an identity join with a 2-bit shortcut (c_out % 64 == 0);
- * conv_w2 also a join with a fused 1x1 downsample on BLOCK64 codes of at
- * most 256 channels. Each variant further needs its weights and input
- * windows to fit its LDS budget.
+ * epilogues as ifq_conv_forward): conv_w2 (one output tile per workgroup),
+ * conv_wp (persistent: a workgroup keeps the weights of its 64 output
+ * channels in LDS and runs a range of pixel tiles) and conv_wv (persistent
+ * with the weights in LDS too, but each wave runs its own range of pixels
+ * with its own input windows and no barrier after the prologue; c_out %
+ * 64 == 0). All take 3x3 pad-1 convs of stride 1 or 2 on 2-bit BLOCK64
+ * codes with c_in % 64 == 0, 2-bit output (U2 or BLOCK64, c_out % 32 == 0,
+ * 27 * c_in <= 32766), no pool, and thresholds or an identity join with a
+ * 2-bit shortcut (c_out % 64 == 0); conv_w2 also a join with a fused 1x1
+ * downsample on BLOCK64 codes of at most 256 channels. Each variant further
+ * needs its weights and input windows to fit its LDS budget.
  *   ifq_conv_variant_count   number of variants (host)
  *   ifq_conv_variant_fp4     1 if variant computes the sums exactly on the
  *                            fp4 scaled MFMA, as ifq_conv_forward_fp4 (its

@@ -22,6 +22,8 @@
 //    other's MFMAs.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "ifq_epilogue.h"
 #include "ifq_internal.h"
 #include "ifq_mfma_common.h"
@@ -400,6 +402,418 @@ __global__ __launch_bounds__(64 * WN, (WN / 4) * OCC) void conv_wp(ConvLaunch a)
 }
 
 // ---------------------------------------------------------------------------
+// Wave-independent persistent 3x3 kernel
+// ---------------------------------------------------------------------------
+// The same contraction and epilogues, but after the prologue (the slice's
+// weights and records in LDS, one barrier) every wave runs its own pixel
+// range with no further barrier: per unit it loads the input window (and
+// shortcut cells) into its own LDS buffers, runs the main loop, writes the
+// unit's codes into its own output tile and stores them. Nothing ties one
+// wave's phases to another's, so while one wave of a SIMD is in its
+// epilogue (VALU) the other's MFMAs keep the matrix core busy, where the
+// workgroup-wide barrier of conv_wp holds the two workgroups of a CU in
+// step. One workgroup of eight waves per CU.
+//
+// Work is split in half units of 32 output pixels: a workgroup takes a
+// contiguous range of them and each wave a contiguous eighth of that, run
+// as units of 64 pixels x the 64-channel slice and, where its count is odd,
+// one last unit of 32 pixels (half the MFMAs). So the two waves of a SIMD
+// carry nearly the same work and neither runs long alone. Per wave the
+// next unit's window and shortcut load, and the previous unit's output
+// stores drain, while the current unit computes (one s_waitcnt per unit).
+template <int MODE, bool F4, int WINB>
+__global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
+  constexpr bool SW = MODE == 0;                 // transposed sums
+  constexpr int NW = 8, FM = 2, FN = 2;
+  constexpr int BM = 64, UN = 64, HU = 32;       // unit: 64 channels x 64 pixels
+  constexpr int KH = F4 ? 1 : 2;
+  constexpr int RB = FM;
+  constexpr int WGTB = 36864;
+  // int8 threshold instance (one channel block: K = 576): the B operand
+  // keeps each 2-bit field in place within its byte (1, 4, 16 or, shifted
+  // down once, 16 times the code) and the weight bytes that meet fields 0
+  // and 1 are scaled by 16 and 4 in LDS, so every product is 16 * w * x:
+  // the sums are 16 a, |16 a| <= 16 * 3 * 576 < 2^15, compared against 16 T.
+  constexpr bool SC16 = SW && !F4;
+  // LDS: the slice's weights, the records (raw for the threshold epilogue,
+  // packed for the identity join), one output tile per wave (the identity
+  // join's raw records sit there until they are packed), then per wave two
+  // windows and two shortcut buffers.
+  constexpr int WGT = 0;
+  constexpr int TBL = WGTB;
+  constexpr int TBL_BYTES = SW ? BM * 16 : (BM / 4) * kIdjGroupBytes;
+  constexpr int OUT = TBL + TBL_BYTES;
+  constexpr int OUT_BYTES = UN * BM / 4;
+  static_assert(SW || NW * OUT_BYTES >= BM * 64, "raw join records in the output tiles");
+  constexpr int WV = OUT + NW * OUT_BYTES;
+  constexpr int SC_BYTES = SW ? 0 : UN * 16;
+  constexpr int WV_BYTES = 2 * WINB + 2 * SC_BYTES;
+  constexpr int LDS_BYTES = WV + NW * WV_BYTES;
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
+  static_assert(WINB % 16 == 0, "window cells");
+
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS_BYTES];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int h = lane >> 5;
+  const int l32 = lane & 31;
+  const int co0 = blockIdx.y * BM;
+  const int G = a.cin >> 6;
+  const int H = a.h, W = a.w, Wo = a.wo, st = a.stride;
+  const int howo = a.ho * a.wo;
+  const int HW = H * W;
+  const int wcells = a.wcells;
+  const int wstr = (wcells + 1) * 16;            // block window + its zero cell
+  // this workgroup's half units, then this wave's contiguous share
+  const int nhu = (a.m + HU - 1) / HU;
+  const int g_lo = (int)((int64_t)blockIdx.x * nhu / gridDim.x);
+  const int g_hi = (int)((int64_t)(blockIdx.x + 1) * nhu / gridDim.x);
+  const int w_lo = g_lo + (g_hi - g_lo) * wave / NW;
+  const int w_hi = g_lo + (g_hi - g_lo) * (wave + 1) / NW;
+  const uint32_t lds0 = lds_addr(lds);
+  const uint32_t wv0 = lds0 + WV + wave * WV_BYTES;
+  uint8_t* const otile = lds + OUT + wave * OUT_BYTES;
+  const uint8_t* zero_src = reinterpret_cast<const uint8_t*>(&g_zero_cell);
+  constexpr int orow = BM / 4;
+  // half units of the unit starting at half unit c: two, or the last one
+  auto unit_len = [&](int c) { return c + 2 <= w_hi ? 2 : 1; };
+
+  // the window of the npx pixels from p0 into this wave's buffer b (segment
+  // i's rows of cells, rounded up to 64 cells, per channel block)
+  auto load_window = [&](int p0, int npx, int b) {
+    WpTile tl;
+    tl.init(a, p0, npx);
+    const uint32_t dst0 = wv0 + b * WINB;
+    int off = 0;
+    for (int i = 0; i < tl.nseg; ++i) {
+      int iya;
+      const int cells = tl.rows(a, i, iya) * W;
+      const int nch = wp_round64(cells) >> 6;
+      for (int j = 0; j < nch; ++j) {
+        const int c = j * 64 + lane;
+        const int64_t src = ((int64_t)(tl.n_first + i) * G * HW + iya * W + c) * 16;
+        for (int g = 0; g < G; ++g)
+          dma16(c < cells ? a.x + src + (int64_t)g * HW * 16 : zero_src,
+                dst0 + (uint32_t)(g * wstr + (off + j * 64) * 16));
+      }
+      off += wp_round64(cells);
+    }
+  };
+  // the shortcut cells of the pixels from p0 (identity join) into buffer b
+  auto load_shortcut = [&](int p0, int b) {
+    const int p = p0 + lane;
+    const uint8_t* sc8 = reinterpret_cast<const uint8_t*>(a.shortcut);
+    const uint8_t* src = zero_src;
+    if (p < a.m) {
+      if (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64) {
+        const int nimg = fdiv(p, a.div_howo);
+        src = sc8 + (((int64_t)nimg * (a.cout >> 6) + (co0 >> 6)) * howo + (p - nimg * howo)) * 16;
+      } else {
+        src = sc8 + ((int64_t)p * a.cout + co0) / 4;
+      }
+    }
+    dma16(src, wv0 + 2 * WINB + b * SC_BYTES);
+  };
+  // this wave's output tile (npx pixels from p0) to HBM: lane = pixel
+  auto store_unit = [&](int p0, int npx) {
+    const int p = p0 + lane;
+    const uint4 v = *reinterpret_cast<const uint4*>(otile + lane * 16);
+    if (lane < npx && p < a.m) {
+      uint8_t* y8 = reinterpret_cast<uint8_t*>(a.y);
+      int64_t off;
+      if (a.out_layout == IFQ_LAYOUT_U2_BLOCK64) {
+        const int nimg = fdiv(p, a.div_howo);
+        off = (((int64_t)nimg * (a.cout >> 6) + (co0 >> 6)) * howo + (p - nimg * howo)) * 16;
+      } else {
+        off = ((int64_t)p * a.cout + co0) / 4;
+      }
+      *reinterpret_cast<uint4*>(y8 + off) = v;
+    }
+  };
+
+  // ---- prologue: records, weights, every wave's first window -------------
+  if constexpr (SW) {
+    if (wave == 0) {
+      const int c = co0 + lane;
+      dma16(c < a.cout ? reinterpret_cast<const uint8_t*>(a.thr + (int64_t)c * 4) : zero_src,
+            lds0 + TBL);
+    }
+  } else {
+    for (int q = wave; q < BM / 16; q += NW) {   // 16 channels x 64 B per chunk
+      const int c = co0 + q * 16 + (lane >> 2);
+      dma16(c < a.cout ? reinterpret_cast<const uint8_t*>(a.table + (int64_t)c * 16 + (lane & 3) * 4)
+                       : zero_src,
+            lds0 + OUT + q * 1024);
+    }
+  }
+  const int nwch = G * kWpTaps * RB * KH;        // 1 KB weight chunks
+  {
+    const int nrb = a.cout_pad >> 5;
+    const int rbw = co0 >> 5;
+    const uint8_t* wbase = reinterpret_cast<const uint8_t*>(a.wgt);
+    const uint32_t voff = (uint32_t)lane * 16;
+    for (int c = wave; c < nwch; c += NW) {
+      const int t = c % KH, rb = (c / KH) % RB, kk = c / (KH * RB);
+      const int64_t off =
+          rbw + rb < nrb ? ((int64_t)(rbw + rb) * (KH * a.nk) + KH * kk + t) * 1024 : a.wzero;
+      dma16s(wbase + off, voff, lds0 + WGT + (uint32_t)(c * 1024));
+    }
+  }
+  if (w_lo < w_hi) {
+    load_window(w_lo * HU, unit_len(w_lo) * HU, 0);
+    if constexpr (!SW) load_shortcut(w_lo * HU, 0);
+  }
+  // the zero cell after every block window of both buffers
+  if (lane < 2 * G) {
+    const int b = lane / G, g = lane - b * G;
+    *reinterpret_cast<uint4*>(lds + WV + wave * WV_BYTES + b * WINB + g * wstr + wcells * 16) =
+        uint4{0, 0, 0, 0};
+  }
+  wait_vmcnt<0>();
+  __syncthreads();
+  if constexpr (!SW) {
+    stage_idj_pk(reinterpret_cast<const int32_t*>(lds + OUT), lds + TBL, BM,
+                 a.cout - co0 < BM ? a.cout - co0 : BM);
+    __syncthreads();
+  }
+  if constexpr (SC16) {
+    // dwords 0 and 1 of every lane's 16 weight bytes of a K32 step meet
+    // fields 0 and 1: x16 and x4 (bytes are 0 or +-1); all reads issued
+    // before the writes
+    const int nq = nwch * 64;
+    for (int q0 = 0; q0 < nq; q0 += 4 * 64 * NW) {
+      uint2 v[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int q = q0 + i * 64 * NW + tid;
+        if (q < nq) v[i] = *reinterpret_cast<const uint2*>(lds + WGT + q * 16);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int q = q0 + i * 64 * NW + tid;
+        if (q < nq)
+          *reinterpret_cast<uint2*>(lds + WGT + q * 16) =
+              uint2{(v[i].x << 4) & 0xF0F0F0F0u, (v[i].y << 2) & 0xFCFCFCFCu};
+      }
+    }
+    __syncthreads();
+  }
+
+  struct Unp {
+    v4i b4[F4 ? 1 : 2][FN];
+    v8i b8[F4 ? FN : 1];
+  };
+
+  // ---- one unit: NB pixel blocks of 32 from p0, window buffer b ----------
+  auto run_unit = [&](auto nb_tag, int p0, int b) {
+    constexpr int NB = decltype(nb_tag)::value;
+    constexpr int kGroups = KH * NB;             // MFMA groups of a tap
+    // per-lane LDS offsets of the nine taps of each pixel block: the
+    // top-left tap's offset plus row and column steps; taps outside the
+    // image, and pixels past the last, read the zero cell
+    int boff[NB][kWpTaps];
+    {
+      WpTile tl;
+      tl.init(a, p0, NB * 32);
+      const int zc = wcells * 16 + 8 * h;
+#pragma unroll
+      for (int fn = 0; fn < NB; ++fn) {
+        const int p = p0 + fn * 32 + l32;
+        const bool pok = p < a.m;
+        const int pc = pok ? p : p0;
+        const int n = fdiv(pc, a.div_howo);
+        const int rem = pc - n * howo;
+        const int oy = fdiv(rem, a.div_wo);
+        const int ox = rem - oy * Wo;
+        int my_off = 0, my_iya = 0, off = 0;
+        for (int i = 0; i < tl.nseg; ++i) {
+          int iya;
+          const int rows = tl.rows(a, i, iya);
+          if (i == n - tl.n_first) {
+            my_off = off;
+            my_iya = iya;
+          }
+          off += wp_round64(rows * W);
+        }
+        const int iy0 = oy * st - 1, ix0 = ox * st - 1;
+        const int base = (my_off + (iy0 - my_iya) * W + ix0) * 16 + 8 * h;
+        const bool rok[3] = {pok && iy0 >= 0, pok, pok && iy0 + 2 < H};
+        const bool cok[3] = {ix0 >= 0, true, ix0 + 2 < W};
+#pragma unroll
+        for (int r = 0; r < 3; ++r)
+#pragma unroll
+          for (int s2 = 0; s2 < 3; ++s2)
+            boff[fn][r * 3 + s2] = rok[r] && cok[s2] ? base + (r * W + s2) * 16 : zc;
+      }
+    }
+
+    // main loop: written first by the zero-addend MFMAs of the first tap
+    v16i acc[FM][NB];
+    v16f accf[F4 ? FM : 1][F4 ? NB : 1];
+    const uint8_t* winb = lds + WV + wave * WV_BYTES + b * WINB;
+    // weight fragments of a tap (K32 halves x channel blocks) and the raw
+    // codes of its pixel blocks
+    auto read_a = [&](int g, int tap, v4i (&af)[KH][FM]) {
+      const uint8_t* as = lds + WGT + (g * kWpTaps + tap) * RB * KH * 1024;
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int t = 0; t < KH; ++t)
+          af[t][fm] = *reinterpret_cast<const v4i*>(as + (fm * KH + t) * 1024 + lane * 16);
+    };
+    auto read_b = [&](int g, int tap, v2i (&br)[NB]) {
+      const uint8_t* win = winb + g * wstr;
+#pragma unroll
+      for (int fn = 0; fn < NB; ++fn)
+        br[fn] = *reinterpret_cast<const v2i*>(win + boff[fn][tap]);
+    };
+    auto unpack_piece = [&](const v2i (&br)[NB], Unp& U, int k) {
+      const int t = k / NB, fn = k % NB;
+      if constexpr (F4) {
+        const uint32_t w0 = (uint32_t)br[fn][0], w1 = (uint32_t)br[fn][1];
+        U.b8[fn] = v8i{(int)(w0 & 0x33333333u), (int)((w0 >> 2) & 0x33333333u),
+                       (int)(w1 & 0x33333333u), (int)((w1 >> 2) & 0x33333333u), 0, 0, 0, 0};
+      } else if constexpr (SC16) {
+        const uint32_t w = (uint32_t)br[fn][t];
+        U.b4[t][fn] = v4i{(int)(w & 0x03030303u), (int)(w & 0x0C0C0C0Cu), (int)(w & 0x30303030u),
+                          (int)((w >> 2) & 0x30303030u)};
+      } else {
+        U.b4[t][fn] = unpack2((uint32_t)br[fn][t]);
+      }
+    };
+    // zc: the first MFMA into each accumulator (zero addend, no clearing)
+    auto mfma_group = [&](auto zc, const v4i (&afr)[KH][FM], const Unp& U, int k) {
+      constexpr bool ZC = decltype(zc)::value;
+      const int t = k / NB, fn = k % NB;
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm) {
+        if constexpr (F4) {
+          const v4i w = afr[0][fm];
+          const v8i af = v8i{w.x, w.y, w.z, w.w, 0, 0, 0, 0};
+          const v16f cf = ZC ? v16f{0.0f} : accf[fm][fn];
+          if constexpr (SW)
+            accf[fm][fn] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                U.b8[fn], af, cf, 4, 4, 0, 127, 0, 127);
+          else
+            accf[fm][fn] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                af, U.b8[fn], cf, 4, 4, 0, 127, 0, 127);
+        } else {
+          const v16i ci = ZC && t == 0 ? v16i{0} : acc[fm][fn];
+          if constexpr (SW)
+            acc[fm][fn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(U.b4[t][fn], afr[t][fm], ci, 0,
+                                                                0, 0);
+          else
+            acc[fm][fn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(afr[t][fm], U.b4[t][fn], ci, 0,
+                                                                0, 0);
+        }
+      }
+    };
+    // Software pipeline over the taps, two deep for the codes: during tap
+    // i's MFMA groups the weight fragments of tap i + 1 and the raw codes of
+    // tap i + 2 are read, and tap i + 1's B operands are unpacked from codes
+    // read a whole tap earlier, one piece after each MFMA group from the
+    // second on.
+    auto run_block = [&](auto zc, int g) {
+      v4i af[2][KH][FM];
+      v2i br[3][NB];
+      Unp uu[2];
+      read_b(g, 0, br[0]);
+      read_a(g, 0, af[0]);
+      read_b(g, 1, br[1]);
+#pragma unroll
+      for (int k = 0; k < kGroups; ++k) unpack_piece(br[0], uu[0], k);
+#pragma unroll
+      for (int tap = 0; tap < kWpTaps; ++tap) {
+        const int c = tap & 1;
+        const bool nxt = tap + 1 < kWpTaps;
+        if (nxt) read_a(g, tap + 1, af[c ^ 1]);
+        if (tap + 2 < kWpTaps) read_b(g, tap + 2, br[(tap + 2) % 3]);
+#pragma unroll
+        for (int k = 0; k < kGroups; ++k) {
+          __builtin_amdgcn_sched_barrier(0);
+          if (tap == 0)
+            mfma_group(zc, af[c], uu[c], k);
+          else
+            mfma_group(std::false_type{}, af[c], uu[c], k);
+          __builtin_amdgcn_sched_barrier(0);
+          if (nxt && k >= 1) unpack_piece(br[(tap + 1) % 3], uu[c ^ 1], k - 1);
+        }
+        if (nxt) unpack_piece(br[(tap + 1) % 3], uu[c ^ 1], kGroups - 1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    __builtin_amdgcn_s_setprio(1);
+    run_block(std::true_type{}, 0);
+    for (int g = 1; g < G; ++g) run_block(std::false_type{}, g);
+    __builtin_amdgcn_s_setprio(0);
+    if constexpr (F4) {
+      // exact integers (every partial sum is an integer below 2^24)
+#pragma unroll
+      for (int fm = 0; fm < FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < NB; ++fn)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) acc[fm][fn][i] = (int)accf[fm][fn][i];
+    }
+
+    // epilogue into this wave's output tile
+#pragma unroll
+    for (int q = 0; q < FM * NB; ++q) {
+      const int fm = q / NB, fn = q % NB;
+      const v16i one[1] = {acc[fm][fn]};
+      if constexpr (SW) {
+        if (a.acc_dump) {
+          const v16i sums[1] = {SC16 ? acc[fm][fn] >> 4 : acc[fm][fn]};
+          dump_acc_t<1>(a, sums, fm, h, l32, co0, p0, fn * 32, NB * 32, a.acc_dump);
+        }
+        epilogue_thr_pk_t<1, SC16 ? 4 : 0>(a, reinterpret_cast<const int4*>(lds + TBL), one, fm,
+                                           h, l32, co0, fn * 32, otile, orow);
+      } else {
+        if (a.acc_dump) {
+          const v16i one2[1][1] = {{acc[fm][fn]}};
+          epilogue32<kE32I32, 1, 1>(a, lds + TBL, one2, fm, fn, h, l32, co0, p0, NB * 32, otile,
+                                    orow, a.acc_dump);
+        }
+        const int pl = fn * 32 + l32;
+        const int cl = fm * 32;
+        const uint2 sc[1] = {*reinterpret_cast<const uint2*>(
+            lds + WV + wave * WV_BYTES + 2 * WINB + b * SC_BYTES + pl * 16 + (cl >> 2))};
+        epilogue_idj_pk<1>(a, lds + TBL, one, sc, fm, h, co0, pl, otile, orow);
+      }
+    }
+    // the output tile's bytes (written by other lanes of this wave) are read
+    // back by store_unit: LDS operations of one wave complete in order; the
+    // empty asm keeps the compiler from moving the reads above the writes
+    asm volatile("" ::: "memory");
+  };
+
+  int b = 0;
+  for (int c = w_lo; c < w_hi; b ^= 1) {
+    const int len = unit_len(c);
+    const int nx = c + len;
+    // the window of this unit has landed (and the stores of two units back
+    // have drained); the next unit's loads and the previous unit's stores
+    // then run under this unit's main loop
+    if (c != w_lo) wait_vmcnt<0>();
+    __builtin_amdgcn_sched_barrier(0);
+    if (nx < w_hi) {
+      load_window(nx * HU, unit_len(nx) * HU, b ^ 1);
+      if constexpr (!SW) load_shortcut(nx * HU, b ^ 1);
+    }
+    if (c != w_lo) store_unit((c - 2) * HU, 2 * HU);   // every unit but the last is whole
+    __builtin_amdgcn_sched_barrier(0);
+    if (len == 2)
+      run_unit(std::integral_constant<int, 2>{}, c * HU, b);
+    else
+      run_unit(std::integral_constant<int, 1>{}, c * HU, b);
+    if (nx >= w_hi) store_unit(c * HU, len * HU);
+    c = nx;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Variants and planning
 // ---------------------------------------------------------------------------
 struct WpVariant {
@@ -431,7 +845,31 @@ const WpVariant kWpVariants[] = {
      IFQ_WP_NAME(4, 2, 2, 0, true, 2, 36864, 16384),
      IFQ_WP_NAME(4, 2, 2, 1, true, 2, 36864, 10240)},
 };
-constexpr int kNumWp = sizeof(kWpVariants) / sizeof(kWpVariants[0]);
+constexpr int kNumWpBlock = sizeof(kWpVariants) / sizeof(kWpVariants[0]);
+
+// The wave-independent kernel: one workgroup of eight waves per CU, a unit
+// of 64 pixels x 64 channels per wave at a time. Fitted the same way: a
+// prologue (weights, records, first windows) and, per unit, a fixed and a
+// per-channel-block cost, with two waves sharing each SIMD.
+struct WvVariant {
+  bool f4;
+  int winb_thr, winb_idj;   // window buffer bytes per wave
+  double pro_us, c_unit_us, c_blk_us, idj_us;
+  const char* thr_name;
+  const char* idj_name;
+};
+#define IFQ_WV_NAME(mode, f4, winb) "conv_wv<" #mode ", " #f4 ", " #winb ">"
+// Index order must match the switch in launch_conv_wp.
+const WvVariant kWvVariants[] = {
+    {false, 7168, 5888, 2.5, 1.2, 1.0, 0.32,
+     IFQ_WV_NAME(0, false, 7168), IFQ_WV_NAME(1, false, 5888)},
+    {true, 7168, 5888, 2.5, 1.0, 0.65, 0.37,
+     IFQ_WV_NAME(0, true, 7168), IFQ_WV_NAME(1, true, 5888)},
+};
+constexpr int kNumWv = sizeof(kWvVariants) / sizeof(kWvVariants[0]);
+constexpr int kNumWp = kNumWpBlock + kNumWv;
+constexpr int kWvWaves = 8;
+constexpr int kWvUnit = 64;
 
 bool wp_fit(const ConvLaunch& a, int v, WpPlan* out) {
   const WpVariant& V = kWpVariants[v];
@@ -455,6 +893,33 @@ bool wp_fit(const ConvLaunch& a, int v, WpPlan* out) {
   return true;
 }
 
+bool wv_fit(const ConvLaunch& a, int v, WpPlan* out) {
+  const WvVariant& V = kWvVariants[v];
+  if (V.f4 != (a.f4 != 0) || a.cout % 64 != 0) return false;
+  const int G = a.cin / 64;
+  const int kh = V.f4 ? 1 : 2;
+  if ((int64_t)G * kWpTaps * 2 * kh * 1024 > 36864) return false;
+  const bool idj = a.join_kind == IFQ_JOIN_IDENTITY;
+  const int winb = idj ? V.winb_idj : V.winb_thr;
+  // units of 64 pixels at any multiple of 32 (a wave's range starts at a
+  // half unit)
+  const int64_t cells = window_cells_max(a, kWvUnit, (int64_t)winb / 16 / G, kWvUnit / 2);
+  if (cells < 0 || (int64_t)G * (cells + 1) * 16 > winb) return false;
+  const int64_t nco = a.cout / 64;
+  const int64_t nhu = (a.m + kWvUnit / 2 - 1) / (kWvUnit / 2);  // half units
+  int64_t gx = kPlanCUs / nco;
+  if (gx < 1) gx = 1;
+  if (gx > (nhu + kWvWaves - 1) / kWvWaves) gx = (nhu + kWvWaves - 1) / kWvWaves;
+  const int64_t hw = (nhu + gx - 1) / gx;                        // half units per workgroup
+  const int64_t per_wave = (hw + kWvWaves - 1) / kWvWaves;
+  const int64_t rounds = (gx * nco + kPlanCUs - 1) / kPlanCUs;   // one workgroup per CU
+  // the two waves of a SIMD: 2 * per_wave half units between them
+  const double c_hu = (V.c_unit_us + G * V.c_blk_us + (idj ? V.idj_us : 0.0)) / 2.0;
+  const double t = kLaunchUs + rounds * (V.pro_us + 2 * per_wave * c_hu);
+  *out = WpPlan{kNumWpBlock + v, kWvUnit, (int)gx, (int)per_wave, (int)cells, t};
+  return true;
+}
+
 bool wp_mode_ok(const ConvLaunch& a) {
   if (!(a.out_mode == 2 && a.rec == 4 && (a.cout & 31) == 0 && 27 * a.cin <= 32766 &&
         a.pool_k == 0))
@@ -467,7 +932,16 @@ bool wp_mode_ok(const ConvLaunch& a) {
 }  // namespace
 
 int wp_variant_count() { return kNumWp; }
-bool wp_variant_fp4(int v) { return v >= 0 && v < kNumWp && kWpVariants[v].f4; }
+bool wp_variant_fp4(int v) {
+  if (v < 0 || v >= kNumWp) return false;
+  return v < kNumWpBlock ? kWpVariants[v].f4 : kWvVariants[v - kNumWpBlock].f4;
+}
+
+namespace {
+bool wp_any_fit(const ConvLaunch& a, int v, WpPlan* out) {
+  return v < kNumWpBlock ? wp_fit(a, v, out) : wv_fit(a, v - kNumWpBlock, out);
+}
+}  // namespace
 
 bool plan_wp(const ConvLaunch& a, int forced, WpPlan* out) {
   if (!(a.in_layout == IFQ_LAYOUT_U2_BLOCK64 && a.in_bits == 2 && a.cin % 64 == 0 &&
@@ -476,11 +950,11 @@ bool plan_wp(const ConvLaunch& a, int forced, WpPlan* out) {
   if (!wp_mode_ok(a)) return false;
   // 32-bit cell indices and offsets
   if ((int64_t)a.n * a.h * a.w * (a.cin / 64) >= (int64_t)1 << 26) return false;
-  if (forced >= 0) return forced < kNumWp && wp_fit(a, forced, out);
+  if (forced >= 0) return forced < kNumWp && wp_any_fit(a, forced, out);
   bool found = false;
   for (int v = 0; v < kNumWp; ++v) {
     WpPlan p;
-    if (wp_fit(a, v, &p) && (!found || p.t_us < out->t_us)) {
+    if (wp_any_fit(a, v, &p) && (!found || p.t_us < out->t_us)) {
       *out = p;
       found = true;
     }
@@ -489,14 +963,38 @@ bool plan_wp(const ConvLaunch& a, int forced, WpPlan* out) {
 }
 
 const char* conv_wp_name(const WpPlan& p, const ConvLaunch& a) {
+  const bool idj = a.join_kind == IFQ_JOIN_IDENTITY;
+  if (p.variant >= kNumWpBlock) {
+    const WvVariant& V = kWvVariants[p.variant - kNumWpBlock];
+    return idj ? V.idj_name : V.thr_name;
+  }
   const WpVariant& V = kWpVariants[p.variant];
-  return a.join_kind == IFQ_JOIN_IDENTITY ? V.idj_name : V.thr_name;
+  return idj ? V.idj_name : V.thr_name;
 }
 
 hipError_t launch_conv_wp(ConvLaunch a, const WpPlan& p, hipStream_t stream) {
   a.bn = p.bn;
   a.wcells = p.wcells;
   a.tiles_wg = p.per;
+  if (p.variant >= kNumWpBlock) {
+    const dim3 grid(p.gx, a.cout / 64);
+    const dim3 block(64 * kWvWaves);
+    const int mode = a.join_kind == IFQ_JOIN_IDENTITY ? 1 : 0;
+    switch ((p.variant - kNumWpBlock) * 2 + mode) {
+#define IFQ_WV_CASE(k, f4, winbt, winbi)                                                   \
+  case 2 * k:                                                                              \
+    hipLaunchKernelGGL((conv_wv<0, f4, winbt>), grid, block, 0, stream, a);                \
+    break;                                                                                 \
+  case 2 * k + 1:                                                                          \
+    hipLaunchKernelGGL((conv_wv<1, f4, winbi>), grid, block, 0, stream, a);                \
+    break;
+      IFQ_WV_CASE(0, false, 7168, 5888)
+      IFQ_WV_CASE(1, true, 7168, 5888)
+#undef IFQ_WV_CASE
+      default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   const WpVariant& V = kWpVariants[p.variant];
   const int bm = 32 * V.fm;
   const dim3 grid(p.gx, (a.cout + bm - 1) / bm);

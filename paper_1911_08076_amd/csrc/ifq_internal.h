@@ -197,22 +197,26 @@ hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream);
 // The largest input window (cells per channel block, each image's rows of
 // cells rounded up to 64) that a tile of bn consecutive output pixels of a
 // 3x3 pad-1 conv needs, over the layer's tiles, or -1 once it exceeds limit.
-// Tile starts repeat modulo ho*wo with period ho*wo / gcd(bn, ho*wo), so one
-// period and the layer's last (partial) tile cover every distinct tile.
-inline int64_t window_cells_max(const ConvLaunch& a, int64_t bn, int64_t limit) {
+// Tiles start at the multiples of step (0: bn), the last ones clipped at m.
+// Tile starts repeat modulo ho*wo with period ho*wo / gcd(step, ho*wo), so
+// one period and the layer's last starts cover every distinct tile.
+inline int64_t window_cells_max(const ConvLaunch& a, int64_t bn, int64_t limit,
+                                int64_t step = 0) {
+  if (step <= 0) step = bn;
   const int64_t howo = (int64_t)a.ho * a.wo;
-  int64_t g = bn, r = howo;
+  int64_t g = step, r = howo;
   while (r) {
     const int64_t t = g % r;
     g = r;
     r = t;
   }
-  const int64_t ntm = (a.m + bn - 1) / bn;
+  const int64_t nst = (a.m + step - 1) / step;           // tile starts
   const int64_t period = howo / g;
+  const int64_t tail = (bn + step - 1) / step;           // starts whose tile reaches m
   int64_t mx = 0;
-  for (int64_t t = 0; t < ntm; ++t) {
-    if (t == period && ntm > period) t = ntm - 1;   // then only the last tile
-    const int64_t p0 = t * bn;
+  for (int64_t t = 0; t < nst; ++t) {
+    if (t == period && nst - tail > period) t = nst - tail;   // then only the last starts
+    const int64_t p0 = t * step;
     const int64_t pend = (p0 + bn < a.m ? p0 + bn : a.m) - 1;
     const int64_t nf = p0 / howo, nl = pend / howo;
     const int64_t oyf = (p0 - nf * howo) / a.wo, oyl = (pend - nl * howo) / a.wo;

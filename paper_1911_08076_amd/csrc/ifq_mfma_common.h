@@ -417,13 +417,21 @@ __device__ __forceinline__ uint32_t pk2_i16(int v) { return ((uint32_t)v & 0xFFF
 // Threshold epilogue (2-bit codes, c_out % 32 == 0, 27 * c_in <= 32766) from
 // the raw {s, T1, T2, T3} records of the tile's channels (recs[c - co0]),
 // with the same packed 16-bit compare and sign flip as epilogue_thr_pk.
-template <int NB>
+// SH > 0: the sums are 2^SH a (|2^SH a| < 2^15); the thresholds, clamped to
+// [-B-1, B] (B = 27 c_in bounds |a|, so no comparison changes), are scaled
+// the same way.
+template <int NB, int SH = 0>
 __device__ __forceinline__ void epilogue_thr_pk_t(const ConvLaunch& a, const int4* recs,
                                                   const v16i (&acc)[NB], int wm, int h,
                                                   int l32, int co0, int pl0, uint8_t* otile,
                                                   int orow) {
   const int t = l32 & 3;
   const int bsel = ((t & 1) << 1) | (t >> 1);    // byte of pixel t in the merged word
+  const int bnd = 27 * a.cin;
+  auto thr = [&](int v) {
+    if constexpr (SH > 0) v = (v < -bnd - 1 ? -bnd - 1 : (v > bnd ? bnd : v)) * (1 << SH);
+    return pk2_i16(v);
+  };
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int cb = (wm * NB + j) * 32;
@@ -431,9 +439,9 @@ __device__ __forceinline__ void epilogue_thr_pk_t(const ConvLaunch& a, const int
     const int cl = cb + l32;
     const int4 r = recs[cl];
     const bool flip = r.x < 0;
-    const uint32_t w1 = pk2_i16(flip ? -r.y - 1 : r.y);
-    const uint32_t w2 = pk2_i16(flip ? -r.z - 1 : r.z);
-    const uint32_t w3 = pk2_i16(flip ? -r.w - 1 : r.w);
+    const uint32_t w1 = thr(flip ? -r.y - 1 : r.y);
+    const uint32_t w2 = thr(flip ? -r.z - 1 : r.z);
+    const uint32_t w3 = thr(flip ? -r.w - 1 : r.w);
     const uint32_t xm = flip ? 0x03030303u : 0u;
 #pragma unroll
     for (int b = 0; b < 4; ++b) {

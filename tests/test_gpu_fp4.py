@@ -31,7 +31,7 @@ def fp4_kernel(name):
 
 # name, n, h, c_in, c_out, stride, expected variant
 FP4 = [
-    ("f4_c64_small_batch", 2, 56, 64, 64, 1, "conv_w2<1, 4, 1, 2, 2, 9, 2, 0, true, 2, 20480>"),
+    ("f4_c64_small_batch", 2, 56, 64, 64, 1, "conv_wv<0, true, 7168>"),
     ("f4_l2", 3, 28, 128, 128, 1, None),
     ("f4_l2_0_s2", 2, 56, 64, 128, 2, None),
     ("f4_l3", 4, 14, 256, 256, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, 0, true, 1, 36864>"),
@@ -73,12 +73,12 @@ def test_fp4_conv_bit_exact(P, case):
 
 
 def test_fp4_offered_for_the_64_channel_tiles(P):
-    # the full-batch 64-channel layers run the persistent kernel (the slice's
-    # weights resident in LDS, two workgroups per CU), which has an fp4
-    # instance
+    # the full-batch 64-channel layers run the wave-independent persistent
+    # kernel (the slice's weights resident in LDS, one workgroup per CU),
+    # which has an fp4 instance
     d = P.conv_desc(64, 56, 56, 64, 64, 3, 1, 1, 2, 2, B64, B64)
-    assert P.ifq_conv_kernel_name(d) == "conv_wp<4, 2, 2, 0, false, 2, 36864, 16384>"
-    assert P.ifq_conv_fp4_kernel_name(d) == "conv_wp<4, 2, 2, 0, true, 2, 36864, 16384>"
+    assert P.ifq_conv_kernel_name(d) == "conv_wv<0, false, 7168>"
+    assert P.ifq_conv_fp4_kernel_name(d) == "conv_wv<0, true, 7168>"
     # a fused pool is not the register-blocked kernel's: the windowed
     # kernel's fp4 instances take it
     pd = P.pool_desc(64, 56, 56, 64, 2, 2, P.IFQ_POOL_VALID, 2, B64)
@@ -89,6 +89,13 @@ def test_fp4_offered_for_the_64_channel_tiles(P):
 # identity join (the blocks' second convs): name, n, h, channels
 FP4_IDJ = [("f4j_l1_small_batch", 2, 56, 64), ("f4j_l2", 3, 28, 128),
            ("f4j_l3", 4, 14, 256), ("f4j_l4", 6, 7, 512)]
+
+
+def _epilogue_mode(kname):
+    """The epilogue mode template argument of a register-blocked 3x3 kernel
+    name (1: identity join)."""
+    args = kname[kname.index("<") + 1:-1].split(", ")
+    return args[{"conv_w2": 7, "conv_wp": 3, "conv_wv": 0}[kname[:kname.index("<")]]]
 
 
 @pytest.mark.parametrize("case", FP4_IDJ, ids=[c[0] for c in FP4_IDJ])
@@ -108,7 +115,7 @@ def test_fp4_identity_join_bit_exact(P, case):
     xd = upload_codes(P, x, B64)
     d = P.conv_desc(n, h, h, c, c, 3, 1, 1, 2, 2, B64, B64)
     kname = P.ifq_conv_fp4_kernel_name(d, join)
-    assert fp4_kernel(kname) and kname[8:-1].split(", ")[7] == "1", kname
+    assert fp4_kernel(kname) and _epilogue_mode(kname) == "1", kname
     wd = to_dev(P.ifq_pack_weights_fp4(d, p["w"]))
     ob = P.ifq_tensor_bytes(n, h, h, c, B64)
     y = torch.full((ob,), 0xA5, dtype=torch.uint8, device=device())

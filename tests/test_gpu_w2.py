@@ -1,6 +1,6 @@
-"""GPU parity of every variant of the register-blocked 3x3 kernels, conv_w2
-and the persistent conv_wp (ifq_conv_forward_variant), int8 and fp4
-instances: int32 sums and output
+"""GPU parity of every variant of the register-blocked 3x3 kernels, conv_w2,
+the persistent conv_wp and the wave-independent conv_wv
+(ifq_conv_forward_variant), int8 and fp4 instances: int32 sums and output
 codes (thresholds of Eq. 7/8, the identity residual join, or the join with
 a 1x1 downsample computed in the kernel) must equal the oracle's bit for
 bit on the same seeded inputs, on small ragged layers that span several
@@ -35,6 +35,10 @@ SMALL = [
     ("s2_14_128_256", 5, 14, 14, 128, 256, 2),
     ("r9_192_64", 1, 9, 9, 192, 64, 1),
     ("r5_128_96", 3, 5, 6, 128, 96, 1),
+    # fewer half units than waves, units across images, ragged tails
+    ("r5x7_64_64", 3, 5, 7, 64, 64, 1),
+    ("r9_64_64", 5, 9, 9, 64, 64, 1),
+    ("r17x23_64_64", 3, 17, 23, 64, 64, 1),
 ]
 
 FULL = [
@@ -51,7 +55,8 @@ FULL = [
 ]
 
 
-NVAR = 12   # conv_w2's ten, then conv_wp's two
+NVAR = 14   # conv_w2's ten, then conv_wp's two and conv_wv's two
+NW2 = 10    # conv_w2's variants
 
 
 def _nvar(P):
@@ -90,7 +95,7 @@ def _combos(cases, full=False):
             if join and (st != 1 or cin != cout):
                 continue
             for v in range(NVAR):
-                if full and name in ("l1_n97", "l1_n160") and v < NVAR - 2:
+                if full and name in ("l1_n97", "l1_n160") and v < NW2:
                     continue   # one tile per workgroup: the batch-64 case covers it
                 if P is not None:
                     ob = B64 if cout % 64 == 0 else U2
