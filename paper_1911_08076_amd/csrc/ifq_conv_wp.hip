@@ -404,23 +404,22 @@ __global__ __launch_bounds__(64 * WN, (WN / 4) * OCC) void conv_wp(ConvLaunch a)
 // ---------------------------------------------------------------------------
 // Wave-independent persistent 3x3 kernel
 // ---------------------------------------------------------------------------
-// The same contraction and epilogues, but after the prologue (the slice's
-// weights and records in LDS, one barrier) every wave runs its own pixel
-// range with no further barrier: per unit it loads the input window (and
-// shortcut cells) into its own LDS buffers, runs the main loop, writes the
-// unit's codes into its own output tile and stores them. Nothing ties one
-// wave's phases to another's, so while one wave of a SIMD is in its
-// epilogue (VALU) the other's MFMAs keep the matrix core busy, where the
-// workgroup-wide barrier of conv_wp holds the two workgroups of a CU in
-// step. One workgroup of eight waves per CU.
+// The same contraction and epilogues, but the prologue brings everything
+// the workgroup will read into LDS at once (the slice's weights and records,
+// the input window of the workgroup's whole pixel range and, for the
+// identity join, that range's shortcut cells), and after its barrier every
+// wave runs its own pixels with no further barrier or wait: per unit the
+// main loop, the epilogue into the wave's own output tile and the stores.
+// Nothing ties one wave's phases to another's, so while one wave of a SIMD
+// is in its epilogue (VALU) the other's MFMAs keep the matrix core busy,
+// where the workgroup-wide barrier of conv_wp holds the two workgroups of a
+// CU in step. One workgroup of eight waves per CU.
 //
 // Work is split in half units of 32 output pixels: a workgroup takes a
 // contiguous range of them and each wave a contiguous eighth of that, run
 // as units of 64 pixels x the 64-channel slice and, where its count is odd,
 // one last unit of 32 pixels (half the MFMAs). So the two waves of a SIMD
-// carry nearly the same work and neither runs long alone. Per wave the
-// next unit's window and shortcut load, and the previous unit's output
-// stores drain, while the current unit computes (one s_waitcnt per unit).
+// carry nearly the same work and neither runs long alone.
 template <int MODE, bool F4, int WINB>
 __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
   constexpr bool SW = MODE == 0;                 // transposed sums
@@ -429,28 +428,28 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
   constexpr int KH = F4 ? 1 : 2;
   constexpr int RB = FM;
   constexpr int WGTB = 36864;
-  // int8 threshold instance (one channel block: K = 576): the B operand
-  // keeps each 2-bit field in place within its byte (1, 4, 16 or, shifted
-  // down once, 16 times the code) and the weight bytes that meet fields 0
-  // and 1 are scaled by 16 and 4 in LDS, so every product is 16 * w * x:
-  // the sums are 16 a, |16 a| <= 16 * 3 * 576 < 2^15, compared against 16 T.
-  constexpr bool SC16 = SW && !F4;
+  // int8 instances (one channel block: K = 576): the code operand keeps each
+  // 2-bit field in place within its byte (1, 4, 16 or, shifted down once,
+  // 16 times the code) and the weight bytes that meet fields 0 and 1 are
+  // scaled by 16 and 4 in LDS, so every product is 16 * w * x: the sums are
+  // 16 a, |16 a| <= 16 * 3 * 576 < 2^15, compared against 16 T.
+  constexpr bool SC16 = !F4;
   // LDS: the slice's weights, the records (raw for the threshold epilogue,
   // packed for the identity join), one output tile per wave (the identity
-  // join's raw records sit there until they are packed), then per wave two
-  // windows and two shortcut buffers.
+  // join's raw records sit there until they are packed), the workgroup's
+  // window (per channel block its cells and a zero cell) and shortcut cells.
   constexpr int WGT = 0;
   constexpr int TBL = WGTB;
   constexpr int TBL_BYTES = SW ? BM * 16 : (BM / 4) * kIdjGroupBytes;
   constexpr int OUT = TBL + TBL_BYTES;
   constexpr int OUT_BYTES = UN * BM / 4;
   static_assert(SW || NW * OUT_BYTES >= BM * 64, "raw join records in the output tiles");
-  constexpr int WV = OUT + NW * OUT_BYTES;
-  constexpr int SC_BYTES = SW ? 0 : UN * 16;
-  constexpr int WV_BYTES = 2 * WINB + 2 * SC_BYTES;
-  constexpr int LDS_BYTES = WV + NW * WV_BYTES;
-  static_assert(LDS_BYTES <= 160 * 1024, "LDS");
-  static_assert(WINB % 16 == 0, "window cells");
+  constexpr int WIN = OUT + NW * OUT_BYTES;
+  constexpr int SCO = WIN + WINB;
+  constexpr int LDS_BYTES = 160 * 1024;
+  constexpr int SCB = LDS_BYTES - SCO;
+  static_assert(SCO <= LDS_BYTES && (SW || SCB >= 1024), "LDS");
+  static_assert(WINB % 1024 == 0, "window bytes");
 
   __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS_BYTES];
 
@@ -472,49 +471,55 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
   const int g_hi = (int)((int64_t)(blockIdx.x + 1) * nhu / gridDim.x);
   const int w_lo = g_lo + (g_hi - g_lo) * wave / NW;
   const int w_hi = g_lo + (g_hi - g_lo) * (wave + 1) / NW;
+  const int P0 = g_lo * HU;
+  const int P1 = g_hi * HU < a.m ? g_hi * HU : a.m;
   const uint32_t lds0 = lds_addr(lds);
-  const uint32_t wv0 = lds0 + WV + wave * WV_BYTES;
   uint8_t* const otile = lds + OUT + wave * OUT_BYTES;
   const uint8_t* zero_src = reinterpret_cast<const uint8_t*>(&g_zero_cell);
   constexpr int orow = BM / 4;
   // half units of the unit starting at half unit c: two, or the last one
   auto unit_len = [&](int c) { return c + 2 <= w_hi ? 2 : 1; };
 
-  // the window of the npx pixels from p0 into this wave's buffer b (segment
-  // i's rows of cells, rounded up to 64 cells, per channel block)
-  auto load_window = [&](int p0, int npx, int b) {
-    WpTile tl;
-    tl.init(a, p0, npx);
-    const uint32_t dst0 = wv0 + b * WINB;
-    int off = 0;
-    for (int i = 0; i < tl.nseg; ++i) {
+  // the workgroup's input window: segment i's rows of cells (each image the
+  // range touches), rounded up to 64 cells, per channel block; chunk j of
+  // the segments' chunk list by wave j % 8
+  WpTile wt;
+  wt.init(a, P0, P1 - P0);
+  auto load_window = [&]() {
+    int off = 0, jbase = 0;
+    for (int i = 0; i < wt.nseg; ++i) {
       int iya;
-      const int cells = tl.rows(a, i, iya) * W;
+      const int cells = wt.rows(a, i, iya) * W;
       const int nch = wp_round64(cells) >> 6;
-      for (int j = 0; j < nch; ++j) {
+      int j = wave - jbase;
+      j += j < 0 ? ((-j + NW - 1) / NW) * NW : 0;
+      for (; j < nch; j += NW) {
         const int c = j * 64 + lane;
-        const int64_t src = ((int64_t)(tl.n_first + i) * G * HW + iya * W + c) * 16;
+        const int64_t src = ((int64_t)(wt.n_first + i) * G * HW + iya * W + c) * 16;
         for (int g = 0; g < G; ++g)
           dma16(c < cells ? a.x + src + (int64_t)g * HW * 16 : zero_src,
-                dst0 + (uint32_t)(g * wstr + (off + j * 64) * 16));
+                lds0 + WIN + (uint32_t)(g * wstr + (off + j * 64) * 16));
       }
+      jbase += nch;
       off += wp_round64(cells);
     }
   };
-  // the shortcut cells of the pixels from p0 (identity join) into buffer b
-  auto load_shortcut = [&](int p0, int b) {
-    const int p = p0 + lane;
+  // the shortcut cells of the workgroup's pixels (identity join), 64 a chunk
+  auto load_shortcut = [&]() {
     const uint8_t* sc8 = reinterpret_cast<const uint8_t*>(a.shortcut);
-    const uint8_t* src = zero_src;
-    if (p < a.m) {
-      if (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64) {
-        const int nimg = fdiv(p, a.div_howo);
-        src = sc8 + (((int64_t)nimg * (a.cout >> 6) + (co0 >> 6)) * howo + (p - nimg * howo)) * 16;
-      } else {
-        src = sc8 + ((int64_t)p * a.cout + co0) / 4;
+    for (int q = wave; q * 64 < P1 - P0; q += NW) {
+      const int p = P0 + q * 64 + lane;
+      const uint8_t* src = zero_src;
+      if (p < P1) {
+        if (a.sc_layout == IFQ_LAYOUT_U2_BLOCK64) {
+          const int nimg = fdiv(p, a.div_howo);
+          src = sc8 + (((int64_t)nimg * (a.cout >> 6) + (co0 >> 6)) * howo + (p - nimg * howo)) * 16;
+        } else {
+          src = sc8 + ((int64_t)p * a.cout + co0) / 4;
+        }
       }
+      dma16(src, lds0 + SCO + (uint32_t)(q * 1024));
     }
-    dma16(src, wv0 + 2 * WINB + b * SC_BYTES);
   };
   // this wave's output tile (npx pixels from p0) to HBM: lane = pixel
   auto store_unit = [&](int p0, int npx) {
@@ -533,7 +538,7 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
     }
   };
 
-  // ---- prologue: records, weights, every wave's first window -------------
+  // ---- prologue: records, weights, the window and shortcut cells ---------
   if constexpr (SW) {
     if (wave == 0) {
       const int c = co0 + lane;
@@ -561,21 +566,17 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
       dma16s(wbase + off, voff, lds0 + WGT + (uint32_t)(c * 1024));
     }
   }
-  if (w_lo < w_hi) {
-    load_window(w_lo * HU, unit_len(w_lo) * HU, 0);
-    if constexpr (!SW) load_shortcut(w_lo * HU, 0);
+  if (P0 < P1) {
+    load_window();
+    if constexpr (!SW) load_shortcut();
   }
-  // the zero cell after every block window of both buffers
-  if (lane < 2 * G) {
-    const int b = lane / G, g = lane - b * G;
-    *reinterpret_cast<uint4*>(lds + WV + wave * WV_BYTES + b * WINB + g * wstr + wcells * 16) =
-        uint4{0, 0, 0, 0};
-  }
+  // the zero cell after every block window
+  if (tid < G) *reinterpret_cast<uint4*>(lds + WIN + tid * wstr + wcells * 16) = uint4{0, 0, 0, 0};
   wait_vmcnt<0>();
   __syncthreads();
   if constexpr (!SW) {
     stage_idj_pk(reinterpret_cast<const int32_t*>(lds + OUT), lds + TBL, BM,
-                 a.cout - co0 < BM ? a.cout - co0 : BM);
+                 a.cout - co0 < BM ? a.cout - co0 : BM, SC16 ? 4 : 0, 27 * a.cin);
     __syncthreads();
   }
   if constexpr (SC16) {
@@ -606,8 +607,8 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
     v8i b8[F4 ? FN : 1];
   };
 
-  // ---- one unit: NB pixel blocks of 32 from p0, window buffer b ----------
-  auto run_unit = [&](auto nb_tag, int p0, int b) {
+  // ---- one unit: NB pixel blocks of 32 from p0 ----------------------------
+  auto run_unit = [&](auto nb_tag, int p0) {
     constexpr int NB = decltype(nb_tag)::value;
     constexpr int kGroups = KH * NB;             // MFMA groups of a tap
     // per-lane LDS offsets of the nine taps of each pixel block: the
@@ -615,8 +616,6 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
     // image, and pixels past the last, read the zero cell
     int boff[NB][kWpTaps];
     {
-      WpTile tl;
-      tl.init(a, p0, NB * 32);
       const int zc = wcells * 16 + 8 * h;
 #pragma unroll
       for (int fn = 0; fn < NB; ++fn) {
@@ -628,10 +627,10 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
         const int oy = fdiv(rem, a.div_wo);
         const int ox = rem - oy * Wo;
         int my_off = 0, my_iya = 0, off = 0;
-        for (int i = 0; i < tl.nseg; ++i) {
+        for (int i = 0; i < wt.nseg; ++i) {
           int iya;
-          const int rows = tl.rows(a, i, iya);
-          if (i == n - tl.n_first) {
+          const int rows = wt.rows(a, i, iya);
+          if (i == n - wt.n_first) {
             my_off = off;
             my_iya = iya;
           }
@@ -652,7 +651,7 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
     // main loop: written first by the zero-addend MFMAs of the first tap
     v16i acc[FM][NB];
     v16f accf[F4 ? FM : 1][F4 ? NB : 1];
-    const uint8_t* winb = lds + WV + wave * WV_BYTES + b * WINB;
+    const uint8_t* winb = lds + WIN;
     // weight fragments of a tap (K32 halves x channel blocks) and the raw
     // codes of its pixel blocks
     auto read_a = [&](int g, int tap, v4i (&af)[KH][FM]) {
@@ -772,14 +771,14 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
                                            h, l32, co0, fn * 32, otile, orow);
       } else {
         if (a.acc_dump) {
-          const v16i one2[1][1] = {{acc[fm][fn]}};
+          const v16i one2[1][1] = {{SC16 ? acc[fm][fn] >> 4 : acc[fm][fn]}};
           epilogue32<kE32I32, 1, 1>(a, lds + TBL, one2, fm, fn, h, l32, co0, p0, NB * 32, otile,
                                     orow, a.acc_dump);
         }
         const int pl = fn * 32 + l32;
         const int cl = fm * 32;
         const uint2 sc[1] = {*reinterpret_cast<const uint2*>(
-            lds + WV + wave * WV_BYTES + 2 * WINB + b * SC_BYTES + pl * 16 + (cl >> 2))};
+            lds + SCO + (p0 - P0 + pl) * 16 + (cl >> 2))};
         epilogue_idj_pk<1>(a, lds + TBL, one, sc, fm, h, co0, pl, otile, orow);
       }
     }
@@ -789,27 +788,14 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
     asm volatile("" ::: "memory");
   };
 
-  int b = 0;
-  for (int c = w_lo; c < w_hi; b ^= 1) {
+  for (int c = w_lo; c < w_hi;) {
     const int len = unit_len(c);
-    const int nx = c + len;
-    // the window of this unit has landed (and the stores of two units back
-    // have drained); the next unit's loads and the previous unit's stores
-    // then run under this unit's main loop
-    if (c != w_lo) wait_vmcnt<0>();
-    __builtin_amdgcn_sched_barrier(0);
-    if (nx < w_hi) {
-      load_window(nx * HU, unit_len(nx) * HU, b ^ 1);
-      if constexpr (!SW) load_shortcut(nx * HU, b ^ 1);
-    }
-    if (c != w_lo) store_unit((c - 2) * HU, 2 * HU);   // every unit but the last is whole
-    __builtin_amdgcn_sched_barrier(0);
     if (len == 2)
-      run_unit(std::integral_constant<int, 2>{}, c * HU, b);
+      run_unit(std::integral_constant<int, 2>{}, c * HU);
     else
-      run_unit(std::integral_constant<int, 1>{}, c * HU, b);
-    if (nx >= w_hi) store_unit(c * HU, len * HU);
-    c = nx;
+      run_unit(std::integral_constant<int, 1>{}, c * HU);
+    store_unit(c * HU, len * HU);
+    c += len;
   }
 }
 
@@ -848,23 +834,29 @@ const WpVariant kWpVariants[] = {
 constexpr int kNumWpBlock = sizeof(kWpVariants) / sizeof(kWpVariants[0]);
 
 // The wave-independent kernel: one workgroup of eight waves per CU, a unit
-// of 64 pixels x 64 channels per wave at a time. Fitted the same way: a
-// prologue (weights, records, first windows) and, per unit, a fixed and a
-// per-channel-block cost, with two waves sharing each SIMD.
+// of 64 pixels x 64 channels per wave at a time. Fitted the same way (the
+// ResNet-18-shaped stack's 64- and 128-channel layers, VGG-16's conv1_2 to
+// conv3_1 and small batches, int8 and fp4): a prologue (weights, records,
+// the workgroup's window) and, per unit, a fixed and a per-channel-block
+// cost, with two waves sharing each SIMD.
 struct WvVariant {
   bool f4;
-  int winb_thr, winb_idj;   // window buffer bytes per wave
+  int winb_thr, winb_idj;   // window bytes of a workgroup
   double pro_us, c_unit_us, c_blk_us, idj_us;
   const char* thr_name;
   const char* idj_name;
 };
 #define IFQ_WV_NAME(mode, f4, winb) "conv_wv<" #mode ", " #f4 ", " #winb ">"
+// The identity join's shortcut cells take the LDS past its window: 160 KB
+// less the weights, packed records, output tiles and window.
+constexpr int kWvLds = 160 * 1024;
+constexpr int kWvFixedIdj = 36864 + 16 * 512 + 8 * 1024;
 // Index order must match the switch in launch_conv_wp.
 const WvVariant kWvVariants[] = {
-    {false, 7168, 5888, 2.5, 1.2, 1.0, 0.32,
-     IFQ_WV_NAME(0, false, 7168), IFQ_WV_NAME(1, false, 5888)},
-    {true, 7168, 5888, 2.5, 1.0, 0.65, 0.37,
-     IFQ_WV_NAME(0, true, 7168), IFQ_WV_NAME(1, true, 5888)},
+    {false, 114688, 77824, 1.7, 1.3, 1.0, 0.2,
+     IFQ_WV_NAME(0, false, 114688), IFQ_WV_NAME(1, false, 77824)},
+    {true, 114688, 77824, 1.7, 1.12, 0.5, 0.5,
+     IFQ_WV_NAME(0, true, 114688), IFQ_WV_NAME(1, true, 77824)},
 };
 constexpr int kNumWv = sizeof(kWvVariants) / sizeof(kWvVariants[0]);
 constexpr int kNumWp = kNumWpBlock + kNumWv;
@@ -893,6 +885,24 @@ bool wp_fit(const ConvLaunch& a, int v, WpPlan* out) {
   return true;
 }
 
+// Cells per channel block of the input window of output pixels [p0, p1)
+// (each image's rows rounded up to 64 cells), as the wave kernel lays it.
+int64_t wv_window_cells(const ConvLaunch& a, int64_t p0, int64_t p1) {
+  const int64_t howo = (int64_t)a.ho * a.wo;
+  const int64_t pend = p1 - 1;
+  const int64_t nf = p0 / howo, nl = pend / howo;
+  const int64_t oyf = (p0 - nf * howo) / a.wo, oyl = (pend - nl * howo) / a.wo;
+  int64_t tot = 0;
+  for (int64_t i = 0; i <= nl - nf; ++i) {
+    const int64_t oya = i == 0 ? oyf : 0, oyb = i == nl - nf ? oyl : a.ho - 1;
+    int64_t iya = oya * a.stride - 1, iyb = oyb * a.stride + 1;
+    if (iya < 0) iya = 0;
+    if (iyb > a.h - 1) iyb = a.h - 1;
+    tot += ((iyb - iya + 1) * a.w + 63) / 64 * 64;
+  }
+  return tot;
+}
+
 bool wv_fit(const ConvLaunch& a, int v, WpPlan* out) {
   const WvVariant& V = kWvVariants[v];
   if (V.f4 != (a.f4 != 0) || a.cout % 64 != 0) return false;
@@ -900,16 +910,33 @@ bool wv_fit(const ConvLaunch& a, int v, WpPlan* out) {
   const int kh = V.f4 ? 1 : 2;
   if ((int64_t)G * kWpTaps * 2 * kh * 1024 > 36864) return false;
   const bool idj = a.join_kind == IFQ_JOIN_IDENTITY;
-  const int winb = idj ? V.winb_idj : V.winb_thr;
-  // units of 64 pixels at any multiple of 32 (a wave's range starts at a
-  // half unit)
-  const int64_t cells = window_cells_max(a, kWvUnit, (int64_t)winb / 16 / G, kWvUnit / 2);
-  if (cells < 0 || (int64_t)G * (cells + 1) * 16 > winb) return false;
+  const int64_t winb = idj ? V.winb_idj : V.winb_thr;
+  const int64_t scb = idj ? kWvLds - kWvFixedIdj - winb : 0;
   const int64_t nco = a.cout / 64;
-  const int64_t nhu = (a.m + kWvUnit / 2 - 1) / (kWvUnit / 2);  // half units
+  const int64_t hu = kWvUnit / 2;
+  const int64_t nhu = (a.m + hu - 1) / hu;                      // half units
   int64_t gx = kPlanCUs / nco;
   if (gx < 1) gx = 1;
   if (gx > (nhu + kWvWaves - 1) / kWvWaves) gx = (nhu + kWvWaves - 1) / kWvWaves;
+  // more workgroups (in rounds) until each one's window and shortcut cells
+  // fit; the window cells of the largest
+  int64_t cells = -1;
+  for (; gx <= nhu; gx *= 2) {
+    int64_t mx = 0, px = 0;
+    for (int64_t k = 0; k < gx; ++k) {
+      const int64_t p0 = k * nhu / gx * hu;
+      int64_t p1 = (k + 1) * nhu / gx * hu;
+      if (p1 > a.m) p1 = a.m;
+      const int64_t c = wv_window_cells(a, p0, p1);
+      if (c > mx) mx = c;
+      if (p1 - p0 > px) px = p1 - p0;
+    }
+    if (G * (mx + 1) * 16 <= winb && (!idj || (px + 63) / 64 * 1024 <= scb)) {
+      cells = mx;
+      break;
+    }
+  }
+  if (cells < 0 || gx > nhu) return false;
   const int64_t hw = (nhu + gx - 1) / gx;                        // half units per workgroup
   const int64_t per_wave = (hw + kWvWaves - 1) / kWvWaves;
   const int64_t rounds = (gx * nco + kPlanCUs - 1) / kPlanCUs;   // one workgroup per CU
@@ -988,8 +1015,8 @@ hipError_t launch_conv_wp(ConvLaunch a, const WpPlan& p, hipStream_t stream) {
   case 2 * k + 1:                                                                          \
     hipLaunchKernelGGL((conv_wv<1, f4, winbi>), grid, block, 0, stream, a);                \
     break;
-      IFQ_WV_CASE(0, false, 7168, 5888)
-      IFQ_WV_CASE(1, true, 7168, 5888)
+      IFQ_WV_CASE(0, false, 114688, 77824)
+      IFQ_WV_CASE(1, true, 114688, 77824)
 #undef IFQ_WV_CASE
       default: return hipErrorInvalidValue;
     }

@@ -293,8 +293,11 @@ __device__ __forceinline__ void epilogue_thr_pk(const ConvLaunch& a, const uint8
 constexpr int kIdjGroupBytes = 512;
 
 // tbl: the bm channels' [4][4] int32 records (global or LDS); channels at or
-// past nch get plain records (their codes are never stored).
-__device__ __forceinline__ void stage_idj_pk(const int32_t* tbl, uint8_t* lds, int bm, int nch) {
+// past nch get plain records (their codes are never stored). sh > 0: for
+// sums kept as 2^sh a, each T' is clamped to [-bnd-1, bnd] (bnd bounds |a|,
+// so no comparison changes) and scaled by 2^sh.
+__device__ __forceinline__ void stage_idj_pk(const int32_t* tbl, uint8_t* lds, int bm, int nch,
+                                             int sh = 0, int bnd = 0) {
   for (int e = threadIdx.x; e < (bm / 4) * 32; e += blockDim.x) {
     const int gq = e >> 5, pr = (e >> 4) & 1, combo = e & 15;
     const int x[2] = {combo & 3, combo >> 2};
@@ -308,7 +311,8 @@ __device__ __forceinline__ void stage_idj_pk(const int32_t* tbl, uint8_t* lds, i
       const int t[3] = {r.y, r.z, r.w};
 #pragma unroll
       for (int k = 0; k < 3; ++k) {
-        const int v = flip ? -t[k] - 1 : t[k];
+        int v = flip ? -t[k] - 1 : t[k];
+        if (sh > 0) v = (v < -bnd - 1 ? -bnd - 1 : (v > bnd ? bnd : v)) * (1 << sh);
         w[k] |= ((uint32_t)v & 0xFFFFu) << (16 * j);
       }
       if (flip) w[3] |= 3u << (16 * j);
