@@ -49,7 +49,8 @@ def build(verbose=False):
             raise RuntimeError("hipcc failed:\n" + err)
         objs.append(obj)
     tmp = LIB + ".tmp" + tag
-    cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
+    cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-Wl,--no-undefined",
+           "-o", tmp] + objs
     r = subprocess.run(cmd, capture_output=True, text=True)
     for o in objs:
         os.remove(o)

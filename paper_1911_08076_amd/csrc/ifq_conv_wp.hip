@@ -420,20 +420,21 @@ __global__ __launch_bounds__(64 * WN, (WN / 4) * OCC) void conv_wp(ConvLaunch a)
 // as units of 64 pixels x the 64-channel slice and, where its count is odd,
 // one last unit of 32 pixels (half the MFMAs). So the two waves of a SIMD
 // carry nearly the same work and neither runs long alone.
-template <int MODE, bool F4, int WINB>
+template <int MODE, bool F4, int WGTB, int WINB>
 __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
   constexpr bool SW = MODE == 0;                 // transposed sums
   constexpr int NW = 8, FM = 2, FN = 2;
   constexpr int BM = 64, UN = 64, HU = 32;       // unit: 64 channels x 64 pixels
   constexpr int KH = F4 ? 1 : 2;
   constexpr int RB = FM;
-  constexpr int WGTB = 36864;
-  // int8 instances (one channel block: K = 576): the code operand keeps each
-  // 2-bit field in place within its byte (1, 4, 16 or, shifted down once,
-  // 16 times the code) and the weight bytes that meet fields 0 and 1 are
-  // scaled by 16 and 4 in LDS, so every product is 16 * w * x: the sums are
-  // 16 a, |16 a| <= 16 * 3 * 576 < 2^15, compared against 16 T.
-  constexpr bool SC16 = !F4;
+  static_assert(WGTB % 1024 == 0, "weight chunks");
+  // int8 instances for one channel block (K = 576, WGTB = 36 KB): the code
+  // operand keeps each 2-bit field in place within its byte (1, 4, 16 or,
+  // shifted down once, 16 times the code) and the weight bytes that meet
+  // fields 0 and 1 are scaled by 16 and 4 in LDS, so every product is
+  // 16 * w * x: the sums are 16 a, |16 a| <= 16 * 3 * 576 < 2^15, compared
+  // against 16 T.
+  constexpr bool SC16 = !F4 && WGTB == 36864;
   // LDS: the slice's weights, the records (raw for the threshold epilogue,
   // packed for the identity join), one output tile per wave (the identity
   // join's raw records sit there until they are packed), the workgroup's
@@ -714,10 +715,17 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
     // tap i + 2 are read, and tap i + 1's B operands are unpacked from codes
     // read a whole tap earlier, one piece after each MFMA group from the
     // second on.
+    // Operand registers rotate through rings of three (weights, raw codes,
+    // unpacked codes): an LDS read or an unpack never writes a register that
+    // one of the last few MFMAs still reads, which would hold the write (and
+    // the wave) until that MFMA has taken its operands. The empty asm at the
+    // end of a tap keeps the tap's operands live to there, so the compiler
+    // cannot hand their registers to the next tap's reads and unpacks; those
+    // of the previous tap too, whose last MFMAs may still be reading them.
     auto run_block = [&](auto zc, int g) {
-      v4i af[2][KH][FM];
+      v4i af[3][KH][FM];
       v2i br[3][NB];
-      Unp uu[2];
+      Unp uu[3];
       read_b(g, 0, br[0]);
       read_a(g, 0, af[0]);
       read_b(g, 1, br[1]);
@@ -725,9 +733,9 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
       for (int k = 0; k < kGroups; ++k) unpack_piece(br[0], uu[0], k);
 #pragma unroll
       for (int tap = 0; tap < kWpTaps; ++tap) {
-        const int c = tap & 1;
+        const int c = tap % 3, n1 = (tap + 1) % 3;
         const bool nxt = tap + 1 < kWpTaps;
-        if (nxt) read_a(g, tap + 1, af[c ^ 1]);
+        if (nxt) read_a(g, tap + 1, af[n1]);
         if (tap + 2 < kWpTaps) read_b(g, tap + 2, br[(tap + 2) % 3]);
 #pragma unroll
         for (int k = 0; k < kGroups; ++k) {
@@ -737,10 +745,30 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
           else
             mfma_group(std::false_type{}, af[c], uu[c], k);
           __builtin_amdgcn_sched_barrier(0);
-          if (nxt && k >= 1) unpack_piece(br[(tap + 1) % 3], uu[c ^ 1], k - 1);
+          if (nxt && k >= 1) unpack_piece(br[n1], uu[n1], k - 1);
         }
-        if (nxt) unpack_piece(br[(tap + 1) % 3], uu[c ^ 1], kGroups - 1);
+        if (nxt) unpack_piece(br[n1], uu[n1], kGroups - 1);
         __builtin_amdgcn_sched_barrier(0);
+        // this tap's operands and the previous tap's stay live to here
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          if (e == 1 && tap == 0) break;
+          const int q = (tap + 3 - e) % 3;
+#pragma unroll
+          for (int t = 0; t < KH; ++t)
+#pragma unroll
+            for (int fm = 0; fm < FM; ++fm) asm volatile("" ::"v"(af[q][t][fm]));
+#pragma unroll
+          for (int fn = 0; fn < NB; ++fn) {
+            if constexpr (F4) {
+#pragma unroll
+              for (int i = 0; i < 4; ++i) asm volatile("" ::"v"(uu[q].b8[fn][i]));
+            } else {
+#pragma unroll
+              for (int t = 0; t < KH; ++t) asm volatile("" ::"v"(uu[q].b4[t][fn]));
+            }
+          }
+        }
       }
     };
     __builtin_amdgcn_s_setprio(1);
@@ -835,28 +863,35 @@ constexpr int kNumWpBlock = sizeof(kWpVariants) / sizeof(kWpVariants[0]);
 
 // The wave-independent kernel: one workgroup of eight waves per CU, a unit
 // of 64 pixels x 64 channels per wave at a time. Fitted the same way (the
-// ResNet-18-shaped stack's 64- and 128-channel layers, VGG-16's conv1_2 to
-// conv3_1 and small batches, int8 and fp4): a prologue (weights, records,
-// the workgroup's window) and, per unit, a fixed and a per-channel-block
-// cost, with two waves sharing each SIMD.
+// ResNet-18-shaped stack's 64- to 256-channel layers, VGG-16's and
+// Tiny-YOLOv2's, small batches, int8 and fp4): a prologue (weights,
+// records, the workgroup's window) and, per unit, a fixed and a
+// per-channel-block cost, with two waves sharing each SIMD.
 struct WvVariant {
   bool f4;
+  int wgtb;                 // weight slab bytes
   int winb_thr, winb_idj;   // window bytes of a workgroup
   double pro_us, c_unit_us, c_blk_us, idj_us;
   const char* thr_name;
   const char* idj_name;
 };
-#define IFQ_WV_NAME(mode, f4, winb) "conv_wv<" #mode ", " #f4 ", " #winb ">"
+#define IFQ_WV_NAME(mode, f4, wgtb, winb) \
+  "conv_wv<" #mode ", " #f4 ", " #wgtb ", " #winb ">"
 // The identity join's shortcut cells take the LDS past its window: 160 KB
 // less the weights, packed records, output tiles and window.
 constexpr int kWvLds = 160 * 1024;
-constexpr int kWvFixedIdj = 36864 + 16 * 512 + 8 * 1024;
-// Index order must match the switch in launch_conv_wp.
+constexpr int kWvFixedIdj = 16 * 512 + 8 * 1024;   // plus the weights
+// Index order must match the switch in launch_conv_wp. Weight slabs of
+// 36 KB (int8: one channel block; fp4: two) or 72 KB (int8: two; fp4: four).
 const WvVariant kWvVariants[] = {
-    {false, 114688, 77824, 1.7, 1.3, 1.0, 0.2,
-     IFQ_WV_NAME(0, false, 114688), IFQ_WV_NAME(1, false, 77824)},
-    {true, 114688, 77824, 1.7, 1.12, 0.5, 0.5,
-     IFQ_WV_NAME(0, true, 114688), IFQ_WV_NAME(1, true, 77824)},
+    {false, 36864, 114688, 77824, 2.86, 0.8, 1.0, 0.4,
+     IFQ_WV_NAME(0, false, 36864, 114688), IFQ_WV_NAME(1, false, 36864, 77824)},
+    {true, 36864, 114688, 77824, 2.0, 0.8, 0.62, 0.53,
+     IFQ_WV_NAME(0, true, 36864, 114688), IFQ_WV_NAME(1, true, 36864, 77824)},
+    {false, 73728, 80896, 49152, 2.58, 0.54, 1.28, 0.37,
+     IFQ_WV_NAME(0, false, 73728, 80896), IFQ_WV_NAME(1, false, 73728, 49152)},
+    {true, 73728, 80896, 49152, 1.73, 0.83, 0.69, 0.6,
+     IFQ_WV_NAME(0, true, 73728, 80896), IFQ_WV_NAME(1, true, 73728, 49152)},
 };
 constexpr int kNumWv = sizeof(kWvVariants) / sizeof(kWvVariants[0]);
 constexpr int kNumWp = kNumWpBlock + kNumWv;
@@ -908,10 +943,10 @@ bool wv_fit(const ConvLaunch& a, int v, WpPlan* out) {
   if (V.f4 != (a.f4 != 0) || a.cout % 64 != 0) return false;
   const int G = a.cin / 64;
   const int kh = V.f4 ? 1 : 2;
-  if ((int64_t)G * kWpTaps * 2 * kh * 1024 > 36864) return false;
+  if ((int64_t)G * kWpTaps * 2 * kh * 1024 > V.wgtb) return false;
   const bool idj = a.join_kind == IFQ_JOIN_IDENTITY;
   const int64_t winb = idj ? V.winb_idj : V.winb_thr;
-  const int64_t scb = idj ? kWvLds - kWvFixedIdj - winb : 0;
+  const int64_t scb = idj ? kWvLds - kWvFixedIdj - V.wgtb - winb : 0;
   const int64_t nco = a.cout / 64;
   const int64_t hu = kWvUnit / 2;
   const int64_t nhu = (a.m + hu - 1) / hu;                      // half units
@@ -1008,15 +1043,17 @@ hipError_t launch_conv_wp(ConvLaunch a, const WpPlan& p, hipStream_t stream) {
     const dim3 block(64 * kWvWaves);
     const int mode = a.join_kind == IFQ_JOIN_IDENTITY ? 1 : 0;
     switch ((p.variant - kNumWpBlock) * 2 + mode) {
-#define IFQ_WV_CASE(k, f4, winbt, winbi)                                                   \
+#define IFQ_WV_CASE(k, f4, wgtb, winbt, winbi)                                             \
   case 2 * k:                                                                              \
-    hipLaunchKernelGGL((conv_wv<0, f4, winbt>), grid, block, 0, stream, a);                \
+    hipLaunchKernelGGL((conv_wv<0, f4, wgtb, winbt>), grid, block, 0, stream, a);          \
     break;                                                                                 \
   case 2 * k + 1:                                                                          \
-    hipLaunchKernelGGL((conv_wv<1, f4, winbi>), grid, block, 0, stream, a);                \
+    hipLaunchKernelGGL((conv_wv<1, f4, wgtb, winbi>), grid, block, 0, stream, a);          \
     break;
-      IFQ_WV_CASE(0, false, 114688, 77824)
-      IFQ_WV_CASE(1, true, 114688, 77824)
+      IFQ_WV_CASE(0, false, 36864, 114688, 77824)
+      IFQ_WV_CASE(1, true, 36864, 114688, 77824)
+      IFQ_WV_CASE(2, false, 73728, 80896, 49152)
+      IFQ_WV_CASE(3, true, 73728, 80896, 49152)
 #undef IFQ_WV_CASE
       default: return hipErrorInvalidValue;
     }

@@ -248,13 +248,13 @@ def test_conv_block64_bit_exact(P, case, io):
 # Workgroup tiles of the size the ResNet-18 layers of the benchmark run with
 # (the 3x3 kernels' tiles of 256, 128 and 64 output pixels, stride-2 layers),
 # at batches the oracle finishes in about a second; the test also pins which
-# kernel variant the planner takes for each (conv_w2; the eighth template
-# argument is its epilogue: 0 thresholds).
+# kernel variant the planner takes for each (conv_w2, whose eighth template
+# argument is its epilogue, 0 thresholds; or the wave-independent conv_wv).
 HALO_TILES = [
-    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_w2<1, 4, 1, 2, 2, 3, 3, 0, false, 2, 20480>"),
+    ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_wv<0, false, 73728, 80896>"),
     ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_w2<1, 4, 2, 2, 2, 3, 2, 0, false, 1, 53248>"),
     ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, 0, false, 1, 36864>"),
-    ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_w2<1, 4, 2, 2, 2, 3, 2, 0, false, 1, 53248>"),
+    ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_wv<0, false, 73728, 80896>"),
     ("halo_l1_b24", 24, 56, 56, 64, 64, 1, "conv_w2<1, 4, 1, 2, 2, 3, 3, 0, false, 2, 20480>"),
     # the stride-2 layers at the full batch of 64, with the largest windows
     ("halo_l2s2_b64", 64, 56, 56, 64, 128, 2, "conv_w2<1, 4, 1, 2, 2, 3, 3, 0, false, 2, 20480>"),

@@ -31,10 +31,10 @@ def fp4_kernel(name):
 
 # name, n, h, c_in, c_out, stride, expected variant
 FP4 = [
-    ("f4_c64_small_batch", 2, 56, 64, 64, 1, "conv_wv<0, true, 114688>"),
+    ("f4_c64_small_batch", 2, 56, 64, 64, 1, "conv_wv<0, true, 73728, 80896>"),
     ("f4_l2", 3, 28, 128, 128, 1, None),
     ("f4_l2_0_s2", 2, 56, 64, 128, 2, None),
-    ("f4_l3", 4, 14, 256, 256, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, 0, true, 1, 36864>"),
+    ("f4_l3", 4, 14, 256, 256, 1, "conv_wv<0, true, 73728, 80896>"),
     ("f4_l4", 6, 7, 512, 512, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, 0, true, 1, 36864>"),
 ]
 
@@ -77,8 +77,8 @@ def test_fp4_offered_for_the_64_channel_tiles(P):
     # kernel (the slice's weights resident in LDS, one workgroup per CU),
     # which has an fp4 instance
     d = P.conv_desc(64, 56, 56, 64, 64, 3, 1, 1, 2, 2, B64, B64)
-    assert P.ifq_conv_kernel_name(d) == "conv_wv<0, false, 114688>"
-    assert P.ifq_conv_fp4_kernel_name(d) == "conv_wv<0, true, 114688>"
+    assert P.ifq_conv_kernel_name(d) == "conv_wv<0, false, 73728, 80896>"
+    assert P.ifq_conv_fp4_kernel_name(d) == "conv_wv<0, true, 36864, 114688>"
     # a fused pool is not the register-blocked kernel's: the windowed
     # kernel's fp4 instances take it
     pd = P.pool_desc(64, 56, 56, 64, 2, 2, P.IFQ_POOL_VALID, 2, B64)

@@ -55,7 +55,7 @@ FULL = [
 ]
 
 
-NVAR = 14   # conv_w2's ten, then conv_wp's two and conv_wv's two
+NVAR = 16   # conv_w2's ten, then conv_wp's two and conv_wv's four
 NW2 = 10    # conv_w2's variants
 
 
