@@ -150,6 +150,32 @@ def test_variant_u2_output(P):
     _check(P, SMALL[0], 0, False, out_layout=U2)
 
 
+@pytest.mark.parametrize("variant", range(NW2 + 2, NVAR), ids=lambda v: "v%d" % v)
+@pytest.mark.parametrize("join", [False, True], ids=["thr", "idj"])
+def test_wave_kernel_nhwc_packed_layouts(P, variant, join):
+    # the wave-independent kernel's own stores and shortcut loads in the NHWC
+    # packed layout (output, and the identity join's shortcut), on a ragged
+    # multi-image layer
+    name, n, h, w, cin, cout, st = ("r17x23_64_64", 3, 17, 23, 64, 64, 1)
+    L = make_layer(name, h, w, cin, cout, 3, st, 1, 2, 2, ("identity", "x") if join else None)
+    seed = zlib.crc32((name + "u2" + str(join)).encode()) % 997
+    p = params_for(seed, L)
+    x = codes_for(seed, (n, h, w, cin), 2)
+    sc = codes_for(seed + 1, (n, h, w, cin), 2) if join else None
+    d = P.conv_desc(n, h, w, cin, cout, 3, st, 1, 2, 2, B64, U2)
+    jn = _thr_join(P, join, p["q_thr"])
+    if jn is not None:
+        jn.layout = U2
+    name_v = P.ifq_conv_variant_name(d, jn, variant)
+    assert name_v.startswith("conv_wv<"), name_v
+    want_acc, want = oracle_layer(L, x, p, shortcut=sc)
+    acc, got = gpu_layer(P, L, n, x, p, in_layout=B64, out_layout=U2, shortcut=sc,
+                         sc_layout=U2, variant=variant)
+    assert np.array_equal(acc, want_acc), variant
+    assert np.array_equal(got, expect_layout(want, U2)), variant
+    assert len(np.unique(want)) > 1
+
+
 # downsampling blocks' second conv with the 1x1 stride-2 downsample fused:
 # (n, h_in, c_in, c_out); ragged, small and the full ResNet-18 shapes
 FUSED = [(2, 56, 64, 128), (3, 28, 128, 256), (2, 14, 256, 512), (5, 13, 64, 128),
