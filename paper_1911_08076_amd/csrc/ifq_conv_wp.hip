@@ -886,7 +886,7 @@ const WvVariant kWvVariants[] = {
      IFQ_WV_NAME(0, false, 36864, 114688), IFQ_WV_NAME(1, false, 36864, 77824)},
     {true, 36864, 114688, 77824, 2.0, 0.8, 0.62, 0.53,
      IFQ_WV_NAME(0, true, 36864, 114688), IFQ_WV_NAME(1, true, 36864, 77824)},
-    {false, 73728, 80896, 49152, 2.58, 0.54, 1.28, 0.37,
+    {false, 73728, 80896, 49152, 2.58, 0.45, 1.28, 0.37,
      IFQ_WV_NAME(0, false, 73728, 80896), IFQ_WV_NAME(1, false, 73728, 49152)},
     {true, 73728, 80896, 49152, 1.73, 0.83, 0.69, 0.6,
      IFQ_WV_NAME(0, true, 73728, 80896), IFQ_WV_NAME(1, true, 73728, 49152)},

@@ -255,9 +255,9 @@ HALO_TILES = [
     ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_w2<1, 4, 2, 2, 2, 3, 2, 0, false, 1, 53248>"),
     ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, 0, false, 1, 36864>"),
     ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_wv<0, false, 73728, 80896>"),
-    ("halo_l1_b24", 24, 56, 56, 64, 64, 1, "conv_w2<1, 4, 1, 2, 2, 3, 3, 0, false, 2, 20480>"),
+    ("halo_l1_b24", 24, 56, 56, 64, 64, 1, "conv_wv<0, false, 73728, 80896>"),
     # the stride-2 layers at the full batch of 64, with the largest windows
-    ("halo_l2s2_b64", 64, 56, 56, 64, 128, 2, "conv_w2<1, 4, 1, 2, 2, 3, 3, 0, false, 2, 20480>"),
+    ("halo_l2s2_b64", 64, 56, 56, 64, 128, 2, "conv_wv<0, false, 73728, 80896>"),
     ("halo_l4s2_b64", 64, 14, 14, 256, 512, 2, "conv_w2<1, 4, 2, 2, 2, 3, 2, 0, false, 1, 53248>"),
 ]
 
