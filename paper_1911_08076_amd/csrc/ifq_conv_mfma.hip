@@ -32,6 +32,9 @@
 // residual join without cross-lane traffic.
 #include <hip/hip_runtime.h>
 
+#include <cstring>
+#include <mutex>
+
 #include "ifq_epilogue.h"
 #include "ifq_internal.h"
 #include "ifq_mfma_common.h"
@@ -372,6 +375,92 @@ bool mfma_eligible(const ConvLaunch& a) {
          (a.in_layout == IFQ_LAYOUT_U2_NHWC_PACKED || a.in_layout == IFQ_LAYOUT_U2_BLOCK64);
 }
 
+// The dispatcher's choice among the three MFMA kernels for one layer, and
+// their plans. Every planner reads only the launch's geometry, layouts,
+// epilogue and K-split fields (no pointer, no quantizer threshold value), so
+// launches with equal values there get the same choice: it is kept in a
+// small table keyed by those fields, which saves the planners' host time
+// (several microseconds per layer, against kernels of ten) on every launch
+// after the first.
+namespace {
+
+struct MfmaChoice {
+  int kind;   // 0 register-blocked (reg3), 1 windowed, 2 tiled, -1 none
+  HaloPlan hp;
+  Reg3Plan rp;
+  Plan pl;
+};
+
+MfmaChoice plan_choice(const ConvLaunch& a) {
+  MfmaChoice c{};
+  const bool halo = plan_halo(a, &c.hp);
+  const bool r3 = plan_reg3(a, -1, &c.rp);
+  if (a.join_kind == IFQ_JOIN_CONV_FUSED) {
+    c.kind = r3 ? 0 : (halo ? 1 : -1);
+    return c;
+  }
+  c.pl = plan_mfma(a);
+  if (r3 && c.rp.t_us <= c.pl.t_us && (!halo || c.rp.t_us <= c.hp.t_us))
+    c.kind = 0;
+  else if (halo && c.hp.t_us < c.pl.t_us)
+    c.kind = 1;
+  else
+    c.kind = 2;
+  return c;
+}
+
+// The launch with its pointers and threshold values cleared (whether a sum
+// dump is asked for stays a flag); compared byte for byte, so equal keys
+// have equal fields.
+ConvLaunch choice_key(const ConvLaunch& a) {
+  ConvLaunch k;
+  std::memcpy(&k, &a, sizeof(k));
+  k.x = nullptr;
+  k.wgt = nullptr;
+  k.rowsum = nullptr;
+  k.thr = nullptr;
+  k.y = nullptr;
+  k.acc_dump = a.acc_dump ? reinterpret_cast<int32_t*>(alignof(int32_t)) : nullptr;
+  k.shortcut = nullptr;
+  k.coef = nullptr;
+  k.table = nullptr;
+  k.dx = nullptr;
+  k.dwgt = nullptr;
+  k.ws_cnt = nullptr;
+  k.ws_part = nullptr;
+  for (double& q : k.qthr) q = 0.0;
+  return k;
+}
+
+struct ChoiceSlot {
+  bool used;
+  ConvLaunch key;
+  MfmaChoice c;
+};
+constexpr int kChoiceSlots = 256;
+ChoiceSlot g_choice[kChoiceSlots];
+std::mutex g_choice_mu;
+
+MfmaChoice choose_mfma(const ConvLaunch& a) {
+  const ConvLaunch k = choice_key(a);
+  uint64_t hsh = 1469598103934665603ull;   // FNV-1a over the key's bytes
+  const unsigned char* b = reinterpret_cast<const unsigned char*>(&k);
+  for (size_t i = 0; i < sizeof(k); ++i) hsh = (hsh ^ b[i]) * 1099511628211ull;
+  ChoiceSlot& slot = g_choice[hsh % kChoiceSlots];
+  {
+    std::lock_guard<std::mutex> lock(g_choice_mu);
+    if (slot.used && std::memcmp(&slot.key, &k, sizeof(k)) == 0) return slot.c;
+  }
+  const MfmaChoice c = plan_choice(a);
+  std::lock_guard<std::mutex> lock(g_choice_mu);
+  std::memcpy(&slot.key, &k, sizeof(k));
+  slot.c = c;
+  slot.used = true;
+  return c;
+}
+
+}  // namespace
+
 // The fast path picks the kernel with the lowest predicted time among the
 // register-blocked 3x3 kernels (one tile per workgroup or persistent), the
 // windowed 3x3 kernel and the tiled kernel. A fused downsample join runs on
@@ -379,46 +468,26 @@ bool mfma_eligible(const ConvLaunch& a) {
 // downsampling block of the ResNet-18-shaped stack as measured), else on the
 // windowed kernel (the host checks fused_supported before launching one).
 const char* conv_mfma_name(const ConvLaunch& a) {
-  HaloPlan hp;
-  const bool halo = plan_halo(a, &hp);
-  Reg3Plan rp;
-  const bool r3 = plan_reg3(a, -1, &rp);
-  if (a.join_kind == IFQ_JOIN_CONV_FUSED) {
-    if (r3) return reg3_name(rp, a);
-    return halo ? conv_halo_name(hp, a) : "";
-  }
-  const Plan pl = plan_mfma(a);
-  if (r3 && rp.t_us <= pl.t_us && (!halo || rp.t_us <= hp.t_us)) return reg3_name(rp, a);
-  if (halo && hp.t_us < pl.t_us) return conv_halo_name(hp, a);
-  return kVariants[pl.variant].name;
+  const MfmaChoice c = choose_mfma(a);
+  if (c.kind == 0) return reg3_name(c.rp, a);
+  if (c.kind == 1) return conv_halo_name(c.hp, a);
+  if (c.kind < 0) return "";
+  return kVariants[c.pl.variant].name;
 }
 
 // The workspace of the kernel launch_conv_mfma picks (the same choice).
 int64_t conv_mfma_workspace_bytes(const ConvLaunch& a) {
-  HaloPlan hp;
-  const bool halo = plan_halo(a, &hp);
-  Reg3Plan rp;
-  const bool r3 = plan_reg3(a, -1, &rp);
-  if (!r3 || rp.persistent) return 0;
-  if (a.join_kind == IFQ_JOIN_CONV_FUSED) return w2_split_bytes(a, rp.w2);
-  const Plan pl = plan_mfma(a);
-  if (rp.t_us <= pl.t_us && (!halo || rp.t_us <= hp.t_us)) return w2_split_bytes(a, rp.w2);
-  return 0;
+  const MfmaChoice c = choose_mfma(a);
+  if (c.kind != 0 || c.rp.persistent) return 0;
+  return w2_split_bytes(a, c.rp.w2);
 }
 
 hipError_t launch_conv_mfma(const ConvLaunch& a, hipStream_t stream) {
-  HaloPlan hp;
-  const bool halo = plan_halo(a, &hp);
-  Reg3Plan rp;
-  const bool r3 = plan_reg3(a, -1, &rp);
-  if (a.join_kind == IFQ_JOIN_CONV_FUSED) {
-    if (r3) return launch_reg3(a, rp, stream);
-    return halo ? launch_conv_halo(a, hp, stream) : hipErrorNotSupported;
-  }
-  const Plan pl = plan_mfma(a);
-  if (r3 && rp.t_us <= pl.t_us && (!halo || rp.t_us <= hp.t_us))
-    return launch_reg3(a, rp, stream);
-  if (halo && hp.t_us < pl.t_us) return launch_conv_halo(a, hp, stream);
+  const MfmaChoice c = choose_mfma(a);
+  if (c.kind == 0) return launch_reg3(a, c.rp, stream);
+  if (c.kind == 1) return launch_conv_halo(a, c.hp, stream);
+  if (c.kind < 0) return hipErrorNotSupported;
+  const Plan& pl = c.pl;
   switch (pl.variant) {
     case 0: return launch_variant<2, 4, 1, 2, 4, 1, 6>(a, pl, stream);
     case 1: return launch_variant<2, 4, 1, 2, 2, 2, 4>(a, pl, stream);
