@@ -783,29 +783,36 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
           for (int i = 0; i < 16; ++i) acc[fm][fn][i] = (int)accf[fm][fn][i];
     }
 
-    // epilogue into this wave's output tile
+    // epilogue into this wave's output tile: the int32 sums first where asked
+    // for, then the codes of all blocks with no branch between them (c_out is
+    // a multiple of 64), so their independent dependency chains interleave
+    if (a.acc_dump) {
+#pragma unroll
+      for (int q = 0; q < FM * NB; ++q) {
+        const int fm = q / NB, fn = q % NB;
+        if constexpr (SW) {
+          const v16i sums[1] = {SC16 ? acc[fm][fn] >> 4 : acc[fm][fn]};
+          dump_acc_t<1>(a, sums, fm, h, l32, co0, p0, fn * 32, NB * 32, a.acc_dump);
+        } else {
+          const v16i one2[1][1] = {{SC16 ? acc[fm][fn] >> 4 : acc[fm][fn]}};
+          epilogue32<kE32I32, 1, 1>(a, lds + TBL, one2, fm, fn, h, l32, co0, p0, NB * 32, otile,
+                                    orow, a.acc_dump);
+        }
+      }
+    }
 #pragma unroll
     for (int q = 0; q < FM * NB; ++q) {
       const int fm = q / NB, fn = q % NB;
       const v16i one[1] = {acc[fm][fn]};
       if constexpr (SW) {
-        if (a.acc_dump) {
-          const v16i sums[1] = {SC16 ? acc[fm][fn] >> 4 : acc[fm][fn]};
-          dump_acc_t<1>(a, sums, fm, h, l32, co0, p0, fn * 32, NB * 32, a.acc_dump);
-        }
-        epilogue_thr_pk_t<1, SC16 ? 4 : 0>(a, reinterpret_cast<const int4*>(lds + TBL), one, fm,
-                                           h, l32, co0, fn * 32, otile, orow);
+        epilogue_thr_pk_t<1, SC16 ? 4 : 0, false>(a, reinterpret_cast<const int4*>(lds + TBL),
+                                                  one, fm, h, l32, co0, fn * 32, otile, orow);
       } else {
-        if (a.acc_dump) {
-          const v16i one2[1][1] = {{SC16 ? acc[fm][fn] >> 4 : acc[fm][fn]}};
-          epilogue32<kE32I32, 1, 1>(a, lds + TBL, one2, fm, fn, h, l32, co0, p0, NB * 32, otile,
-                                    orow, a.acc_dump);
-        }
         const int pl = fn * 32 + l32;
         const int cl = fm * 32;
         const uint2 sc[1] = {*reinterpret_cast<const uint2*>(
             lds + SCO + (p0 - P0 + pl) * 16 + (cl >> 2))};
-        epilogue_idj_pk<1>(a, lds + TBL, one, sc, fm, h, co0, pl, otile, orow);
+        epilogue_idj_pk<1, false>(a, lds + TBL, one, sc, fm, h, co0, pl, otile, orow);
       }
     }
     // the output tile's bytes (written by other lanes of this wave) are read

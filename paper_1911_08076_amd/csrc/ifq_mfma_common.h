@@ -341,7 +341,8 @@ __device__ __forceinline__ uint2 shortcut8(const ConvLaunch& a, int p, int co) {
 
 // Identity-join epilogue for 2-bit packed output from the records of
 // stage_idj_pk; sc[fm]: shortcut8 of the lane's pixel for block fm.
-template <int NB>
+// CK as for epilogue_thr_pk_t.
+template <int NB, bool CK = true>
 __device__ __forceinline__ void epilogue_idj_pk(const ConvLaunch& a, const uint8_t* lds,
                                                 const v16i (&acc)[NB], const uint2 (&sc)[NB],
                                                 int wm, int h, int co0, int pl,
@@ -349,7 +350,7 @@ __device__ __forceinline__ void epilogue_idj_pk(const ConvLaunch& a, const uint8
 #pragma unroll
   for (int fm = 0; fm < NB; ++fm) {
     const int cb = (wm * NB + fm) * 32;
-    if (co0 + cb >= a.cout) continue;
+    if (CK && co0 + cb >= a.cout) continue;
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
       const int cl = cb + 8 * b + 4 * h;
@@ -418,46 +419,86 @@ __device__ __forceinline__ uint32_t quad_or(uint32_t w) {
 
 __device__ __forceinline__ uint32_t pk2_i16(int v) { return ((uint32_t)v & 0xFFFFu) * 0x10001u; }
 
+// Code of two sums (int16 halves of p) against thresholds sorted ascending,
+// w1 <= w2 <= w3 (each an int16 pair): the count of thresholds below a sum
+// is the same in any order, and with sorted ones it is 2 [p > T2] plus
+// [p > T3] where p > T2, else [p > T1]. Saturating differences keep the sign.
+__device__ __forceinline__ uint32_t count3_sorted_pk(s16x2 p, uint32_t w1, uint32_t w2,
+                                                     uint32_t w3) {
+  const s16x2 d2 = __builtin_elementwise_sub_sat(__builtin_bit_cast(s16x2, w2), p);
+  uint32_t m = __builtin_bit_cast(uint32_t, d2 >> (short)15);   // 0xFFFF: p > T2
+  // opaque to the optimizer, which would otherwise turn the bit-field select
+  // below into compares and selects per half
+  asm("" : "+v"(m));
+  const uint32_t ts = (m & w3) | (~m & w1);
+  const s16x2 ds = __builtin_elementwise_sub_sat(__builtin_bit_cast(s16x2, ts), p);
+  const uint32_t lo = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, ds) >> (unsigned short)15);
+  return (m & 0x00020002u) | lo;
+}
+
 // Threshold epilogue (2-bit codes, c_out % 32 == 0, 27 * c_in <= 32766) from
 // the raw {s, T1, T2, T3} records of the tile's channels (recs[c - co0]),
 // with the same packed 16-bit compare and sign flip as epilogue_thr_pk.
 // SH > 0: the sums are 2^SH a (|2^SH a| < 2^15); the thresholds, clamped to
 // [-B-1, B] (B = 27 c_in bounds |a|, so no comparison changes), are scaled
 // the same way.
-template <int NB, int SH = 0>
+// Each lane holds one channel of a block; its 16 codes are gathered into one
+// word (byte k: pixels {0, 2, 1, 3}[k] of the four row groups, group g in
+// bits 2g), and a 4x4 transpose of 2-bit fields across the lane quad (two
+// exchanges with the lanes at xor 1 and xor 2, each a rotate and a bit-field
+// select) leaves lane t with the bytes of row group t: the four channels of
+// the quad for each of its pixels.
+// CK false: the caller guarantees every block's channels exist (no check,
+// so the blocks of one call site form one straight-line region).
+template <int NB, int SH = 0, bool CK = true>
 __device__ __forceinline__ void epilogue_thr_pk_t(const ConvLaunch& a, const int4* recs,
                                                   const v16i (&acc)[NB], int wm, int h,
                                                   int l32, int co0, int pl0, uint8_t* otile,
                                                   int orow) {
   const int t = l32 & 3;
-  const int bsel = ((t & 1) << 1) | (t >> 1);    // byte of pixel t in the merged word
+  const uint32_t r1 = (t & 1) ? 2u : 30u, r2 = (t & 2) ? 4u : 28u;
+  const uint32_t k1 = (t & 1) ? 0xCCCCCCCCu : 0x33333333u;
+  const uint32_t k2 = (t & 2) ? 0xF0F0F0F0u : 0x0F0F0F0Fu;
   const int bnd = 27 * a.cin;
   auto thr = [&](int v) {
     if constexpr (SH > 0) v = (v < -bnd - 1 ? -bnd - 1 : (v > bnd ? bnd : v)) * (1 << SH);
-    return pk2_i16(v);
+    return (int)(int16_t)v;    // compared as 16-bit halves
   };
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int cb = (wm * NB + j) * 32;
-    if (co0 + cb >= a.cout) continue;
+    if (CK && co0 + cb >= a.cout) continue;
     const int cl = cb + l32;
     const int4 r = recs[cl];
     const bool flip = r.x < 0;
-    const uint32_t w1 = thr(flip ? -r.y - 1 : r.y);
-    const uint32_t w2 = thr(flip ? -r.z - 1 : r.z);
-    const uint32_t w3 = thr(flip ? -r.w - 1 : r.w);
-    const uint32_t xm = flip ? 0x03030303u : 0u;
+    const int v1 = thr(flip ? -r.y - 1 : r.y);
+    const int v2 = thr(flip ? -r.z - 1 : r.z);
+    const int v3 = thr(flip ? -r.w - 1 : r.w);
+    const int tlo = min(v1, min(v2, v3)), thi = max(v1, max(v2, v3));
+    const int tmd = max(min(v1, v2), min(max(v1, v2), v3));
+    const uint32_t w1 = pk2_i16(tlo), w2 = pk2_i16(tmd), w3 = pk2_i16(thi);
+    uint32_t wd = 0;
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
       const s16x2 p01 = __builtin_amdgcn_cvt_pk_i16(acc[j][4 * b], acc[j][4 * b + 1]);
       const s16x2 p23 = __builtin_amdgcn_cvt_pk_i16(acc[j][4 * b + 2], acc[j][4 * b + 3]);
-      // codes of pixels 0 and 1 in the halves of c01, 2 and 3 in c23: the
-      // word's bytes are pixels 0, 2, 1, 3
-      const uint32_t c01 = count3_pk(p01, w1, w2, w3);
-      const uint32_t c23 = count3_pk(p23, w1, w2, w3);
-      const uint32_t w = quad_or(((c01 | (c23 << 8)) ^ xm) << (2 * t));
-      otile[(pl0 + 8 * b + 4 * h + t) * orow + (cl >> 2)] = (uint8_t)(w >> (8 * bsel));
+      const uint32_t c01 = count3_sorted_pk(p01, w1, w2, w3);
+      const uint32_t c23 = count3_sorted_pk(p23, w1, w2, w3);
+      wd |= (c01 | (c23 << 8)) << (2 * b);
     }
+    if (flip) wd = ~wd;
+    uint32_t q = (uint32_t)__builtin_amdgcn_mov_dpp((int)wd, 0xB1, 0xF, 0xF, true);
+    q = __builtin_rotateright32(q, r1);
+    wd = q ^ ((wd ^ q) & k1);
+    q = (uint32_t)__builtin_amdgcn_mov_dpp((int)wd, 0x4E, 0xF, 0xF, true);
+    q = __builtin_rotateright32(q, r2);
+    wd = q ^ ((wd ^ q) & k2);
+    uint8_t* o = otile + (pl0 + 8 * t + 4 * h) * orow + (cl >> 2);
+    const uint32_t w8 = wd >> 8;
+    o[0] = (uint8_t)wd;
+    o[orow] = (uint8_t)(wd >> 16);
+    o[2 * orow] = (uint8_t)w8;
+    o[3 * orow] = (uint8_t)(w8 >> 16);
   }
 }
 
