@@ -255,6 +255,23 @@ __device__ __forceinline__ uint32_t count3_pk(s16x2 p, uint32_t w1, uint32_t w2,
          __builtin_bit_cast(uint32_t, s3);
 }
 
+// Code of two sums (int16 halves of p) against thresholds sorted ascending,
+// w1 <= w2 <= w3 (each an int16 pair): the count of thresholds below a sum
+// is the same in any order, and with sorted ones it is 2 [p > T2] plus
+// [p > T3] where p > T2, else [p > T1]. Saturating differences keep the sign.
+__device__ __forceinline__ uint32_t count3_sorted_pk(s16x2 p, uint32_t w1, uint32_t w2,
+                                                     uint32_t w3) {
+  const s16x2 d2 = __builtin_elementwise_sub_sat(__builtin_bit_cast(s16x2, w2), p);
+  uint32_t m = __builtin_bit_cast(uint32_t, d2 >> (short)15);   // 0xFFFF: p > T2
+  // opaque to the optimizer, which would otherwise turn the bit-field select
+  // below into compares and selects per half
+  asm("" : "+v"(m));
+  const uint32_t ts = (m & w3) | (~m & w1);
+  const s16x2 ds = __builtin_elementwise_sub_sat(__builtin_bit_cast(s16x2, ts), p);
+  const uint32_t lo = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, ds) >> (unsigned short)15);
+  return (m & 0x00020002u) | lo;
+}
+
 // Threshold epilogue for 2-bit packed output from the records of
 // stage_thr_pk: per lane, accumulator blocks fm of rows (wm*NB + fm)*32 and
 // the pixel column pl of the output tile. Each group of four channels of a
@@ -309,12 +326,19 @@ __device__ __forceinline__ void stage_idj_pk(const int32_t* tbl, uint8_t* lds, i
       if (c < nch) r = *reinterpret_cast<const int4*>(tbl + (c * 4 + x[j]) * 4);
       const bool flip = r.x < 0;
       const int t[3] = {r.y, r.z, r.w};
+      int v[3];
 #pragma unroll
       for (int k = 0; k < 3; ++k) {
-        int v = flip ? -t[k] - 1 : t[k];
-        if (sh > 0) v = (v < -bnd - 1 ? -bnd - 1 : (v > bnd ? bnd : v)) * (1 << sh);
-        w[k] |= ((uint32_t)v & 0xFFFFu) << (16 * j);
+        v[k] = flip ? -t[k] - 1 : t[k];
+        if (sh > 0) v[k] = (v[k] < -bnd - 1 ? -bnd - 1 : (v[k] > bnd ? bnd : v[k])) * (1 << sh);
+        v[k] = (int16_t)v[k];     // compared as 16-bit halves
       }
+      // sorted ascending for count3_sorted_pk (the count is order-free)
+      const int lo = min(v[0], min(v[1], v[2])), hi = max(v[0], max(v[1], v[2]));
+      const int md = max(min(v[0], v[1]), min(max(v[0], v[1]), v[2]));
+      w[0] |= ((uint32_t)lo & 0xFFFFu) << (16 * j);
+      w[1] |= ((uint32_t)md & 0xFFFFu) << (16 * j);
+      w[2] |= ((uint32_t)hi & 0xFFFFu) << (16 * j);
       if (flip) w[3] |= 3u << (16 * j);
     }
     *reinterpret_cast<uint4*>(lds + gq * kIdjGroupBytes + pr * 256 + combo * 16) =
@@ -361,8 +385,8 @@ __device__ __forceinline__ void epilogue_idj_pk(const ConvLaunch& a, const uint8
       const uint4 e23 = *reinterpret_cast<const uint4*>(g + 256 + ((xs >> 4) & 15u) * 16);
       const s16x2 p01 = __builtin_amdgcn_cvt_pk_i16(acc[fm][4 * b], acc[fm][4 * b + 1]);
       const s16x2 p23 = __builtin_amdgcn_cvt_pk_i16(acc[fm][4 * b + 2], acc[fm][4 * b + 3]);
-      const uint32_t c01 = count3_pk(p01, e01.x, e01.y, e01.z) ^ e01.w;
-      const uint32_t c23 = count3_pk(p23, e23.x, e23.y, e23.z) ^ e23.w;
+      const uint32_t c01 = count3_sorted_pk(p01, e01.x, e01.y, e01.z) ^ e01.w;
+      const uint32_t c23 = count3_sorted_pk(p23, e23.x, e23.y, e23.z) ^ e23.w;
       const uint32_t t = c01 | (c23 << 4);
       otile[pl * orow + (cl >> 2)] = (uint8_t)(t | (t >> 14));
     }
@@ -418,23 +442,6 @@ __device__ __forceinline__ uint32_t quad_or(uint32_t w) {
 }
 
 __device__ __forceinline__ uint32_t pk2_i16(int v) { return ((uint32_t)v & 0xFFFFu) * 0x10001u; }
-
-// Code of two sums (int16 halves of p) against thresholds sorted ascending,
-// w1 <= w2 <= w3 (each an int16 pair): the count of thresholds below a sum
-// is the same in any order, and with sorted ones it is 2 [p > T2] plus
-// [p > T3] where p > T2, else [p > T1]. Saturating differences keep the sign.
-__device__ __forceinline__ uint32_t count3_sorted_pk(s16x2 p, uint32_t w1, uint32_t w2,
-                                                     uint32_t w3) {
-  const s16x2 d2 = __builtin_elementwise_sub_sat(__builtin_bit_cast(s16x2, w2), p);
-  uint32_t m = __builtin_bit_cast(uint32_t, d2 >> (short)15);   // 0xFFFF: p > T2
-  // opaque to the optimizer, which would otherwise turn the bit-field select
-  // below into compares and selects per half
-  asm("" : "+v"(m));
-  const uint32_t ts = (m & w3) | (~m & w1);
-  const s16x2 ds = __builtin_elementwise_sub_sat(__builtin_bit_cast(s16x2, ts), p);
-  const uint32_t lo = __builtin_bit_cast(uint32_t, __builtin_bit_cast(u16x2, ds) >> (unsigned short)15);
-  return (m & 0x00020002u) | lo;
-}
 
 // Threshold epilogue (2-bit codes, c_out % 32 == 0, 27 * c_in <= 32766) from
 // the raw {s, T1, T2, T3} records of the tile's channels (recs[c - co0]),
