@@ -89,8 +89,8 @@ def kernel_peak(name):
         fp4 = name[len("conv_w2<"):-1].split(", ")[8] == "true"
     elif name.startswith("conv_wp<"):
         fp4 = name[len("conv_wp<"):-1].split(", ")[4] == "true"
-    elif name.startswith("conv_wv<"):
-        fp4 = name[len("conv_wv<"):-1].split(", ")[1] == "true"
+    elif name.startswith(("conv_wv<", "conv_wvh<")):
+        fp4 = name[name.index("<") + 1:-1].split(", ")[1] == "true"
     return PEAK_FP4_TFLOPS if fp4 else PEAK_INT8_TOPS
 
 

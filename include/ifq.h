@@ -424,7 +424,8 @@ IFQ_API const char* ifq_conv_kernel_name(const ifq_conv_desc* d, const ifq_join*
  * channels in LDS and runs a range of pixel tiles) and conv_wv (persistent
  * with the weights in LDS too, but each wave runs its own range of pixels
  * with its own input windows and no barrier after the prologue; c_out %
- * 64 == 0). All take 3x3 pad-1 convs of stride 1 or 2 on 2-bit BLOCK64
+ * 64 == 0; conv_wvh the same with 32 output channels per workgroup, for
+ * weights of up to 256 input channels in its slab). All take 3x3 pad-1 convs of stride 1 or 2 on 2-bit BLOCK64
  * codes with c_in % 64 == 0, 2-bit output (U2 or BLOCK64, c_out % 32 == 0,
  * 27 * c_in <= 32766), no pool, and thresholds or an identity join with a
  * 2-bit shortcut (c_out % 64 == 0); conv_w2 also a join with a fused 1x1

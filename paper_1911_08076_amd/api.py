@@ -324,10 +324,10 @@ def ifq_conv_variant_fp4(variant):
 def kernel_is_fp4(name):
     """Whether a kernel name (as ifq_conv_kernel_name returns it) is an fp4
     instance: the fp4 flag true (the windowed kernel's last template
-    argument, conv_w2's ninth, conv_wp's fifth, conv_wv's second)."""
+    argument, conv_w2's ninth, conv_wp's fifth, conv_wv's and conv_wvh's second)."""
     if name.startswith("conv_halo<"):
         return name.endswith(", true>")
-    for kern, pos in (("conv_w2<", 8), ("conv_wp<", 4), ("conv_wv<", 1)):
+    for kern, pos in (("conv_w2<", 8), ("conv_wp<", 4), ("conv_wv<", 1), ("conv_wvh<", 1)):
         if name.startswith(kern):
             return name[len(kern):-1].split(", ")[pos] == "true"
     return False

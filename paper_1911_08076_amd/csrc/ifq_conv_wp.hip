@@ -420,11 +420,14 @@ __global__ __launch_bounds__(64 * WN, (WN / 4) * OCC) void conv_wp(ConvLaunch a)
 // as units of 64 pixels x the 64-channel slice and, where its count is odd,
 // one last unit of 32 pixels (half the MFMAs). So the two waves of a SIMD
 // carry nearly the same work and neither runs long alone.
-template <int MODE, bool F4, int WGTB, int WINB>
-__global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
+// FMT row blocks of 32 channels per workgroup: 2 (conv_wv, a 64-channel
+// slice) or 1 (conv_wvh, half of one 64-channel cell of the output, for
+// layers whose 64-channel slice of weights does not fit the slab).
+template <int MODE, bool F4, int WGTB, int WINB, int FMT>
+__device__ __forceinline__ void conv_wv_body(const ConvLaunch& a) {
   constexpr bool SW = MODE == 0;                 // transposed sums
-  constexpr int NW = 8, FM = 2, FN = 2;
-  constexpr int BM = 64, UN = 64, HU = 32;       // unit: 64 channels x 64 pixels
+  constexpr int NW = 8, FM = FMT, FN = 2;
+  constexpr int BM = 32 * FM, UN = 64, HU = 32;  // unit: BM channels x 64 pixels
   constexpr int KH = F4 ? 1 : 2;
   constexpr int RB = FM;
   static_assert(WGTB % 1024 == 0, "weight chunks");
@@ -441,7 +444,8 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
   // window (per channel block its cells and a zero cell) and shortcut cells.
   constexpr int WGT = 0;
   constexpr int TBL = WGTB;
-  constexpr int TBL_BYTES = SW ? BM * 16 : (BM / 4) * kIdjGroupBytes;
+  // (threshold records: one 64-lane load, 1 KB, whatever BM)
+  constexpr int TBL_BYTES = SW ? (BM * 16 > 1024 ? BM * 16 : 1024) : (BM / 4) * kIdjGroupBytes;
   constexpr int OUT = TBL + TBL_BYTES;
   constexpr int OUT_BYTES = UN * BM / 4;
   static_assert(SW || NW * OUT_BYTES >= BM * 64, "raw join records in the output tiles");
@@ -516,26 +520,29 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
           const int nimg = fdiv(p, a.div_howo);
           src = sc8 + (((int64_t)nimg * (a.cout >> 6) + (co0 >> 6)) * howo + (p - nimg * howo)) * 16;
         } else {
-          src = sc8 + ((int64_t)p * a.cout + co0) / 4;
+          src = sc8 + ((int64_t)p * a.cout + (co0 & ~63)) / 4;
         }
       }
       dma16(src, lds0 + SCO + (uint32_t)(q * 1024));
     }
   };
-  // this wave's output tile (npx pixels from p0) to HBM: lane = pixel
+  // this wave's output tile (npx pixels from p0) to HBM: lane = pixel, BM / 4
+  // bytes (of a 64-channel cell: from byte (co0 % 64) / 4)
   auto store_unit = [&](int p0, int npx) {
     const int p = p0 + lane;
-    const uint4 v = *reinterpret_cast<const uint4*>(otile + lane * 16);
+    using Row = std::conditional_t<BM == 64, uint4, uint2>;
+    const Row v = *reinterpret_cast<const Row*>(otile + lane * orow);
     if (lane < npx && p < a.m) {
       uint8_t* y8 = reinterpret_cast<uint8_t*>(a.y);
       int64_t off;
       if (a.out_layout == IFQ_LAYOUT_U2_BLOCK64) {
         const int nimg = fdiv(p, a.div_howo);
-        off = (((int64_t)nimg * (a.cout >> 6) + (co0 >> 6)) * howo + (p - nimg * howo)) * 16;
+        off = (((int64_t)nimg * (a.cout >> 6) + (co0 >> 6)) * howo + (p - nimg * howo)) * 16 +
+              ((co0 & 63) >> 2);
       } else {
         off = ((int64_t)p * a.cout + co0) / 4;
       }
-      *reinterpret_cast<uint4*>(y8 + off) = v;
+      *reinterpret_cast<Row*>(y8 + off) = v;
     }
   };
 
@@ -811,7 +818,7 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
         const int pl = fn * 32 + l32;
         const int cl = fm * 32;
         const uint2 sc[1] = {*reinterpret_cast<const uint2*>(
-            lds + SCO + (p0 - P0 + pl) * 16 + (cl >> 2))};
+            lds + SCO + (p0 - P0 + pl) * 16 + ((co0 & 63) >> 2) + (cl >> 2))};
         epilogue_idj_pk<1, false>(a, lds + TBL, one, sc, fm, h, co0, pl, otile, orow);
       }
     }
@@ -830,6 +837,16 @@ __global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
     store_unit(c * HU, len * HU);
     c += len;
   }
+}
+
+template <int MODE, bool F4, int WGTB, int WINB>
+__global__ __launch_bounds__(512, 1) void conv_wv(ConvLaunch a) {
+  conv_wv_body<MODE, F4, WGTB, WINB, 2>(a);
+}
+
+template <int MODE, bool F4, int WGTB, int WINB>
+__global__ __launch_bounds__(512, 1) void conv_wvh(ConvLaunch a) {
+  conv_wv_body<MODE, F4, WGTB, WINB, 1>(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -874,29 +891,39 @@ constexpr int kNumWpBlock = sizeof(kWpVariants) / sizeof(kWpVariants[0]);
 // per-channel-block cost, with two waves sharing each SIMD.
 struct WvVariant {
   bool f4;
+  int fm;                   // row blocks of 32 channels per workgroup (2: conv_wv, 1: conv_wvh)
   int wgtb;                 // weight slab bytes
   int winb_thr, winb_idj;   // window bytes of a workgroup
   double pro_us, c_unit_us, c_blk_us, idj_us;
   const char* thr_name;
   const char* idj_name;
 };
-#define IFQ_WV_NAME(mode, f4, wgtb, winb) \
-  "conv_wv<" #mode ", " #f4 ", " #wgtb ", " #winb ">"
+#define IFQ_WV_NAME(kern, mode, f4, wgtb, winb) \
+  #kern "<" #mode ", " #f4 ", " #wgtb ", " #winb ">"
 // The identity join's shortcut cells take the LDS past its window: 160 KB
-// less the weights, packed records, output tiles and window.
+// less the weights, packed records (BM / 4 groups of 512 B), output tiles
+// (eight of 64 pixels x BM / 4 bytes) and window.
 constexpr int kWvLds = 160 * 1024;
-constexpr int kWvFixedIdj = 16 * 512 + 8 * 1024;   // plus the weights
+constexpr int wv_fixed_idj(int bm) { return (bm / 4) * 512 + 8 * 64 * (bm / 4); }
 // Index order must match the switch in launch_conv_wp. Weight slabs of
-// 36 KB (int8: one channel block; fp4: two) or 72 KB (int8: two; fp4: four).
+// 36 KB (int8: one channel block; fp4: two) or 72 KB (int8: two; fp4: four)
+// for a 64-channel slice; the 32-channel instance's 72 KB slab holds four
+// int8 channel blocks (c_in 256). Its window sizes fill the LDS left by its
+// smaller records and output tiles; it takes stride 1 only (at stride 2 each
+// of twice as many channel slices re-reads a window of the same pixels: the
+// ResNet-18 l4.0.conv1 shape measured 14.3 us against 12.1 on conv_w2).
+// Coefficients fitted to six measured stride-1 shapes (within about 7%).
 const WvVariant kWvVariants[] = {
-    {false, 36864, 114688, 77824, 2.86, 0.8, 1.0, 0.4,
-     IFQ_WV_NAME(0, false, 36864, 114688), IFQ_WV_NAME(1, false, 36864, 77824)},
-    {true, 36864, 114688, 77824, 2.0, 0.8, 0.62, 0.53,
-     IFQ_WV_NAME(0, true, 36864, 114688), IFQ_WV_NAME(1, true, 36864, 77824)},
-    {false, 73728, 80896, 49152, 2.58, 0.45, 1.28, 0.37,
-     IFQ_WV_NAME(0, false, 73728, 80896), IFQ_WV_NAME(1, false, 73728, 49152)},
-    {true, 73728, 80896, 49152, 1.73, 0.83, 0.69, 0.6,
-     IFQ_WV_NAME(0, true, 73728, 80896), IFQ_WV_NAME(1, true, 73728, 49152)},
+    {false, 2, 36864, 114688, 77824, 2.86, 0.8, 1.0, 0.4,
+     IFQ_WV_NAME(conv_wv, 0, false, 36864, 114688), IFQ_WV_NAME(conv_wv, 1, false, 36864, 77824)},
+    {true, 2, 36864, 114688, 77824, 2.0, 0.8, 0.62, 0.53,
+     IFQ_WV_NAME(conv_wv, 0, true, 36864, 114688), IFQ_WV_NAME(conv_wv, 1, true, 36864, 77824)},
+    {false, 2, 73728, 80896, 49152, 2.58, 0.45, 1.28, 0.37,
+     IFQ_WV_NAME(conv_wv, 0, false, 73728, 80896), IFQ_WV_NAME(conv_wv, 1, false, 73728, 49152)},
+    {true, 2, 73728, 80896, 49152, 1.73, 0.83, 0.69, 0.6,
+     IFQ_WV_NAME(conv_wv, 0, true, 73728, 80896), IFQ_WV_NAME(conv_wv, 1, true, 73728, 49152)},
+    {false, 1, 73728, 84992, 57344, 1.25, 0.36, 0.86, 0.37,
+     IFQ_WV_NAME(conv_wvh, 0, false, 73728, 84992), IFQ_WV_NAME(conv_wvh, 1, false, 73728, 57344)},
 };
 constexpr int kNumWv = sizeof(kWvVariants) / sizeof(kWvVariants[0]);
 constexpr int kNumWp = kNumWpBlock + kNumWv;
@@ -948,11 +975,16 @@ bool wv_fit(const ConvLaunch& a, int v, WpPlan* out) {
   if (V.f4 != (a.f4 != 0) || a.cout % 64 != 0) return false;
   const int G = a.cin / 64;
   const int kh = V.f4 ? 1 : 2;
-  if ((int64_t)G * kWpTaps * 2 * kh * 1024 > V.wgtb) return false;
+  const int bm = 32 * V.fm;
+  if ((int64_t)G * kWpTaps * V.fm * kh * 1024 > V.wgtb) return false;
+  // the 32-channel instance only where no 64-channel slab holds the weights
+  // (it measured slower than conv_wv on the 64- and 128-channel layers)
+  if (V.fm == 1 && (a.stride != 1 || (int64_t)G * kWpTaps * 2 * kh * 1024 <= 73728))
+    return false;
   const bool idj = a.join_kind == IFQ_JOIN_IDENTITY;
   const int64_t winb = idj ? V.winb_idj : V.winb_thr;
-  const int64_t scb = idj ? kWvLds - kWvFixedIdj - V.wgtb - winb : 0;
-  const int64_t nco = a.cout / 64;
+  const int64_t scb = idj ? kWvLds - wv_fixed_idj(bm) - V.wgtb - winb : 0;
+  const int64_t nco = a.cout / bm;
   const int64_t hu = kWvUnit / 2;
   const int64_t nhu = (a.m + hu - 1) / hu;                      // half units
   int64_t gx = kPlanCUs / nco;
@@ -1044,21 +1076,22 @@ hipError_t launch_conv_wp(ConvLaunch a, const WpPlan& p, hipStream_t stream) {
   a.wcells = p.wcells;
   a.tiles_wg = p.per;
   if (p.variant >= kNumWpBlock) {
-    const dim3 grid(p.gx, a.cout / 64);
+    const dim3 grid(p.gx, a.cout / (32 * kWvVariants[p.variant - kNumWpBlock].fm));
     const dim3 block(64 * kWvWaves);
     const int mode = a.join_kind == IFQ_JOIN_IDENTITY ? 1 : 0;
     switch ((p.variant - kNumWpBlock) * 2 + mode) {
-#define IFQ_WV_CASE(k, f4, wgtb, winbt, winbi)                                             \
+#define IFQ_WV_CASE(k, kern, f4, wgtb, winbt, winbi)                                       \
   case 2 * k:                                                                              \
-    hipLaunchKernelGGL((conv_wv<0, f4, wgtb, winbt>), grid, block, 0, stream, a);          \
+    hipLaunchKernelGGL((kern<0, f4, wgtb, winbt>), grid, block, 0, stream, a);             \
     break;                                                                                 \
   case 2 * k + 1:                                                                          \
-    hipLaunchKernelGGL((conv_wv<1, f4, wgtb, winbi>), grid, block, 0, stream, a);          \
+    hipLaunchKernelGGL((kern<1, f4, wgtb, winbi>), grid, block, 0, stream, a);             \
     break;
-      IFQ_WV_CASE(0, false, 36864, 114688, 77824)
-      IFQ_WV_CASE(1, true, 36864, 114688, 77824)
-      IFQ_WV_CASE(2, false, 73728, 80896, 49152)
-      IFQ_WV_CASE(3, true, 73728, 80896, 49152)
+      IFQ_WV_CASE(0, conv_wv, false, 36864, 114688, 77824)
+      IFQ_WV_CASE(1, conv_wv, true, 36864, 114688, 77824)
+      IFQ_WV_CASE(2, conv_wv, false, 73728, 80896, 49152)
+      IFQ_WV_CASE(3, conv_wv, true, 73728, 80896, 49152)
+      IFQ_WV_CASE(4, conv_wvh, false, 73728, 84992, 57344)
 #undef IFQ_WV_CASE
       default: return hipErrorInvalidValue;
     }

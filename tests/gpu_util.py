@@ -136,7 +136,7 @@ def gpu_layer(P, L, n, x, p, in_layout=I8, out_layout=None, shortcut=None,
         P.ifq_conv_forward(d, xd, wd, td, y, join=join, acc_dump=acc, ws=ws)
     else:
         name = P.ifq_conv_variant_name(d, join, variant)
-        assert name.startswith(("conv_w2<", "conv_wp<", "conv_wv<")), (variant, name)
+        assert name.startswith(("conv_w2<", "conv_wp<", "conv_wv<", "conv_wvh<")), (variant, name)
         assert P.kernel_is_fp4(name) == fp4, (variant, name)
         print("variant %d: %s n=%d %dx%dx%d -> %d s%d" % (variant, name, n, L.h, L.w, L.cin,
                                                           L.cout, L.stride), flush=True)

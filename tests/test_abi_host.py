@@ -726,7 +726,7 @@ def test_fp4_entry_points_host_side():
     # argument, the windowed kernel's last)
     d = P.conv_desc(2, 28, 28, 128, 128, 3, 1, 1, 2, 2, B64, B64)
     name = P.ifq_conv_fp4_kernel_name(d)
-    assert name.startswith(("conv_w2<", "conv_wp<", "conv_wv<")) and P.kernel_is_fp4(name), name
+    assert name.startswith(("conv_w2<", "conv_wp<", "conv_wv<", "conv_wvh<")) and P.kernel_is_fp4(name), name
     k = 9 * 128
     assert P._ffi.load().ifq_packed_weight_bytes_fp4(ctypes.byref(d)) == (128 // 32) * (k // 64) * 1024 + 1024
     w = np.ones((128, 128, 3, 3), dtype=np.int8)

@@ -23,6 +23,7 @@ def test_fp4_kernels_priced_against_the_fp4_peak():
         bench.PEAK_FP4_TFLOPS
     assert bench.kernel_peak("conv_wv<0, true, 36864, 114688>") == bench.PEAK_FP4_TFLOPS
     assert bench.kernel_peak("conv_wv<1, false, 36864, 77824>") == bench.PEAK_INT8_TOPS
+    assert bench.kernel_peak("conv_wvh<0, false, 73728, 84992>") == bench.PEAK_INT8_TOPS
     for int8 in ("conv_w2<2, 4, 1, 2, 2, 3, 3, 0, false, 1, 49152>",
                  "conv_wp<4, 2, 2, 1, false, 2, 36864, 10240>",
                  "conv_w2<1, 4, 1, 2, 2, 3, 3, 1, false, 2, 20480>",

@@ -249,10 +249,11 @@ def test_conv_block64_bit_exact(P, case, io):
 # (the 3x3 kernels' tiles of 256, 128 and 64 output pixels, stride-2 layers),
 # at batches the oracle finishes in about a second; the test also pins which
 # kernel variant the planner takes for each (conv_w2, whose eighth template
-# argument is its epilogue, 0 thresholds; or the wave-independent conv_wv).
+# argument is its epilogue, 0 thresholds; or the wave-independent conv_wv and
+# its 32-channel form conv_wvh).
 HALO_TILES = [
     ("halo_l2_b83", 83, 28, 28, 128, 128, 1, "conv_wv<0, false, 73728, 80896>"),
-    ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_w2<1, 4, 2, 2, 2, 3, 2, 0, false, 1, 53248>"),
+    ("halo_l3_b83", 83, 14, 14, 256, 256, 1, "conv_wvh<0, false, 73728, 84992>"),
     ("halo_l4_b83", 83, 7, 7, 512, 512, 1, "conv_w2<1, 2, 4, 2, 2, 3, 2, 0, false, 1, 36864>"),
     ("halo_s2_b40", 40, 28, 28, 128, 256, 2, "conv_wv<0, false, 73728, 80896>"),
     ("halo_l1_b24", 24, 56, 56, 64, 64, 1, "conv_wv<0, false, 73728, 80896>"),
@@ -339,7 +340,7 @@ def test_identity_join_64_channel_variant(P):
     vs = [v for v in range(P.ifq_conv_variant_count())
           if P.ifq_conv_variant_name(d, jn, v) == name]
     assert vs, name
-    assert P.ifq_conv_kernel_name(d, jn).startswith(("conv_w2<", "conv_wp<", "conv_wv<"))
+    assert P.ifq_conv_kernel_name(d, jn).startswith(("conv_w2<", "conv_wp<", "conv_wv<", "conv_wvh<"))
     L = make_layer("join_id", h, h, c, c, 3, 1, 1, join=("identity", "s"))
     p = params_for(41, L)
     x = codes_for(41, (n, h, h, c), 2)

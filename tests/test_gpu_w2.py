@@ -55,7 +55,7 @@ FULL = [
 ]
 
 
-NVAR = 16   # conv_w2's ten, then conv_wp's two and conv_wv's four
+NVAR = 17   # conv_w2's ten, then conv_wp's two, conv_wv's four and conv_wvh's one
 NW2 = 10    # conv_w2's variants
 
 
@@ -155,19 +155,26 @@ def test_variant_u2_output(P):
 def test_wave_kernel_nhwc_packed_layouts(P, variant, join):
     # the wave-independent kernel's own stores and shortcut loads in the NHWC
     # packed layout (output, and the identity join's shortcut), on a ragged
-    # multi-image layer
-    name, n, h, w, cin, cout, st = ("r17x23_64_64", 3, 17, 23, 64, 64, 1)
+    # multi-image layer: 64 channels, or 256 for the 32-channel instance
+    # (which writes and reads half of each 64-channel cell)
+    for case in (("r17x23_64_64", 3, 17, 23, 64, 64, 1), ("r9x13_256_256", 3, 9, 13, 256, 256, 1)):
+        name, n, h, w, cin, cout, st = case
+        d = P.conv_desc(n, h, w, cin, cout, 3, st, 1, 2, 2, B64, U2)
+        jn = _thr_join(P, join)
+        if jn is not None:
+            jn.layout = U2
+        if P.ifq_conv_variant_name(d, jn, variant):
+            break
     L = make_layer(name, h, w, cin, cout, 3, st, 1, 2, 2, ("identity", "x") if join else None)
     seed = zlib.crc32((name + "u2" + str(join)).encode()) % 997
     p = params_for(seed, L)
     x = codes_for(seed, (n, h, w, cin), 2)
     sc = codes_for(seed + 1, (n, h, w, cin), 2) if join else None
-    d = P.conv_desc(n, h, w, cin, cout, 3, st, 1, 2, 2, B64, U2)
     jn = _thr_join(P, join, p["q_thr"])
     if jn is not None:
         jn.layout = U2
     name_v = P.ifq_conv_variant_name(d, jn, variant)
-    assert name_v.startswith("conv_wv<"), name_v
+    assert name_v.startswith(("conv_wv<", "conv_wvh<")), name_v
     want_acc, want = oracle_layer(L, x, p, shortcut=sc)
     acc, got = gpu_layer(P, L, n, x, p, in_layout=B64, out_layout=U2, shortcut=sc,
                          sc_layout=U2, variant=variant)
