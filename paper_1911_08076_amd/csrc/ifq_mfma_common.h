@@ -517,6 +517,11 @@ __device__ __forceinline__ void epilogue_cjoin_t(const ConvLaunch& a, const uint
                                                  int wm, int h, int l32, int co0, int pl0,
                                                  uint8_t* otile, int orow) {
   const double q1 = a.qthr[0], q2 = a.qthr[1], q3 = a.qthr[2];
+  // the three thresholds sorted (the count #{i : z > q_i} is order-free):
+  // then the code is 2 [z > mid] + [z > (z > mid ? high : low)], two fp64
+  // compares per output instead of three, the same count for every z
+  const double qlo = fmin(q1, fmin(q2, q3)), qhi = fmax(q1, fmax(q2, q3));
+  const double qmd = fmax(fmin(q1, q2), fmin(fmax(q1, q2), q3));
   const double* cf = reinterpret_cast<const double*>(lds + kJoinCoefOff);
   const int t = l32 & 3;
 #pragma unroll
@@ -531,7 +536,8 @@ __device__ __forceinline__ void epilogue_cjoin_t(const ConvLaunch& a, const uint
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const double z = fma(p, (double)acc[j][4 * b + i], fma(q, (double)accd[j][4 * b + i], cc));
-        const uint32_t code = (uint32_t)(z > q1) + (uint32_t)(z > q2) + (uint32_t)(z > q3);
+        const bool up = z > qmd;
+        const uint32_t code = 2u * (uint32_t)up + (uint32_t)(z > (up ? qhi : qlo));
         w |= code << (8 * i);
       }
       w = quad_or(w << (2 * t));
