@@ -610,6 +610,16 @@ __device__ __forceinline__ void conv_wv_body(const ConvLaunch& a) {
     __syncthreads();
   }
 
+  // the threshold epilogue's packed thresholds of the lane's channel in each
+  // row block: the same for every unit, so taken once
+  ThrPk thp[SW ? FM : 1];
+  if constexpr (SW) {
+#pragma unroll
+    for (int fm = 0; fm < FM; ++fm)
+      thp[fm] = thr_pk_of<SC16 ? 4 : 0>(reinterpret_cast<const int4*>(lds + TBL)[fm * 32 + l32],
+                                        27 * a.cin);
+  }
+
   struct Unp {
     v4i b4[F4 ? 1 : 2][FN];
     v8i b8[F4 ? FN : 1];
@@ -812,8 +822,7 @@ __device__ __forceinline__ void conv_wv_body(const ConvLaunch& a) {
       const int fm = q / NB, fn = q % NB;
       const v16i one[1] = {acc[fm][fn]};
       if constexpr (SW) {
-        epilogue_thr_pk_t<1, SC16 ? 4 : 0, false>(a, reinterpret_cast<const int4*>(lds + TBL),
-                                                  one, fm, h, l32, co0, fn * 32, otile, orow);
+        epilogue_thr_pk_block(one[0], thp[fm], h, l32, fm * 32 + l32, fn * 32, otile, orow);
       } else {
         const int pl = fn * 32 + l32;
         const int cl = fm * 32;

@@ -443,6 +443,61 @@ __device__ __forceinline__ uint32_t quad_or(uint32_t w) {
 
 __device__ __forceinline__ uint32_t pk2_i16(int v) { return ((uint32_t)v & 0xFFFFu) * 0x10001u; }
 
+// The packed thresholds of one channel for the transposed epilogue: the
+// record's three thresholds (sign rule applied, clamped and scaled by 2^SH
+// where SH > 0), sorted ascending as int16 pairs, and its flip.
+struct ThrPk {
+  uint32_t w1, w2, w3;
+  bool flip;
+};
+template <int SH>
+__device__ __forceinline__ ThrPk thr_pk_of(const int4 r, int bnd) {
+  const bool flip = r.x < 0;
+  auto thr = [&](int v) {
+    if constexpr (SH > 0) v = (v < -bnd - 1 ? -bnd - 1 : (v > bnd ? bnd : v)) * (1 << SH);
+    return (int)(int16_t)v;    // compared as 16-bit halves
+  };
+  const int v1 = thr(flip ? -r.y - 1 : r.y);
+  const int v2 = thr(flip ? -r.z - 1 : r.z);
+  const int v3 = thr(flip ? -r.w - 1 : r.w);
+  const int tlo = min(v1, min(v2, v3)), thi = max(v1, max(v2, v3));
+  const int tmd = max(min(v1, v2), min(max(v1, v2), v3));
+  return ThrPk{pk2_i16(tlo), pk2_i16(tmd), pk2_i16(thi), flip};
+}
+
+// One 32x32 block of the transposed threshold epilogue, for the lane's
+// channel cl (thresholds th) and pixel rows pl0 + 0..31.
+__device__ __forceinline__ void epilogue_thr_pk_block(const v16i& acc, const ThrPk& th, int h,
+                                                      int l32, int cl, int pl0, uint8_t* otile,
+                                                      int orow) {
+  const int t = l32 & 3;
+  const uint32_t r1 = (t & 1) ? 2u : 30u, r2 = (t & 2) ? 4u : 28u;
+  const uint32_t k1 = (t & 1) ? 0xCCCCCCCCu : 0x33333333u;
+  const uint32_t k2 = (t & 2) ? 0xF0F0F0F0u : 0x0F0F0F0Fu;
+  uint32_t wd = 0;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const s16x2 p01 = __builtin_amdgcn_cvt_pk_i16(acc[4 * b], acc[4 * b + 1]);
+    const s16x2 p23 = __builtin_amdgcn_cvt_pk_i16(acc[4 * b + 2], acc[4 * b + 3]);
+    const uint32_t c01 = count3_sorted_pk(p01, th.w1, th.w2, th.w3);
+    const uint32_t c23 = count3_sorted_pk(p23, th.w1, th.w2, th.w3);
+    wd |= (c01 | (c23 << 8)) << (2 * b);
+  }
+  if (th.flip) wd = ~wd;
+  uint32_t q = (uint32_t)__builtin_amdgcn_mov_dpp((int)wd, 0xB1, 0xF, 0xF, true);
+  q = __builtin_rotateright32(q, r1);
+  wd = q ^ ((wd ^ q) & k1);
+  q = (uint32_t)__builtin_amdgcn_mov_dpp((int)wd, 0x4E, 0xF, 0xF, true);
+  q = __builtin_rotateright32(q, r2);
+  wd = q ^ ((wd ^ q) & k2);
+  uint8_t* o = otile + (pl0 + 8 * t + 4 * h) * orow + (cl >> 2);
+  const uint32_t w8 = wd >> 8;
+  o[0] = (uint8_t)wd;
+  o[orow] = (uint8_t)(wd >> 16);
+  o[2 * orow] = (uint8_t)w8;
+  o[3 * orow] = (uint8_t)(w8 >> 16);
+}
+
 // Threshold epilogue (2-bit codes, c_out % 32 == 0, 27 * c_in <= 32766) from
 // the raw {s, T1, T2, T3} records of the tile's channels (recs[c - co0]),
 // with the same packed 16-bit compare and sign flip as epilogue_thr_pk.
@@ -462,50 +517,13 @@ __device__ __forceinline__ void epilogue_thr_pk_t(const ConvLaunch& a, const int
                                                   const v16i (&acc)[NB], int wm, int h,
                                                   int l32, int co0, int pl0, uint8_t* otile,
                                                   int orow) {
-  const int t = l32 & 3;
-  const uint32_t r1 = (t & 1) ? 2u : 30u, r2 = (t & 2) ? 4u : 28u;
-  const uint32_t k1 = (t & 1) ? 0xCCCCCCCCu : 0x33333333u;
-  const uint32_t k2 = (t & 2) ? 0xF0F0F0F0u : 0x0F0F0F0Fu;
   const int bnd = 27 * a.cin;
-  auto thr = [&](int v) {
-    if constexpr (SH > 0) v = (v < -bnd - 1 ? -bnd - 1 : (v > bnd ? bnd : v)) * (1 << SH);
-    return (int)(int16_t)v;    // compared as 16-bit halves
-  };
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int cb = (wm * NB + j) * 32;
     if (CK && co0 + cb >= a.cout) continue;
     const int cl = cb + l32;
-    const int4 r = recs[cl];
-    const bool flip = r.x < 0;
-    const int v1 = thr(flip ? -r.y - 1 : r.y);
-    const int v2 = thr(flip ? -r.z - 1 : r.z);
-    const int v3 = thr(flip ? -r.w - 1 : r.w);
-    const int tlo = min(v1, min(v2, v3)), thi = max(v1, max(v2, v3));
-    const int tmd = max(min(v1, v2), min(max(v1, v2), v3));
-    const uint32_t w1 = pk2_i16(tlo), w2 = pk2_i16(tmd), w3 = pk2_i16(thi);
-    uint32_t wd = 0;
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const s16x2 p01 = __builtin_amdgcn_cvt_pk_i16(acc[j][4 * b], acc[j][4 * b + 1]);
-      const s16x2 p23 = __builtin_amdgcn_cvt_pk_i16(acc[j][4 * b + 2], acc[j][4 * b + 3]);
-      const uint32_t c01 = count3_sorted_pk(p01, w1, w2, w3);
-      const uint32_t c23 = count3_sorted_pk(p23, w1, w2, w3);
-      wd |= (c01 | (c23 << 8)) << (2 * b);
-    }
-    if (flip) wd = ~wd;
-    uint32_t q = (uint32_t)__builtin_amdgcn_mov_dpp((int)wd, 0xB1, 0xF, 0xF, true);
-    q = __builtin_rotateright32(q, r1);
-    wd = q ^ ((wd ^ q) & k1);
-    q = (uint32_t)__builtin_amdgcn_mov_dpp((int)wd, 0x4E, 0xF, 0xF, true);
-    q = __builtin_rotateright32(q, r2);
-    wd = q ^ ((wd ^ q) & k2);
-    uint8_t* o = otile + (pl0 + 8 * t + 4 * h) * orow + (cl >> 2);
-    const uint32_t w8 = wd >> 8;
-    o[0] = (uint8_t)wd;
-    o[orow] = (uint8_t)(wd >> 16);
-    o[2 * orow] = (uint8_t)w8;
-    o[3 * orow] = (uint8_t)(w8 >> 16);
+    epilogue_thr_pk_block(acc[j], thr_pk_of<SH>(recs[cl], bnd), h, l32, cl, pl0, otile, orow);
   }
 }
 
